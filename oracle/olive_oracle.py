@@ -1,0 +1,236 @@
+"""Plain fp64 CPU oracle for the per-position scoring of the method.
+
+TEST INFRASTRUCTURE ONLY. Nothing on the product path may import, call or link
+this module: only the test suite, the package smoke check and the benchmark's
+CPU-baseline leg use it. It shares no code with the HIP path.
+
+What it computes (for every packed position of a batch of stitched rollouts):
+  * z_X[v] = s_X * sum_k h_X[k] * W_X[k, v]     -- the vocabulary projection of
+    each model X in {student S, teacher T} (the language-model parameterisation of
+    pi_theta and pi_T used throughout Sec. 3.1; s_X = 1/temperature, and the
+    configuration table of App. A (Table 3) fixes the training temperature at 1.0);
+  * lse_X = M_X + ln sum_v exp(z_X[v] - M_X), M_X = max_v z_X[v]   -- the
+    normaliser of the softmax over the full vocabulary;
+  * logp_X = z_X[y] - lse_X for the realised token y   -- the per-token log-prob
+    whose negative sum over the teacher continuation is the loss of Eq. 1;
+  * KL(p_T || p_S) = sum_v p_T[v] (log p_T[v] - log p_S[v])   -- the full
+    vocabulary divergence between teacher and student (knowledge distillation
+    minimises it, Sec. 6; OPD scores student tokens with the teacher, Sec. 1);
+  * argmax_X = lowest v attaining M_X   -- the greedy token (the K = 1 case of the
+    top-K overlap statistic of Sec. 4.1);
+  * masks: a position is valid when it precedes the sequence's valid length, and
+    in-region (scored) for the teacher region when it is at or past the cut, the
+    prompt and student prefix being masked out of Eq. 1's loss (Sec. 3.1).
+
+Everything is the plain two-pass definition in float64 over the exact values of
+the (bf16- or fp32-) rounded inputs: one library matmul per row chunk, then max,
+exp, an exactly rounded sum (math.fsum), log. No online rescaling, no vocabulary
+splitting, no fusion.
+"""
+from __future__ import annotations
+
+import math
+from typing import Optional
+
+import numpy as np
+
+REGION_TEACHER = 0   # t >= cut: the teacher continuation (Eq. 1's scored tokens)
+REGION_STUDENT = 1   # t <  cut: the student prefix (OPD's scored tokens)
+REGION_ALL = 2       # every valid position
+
+
+def _f64(a) -> np.ndarray:
+    return np.asarray(a, dtype=np.float64)
+
+
+def masks(cu_seqlens, cut, valid_len=None, region: int = REGION_TEACHER) -> dict:
+    """Position masks and counts (Sec. 3.1, Eq. 1 and the sentence after it).
+
+    Sequence b occupies packed rows [cu[b], cu[b+1]); local index t = row - cu[b].
+    valid(t) = t < valid_len[b] (valid_len defaults to the sequence length);
+    in-region(t) = valid(t) and (t >= cut[b] | t < cut[b] | true) for the
+    teacher / student / all regions.
+    """
+    cu = np.asarray(cu_seqlens, dtype=np.int64)
+    cut = np.asarray(cut, dtype=np.int64)
+    B = len(cu) - 1
+    T = int(cu[-1])
+    lengths = cu[1:] - cu[:-1]
+    vl = lengths.copy() if valid_len is None else np.asarray(valid_len, dtype=np.int64)
+    seq_id = np.empty(T, dtype=np.int64)
+    local_t = np.empty(T, dtype=np.int64)
+    valid = np.zeros(T, dtype=bool)
+    inreg = np.zeros(T, dtype=bool)
+    for b in range(B):
+        t = np.arange(lengths[b], dtype=np.int64)
+        rows = slice(cu[b], cu[b + 1])
+        seq_id[rows] = b
+        local_t[rows] = t
+        v = t < vl[b]
+        valid[rows] = v
+        if region == REGION_TEACHER:
+            r = t >= cut[b]
+        elif region == REGION_STUDENT:
+            r = t < cut[b]
+        elif region == REGION_ALL:
+            r = np.ones_like(v)
+        else:
+            raise ValueError("unknown region %r" % (region,))
+        inreg[rows] = v & r
+    return dict(seq_id=seq_id, local_t=local_t, valid=valid, in_region=inreg,
+                n_scored=int(inreg.sum()), t_valid=int(valid.sum()))
+
+
+def project(h_rows, w, scale: float = 1.0) -> np.ndarray:
+    """z = scale * (h @ W): the vocabulary logits of a model, [n, V] in float64.
+
+    h_rows: [n, d]; w: [d, V] (the layout of the workloads). The product of two
+    bf16 values is exact in float64; the d-term sum is one library matmul.
+    """
+    return float(scale) * (_f64(h_rows) @ _f64(w))
+
+
+def log_softmax_stats(z_row) -> dict:
+    """Max, log-normaliser, greedy index and top-2 gap of one logit row (fp64)."""
+    z = _f64(z_row)
+    M = float(z.max())
+    lse = M + math.log(math.fsum(np.exp(z - M).tolist()))
+    am = int(np.argmax(z))                      # first index attaining the max
+    if z.shape[0] >= 2:
+        second = float(np.partition(z, -2)[-2])
+        gap = M - second
+    else:
+        gap = math.inf
+    return dict(max=M, lse=lse, argmax=am, gap=gap)
+
+
+def kl_teacher_student(z_t, lse_t: float, z_s, lse_s: float) -> tuple:
+    """KL(p_T || p_S) of one row, two ways (fp64, exactly rounded sums).
+
+    direct: sum_v p_T (log p_T - log p_S).
+    nonneg: sum_v p_T (expm1(d) - d), d = log p_S - log p_T, whose every term is
+            >= 0; it equals the direct form because sum p_S = sum p_T = 1.
+    """
+    lp_t = _f64(z_t) - lse_t
+    lp_s = _f64(z_s) - lse_s
+    p_t = np.exp(lp_t)
+    direct = math.fsum((p_t * (lp_t - lp_s)).tolist())
+    d = lp_s - lp_t
+    with np.errstate(over="ignore", invalid="ignore"):
+        term = p_t * (np.expm1(d) - d)
+    big = ~np.isfinite(term)
+    if big.any():   # p_T * e^d = p_S exactly; use it where expm1 overflows
+        term[big] = np.exp(lp_s[big]) - p_t[big] * (1.0 + d[big])
+    nonneg = math.fsum(term.tolist())
+    return direct, nonneg
+
+
+def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1.0,
+               h_teacher_rows=None, w_teacher=None, scale_teacher: float = 1.0,
+               chunk: Optional[int] = None) -> dict:
+    """Unmasked per-row quantities for a set of rows (every row treated as valid).
+
+    Returns float64 / int64 arrays of length n: z_y_s, lse_s, logp_s, argmax_s,
+    gap_s, max_s, and with a teacher the same for t plus kl (direct) and
+    kl_nonneg.
+    """
+    hs = _f64(h_student_rows)
+    n = hs.shape[0]
+    y = np.asarray(targets_rows, dtype=np.int64)
+    ws = _f64(w_student)
+    V = ws.shape[1]
+    has_t = h_teacher_rows is not None
+    if has_t:
+        ht = _f64(h_teacher_rows)
+        wt = _f64(w_teacher)
+        assert wt.shape[1] == V, "student and teacher share one vocabulary"
+    if chunk is None:
+        chunk = max(1, min(256, (1 << 22) // max(V, 1)))
+    out = {k: np.zeros(n) for k in ("z_y_s", "lse_s", "logp_s", "gap_s", "max_s")}
+    out["argmax_s"] = np.zeros(n, dtype=np.int64)
+    if has_t:
+        for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg"):
+            out[k] = np.zeros(n)
+        out["argmax_t"] = np.zeros(n, dtype=np.int64)
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        zs = project(hs[r0:r1], ws, scale_student)
+        zt = project(ht[r0:r1], wt, scale_teacher) if has_t else None
+        for i in range(r1 - r0):
+            g = r0 + i
+            st = log_softmax_stats(zs[i])
+            out["z_y_s"][g] = zs[i, y[g]]
+            out["lse_s"][g] = st["lse"]
+            out["logp_s"][g] = zs[i, y[g]] - st["lse"]
+            out["argmax_s"][g] = st["argmax"]
+            out["gap_s"][g] = st["gap"]
+            out["max_s"][g] = st["max"]
+            if has_t:
+                tt = log_softmax_stats(zt[i])
+                out["z_y_t"][g] = zt[i, y[g]]
+                out["lse_t"][g] = tt["lse"]
+                out["logp_t"][g] = zt[i, y[g]] - tt["lse"]
+                out["argmax_t"][g] = tt["argmax"]
+                out["gap_t"][g] = tt["gap"]
+                out["max_t"][g] = tt["max"]
+                kl, klp = kl_teacher_student(zt[i], tt["lse"], zs[i], st["lse"])
+                out["kl"][g] = kl
+                out["kl_nonneg"][g] = klp
+    return out
+
+
+def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
+          h_teacher=None, w_teacher=None, scale_student: float = 1.0,
+          scale_teacher: float = 1.0, region: int = REGION_TEACHER,
+          rows=None) -> dict:
+    """The whole scoring of a packed batch, masked.
+
+    Outputs per packed position (length T): logp_s, logp_t, argmax_s, argmax_t,
+    kl (KL(teacher || student) in-region, exactly +0.0 elsewhere); at positions
+    past the valid length logp = 0 and argmax = -1. Per sequence: ce (Eq. 1's
+    loss, minus the sum of the student's log-probs over the in-region positions).
+    Counts: n_scored (in-region positions) and t_valid (valid positions).
+
+    rows: optional subset of packed rows to evaluate (the others are left at the
+    masked values and reported in `evaluated`); masks and counts are always full.
+    """
+    m = masks(cu_seqlens, cut, valid_len, region)
+    T = m["valid"].shape[0]
+    B = len(np.asarray(cu_seqlens)) - 1
+    has_t = h_teacher is not None
+    sel = np.arange(T) if rows is None else np.unique(np.asarray(rows, dtype=np.int64))
+    sel = sel[m["valid"][sel]]
+    y = np.asarray(targets, dtype=np.int64)
+    if sel.size:
+        r = row_scores(np.asarray(h_student)[sel], w_student, y[sel], scale_student,
+                       None if not has_t else np.asarray(h_teacher)[sel], w_teacher,
+                       scale_teacher)
+    out = dict(logp_s=np.zeros(T), argmax_s=np.full(T, -1, dtype=np.int64),
+               lse_s=np.zeros(T), gap_s=np.full(T, math.inf), kl=np.zeros(T),
+               kl_nonneg=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
+    if has_t:
+        out.update(logp_t=np.zeros(T), argmax_t=np.full(T, -1, dtype=np.int64),
+                   lse_t=np.zeros(T), gap_t=np.full(T, math.inf))
+    if sel.size:
+        out["evaluated"][sel] = True
+        for k in ("logp_s", "argmax_s", "lse_s", "gap_s"):
+            out[k][sel] = r[k]
+        if has_t:
+            for k in ("logp_t", "argmax_t", "lse_t", "gap_t"):
+                out[k][sel] = r[k]
+            inr = m["in_region"][sel]
+            out["kl"][sel[inr]] = r["kl"][inr]
+            out["kl_nonneg"][sel[inr]] = r["kl_nonneg"][inr]
+    # Eq. 1: the loss of sequence b is minus the sum of the student's log-probs of
+    # its in-region tokens; an empty region gives 0.
+    ce = np.zeros(B)
+    seq = m["seq_id"]
+    for b in range(B):
+        idx = np.nonzero((seq == b) & m["in_region"] & out["evaluated"])[0]
+        ce[b] = -math.fsum(out["logp_s"][idx].tolist()) if idx.size else 0.0
+    out["ce"] = ce
+    out["n_scored"] = m["n_scored"]
+    out["t_valid"] = m["t_valid"]
+    out["valid"] = m["valid"]
+    out["in_region"] = m["in_region"]
+    return out

@@ -1,0 +1,107 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and check that the pins fail.
+
+Each mutant replaces one oracle function with a version carrying a single, plausible
+slip (a dropped term, a wrong sign or direction, a wrong tie-break, an off-by-one
+mask, a lost scale). The pin tests of test_oracle_pins.py are then run against the
+mutant and at least one of them must fail.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import olive_oracle as O
+from tests import test_oracle_pins as P
+
+_orig_lss = O.log_softmax_stats
+_orig_kl = O.kl_teacher_student
+_orig_masks = O.masks
+_orig_project = O.project
+
+
+def lss_dropped_max(z_row):
+    r = _orig_lss(z_row)
+    z = np.asarray(z_row, dtype=np.float64)
+    r["lse"] = math.log(math.fsum(np.exp(z - r["max"]).tolist()))
+    return r
+
+
+def lss_last_index(z_row):
+    r = _orig_lss(z_row)
+    z = np.asarray(z_row, dtype=np.float64)
+    r["argmax"] = int(len(z) - 1 - np.argmax(z[::-1]))
+    return r
+
+
+def lss_plain_sum_of_logits(z_row):
+    r = _orig_lss(z_row)
+    z = np.asarray(z_row, dtype=np.float64)
+    r["lse"] = r["max"] + math.log(math.fsum(np.exp(z - r["max"]).tolist()) + 1.0 / len(z))
+    return r
+
+
+def kl_reversed(z_t, lse_t, z_s, lse_s):
+    return _orig_kl(z_s, lse_s, z_t, lse_t)
+
+
+def kl_wrong_sign(z_t, lse_t, z_s, lse_s):
+    a, b = _orig_kl(z_t, lse_t, z_s, lse_s)
+    return -a, -b
+
+
+def masks_off_by_one(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER):
+    return _orig_masks(cu_seqlens, np.asarray(cut) + 1, valid_len, region)
+
+
+def masks_ignore_valid(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER):
+    return _orig_masks(cu_seqlens, cut, None, region)
+
+
+def project_no_scale(h_rows, w, scale=1.0):
+    return _orig_project(h_rows, w, 1.0)
+
+
+def project_dropped_last_k(h_rows, w, scale=1.0):
+    h = np.asarray(h_rows, dtype=np.float64).copy()
+    if h.shape[1] > 1:
+        h[:, -1] = 0.0
+    return _orig_project(h, w, scale)
+
+
+MUTANTS = [
+    ("log_softmax_stats", lss_dropped_max),
+    ("log_softmax_stats", lss_last_index),
+    ("log_softmax_stats", lss_plain_sum_of_logits),
+    ("kl_teacher_student", kl_reversed),
+    ("kl_teacher_student", kl_wrong_sign),
+    ("masks", masks_off_by_one),
+    ("masks", masks_ignore_valid),
+    ("project", project_no_scale),
+    ("project", project_dropped_last_k),
+]
+
+PINS = [
+    lambda: [P.test_decimal_brute_force(s) for s in range(6)],
+    P.test_golden_worked_examples,
+    lambda: [P.test_equal_columns_give_uniform(V) for V in (1, 2, 7, 1000)],
+    P.test_two_token_softplus_and_bernoulli_kl,
+    P.test_probabilities_sum_to_one_and_lse_bounds,
+    P.test_kl_nonnegative_and_two_forms_agree,
+    P.test_kl_cross_entropy_identity,
+    P.test_argmax_exact_ties_take_lowest_index,
+    P.test_mask_counts_enumerated,
+    P.test_eq1_masks_prefix_and_scores_continuation,
+    P.test_masked_outputs_exact_values,
+]
+
+
+@pytest.mark.parametrize("target,mutant", MUTANTS, ids=[m.__name__ for _, m in MUTANTS])
+def test_pins_catch_mutant(monkeypatch, target, mutant):
+    monkeypatch.setattr(O, target, mutant)
+    caught = 0
+    for pin in PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError, IndexError):
+            caught += 1
+    assert caught >= 1, "no pin caught mutant %s" % mutant.__name__

@@ -1,0 +1,296 @@
+"""Pins of the fp64 oracle to facts it does not compute itself.
+
+Each test checks the oracle against something fixed by the mathematics of the
+scoring (Sec. 3.1 Eq. 1 for the log-prob and the cut mask; the full-vocabulary
+KL(teacher || student) that distillation minimises, Sec. 6): exact rational
+arithmetic at 50 digits, closed forms, invariants, limits and brute-force
+enumeration. test_oracle_mutations.py plants plausible mistakes in a copy of the
+oracle and checks that these pins catch them.
+"""
+import json
+import math
+import os
+from decimal import Decimal, getcontext
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import olive_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def bf16_values(shape, rng, std=1.0):
+    """Random values exactly representable in bf16 (and hence in fp64)."""
+    x = torch.from_numpy(rng.standard_normal(shape).astype(np.float32) * std)
+    return x.to(torch.bfloat16).float().numpy().astype(np.float64)
+
+
+# ----------------------------------------------------------------------------- exact arithmetic
+def decimal_row(h, w, scale):
+    """z, lse, log-softmax of one row in 50-digit decimal arithmetic, no max shift."""
+    getcontext().prec = 50
+    d, V = w.shape
+    z = []
+    for v in range(V):
+        acc = Decimal(0)
+        for k in range(d):
+            acc += Decimal(float(h[k])) * Decimal(float(w[k, v]))
+        z.append(Decimal(repr(float(scale))) * acc)
+    tot = sum((zi.exp() for zi in z), Decimal(0))
+    lse = tot.ln()
+    logp = [zi - lse for zi in z]
+    return z, lse, logp
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_decimal_brute_force(seed):
+    rng = np.random.default_rng(100 + seed)
+    V = int(rng.integers(2, 17))
+    ds, dt = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+    n = 3
+    hs = bf16_values((n, ds), rng, 2.0)
+    ht = bf16_values((n, dt), rng, 2.0)
+    ws = bf16_values((ds, V), rng, 1.0)
+    wt = bf16_values((dt, V), rng, 1.0)
+    y = rng.integers(0, V, size=n)
+    sS, sT = [1.0, 4.0, 0.5][seed % 3], [1.0, 2.0, 4.0][seed % 3]
+    r = O.row_scores(hs, ws, y, sS, ht, wt, sT)
+    for i in range(n):
+        zs, lse_s, lps = decimal_row(hs[i], ws, sS)
+        zt, lse_t, lpt = decimal_row(ht[i], wt, sT)
+        assert abs(r["lse_s"][i] - float(lse_s)) <= 1e-13 * max(1.0, abs(float(lse_s)))
+        assert abs(r["lse_t"][i] - float(lse_t)) <= 1e-13 * max(1.0, abs(float(lse_t)))
+        assert abs(r["logp_s"][i] - float(lps[y[i]])) <= 1e-13 * max(1.0, abs(float(lps[y[i]])))
+        assert abs(r["logp_t"][i] - float(lpt[y[i]])) <= 1e-13 * max(1.0, abs(float(lpt[y[i]])))
+        kl = sum((lt.exp() * (lt - ls) for lt, ls in zip(lpt, lps)), Decimal(0))
+        assert abs(r["kl"][i] - float(kl)) <= 1e-13 * max(1.0, float(kl))
+        assert abs(r["kl_nonneg"][i] - float(kl)) <= 1e-13 * max(1.0, float(kl))
+        # greedy token: first index attaining the exact maximum
+        ms = max(zs)
+        assert r["argmax_s"][i] == min(v for v in range(V) if zs[v] == ms)
+        mt = max(zt)
+        assert r["argmax_t"][i] == min(v for v in range(V) if zt[v] == mt)
+
+
+# ----------------------------------------------------------------------------- closed forms
+def test_golden_worked_examples():
+    with open(os.path.join(GOLDEN, "worked_examples.json")) as f:
+        data = json.load(f)
+    for c in data["cases"]:
+        out = O.score(np.array(c["h_student"]), np.array(c["w_student"]), np.array(c["targets"]),
+                      np.array(c["cu_seqlens"]), np.array(c["cut"]),
+                      None if c["valid_len"] is None else np.array(c["valid_len"]),
+                      np.array(c["h_teacher"]), np.array(c["w_teacher"]))
+        e = c["expect"]
+        for k in ("logp_s", "logp_t", "kl", "ce", "lse_s", "lse_t"):
+            if k in e:
+                np.testing.assert_allclose(out[k], e[k], rtol=0, atol=1e-14, err_msg=c["name"] + k)
+        for k in ("argmax_s", "argmax_t"):
+            np.testing.assert_array_equal(out[k], e[k], err_msg=c["name"] + k)
+        assert out["n_scored"] == e["n_scored"] and out["t_valid"] == e["t_valid"]
+
+
+@pytest.mark.parametrize("V", [1, 2, 7, 1000])
+def test_equal_columns_give_uniform(V):
+    rng = np.random.default_rng(V)
+    d = 5
+    col = bf16_values((d, 1), rng)
+    w = np.repeat(col, V, axis=1)
+    h = bf16_values((4, d), rng, 3.0)
+    r = O.row_scores(h, w, np.zeros(4, dtype=np.int64), 1.0, h, w, 1.0)
+    np.testing.assert_allclose(r["logp_s"], -math.log(V), rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(r["argmax_s"], 0)       # all tied: lowest index
+    assert np.all(np.abs(r["kl"]) <= 1e-15)
+
+
+def test_two_token_softplus_and_bernoulli_kl():
+    rng = np.random.default_rng(7)
+    for _ in range(20):
+        a = bf16_values((1, 2), rng, 3.0)
+        b = bf16_values((1, 2), rng, 3.0)
+        y = int(rng.integers(0, 2))
+        r = O.row_scores(np.ones((1, 1)), a, [y], 1.0, np.ones((1, 1)), b, 1.0)
+        other = 1 - y
+        want = -np.logaddexp(0.0, a[0, other] - a[0, y])
+        assert abs(r["logp_s"][0] - want) <= 1e-14
+        p = 1.0 / (1.0 + math.exp(b[0, 0] - b[0, 1]))   # teacher P(token 1)
+        q = 1.0 / (1.0 + math.exp(a[0, 0] - a[0, 1]))   # student P(token 1)
+        kl = p * math.log(p / q) + (1 - p) * math.log((1 - p) / (1 - q))
+        assert abs(r["kl"][0] - kl) <= 1e-13
+
+
+# ----------------------------------------------------------------------------- invariants
+def plain_logits(h, w, scale):
+    """Logits by explicit Python loops (tiny sizes only), independent of the oracle."""
+    n, d = h.shape
+    V = w.shape[1]
+    return [[scale * math.fsum(h[i, k] * w[k, v] for k in range(d)) for v in range(V)]
+            for i in range(n)]
+
+
+def test_probabilities_sum_to_one_and_lse_bounds():
+    rng = np.random.default_rng(3)
+    h = bf16_values((6, 8), rng, 2.0)
+    w = bf16_values((8, 50), rng, 1.5)
+    r = O.row_scores(h, w, np.zeros(6, dtype=np.int64), 2.0)
+    z = plain_logits(h, w, 2.0)
+    for i in range(6):
+        s = math.fsum(math.exp(zv - r["lse_s"][i]) for zv in z[i])
+        assert abs(s - 1.0) <= 1e-12
+        M = max(z[i])
+        assert M <= r["lse_s"][i] <= M + math.log(50) + 1e-12
+        assert abs(r["max_s"][i] - M) <= 1e-12
+        srt = sorted(z[i])
+        assert abs(r["gap_s"][i] - (srt[-1] - srt[-2])) <= 1e-12
+
+
+def test_kl_nonnegative_and_two_forms_agree():
+    rng = np.random.default_rng(4)
+    n, V = 16, 3000
+    hs, ht = bf16_values((n, 32), rng), bf16_values((n, 48), rng)
+    ws, wt = bf16_values((32, V), rng, 0.4), bf16_values((48, V), rng, 0.4)
+    r = O.row_scores(hs, ws, np.zeros(n, dtype=np.int64), 1.0, ht, wt, 4.0)
+    assert np.all(r["kl_nonneg"] >= 0.0)
+    assert np.all(r["kl"] >= -1e-12)
+    np.testing.assert_allclose(r["kl"], r["kl_nonneg"], rtol=1e-12, atol=1e-12)
+
+
+def test_kl_cross_entropy_identity():
+    """KL(p_T||p_S) = H(p_T, p_S) - H(p_T): cross-entropy minus entropy."""
+    rng = np.random.default_rng(12)
+    hs, ht = bf16_values((4, 16), rng), bf16_values((4, 24), rng)
+    ws, wt = bf16_values((16, 200), rng), bf16_values((24, 200), rng)
+    r = O.row_scores(hs, ws, np.zeros(4, dtype=np.int64), 1.0, ht, wt, 1.0)
+    zs, zt = plain_logits(hs, ws, 1.0), plain_logits(ht, wt, 1.0)
+    for i in range(4):
+        lt = [v - r["lse_t"][i] for v in zt[i]]
+        ls = [v - r["lse_s"][i] for v in zs[i]]
+        pt = [math.exp(v) for v in lt]
+        cross = -math.fsum(p * l for p, l in zip(pt, ls))
+        ent = -math.fsum(p * l for p, l in zip(pt, lt))
+        assert abs(r["kl"][i] - (cross - ent)) <= 1e-12
+
+
+def test_kl_zero_for_identical_models_and_row_shift():
+    rng = np.random.default_rng(5)
+    n, d, V = 8, 16, 777
+    hs = bf16_values((n, d), rng)
+    ws = bf16_values((d, V), rng, 0.5)
+    r = O.row_scores(hs, ws, np.arange(n), 1.0, hs, ws, 1.0)
+    assert np.all(r["kl"] == 0.0)
+    np.testing.assert_array_equal(r["logp_s"], r["logp_t"])
+    # teacher logits = student logits + a per-row constant: identical distributions
+    c = bf16_values((1, V), rng)[0] * 0 + 3.0
+    ht = np.concatenate([hs, bf16_values((n, 1), rng)], axis=1)
+    wt = np.concatenate([ws, np.full((1, V), c[0])], axis=0)
+    r2 = O.row_scores(hs, ws, np.arange(n), 1.0, ht, wt, 1.0)
+    assert np.all(np.abs(r2["kl"]) <= 1e-12)
+    assert np.all(np.abs(r2["logp_t"] - r2["logp_s"]) <= 1e-12)
+
+
+def test_peaked_teacher_limit():
+    """As p_T becomes one-hot at v*, KL(p_T||p_S) -> -log p_S(v*)."""
+    rng = np.random.default_rng(6)
+    hs, ht = bf16_values((3, 8), rng), bf16_values((3, 8), rng)
+    ws, wt = bf16_values((8, 64), rng), bf16_values((8, 64), rng)
+    r = O.row_scores(hs, ws, np.zeros(3, dtype=np.int64), 1.0, ht, wt, 1.0)
+    for s in (64.0, 256.0):
+        rr = O.row_scores(hs, ws, r["argmax_t"], 1.0, ht, wt, s)
+        np.testing.assert_allclose(rr["kl"], -rr["logp_s"], rtol=0, atol=1e-6 * (64.0 / s) + 1e-9)
+
+
+def test_lse_of_iid_gaussian_logits():
+    """For V iid N(0, sigma^2) logits, lse ~= ln V + sigma^2 / 2 (law of large numbers)."""
+    rng = np.random.default_rng(8)
+    V, sigma = 151936, 1.0
+    z = rng.standard_normal((4, V)) * sigma
+    for i in range(4):
+        st = O.log_softmax_stats(z[i])
+        assert abs(st["lse"] - (math.log(V) + sigma ** 2 / 2)) < 0.02
+
+
+def test_argmax_exact_ties_take_lowest_index():
+    rng = np.random.default_rng(9)
+    d, V = 6, 40
+    w = bf16_values((d, V), rng)
+    h = bf16_values((5, d), rng)
+    z = h @ w
+    for i in range(5):
+        j = int(np.argmax(z[i]))
+        w2 = w.copy()
+        lo = int(rng.integers(0, j + 1))
+        w2[:, lo] = w[:, j]        # duplicate the best column at a lower or equal index
+        r = O.row_scores(h[i:i + 1], w2, [0], 1.0)
+        assert r["argmax_s"][0] == lo
+        assert r["gap_s"][0] == (0.0 if lo != j else r["gap_s"][0])
+
+
+# ----------------------------------------------------------------------------- masks and Eq. 1
+def test_mask_counts_enumerated():
+    """All (len, cut, valid_len) with len <= 12: counts equal their closed forms."""
+    for L in range(0, 13):
+        for cut in range(0, L + 1):
+            for vl in range(0, L + 1):
+                cu = np.array([0, L])
+                mt = O.masks(cu, [cut], [vl], O.REGION_TEACHER)
+                ms = O.masks(cu, [cut], [vl], O.REGION_STUDENT)
+                ma = O.masks(cu, [cut], [vl], O.REGION_ALL)
+                assert mt["n_scored"] == max(0, vl - cut)
+                assert ms["n_scored"] == min(cut, vl)
+                assert ma["n_scored"] == vl
+                assert mt["t_valid"] == vl
+                # the scored teacher positions are exactly local t in [cut, vl)
+                np.testing.assert_array_equal(np.nonzero(mt["in_region"])[0],
+                                              np.arange(cut, max(cut, vl)))
+
+
+def test_eq1_masks_prefix_and_scores_continuation():
+    """A stitched trace (prefix y_1..y_k, continuation c_1..c_l): the teacher region
+    scores exactly the l continuation tokens, and the loss is minus the sum of their
+    student log-probs (Eq. 1)."""
+    rng = np.random.default_rng(10)
+    V, d = 50, 8
+    w = bf16_values((d, V), rng)
+    seqs = [(5, 3), (1, 6), (0, 4), (7, 0)]          # (k prefix tokens, l continuation tokens)
+    lengths = [k + l for k, l in seqs]
+    cu = np.concatenate([[0], np.cumsum(lengths)])
+    T = int(cu[-1])
+    h = bf16_values((T, d), rng)
+    prefix_tok, cont_tok = 1000, 2000                 # labels, mapped into [0, V) below
+    labels = []
+    for k, l in seqs:
+        labels += [prefix_tok] * k + [cont_tok] * l
+    labels = np.array(labels)
+    y = rng.integers(0, V, size=T)
+    out = O.score(h, w, y, cu, [k for k, _ in seqs], None, h, w)
+    assert out["n_scored"] == sum(l for _, l in seqs)
+    np.testing.assert_array_equal(labels[out["in_region"]], cont_tok)
+    r = O.row_scores(h, w, y, 1.0)
+    for b, (k, l) in enumerate(seqs):
+        idx = np.arange(cu[b] + k, cu[b] + k + l)
+        assert abs(out["ce"][b] - (-math.fsum(r["logp_s"][idx]))) <= 1e-12
+    # cut = 0 (offline SFT on whole teacher traces) scores every valid position;
+    # cut = len scores none
+    o0 = O.score(h, w, y, cu, [0] * 4)
+    assert o0["n_scored"] == T
+    oL = O.score(h, w, y, cu, lengths)
+    assert oL["n_scored"] == 0 and np.all(oL["ce"] == 0.0) and np.all(oL["kl"] == 0.0)
+
+
+def test_masked_outputs_exact_values():
+    rng = np.random.default_rng(11)
+    cu = np.array([0, 10, 10, 25])                  # includes an empty sequence
+    cut, vl = np.array([4, 0, 7]), np.array([8, 0, 13])
+    T, d, V = 25, 4, 30
+    h, w = bf16_values((T, d), rng), bf16_values((d, V), rng)
+    y = rng.integers(0, V, size=T)
+    out = O.score(h, w, y, cu, cut, vl, h * 0.5, w)
+    inval = ~out["valid"]
+    assert np.all(out["logp_s"][inval] == 0.0) and np.all(out["argmax_s"][inval] == -1)
+    outside = ~out["in_region"]
+    assert np.all(out["kl"][outside] == 0.0)
+    assert not np.any(np.signbit(out["kl"][outside]))
+    assert out["t_valid"] == 8 + 0 + 13 and out["n_scored"] == 4 + 0 + 6
+    assert out["ce"][1] == 0.0
