@@ -1,0 +1,191 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused per-position scoring path on one MI355X.
+
+One step = one olive_kl_masked call over one packed batch already resident in HBM:
+vocabulary projection of both models (bf16 MFMA, fp32 accumulate), online
+log-softmax over the full vocabulary, realised-token log-probs, masked
+KL(teacher || student), greedy argmax with the exact near-tie re-decision, and
+Eq. 1's per-sequence loss. Default workload: long_rollout (B=8 x L=4096,
+V=151,936, d_S=2048, d_T=4096, logits x4, EOS-truncated).
+
+Prints one JSON line: positions/s (valid positions scored per second), the
+scoring kernel's achieved bf16 TFLOP/s against the MI355X dense peak, and the fp64
+CPU oracle's rate on a bounded row sample.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (no sparsity)
+TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
+                            "traffic.json")
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(wl, seconds: float):
+    """The fp64 oracle on a bounded, seeded sample of the workload's valid rows."""
+    import numpy as np
+    import torch
+    from threadpoolctl import threadpool_info
+    from oracle import olive_oracle as O
+
+    def np32(t):
+        return (t.float() if t.dtype == torch.bfloat16 else t).cpu().numpy()
+    cu = wl["cu_seqlens"].cpu().numpy()
+    cut = wl["cut"].cpu().numpy()
+    vl = None if wl["valid_len"] is None else wl["valid_len"].cpu().numpy()
+    m = O.masks(cu, cut, vl)
+    valid_rows = np.nonzero(m["valid"])[0]
+    rng = np.random.default_rng(12345)
+    order = rng.permutation(valid_rows)
+    ws = np32(wl["w_student"]).astype(np.float64)   # input marshalling, untimed
+    wt = np32(wl["w_teacher"]).astype(np.float64)
+
+    def run(rows):
+        idx = torch.from_numpy(np.sort(rows)).cuda()
+        hs = np32(wl["h_student"][idx]).astype(np.float64)
+        ht = np32(wl["h_teacher"][idx]).astype(np.float64)
+        y = wl["targets"][idx].cpu().numpy()
+        t0 = time.perf_counter()
+        O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"])
+        return time.perf_counter() - t0
+    t_cal = run(order[:4])
+    n = int(max(8, min(4000, seconds / max(t_cal / 4, 1e-6))))
+    n = min(n, len(order))
+    t = run(order[4:4 + n])
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
+    return dict(value=n / t, unit="positions/s", cores=int(threads), kind="oracle",
+                sample="%d random valid rows of the workload (seed 12345), fp64 numpy oracle "
+                       "row_scores (both models + KL), weights converted to float64 before "
+                       "the timed region; %.1f s" % (n, t))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="long_rollout")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus %d requested)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    if not 1 <= args.steps <= 64:
+        print("--steps must be in [1, 64]", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_36246_amd import _lib as L
+    from paper_2609_36246_amd import workloads as W
+
+    L.load()
+    log("generating workload", args.workload)
+    t0 = time.time()
+    wl = W.make_workload(args.workload, args.seed, device="cuda")
+    spec = wl["spec"]
+    T = wl["total_positions"]
+    B = spec.num_seqs
+    log("workload ready in %.1fs: T=%d" % (time.time() - t0, T))
+    desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher,
+                       L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
+                       wl["scale_student"], wl["scale_teacher"], max_positions=T, max_seqs=B,
+                       flags=L.OLIVE_FLAG_KERNEL_TIMING)
+    stream = torch.cuda.current_stream()
+    ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"], stream)
+    dev = wl["h_student"].device
+    kl = torch.empty(T, dtype=torch.float32, device=dev)
+    counts = torch.empty(2, dtype=torch.int64, device=dev)
+    lps = torch.empty(T, dtype=torch.float32, device=dev)
+    lpt = torch.empty(T, dtype=torch.float32, device=dev)
+    ams = torch.empty(T, dtype=torch.int32, device=dev)
+    amt = torch.empty(T, dtype=torch.int32, device=dev)
+    ce = torch.empty(B, dtype=torch.float32, device=dev)
+    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
+                         wl["h_teacher"], wl["valid_len"], L.OLIVE_REGION_TEACHER)
+
+    def step():
+        L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / args.steps
+    kms = L.olive_score_kernel_times(ctx, args.steps)
+    kernel_ms = sum(kms) / len(kms)
+    stats = L.olive_score_last_stats(ctx)
+    err = L.olive_score_last_error(ctx)
+    n_scored, t_valid = [int(x) for x in counts.cpu().tolist()]
+    log("timed %d steps: %.3f ms/step, scoring kernel %.3f ms, stats %s, err %d"
+        % (args.steps, ms_step, kernel_ms, stats, err))
+    flops = 2.0 * t_valid * spec.vocab * (spec.d_student + spec.d_teacher)
+    achieved = flops / (kernel_ms * 1e-3) / 1e12
+    traffic = None
+    if os.path.exists(TRAFFIC_FILE):
+        with open(TRAFFIC_FILE) as f:
+            tr = json.load(f)
+        ent = tr.get(args.workload)
+        if ent and ent.get("kernel_source_sha") == kernel_source_sha():
+            traffic = ent.get("bytes_per_launch")
+    out = {
+        "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
+        "value": t_valid / (ms_step * 1e-3),
+        "unit": "positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded; random hidden states and weights of the workload's shapes)",
+        "config": {
+            "workload": args.workload, "num_seqs": B, "total_positions": T,
+            "valid_positions": t_valid, "scored_positions": n_scored, "vocab": spec.vocab,
+            "d_student": spec.d_student, "d_teacher": spec.d_teacher,
+            "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
+            "near_tie_rows": stats["flagged"], "grid": stats["grid"],
+            "step_tflops": flops / (ms_step * 1e-3) / 1e12,
+            "pct_bf16_peak_step": 100.0 * flops / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+            "kernel_ms": kernel_ms,
+        },
+        "roofline": {
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+        },
+    }
+    L.olive_score_free(ctx)
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) on a bounded sample ...")
+        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def kernel_source_sha() -> str:
+    import hashlib
+    p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36246_amd", "csrc",
+                     "score_mfma.hip")
+    with open(p, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,190 @@
+/*
+ * olive_score.h -- C ABI of the fused per-position scoring library (gfx950).
+ *
+ * The method trains a student on teacher continuations of its own prefixes: each
+ * packed sequence is a student prefix followed by a teacher continuation, split at
+ * a per-sequence cut point (Sec. 3.1, Alg. 1). This library scores such a batch in
+ * one pass over the vocabulary, for a student model S and optionally a teacher
+ * model T that share one vocabulary of V tokens:
+ *
+ *   z_X[t, v]  = s_X * sum_k h_X[t, k] * W_X[k, v]          (vocabulary projection)
+ *   lse_X[t]   = log sum_v exp(z_X[t, v])                    (full-vocabulary normaliser)
+ *   logp_X[t]  = z_X[t, y_t] - lse_X[t]                      (log-prob of the realised
+ *                token; Eq. 1's loss is minus its sum over the continuation)
+ *   kl[t]      = sum_v p_T[t, v] (log p_T[t, v] - log p_S[t, v])
+ *                (KL(teacher || student), the divergence distillation minimises, Sec. 6,
+ *                 reported only inside the selected region, exactly +0.0 elsewhere)
+ *   argmax_X[t]= lowest v attaining max_v z_X[t, v]          (greedy token; the K = 1
+ *                case of the top-K overlap statistic of Sec. 4.1)
+ *   ce[b]      = - sum over scored t of sequence b of logp_S[t]   (Eq. 1, per sequence)
+ *
+ * s_X is the logit scale (1/temperature; the paper trains at temperature 1.0,
+ * App. A, Table 3). Positions are pre-shifted: hidden row t scores targets[t].
+ *
+ * Conventions for every call:
+ *   - All pointers named as device pointers must be device (HBM) memory on the
+ *     current HIP device; host pointers are marked "host".
+ *   - Calls that take a stream are asynchronous on it (0 = the null stream): they
+ *     only validate host-visible arguments and enqueue kernels. The caller keeps
+ *     every input and output alive until the stream has finished.
+ *   - No call allocates device memory except olive_score_init; every workspace is
+ *     owned by the context and sized at init.
+ *   - A context is not safe for concurrent use from several host threads or for
+ *     overlapping calls on different streams.
+ *   - Functions return an olive_status and never throw or abort.
+ */
+#ifndef OLIVE_SCORE_H
+#define OLIVE_SCORE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct olive_score_ctx olive_score_ctx; /* opaque */
+
+typedef enum {
+    OLIVE_OK = 0,
+    OLIVE_E_NULL = 1,        /* a required pointer is NULL */
+    OLIVE_E_SHAPE = 2,       /* a size is <= 0, or exceeds what the context was built for */
+    OLIVE_E_DTYPE = 3,       /* unknown dtype or weight layout */
+    OLIVE_E_RANGE = 4,       /* a value is out of range (logit scale not finite and > 0, region) */
+    OLIVE_E_HIP = 5,         /* a HIP runtime call failed */
+    OLIVE_E_NOMEM = 6,       /* device allocation failed at init */
+    OLIVE_E_UNSUPPORTED = 7  /* valid but not supported by this build (see each field) */
+} olive_status;
+
+typedef enum { OLIVE_F32 = 0, OLIVE_BF16 = 1 } olive_dtype;   /* of h and W; accumulate fp32 */
+
+typedef enum {
+    OLIVE_W_DV = 0,  /* W given as [d][V] row-major (the workloads' layout): init repacks it */
+    OLIVE_W_VD = 1   /* W given as [V][d] row-major (an nn.Linear weight): borrowed, no copy */
+} olive_wlayout;
+
+typedef enum {
+    OLIVE_REGION_TEACHER = 0, /* local t >= cut: the teacher continuation, Eq. 1's scored tokens */
+    OLIVE_REGION_STUDENT = 1, /* local t <  cut: the student prefix (OPD scores these, Sec. 1) */
+    OLIVE_REGION_ALL = 2      /* every valid position */
+} olive_region;
+
+/* Fixed at init. */
+typedef struct {
+    int64_t vocab;              /* V >= 1, shared by both models, V < 2^31 */
+    int32_t d_student;          /* hidden width of S, in [1, 16384] */
+    int32_t d_teacher;          /* hidden width of T in [1, 16384], or 0 for student-only */
+    int32_t dtype;              /* olive_dtype of h and W */
+    int32_t w_layout;           /* olive_wlayout of the weights passed to init */
+    float logit_scale_student;  /* s_S, finite and > 0 (1.0 = temperature 1) */
+    float logit_scale_teacher;  /* s_T, finite and > 0; ignored for student-only */
+    int64_t max_positions;      /* largest packed batch T a call may pass, >= 1, < 2^31 */
+    int32_t max_seqs;           /* largest number of sequences B a call may pass, >= 1 */
+    int32_t flags;              /* bit set of OLIVE_FLAG_* (0 = defaults) */
+} olive_score_desc;
+
+/* Force the generic fp32-FMA kernel even where the bf16 MFMA kernel applies. */
+#define OLIVE_FLAG_SIMPLE_KERNEL 1
+/* Record HIP events around the vocabulary-scoring kernel of every call (for
+ * olive_score_kernel_times); costs two event records per call. */
+#define OLIVE_FLAG_KERNEL_TIMING 2
+
+/* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */
+typedef struct {
+    int32_t num_seqs;            /* B >= 1 (<= desc.max_seqs) */
+    int32_t region;              /* olive_region selecting where kl and ce are taken */
+    int64_t total_positions;     /* T = cu_seqlens[B] (host copy of it), 0 < T <= max_positions */
+    const int32_t *cu_seqlens;   /* device [B+1]: cu[0] = 0, nondecreasing, cu[B] = T */
+    const int32_t *cut;          /* device [B]: local cut index in [0, len_b] */
+    const int32_t *valid_len;    /* device [B] or NULL (= len_b): positions t >= valid_len_b
+                                    (past an end-of-sequence) are not scored; in [0, len_b] */
+    const int32_t *targets;      /* device [T]: realised token of each position, in [0, V) */
+    const void *h_student;       /* device [T][d_student] row-major, desc.dtype */
+    const void *h_teacher;       /* device [T][d_teacher] row-major, or NULL (student only) */
+} olive_batch;
+
+/*
+ * Create a scoring context for one pair of projection weights.
+ *   out        host: receives the context (NULL on failure).
+ *   desc       host: sizes, dtype, layout, scales (copied).
+ *   w_student  device: W_S in desc.w_layout ([d_S][V] or [V][d_S]).
+ *   w_teacher  device: W_T likewise, or NULL when desc.d_teacher == 0.
+ *   hip_stream the stream the repack runs on; init synchronises it before returning.
+ * With OLIVE_W_DV the context owns a repacked [V][d] copy of each weight; with
+ * OLIVE_W_VD it borrows the caller's buffers, which must outlive the context.
+ * Errors: E_NULL, E_SHAPE, E_DTYPE, E_RANGE, E_NOMEM, E_HIP.
+ */
+olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *desc,
+                              const void *w_student, const void *w_teacher, void *hip_stream);
+
+/*
+ * Per-position log-probs and greedy tokens of both models (Eq. 1's summands, at
+ * every valid position, prefix and continuation alike).
+ *   logp_student  device [T] fp32: logp_S, 0 at positions past the valid length.
+ *   logp_teacher  device [T] fp32 or NULL; must be NULL on a student-only context
+ *                 or when b->h_teacher is NULL.
+ *   argmax_student, argmax_teacher  device [T] int32 or NULL: greedy token, -1 past
+ *                 the valid length.
+ * Errors: E_NULL, E_SHAPE, E_RANGE, E_UNSUPPORTED, E_HIP. Content errors found on the
+ * device (a target outside [0, V), a cut or valid length outside [0, len_b], a
+ * decreasing cu_seqlens) set the context's device error word (olive_score_last_error)
+ * and make the affected outputs NaN.
+ */
+olive_status olive_token_logprobs(olive_score_ctx *ctx, const olive_batch *b,
+                                  float *logp_student, float *logp_teacher,
+                                  int32_t *argmax_student, int32_t *argmax_teacher,
+                                  void *hip_stream);
+
+/*
+ * The fused scoring of both models in one pass: masked KL(teacher || student) per
+ * position, the counts, and optionally every output of olive_token_logprobs and
+ * Eq. 1's per-sequence loss. Needs a teacher context and b->h_teacher.
+ *   kl          device [T] fp32: KL in the region, exactly +0.0 elsewhere.
+ *   counts      device [2] int64 or NULL: counts[0] = positions in the region and
+ *               valid (scored), counts[1] = valid positions.
+ *   logp_*, argmax_*  as in olive_token_logprobs, each may be NULL.
+ *   ce_per_seq  device [B] fp32 or NULL: minus the sum of logp_S over the scored
+ *               positions of each sequence (0 for an empty region).
+ * Errors: as olive_token_logprobs, plus E_UNSUPPORTED on a student-only context.
+ */
+olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *kl,
+                             int64_t *counts, float *logp_student, float *logp_teacher,
+                             int32_t *argmax_student, int32_t *argmax_teacher,
+                             float *ce_per_seq, void *hip_stream);
+
+/* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
+olive_status olive_score_free(olive_score_ctx *ctx);
+
+/* A static, NUL-terminated description of a status code (never NULL). */
+const char *olive_status_string(olive_status s);
+
+/*
+ * Read and clear the context's device error word (synchronises the device).
+ *   device_code host: receives a bit set, 0 when no content error occurred:
+ *   1 = target out of [0, V), 2 = cut out of [0, len], 4 = valid_len out of [0, len],
+ *   8 = cu_seqlens not nondecreasing from 0 or cu[B] != T.
+ */
+olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
+
+/*
+ * Diagnostics of the last scoring call (synchronises the device).
+ *   out host [4] int64: [0] vocabulary splits used, [1] rows whose greedy token was
+ *   re-decided in fp64 because its top-2 logit gap was within the fp32 error window,
+ *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched.
+ */
+olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out);
+
+/*
+ * Durations of the vocabulary-scoring kernel (the fused projection + softmax pass)
+ * of the last n calls, oldest first, from events recorded on the call's stream
+ * (synchronises the device). Needs OLIVE_FLAG_KERNEL_TIMING at init.
+ *   out host [n] fp32: milliseconds; n in [1, 64] and at most the number of calls
+ *   made since init. Errors: E_NULL, E_RANGE (n out of range), E_UNSUPPORTED (no
+ *   timing flag), E_HIP.
+ */
+olive_status olive_score_kernel_times(olive_score_ctx *ctx, float *out, int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OLIVE_SCORE_H */

@@ -1,0 +1,215 @@
+// Split combine, realised-token gather and finalisation (one wavefront per row).
+//
+// For each valid compacted row: merges the per-split partial statistics in a fixed
+// order, gathers the realised token's logit of each model as a coalesced dot
+// product of the hidden row with the token's weight row, and writes
+//   logp_X = s_X z_X[y] - lse_X,   lse_X = s_X best_X + ln Z_X,
+//   kl     = A / Z_T - lse_T + lse_S   (KL(teacher || student), in-region only),
+//   argmax_X = lowest index attaining the max,
+// queueing rows whose top-2 gap is inside the fp32 error window for the exact
+// re-decision of their greedy token.
+#include <hip/hip_runtime.h>
+
+#include "olive_device.hpp"
+#include "olive_internal.hpp"
+
+namespace olive {
+
+// Relative top-2 gap (in scaled logits) below which the greedy token is re-decided.
+constexpr float kTieWindow = 1.0f / 16384.0f;
+
+template <typename E>
+__device__ __forceinline__ float wave_dot(const E *h, const E *w, int d, int lane);
+
+template <>
+__device__ __forceinline__ float wave_dot<uint16_t>(const uint16_t *h, const uint16_t *w, int d,
+                                                    int lane) {
+    float acc = 0.f;
+    if ((d & 7) == 0 && ((uintptr_t)h & 15) == 0 && ((uintptr_t)w & 15) == 0) {
+        const uint4 *h4 = (const uint4 *)h;
+        const uint4 *w4 = (const uint4 *)w;
+        for (int i = lane; i < (d >> 3); i += 64) {
+            uint4 x = h4[i], y = w4[i];
+            uint32_t xs[4] = {x.x, x.y, x.z, x.w}, ys[4] = {y.x, y.y, y.z, y.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                acc = fmaf(__uint_as_float(xs[q] << 16), __uint_as_float(ys[q] << 16), acc);
+                acc = fmaf(__uint_as_float(xs[q] & 0xffff0000u),
+                           __uint_as_float(ys[q] & 0xffff0000u), acc);
+            }
+        }
+    } else {
+        for (int k = lane; k < d; k += 64)
+            acc = fmaf(bf16_bits_to_f32(h[k]), bf16_bits_to_f32(w[k]), acc);
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+template <>
+__device__ __forceinline__ float wave_dot<float>(const float *h, const float *w, int d, int lane) {
+    float acc = 0.f;
+    for (int k = lane; k < d; k += 64) acc = fmaf(h[k], w[k], acc);
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+// sum_k |h_k| |w_k| over one row pair (the rounding-bound weight of a dot product).
+template <typename E>
+__device__ __forceinline__ float wave_absdot(const E *h, const E *w, int d, int lane) {
+    float acc = 0.f;
+    for (int k = lane; k < d; k += 64)
+        acc = fmaf(fabsf(load_elem(h, k)), fabsf(load_elem(w, k)), acc);
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+__device__ __forceinline__ Stat load_stat(const float *P, int64_t ps, int fb, int s, int64_t j) {
+    Stat r;
+    r.best = P[((fb + 0) * MAX_SPLITS + s) * ps + j];
+    r.sec = P[((fb + 1) * MAX_SPLITS + s) * ps + j];
+    r.idx = __float_as_int(P[((fb + 2) * MAX_SPLITS + s) * ps + j]);
+    r.z = P[((fb + 3) * MAX_SPLITS + s) * ps + j];
+    return r;
+}
+
+__device__ __forceinline__ void wave_merge(Stat &st, float &acc, float c) {
+    for (int off = 32; off > 0; off >>= 1) {
+        Stat o;
+        o.best = __shfl_xor(st.best, off);
+        o.sec = __shfl_xor(st.sec, off);
+        o.idx = __shfl_xor(st.idx, off);
+        o.z = __shfl_xor(st.z, off);
+        float oa = __shfl_xor(acc, off);
+        stat_merge(st, acc, o, oa, c);
+    }
+}
+
+__device__ __forceinline__ bool near_tie(const Stat &st, float s) {
+    float gap = s * (st.best - st.sec);
+    float mag = fabsf(s * st.best);
+    return gap <= kTieWindow * (mag > 1.f ? mag : 1.f);
+}
+
+template <typename E, bool HAS_T>
+__global__ void __launch_bounds__(256)
+combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
+               int32_t *__restrict__ err, float *__restrict__ logp_s, float *__restrict__ logp_t,
+               int32_t *__restrict__ am_s, int32_t *__restrict__ am_t, float *__restrict__ kl,
+               float *__restrict__ logp_tmp, int32_t *__restrict__ flagged, int flag_cap) {
+    const int lane = threadIdx.x & 63;
+    const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    Sched *sched = const_cast<Sched *>(a.sched);
+    if (j >= sched->t_valid) return;
+    const uint32_t rm = a.rowmap[j];
+    const int64_t g = rm & 0x7fffffffu;
+    const bool inr = (rm >> 31) != 0;
+    const int32_t y = targets[g];
+    if (y < 0 || y >= a.V) {
+        if (lane == 0) {
+            atomicOr(err, ERR_TARGET);
+            const float qnan = __builtin_nanf("");
+            if (logp_s) logp_s[g] = qnan;
+            if (logp_tmp) logp_tmp[g] = qnan;
+            if (HAS_T && logp_t) logp_t[g] = qnan;
+            if (am_s) am_s[g] = -1;
+            if (HAS_T && am_t) am_t[g] = -1;
+            if (HAS_T && kl) kl[g] = inr ? qnan : 0.f;
+        }
+        return;
+    }
+    const E *hs = (const E *)a.hs;
+    const E *ws = (const E *)a.ws;
+    const float zy_s = wave_dot<E>(hs + g * a.ds, ws + (int64_t)y * a.ds, a.ds, lane);
+    float zy_t = 0.f;
+    if (HAS_T) {
+        const E *ht = (const E *)a.ht;
+        const E *wt = (const E *)a.wt;
+        zy_t = wave_dot<E>(ht + g * a.dt, wt + (int64_t)y * a.dt, a.dt, lane);
+    }
+    const int ns = sched->n_splits;
+    Stat ss = stat_identity(), st = stat_identity();
+    float acc_a = 0.f, dummy = 0.f;
+    if (lane < ns) {
+        ss = load_stat(a.part, a.pstride, F_BEST_S, lane, j);
+        if (HAS_T) {
+            st = load_stat(a.part, a.pstride, F_BEST_T, lane, j);
+            acc_a = a.part[(F_A * MAX_SPLITS + lane) * a.pstride + j];
+        }
+    }
+    wave_merge(ss, dummy, a.cS);
+    if (HAS_T) wave_merge(st, acc_a, a.cT);
+    // Every lane now holds the merged statistics.
+    int fl = (am_s && near_tie(ss, a.sS)) ? 1 : 0;
+    if (HAS_T) fl |= (am_t && near_tie(st, a.sT)) ? 2 : 0;
+    float theta_s = 0.f, theta_t = 0.f;
+    if (fl) {
+        // Lower bound of the exact max: fp32 max minus its rounding bound.
+        if (fl & 1) {
+            float za = wave_absdot<E>(hs + g * a.ds, ws + (int64_t)ss.idx * a.ds, a.ds, lane);
+            theta_s = ss.best - (float)a.ds * (1.0f / 8388608.0f) * za;
+        }
+        if (HAS_T && (fl & 2)) {
+            const E *ht = (const E *)a.ht;
+            const E *wt = (const E *)a.wt;
+            float za = wave_absdot<E>(ht + g * a.dt, wt + (int64_t)st.idx * a.dt, a.dt, lane);
+            theta_t = st.best - (float)a.dt * (1.0f / 8388608.0f) * za;
+        }
+    }
+    if (lane != 0) return;
+    const float lse_s = a.sS * ss.best + fast_log2(ss.z) * kLn2;
+    const float lp_s = a.sS * zy_s - lse_s;
+    if (logp_s) logp_s[g] = lp_s;
+    if (logp_tmp) logp_tmp[g] = lp_s;
+    if (am_s) am_s[g] = ss.idx;
+    if (HAS_T) {
+        const float lse_t = a.sT * st.best + fast_log2(st.z) * kLn2;
+        if (logp_t) logp_t[g] = a.sT * zy_t - lse_t;
+        if (am_t) am_t[g] = st.idx;
+        if (kl) {
+            float an = same_scale ? a.sT * acc_a : acc_a;
+            float v = an / st.z - lse_t + lse_s;
+            kl[g] = inr ? v : 0.f;
+        }
+    }
+    if (fl && flagged) {
+        int q = atomicAdd(&sched->n_flagged, 1);
+        if (q < flag_cap) {
+            flagged[4 * q] = (int32_t)j;
+            flagged[4 * q + 1] = fl;
+            flagged[4 * q + 2] = __float_as_int(theta_s);
+            flagged[4 * q + 3] = __float_as_int(theta_t);
+        }
+    }
+}
+
+hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
+                          const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
+                          int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
+                          int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st) {
+    if (max_rows <= 0) return hipSuccess;
+    dim3 grid((unsigned)((max_rows + 3) / 4));
+    int same = same_scale ? 1 : 0;
+    if (bf16) {
+        if (has_t)
+            combine_kernel<uint16_t, true><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
+                                                                 logp_t, am_s, am_t, kl, logp_tmp,
+                                                                 flagged, flag_cap);
+        else
+            combine_kernel<uint16_t, false><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
+                                                                  logp_t, am_s, am_t, kl,
+                                                                  logp_tmp, flagged, flag_cap);
+    } else {
+        if (has_t)
+            combine_kernel<float, true><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
+                                                              logp_t, am_s, am_t, kl, logp_tmp,
+                                                              flagged, flag_cap);
+        else
+            combine_kernel<float, false><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
+                                                               logp_t, am_s, am_t, kl, logp_tmp,
+                                                               flagged, flag_cap);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace olive

@@ -1,0 +1,314 @@
+// Host side of the C ABI declared in include/olive_score.h: argument validation,
+// workspace ownership, and the per-call launch sequence
+//   prep -> rowmap -> score (MFMA or generic) -> combine -> [fixup] -> [ce].
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstring>
+#include <new>
+
+#include "olive_internal.hpp"
+
+using namespace olive;
+
+struct olive_score_ctx {
+    olive_score_desc desc;
+    int device = 0;
+    int n_cu = 0;
+    const void *ws = nullptr, *wt = nullptr;   // [V][d] weights used by the kernels
+    void *ws_own = nullptr, *wt_own = nullptr; // repacked copies (OLIVE_W_DV)
+    uint32_t *rowmap = nullptr;
+    int32_t *seqbuf = nullptr;
+    Sched *sched = nullptr;
+    float *part = nullptr;
+    int64_t pstride = 0;
+    float *logp_tmp = nullptr;
+    int32_t *flagged = nullptr;
+    int flag_cap = 0;
+    void *fx_scratch = nullptr;
+    int32_t *err = nullptr;
+    bool bf16 = false, has_t = false, mfma_ok = false;
+    int last_kernel = -1, last_grid = 0;
+    bool timing = false;
+    hipEvent_t ev[2][64] = {};     // start / end of the scoring kernel, ring of 64 calls
+    int64_t n_calls = 0;
+};
+
+namespace {
+
+constexpr int kFixupCapRows = 8192;
+
+void release(olive_score_ctx *c) {
+    if (!c) return;
+    for (int k = 0; k < 2; ++k)
+        for (int i = 0; i < 64; ++i)
+            if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
+    void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
+                    c->logp_tmp, c->flagged, c->fx_scratch, c->err};
+    for (void *p : ptrs)
+        if (p) (void)hipFree(p);
+    delete c;
+}
+
+bool finite_positive(float x) { return std::isfinite(x) && x > 0.f; }
+
+template <typename T>
+olive_status dev_alloc(T **p, size_t bytes) {
+    *p = nullptr;
+    if (bytes == 0) bytes = 16;
+    if (hipMalloc((void **)p, bytes) != hipSuccess) { *p = nullptr; return OLIVE_E_NOMEM; }
+    return OLIVE_OK;
+}
+
+olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP; }
+
+// The scoring of one batch, shared by olive_token_logprobs and olive_kl_masked.
+olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t *counts,
+                 float *logp_s, float *logp_t, int32_t *am_s, int32_t *am_t, float *ce,
+                 hipStream_t st) {
+    const olive_score_desc &d = ctx->desc;
+    if (!b->cu_seqlens || !b->cut || !b->targets || !b->h_student) return OLIVE_E_NULL;
+    if (b->num_seqs < 1 || b->num_seqs > d.max_seqs) return OLIVE_E_SHAPE;
+    if (b->total_positions < 1 || b->total_positions > d.max_positions) return OLIVE_E_SHAPE;
+    if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) return OLIVE_E_RANGE;
+    const bool want_t = kl || logp_t || am_t;
+    if (want_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
+    const bool has_t = want_t;
+    const int64_t T = b->total_positions;
+    const int64_t V = d.vocab;
+    const int n_vtiles = (int)((V + 255) / 256);
+    const bool mfma = ctx->mfma_ok;
+    float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
+
+    olive_status s;
+    int grid = 0;
+    int fixed_splits = 1;
+    int64_t max_units = 0;
+    if (mfma) {
+        grid = ctx->n_cu;
+    } else {
+        int64_t pt = (T + SIMPLE_BT - 1) / SIMPLE_BT;
+        int64_t want = (2048 + pt - 1) / pt;
+        int lim = n_vtiles < MAX_SPLITS ? n_vtiles : MAX_SPLITS;
+        fixed_splits = (int)(want < 1 ? 1 : (want > lim ? lim : want));
+        max_units = pt * fixed_splits;
+    }
+    s = check_hip(launch_prep(*b, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
+                              mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
+                              fixed_splits, st));
+    if (s) return s;
+    s = check_hip(launch_rowmap(*b, V, ctx->seqbuf, ctx->sched, ctx->rowmap, ctx->err, logp_s,
+                                has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
+                                has_t ? kl : nullptr, logp_tmp, st));
+    if (s) return s;
+
+    ScoreArgs a;
+    a.hs = b->h_student;
+    a.ht = has_t ? b->h_teacher : nullptr;
+    a.ws = ctx->ws;
+    a.wt = has_t ? ctx->wt : nullptr;
+    a.rowmap = ctx->rowmap;
+    a.sched = ctx->sched;
+    a.part = ctx->part;
+    a.pstride = ctx->pstride;
+    a.V = (int32_t)V;
+    a.ds = d.d_student;
+    a.dt = has_t ? d.d_teacher : 0;
+    a.n_vtiles = n_vtiles;
+    a.sS = d.logit_scale_student;
+    a.sT = has_t ? d.logit_scale_teacher : 1.f;
+    a.cS = a.sS * 1.4426950408889634f;
+    a.cT = a.sT * 1.4426950408889634f;
+    const bool same_scale = has_t && (a.sS == a.sT);
+
+    const int slot = (int)(ctx->n_calls % 64);
+    if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
+    if (mfma)
+        s = check_hip(launch_score_mfma(a, has_t, same_scale, grid, st));
+    else
+        s = check_hip(launch_score_simple(a, ctx->bf16, has_t, max_units, st));
+    if (s) return s;
+    if (ctx->timing && hipEventRecord(ctx->ev[1][slot], st) != hipSuccess) return OLIVE_E_HIP;
+    ctx->n_calls++;
+    ctx->last_kernel = mfma ? 0 : 1;
+    ctx->last_grid = mfma ? grid : (int)max_units;
+
+    int32_t *flagged = (am_s || (has_t && am_t)) ? ctx->flagged : nullptr;
+    s = check_hip(launch_combine(a, ctx->bf16, has_t, same_scale, b->targets, ctx->err, logp_s,
+                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
+                                 has_t ? kl : nullptr, logp_tmp, flagged, ctx->flag_cap, T, st));
+    if (s) return s;
+    if (flagged) {
+        s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
+                                        am_s, has_t ? am_t : nullptr, st));
+        if (s) return s;
+    }
+    if (ce) {
+        s = check_hip(launch_ce(*b, ctx->seqbuf, ctx->sched, logp_s ? logp_s : ctx->logp_tmp,
+                                ce, st));
+        if (s) return s;
+    }
+    return OLIVE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *olive_status_string(olive_status s) {
+    switch (s) {
+        case OLIVE_OK: return "OLIVE_OK: success";
+        case OLIVE_E_NULL: return "OLIVE_E_NULL: a required pointer is NULL";
+        case OLIVE_E_SHAPE: return "OLIVE_E_SHAPE: a size is out of range for this context";
+        case OLIVE_E_DTYPE: return "OLIVE_E_DTYPE: unknown dtype or weight layout";
+        case OLIVE_E_RANGE: return "OLIVE_E_RANGE: a value is out of range";
+        case OLIVE_E_HIP: return "OLIVE_E_HIP: a HIP runtime call failed";
+        case OLIVE_E_NOMEM: return "OLIVE_E_NOMEM: device allocation failed";
+        case OLIVE_E_UNSUPPORTED: return "OLIVE_E_UNSUPPORTED: not supported by this context";
+    }
+    return "OLIVE: unknown status";
+}
+
+olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *desc,
+                              const void *w_student, const void *w_teacher, void *hip_stream) {
+    if (!out || !desc) return OLIVE_E_NULL;
+    *out = nullptr;
+    const olive_score_desc &d = *desc;
+    if (d.dtype != OLIVE_F32 && d.dtype != OLIVE_BF16) return OLIVE_E_DTYPE;
+    if (d.w_layout != OLIVE_W_DV && d.w_layout != OLIVE_W_VD) return OLIVE_E_DTYPE;
+    if (d.vocab < 1 || d.vocab >= (int64_t)1 << 31) return OLIVE_E_SHAPE;
+    if (d.d_student < 1 || d.d_teacher < 0) return OLIVE_E_SHAPE;
+    if (d.max_positions < 1 || d.max_positions >= ((int64_t)1 << 31) - 1) return OLIVE_E_SHAPE;
+    if (d.max_seqs < 1) return OLIVE_E_SHAPE;
+    if (d.d_student > 16384 || d.d_teacher > 16384) return OLIVE_E_UNSUPPORTED;
+    if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
+    if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
+    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING)) return OLIVE_E_RANGE;
+    if (!w_student) return OLIVE_E_NULL;
+    if (d.d_teacher > 0 && !w_teacher) return OLIVE_E_NULL;
+
+    olive_score_ctx *c = new (std::nothrow) olive_score_ctx();
+    if (!c) return OLIVE_E_NOMEM;
+    c->desc = d;
+    c->bf16 = d.dtype == OLIVE_BF16;
+    c->has_t = d.d_teacher > 0;
+    hipStream_t st = (hipStream_t)hip_stream;
+    if (hipGetDevice(&c->device) != hipSuccess ||
+        hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, c->device) !=
+            hipSuccess) {
+        release(c);
+        return OLIVE_E_HIP;
+    }
+    c->mfma_ok = c->bf16 && (d.d_student % 128 == 0) && (d.d_teacher % 128 == 0) &&
+                 d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL);
+    const int esz = c->bf16 ? 2 : 4;
+    const int64_t V = d.vocab;
+    olive_status s = OLIVE_OK;
+    if (d.w_layout == OLIVE_W_DV) {
+        s = dev_alloc(&c->ws_own, (size_t)V * d.d_student * esz);
+        if (!s && c->has_t) s = dev_alloc(&c->wt_own, (size_t)V * d.d_teacher * esz);
+        if (s) { release(c); return s; }
+        if (launch_repack(w_student, c->ws_own, d.d_student, V, esz, st) != hipSuccess ||
+            (c->has_t && launch_repack(w_teacher, c->wt_own, d.d_teacher, V, esz, st) != hipSuccess)) {
+            release(c);
+            return OLIVE_E_HIP;
+        }
+        c->ws = c->ws_own;
+        c->wt = c->wt_own;
+    } else {
+        c->ws = w_student;
+        c->wt = c->has_t ? w_teacher : nullptr;
+    }
+    const int64_t P = d.max_positions;
+    c->pstride = (P + 255) / 256 * 256;
+    c->flag_cap = (int)(P < kFixupCapRows ? P : kFixupCapRows);
+    if (!s) s = dev_alloc(&c->rowmap, (size_t)P * sizeof(uint32_t));
+    if (!s) s = dev_alloc(&c->seqbuf, (size_t)seqbuf_entries(d.max_seqs) * sizeof(int32_t));
+    if (!s) s = dev_alloc(&c->sched, sizeof(Sched));
+    if (!s) s = dev_alloc(&c->part, (size_t)NFIELDS * MAX_SPLITS * c->pstride * sizeof(float));
+    if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
+    if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
+    if (!s)
+        s = dev_alloc(&c->fx_scratch,
+                      (size_t)c->flag_cap * fixup_chunks(V) * 2 * fixup_result_bytes());
+    if (!s) s = dev_alloc(&c->err, sizeof(int32_t));
+    if (s) { release(c); return s; }
+    c->timing = (d.flags & OLIVE_FLAG_KERNEL_TIMING) != 0;
+    if (c->timing) {
+        for (int k = 0; k < 2; ++k)
+            for (int i = 0; i < 64; ++i)
+                if (hipEventCreate(&c->ev[k][i]) != hipSuccess) { release(c); return OLIVE_E_HIP; }
+    }
+    if (hipMemsetAsync(c->err, 0, sizeof(int32_t), st) != hipSuccess ||
+        hipMemsetAsync(c->sched, 0, sizeof(Sched), st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess) {
+        release(c);
+        return OLIVE_E_HIP;
+    }
+    *out = c;
+    return OLIVE_OK;
+}
+
+olive_status olive_token_logprobs(olive_score_ctx *ctx, const olive_batch *b, float *logp_student,
+                                  float *logp_teacher, int32_t *argmax_student,
+                                  int32_t *argmax_teacher, void *hip_stream) {
+    if (!ctx || !b || !logp_student) return OLIVE_E_NULL;
+    return run(ctx, b, nullptr, nullptr, logp_student, logp_teacher, argmax_student,
+               argmax_teacher, nullptr, (hipStream_t)hip_stream);
+}
+
+olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *kl,
+                             int64_t *counts, float *logp_student, float *logp_teacher,
+                             int32_t *argmax_student, int32_t *argmax_teacher, float *ce_per_seq,
+                             void *hip_stream) {
+    if (!ctx || !b || !kl) return OLIVE_E_NULL;
+    if (!ctx->has_t) return OLIVE_E_UNSUPPORTED;
+    return run(ctx, b, kl, counts, logp_student, logp_teacher, argmax_student, argmax_teacher,
+               ce_per_seq, (hipStream_t)hip_stream);
+}
+
+olive_status olive_score_free(olive_score_ctx *ctx) {
+    if (!ctx) return OLIVE_OK;
+    hipError_t e = hipDeviceSynchronize();
+    release(ctx);
+    return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP;
+}
+
+olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code) {
+    if (!ctx || !device_code) return OLIVE_E_NULL;
+    if (hipDeviceSynchronize() != hipSuccess) return OLIVE_E_HIP;
+    int32_t v = 0;
+    if (hipMemcpy(&v, ctx->err, sizeof(v), hipMemcpyDeviceToHost) != hipSuccess) return OLIVE_E_HIP;
+    if (hipMemset(ctx->err, 0, sizeof(int32_t)) != hipSuccess) return OLIVE_E_HIP;
+    *device_code = v;
+    return OLIVE_OK;
+}
+
+olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out) {
+    if (!ctx || !out) return OLIVE_E_NULL;
+    if (hipDeviceSynchronize() != hipSuccess) return OLIVE_E_HIP;
+    Sched s;
+    if (hipMemcpy(&s, ctx->sched, sizeof(s), hipMemcpyDeviceToHost) != hipSuccess) return OLIVE_E_HIP;
+    out[0] = s.n_splits;
+    out[1] = s.n_flagged;
+    out[2] = ctx->last_kernel;
+    out[3] = ctx->last_grid;
+    return OLIVE_OK;
+}
+
+olive_status olive_score_kernel_times(olive_score_ctx *ctx, float *out, int32_t n) {
+    if (!ctx || !out) return OLIVE_E_NULL;
+    if (!ctx->timing) return OLIVE_E_UNSUPPORTED;
+    if (n < 1 || n > 64 || n > ctx->n_calls) return OLIVE_E_RANGE;
+    if (hipDeviceSynchronize() != hipSuccess) return OLIVE_E_HIP;
+    for (int i = 0; i < n; ++i) {
+        const int slot = (int)((ctx->n_calls - n + i) % 64);
+        float ms = 0.f;
+        if (hipEventElapsedTime(&ms, ctx->ev[0][slot], ctx->ev[1][slot]) != hipSuccess)
+            return OLIVE_E_HIP;
+        out[i] = ms;
+    }
+    return OLIVE_OK;
+}
+
+}  // extern "C"

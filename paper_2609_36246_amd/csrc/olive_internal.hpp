@@ -1,0 +1,96 @@
+// Internal definitions shared by the host ABI and the gfx950 kernels of the
+// fused per-position scoring library. Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "olive_score.h"
+
+namespace olive {
+
+// Per-(row, vocabulary split) partial statistics, stored as planes of floats:
+// plane (field * max_splits + split) holds one value per compacted row.
+//   BEST/SEC: largest and second-largest raw logit (unscaled h.W) seen;
+//   IDX:      lowest vocabulary index attaining BEST (int32 bits);
+//   Z:        sum_v exp(s * (z_v - BEST)) over the split;
+//   A:        sum_v exp(s_T * (zT_v - BEST_T)) * D_v, the teacher-weighted logit
+//             difference D_v = zT_v - zS_v (equal scales; multiplied by s at the
+//             end) or s_T zT_v - s_S zS_v (different scales).
+enum Field {
+    F_BEST_S = 0, F_SEC_S = 1, F_IDX_S = 2, F_Z_S = 3,
+    F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8,
+    NFIELDS = 9
+};
+
+// Device-side schedule of one call, written by the preparation kernel.
+struct Sched {
+    int32_t t_valid;    // valid (scored or context) positions = compacted rows
+    int32_t n_ptiles;   // ceil(t_valid / tile_rows) for the kernel in use
+    int32_t n_splits;   // vocabulary splits
+    int32_t n_units;    // n_ptiles * n_splits
+    int64_t n_scored;   // in-region valid positions
+    int32_t n_flagged;  // rows queued for the near-tie argmax re-decision
+    int32_t cu_bad;     // cu_seqlens malformed: nothing is scored
+};
+
+// Bits of the device error word.
+enum {
+    ERR_TARGET = 1,
+    ERR_CUT = 2,
+    ERR_VALID = 4,
+    ERR_CU = 8,
+};
+
+constexpr int MFMA_BV = 256;     // vocabulary rows per tile (MFMA M)
+constexpr int MFMA_BT = 128;     // positions per tile (MFMA N)
+constexpr int SIMPLE_BT = 16;    // positions per tile of the generic kernel
+constexpr int SIMPLE_VC = 256;   // vocabulary chunk of the generic kernel
+constexpr int MAX_SPLITS = 32;   // vocabulary splits a call may use
+
+struct ScoreArgs {
+    const void *hs, *ht;         // hidden states [T][d] (caller)
+    const void *ws, *wt;         // weights [V][d] (repacked or borrowed)
+    const uint32_t *rowmap;      // [t_valid]: packed row | in-region << 31
+    const Sched *sched;
+    float *part;                 // partial planes
+    int64_t pstride;             // floats per plane
+    int32_t V, ds, dt;
+    int32_t n_vtiles;            // vocabulary tiles (MFMA) or chunks (generic)
+    float cS, cT;                // s * log2(e)
+    float sS, sT;                // logit scales
+};
+
+// Host-side launchers (each defined beside its kernel).
+hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int elem_bytes,
+                         hipStream_t st);
+hipError_t launch_prep(const olive_batch &b, int64_t V, int32_t *seqbuf, Sched *sched,
+                       int32_t *err, int64_t *counts, int tile_rows, int policy,
+                       int n_vtiles, int grid, int fixed_splits, hipStream_t st);
+hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
+                         const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
+                         float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
+                         hipStream_t st);
+hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_t max_units,
+                               hipStream_t st);
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, int grid,
+                             hipStream_t st);
+hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
+                          const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
+                          int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
+                          int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st);
+hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
+                             void *scratch, int32_t *am_s, int32_t *am_t, hipStream_t st);
+int fixup_chunks(int64_t V);
+size_t fixup_result_bytes();
+hipError_t launch_ce(const olive_batch &b, const int32_t *seqbuf, const Sched *sched,
+                     const float *logp_s, float *ce, hipStream_t st);
+
+// Layout of the per-sequence workspace (int32, 4 * (max_seqs + 1) entries).
+//   [0, B+1)          exclusive prefix sum of valid lengths (compacted row offsets)
+//   [B+1, 2B+2)       effective valid length per sequence (0 for a bad sequence)
+//   [2B+2, 3B+3)      effective cut per sequence
+//   [3B+3, 4B+4)      1 when the sequence's cut / valid length was out of range
+inline int64_t seqbuf_entries(int64_t max_seqs) { return 4 * (max_seqs + 1); }
+
+}  // namespace olive

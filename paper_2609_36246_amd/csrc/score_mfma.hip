@@ -1,0 +1,460 @@
+// Fused bf16 scoring kernel for gfx950 (MFMA 32x32x16, LDS ring fed by direct
+// global->LDS loads).
+//
+// A workgroup (4 wavefronts) owns a tile of 256 vocabulary rows x 128 compacted
+// positions and sweeps the vocabulary tiles of one split for one position tile.
+// For every vocabulary tile it accumulates the student logits (K = d_S) and then
+// the teacher logits (K = d_T) of the same 256 x 128 block in fp32 registers --
+// the [T, V] logits never reach HBM -- and folds both blocks into per-lane running
+// statistics: max, second max, lowest argmax and rescaled exp-sum per model, plus
+// the teacher-weighted difference sum that yields KL(teacher || student).
+//
+// Operand roles are swapped (weights are the MFMA A/row operand, hidden states the
+// B/column operand) so that every lane owns whole position columns and holds 64
+// vocabulary entries of each: the softmax statistics reduce inside registers and
+// only lanes l / l+32 and the two vocabulary-half wavefronts need merging at the
+// end of a split.
+//
+// Pipeline: K advances 32 elements (64 bytes per row) per step; each step's W tile
+// (256 x 64 B) and H tile (128 x 64 B) land in one of 4 LDS stages through
+// global_load_lds_dwordx4, issued 3 steps ahead. Stage rows are XOR-swizzled at
+// 16-byte granularity so the ds_read_b128 operand fetches are bank-conflict free.
+// Hidden widths must be multiples of 128 so every model's step count is a multiple
+// of the ring depth (each stage is a distinct LDS object with static indices).
+//
+// The grid is persistent (one workgroup per CU). Work units (position tile,
+// split) are ordered so that the 32 workgroups of one XCD share 8 position tiles x
+// 4 splits at any time and the 8 XCDs share the same 4 splits: W tiles are reused
+// across position tiles through L2 and the infinity cache, H tiles across splits.
+#include <hip/hip_runtime.h>
+
+#include "olive_device.hpp"
+#include "olive_internal.hpp"
+
+namespace olive {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int BV = MFMA_BV;              // 256
+constexpr int BT = MFMA_BT;              // 128
+constexpr int ROWB = 64;                 // bytes per row per step (32 bf16)
+constexpr int WT_BYTES = BV * ROWB;      // 16 KB
+constexpr int HT_BYTES = BT * ROWB;      // 8 KB
+constexpr float kMasked = -1.0e30f;      // logit of vocabulary rows outside the tile range
+
+__shared__ __attribute__((aligned(1024))) char g_lw0[WT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lw1[WT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lw2[WT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lw3[WT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lh0[HT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lh1[HT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lh2[HT_BYTES];
+__shared__ __attribute__((aligned(1024))) char g_lh3[HT_BYTES];
+
+template <int S> __device__ __forceinline__ char *lw() {
+    return S == 0 ? g_lw0 : S == 1 ? g_lw1 : S == 2 ? g_lw2 : g_lw3;
+}
+template <int S> __device__ __forceinline__ char *lh() {
+    return S == 0 ? g_lh0 : S == 1 ? g_lh1 : S == 2 ? g_lh2 : g_lh3;
+}
+
+// max(a, b) for non-NaN operands as one v_med3_f32 (no NaN canonicalisation).
+__device__ __forceinline__ float max2(float a, float b) {
+    return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
+}
+
+// 16-byte slot swizzle of a 64-byte stage row.
+__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+
+// Read one accumulator element where it lives (an AGPR). Issuing the read at the
+// point of use keeps the register allocator from copying whole accumulator tuples
+// into VGPRs ahead of the epilogue.
+__device__ __forceinline__ float agpr_read(float x) {
+    float y;
+    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(y) : "a"(x));
+    return y;
+}
+
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+__device__ __forceinline__ void dma16(const char *g, char *l) {
+    __builtin_amdgcn_global_load_lds((const void *)g, (lds_void *)l, 16, 0, 0);
+}
+
+struct Lane {
+    int lane, wid, wv, wt, h, l32;
+    int ldsoff[2];          // operand fetch offsets for the two k16 sub-steps
+    uint32_t wvoff[2][4];   // per model, per W DMA: row * rowbytes + chunk * 16
+    const char *hp[2][2];   // per model, per H DMA: pointer to the row chunk
+};
+
+struct Run {                // running statistics of one position column
+    float best, sec, z;
+    int idx;
+};
+
+template <bool HAS_T, bool SAME>
+struct Kernel {
+    // Issue the 6 DMAs of one step (4 W, 2 H) of model `m` into stage S.
+    template <int S>
+    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int m, int kk,
+                                                 int vt) {
+        const int d = m ? a.dt : a.ds;
+        const int64_t rowbytes = (int64_t)d * 2;
+        const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+        const char *wt = (const char *)(m ? a.wt : a.ws) + (int64_t)row0 * rowbytes + kk * ROWB;
+        char *lwp = lw<S>() + L.wid * 4 * 1024;
+        char *lhp = lh<S>() + L.wid * 2 * 1024;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) dma16(wt + (m ? L.wvoff[1][i] : L.wvoff[0][i]), lwp + i * 1024);
+#pragma unroll
+        for (int i = 0; i < 2; ++i) dma16((m ? L.hp[1][i] : L.hp[0][i]) + kk * ROWB, lhp + i * 1024);
+    }
+
+    template <int S>
+    static __device__ __forceinline__ void mma(const Lane &L, floatx16 (&acc)[4][2]) {
+        const char *wb = lw<S>() + L.wv * 128 * ROWB;
+        const char *hb = lh<S>() + L.wt * 64 * ROWB;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+            bf16x8 A[4], B[2];
+#pragma unroll
+            for (int vb = 0; vb < 4; ++vb)
+                A[vb] = *(const bf16x8 *)(wb + vb * 32 * ROWB + L.ldsoff[s]);
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+                B[cb] = *(const bf16x8 *)(hb + cb * 32 * ROWB + L.ldsoff[s]);
+#pragma unroll
+            for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+                    acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[vb], B[cb],
+                                                                          acc[vb][cb], 0, 0, 0);
+        }
+    }
+
+    // One pipeline step in stage S: wait for its data (the 2 later steps' 12 DMAs
+    // may stay in flight), then prefetch 3 steps ahead and multiply. The prefetch is
+    // issued unconditionally -- past the end of a unit it re-reads in-bounds
+    // addresses -- so the compiler's wait tracking never joins a path without it.
+    template <int S>
+    static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, int pm, int pk,
+                                                int pvt, floatx16 (&acc)[4][2]) {
+        __builtin_amdgcn_s_waitcnt(0x0F7C);   // vmcnt(12)
+        compiler_fence();
+        __builtin_amdgcn_s_barrier();
+        compiler_fence();
+        issue<(S + 3) & 3>(a, L, pm, pk, pvt);
+        mma<S>(L, acc);
+    }
+
+    // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
+    // vb, column cb) into a model's running statistics. Returns the exp weights'
+    // rescale through `e[]` so the teacher can form its difference sum.
+    static __device__ __forceinline__ void fold_block(const float (&z)[16], Run &R, float &Aacc,
+                                                      bool teacher, const float (&zs)[16],
+                                                      float c, float sS, float sT, int vcode0) {
+        float tm = R.best, ts = R.sec;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            ts = __builtin_amdgcn_fmed3f(z[r], tm, ts);
+            tm = max2(tm, z[r]);
+        }
+        // Branch-free: lowest row of this block equal to the new max (used only when
+        // the block raised the max), and the rescale of the running sums (1 when not).
+        int code = 0;
+#pragma unroll
+        for (int r = 15; r >= 0; --r) code = (z[r] == tm) ? 8 * (r >> 2) + (r & 3) : code;
+        const bool up = tm > R.best;
+        const float resc = fast_exp2((R.best - tm) * c);
+        R.z *= resc;
+        if (teacher) Aacc *= resc;
+        R.idx = up ? vcode0 + code : R.idx;
+        R.best = tm;
+        R.sec = ts;
+        const float mneg = -tm * c;
+        float zsum = 0.f, asum = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            const float e = fast_exp2(fmaf(z[r], c, mneg));
+            zsum += e;
+            if (teacher) {
+                float dlt;
+                {
+#pragma clang fp contract(off)
+                    dlt = SAME ? (z[r] - zs[r]) : (sT * z[r] - sS * zs[r]);
+                }
+                asum = fmaf(e, dlt, asum);
+            }
+        }
+        R.z += zsum;
+        if (teacher) Aacc += asum;
+    }
+
+    // Add kMasked to the rows of a shifted last tile whose vocabulary index is below
+    // vlo, with one MFMA per block (A: kMasked in k = 0 of masked rows, B: ones), so the
+    // accumulators are only ever touched by MFMAs.
+    static __device__ __forceinline__ void mask_mma(const Lane &L, floatx16 (&accS)[4][2],
+                                                    floatx16 (&accT)[4][2], int row0, int vlo) {
+        bf16x8 ones, bias[4];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb) {
+            const int v = row0 + L.wv * 128 + vb * 32 + L.l32;   // A-operand row of this lane
+#pragma unroll
+            for (int e = 0; e < 8; ++e) bias[vb][e] = (__bf16)0.0f;
+            if (L.h == 0 && v < vlo) bias[vb][0] = (__bf16)kMasked;
+        }
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                accS[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bias[vb], ones,
+                                                                       accS[vb][cb], 0, 0, 0);
+                if (HAS_T)
+                    accT[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bias[vb], ones,
+                                                                           accT[vb][cb], 0, 0, 0);
+            }
+    }
+
+    // Fold the lane's 2 columns x 64 rows of both models, block by block.
+    static __device__ __forceinline__ void fold(const floatx16 (&accS)[4][2],
+                                                const floatx16 (&accT)[4][2], Run (&RS)[2],
+                                                Run (&RT)[2], float (&A)[2], const ScoreArgs &a,
+                                                int vbase) {
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+            for (int vb = 0; vb < 4; ++vb) {
+                // Keep the scheduler from hoisting accumulator reads of later blocks.
+                __builtin_amdgcn_sched_barrier(0);
+                float zs[16], zt[16];
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    zs[r] = agpr_read(accS[vb][cb][r]);
+                    if (HAS_T) zt[r] = agpr_read(accT[vb][cb][r]);
+                }
+                fold_block(zs, RS[cb], A[cb], false, zs, a.cS, a.sS, a.sT, vbase + vb * 32);
+                if (HAS_T) fold_block(zt, RT[cb], A[cb], true, zs, a.cT, a.sS, a.sT, vbase + vb * 32);
+            }
+    }
+
+    static __device__ __forceinline__ void zero_acc(floatx16 (&accS)[4][2],
+                                                    floatx16 (&accT)[4][2]) {
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                accS[vb][cb] = floatx16{0.f};
+                if (HAS_T) accT[vb][cb] = floatx16{0.f};
+            }
+    }
+
+    static __device__ __forceinline__ void merge_run(Run &x, float &xa, const Run &y, float ya,
+                                                     float c) {
+        Stat a{x.best, x.sec, x.idx, x.z}, b{y.best, y.sec, y.idx, y.z};
+        stat_merge(a, xa, b, ya, c);
+        x.best = a.best; x.sec = a.sec; x.idx = a.idx; x.z = a.z;
+    }
+
+    static __device__ void run(ScoreArgs a) {
+        const int t_valid = a.sched->t_valid;
+        const int n_p = a.sched->n_ptiles;
+        const int ns = a.sched->n_splits;
+        const int n_units = a.sched->n_units;
+        Lane L;
+        L.lane = threadIdx.x & 63;
+        L.wid = threadIdx.x >> 6;
+        L.wv = L.wid & 1;
+        L.wt = L.wid >> 1;
+        L.h = L.lane >> 5;
+        L.l32 = L.lane & 31;
+#pragma unroll
+        for (int s = 0; s < 2; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+        const int nS = a.ds / 32, nT = HAS_T ? a.dt / 32 : 0;
+        const int spv = nS + nT;
+        // W DMA rows: R = (wid*4 + i)*16 + lane/4, chunk = (lane&3) ^ swz(R).
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int R = (L.wid * 4 + i) * 16 + (L.lane >> 2);
+            const int ch = (L.lane & 3) ^ swz(R);
+            L.wvoff[0][i] = (uint32_t)(R * a.ds * 2 + ch * 16);
+            L.wvoff[1][i] = HAS_T ? (uint32_t)(R * a.dt * 2 + ch * 16) : 0u;
+        }
+        const int G = gridDim.x;
+        const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+        const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+        const int nsb = ns >> 2, rem = ns & 3;
+        const int64_t full_units = (int64_t)nsb * 4 * n_p;
+
+        for (int64_t q = my; q < n_units; q += G) {
+            int p, s;
+            if (q < full_units) {
+                const int64_t w = q % (4 * (int64_t)n_p);
+                p = (int)(w >> 2);
+                s = (int)(q / (4 * (int64_t)n_p)) * 4 + (int)(w & 3);
+            } else {
+                const int64_t w = q - full_units;
+                p = (int)(w / rem);
+                s = nsb * 4 + (int)(w % rem);
+            }
+            // H DMA rows of this position tile.
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int R = (L.wid * 2 + i) * 16 + (L.lane >> 2);
+                const int ch = (L.lane & 3) ^ swz(R);
+                int j = p * BT + R;
+                j = j < t_valid ? j : t_valid - 1;
+                const int64_t g = a.rowmap[j] & 0x7fffffffu;
+                L.hp[0][i] = (const char *)a.hs + g * a.ds * 2 + ch * 16;
+                L.hp[1][i] = HAS_T ? (const char *)a.ht + g * a.dt * 2 + ch * 16 : nullptr;
+            }
+            const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
+            const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
+            const int total = (vt1 - vt0) * spv;
+
+            Run RS[2], RT[2];
+            float AA[2] = {0.f, 0.f};
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                RS[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
+                RT[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
+            }
+            floatx16 accS[4][2], accT[4][2];
+#pragma unroll
+            for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    accS[vb][cb] = floatx16{0.f};
+                    accT[vb][cb] = floatx16{0.f};
+                }
+
+            // Issue cursor: (vtile, position within the vtile's steps).
+            int ivt = vt0, ir = 0;
+            auto adv = [&]() { if (++ir == spv) { ir = 0; ++ivt; } };
+            auto im = [&]() { return ir < nS ? 0 : 1; };
+            auto ik = [&]() { return ir < nS ? ir : ir - nS; };
+            // Prologue: steps 0, 1, 2 (total >= 4 always).
+            issue<0>(a, L, im(), ik(), ivt); adv();
+            issue<1>(a, L, im(), ik(), ivt); adv();
+            issue<2>(a, L, im(), ik(), ivt); adv();
+
+            int n = 0;   // global step index within the unit
+#define OLIVE_STEP(S_, ACC_)                                                             \
+            {                                                                            \
+                step<S_>(a, L, im(), ik(), ivt, ACC_);                                   \
+                if (n + S_ + 3 < total) adv();                                           \
+            }
+            for (int vt = vt0; vt < vt1; ++vt) {
+                // The last tile, when V is not a multiple of 256, is shifted back to end
+                // at V; its rows below vt*BV were covered by the previous tile. One more
+                // MFMA adds -1e30 to those rows (|z| << 1e30 is absorbed), so they drop
+                // out of every statistic and the fold needs no masking.
+                const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+                const int vbase = row0 + L.wv * 128 + 4 * L.h;
+                zero_acc(accS, accT);
+                // Each model's step count is a multiple of the ring depth (4), so the
+                // stage of a step is static inside these loops.
+                for (int k = 0; k < nS; k += 4, n += 4) {
+                    OLIVE_STEP(0, accS) OLIVE_STEP(1, accS) OLIVE_STEP(2, accS) OLIVE_STEP(3, accS)
+                }
+                if (HAS_T) {
+                    for (int k = 0; k < nT; k += 4, n += 4) {
+                        OLIVE_STEP(0, accT) OLIVE_STEP(1, accT) OLIVE_STEP(2, accT)
+                        OLIVE_STEP(3, accT)
+                    }
+                }
+                if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
+                fold(accS, accT, RS, RT, AA, a, vbase);
+            }
+#undef OLIVE_STEP
+
+            // Merge lanes l and l+32 (same columns, interleaved vocabulary rows).
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                Run o{__shfl_xor(RS[cb].best, 32), __shfl_xor(RS[cb].sec, 32),
+                      __shfl_xor(RS[cb].z, 32), __shfl_xor(RS[cb].idx, 32)};
+                float dummy = 0.f;
+                merge_run(RS[cb], dummy, o, 0.f, a.cS);
+                if (HAS_T) {
+                    Run q2{__shfl_xor(RT[cb].best, 32), __shfl_xor(RT[cb].sec, 32),
+                           __shfl_xor(RT[cb].z, 32), __shfl_xor(RT[cb].idx, 32)};
+                    float qa = __shfl_xor(AA[cb], 32);
+                    merge_run(RT[cb], AA[cb], q2, qa, a.cT);
+                }
+            }
+            // Merge the two vocabulary halves (wv = 1 into wv = 0) through LDS, once
+            // the trailing prefetches into the stages have landed.
+            float *xs = (float *)g_lw0;   // [wt][cb][l32][9]
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __builtin_amdgcn_s_barrier();
+            compiler_fence();
+            if (L.wv == 1 && L.h == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 9;
+                    o[0] = RS[cb].best; o[1] = RS[cb].sec; o[2] = __int_as_float(RS[cb].idx);
+                    o[3] = RS[cb].z;
+                    o[4] = RT[cb].best; o[5] = RT[cb].sec; o[6] = __int_as_float(RT[cb].idx);
+                    o[7] = RT[cb].z; o[8] = AA[cb];
+                }
+            }
+            compiler_fence();
+            __syncthreads();
+            if (L.wv == 0 && L.h == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 9;
+                    Run ys{o[0], o[1], o[3], __float_as_int(o[2])};
+                    float dummy = 0.f;
+                    merge_run(RS[cb], dummy, ys, 0.f, a.cS);
+                    if (HAS_T) {
+                        Run yt{o[4], o[5], o[7], __float_as_int(o[6])};
+                        merge_run(RT[cb], AA[cb], yt, o[8], a.cT);
+                    }
+                    const int j = p * BT + L.wt * 64 + cb * 32 + L.l32;
+                    if (j < t_valid) {
+                        float *P = a.part;
+                        const int64_t ps = a.pstride;
+                        P[(F_BEST_S * MAX_SPLITS + s) * ps + j] = RS[cb].best;
+                        P[(F_SEC_S * MAX_SPLITS + s) * ps + j] = RS[cb].sec;
+                        P[(F_IDX_S * MAX_SPLITS + s) * ps + j] = __int_as_float(RS[cb].idx);
+                        P[(F_Z_S * MAX_SPLITS + s) * ps + j] = RS[cb].z;
+                        if (HAS_T) {
+                            P[(F_BEST_T * MAX_SPLITS + s) * ps + j] = RT[cb].best;
+                            P[(F_SEC_T * MAX_SPLITS + s) * ps + j] = RT[cb].sec;
+                            P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT[cb].idx);
+                            P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT[cb].z;
+                            P[(F_A * MAX_SPLITS + s) * ps + j] = AA[cb];
+                        }
+                    }
+                }
+            }
+            compiler_fence();
+            __syncthreads();
+        }
+    }
+};
+
+template <bool HAS_T, bool SAME>
+__global__ void __launch_bounds__(256, 1) score_mfma_kernel(ScoreArgs a) {
+    Kernel<HAS_T, SAME>::run(a);
+}
+
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, int grid,
+                             hipStream_t st) {
+    if (grid <= 0) return hipSuccess;
+    if (has_t) {
+        if (same_scale) score_mfma_kernel<true, true><<<grid, 256, 0, st>>>(a);
+        else score_mfma_kernel<true, false><<<grid, 256, 0, st>>>(a);
+    } else {
+        score_mfma_kernel<false, true><<<grid, 256, 0, st>>>(a);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace olive

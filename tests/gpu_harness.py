@@ -1,0 +1,185 @@
+"""Shared helpers of the GPU tests: run the HIP path through the C ABI and the fp64
+oracle on the same seeded workload, and compare them at the acceptance tolerances.
+
+Tolerances: per-token log-prob within 2e-3 absolute; per-position KL within
+1e-3 + 1e-3 |KL|; masked counts, valid counts and greedy argmax bit-exact; Eq. 1's
+per-sequence loss within 1e-3 relative (plus 1e-3 absolute for tiny sums).
+"""
+import math
+import sys
+import time
+
+import numpy as np
+import torch
+
+from oracle import olive_oracle as O
+from paper_2609_36246_amd import _lib as L
+
+LOGP_ATOL = 2e-3
+KL_ATOL = 1e-3
+KL_RTOL = 1e-3
+CE_RTOL = 1e-3
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+    sys.stdout.flush()
+
+
+def to_np(t):
+    if t is None:
+        return None
+    if t.dtype == torch.bfloat16:
+        t = t.float()
+    return t.detach().cpu().numpy()
+
+
+def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
+            outputs=("kl", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
+            poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1):
+    """Score a workload on the GPU; returns numpy outputs (and stats)."""
+    dev = wl["h_student"].device
+    spec = wl["spec"]
+    T = wl["total_positions"]
+    B = wl["cu_seqlens"].shape[0] - 1
+    own = ctx is None
+    if own:
+        flags = (L.OLIVE_FLAG_SIMPLE_KERNEL if simple else 0) | \
+                (L.OLIVE_FLAG_KERNEL_TIMING if timing else 0)
+        desc = L.make_desc(spec.vocab, spec.d_student, 0 if student_only else spec.d_teacher,
+                           L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
+                           wl["scale_student"], wl["scale_teacher"], max_positions=T,
+                           max_seqs=B, flags=flags)
+        ctx = L.olive_score_init(desc, wl["w_student"],
+                                 None if student_only else wl["w_teacher"])
+    fill = float("nan") if poison else 0.0
+
+    def f32():
+        return torch.full((T,), fill, dtype=torch.float32, device=dev)
+
+    def i32():
+        return torch.full((T,), -7, dtype=torch.int32, device=dev)
+    out = {}
+    out["kl"] = f32() if "kl" in outputs and not student_only else None
+    out["counts"] = torch.full((2,), -1, dtype=torch.int64, device=dev) \
+        if "counts" in outputs else None
+    out["logp_s"] = f32() if "logp_s" in outputs else None
+    out["logp_t"] = f32() if "logp_t" in outputs and not student_only else None
+    out["am_s"] = i32() if "am_s" in outputs else None
+    out["am_t"] = i32() if "am_t" in outputs and not student_only else None
+    out["ce"] = torch.full((B,), fill, dtype=torch.float32, device=dev) \
+        if "ce" in outputs and not student_only else None
+    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
+                         None if student_only else wl["h_teacher"], wl["valid_len"], region)
+    for _ in range(repeat):
+        if student_only or out["kl"] is None:
+            L.olive_token_logprobs(ctx, batch, out["logp_s"], out["logp_t"], out["am_s"],
+                                   out["am_t"])
+        else:
+            L.olive_kl_masked(ctx, batch, out["kl"], out["counts"], out["logp_s"], out["logp_t"],
+                              out["am_s"], out["am_t"], out["ce"])
+    torch.cuda.synchronize()
+    res = {k: to_np(v) for k, v in out.items() if v is not None}
+    res["stats"] = L.olive_score_last_stats(ctx)
+    res["err"] = L.olive_score_last_error(ctx)
+    if keep_ctx:
+        res["ctx"] = ctx
+    elif own:
+        L.olive_score_free(ctx)
+    return res
+
+
+def oracle_rows(wl, rows, student_only=False):
+    """fp64 oracle on a subset of packed rows (all rows treated as valid)."""
+    rows = np.asarray(rows, dtype=np.int64)
+    idx = torch.from_numpy(rows).to(wl["h_student"].device)
+    hs = to_np(wl["h_student"][idx])
+    ht = None if student_only else to_np(wl["h_teacher"][idx])
+    y = to_np(wl["targets"][idx])
+    ws = to_np(wl["w_student"])
+    wt = None if student_only else to_np(wl["w_teacher"])
+    t0 = time.time()
+    r = O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"])
+    say("oracle on %d rows took %.1fs" % (len(rows), time.time() - t0))
+    return r
+
+
+def structure_np(wl):
+    return (to_np(wl["cu_seqlens"]), to_np(wl["cut"]),
+            None if wl["valid_len"] is None else to_np(wl["valid_len"]))
+
+
+def stratified_rows(wl, n_random=128, seed=1):
+    """Rows of a large workload the oracle evaluates: around every cut and end of
+    sequence, first/last rows, every outlier row, and random rows."""
+    cu, cut, vl = structure_np(wl)
+    B = len(cu) - 1
+    lengths = np.diff(cu)
+    vlen = lengths if vl is None else vl
+    picks = set()
+    for b in range(B):
+        for t in (0, cut[b] - 1, cut[b], cut[b] + 1, vlen[b] - 1, vlen[b], lengths[b] - 1):
+            if 0 <= t < lengths[b]:
+                picks.add(int(cu[b] + t))
+    for r in wl.get("outlier_rows", []):
+        picks.add(int(r))
+    rng = np.random.default_rng(seed)
+    T = int(cu[-1])
+    picks.update(int(x) for x in rng.choice(T, size=min(n_random, T), replace=False))
+    return np.array(sorted(picks), dtype=np.int64)
+
+
+def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, check_ce=True,
+            label=""):
+    """Compare HIP outputs with the oracle, element by element, at the acceptance bar."""
+    cu, cut, vl = structure_np(wl)
+    m = O.masks(cu, cut, vl, region)
+    T = len(m["valid"])
+    if "counts" in hip:
+        assert int(hip["counts"][0]) == m["n_scored"], (label, hip["counts"], m["n_scored"])
+        assert int(hip["counts"][1]) == m["t_valid"], (label, hip["counts"], m["t_valid"])
+    valid, inr = m["valid"], m["in_region"]
+    # fixed values outside the valid prefix, bit-exact
+    inval = ~valid
+    assert np.all(hip["logp_s"][inval] == 0.0), label
+    if "am_s" in hip:
+        assert np.all(hip["am_s"][inval] == -1), label
+    if not student_only and "kl" in hip:
+        assert np.all(hip["kl"][~inr] == 0.0) and not np.any(np.signbit(hip["kl"][~inr])), label
+    sel = np.arange(T) if rows is None else np.asarray(rows)
+    sel = sel[valid[sel]]
+    r = oracle_rows(wl, sel, student_only)
+    worst = {}
+
+    def chk(name, got, want, atol, rtol=0.0):
+        err = np.abs(got - want)
+        bound = atol + rtol * np.abs(want)
+        bad = np.nonzero(~(err <= bound))[0]
+        worst[name] = float(err.max()) if err.size else 0.0
+        assert bad.size == 0, "%s %s: %d/%d rows off, first row %d got %r want %r" % (
+            label, name, bad.size, err.size, sel[bad[0]], got[bad[0]], want[bad[0]])
+    chk("logp_s", hip["logp_s"][sel], r["logp_s"], LOGP_ATOL)
+    if "am_s" in hip:
+        mism = np.nonzero(hip["am_s"][sel] != r["argmax_s"])[0]
+        assert mism.size == 0, "%s argmax_s mismatch at rows %s (gap %s)" % (
+            label, sel[mism[:5]], r["gap_s"][mism[:5]])
+    if not student_only:
+        if "logp_t" in hip:
+            chk("logp_t", hip["logp_t"][sel], r["logp_t"], LOGP_ATOL)
+        if "am_t" in hip:
+            mism = np.nonzero(hip["am_t"][sel] != r["argmax_t"])[0]
+            assert mism.size == 0, "%s argmax_t mismatch at rows %s (gap %s)" % (
+                label, sel[mism[:5]], r["gap_t"][mism[:5]])
+        if "kl" in hip:
+            want = np.where(inr[sel], r["kl"], 0.0)
+            chk("kl", hip["kl"][sel], want, KL_ATOL, KL_RTOL)
+        if check_ce and "ce" in hip and rows is None:
+            B = len(cu) - 1
+            for b in range(B):
+                idx = np.nonzero((m["seq_id"] == b) & inr)[0]
+                want = -math.fsum(r["logp_s"][np.searchsorted(sel, idx)].tolist()) \
+                    if idx.size else 0.0
+                assert abs(hip["ce"][b] - want) <= CE_RTOL * abs(want) + 1e-3, (label, b)
+    say("%s parity ok on %d rows; worst %s" % (label, sel.size,
+                                                {k: "%.2e" % v for k, v in worst.items()}))
+    return r

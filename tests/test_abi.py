@@ -1,0 +1,118 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library must load, export every function declared in include/olive_score.h,
+describe every status code, and reject malformed arguments on the host before it
+touches the device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_36246_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "olive_score.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(L.LIB_PATH):
+        from paper_2609_36246_amd import build
+        build.build()
+    return L.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(olive_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for n in ("olive_score_init", "olive_token_logprobs", "olive_kl_masked",
+              "olive_score_free", "olive_status_string", "olive_score_last_error",
+              "olive_score_last_stats", "olive_score_kernel_times"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for n in declared_functions():
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    seen = set()
+    for code in L.STATUS_CODES:
+        s = L.olive_status_string(code)
+        assert s.startswith("OLIVE_")
+        seen.add(s)
+    assert len(seen) == len(L.STATUS_CODES)
+    assert "unknown" in L.olive_status_string(99)
+
+
+def test_struct_layouts_match_header():
+    assert ctypes.sizeof(L.olive_score_desc) == 48
+    assert L.olive_score_desc.max_positions.offset == 32
+    assert ctypes.sizeof(L.olive_batch) == 64
+    assert L.olive_batch.h_teacher.offset == 56
+
+
+def _init(desc, ws=1, wt=1):
+    return L.olive_score_init(desc, ws, wt, stream=None, check=False)
+
+
+@pytest.mark.parametrize("field,value,expect", [
+    ("dtype", 7, L.OLIVE_E_DTYPE),
+    ("w_layout", 5, L.OLIVE_E_DTYPE),
+    ("vocab", 0, L.OLIVE_E_SHAPE),
+    ("vocab", 1 << 31, L.OLIVE_E_SHAPE),
+    ("d_student", 0, L.OLIVE_E_SHAPE),
+    ("d_teacher", -1, L.OLIVE_E_SHAPE),
+    ("max_positions", 0, L.OLIVE_E_SHAPE),
+    ("max_seqs", 0, L.OLIVE_E_SHAPE),
+    ("d_student", 20000, L.OLIVE_E_UNSUPPORTED),
+    ("logit_scale_student", 0.0, L.OLIVE_E_RANGE),
+    ("logit_scale_student", float("inf"), L.OLIVE_E_RANGE),
+    ("logit_scale_teacher", -1.0, L.OLIVE_E_RANGE),
+    ("logit_scale_teacher", float("nan"), L.OLIVE_E_RANGE),
+    ("flags", 64, L.OLIVE_E_RANGE),
+])
+def test_init_rejects_bad_descriptors_on_host(lib, field, value, expect):
+    d = L.make_desc(1000, 64, 96, max_positions=64, max_seqs=2)
+    setattr(d, field, value)
+    status, handle = _init(d)
+    assert status == expect and handle is None
+
+
+def test_init_null_pointers(lib):
+    d = L.make_desc(1000, 64, 96, max_positions=64, max_seqs=2)
+    assert _init(d, ws=None)[0] == L.OLIVE_E_NULL
+    assert _init(d, wt=None)[0] == L.OLIVE_E_NULL
+    h = ctypes.c_void_p()
+    assert lib.olive_score_init(ctypes.byref(h), None, 1, 1, None) == L.OLIVE_E_NULL
+    assert lib.olive_score_init(None, ctypes.byref(d), 1, 1, None) == L.OLIVE_E_NULL
+
+
+def test_calls_on_null_context(lib):
+    b = L.olive_batch()
+    assert lib.olive_token_logprobs(None, ctypes.byref(b), 1, None, None, None,
+                                    None) == L.OLIVE_E_NULL
+    assert lib.olive_kl_masked(None, ctypes.byref(b), 1, None, None, None, None, None, None,
+                               None) == L.OLIVE_E_NULL
+    assert lib.olive_score_free(None) == L.OLIVE_OK
+    v = ctypes.c_int32()
+    assert lib.olive_score_last_error(None, ctypes.byref(v)) == L.OLIVE_E_NULL
+    out = (ctypes.c_int64 * 4)()
+    assert lib.olive_score_last_stats(None, out) == L.OLIVE_E_NULL
+    f = (ctypes.c_float * 4)()
+    assert lib.olive_score_kernel_times(None, f, 1) == L.OLIVE_E_NULL
+
+
+def test_binding_refuses_to_run_without_the_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(L, "_lib", None)
+    monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        L.load()

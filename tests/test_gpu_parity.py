@@ -1,0 +1,181 @@
+"""GPU parity of the HIP scoring path against the fp64 oracle (through the C ABI).
+
+Small workloads are compared on every position (they span several vocabulary and
+position tiles and end in ragged tails); the five named workloads are compared in
+full where the oracle finishes in seconds (tiny, small) and on a stratified row
+sample otherwise (large_vocab, long_rollout, ragged), at the launch configuration
+the benchmark times. Masks and counts are always compared in full.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import olive_oracle as O
+from paper_2609_36246_amd import _lib as L
+from paper_2609_36246_amd import workloads as W
+from tests.gpu_harness import compare, run_hip, say, stratified_rows
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    L.load()
+
+
+def custom(name, seed=0, **kw):
+    spec = W.custom_spec(name=name, **kw)
+    return W.make_workload(name, seed, device="cuda", spec=spec)
+
+
+CASES = {
+    # ragged lengths, V not a multiple of 256, EOS cut-off, 3 position tiles
+    "ragged_v1000": dict(num_seqs=3, ragged_len=(40, 300), vocab=1000, d_student=128,
+                         d_teacher=256, cut_rule=("frac", 0.1, 0.9), eos=True),
+    # several vocabulary tiles per split, many position tiles, peaked (scale 4)
+    "multi_tile": dict(num_seqs=5, ragged_len=(700, 1300), vocab=5000, d_student=256,
+                       d_teacher=128, logit_scale=4.0, target_source="student",
+                       cut_rule=("frac", 0.1, 0.9)),
+    # vocabulary a multiple of 256, teacher-sampled targets, outlier rows
+    "even_v": dict(num_seqs=2, seq_len=200, vocab=2048, d_student=384, d_teacher=512,
+                   target_source="teacher", cut_rule=("abs", 1, 199), outlier_frac=0.05,
+                   outlier_mul=8.0),
+}
+
+
+@pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
+@pytest.mark.parametrize("case", list(CASES))
+def test_custom_parity_full(case, simple):
+    say("custom parity", case, "generic" if simple else "mfma")
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl, simple=simple)
+    assert hip["stats"]["kernel"] == ("generic" if simple else "mfma")
+    assert hip["err"] == 0
+    compare(hip, wl, label=case)
+
+
+@pytest.mark.parametrize("region", [O.REGION_TEACHER, O.REGION_STUDENT, O.REGION_ALL])
+def test_regions(region):
+    say("regions", region)
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    hip = run_hip(wl, region=region)
+    compare(hip, wl, region=region, label="region%d" % region)
+
+
+def test_different_scales_general_difference_path():
+    say("different logit scales")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    wl["scale_student"], wl["scale_teacher"] = 1.0, 2.5
+    for simple in (False, True):
+        hip = run_hip(wl, simple=simple)
+        compare(hip, wl, label="scales-%s" % ("generic" if simple else "mfma"))
+
+
+def test_student_only_token_logprobs():
+    say("student only")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    hip = run_hip(wl, student_only=True, outputs=("logp_s", "am_s"))
+    compare(hip, wl, student_only=True, label="student-only")
+
+
+def test_tiny_workload_full():
+    say("tiny workload (fp32, generic kernel)")
+    wl = W.make_workload("tiny", 0, device="cuda")
+    hip = run_hip(wl)
+    assert hip["stats"]["kernel"] == "generic"
+    compare(hip, wl, label="tiny")
+
+
+def test_small_workload_full():
+    say("small workload full parity")
+    wl = W.make_workload("small", 0, device="cuda")
+    hip = run_hip(wl)
+    assert hip["stats"]["kernel"] == "mfma"
+    say("small stats", hip["stats"])
+    compare(hip, wl, label="small")
+
+
+@pytest.mark.parametrize("name", ["large_vocab", "long_rollout", "ragged"])
+def test_large_workload_sampled(name):
+    say("workload", name, "sampled parity")
+    wl = W.make_workload(name, 0, device="cuda")
+    hip = run_hip(wl)
+    say(name, "stats", hip["stats"])
+    assert hip["stats"]["kernel"] == "mfma"
+    rows = stratified_rows(wl, n_random=96)
+    compare(hip, wl, rows=rows, label=name)
+    del wl
+    torch.cuda.empty_cache()
+
+
+# ----------------------------------------------------------------------------- properties
+def test_identical_teacher_gives_exact_zero_kl():
+    say("teacher == student")
+    wl = custom("multi_tile", **CASES["multi_tile"])
+    wl["h_teacher"] = wl["h_student"]
+    wl["w_teacher"] = wl["w_student"]
+    spec = wl["spec"]
+    wl["spec"] = W.custom_spec(name="same", num_seqs=spec.num_seqs, ragged_len=spec.ragged_len,
+                               vocab=spec.vocab, d_student=spec.d_student,
+                               d_teacher=spec.d_student, logit_scale=spec.logit_scale)
+    for simple in (False, True):
+        hip = run_hip(wl, simple=simple, region=O.REGION_ALL)
+        assert np.all(hip["kl"] == 0.0)
+        np.testing.assert_array_equal(hip["logp_s"], hip["logp_t"])
+        np.testing.assert_array_equal(hip["am_s"], hip["am_t"])
+
+
+def test_duplicate_best_column_takes_lowest_index():
+    say("duplicate best column")
+    wl = custom("even_v", **CASES["even_v"])
+    hip = run_hip(wl)
+    # copy the winning column of row 0 to a lower index: every row whose greedy token
+    # was that column now ties, and must report the lower index
+    j = int(hip["am_s"][0])
+    lo = j // 3
+    wl["w_student"][:, lo] = wl["w_student"][:, j]
+    hip2 = run_hip(wl)
+    tied = hip["am_s"] == j
+    assert tied.any()
+    assert np.all(hip2["am_s"][tied] == lo)
+    compare(hip2, wl, label="dup-column")
+
+
+def test_deterministic_and_fully_written():
+    say("determinism / poisoned outputs")
+    wl = custom("multi_tile", **CASES["multi_tile"])
+    a = run_hip(wl, poison=True)
+    b = run_hip(wl, poison=True)
+    for k in ("kl", "logp_s", "logp_t", "ce"):
+        assert not np.isnan(a[k]).any(), k
+        np.testing.assert_array_equal(a[k], b[k])
+    for k in ("am_s", "am_t"):
+        np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_cut_extremes():
+    say("cut = 0 and cut = len")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    cu = wl["cu_seqlens"].cpu().numpy()
+    lens = np.diff(cu)
+    wl["valid_len"] = None
+    wl["cut"] = torch.zeros_like(wl["cut"])
+    h0 = run_hip(wl)
+    assert int(h0["counts"][0]) == int(h0["counts"][1]) == int(cu[-1])
+    compare(h0, wl, label="cut0")
+    wl["cut"] = torch.from_numpy(lens.astype(np.int32)).cuda()
+    hl = run_hip(wl)
+    assert int(hl["counts"][0]) == 0
+    assert np.all(hl["kl"] == 0.0) and np.all(hl["ce"] == 0.0)
+
+
+def test_bad_target_sets_error_word_and_nan():
+    say("bad target")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    wl["valid_len"] = None
+    wl["targets"][5] = wl["spec"].vocab + 3
+    hip = run_hip(wl)
+    assert hip["err"] & 1
+    assert np.isnan(hip["logp_s"][5])
+    assert not np.isnan(hip["logp_s"][6])
