@@ -71,8 +71,8 @@ typedef enum {
 /* Fixed at init. */
 typedef struct {
     int64_t vocab;              /* V >= 1, shared by both models, V < 2^31 */
-    int32_t d_student;          /* hidden width of S, in [1, 16384] */
-    int32_t d_teacher;          /* hidden width of T in [1, 16384], or 0 for student-only */
+    int32_t d_student;          /* hidden width of S, in [1, 12288] */
+    int32_t d_teacher;          /* hidden width of T in [1, 12288], or 0 for student-only */
     int32_t dtype;              /* olive_dtype of h and W */
     int32_t w_layout;           /* olive_wlayout of the weights passed to init */
     float logit_scale_student;  /* s_S, finite and > 0 (1.0 = temperature 1) */

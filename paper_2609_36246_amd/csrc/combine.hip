@@ -16,7 +16,7 @@
 namespace olive {
 
 // Relative top-2 gap (in scaled logits) below which the greedy token is re-decided.
-constexpr float kTieWindow = 1.0f / 16384.0f;
+constexpr float kTieWindow = 1.0f / 65536.0f;
 
 template <typename E>
 __device__ __forceinline__ float wave_dot(const E *h, const E *w, int d, int lane);

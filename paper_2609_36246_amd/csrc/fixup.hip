@@ -4,13 +4,13 @@
 // The scoring kernels take the argmax of fp32 logits. Where the best and second
 // best are closer than the window, rounding could have swapped them relative to
 // the exact values. For each such (row, model) this pass recomputes every logit of
-// the row in fp32 together with a rigorous rounding bound
-//   e_v = d * 2^-23 * sum_k |h_k| |w_kv|,
-// keeps the entries that could still be the exact maximum
+// the row in fp32 and bounds its rounding error by
+//   e_v = d * 2^-23 * ||h|| * ||w_v||  >=  d * 2^-23 * sum_k |h_k| |w_kv|
+// (Cauchy-Schwarz; the weight-row norms are computed once at init). Entries that
+// could still be the exact maximum,
 //   z_v + e_v >= theta = (fp32 max of the scoring pass) - (its own bound),
-// evaluates those in fp64 and picks the largest, lowest index first. The work is
-// split over vocabulary chunks (phase 1) and merged per row in a fixed order
-// (phase 2).
+// are evaluated in fp64 and the largest wins, lowest index first. The work is split
+// over vocabulary chunks (phase 1) and merged per row in a fixed order (phase 2).
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -27,13 +27,49 @@ struct FxResult {
     int32_t pad;
 };
 
+// 8 consecutive elements of a row as fp32 (one 16-byte load for bf16, two for fp32).
+__device__ __forceinline__ void load8(const uint16_t *p, float (&x)[8]) {
+    const uint4 q = *(const uint4 *)p;
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        x[2 * i] = __uint_as_float(w[i] << 16);
+        x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+}
+__device__ __forceinline__ void load8(const float *p, float (&x)[8]) {
+    const float4 a = *(const float4 *)p, b = *(const float4 *)(p + 4);
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+// Squared L2 norm of every weight row (init only): one wavefront per row.
+template <typename E>
+__global__ void __launch_bounds__(256)
+row_norm_kernel(const E *__restrict__ w, int64_t V, int d, float *__restrict__ out) {
+    const int lane = threadIdx.x & 63;
+    for (int64_t v = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); v < V;
+         v += (int64_t)gridDim.x * 4) {
+        const E *r = w + v * d;
+        double acc = 0.0;
+        for (int k = lane; k < d; k += 64) {
+            const double x = load_elem(r, k);
+            acc += x * x;
+        }
+        for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+        if (lane == 0) out[v] = (float)sqrt(acc) * 1.0001f;   // rounded up
+    }
+}
+
 template <typename E>
 __global__ void __launch_bounds__(FX_THREADS)
 fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int n_chunks,
+                  const float *__restrict__ wn_s, const float *__restrict__ wn_t,
                   FxResult *__restrict__ out) {
     extern __shared__ float hrow[];
     __shared__ double red_v[FX_THREADS];
     __shared__ int red_i[FX_THREADS];
+    __shared__ float s_hn;
     const int nf_all = a.sched->n_flagged;
     const int nf = nf_all < cap ? nf_all : cap;
     const int64_t n_items = (int64_t)nf * n_chunks * 2;
@@ -48,25 +84,49 @@ fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int
         const float theta = __int_as_float(flagged[4 * f + 2 + m]);
         double best_v = -__builtin_inf();
         int best_i = 0x7fffffff;
-        if (mask & (1 << m)) {
+        if (mask & (1 << m)) {   // uniform over the workgroup
             const int d = m ? a.dt : a.ds;
             const E *h = (const E *)(m ? a.ht : a.hs) + (int64_t)(a.rowmap[j] & 0x7fffffffu) * d;
             const E *w = (const E *)(m ? a.wt : a.ws);
+            const float *wn = m ? wn_t : wn_s;
             __syncthreads();
             for (int k = tid; k < d; k += FX_THREADS) hrow[k] = load_elem(h, k);
             __syncthreads();
-            const float bound = (float)d * (1.0f / 8388608.0f);
-            for (int v = c * FX_CHUNK + tid; v < (c + 1) * FX_CHUNK && v < a.V; v += FX_THREADS) {
-                const E *wr = w + (int64_t)v * d;
-                float z = 0.f, za = 0.f;
-                for (int k = 0; k < d; ++k) {
-                    float wv = load_elem(wr, k);
-                    z = fmaf(hrow[k], wv, z);
-                    za = fmaf(fabsf(hrow[k]), fabsf(wv), za);
+            if (tid == 0) {
+                double hh = 0.0;
+                for (int k = 0; k < d; ++k) hh += (double)hrow[k] * hrow[k];
+                s_hn = (float)sqrt(hh) * 1.0001f;
+            }
+            __syncthreads();
+            const float ebound = (float)d * (1.0f / 8388608.0f) * s_hn;
+            // 8 lanes per vocabulary row: each pass of a group reads 128 contiguous
+            // bytes of its row (coalesced), 8 rows per wavefront at a time.
+            const int lane = tid & 63, g8 = lane & 7;
+            const int rows_per_pass = FX_THREADS / 8;
+            const bool vec = (d & 63) == 0 && (((uintptr_t)w & 15) == 0);
+            const int v_end = (c + 1) * FX_CHUNK < a.V ? (c + 1) * FX_CHUNK : a.V;
+            for (int v0 = c * FX_CHUNK; v0 < v_end; v0 += rows_per_pass) {
+                const int v = v0 + (tid >> 3);
+                const bool ok = v < v_end;
+                const E *wr = w + (int64_t)(ok ? v : v_end - 1) * d;
+                float z = 0.f;
+                if (vec) {
+                    for (int k = g8 * 8; k < d; k += 64) {
+                        float x[8];
+                        load8(wr + k, x);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) z = fmaf(hrow[k + q], x[q], z);
+                    }
+                } else {
+                    for (int k = g8; k < d; k += 8) z = fmaf(hrow[k], load_elem(wr, k), z);
                 }
-                if (z + bound * za >= theta) {
+                z += __shfl_xor(z, 1);
+                z += __shfl_xor(z, 2);
+                z += __shfl_xor(z, 4);
+                if (ok && g8 == 0 && z + ebound * wn[v] >= theta) {
                     double zd = 0.0;
-                    for (int k = 0; k < d; ++k) zd = fma((double)hrow[k], (double)load_elem(wr, k), zd);
+                    for (int k = 0; k < d; ++k)
+                        zd = fma((double)hrow[k], (double)load_elem(wr, k), zd);
                     if (zd > best_v || (zd == best_v && v < best_i)) { best_v = zd; best_i = v; }
                 }
             }
@@ -89,6 +149,7 @@ fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int
             out[item].val = red_v[0];
             out[item].idx = red_i[0];
         }
+        __syncthreads();
     }
 }
 
@@ -118,16 +179,29 @@ fixup_merge_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, in
     }
 }
 
+hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *out,
+                            hipStream_t st) {
+    const int64_t blocks = (V + 3) / 4 < 4096 ? (V + 3) / 4 : 4096;
+    if (bf16)
+        row_norm_kernel<uint16_t><<<(unsigned)blocks, 256, 0, st>>>((const uint16_t *)w, V, d, out);
+    else
+        row_norm_kernel<float><<<(unsigned)blocks, 256, 0, st>>>((const float *)w, V, d, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
-                             void *scratch, int32_t *am_s, int32_t *am_t, hipStream_t st) {
+                             void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
+                             int32_t *am_t, hipStream_t st) {
     const int n_chunks = (a.V + FX_CHUNK - 1) / FX_CHUNK;
     const int dmax = a.ds > a.dt ? a.ds : a.dt;
     const size_t lds = (size_t)dmax * sizeof(float);
     FxResult *res = (FxResult *)scratch;
     if (bf16)
-        fixup_scan_kernel<uint16_t><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, res);
+        fixup_scan_kernel<uint16_t><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks,
+                                                                   wn_s, wn_t, res);
     else
-        fixup_scan_kernel<float><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, res);
+        fixup_scan_kernel<float><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, wn_s,
+                                                                wn_t, res);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     fixup_merge_kernel<<<64, 64, 0, st>>>(a, flagged, cap, n_chunks, res, am_s, am_t);

@@ -26,6 +26,7 @@ struct olive_score_ctx {
     int32_t *flagged = nullptr;
     int flag_cap = 0;
     void *fx_scratch = nullptr;
+    float *wn_s = nullptr, *wn_t = nullptr;     // weight-row L2 norms (rounding bounds)
     int32_t *err = nullptr;
     bool bf16 = false, has_t = false, mfma_ok = false;
     int last_kernel = -1, last_grid = 0;
@@ -44,7 +45,7 @@ void release(olive_score_ctx *c) {
         for (int i = 0; i < 64; ++i)
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
-                    c->logp_tmp, c->flagged, c->fx_scratch, c->err};
+                    c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -140,7 +141,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t 
     if (s) return s;
     if (flagged) {
         s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
-                                        am_s, has_t ? am_t : nullptr, st));
+                                        ctx->wn_s, ctx->wn_t, am_s, has_t ? am_t : nullptr, st));
         if (s) return s;
     }
     if (ce) {
@@ -180,7 +181,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (d.d_student < 1 || d.d_teacher < 0) return OLIVE_E_SHAPE;
     if (d.max_positions < 1 || d.max_positions >= ((int64_t)1 << 31) - 1) return OLIVE_E_SHAPE;
     if (d.max_seqs < 1) return OLIVE_E_SHAPE;
-    if (d.d_student > 16384 || d.d_teacher > 16384) return OLIVE_E_UNSUPPORTED;
+    if (d.d_student > 12288 || d.d_teacher > 12288) return OLIVE_E_UNSUPPORTED;
     if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
     if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
     if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING)) return OLIVE_E_RANGE;
@@ -199,7 +200,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         release(c);
         return OLIVE_E_HIP;
     }
-    c->mfma_ok = c->bf16 && (d.d_student % 128 == 0) && (d.d_teacher % 128 == 0) &&
+    c->mfma_ok = c->bf16 && (d.d_student % 32 == 0) && (d.d_teacher % 32 == 0) &&
                  d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL);
     const int esz = c->bf16 ? 2 : 4;
     const int64_t V = d.vocab;
@@ -232,7 +233,14 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         s = dev_alloc(&c->fx_scratch,
                       (size_t)c->flag_cap * fixup_chunks(V) * 2 * fixup_result_bytes());
     if (!s) s = dev_alloc(&c->err, sizeof(int32_t));
+    if (!s) s = dev_alloc(&c->wn_s, (size_t)V * sizeof(float));
+    if (!s && c->has_t) s = dev_alloc(&c->wn_t, (size_t)V * sizeof(float));
     if (s) { release(c); return s; }
+    if (launch_row_norms(c->ws, V, d.d_student, c->bf16, c->wn_s, st) != hipSuccess ||
+        (c->has_t && launch_row_norms(c->wt, V, d.d_teacher, c->bf16, c->wn_t, st) != hipSuccess)) {
+        release(c);
+        return OLIVE_E_HIP;
+    }
     c->timing = (d.flags & OLIVE_FLAG_KERNEL_TIMING) != 0;
     if (c->timing) {
         for (int k = 0; k < 2; ++k)

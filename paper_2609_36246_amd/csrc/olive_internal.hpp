@@ -80,7 +80,10 @@ hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_s
                           int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
                           int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st);
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
-                             void *scratch, int32_t *am_s, int32_t *am_t, hipStream_t st);
+                             void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
+                             int32_t *am_t, hipStream_t st);
+hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *out,
+                            hipStream_t st);
 int fixup_chunks(int64_t V);
 size_t fixup_result_bytes();
 hipError_t launch_ce(const olive_batch &b, const int32_t *seqbuf, const Sched *sched,

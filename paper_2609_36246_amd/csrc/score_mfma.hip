@@ -16,11 +16,10 @@
 // end of a split.
 //
 // Pipeline: K advances 32 elements (64 bytes per row) per step; each step's W tile
-// (256 x 64 B) and H tile (128 x 64 B) land in one of 4 LDS stages through
-// global_load_lds_dwordx4, issued 3 steps ahead. Stage rows are XOR-swizzled at
+// (256 x 64 B) and H tile (128 x 64 B) land in one of 6 LDS stages through
+// global_load_lds_dwordx4, issued 6 steps ahead. Stage rows are XOR-swizzled at
 // 16-byte granularity so the ds_read_b128 operand fetches are bank-conflict free.
-// Hidden widths must be multiples of 128 so every model's step count is a multiple
-// of the ring depth (each stage is a distinct LDS object with static indices).
+// Hidden widths must be multiples of 32 (one step).
 //
 // The grid is persistent (one workgroup per CU). Work units (position tile,
 // split) are ordered so that the 32 workgroups of one XCD share 8 position tiles x
@@ -42,31 +41,35 @@ constexpr int BT = MFMA_BT;              // 128
 constexpr int ROWB = 64;                 // bytes per row per step (32 bf16)
 constexpr int WT_BYTES = BV * ROWB;      // 16 KB
 constexpr int HT_BYTES = BT * ROWB;      // 8 KB
-constexpr float kMasked = -1.0e30f;      // logit of vocabulary rows outside the tile range
+// Logit of vocabulary rows outside the tile range: -2^99. A power of two, so that
+// kMasked * c is exact and a block whose running max is kMasked folds to exp2(0) = 1
+// rather than to the rounding residual of the product; z + kMasked rounds back to
+// exactly kMasked for any |z| < 2^74, in both models (their difference is 0).
+constexpr float kMasked = -0x1p99f;
 
-__shared__ __attribute__((aligned(1024))) char g_lw0[WT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lw1[WT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lw2[WT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lw3[WT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lh0[HT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lh1[HT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lh2[HT_BYTES];
-__shared__ __attribute__((aligned(1024))) char g_lh3[HT_BYTES];
+// Ring of NST LDS stages; stage i holds the W tile [256 rows x 64 B] followed by
+// the H tile [128 rows x 64 B] of one K step.
+constexpr int NST = 6;
+constexpr int STAGE_BYTES = WT_BYTES + HT_BYTES;     // 24 KB; 6 stages = 144 KB
+__shared__ __attribute__((aligned(1024))) char g_ring[NST * STAGE_BYTES];
 
-template <int S> __device__ __forceinline__ char *lw() {
-    return S == 0 ? g_lw0 : S == 1 ? g_lw1 : S == 2 ? g_lw2 : g_lw3;
+__device__ __forceinline__ uint32_t ring_addr() {
+    return (uint32_t)(uintptr_t)(lds_void *)g_ring;
 }
-template <int S> __device__ __forceinline__ char *lh() {
-    return S == 0 ? g_lh0 : S == 1 ? g_lh1 : S == 2 ? g_lh2 : g_lh3;
-}
+
+// s_waitcnt immediate for "vmcnt <= n" (gfx9 encoding: vmcnt bits [3:0] and [15:14];
+// expcnt and lgkmcnt left at their maxima).
+constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (0xF << 8) | (7 << 4); }
 
 // max(a, b) for non-NaN operands as one v_med3_f32 (no NaN canonicalisation).
 __device__ __forceinline__ float max2(float a, float b) {
     return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
 }
 
-// 16-byte slot swizzle of a 64-byte stage row.
-__device__ __forceinline__ int swz(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
+// 16-byte slot swizzle of a 64-byte stage row: slot = chunk ^ ((row >> 2) & 3).
+// Measured on gfx950 to keep the ds_read_b128 operand fetches (32 rows x 2 chunks
+// per instruction) free of bank conflicts at the full 256 B/clk LDS read rate.
+__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
 
 // Read one accumulator element where it lives (an AGPR). Issuing the read at the
 // point of use keeps the register allocator from copying whole accumulator tuples
@@ -79,8 +82,20 @@ __device__ __forceinline__ float agpr_read(float x) {
 
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
-__device__ __forceinline__ void dma16(const char *g, char *l) {
-    __builtin_amdgcn_global_load_lds((const void *)g, (lds_void *)l, 16, 0, 0);
+// One global -> LDS DMA of 16 bytes per lane: lane i's bytes land at the wave-uniform
+// LDS address `l` + 16 i. Issued as inline assembly so that the compiler's wait-count
+// analysis does not see an LDS write in flight (it would then wait for every LDS read
+// with lgkmcnt(0)); completion is ordered by the explicit vmcnt waits and barriers of
+// the pipeline. m0 is written here only: the kernel has no other m0 user.
+__device__ __forceinline__ void dma16(const char *g, uint32_t la) {
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+    // s_nop: one wait state between the m0 write and the DMA that reads it.
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(la), "v"(g)
+                 : "memory", "m0");
+#pragma clang diagnostic pop
 }
 
 struct Lane {
@@ -97,57 +112,81 @@ struct Run {                // running statistics of one position column
 
 template <bool HAS_T, bool SAME>
 struct Kernel {
-    // Issue the 6 DMAs of one step (4 W, 2 H) of model `m` into stage S.
-    template <int S>
-    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int m, int kk,
-                                                 int vt) {
+    // Issue the 6 DMAs of one step (4 W, 2 H) of model `m`, K step kk, vocabulary
+    // tile vt into ring stage `st`.
+    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int st, int m,
+                                                 int kk, int vt) {
         const int d = m ? a.dt : a.ds;
         const int64_t rowbytes = (int64_t)d * 2;
         const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
         const char *wt = (const char *)(m ? a.wt : a.ws) + (int64_t)row0 * rowbytes + kk * ROWB;
-        char *lwp = lw<S>() + L.wid * 4 * 1024;
-        char *lhp = lh<S>() + L.wid * 2 * 1024;
+        const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;   // wave-uniform
+        const uint32_t lwp = base + (uint32_t)L.wid * 4096u;
+        const uint32_t lhp = base + WT_BYTES + (uint32_t)L.wid * 2048u;
 #pragma unroll
         for (int i = 0; i < 4; ++i) dma16(wt + (m ? L.wvoff[1][i] : L.wvoff[0][i]), lwp + i * 1024);
 #pragma unroll
         for (int i = 0; i < 2; ++i) dma16((m ? L.hp[1][i] : L.hp[0][i]) + kk * ROWB, lhp + i * 1024);
     }
 
-    template <int S>
-    static __device__ __forceinline__ void mma(const Lane &L, floatx16 (&acc)[4][2]) {
-        const char *wb = lw<S>() + L.wv * 128 * ROWB;
-        const char *hb = lh<S>() + L.wt * 64 * ROWB;
+    // Operand fragments of one k16 sub-step: 4 W row blocks, 2 H column blocks.
+    struct Frag {
+        bf16x8 A[4], B[2];
+    };
+
+    template <int SUB>
+    static __device__ __forceinline__ void read_frag(const Lane &L, int st, Frag &F) {
+        const char *stage = g_ring + st * STAGE_BYTES;
+        const char *wb = stage + L.wv * 128 * ROWB + L.ldsoff[SUB];
+        const char *hb = stage + WT_BYTES + L.wt * 64 * ROWB + L.ldsoff[SUB];
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-            bf16x8 A[4], B[2];
+        for (int vb = 0; vb < 4; ++vb) F.A[vb] = *(const bf16x8 *)(wb + vb * 32 * ROWB);
 #pragma unroll
-            for (int vb = 0; vb < 4; ++vb)
-                A[vb] = *(const bf16x8 *)(wb + vb * 32 * ROWB + L.ldsoff[s]);
-#pragma unroll
-            for (int cb = 0; cb < 2; ++cb)
-                B[cb] = *(const bf16x8 *)(hb + cb * 32 * ROWB + L.ldsoff[s]);
-#pragma unroll
-            for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-                for (int cb = 0; cb < 2; ++cb)
-                    acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[vb], B[cb],
-                                                                          acc[vb][cb], 0, 0, 0);
-        }
+        for (int cb = 0; cb < 2; ++cb) F.B[cb] = *(const bf16x8 *)(hb + cb * 32 * ROWB);
     }
 
-    // One pipeline step in stage S: wait for its data (the 2 later steps' 12 DMAs
-    // may stay in flight), then prefetch 3 steps ahead and multiply. The prefetch is
-    // issued unconditionally -- past the end of a unit it re-reads in-bounds
-    // addresses -- so the compiler's wait tracking never joins a path without it.
-    template <int S>
-    static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, int pm, int pk,
-                                                int pvt, floatx16 (&acc)[4][2]) {
-        __builtin_amdgcn_s_waitcnt(0x0F7C);   // vmcnt(12)
+    static __device__ __forceinline__ void mma(const Frag &F, floatx16 (&acc)[4][2]) {
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+                acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[vb], F.B[cb],
+                                                                      acc[vb][cb], 0, 0, 0);
+    }
+
+    // Wait until this wave's DMAs of the next step have landed (the NST-2 steps after
+    // it may stay in flight), then barrier: after it every wave's data for that step
+    // is in LDS and every wave has finished reading the stage the next DMA overwrites.
+    static __device__ __forceinline__ void arrive() {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 2) * 6));
         compiler_fence();
         __builtin_amdgcn_s_barrier();
         compiler_fence();
-        issue<(S + 3) & 3>(a, L, pm, pk, pvt);
-        mma<S>(L, acc);
+    }
+
+    // One pipeline step in stage `st`, software-pipelined across steps: F0 holds the
+    // first sub-step's fragments (read at the end of the previous step). The second
+    // sub-step's fragments are read while the first sub-step's MFMAs run, and its
+    // MFMAs are issued before the barrier so the matrix core keeps working while the
+    // wave waits, prefetches step n+NST into stage `st` (its reads are done) and
+    // reads the next step's first fragments. Past the end of a unit the prefetch
+    // repeats the last step's in-bounds addresses, so no DMA sits under a branch.
+    static __device__ __forceinline__ int step(const ScoreArgs &a, const Lane &L, int st, int pm,
+                                               int pk, int pvt, floatx16 (&acc)[4][2],
+                                               Frag &F0) {
+        Frag F1;
+        read_frag<1>(L, st, F1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(F0, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        mma(F1, acc);
+        arrive();
+        issue(a, L, st, pm, pk, pvt);
+        const int nx = st + 1 == NST ? 0 : st + 1;
+        read_frag<0>(L, nx, F0);
+        __builtin_amdgcn_sched_barrier(0);
+        return nx;
     }
 
     // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
@@ -267,7 +306,7 @@ struct Kernel {
         const int n_units = a.sched->n_units;
         Lane L;
         L.lane = threadIdx.x & 63;
-        L.wid = threadIdx.x >> 6;
+        L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
         L.wv = L.wid & 1;
         L.wt = L.wid >> 1;
         L.h = L.lane >> 5;
@@ -332,45 +371,58 @@ struct Kernel {
                     accT[vb][cb] = floatx16{0.f};
                 }
 
-            // Issue cursor: (vtile, position within the vtile's steps).
+            // Issue cursor: (vtile, position within the vtile's steps) of the next step
+            // to prefetch, saturating at the unit's last step.
             int ivt = vt0, ir = 0;
-            auto adv = [&]() { if (++ir == spv) { ir = 0; ++ivt; } };
+            // Branch-free advance: control flow between steps would make the compiler
+            // merge its LDS wait state conservatively (lgkmcnt(0)) at every join.
+            auto adv_if = [&](bool go) {
+                ir += go ? 1 : 0;
+                const bool wrap = ir == spv;
+                ir = wrap ? 0 : ir;
+                ivt += wrap ? 1 : 0;
+            };
             auto im = [&]() { return ir < nS ? 0 : 1; };
             auto ik = [&]() { return ir < nS ? ir : ir - nS; };
-            // Prologue: steps 0, 1, 2 (total >= 4 always).
-            issue<0>(a, L, im(), ik(), ivt); adv();
-            issue<1>(a, L, im(), ik(), ivt); adv();
-            issue<2>(a, L, im(), ik(), ivt); adv();
-
-            int n = 0;   // global step index within the unit
-#define OLIVE_STEP(S_, ACC_)                                                             \
-            {                                                                            \
-                step<S_>(a, L, im(), ik(), ivt, ACC_);                                   \
-                if (n + S_ + 3 < total) adv();                                           \
+            // Prologue: steps 0..NST-2 into stages 0..NST-2, step 0's arrival, step
+            // NST-1 into the last stage and step 0's first fragments.
+#pragma unroll
+            for (int i = 0; i < NST - 1; ++i) {
+                issue(a, L, i, im(), ik(), ivt);
+                adv_if(i + 1 < total);
             }
+            arrive();
+            issue(a, L, NST - 1, im(), ik(), ivt);
+            adv_if(NST < total);
+            Frag F0;
+            read_frag<0>(L, 0, F0);
+            // Drain scalar loads before the loops: an SMEM load still pending at a loop
+            // header would force lgkmcnt(0) (full LDS waits) inside every step.
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+
+            int n = 0;    // global step index within the unit
+            int st = 0;   // ring stage of step n
             for (int vt = vt0; vt < vt1; ++vt) {
                 // The last tile, when V is not a multiple of 256, is shifted back to end
                 // at V; its rows below vt*BV were covered by the previous tile. One more
-                // MFMA adds -1e30 to those rows (|z| << 1e30 is absorbed), so they drop
+                // MFMA adds kMasked to those rows (the logit is absorbed), so they drop
                 // out of every statistic and the fold needs no masking.
                 const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
                 const int vbase = row0 + L.wv * 128 + 4 * L.h;
                 zero_acc(accS, accT);
-                // Each model's step count is a multiple of the ring depth (4), so the
-                // stage of a step is static inside these loops.
-                for (int k = 0; k < nS; k += 4, n += 4) {
-                    OLIVE_STEP(0, accS) OLIVE_STEP(1, accS) OLIVE_STEP(2, accS) OLIVE_STEP(3, accS)
+                for (int k = 0; k < nS; ++k, ++n) {
+                    st = step(a, L, st, im(), ik(), ivt, accS, F0);
+                    adv_if(n + NST + 1 < total);
                 }
                 if (HAS_T) {
-                    for (int k = 0; k < nT; k += 4, n += 4) {
-                        OLIVE_STEP(0, accT) OLIVE_STEP(1, accT) OLIVE_STEP(2, accT)
-                        OLIVE_STEP(3, accT)
+                    for (int k = 0; k < nT; ++k, ++n) {
+                        st = step(a, L, st, im(), ik(), ivt, accT, F0);
+                        adv_if(n + NST + 1 < total);
                     }
                 }
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
                 fold(accS, accT, RS, RT, AA, a, vbase);
             }
-#undef OLIVE_STEP
 
             // Merge lanes l and l+32 (same columns, interleaved vocabulary rows).
 #pragma unroll
@@ -388,7 +440,7 @@ struct Kernel {
             }
             // Merge the two vocabulary halves (wv = 1 into wv = 0) through LDS, once
             // the trailing prefetches into the stages have landed.
-            float *xs = (float *)g_lw0;   // [wt][cb][l32][9]
+            float *xs = (float *)g_ring;   // [wt][cb][l32][9]
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
             compiler_fence();
             __builtin_amdgcn_s_barrier();
@@ -441,7 +493,8 @@ struct Kernel {
 };
 
 template <bool HAS_T, bool SAME>
-__global__ void __launch_bounds__(256, 1) score_mfma_kernel(ScoreArgs a) {
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+score_mfma_kernel(ScoreArgs a) {
     Kernel<HAS_T, SAME>::run(a);
 }
 

@@ -73,7 +73,7 @@ def _init(desc, ws=1, wt=1):
     ("d_teacher", -1, L.OLIVE_E_SHAPE),
     ("max_positions", 0, L.OLIVE_E_SHAPE),
     ("max_seqs", 0, L.OLIVE_E_SHAPE),
-    ("d_student", 20000, L.OLIVE_E_UNSUPPORTED),
+    ("d_student", 12289, L.OLIVE_E_UNSUPPORTED),
     ("logit_scale_student", 0.0, L.OLIVE_E_RANGE),
     ("logit_scale_student", float("inf"), L.OLIVE_E_RANGE),
     ("logit_scale_teacher", -1.0, L.OLIVE_E_RANGE),

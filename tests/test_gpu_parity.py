@@ -37,6 +37,12 @@ CASES = {
     "multi_tile": dict(num_seqs=5, ragged_len=(700, 1300), vocab=5000, d_student=256,
                        d_teacher=128, logit_scale=4.0, target_source="student",
                        cut_rule=("frac", 0.1, 0.9)),
+    # hidden widths that are multiples of 32 only (one K step), short unit pipelines
+    "narrow_k": dict(num_seqs=2, ragged_len=(100, 250), vocab=700, d_student=32,
+                     d_teacher=96, cut_rule=("frac", 0.2, 0.8)),
+    # last vocabulary tile with a single valid row: whole lanes see only masked rows
+    "v257": dict(num_seqs=2, seq_len=150, vocab=257, d_student=64, d_teacher=64,
+                 logit_scale=2.0, cut_rule=("abs", 1, 149)),
     # vocabulary a multiple of 256, teacher-sampled targets, outlier rows
     "even_v": dict(num_seqs=2, seq_len=200, vocab=2048, d_student=384, d_teacher=512,
                    target_source="teacher", cut_rule=("abs", 1, 199), outlier_frac=0.05,
