@@ -17,7 +17,7 @@
 //
 // Pipeline: K advances 32 elements (64 bytes per row) per step; each step's W tile
 // (256 x 64 B) and H tile (128 x 64 B) land in one of 6 LDS stages through
-// global_load_lds_dwordx4, issued 6 steps ahead. Stage rows are XOR-swizzled at
+// global_load_lds_dwordx4, issued 5 steps ahead. Stage rows are XOR-swizzled at
 // 16-byte granularity so the ds_read_b128 operand fetches are bank-conflict free.
 // Hidden widths must be multiples of 32 (one step).
 //
@@ -154,37 +154,38 @@ struct Kernel {
                                                                       acc[vb][cb], 0, 0, 0);
     }
 
-    // Wait until this wave's DMAs of the next step have landed (the NST-2 steps after
-    // it may stay in flight), then barrier: after it every wave's data for that step
-    // is in LDS and every wave has finished reading the stage the next DMA overwrites.
+    // Wait until this wave's DMAs for step n+2 have landed (the NST-4 steps issued
+    // after it may stay in flight), then barrier: after it every wave's data for step
+    // n+2 is in LDS and every wave has issued its MFMAs of step n-1, so the stage of
+    // step n-1 may be overwritten.
     static __device__ __forceinline__ void arrive() {
         __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 2) * 6));
+        __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 4) * 6));
         compiler_fence();
         __builtin_amdgcn_s_barrier();
         compiler_fence();
     }
 
-    // One pipeline step in stage `st`, software-pipelined across steps: F0 holds the
-    // first sub-step's fragments (read at the end of the previous step). The second
-    // sub-step's fragments are read while the first sub-step's MFMAs run, and its
-    // MFMAs are issued before the barrier so the matrix core keeps working while the
-    // wave waits, prefetches step n+NST into stage `st` (its reads are done) and
-    // reads the next step's first fragments. Past the end of a unit the prefetch
-    // repeats the last step's in-bounds addresses, so no DMA sits under a branch.
+    // One pipeline step n in stage `st`. Fc holds step n's first sub-step fragments
+    // (read one step earlier). The step reads its second sub-step fragments and step
+    // n+1's first ones, issues the first sub-step's MFMAs, meets the barrier while
+    // those run, prefetches step n+NST-1 into the stage of step n-1 and issues the
+    // second sub-step's MFMAs. Past the end of a unit the prefetch repeats the last
+    // step's in-bounds addresses, so no DMA sits under a branch.
     static __device__ __forceinline__ int step(const ScoreArgs &a, const Lane &L, int st, int pm,
                                                int pk, int pvt, floatx16 (&acc)[4][2],
-                                               Frag &F0) {
+                                               const Frag &Fc, Frag &Fn) {
+        const int nx = st + 1 == NST ? 0 : st + 1;
+        const int pv = st == 0 ? NST - 1 : st - 1;
         Frag F1;
         read_frag<1>(L, st, F1);
+        read_frag<0>(L, nx, Fn);
         __builtin_amdgcn_sched_barrier(0);
-        mma(F0, acc);
+        mma(Fc, acc);
+        arrive();
+        issue(a, L, pv, pm, pk, pvt);
         __builtin_amdgcn_sched_barrier(0);
         mma(F1, acc);
-        arrive();
-        issue(a, L, st, pm, pk, pvt);
-        const int nx = st + 1 == NST ? 0 : st + 1;
-        read_frag<0>(L, nx, F0);
         __builtin_amdgcn_sched_barrier(0);
         return nx;
     }
@@ -384,24 +385,45 @@ struct Kernel {
             };
             auto im = [&]() { return ir < nS ? 0 : 1; };
             auto ik = [&]() { return ir < nS ? ir : ir - nS; };
-            // Prologue: steps 0..NST-2 into stages 0..NST-2, step 0's arrival, step
-            // NST-1 into the last stage and step 0's first fragments.
+            // Prologue: steps 0..NST-2 into stages 0..NST-2; wait for steps 0 and 1
+            // (the NST-3 later steps may stay in flight) and read step 0's fragments.
 #pragma unroll
             for (int i = 0; i < NST - 1; ++i) {
                 issue(a, L, i, im(), ik(), ivt);
                 adv_if(i + 1 < total);
             }
-            arrive();
-            issue(a, L, NST - 1, im(), ik(), ivt);
-            adv_if(NST < total);
-            Frag F0;
-            read_frag<0>(L, 0, F0);
+            __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 3) * 6));
+            compiler_fence();
+            __builtin_amdgcn_s_barrier();
+            compiler_fence();
+            Frag FA, FB;
+            read_frag<0>(L, 0, FA);
             // Drain scalar loads before the loops: an SMEM load still pending at a loop
             // header would force lgkmcnt(0) (full LDS waits) inside every step.
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
 
             int n = 0;    // global step index within the unit
             int st = 0;   // ring stage of step n
+            // Steps alternate the fragment registers FA -> FB -> FA; a model loop with an
+            // odd step count ends with one copy back into FA.
+#define OLIVE_STEPS(ACC_, COUNT_)                                                        \
+            {                                                                            \
+                int k = 0;                                                               \
+                for (; k + 1 < (COUNT_); k += 2) {                                       \
+                    st = step(a, L, st, im(), ik(), ivt, ACC_, FA, FB);                  \
+                    adv_if(n + NST < total);                                             \
+                    ++n;                                                                 \
+                    st = step(a, L, st, im(), ik(), ivt, ACC_, FB, FA);                  \
+                    adv_if(n + NST < total);                                             \
+                    ++n;                                                                 \
+                }                                                                        \
+                if (k < (COUNT_)) {                                                      \
+                    st = step(a, L, st, im(), ik(), ivt, ACC_, FA, FB);                  \
+                    adv_if(n + NST < total);                                             \
+                    ++n;                                                                 \
+                    FA = FB;                                                             \
+                }                                                                        \
+            }
             for (int vt = vt0; vt < vt1; ++vt) {
                 // The last tile, when V is not a multiple of 256, is shifted back to end
                 // at V; its rows below vt*BV were covered by the previous tile. One more
@@ -410,19 +432,12 @@ struct Kernel {
                 const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
                 const int vbase = row0 + L.wv * 128 + 4 * L.h;
                 zero_acc(accS, accT);
-                for (int k = 0; k < nS; ++k, ++n) {
-                    st = step(a, L, st, im(), ik(), ivt, accS, F0);
-                    adv_if(n + NST + 1 < total);
-                }
-                if (HAS_T) {
-                    for (int k = 0; k < nT; ++k, ++n) {
-                        st = step(a, L, st, im(), ik(), ivt, accT, F0);
-                        adv_if(n + NST + 1 < total);
-                    }
-                }
+                OLIVE_STEPS(accS, nS)
+                if (HAS_T) OLIVE_STEPS(accT, nT)
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
                 fold(accS, accT, RS, RT, AA, a, vbase);
             }
+#undef OLIVE_STEPS
 
             // Merge lanes l and l+32 (same columns, interleaved vocabulary rows).
 #pragma unroll
