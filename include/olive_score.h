@@ -82,7 +82,10 @@ typedef struct {
     int32_t flags;              /* bit set of OLIVE_FLAG_* (0 = defaults) */
 } olive_score_desc;
 
-/* Force the generic fp32-FMA kernel even where the bf16 MFMA kernel applies. */
+/* Force the generic fp32-FMA kernel even where the bf16 MFMA kernel applies. The
+ * MFMA kernel applies to bf16 contexts whose hidden widths are multiples of 64, with
+ * V >= 256 and 16-byte aligned weight and hidden-state buffers; every other case runs
+ * the generic kernel, which returns the same outputs more slowly. */
 #define OLIVE_FLAG_SIMPLE_KERNEL 1
 /* Record HIP events around the vocabulary-scoring kernel of every call (for
  * olive_score_kernel_times); costs two event records per call. */

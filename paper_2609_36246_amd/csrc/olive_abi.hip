@@ -78,7 +78,10 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t 
     const int64_t T = b->total_positions;
     const int64_t V = d.vocab;
     const int n_vtiles = (int)((V + 255) / 256);
-    const bool mfma = ctx->mfma_ok;
+    // The MFMA kernel streams hidden rows with 16-byte DMAs: it needs 16-byte aligned
+    // hidden-state buffers; others take the generic kernel.
+    const bool mfma = ctx->mfma_ok && ((uintptr_t)b->h_student & 15) == 0 &&
+                      (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
 
     olive_status s;
@@ -200,8 +203,11 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         release(c);
         return OLIVE_E_HIP;
     }
-    c->mfma_ok = c->bf16 && (d.d_student % 32 == 0) && (d.d_teacher % 32 == 0) &&
-                 d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL);
+    c->mfma_ok = c->bf16 && (d.d_student % 64 == 0) && (d.d_teacher % 64 == 0) &&
+                 d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL) &&
+                 (d.w_layout == OLIVE_W_DV ||      // borrowed weights: 16-byte rows
+                  (((uintptr_t)w_student & 15) == 0 &&
+                   (!c->has_t || ((uintptr_t)w_teacher & 15) == 0)));
     const int esz = c->bf16 ? 2 : 4;
     const int64_t V = d.vocab;
     olive_status s = OLIVE_OK;

@@ -15,11 +15,13 @@
 // only lanes l / l+32 and the two vocabulary-half wavefronts need merging at the
 // end of a split.
 //
-// Pipeline: K advances 32 elements (64 bytes per row) per step; each step's W tile
-// (256 x 64 B) and H tile (128 x 64 B) land in one of 6 LDS stages through
-// global_load_lds_dwordx4, issued 5 steps ahead. Stage rows are XOR-swizzled at
-// 16-byte granularity so the ds_read_b128 operand fetches are bank-conflict free.
-// Hidden widths must be multiples of 32 (one step).
+// Pipeline: K advances 64 elements (one 128-byte line per row) per step; each step's
+// W tile (256 x 128 B) and H tile (128 x 128 B) land in one of 3 LDS stages through
+// global_load_lds_dwordx4, issued two steps ahead. Whole-line requests matter: the
+// path from L2 to a CU is bound by the number of requests, and 64-byte row pieces
+// would halve the bytes per request. Stage rows are XOR-swizzled at 16-byte
+// granularity so the ds_read_b128 operand fetches are bank-conflict free. Hidden
+// widths must be multiples of 64 (one step).
 //
 // The grid is persistent (one workgroup per CU). Work units (position tile,
 // split) are ordered so that the 32 workgroups of one XCD share 8 position tiles x
@@ -38,38 +40,43 @@ typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int BV = MFMA_BV;              // 256
 constexpr int BT = MFMA_BT;              // 128
-constexpr int ROWB = 64;                 // bytes per row per step (32 bf16)
-constexpr int WT_BYTES = BV * ROWB;      // 16 KB
-constexpr int HT_BYTES = BT * ROWB;      // 8 KB
+constexpr int BK = 64;                   // K elements per pipeline step
+constexpr int ROWB = BK * 2;             // bytes per row per step: one 128-byte line
+constexpr int WT_BYTES = BV * ROWB;      // 32 KB
+constexpr int HT_BYTES = BT * ROWB;      // 16 KB
 // Logit of vocabulary rows outside the tile range: -2^99. A power of two, so that
 // kMasked * c is exact and a block whose running max is kMasked folds to exp2(0) = 1
 // rather than to the rounding residual of the product; z + kMasked rounds back to
 // exactly kMasked for any |z| < 2^74, in both models (their difference is 0).
 constexpr float kMasked = -0x1p99f;
 
-// Ring of NST LDS stages; stage i holds the W tile [256 rows x 64 B] followed by
-// the H tile [128 rows x 64 B] of one K step.
-constexpr int NST = 6;
-constexpr int STAGE_BYTES = WT_BYTES + HT_BYTES;     // 24 KB; 6 stages = 144 KB
+// Ring of NST LDS stages; stage i holds the W tile [256 rows x 128 B] followed by
+// the H tile [128 rows x 128 B] of one K step.
+constexpr int NST = 3;
+constexpr int STAGE_BYTES = WT_BYTES + HT_BYTES;     // 48 KB; 3 stages = 144 KB
+constexpr int W_DMA = WT_BYTES / 1024 / 4;           // 16-byte-per-lane DMAs per wave: 8
+constexpr int H_DMA = HT_BYTES / 1024 / 4;           // 4
+constexpr int DMA_PER_STEP = W_DMA + H_DMA;          // 12
 __shared__ __attribute__((aligned(1024))) char g_ring[NST * STAGE_BYTES];
 
 __device__ __forceinline__ uint32_t ring_addr() {
     return (uint32_t)(uintptr_t)(lds_void *)g_ring;
 }
 
-// s_waitcnt immediate for "vmcnt <= n" (gfx9 encoding: vmcnt bits [3:0] and [15:14];
-// expcnt and lgkmcnt left at their maxima).
+// s_waitcnt immediates (gfx9 encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4],
+// lgkmcnt [11:8]): "vmcnt <= n" alone, and together with "lgkmcnt = 0".
 constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (0xF << 8) | (7 << 4); }
+constexpr int vmcnt_lgkm0_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
 // max(a, b) for non-NaN operands as one v_med3_f32 (no NaN canonicalisation).
 __device__ __forceinline__ float max2(float a, float b) {
     return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
 }
 
-// 16-byte slot swizzle of a 64-byte stage row: slot = chunk ^ ((row >> 2) & 3).
+// 16-byte slot swizzle of a 128-byte stage row: slot = chunk ^ ((row >> 1) & 7).
 // Measured on gfx950 to keep the ds_read_b128 operand fetches (32 rows x 2 chunks
-// per instruction) free of bank conflicts at the full 256 B/clk LDS read rate.
-__device__ __forceinline__ int swz(int r) { return (r >> 2) & 3; }
+// per instruction, any of the 4 sub-steps) free of bank conflicts.
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
 
 // Read one accumulator element where it lives (an AGPR). Issuing the read at the
 // point of use keeps the register allocator from copying whole accumulator tuples
@@ -100,9 +107,9 @@ __device__ __forceinline__ void dma16(const char *g, uint32_t la) {
 
 struct Lane {
     int lane, wid, wv, wt, h, l32;
-    int ldsoff[2];          // operand fetch offsets for the two k16 sub-steps
-    uint32_t wvoff[2][4];   // per model, per W DMA: row * rowbytes + chunk * 16
-    const char *hp[2][2];   // per model, per H DMA: pointer to the row chunk
+    int ldsoff[4];          // operand fetch offsets for the four k16 sub-steps
+    uint32_t wvoff[2][2];   // per model, per W DMA parity: lane part of row * rowbytes + chunk * 16
+    const char *hp[2][H_DMA];   // per model, per H DMA: pointer to the row chunk
 };
 
 struct Run {                // running statistics of one position column
@@ -112,21 +119,48 @@ struct Run {                // running statistics of one position column
 
 template <bool HAS_T, bool SAME>
 struct Kernel {
-    // Issue the 6 DMAs of one step (4 W, 2 H) of model `m`, K step kk, vocabulary
-    // tile vt into ring stage `st`.
-    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int st, int m,
+    // Addresses of the 12 DMAs of one step (8 W, 4 H) of model `m`, K step kk,
+    // vocabulary tile vt, into ring stage `st`. DMA i of a wave fills stage rows
+    // 8i .. 8i+7 of the wave's slice: every 8 lanes read one full 128-byte line of a row.
+    struct Issue {
+        const char *wt;         // W tile row 0 at K step kk (wave-uniform)
+        int64_t wstep;          // 8 rows of W (wave-uniform)
+        uint32_t wo0, wo1;      // lane offsets for even / odd W DMAs
+        int hoff;               // K step offset into the H rows
+        int m;
+        uint32_t lwp, lhp;      // LDS targets (wave-uniform)
+    };
+    static __device__ __forceinline__ Issue plan(const ScoreArgs &a, const Lane &L, int st, int m,
                                                  int kk, int vt) {
+        Issue I;
         const int d = m ? a.dt : a.ds;
         const int64_t rowbytes = (int64_t)d * 2;
         const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
-        const char *wt = (const char *)(m ? a.wt : a.ws) + (int64_t)row0 * rowbytes + kk * ROWB;
+        I.wt = (const char *)(m ? a.wt : a.ws) + (int64_t)row0 * rowbytes + kk * ROWB;
+        I.wstep = 8 * rowbytes;
+        I.wo0 = m ? L.wvoff[1][0] : L.wvoff[0][0];
+        I.wo1 = m ? L.wvoff[1][1] : L.wvoff[0][1];
+        I.hoff = kk * ROWB;
+        I.m = m;
         const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;   // wave-uniform
-        const uint32_t lwp = base + (uint32_t)L.wid * 4096u;
-        const uint32_t lhp = base + WT_BYTES + (uint32_t)L.wid * 2048u;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) dma16(wt + (m ? L.wvoff[1][i] : L.wvoff[0][i]), lwp + i * 1024);
-#pragma unroll
-        for (int i = 0; i < 2; ++i) dma16((m ? L.hp[1][i] : L.hp[0][i]) + kk * ROWB, lhp + i * 1024);
+        I.lwp = base + (uint32_t)L.wid * (W_DMA * 1024u);
+        I.lhp = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
+        return I;
+    }
+    template <int Q>
+    static __device__ __forceinline__ void dma_q(const Lane &L, const Issue &I) {
+        if (Q < W_DMA)
+            dma16(I.wt + Q * I.wstep + ((Q & 1) ? I.wo1 : I.wo0), I.lwp + Q * 1024);
+        else
+            dma16((I.m ? L.hp[1][Q - W_DMA] : L.hp[0][Q - W_DMA]) + I.hoff,
+                  I.lhp + (Q - W_DMA) * 1024);
+    }
+    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int st, int m,
+                                                 int kk, int vt) {
+        const Issue I = plan(a, L, st, m, kk, vt);
+        dma_q<0>(L, I); dma_q<1>(L, I); dma_q<2>(L, I); dma_q<3>(L, I);
+        dma_q<4>(L, I); dma_q<5>(L, I); dma_q<6>(L, I); dma_q<7>(L, I);
+        dma_q<8>(L, I); dma_q<9>(L, I); dma_q<10>(L, I); dma_q<11>(L, I);
     }
 
     // Operand fragments of one k16 sub-step: 4 W row blocks, 2 H column blocks.
@@ -154,40 +188,74 @@ struct Kernel {
                                                                       acc[vb][cb], 0, 0, 0);
     }
 
-    // Wait until this wave's DMAs for step n+2 have landed (the NST-4 steps issued
-    // after it may stay in flight), then barrier: after it every wave's data for step
-    // n+2 is in LDS and every wave has issued its MFMAs of step n-1, so the stage of
-    // step n-1 may be overwritten.
+    // The MFMAs of one sub-step with the 12 DMAs of a step issued between them (two
+    // after each of the first four, one after each of the others), so the matrix pipe
+    // stays busy while the addresses are formed and the requests go out.
+    static __device__ __forceinline__ void mma_issue(const Frag &F, floatx16 (&acc)[4][2],
+                                                     const Lane &L, const Issue &I) {
+#define OLIVE_MI(VB_, CB_, ...)                                                            \
+        __builtin_amdgcn_sched_barrier(0);                                               \
+        acc[VB_][CB_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[VB_], F.B[CB_],        \
+                                                                acc[VB_][CB_], 0, 0, 0); \
+        __builtin_amdgcn_sched_barrier(0);                                               \
+        __VA_ARGS__
+        OLIVE_MI(0, 0, dma_q<0>(L, I); dma_q<1>(L, I);)
+        OLIVE_MI(0, 1, dma_q<2>(L, I); dma_q<3>(L, I);)
+        OLIVE_MI(1, 0, dma_q<4>(L, I); dma_q<5>(L, I);)
+        OLIVE_MI(1, 1, dma_q<6>(L, I); dma_q<7>(L, I);)
+        OLIVE_MI(2, 0, dma_q<8>(L, I);)
+        OLIVE_MI(2, 1, dma_q<9>(L, I);)
+        OLIVE_MI(3, 0, dma_q<10>(L, I);)
+        OLIVE_MI(3, 1, dma_q<11>(L, I);)
+#undef OLIVE_MI
+        __builtin_amdgcn_sched_barrier(0);
+    }
+
+    // Stage barrier at the start of step n: wait until this wave's DMAs of step n have
+    // landed (those of step n+1 may stay in flight) and its LDS reads of step n-1 have
+    // returned, then barrier. After it every wave's data of step n is in LDS and no
+    // wave reads the stage of step n-1 any more, so step n+2 may be issued into it.
     static __device__ __forceinline__ void arrive() {
         __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 4) * 6));
+        __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_imm(DMA_PER_STEP));
         compiler_fence();
         __builtin_amdgcn_s_barrier();
         compiler_fence();
     }
 
-    // One pipeline step n in stage `st`. Fc holds step n's first sub-step fragments
-    // (read one step earlier). The step reads its second sub-step fragments and step
-    // n+1's first ones, issues the first sub-step's MFMAs, meets the barrier while
-    // those run, prefetches step n+NST-1 into the stage of step n-1 and issues the
-    // second sub-step's MFMAs. Past the end of a unit the prefetch repeats the last
-    // step's in-bounds addresses, so no DMA sits under a branch.
-    static __device__ __forceinline__ int step(const ScoreArgs &a, const Lane &L, int st, int pm,
-                                               int pk, int pvt, floatx16 (&acc)[4][2],
-                                               const Frag &Fc, Frag &Fn) {
-        const int nx = st + 1 == NST ? 0 : st + 1;
+    // One pipeline step n in stage `st`: meet the stage barrier, prefetch step n+2 into
+    // the stage of step n-1, then run the step's four k16 sub-steps, each one's LDS
+    // reads issued under the previous one's MFMAs. With PEND, the last sub-step of
+    // step n-1 (fragments in P) runs under the first reads. On return P holds this
+    // step's last sub-step, still to be run. Past the end of a unit the prefetch
+    // repeats the last step's in-bounds addresses, so no DMA sits under a branch.
+    template <bool PEND>
+    static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, int st, int pm,
+                                                int pk, int pvt, floatx16 (&acc)[4][2],
+                                                Frag &P) {
         const int pv = st == 0 ? NST - 1 : st - 1;
-        Frag F1;
-        read_frag<1>(L, st, F1);
-        read_frag<0>(L, nx, Fn);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(Fc, acc);
         arrive();
-        issue(a, L, pv, pm, pk, pvt);
+        const Issue I = plan(a, L, pv, pm, pk, pvt);
+        Frag F0, F1, F2;
+        read_frag<0>(L, st, F0);
+        __builtin_amdgcn_sched_barrier(0);
+        if (PEND) {
+            mma_issue(P, acc, L, I);
+            read_frag<1>(L, st, F1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma(F0, acc);
+        } else {
+            read_frag<1>(L, st, F1);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_issue(F0, acc, L, I);
+        }
+        read_frag<2>(L, st, F2);
         __builtin_amdgcn_sched_barrier(0);
         mma(F1, acc);
+        read_frag<3>(L, st, P);
         __builtin_amdgcn_sched_barrier(0);
-        return nx;
+        mma(F2, acc);
+        __builtin_amdgcn_sched_barrier(0);
     }
 
     // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
@@ -313,16 +381,17 @@ struct Kernel {
         L.h = L.lane >> 5;
         L.l32 = L.lane & 31;
 #pragma unroll
-        for (int s = 0; s < 2; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
-        const int nS = a.ds / 32, nT = HAS_T ? a.dt / 32 : 0;
+        for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+        const int nS = a.ds / BK, nT = HAS_T ? a.dt / BK : 0;
         const int spv = nS + nT;
-        // W DMA rows: R = (wid*4 + i)*16 + lane/4, chunk = (lane&3) ^ swz(R).
+        // W DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7 with
+        // chunk (lane&7) ^ swz(R); swz(R) depends on i only through its parity.
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int R = (L.wid * 4 + i) * 16 + (L.lane >> 2);
-            const int ch = (L.lane & 3) ^ swz(R);
-            L.wvoff[0][i] = (uint32_t)(R * a.ds * 2 + ch * 16);
-            L.wvoff[1][i] = HAS_T ? (uint32_t)(R * a.dt * 2 + ch * 16) : 0u;
+        for (int par = 0; par < 2; ++par) {
+            const int R0 = L.wid * 8 * W_DMA + (L.lane >> 3);
+            const int ch = (L.lane & 7) ^ swz(R0 + 8 * par);
+            L.wvoff[0][par] = (uint32_t)(R0 * a.ds * 2 + ch * 16);
+            L.wvoff[1][par] = HAS_T ? (uint32_t)(R0 * a.dt * 2 + ch * 16) : 0u;
         }
         const int G = gridDim.x;
         const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
@@ -341,11 +410,11 @@ struct Kernel {
                 p = (int)(w / rem);
                 s = nsb * 4 + (int)(w % rem);
             }
-            // H DMA rows of this position tile.
+            // H DMA i of wave wid fills stage rows R = wid*32 + 8i + lane/8.
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int R = (L.wid * 2 + i) * 16 + (L.lane >> 2);
-                const int ch = (L.lane & 3) ^ swz(R);
+            for (int i = 0; i < H_DMA; ++i) {
+                const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
+                const int ch = (L.lane & 7) ^ swz(R);
                 int j = p * BT + R;
                 j = j < t_valid ? j : t_valid - 1;
                 const int64_t g = a.rowmap[j] & 0x7fffffffu;
@@ -385,44 +454,36 @@ struct Kernel {
             };
             auto im = [&]() { return ir < nS ? 0 : 1; };
             auto ik = [&]() { return ir < nS ? ir : ir - nS; };
-            // Prologue: steps 0..NST-2 into stages 0..NST-2; wait for steps 0 and 1
-            // (the NST-3 later steps may stay in flight) and read step 0's fragments.
+            // Prologue: steps 0 .. NST-2 into stages 0 .. NST-2; the first step's barrier
+            // waits for step 0.
 #pragma unroll
             for (int i = 0; i < NST - 1; ++i) {
                 issue(a, L, i, im(), ik(), ivt);
                 adv_if(i + 1 < total);
             }
-            __builtin_amdgcn_s_waitcnt(vmcnt_imm((NST - 3) * 6));
-            compiler_fence();
-            __builtin_amdgcn_s_barrier();
-            compiler_fence();
-            Frag FA, FB;
-            read_frag<0>(L, 0, FA);
             // Drain scalar loads before the loops: an SMEM load still pending at a loop
             // header would force lgkmcnt(0) (full LDS waits) inside every step.
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
 
             int n = 0;    // global step index within the unit
             int st = 0;   // ring stage of step n
-            // Steps alternate the fragment registers FA -> FB -> FA; a model loop with an
-            // odd step count ends with one copy back into FA.
+            // A model block of COUNT_ steps: the first step has no pending sub-step, the
+            // block's last sub-step runs after the loop.
 #define OLIVE_STEPS(ACC_, COUNT_)                                                        \
             {                                                                            \
-                int k = 0;                                                               \
-                for (; k + 1 < (COUNT_); k += 2) {                                       \
-                    st = step(a, L, st, im(), ik(), ivt, ACC_, FA, FB);                  \
+                Frag P;                                                                  \
+                step<false>(a, L, st, im(), ik(), ivt, ACC_, P);                         \
+                adv_if(n + NST < total);                                                 \
+                ++n;                                                                     \
+                st = st + 1 == NST ? 0 : st + 1;                                         \
+                for (int k = 1; k < (COUNT_); ++k) {                                     \
+                    step<true>(a, L, st, im(), ik(), ivt, ACC_, P);                      \
                     adv_if(n + NST < total);                                             \
                     ++n;                                                                 \
-                    st = step(a, L, st, im(), ik(), ivt, ACC_, FB, FA);                  \
-                    adv_if(n + NST < total);                                             \
-                    ++n;                                                                 \
+                    st = st + 1 == NST ? 0 : st + 1;                                     \
                 }                                                                        \
-                if (k < (COUNT_)) {                                                      \
-                    st = step(a, L, st, im(), ik(), ivt, ACC_, FA, FB);                  \
-                    adv_if(n + NST < total);                                             \
-                    ++n;                                                                 \
-                    FA = FB;                                                             \
-                }                                                                        \
+                mma(P, ACC_);                                                            \
+                __builtin_amdgcn_sched_barrier(0);                                       \
             }
             for (int vt = vt0; vt < vt1; ++vt) {
                 // The last tile, when V is not a multiple of 256, is shifted back to end

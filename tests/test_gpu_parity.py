@@ -37,9 +37,9 @@ CASES = {
     "multi_tile": dict(num_seqs=5, ragged_len=(700, 1300), vocab=5000, d_student=256,
                        d_teacher=128, logit_scale=4.0, target_source="student",
                        cut_rule=("frac", 0.1, 0.9)),
-    # hidden widths that are multiples of 32 only (one K step), short unit pipelines
-    "narrow_k": dict(num_seqs=2, ragged_len=(100, 250), vocab=700, d_student=32,
-                     d_teacher=96, cut_rule=("frac", 0.2, 0.8)),
+    # one K step for the student, an odd count (3) for the teacher: short unit pipelines
+    "narrow_k": dict(num_seqs=2, ragged_len=(100, 250), vocab=700, d_student=64,
+                     d_teacher=192, cut_rule=("frac", 0.2, 0.8)),
     # last vocabulary tile with a single valid row: whole lanes see only masked rows
     "v257": dict(num_seqs=2, seq_len=150, vocab=257, d_student=64, d_teacher=64,
                  logit_scale=2.0, cut_rule=("abs", 1, 149)),
@@ -67,6 +67,30 @@ def test_regions(region):
     wl = custom("ragged_v1000", **CASES["ragged_v1000"])
     hip = run_hip(wl, region=region)
     compare(hip, wl, region=region, label="region%d" % region)
+
+
+def test_widths_off_the_mfma_step_take_the_generic_kernel():
+    say("hidden widths not multiples of 64")
+    wl = custom("w96", num_seqs=2, ragged_len=(60, 140), vocab=900, d_student=96,
+                d_teacher=160, cut_rule=("frac", 0.2, 0.8))
+    hip = run_hip(wl)
+    assert hip["stats"]["kernel"] == "generic"
+    compare(hip, wl, label="w96")
+
+
+def test_misaligned_hidden_states_take_the_generic_kernel():
+    say("hidden states not 16-byte aligned")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    for key in ("h_student", "h_teacher"):
+        h = wl[key]
+        buf = torch.empty(h.numel() + 1, dtype=h.dtype, device=h.device)
+        view = buf[1:].view(h.shape)          # 2-byte offset from the allocation
+        view.copy_(h)
+        assert view.data_ptr() % 16 != 0
+        wl[key] = view
+    hip = run_hip(wl)
+    assert hip["stats"]["kernel"] == "generic"
+    compare(hip, wl, label="misaligned")
 
 
 def test_different_scales_general_difference_path():
