@@ -188,25 +188,35 @@ struct Kernel {
                                                                       acc[vb][cb], 0, 0, 0);
     }
 
-    // The MFMAs of one sub-step with the 12 DMAs of a step issued between them (two
-    // after each of the first four, one after each of the others), so the matrix pipe
-    // stays busy while the addresses are formed and the requests go out.
+    template <int QB, int QE>
+    static __device__ __forceinline__ void dmas(const Lane &L, const Issue &I) {
+        if constexpr (QB < QE) {
+            dma_q<QB>(L, I);
+            dmas<QB + 1, QE>(L, I);
+        }
+    }
+
+    // The 8 MFMAs of one sub-step with DMAs Q0 .. Q0+NQ-1 of the step's refill spread
+    // between them. Each 1 KB DMA holds the CU's address path for about 16 cycles, so
+    // the refill is spread over the whole step: issued in a burst, the DMAs back up
+    // and stall the wave in front of its next MFMA.
+    template <int Q0, int NQ>
     static __device__ __forceinline__ void mma_issue(const Frag &F, floatx16 (&acc)[4][2],
                                                      const Lane &L, const Issue &I) {
-#define OLIVE_MI(VB_, CB_, ...)                                                            \
+#define OLIVE_MI(J_, VB_, CB_)                                                             \
         __builtin_amdgcn_sched_barrier(0);                                               \
         acc[VB_][CB_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[VB_], F.B[CB_],        \
                                                                 acc[VB_][CB_], 0, 0, 0); \
         __builtin_amdgcn_sched_barrier(0);                                               \
-        __VA_ARGS__
-        OLIVE_MI(0, 0, dma_q<0>(L, I); dma_q<1>(L, I);)
-        OLIVE_MI(0, 1, dma_q<2>(L, I); dma_q<3>(L, I);)
-        OLIVE_MI(1, 0, dma_q<4>(L, I); dma_q<5>(L, I);)
-        OLIVE_MI(1, 1, dma_q<6>(L, I); dma_q<7>(L, I);)
-        OLIVE_MI(2, 0, dma_q<8>(L, I);)
-        OLIVE_MI(2, 1, dma_q<9>(L, I);)
-        OLIVE_MI(3, 0, dma_q<10>(L, I);)
-        OLIVE_MI(3, 1, dma_q<11>(L, I);)
+        dmas<Q0 + ((J_) * NQ + 7) / 8, Q0 + ((J_) * NQ + NQ + 7) / 8>(L, I);
+        OLIVE_MI(0, 0, 0)
+        OLIVE_MI(1, 0, 1)
+        OLIVE_MI(2, 1, 0)
+        OLIVE_MI(3, 1, 1)
+        OLIVE_MI(4, 2, 0)
+        OLIVE_MI(5, 2, 1)
+        OLIVE_MI(6, 3, 0)
+        OLIVE_MI(7, 3, 1)
 #undef OLIVE_MI
         __builtin_amdgcn_sched_barrier(0);
     }
@@ -240,22 +250,27 @@ struct Kernel {
         read_frag<0>(L, st, F0);
         __builtin_amdgcn_sched_barrier(0);
         if (PEND) {
-            mma_issue(P, acc, L, I);
+            mma_issue<0, 3>(P, acc, L, I);
             read_frag<1>(L, st, F1);
             __builtin_amdgcn_sched_barrier(0);
-            mma(F0, acc);
+            mma_issue<3, 3>(F0, acc, L, I);
+            read_frag<2>(L, st, F2);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_issue<6, 3>(F1, acc, L, I);
+            read_frag<3>(L, st, P);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_issue<9, 3>(F2, acc, L, I);
         } else {
             read_frag<1>(L, st, F1);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue(F0, acc, L, I);
+            mma_issue<0, 4>(F0, acc, L, I);
+            read_frag<2>(L, st, F2);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_issue<4, 4>(F1, acc, L, I);
+            read_frag<3>(L, st, P);
+            __builtin_amdgcn_sched_barrier(0);
+            mma_issue<8, 4>(F2, acc, L, I);
         }
-        read_frag<2>(L, st, F2);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(F1, acc);
-        read_frag<3>(L, st, P);
-        __builtin_amdgcn_sched_barrier(0);
-        mma(F2, acc);
-        __builtin_amdgcn_sched_barrier(0);
     }
 
     // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
