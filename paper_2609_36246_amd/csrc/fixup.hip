@@ -5,12 +5,18 @@
 // best are closer than the window, rounding could have swapped them relative to
 // the exact values. For each such (row, model) this pass recomputes every logit of
 // the row in fp32 and bounds its rounding error by
-//   e_v = d * 2^-23 * ||h|| * ||w_v||  >=  d * 2^-23 * sum_k |h_k| |w_kv|
-// (Cauchy-Schwarz; the weight-row norms are computed once at init). Entries that
+//   e_v = d * 2^-22 * ||h|| * ||w_v||  >=  2 * d * 2^-23 * sum_k |h_k| |w_kv|
+// (Cauchy-Schwarz, with a factor 2 over the bound of d fp32 roundings so that the
+// packed dot instruction's internal rounding is covered; the weight-row norms are
+// computed once at init). Entries that
 // could still be the exact maximum,
 //   z_v + e_v >= theta = (fp32 max of the scoring pass) - (its own bound),
-// are evaluated in fp64 and the largest wins, lowest index first. The work is split
-// over vocabulary chunks (phase 1) and merged per row in a fixed order (phase 2).
+// are evaluated in fp64 and the largest wins, lowest index first.
+//
+// Work items are (batch of up to FB flagged rows, vocabulary chunk, model): the
+// batch's hidden rows are staged in LDS and every weight row of the chunk is read
+// once for all of them, so W streams from HBM once per batch rather than once per
+// flagged row. Per-chunk winners are merged per row in a fixed order (phase 2).
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -18,8 +24,11 @@
 
 namespace olive {
 
-constexpr int FX_CHUNK = 2048;
+constexpr int FX_CHUNK = 1024;          // vocabulary rows per work item
 constexpr int FX_THREADS = 256;
+constexpr int FX_GROUPS = FX_THREADS / 8;   // 8 lanes per weight row
+constexpr int FX_MAXB = 8;              // flagged rows per pass over W
+constexpr int FX_LDS = 65536;           // bytes of staged hidden rows per work item
 
 struct FxResult {
     double val;
@@ -43,6 +52,27 @@ __device__ __forceinline__ void load8(const float *p, float (&x)[8]) {
     x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// acc + a.lo * b.lo + a.hi * b.hi for two packed bf16 pairs (v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2bf(uint32_t a, uint32_t b, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
+                                           __builtin_bit_cast(bf16x2_t, b), acc, false);
+}
+
+// z[i] += sum over 8 elements at k of h_i[k..k+8) * w[k..k+8), for FB staged rows.
+template <int FB>
+__device__ __forceinline__ void dot8(const uint16_t *hrows, int d, int k, const uint4 &wq,
+                                     float (&z)[FB]) {
+#pragma unroll
+    for (int i = 0; i < FB; ++i) {
+        const uint4 hq = *(const uint4 *)(hrows + i * d + k);
+        z[i] = dot2bf(hq.x, wq.x, z[i]);
+        z[i] = dot2bf(hq.y, wq.y, z[i]);
+        z[i] = dot2bf(hq.z, wq.z, z[i]);
+        z[i] = dot2bf(hq.w, wq.w, z[i]);
+    }
+}
 // Squared L2 norm of every weight row (init only): one wavefront per row.
 template <typename E>
 __global__ void __launch_bounds__(256)
@@ -61,95 +91,175 @@ row_norm_kernel(const E *__restrict__ w, int64_t V, int d, float *__restrict__ o
     }
 }
 
-template <typename E>
+template <typename E, int FB>
 __global__ void __launch_bounds__(FX_THREADS)
 fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int n_chunks,
                   const float *__restrict__ wn_s, const float *__restrict__ wn_t,
                   FxResult *__restrict__ out) {
-    extern __shared__ float hrow[];
-    __shared__ double red_v[FX_THREADS];
-    __shared__ int red_i[FX_THREADS];
-    __shared__ float s_hn;
+    extern __shared__ __attribute__((aligned(16))) char fx_smem[];   // [FB][d] of E
+    __shared__ float s_eb[FB], s_theta[FB];
+    __shared__ double red_v[FX_GROUPS][FB];
+    __shared__ int red_i[FX_GROUPS][FB];
+    E *hrows = (E *)fx_smem;
     const int nf_all = a.sched->n_flagged;
     const int nf = nf_all < cap ? nf_all : cap;
-    const int64_t n_items = (int64_t)nf * n_chunks * 2;
-    const int tid = threadIdx.x;
+    const int n_batches = (nf + FB - 1) / FB;
+    const int64_t n_items = (int64_t)n_batches * n_chunks * 2;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g8 = lane & 7;
     for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
         const int m = (int)(item & 1);
-        const int64_t fc = item >> 1;
-        const int f = (int)(fc % nf);
-        const int c = (int)(fc / nf);
-        const int32_t j = flagged[4 * f];
-        const int32_t mask = flagged[4 * f + 1];
-        const float theta = __int_as_float(flagged[4 * f + 2 + m]);
-        double best_v = -__builtin_inf();
-        int best_i = 0x7fffffff;
-        if (mask & (1 << m)) {   // uniform over the workgroup
-            const int d = m ? a.dt : a.ds;
-            const E *h = (const E *)(m ? a.ht : a.hs) + (int64_t)(a.rowmap[j] & 0x7fffffffu) * d;
-            const E *w = (const E *)(m ? a.wt : a.ws);
-            const float *wn = m ? wn_t : wn_s;
-            __syncthreads();
-            for (int k = tid; k < d; k += FX_THREADS) hrow[k] = load_elem(h, k);
-            __syncthreads();
-            if (tid == 0) {
-                double hh = 0.0;
-                for (int k = 0; k < d; ++k) hh += (double)hrow[k] * hrow[k];
-                s_hn = (float)sqrt(hh) * 1.0001f;
-            }
-            __syncthreads();
-            const float ebound = (float)d * (1.0f / 8388608.0f) * s_hn;
-            // 8 lanes per vocabulary row: each pass of a group reads 128 contiguous
-            // bytes of its row (coalesced), 8 rows per wavefront at a time.
-            const int lane = tid & 63, g8 = lane & 7;
-            const int rows_per_pass = FX_THREADS / 8;
-            const bool vec = (d & 63) == 0 && (((uintptr_t)w & 15) == 0);
-            const int v_end = (c + 1) * FX_CHUNK < a.V ? (c + 1) * FX_CHUNK : a.V;
-            for (int v0 = c * FX_CHUNK; v0 < v_end; v0 += rows_per_pass) {
-                const int v = v0 + (tid >> 3);
-                const bool ok = v < v_end;
-                const E *wr = w + (int64_t)(ok ? v : v_end - 1) * d;
-                float z = 0.f;
-                if (vec) {
-                    for (int k = g8 * 8; k < d; k += 64) {
-                        float x[8];
-                        load8(wr + k, x);
+        const int64_t rest = item >> 1;
+        const int c = (int)(rest % n_chunks);
+        const int f0 = (int)(rest / n_chunks) * FB;
+        const int d = m ? a.dt : a.ds;
+        const E *H = (const E *)(m ? a.ht : a.hs);
+        const E *W = (const E *)(m ? a.wt : a.ws);
+        const float *wn = m ? wn_t : wn_s;
+        // Stage the batch's hidden rows (zeros for rows absent or not flagged for m)
+        // and form each row's error-bound factor d * 2^-23 * ||h|| and its theta.
+        __syncthreads();
+        for (int i = wave; i < FB; i += FX_THREADS / 64) {
+            const int f = f0 + i;
+            const bool use = f < nf && (flagged[4 * (f < nf ? f : 0) + 1] & (1 << m));
+            const E *h = H + (use ? (int64_t)(a.rowmap[flagged[4 * f]] & 0x7fffffffu) * d : 0);
+            double hh = 0.0;
+            bool staged = false;
+            if constexpr (sizeof(E) == 2) {
+                if ((d & 7) == 0 && ((uintptr_t)h & 15) == 0) {
+                staged = true;
+                for (int k = lane * 8; k < d; k += 512) {     // 16-byte pieces
+                    const uint4 q = use ? *(const uint4 *)(h + k) : make_uint4(0, 0, 0, 0);
+                    *(uint4 *)(hrows + i * d + k) = q;
+                    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-                        for (int q = 0; q < 8; ++q) z = fmaf(hrow[k + q], x[q], z);
+                    for (int e = 0; e < 4; ++e) {
+                        const double lo = __uint_as_float(w[e] << 16);
+                        const double hi = __uint_as_float(w[e] & 0xffff0000u);
+                        hh += lo * lo + hi * hi;
                     }
+                }
+                }
+            }
+            if (!staged) {
+                for (int k = lane; k < d; k += 64) {
+                    const E x = use ? h[k] : (E)0;
+                    hrows[i * d + k] = x;
+                    const double xd = load_elem(&x, 0);
+                    hh += xd * xd;
+                }
+            }
+            for (int off = 32; off > 0; off >>= 1) hh += __shfl_xor(hh, off);
+            if (lane == 0) {
+                s_eb[i] = (float)d * (1.0f / 4194304.0f) * ((float)sqrt(hh) * 1.0001f);
+                s_theta[i] = use ? __int_as_float(flagged[4 * f + 2 + m]) : __builtin_inff();
+            }
+        }
+        __syncthreads();
+        float eb[FB], th[FB];
+        double best_v[FB];
+        int best_i[FB];
+#pragma unroll
+        for (int i = 0; i < FB; ++i) {
+            eb[i] = s_eb[i];
+            th[i] = s_theta[i];
+            best_v[i] = -__builtin_inf();
+            best_i[i] = 0x7fffffff;
+        }
+        // 8 lanes per weight row: each pass of a group reads 128 contiguous bytes of its
+        // row (bf16), so a wavefront reads 8 rows at a time, coalesced.
+        const bool vec = (d & 63) == 0 && (((uintptr_t)W & 15) == 0);
+        const int v_end = (c + 1) * FX_CHUNK < a.V ? (c + 1) * FX_CHUNK : a.V;
+        for (int v0 = c * FX_CHUNK; v0 < v_end; v0 += FX_GROUPS) {
+            const int v = v0 + (tid >> 3);
+            const bool ok = v < v_end;
+            const E *wr = W + (int64_t)(ok ? v : v_end - 1) * d;
+            float z[FB];
+#pragma unroll
+            for (int i = 0; i < FB; ++i) z[i] = 0.f;
+            if constexpr (sizeof(E) == 2) {
+                if (vec) {
+                    // 8 independent 16-byte loads in flight per lane (latency, not the
+                    // arithmetic, bounds a row scan), then the packed dot products.
+                    int k = g8 * 8;
+                    for (; k + 7 * 64 < d; k += 8 * 64) {
+                        uint4 wq[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) wq[j] = *(const uint4 *)(wr + k + j * 64);
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) dot8<FB>(hrows, d, k + j * 64, wq[j], z);
+                    }
+                    for (; k < d; k += 64) dot8<FB>(hrows, d, k, *(const uint4 *)(wr + k), z);
                 } else {
-                    for (int k = g8; k < d; k += 8) z = fmaf(hrow[k], load_elem(wr, k), z);
+                    for (int k = g8; k < d; k += 8) {
+                        const float x = load_elem(wr, k);
+#pragma unroll
+                        for (int i = 0; i < FB; ++i)
+                            z[i] = fmaf(load_elem(hrows + i * d, k), x, z[i]);
+                    }
                 }
-                z += __shfl_xor(z, 1);
-                z += __shfl_xor(z, 2);
-                z += __shfl_xor(z, 4);
-                if (ok && g8 == 0 && z + ebound * wn[v] >= theta) {
+            } else if (vec) {
+                for (int k = g8 * 8; k < d; k += 64) {
+                    float x[8];
+                    load8(wr + k, x);
+#pragma unroll
+                    for (int i = 0; i < FB; ++i) {
+                        float hv[8];
+                        load8(hrows + i * d + k, hv);
+#pragma unroll
+                        for (int q = 0; q < 8; ++q) z[i] = fmaf(hv[q], x[q], z[i]);
+                    }
+                }
+            } else {
+                for (int k = g8; k < d; k += 8) {
+                    const float x = load_elem(wr, k);
+#pragma unroll
+                    for (int i = 0; i < FB; ++i) z[i] = fmaf(load_elem(hrows + i * d, k), x, z[i]);
+                }
+            }
+            const float wnv = wn[ok ? v : v_end - 1];
+#pragma unroll
+            for (int i = 0; i < FB; ++i) {
+                z[i] += __shfl_xor(z[i], 1);
+                z[i] += __shfl_xor(z[i], 2);
+                z[i] += __shfl_xor(z[i], 4);
+                // Same decision on the 8 lanes of the group; they then form the fp64
+                // logit together (fixed split and reduction order).
+                if (ok && z[i] + eb[i] * wnv >= th[i]) {
                     double zd = 0.0;
-                    for (int k = 0; k < d; ++k)
-                        zd = fma((double)hrow[k], (double)load_elem(wr, k), zd);
-                    if (zd > best_v || (zd == best_v && v < best_i)) { best_v = zd; best_i = v; }
+                    for (int k = g8; k < d; k += 8)
+                        zd = fma((double)load_elem(hrows + i * d, k), (double)load_elem(wr, k), zd);
+                    zd += __shfl_xor(zd, 1, 8);
+                    zd += __shfl_xor(zd, 2, 8);
+                    zd += __shfl_xor(zd, 4, 8);
+                    if (zd > best_v[i] || (zd == best_v[i] && v < best_i[i])) {
+                        best_v[i] = zd;
+                        best_i[i] = v;
+                    }
                 }
             }
         }
-        red_v[tid] = best_v;
-        red_i[tid] = best_i;
-        __syncthreads();
-        for (int off = FX_THREADS / 2; off > 0; off >>= 1) {
-            if (tid < off) {
-                double ov = red_v[tid + off];
-                int oi = red_i[tid + off];
-                if (ov > red_v[tid] || (ov == red_v[tid] && oi < red_i[tid])) {
-                    red_v[tid] = ov;
-                    red_i[tid] = oi;
-                }
+        if (g8 == 0) {
+#pragma unroll
+            for (int i = 0; i < FB; ++i) {
+                red_v[tid >> 3][i] = best_v[i];
+                red_i[tid >> 3][i] = best_i[i];
             }
-            __syncthreads();
-        }
-        if (tid == 0) {
-            out[item].val = red_v[0];
-            out[item].idx = red_i[0];
         }
         __syncthreads();
+        if (tid < FB && f0 + tid < nf) {
+            double bv = -__builtin_inf();
+            int bi = 0x7fffffff;
+            for (int g = 0; g < FX_GROUPS; ++g) {
+                const double ov = red_v[g][tid];
+                const int oi = red_i[g][tid];
+                if (ov > bv || (ov == bv && oi < bi)) { bv = ov; bi = oi; }
+            }
+            FxResult r;
+            r.val = bv;
+            r.idx = bi;
+            r.pad = 0;
+            out[((int64_t)c * nf + f0 + tid) * 2 + m] = r;
+        }
     }
 }
 
@@ -189,19 +299,40 @@ hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *o
     return hipGetLastError();
 }
 
+template <typename E, int FB>
+static void launch_scan(const ScoreArgs &a, const int32_t *flagged, int cap, int n_chunks,
+                        size_t lds, const float *wn_s, const float *wn_t, FxResult *res,
+                        hipStream_t st) {
+    fixup_scan_kernel<E, FB><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, wn_s,
+                                                             wn_t, res);
+}
+
+template <typename E>
+static void launch_scan_fb(int fb, const ScoreArgs &a, const int32_t *flagged, int cap,
+                           int n_chunks, size_t lds, const float *wn_s, const float *wn_t,
+                           FxResult *res, hipStream_t st) {
+    if (fb >= 8) launch_scan<E, 8>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+    else if (fb >= 4) launch_scan<E, 4>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+    else if (fb >= 2) launch_scan<E, 2>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+    else launch_scan<E, 1>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+}
+
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
                              void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
                              int32_t *am_t, hipStream_t st) {
     const int n_chunks = (a.V + FX_CHUNK - 1) / FX_CHUNK;
     const int dmax = a.ds > a.dt ? a.ds : a.dt;
-    const size_t lds = (size_t)dmax * sizeof(float);
+    const int esz = bf16 ? 2 : 4;
+    // Rows per batch: as many hidden rows as fit the staging budget, a power of two.
+    int fb = FX_LDS / (dmax * esz);
+    fb = fb > FX_MAXB ? FX_MAXB : (fb < 1 ? 1 : fb);
+    fb = fb >= 8 ? 8 : (fb >= 4 ? 4 : (fb >= 2 ? 2 : 1));
+    const size_t lds = (size_t)fb * dmax * esz;
     FxResult *res = (FxResult *)scratch;
     if (bf16)
-        fixup_scan_kernel<uint16_t><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks,
-                                                                   wn_s, wn_t, res);
+        launch_scan_fb<uint16_t>(fb, a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
     else
-        fixup_scan_kernel<float><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, wn_s,
-                                                                wn_t, res);
+        launch_scan_fb<float>(fb, a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     fixup_merge_kernel<<<64, 64, 0, st>>>(a, flagged, cap, n_chunks, res, am_s, am_t);
