@@ -19,8 +19,7 @@ import sys
 import time
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA (no sparsity)
-TRAFFIC_FILE = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles",
-                            "traffic.json")
+PROFILES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles")
 
 
 def log(*a):
@@ -54,10 +53,13 @@ def cpu_baseline(wl, seconds: float):
         t0 = time.perf_counter()
         O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"])
         return time.perf_counter() - t0
-    t_cal = run(order[:4])
-    n = int(max(8, min(4000, seconds / max(t_cal / 4, 1e-6))))
-    n = min(n, len(order))
-    t = run(order[4:4 + n])
+    # Rows in chunks until the timed oracle work reaches `seconds` (only the oracle
+    # calls are timed; gathering the rows is not).
+    n, t, chunk = 0, 0.0, 16
+    while t < seconds and n < len(order):
+        rows = order[n:n + chunk]
+        t += run(rows)
+        n += len(rows)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
     return dict(value=n / t, unit="positions/s", cores=int(threads), kind="oracle",
                 sample="%d random valid rows of the workload (seed 12345), fp64 numpy oracle "
@@ -150,13 +152,7 @@ def main():
         % (args.steps, ms_step, kernel_ms, stats, err))
     flops = 2.0 * t_valid * spec.vocab * (spec.d_student + spec.d_teacher)
     achieved = flops / (kernel_ms * 1e-3) / 1e12
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
-            tr = json.load(f)
-        ent = tr.get(args.workload)
-        if ent and ent.get("kernel_source_sha") == kernel_source_sha():
-            traffic = ent.get("bytes_per_launch")
+    traffic = measured_traffic(args.workload)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
         "value": t_valid / (ms_step * 1e-3),
@@ -190,6 +186,27 @@ def main():
         log("cpu baseline (oracle) on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the scoring kernel from the committed rocprofv3 counter
+    summary of this workload (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's
+    readings), or None when there is none for the current kernel source."""
+    path = os.path.join(PROFILES, "score_mfma_%s_traffic.txt" % workload)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if ":" in line and not line.startswith((" ", "#", "$")):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("kernel_source_sha") != kernel_source_sha():
+        return None
+    try:
+        return float(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def kernel_source_sha() -> str:
