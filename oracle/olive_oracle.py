@@ -16,6 +16,8 @@ What it computes (for every packed position of a batch of stitched rollouts):
   * KL(p_T || p_S) = sum_v p_T[v] (log p_T[v] - log p_S[v])   -- the full
     vocabulary divergence between teacher and student (knowledge distillation
     minimises it, Sec. 6; OPD scores student tokens with the teacher, Sec. 1);
+  * KL(p_S || p_T) = sum_v p_S[v] (log p_S[v] - log p_T[v])   -- the reverse
+    direction, the per-token objective of on-policy distillation (Sec. 1);
   * argmax_X = lowest v attaining M_X   -- the greedy token (the K = 1 case of the
     top-K overlap statistic of Sec. 4.1);
   * masks: a position is valid when it precedes the sequence's valid length, and
@@ -125,6 +127,17 @@ def kl_teacher_student(z_t, lse_t: float, z_s, lse_s: float) -> tuple:
     return direct, nonneg
 
 
+def kl_student_teacher(z_s, lse_s: float, z_t, lse_t: float) -> tuple:
+    """Reverse KL(p_S || p_T) of one row: sum_v p_S (log p_S - log p_T), the
+    divergence on-policy distillation minimises on student tokens (Sec. 1).
+
+    The same definition as kl_teacher_student with the roles of the two
+    distributions exchanged (the first argument is the one the sum weights by);
+    returns the direct and the pointwise non-negative forms.
+    """
+    return kl_teacher_student(z_s, lse_s, z_t, lse_t)
+
+
 def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1.0,
                h_teacher_rows=None, w_teacher=None, scale_teacher: float = 1.0,
                chunk: Optional[int] = None) -> dict:
@@ -132,7 +145,8 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
 
     Returns float64 / int64 arrays of length n: z_y_s, lse_s, logp_s, argmax_s,
     gap_s, max_s, and with a teacher the same for t plus kl (direct) and
-    kl_nonneg.
+    kl_nonneg (KL(teacher || student)), kl_rev and kl_rev_nonneg (KL(student ||
+    teacher)).
     """
     hs = _f64(h_student_rows)
     n = hs.shape[0]
@@ -149,7 +163,8 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     out = {k: np.zeros(n) for k in ("z_y_s", "lse_s", "logp_s", "gap_s", "max_s")}
     out["argmax_s"] = np.zeros(n, dtype=np.int64)
     if has_t:
-        for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg"):
+        for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg", "kl_rev",
+                  "kl_rev_nonneg"):
             out[k] = np.zeros(n)
         out["argmax_t"] = np.zeros(n, dtype=np.int64)
     for r0 in range(0, n, chunk):
@@ -176,6 +191,9 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
                 kl, klp = kl_teacher_student(zt[i], tt["lse"], zs[i], st["lse"])
                 out["kl"][g] = kl
                 out["kl_nonneg"][g] = klp
+                klr, klrp = kl_student_teacher(zs[i], st["lse"], zt[i], tt["lse"])
+                out["kl_rev"][g] = klr
+                out["kl_rev_nonneg"][g] = klrp
     return out
 
 
@@ -186,7 +204,8 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
     """The whole scoring of a packed batch, masked.
 
     Outputs per packed position (length T): logp_s, logp_t, argmax_s, argmax_t,
-    kl (KL(teacher || student) in-region, exactly +0.0 elsewhere); at positions
+    kl (KL(teacher || student) in-region, exactly +0.0 elsewhere), kl_rev
+    (KL(student || teacher), masked the same way); at positions
     past the valid length logp = 0 and argmax = -1. Per sequence: ce (Eq. 1's
     loss, minus the sum of the student's log-probs over the in-region positions).
     Counts: n_scored (in-region positions) and t_valid (valid positions).
@@ -207,7 +226,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
                        scale_teacher)
     out = dict(logp_s=np.zeros(T), argmax_s=np.full(T, -1, dtype=np.int64),
                lse_s=np.zeros(T), gap_s=np.full(T, math.inf), kl=np.zeros(T),
-               kl_nonneg=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
+               kl_nonneg=np.zeros(T), kl_rev=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
     if has_t:
         out.update(logp_t=np.zeros(T), argmax_t=np.full(T, -1, dtype=np.int64),
                    lse_t=np.zeros(T), gap_t=np.full(T, math.inf))
@@ -221,6 +240,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
             inr = m["in_region"][sel]
             out["kl"][sel[inr]] = r["kl"][inr]
             out["kl_nonneg"][sel[inr]] = r["kl_nonneg"][inr]
+            out["kl_rev"][sel[inr]] = r["kl_rev"][inr]
     # Eq. 1: the loss of sequence b is minus the sum of the student's log-probs of
     # its in-region tokens; an empty region gives 0.
     ce = np.zeros(B)

@@ -3,7 +3,8 @@
 The paper prints no numeric example of the scoring, so each case here is chosen so
 that its answer follows by hand from the definitions the scoring uses: the softmax
 log-prob of a realised token (the summand of Eq. 1, Sec. 3.1), the full-vocabulary
-KL(teacher || student) (the divergence distillation minimises, Sec. 6), the cut
+KL(teacher || student) (the divergence distillation minimises, Sec. 6) and its
+reverse KL(student || teacher) (on-policy distillation's objective, Sec. 1), the cut
 mask of Eq. 1 (prompt and prefix excluded, continuation scored) and the greedy
 (lowest-index) argmax. The expected values are evaluated from those closed forms
 with the standard `math` module only; nothing here calls the oracle or the GPU
@@ -30,9 +31,11 @@ cases.append(dict(
         lse_t=[math.log(6.0)], lse_s=[math.log(3.0)],
         logp_t=[math.log(0.5)], logp_s=[-math.log(3.0)],
         kl=[(1.0 / 6.0) * math.log(0.5) + 0.5 * math.log(1.5)],
+        kl_rev=[math.log(4.0 / 3.0) / 3.0],
         argmax_t=[2], argmax_s=[0], n_scored=1, t_valid=1,
         ce=[math.log(3.0)]),
     derivation="p_T = (1,2,3)/6; p_S = (1,1,1)/3; KL = sum p_T ln(p_T/p_S); "
+               "reverse KL = sum p_S ln(p_S/p_T) = (1/3)(ln 2 + ln 1 + ln(2/3)); "
                "student argmax is the lowest of three tied zeros"))
 
 # 2. A stitched sequence of length 7, cut 4, valid length 6 (one token past EOS):
@@ -46,7 +49,7 @@ cases.append(dict(
     targets=[0, 1, 2, 3, 0, 1, 2], cu_seqlens=[0, 7], cut=[4], valid_len=[6],
     expect=dict(
         logp_s=[-math.log(4.0)] * 6 + [0.0], logp_t=[-math.log(4.0)] * 6 + [0.0],
-        kl=[0.0] * 7, argmax_s=[0] * 6 + [-1], argmax_t=[0] * 6 + [-1],
+        kl=[0.0] * 7, kl_rev=[0.0] * 7, argmax_s=[0] * 6 + [-1], argmax_t=[0] * 6 + [-1],
         n_scored=2, t_valid=6, ce=[2.0 * math.log(4.0)]),
     derivation="equal logits -> p = 1/4; scored t in {4,5}; t = 6 is past the valid length"))
 
@@ -59,6 +62,7 @@ def softplus(x):
 ps1 = 1.0 / (1.0 + math.exp(zs[0] - zs[1]))
 pt1 = 1.0 / (1.0 + math.exp(zt[0] - zt[1]))
 kl_bern = pt1 * math.log(pt1 / ps1) + (1 - pt1) * math.log((1 - pt1) / (1 - ps1))
+kl_bern_rev = ps1 * math.log(ps1 / pt1) + (1 - ps1) * math.log((1 - ps1) / (1 - pt1))
 cases.append(dict(
     name="two_token_closed_form",
     d_student=1, d_teacher=1, vocab=2,
@@ -67,12 +71,13 @@ cases.append(dict(
     targets=[0], cu_seqlens=[0, 1], cut=[0], valid_len=None,
     expect=dict(
         logp_s=[-softplus(zs[1] - zs[0])], logp_t=[-softplus(zt[1] - zt[0])],
-        kl=[kl_bern], argmax_s=[0], argmax_t=[1], n_scored=1, t_valid=1,
+        kl=[kl_bern], kl_rev=[kl_bern_rev], argmax_s=[0], argmax_t=[1], n_scored=1, t_valid=1,
         ce=[softplus(zs[1] - zs[0])]),
-    derivation="Bernoulli: p(1) = sigmoid(z1 - z0); KL = p ln(p/q) + (1-p) ln((1-p)/(1-q))"))
+    derivation="Bernoulli: p(1) = sigmoid(z1 - z0); KL = p ln(p/q) + (1-p) ln((1-p)/(1-q)); "
+               "the reverse exchanges p and q"))
 
 out = dict(
-    source="closed forms of the scoring definitions (Sec. 3.1 Eq. 1; Sec. 6 KL); "
+    source="closed forms of the scoring definitions (Sec. 3.1 Eq. 1; Sec. 6 KL; Sec. 1 reverse KL); "
            "the paper prints no numeric worked example",
     cases=cases)
 path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "worked_examples.json")

@@ -15,6 +15,7 @@ from tests import test_oracle_pins as P
 
 _orig_lss = O.log_softmax_stats
 _orig_kl = O.kl_teacher_student
+_orig_klr = O.kl_student_teacher
 _orig_masks = O.masks
 _orig_project = O.project
 
@@ -49,6 +50,18 @@ def kl_wrong_sign(z_t, lse_t, z_s, lse_s):
     return -a, -b
 
 
+def klr_forward(z_s, lse_s, z_t, lse_t):
+    return _orig_klr(z_t, lse_t, z_s, lse_s)
+
+
+def klr_dropped_cross_term(z_s, lse_s, z_t, lse_t):
+    # sum p_S log p_S only (the entropy part): forgets the teacher term
+    a, b = _orig_klr(z_s, lse_s, z_s, lse_s)
+    lp = np.asarray(z_s, dtype=np.float64) - lse_s
+    ent = -math.fsum((np.exp(lp) * lp).tolist())
+    return a - ent, b - ent
+
+
 def masks_off_by_one(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER):
     return _orig_masks(cu_seqlens, np.asarray(cut) + 1, valid_len, region)
 
@@ -74,6 +87,8 @@ MUTANTS = [
     ("log_softmax_stats", lss_plain_sum_of_logits),
     ("kl_teacher_student", kl_reversed),
     ("kl_teacher_student", kl_wrong_sign),
+    ("kl_student_teacher", klr_forward),
+    ("kl_student_teacher", klr_dropped_cross_term),
     ("masks", masks_off_by_one),
     ("masks", masks_ignore_valid),
     ("project", project_no_scale),
@@ -88,6 +103,8 @@ PINS = [
     P.test_probabilities_sum_to_one_and_lse_bounds,
     P.test_kl_nonnegative_and_two_forms_agree,
     P.test_kl_cross_entropy_identity,
+    P.test_kl_zero_for_identical_models_and_row_shift,
+    P.test_peaked_student_limit_of_reverse_kl,
     P.test_argmax_exact_ties_take_lowest_index,
     P.test_mask_counts_enumerated,
     P.test_eq1_masks_prefix_and_scores_continuation,

@@ -67,6 +67,9 @@ def test_decimal_brute_force(seed):
         kl = sum((lt.exp() * (lt - ls) for lt, ls in zip(lpt, lps)), Decimal(0))
         assert abs(r["kl"][i] - float(kl)) <= 1e-13 * max(1.0, float(kl))
         assert abs(r["kl_nonneg"][i] - float(kl)) <= 1e-13 * max(1.0, float(kl))
+        klr = sum((ls.exp() * (ls - lt) for lt, ls in zip(lpt, lps)), Decimal(0))
+        assert abs(r["kl_rev"][i] - float(klr)) <= 1e-13 * max(1.0, float(klr))
+        assert abs(r["kl_rev_nonneg"][i] - float(klr)) <= 1e-13 * max(1.0, float(klr))
         # greedy token: first index attaining the exact maximum
         ms = max(zs)
         assert r["argmax_s"][i] == min(v for v in range(V) if zs[v] == ms)
@@ -84,7 +87,7 @@ def test_golden_worked_examples():
                       None if c["valid_len"] is None else np.array(c["valid_len"]),
                       np.array(c["h_teacher"]), np.array(c["w_teacher"]))
         e = c["expect"]
-        for k in ("logp_s", "logp_t", "kl", "ce", "lse_s", "lse_t"):
+        for k in ("logp_s", "logp_t", "kl", "kl_rev", "ce", "lse_s", "lse_t"):
             if k in e:
                 np.testing.assert_allclose(out[k], e[k], rtol=0, atol=1e-14, err_msg=c["name"] + k)
         for k in ("argmax_s", "argmax_t"):
@@ -119,6 +122,8 @@ def test_two_token_softplus_and_bernoulli_kl():
         q = 1.0 / (1.0 + math.exp(a[0, 0] - a[0, 1]))   # student P(token 1)
         kl = p * math.log(p / q) + (1 - p) * math.log((1 - p) / (1 - q))
         assert abs(r["kl"][0] - kl) <= 1e-13
+        klr = q * math.log(q / p) + (1 - q) * math.log((1 - q) / (1 - p))
+        assert abs(r["kl_rev"][0] - klr) <= 1e-13
 
 
 # ----------------------------------------------------------------------------- invariants
@@ -155,6 +160,11 @@ def test_kl_nonnegative_and_two_forms_agree():
     assert np.all(r["kl_nonneg"] >= 0.0)
     assert np.all(r["kl"] >= -1e-12)
     np.testing.assert_allclose(r["kl"], r["kl_nonneg"], rtol=1e-12, atol=1e-12)
+    assert np.all(r["kl_rev_nonneg"] >= 0.0)
+    assert np.all(r["kl_rev"] >= -1e-12)
+    np.testing.assert_allclose(r["kl_rev"], r["kl_rev_nonneg"], rtol=1e-12, atol=1e-12)
+    # the two directions differ for distinct distributions
+    assert np.all(np.abs(r["kl_rev"] - r["kl"]) > 1e-6)
 
 
 def test_kl_cross_entropy_identity():
@@ -171,6 +181,11 @@ def test_kl_cross_entropy_identity():
         cross = -math.fsum(p * l for p, l in zip(pt, ls))
         ent = -math.fsum(p * l for p, l in zip(pt, lt))
         assert abs(r["kl"][i] - (cross - ent)) <= 1e-12
+        # reverse: KL(p_S||p_T) = H(p_S, p_T) - H(p_S)
+        ps = [math.exp(v) for v in ls]
+        cross_r = -math.fsum(p * l for p, l in zip(ps, lt))
+        ent_r = -math.fsum(p * l for p, l in zip(ps, ls))
+        assert abs(r["kl_rev"][i] - (cross_r - ent_r)) <= 1e-12
 
 
 def test_kl_zero_for_identical_models_and_row_shift():
@@ -180,6 +195,7 @@ def test_kl_zero_for_identical_models_and_row_shift():
     ws = bf16_values((d, V), rng, 0.5)
     r = O.row_scores(hs, ws, np.arange(n), 1.0, hs, ws, 1.0)
     assert np.all(r["kl"] == 0.0)
+    assert np.all(r["kl_rev"] == 0.0)
     np.testing.assert_array_equal(r["logp_s"], r["logp_t"])
     # teacher logits = student logits + a per-row constant: identical distributions
     c = bf16_values((1, V), rng)[0] * 0 + 3.0
@@ -187,6 +203,7 @@ def test_kl_zero_for_identical_models_and_row_shift():
     wt = np.concatenate([ws, np.full((1, V), c[0])], axis=0)
     r2 = O.row_scores(hs, ws, np.arange(n), 1.0, ht, wt, 1.0)
     assert np.all(np.abs(r2["kl"]) <= 1e-12)
+    assert np.all(np.abs(r2["kl_rev"]) <= 1e-12)
     assert np.all(np.abs(r2["logp_t"] - r2["logp_s"]) <= 1e-12)
 
 
@@ -199,6 +216,18 @@ def test_peaked_teacher_limit():
     for s in (64.0, 256.0):
         rr = O.row_scores(hs, ws, r["argmax_t"], 1.0, ht, wt, s)
         np.testing.assert_allclose(rr["kl"], -rr["logp_s"], rtol=0, atol=1e-6 * (64.0 / s) + 1e-9)
+
+
+def test_peaked_student_limit_of_reverse_kl():
+    """As p_S becomes one-hot at v*, KL(p_S||p_T) -> -log p_T(v*)."""
+    rng = np.random.default_rng(16)
+    hs, ht = bf16_values((3, 8), rng), bf16_values((3, 8), rng)
+    ws, wt = bf16_values((8, 64), rng), bf16_values((8, 64), rng)
+    r = O.row_scores(hs, ws, np.zeros(3, dtype=np.int64), 1.0, ht, wt, 1.0)
+    for s in (64.0, 256.0):
+        rr = O.row_scores(hs, ws, r["argmax_s"], s, ht, wt, 1.0)
+        np.testing.assert_allclose(rr["kl_rev"], -rr["logp_t"], rtol=0,
+                                   atol=1e-6 * (64.0 / s) + 1e-9)
 
 
 def test_lse_of_iid_gaussian_logits():
