@@ -154,6 +154,36 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
                              int32_t *argmax_student, int32_t *argmax_teacher,
                              float *ce_per_seq, void *hip_stream);
 
+/*
+ * Output set of olive_score_batch. Every pointer may be NULL (that output is not
+ * formed); at least one must be set. Device buffers, caller-owned, as in
+ * olive_kl_masked.
+ */
+typedef struct {
+    int32_t size;                /* host: sizeof(olive_score_outputs) (checked) */
+    int32_t reserved;            /* 0 */
+    float *kl;                   /* [T] fp32: KL(teacher || student) in the region, +0.0
+                                    elsewhere (the divergence distillation minimises, Sec. 6) */
+    float *kl_reverse;           /* [T] fp32: KL(student || teacher), masked the same way (the
+                                    per-token objective of on-policy distillation, Sec. 1) */
+    int64_t *counts;             /* [2] int64: scored (region and valid) and valid positions */
+    float *logp_student;         /* [T] fp32, as in olive_token_logprobs */
+    float *logp_teacher;         /* [T] fp32 */
+    int32_t *argmax_student;     /* [T] int32 */
+    int32_t *argmax_teacher;     /* [T] int32 */
+    float *ce_per_seq;           /* [B] fp32: Eq. 1's loss per sequence */
+} olive_score_outputs;
+
+/*
+ * Every per-position output of one batch in one fused pass over the vocabulary:
+ * olive_kl_masked's outputs plus the reverse KL. Teacher outputs (kl, kl_reverse,
+ * logp_teacher, argmax_teacher) need a teacher context and b->h_teacher.
+ * Errors: E_NULL (out, or every output pointer, NULL), E_RANGE (out->size wrong),
+ * and as olive_kl_masked.
+ */
+olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
+                               const olive_score_outputs *out, void *hip_stream);
+
 /* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
 olive_status olive_score_free(olive_score_ctx *ctx);
 

@@ -52,6 +52,14 @@ class olive_batch(ctypes.Structure):
                 ("h_teacher", ctypes.c_void_p)]
 
 
+class olive_score_outputs(ctypes.Structure):
+    _fields_ = [("size", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("kl", ctypes.c_void_p), ("kl_reverse", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p), ("logp_student", ctypes.c_void_p),
+                ("logp_teacher", ctypes.c_void_p), ("argmax_student", ctypes.c_void_p),
+                ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p)]
+
+
 class OliveError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
@@ -81,6 +89,9 @@ def load() -> ctypes.CDLL:
     lib.olive_kl_masked.argtypes = [vp, ctypes.POINTER(olive_batch), f32p, i64p, f32p, f32p,
                                     i32p, i32p, f32p, vp]
     lib.olive_kl_masked.restype = st
+    lib.olive_score_batch.argtypes = [vp, ctypes.POINTER(olive_batch),
+                                      ctypes.POINTER(olive_score_outputs), vp]
+    lib.olive_score_batch.restype = st
     lib.olive_score_free.argtypes = [vp]
     lib.olive_score_free.restype = st
     lib.olive_status_string.argtypes = [st]
@@ -171,6 +182,27 @@ def olive_kl_masked(ctx, batch: olive_batch, kl, counts=None, logp_student=None,
                                _ptr(argmax_teacher), _ptr(ce_per_seq), _stream(stream))
     if check:
         _check(s, "olive_kl_masked")
+    return s
+
+
+def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_teacher=None,
+                 argmax_student=None, argmax_teacher=None, ce_per_seq=None) -> olive_score_outputs:
+    o = olive_score_outputs()
+    o.size = ctypes.sizeof(olive_score_outputs)
+    o.reserved = 0
+    o.kl, o.kl_reverse, o.counts = _ptr(kl), _ptr(kl_reverse), _ptr(counts)
+    o.logp_student, o.logp_teacher = _ptr(logp_student), _ptr(logp_teacher)
+    o.argmax_student, o.argmax_teacher = _ptr(argmax_student), _ptr(argmax_teacher)
+    o.ce_per_seq = _ptr(ce_per_seq)
+    return o
+
+
+def olive_score_batch(ctx, batch: olive_batch, outputs: olive_score_outputs, stream=None,
+                      check: bool = True) -> int:
+    s = load().olive_score_batch(ctx, ctypes.byref(batch), ctypes.byref(outputs),
+                                 _stream(stream))
+    if check:
+        _check(s, "olive_score_batch")
     return s
 
 

@@ -5,6 +5,7 @@
 // product of the hidden row with the token's weight row, and writes
 //   logp_X = s_X z_X[y] - lse_X,   lse_X = s_X best_X + ln Z_X,
 //   kl     = A / Z_T - lse_T + lse_S   (KL(teacher || student), in-region only),
+//   kl_rev = B / Z_S - lse_S + lse_T   (KL(student || teacher), in-region only),
 //   argmax_X = lowest index attaining the max,
 // queueing rows whose top-2 gap is inside the fp32 error window for the exact
 // re-decision of their greedy token.
@@ -96,7 +97,8 @@ __global__ void __launch_bounds__(256)
 combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
                int32_t *__restrict__ err, float *__restrict__ logp_s, float *__restrict__ logp_t,
                int32_t *__restrict__ am_s, int32_t *__restrict__ am_t, float *__restrict__ kl,
-               float *__restrict__ logp_tmp, int32_t *__restrict__ flagged, int flag_cap) {
+               float *__restrict__ kl_rev, float *__restrict__ logp_tmp,
+               int32_t *__restrict__ flagged, int flag_cap) {
     const int lane = threadIdx.x & 63;
     const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     Sched *sched = const_cast<Sched *>(a.sched);
@@ -115,6 +117,7 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
             if (am_s) am_s[g] = -1;
             if (HAS_T && am_t) am_t[g] = -1;
             if (HAS_T && kl) kl[g] = inr ? qnan : 0.f;
+            if (HAS_T && kl_rev) kl_rev[g] = inr ? qnan : 0.f;
         }
         return;
     }
@@ -129,15 +132,16 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
     }
     const int ns = sched->n_splits;
     Stat ss = stat_identity(), st = stat_identity();
-    float acc_a = 0.f, dummy = 0.f;
+    float acc_a = 0.f, acc_b = 0.f;
     if (lane < ns) {
         ss = load_stat(a.part, a.pstride, F_BEST_S, lane, j);
         if (HAS_T) {
             st = load_stat(a.part, a.pstride, F_BEST_T, lane, j);
             acc_a = a.part[(F_A * MAX_SPLITS + lane) * a.pstride + j];
+            if (kl_rev) acc_b = a.part[(F_B * MAX_SPLITS + lane) * a.pstride + j];
         }
     }
-    wave_merge(ss, dummy, a.cS);
+    wave_merge(ss, acc_b, a.cS);
     if (HAS_T) wave_merge(st, acc_a, a.cT);
     // Every lane now holds the merged statistics.
     int fl = (am_s && near_tie(ss, a.sS)) ? 1 : 0;
@@ -171,6 +175,12 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
             float v = an / st.z - lse_t + lse_s;
             kl[g] = inr ? v : 0.f;
         }
+        if (kl_rev) {
+            // KL(student || teacher) = sum p_S (s_S zS - s_T zT) - lse_S + lse_T
+            float bn = same_scale ? a.sS * acc_b : acc_b;
+            float v = bn / ss.z - lse_s + lse_t;
+            kl_rev[g] = inr ? v : 0.f;
+        }
     }
     if (fl && flagged) {
         int q = atomicAdd(&sched->n_flagged, 1);
@@ -185,30 +195,22 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
 
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
-                          int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
+                          int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,
                           int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st) {
     if (max_rows <= 0) return hipSuccess;
     dim3 grid((unsigned)((max_rows + 3) / 4));
     int same = same_scale ? 1 : 0;
+#define OLIVE_COMBINE(E_, T_)                                                                \
+    combine_kernel<E_, T_><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s, logp_t, am_s, \
+                                                 am_t, kl, kl_rev, logp_tmp, flagged, flag_cap)
     if (bf16) {
-        if (has_t)
-            combine_kernel<uint16_t, true><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
-                                                                 logp_t, am_s, am_t, kl, logp_tmp,
-                                                                 flagged, flag_cap);
-        else
-            combine_kernel<uint16_t, false><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
-                                                                  logp_t, am_s, am_t, kl,
-                                                                  logp_tmp, flagged, flag_cap);
+        if (has_t) OLIVE_COMBINE(uint16_t, true);
+        else OLIVE_COMBINE(uint16_t, false);
     } else {
-        if (has_t)
-            combine_kernel<float, true><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
-                                                              logp_t, am_s, am_t, kl, logp_tmp,
-                                                              flagged, flag_cap);
-        else
-            combine_kernel<float, false><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s,
-                                                               logp_t, am_s, am_t, kl, logp_tmp,
-                                                               flagged, flag_cap);
+        if (has_t) OLIVE_COMBINE(float, true);
+        else OLIVE_COMBINE(float, false);
     }
+#undef OLIVE_COMBINE
     return hipGetLastError();
 }
 

@@ -63,16 +63,16 @@ olive_status dev_alloc(T **p, size_t bytes) {
 
 olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP; }
 
-// The scoring of one batch, shared by olive_token_logprobs and olive_kl_masked.
-olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t *counts,
-                 float *logp_s, float *logp_t, int32_t *am_s, int32_t *am_t, float *ce,
-                 hipStream_t st) {
+// The scoring of one batch, shared by every scoring entry point.
+olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, float *kl_rev,
+                 int64_t *counts, float *logp_s, float *logp_t, int32_t *am_s, int32_t *am_t,
+                 float *ce, hipStream_t st) {
     const olive_score_desc &d = ctx->desc;
     if (!b->cu_seqlens || !b->cut || !b->targets || !b->h_student) return OLIVE_E_NULL;
     if (b->num_seqs < 1 || b->num_seqs > d.max_seqs) return OLIVE_E_SHAPE;
     if (b->total_positions < 1 || b->total_positions > d.max_positions) return OLIVE_E_SHAPE;
     if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) return OLIVE_E_RANGE;
-    const bool want_t = kl || logp_t || am_t;
+    const bool want_t = kl || kl_rev || logp_t || am_t;
     if (want_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
     const bool has_t = want_t;
     const int64_t T = b->total_positions;
@@ -103,7 +103,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t 
     if (s) return s;
     s = check_hip(launch_rowmap(*b, V, ctx->seqbuf, ctx->sched, ctx->rowmap, ctx->err, logp_s,
                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
-                                has_t ? kl : nullptr, logp_tmp, st));
+                                has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, st));
     if (s) return s;
 
     ScoreArgs a;
@@ -128,7 +128,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t 
     const int slot = (int)(ctx->n_calls % 64);
     if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
     if (mfma)
-        s = check_hip(launch_score_mfma(a, has_t, same_scale, grid, st));
+        s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, grid, st));
     else
         s = check_hip(launch_score_simple(a, ctx->bf16, has_t, max_units, st));
     if (s) return s;
@@ -140,7 +140,8 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, int64_t 
     int32_t *flagged = (am_s || (has_t && am_t)) ? ctx->flagged : nullptr;
     s = check_hip(launch_combine(a, ctx->bf16, has_t, same_scale, b->targets, ctx->err, logp_s,
                                  has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
-                                 has_t ? kl : nullptr, logp_tmp, flagged, ctx->flag_cap, T, st));
+                                 has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, flagged,
+                                 ctx->flag_cap, T, st));
     if (s) return s;
     if (flagged) {
         s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
@@ -267,7 +268,7 @@ olive_status olive_token_logprobs(olive_score_ctx *ctx, const olive_batch *b, fl
                                   float *logp_teacher, int32_t *argmax_student,
                                   int32_t *argmax_teacher, void *hip_stream) {
     if (!ctx || !b || !logp_student) return OLIVE_E_NULL;
-    return run(ctx, b, nullptr, nullptr, logp_student, logp_teacher, argmax_student,
+    return run(ctx, b, nullptr, nullptr, nullptr, logp_student, logp_teacher, argmax_student,
                argmax_teacher, nullptr, (hipStream_t)hip_stream);
 }
 
@@ -277,8 +278,20 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
                              void *hip_stream) {
     if (!ctx || !b || !kl) return OLIVE_E_NULL;
     if (!ctx->has_t) return OLIVE_E_UNSUPPORTED;
-    return run(ctx, b, kl, counts, logp_student, logp_teacher, argmax_student, argmax_teacher,
-               ce_per_seq, (hipStream_t)hip_stream);
+    return run(ctx, b, kl, nullptr, counts, logp_student, logp_teacher, argmax_student,
+               argmax_teacher, ce_per_seq, (hipStream_t)hip_stream);
+}
+
+olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
+                               const olive_score_outputs *out, void *hip_stream) {
+    if (!ctx || !b || !out) return OLIVE_E_NULL;
+    if (out->size != (int32_t)sizeof(olive_score_outputs)) return OLIVE_E_RANGE;
+    if (!out->kl && !out->kl_reverse && !out->counts && !out->logp_student &&
+        !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq)
+        return OLIVE_E_NULL;
+    return run(ctx, b, out->kl, out->kl_reverse, out->counts, out->logp_student,
+               out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
+               (hipStream_t)hip_stream);
 }
 
 olive_status olive_score_free(olive_score_ctx *ctx) {

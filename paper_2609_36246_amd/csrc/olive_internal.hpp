@@ -16,11 +16,13 @@ namespace olive {
 //   Z:        sum_v exp(s * (z_v - BEST)) over the split;
 //   A:        sum_v exp(s_T * (zT_v - BEST_T)) * D_v, the teacher-weighted logit
 //             difference D_v = zT_v - zS_v (equal scales; multiplied by s at the
-//             end) or s_T zT_v - s_S zS_v (different scales).
+//             end) or s_T zT_v - s_S zS_v (different scales);
+//   B:        sum_v exp(s_S * (zS_v - BEST_S)) * (-D_v), the student-weighted
+//             difference (reverse KL; written only when it is requested).
 enum Field {
     F_BEST_S = 0, F_SEC_S = 1, F_IDX_S = 2, F_Z_S = 3,
-    F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8,
-    NFIELDS = 9
+    F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8, F_B = 9,
+    NFIELDS = 10
 };
 
 // Device-side schedule of one call, written by the preparation kernel.
@@ -69,15 +71,15 @@ hipError_t launch_prep(const olive_batch &b, int64_t V, int32_t *seqbuf, Sched *
                        int n_vtiles, int grid, int fixed_splits, hipStream_t st);
 hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
-                         float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
-                         hipStream_t st);
+                         float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
+                         float *logp_tmp, hipStream_t st);
 hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_t max_units,
                                hipStream_t st);
-hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, int grid,
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev, int grid,
                              hipStream_t st);
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
-                          int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
+                          int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,
                           int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st);
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
                              void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,

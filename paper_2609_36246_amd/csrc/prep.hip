@@ -142,7 +142,8 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
               const int32_t *__restrict__ seqbuf, const Sched *__restrict__ sched,
               uint32_t *__restrict__ rowmap, float *__restrict__ logp_s,
               float *__restrict__ logp_t, int32_t *__restrict__ am_s, int32_t *__restrict__ am_t,
-              float *__restrict__ kl, float *__restrict__ logp_tmp) {
+              float *__restrict__ kl, float *__restrict__ kl_rev,
+              float *__restrict__ logp_tmp) {
     const int32_t *cvalid = seqbuf;
     const int32_t *vl_eff = seqbuf + (B + 1);
     const int32_t *cut_eff = seqbuf + 2 * (B + 1);
@@ -169,6 +170,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (am_s) am_s[g] = -1;
             if (am_t) am_t[g] = -1;
             if (kl) kl[g] = qnan;
+            if (kl_rev) kl_rev[g] = qnan;
             if (logp_tmp) logp_tmp[g] = qnan;
             continue;
         }
@@ -181,6 +183,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (am_s) am_s[g] = -1;
             if (am_t) am_t[g] = -1;
             if (kl) kl[g] = 0.f;
+            if (kl_rev) kl_rev[g] = 0.f;
             if (logp_tmp) logp_tmp[g] = 0.f;
         }
     }
@@ -260,8 +263,8 @@ hipError_t launch_prep(const olive_batch &b, int64_t V, int32_t *seqbuf, Sched *
 
 hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
-                         float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *logp_tmp,
-                         hipStream_t st) {
+                         float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
+                         float *logp_tmp, hipStream_t st) {
     (void)V; (void)err;
     int64_t T = b.total_positions;
     int64_t blocks = (T + 255) / 256;
@@ -269,7 +272,7 @@ hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
     if (blocks < 1) blocks = 1;
     rowmap_kernel<<<(unsigned)blocks, 256, 0, st>>>(b.cu_seqlens, b.num_seqs, T, b.region,
                                                     seqbuf, sched, rowmap, logp_s, logp_t, am_s,
-                                                    am_t, kl, logp_tmp);
+                                                    am_t, kl, kl_rev, logp_tmp);
     return hipGetLastError();
 }
 

@@ -117,7 +117,7 @@ struct Run {                // running statistics of one position column
     int idx;
 };
 
-template <bool HAS_T, bool SAME>
+template <bool HAS_T, bool SAME, bool REV>
 struct Kernel {
     // Addresses of the 12 DMAs of one step (8 W, 4 H) of model `m`, K step kk,
     // vocabulary tile vt, into ring stage `st`. DMA i of a wave fills stage rows
@@ -274,11 +274,14 @@ struct Kernel {
     }
 
     // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
-    // vb, column cb) into a model's running statistics. Returns the exp weights'
-    // rescale through `e[]` so the teacher can form its difference sum.
+    // vb, column cb) into a model's running statistics. With DIFF, also the sum of
+    // the block's exp weights times the logit difference to the other model
+    // (z - o with equal scales, s_self z - s_other o otherwise) into Aacc: the
+    // teacher's forms the forward KL, the student's the reverse one.
+    template <bool DIFF>
     static __device__ __forceinline__ void fold_block(const float (&z)[16], Run &R, float &Aacc,
-                                                      bool teacher, const float (&zs)[16],
-                                                      float c, float sS, float sT, int vcode0) {
+                                                      const float (&o)[16], float c, float s_self,
+                                                      float s_other, int vcode0) {
         float tm = R.best, ts = R.sec;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
@@ -293,7 +296,7 @@ struct Kernel {
         const bool up = tm > R.best;
         const float resc = fast_exp2((R.best - tm) * c);
         R.z *= resc;
-        if (teacher) Aacc *= resc;
+        if (DIFF) Aacc *= resc;
         R.idx = up ? vcode0 + code : R.idx;
         R.best = tm;
         R.sec = ts;
@@ -303,17 +306,17 @@ struct Kernel {
         for (int r = 0; r < 16; ++r) {
             const float e = fast_exp2(fmaf(z[r], c, mneg));
             zsum += e;
-            if (teacher) {
+            if (DIFF) {
                 float dlt;
                 {
 #pragma clang fp contract(off)
-                    dlt = SAME ? (z[r] - zs[r]) : (sT * z[r] - sS * zs[r]);
+                    dlt = SAME ? (z[r] - o[r]) : (s_self * z[r] - s_other * o[r]);
                 }
                 asum = fmaf(e, dlt, asum);
             }
         }
         R.z += zsum;
-        if (teacher) Aacc += asum;
+        if (DIFF) Aacc += asum;
     }
 
     // Add kMasked to the rows of a shifted last tile whose vocabulary index is below
@@ -346,8 +349,8 @@ struct Kernel {
     // Fold the lane's 2 columns x 64 rows of both models, block by block.
     static __device__ __forceinline__ void fold(const floatx16 (&accS)[4][2],
                                                 const floatx16 (&accT)[4][2], Run (&RS)[2],
-                                                Run (&RT)[2], float (&A)[2], const ScoreArgs &a,
-                                                int vbase) {
+                                                Run (&RT)[2], float (&A)[2], float (&Bq)[2],
+                                                const ScoreArgs &a, int vbase) {
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -360,8 +363,9 @@ struct Kernel {
                     zs[r] = agpr_read(accS[vb][cb][r]);
                     if (HAS_T) zt[r] = agpr_read(accT[vb][cb][r]);
                 }
-                fold_block(zs, RS[cb], A[cb], false, zs, a.cS, a.sS, a.sT, vbase + vb * 32);
-                if (HAS_T) fold_block(zt, RT[cb], A[cb], true, zs, a.cT, a.sS, a.sT, vbase + vb * 32);
+                fold_block<HAS_T && REV>(zs, RS[cb], Bq[cb], zt, a.cS, a.sS, a.sT, vbase + vb * 32);
+                if (HAS_T)
+                    fold_block<true>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
             }
     }
 
@@ -441,7 +445,7 @@ struct Kernel {
             const int total = (vt1 - vt0) * spv;
 
             Run RS[2], RT[2];
-            float AA[2] = {0.f, 0.f};
+            float AA[2] = {0.f, 0.f}, BB[2] = {0.f, 0.f};
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 RS[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
@@ -511,7 +515,7 @@ struct Kernel {
                 OLIVE_STEPS(accS, nS)
                 if (HAS_T) OLIVE_STEPS(accT, nT)
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
-                fold(accS, accT, RS, RT, AA, a, vbase);
+                fold(accS, accT, RS, RT, AA, BB, a, vbase);
             }
 #undef OLIVE_STEPS
 
@@ -520,8 +524,8 @@ struct Kernel {
             for (int cb = 0; cb < 2; ++cb) {
                 Run o{__shfl_xor(RS[cb].best, 32), __shfl_xor(RS[cb].sec, 32),
                       __shfl_xor(RS[cb].z, 32), __shfl_xor(RS[cb].idx, 32)};
-                float dummy = 0.f;
-                merge_run(RS[cb], dummy, o, 0.f, a.cS);
+                const float ob = REV ? __shfl_xor(BB[cb], 32) : 0.f;
+                merge_run(RS[cb], BB[cb], o, ob, a.cS);
                 if (HAS_T) {
                     Run q2{__shfl_xor(RT[cb].best, 32), __shfl_xor(RT[cb].sec, 32),
                            __shfl_xor(RT[cb].z, 32), __shfl_xor(RT[cb].idx, 32)};
@@ -531,7 +535,7 @@ struct Kernel {
             }
             // Merge the two vocabulary halves (wv = 1 into wv = 0) through LDS, once
             // the trailing prefetches into the stages have landed.
-            float *xs = (float *)g_ring;   // [wt][cb][l32][9]
+            float *xs = (float *)g_ring;   // [wt][cb][l32][10]
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
             compiler_fence();
             __builtin_amdgcn_s_barrier();
@@ -539,11 +543,11 @@ struct Kernel {
             if (L.wv == 1 && L.h == 0) {
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb) {
-                    float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 9;
+                    float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 10;
                     o[0] = RS[cb].best; o[1] = RS[cb].sec; o[2] = __int_as_float(RS[cb].idx);
                     o[3] = RS[cb].z;
                     o[4] = RT[cb].best; o[5] = RT[cb].sec; o[6] = __int_as_float(RT[cb].idx);
-                    o[7] = RT[cb].z; o[8] = AA[cb];
+                    o[7] = RT[cb].z; o[8] = AA[cb]; o[9] = BB[cb];
                 }
             }
             compiler_fence();
@@ -551,10 +555,9 @@ struct Kernel {
             if (L.wv == 0 && L.h == 0) {
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb) {
-                    const float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 9;
+                    const float *o = xs + ((L.wt * 2 + cb) * 32 + L.l32) * 10;
                     Run ys{o[0], o[1], o[3], __float_as_int(o[2])};
-                    float dummy = 0.f;
-                    merge_run(RS[cb], dummy, ys, 0.f, a.cS);
+                    merge_run(RS[cb], BB[cb], ys, REV ? o[9] : 0.f, a.cS);
                     if (HAS_T) {
                         Run yt{o[4], o[5], o[7], __float_as_int(o[6])};
                         merge_run(RT[cb], AA[cb], yt, o[8], a.cT);
@@ -573,6 +576,7 @@ struct Kernel {
                             P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT[cb].idx);
                             P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT[cb].z;
                             P[(F_A * MAX_SPLITS + s) * ps + j] = AA[cb];
+                            if (REV) P[(F_B * MAX_SPLITS + s) * ps + j] = BB[cb];
                         }
                     }
                 }
@@ -583,20 +587,25 @@ struct Kernel {
     }
 };
 
-template <bool HAS_T, bool SAME>
+template <bool HAS_T, bool SAME, bool REV>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_mfma_kernel(ScoreArgs a) {
-    Kernel<HAS_T, SAME>::run(a);
+    Kernel<HAS_T, SAME, REV>::run(a);
 }
 
-hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, int grid,
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev, int grid,
                              hipStream_t st) {
     if (grid <= 0) return hipSuccess;
     if (has_t) {
-        if (same_scale) score_mfma_kernel<true, true><<<grid, 256, 0, st>>>(a);
-        else score_mfma_kernel<true, false><<<grid, 256, 0, st>>>(a);
+        if (same_scale) {
+            if (rev) score_mfma_kernel<true, true, true><<<grid, 256, 0, st>>>(a);
+            else score_mfma_kernel<true, true, false><<<grid, 256, 0, st>>>(a);
+        } else {
+            if (rev) score_mfma_kernel<true, false, true><<<grid, 256, 0, st>>>(a);
+            else score_mfma_kernel<true, false, false><<<grid, 256, 0, st>>>(a);
+        }
     } else {
-        score_mfma_kernel<false, true><<<grid, 256, 0, st>>>(a);
+        score_mfma_kernel<false, true, false><<<grid, 256, 0, st>>>(a);
     }
     return hipGetLastError();
 }

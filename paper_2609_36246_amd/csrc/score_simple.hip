@@ -6,7 +6,8 @@
 // it forms the logits of both models in registers (one vocabulary entry per
 // thread), stages them through LDS, and folds them into per-lane running
 // statistics (max, second max, lowest argmax, rescaled exp-sums and the teacher-
-// weighted difference), merged across lanes at the end of the split.
+// and student-weighted logit differences of the two KL directions), merged across
+// lanes at the end of the split.
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -40,9 +41,14 @@ score_simple_kernel(ScoreArgs a, int same_scale) {
     const E *ws = (const E *)a.ws;
     const E *wt = (const E *)a.wt;
     Stat st_s[4], st_t[4];
-    float acc_a[4];
+    float acc_a[4], acc_b[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) { st_s[i] = stat_identity(); st_t[i] = stat_identity(); acc_a[i] = 0.f; }
+    for (int i = 0; i < 4; ++i) {
+        st_s[i] = stat_identity();
+        st_t[i] = stat_identity();
+        acc_a[i] = 0.f;
+        acc_b[i] = 0.f;
+    }
 
     for (int c = c0; c < c1; ++c) {
         const int64_t v = (int64_t)c * SIMPLE_VC + tid;
@@ -84,20 +90,23 @@ score_simple_kernel(ScoreArgs a, int same_scale) {
                 const int64_t vg = (int64_t)c * SIMPLE_VC + vv;
                 if (vg >= a.V) break;
                 const float zs = zsh[0][r][vv];
+                const float zt = HAS_T ? zsh[1][r][vv] : 0.f;
+                float dlt = 0.f;
+                if (HAS_T) {
+#pragma clang fp contract(off)
+                    dlt = same_scale ? (zt - zs) : (a.sT * zt - a.sS * zs);
+                }
                 Stat &S = st_s[rr];
                 if (zs > S.best) {
                     float rs = fast_exp2((S.best - zs) * a.cS);
                     S.z = S.z * rs + 1.f; S.sec = S.best; S.best = zs; S.idx = (int32_t)vg;
+                    if (HAS_T) acc_b[rr] = acc_b[rr] * rs - dlt;
                 } else {
-                    S.z += fast_exp2((zs - S.best) * a.cS); S.sec = fmaxf(S.sec, zs);
+                    const float e = fast_exp2((zs - S.best) * a.cS);
+                    S.z += e; S.sec = fmaxf(S.sec, zs);
+                    if (HAS_T) acc_b[rr] = fmaf(-e, dlt, acc_b[rr]);
                 }
                 if (HAS_T) {
-                    const float zt = zsh[1][r][vv];
-                    float dlt;
-                    {
-#pragma clang fp contract(off)
-                        dlt = same_scale ? (zt - zs) : (a.sT * zt - a.sS * zs);
-                    }
                     Stat &Q = st_t[rr];
                     if (zt > Q.best) {
                         float rt = fast_exp2((Q.best - zt) * a.cT);
@@ -120,8 +129,8 @@ score_simple_kernel(ScoreArgs a, int same_scale) {
             o.sec = __shfl_xor(st_s[rr].sec, off);
             o.idx = __shfl_xor(st_s[rr].idx, off);
             o.z = __shfl_xor(st_s[rr].z, off);
-            float dummy = 0.f;
-            stat_merge(st_s[rr], dummy, o, 0.f, a.cS);
+            const float ob = __shfl_xor(acc_b[rr], off);
+            stat_merge(st_s[rr], acc_b[rr], o, ob, a.cS);
             if (HAS_T) {
                 Stat q;
                 q.best = __shfl_xor(st_t[rr].best, off);
@@ -146,6 +155,7 @@ score_simple_kernel(ScoreArgs a, int same_scale) {
                 P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(st_t[rr].idx);
                 P[(F_Z_T * MAX_SPLITS + s) * ps + j] = st_t[rr].z;
                 P[(F_A * MAX_SPLITS + s) * ps + j] = acc_a[rr];
+                P[(F_B * MAX_SPLITS + s) * ps + j] = acc_b[rr];
             }
         }
     }

@@ -1,8 +1,9 @@
 """Shared helpers of the GPU tests: run the HIP path through the C ABI and the fp64
 oracle on the same seeded workload, and compare them at the acceptance tolerances.
 
-Tolerances: per-token log-prob within 2e-3 absolute; per-position KL within
-1e-3 + 1e-3 |KL|; masked counts, valid counts and greedy argmax bit-exact; Eq. 1's
+Tolerances: per-token log-prob within 2e-3 absolute; per-position KL (either
+direction) within 1e-3 + 1e-3 |KL|; masked counts, valid counts and greedy argmax
+bit-exact; Eq. 1's
 per-sequence loss within 1e-3 relative (plus 1e-3 absolute for tiny sums).
 """
 import math
@@ -61,6 +62,7 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
         return torch.full((T,), -7, dtype=torch.int32, device=dev)
     out = {}
     out["kl"] = f32() if "kl" in outputs and not student_only else None
+    out["kl_rev"] = f32() if "kl_rev" in outputs and not student_only else None
     out["counts"] = torch.full((2,), -1, dtype=torch.int64, device=dev) \
         if "counts" in outputs else None
     out["logp_s"] = f32() if "logp_s" in outputs else None
@@ -72,7 +74,13 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
     batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
                          None if student_only else wl["h_teacher"], wl["valid_len"], region)
     for _ in range(repeat):
-        if student_only or out["kl"] is None:
+        if out["kl_rev"] is not None:
+            o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
+                               logp_student=out["logp_s"], logp_teacher=out["logp_t"],
+                               argmax_student=out["am_s"], argmax_teacher=out["am_t"],
+                               ce_per_seq=out["ce"])
+            L.olive_score_batch(ctx, batch, o)
+        elif student_only or out["kl"] is None:
             L.olive_token_logprobs(ctx, batch, out["logp_s"], out["logp_t"], out["am_s"],
                                    out["am_t"])
         else:
@@ -144,8 +152,10 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
     assert np.all(hip["logp_s"][inval] == 0.0), label
     if "am_s" in hip:
         assert np.all(hip["am_s"][inval] == -1), label
-    if not student_only and "kl" in hip:
-        assert np.all(hip["kl"][~inr] == 0.0) and not np.any(np.signbit(hip["kl"][~inr])), label
+    for key in ("kl", "kl_rev"):
+        if not student_only and key in hip:
+            assert np.all(hip[key][~inr] == 0.0) and not np.any(np.signbit(hip[key][~inr])), \
+                (label, key)
     sel = np.arange(T) if rows is None else np.asarray(rows)
     sel = sel[valid[sel]]
     r = oracle_rows(wl, sel, student_only)
@@ -173,6 +183,9 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
         if "kl" in hip:
             want = np.where(inr[sel], r["kl"], 0.0)
             chk("kl", hip["kl"][sel], want, KL_ATOL, KL_RTOL)
+        if "kl_rev" in hip:
+            want = np.where(inr[sel], r["kl_rev"], 0.0)
+            chk("kl_rev", hip["kl_rev"][sel], want, KL_ATOL, KL_RTOL)
         if check_ce and "ce" in hip and rows is None:
             B = len(cu) - 1
             for b in range(B):

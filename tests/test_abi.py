@@ -34,7 +34,7 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("olive_score_init", "olive_token_logprobs", "olive_kl_masked",
               "olive_score_free", "olive_status_string", "olive_score_last_error",
-              "olive_score_last_stats", "olive_score_kernel_times"):
+              "olive_score_last_stats", "olive_score_kernel_times", "olive_score_batch"):
         assert n in names
 
 
@@ -58,6 +58,9 @@ def test_struct_layouts_match_header():
     assert L.olive_score_desc.max_positions.offset == 32
     assert ctypes.sizeof(L.olive_batch) == 64
     assert L.olive_batch.h_teacher.offset == 56
+    assert ctypes.sizeof(L.olive_score_outputs) == 72
+    assert L.olive_score_outputs.kl.offset == 8
+    assert L.olive_score_outputs.ce_per_seq.offset == 64
 
 
 def _init(desc, ws=1, wt=1):
@@ -109,6 +112,8 @@ def test_calls_on_null_context(lib):
     assert lib.olive_score_last_stats(None, out) == L.OLIVE_E_NULL
     f = (ctypes.c_float * 4)()
     assert lib.olive_score_kernel_times(None, f, 1) == L.OLIVE_E_NULL
+    o = L.make_outputs()
+    assert lib.olive_score_batch(None, ctypes.byref(b), ctypes.byref(o), None) == L.OLIVE_E_NULL
 
 
 def test_binding_refuses_to_run_without_the_library(monkeypatch, tmp_path):

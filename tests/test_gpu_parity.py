@@ -102,6 +102,39 @@ def test_different_scales_general_difference_path():
         compare(hip, wl, label="scales-%s" % ("generic" if simple else "mfma"))
 
 
+ALL_OUT = ("kl", "kl_rev", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce")
+
+
+@pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
+@pytest.mark.parametrize("case", ["ragged_v1000", "multi_tile", "narrow_k", "v257"])
+def test_reverse_kl_full(case, simple):
+    say("reverse KL", case, "generic" if simple else "mfma")
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl, simple=simple, outputs=ALL_OUT)
+    assert hip["stats"]["kernel"] == ("generic" if simple else "mfma")
+    compare(hip, wl, label="rev-" + case)
+
+
+@pytest.mark.parametrize("region", [O.REGION_STUDENT, O.REGION_ALL])
+def test_reverse_kl_regions_and_scales(region):
+    say("reverse KL region", region)
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    wl["scale_student"], wl["scale_teacher"] = 2.0, 0.5
+    for simple in (False, True):
+        hip = run_hip(wl, region=region, simple=simple, outputs=ALL_OUT)
+        compare(hip, wl, region=region, label="rev-scales-%d" % region)
+
+
+def test_reverse_kl_on_long_rollout_sampled():
+    say("reverse KL, long_rollout sampled")
+    wl = W.make_workload("long_rollout", 0, device="cuda")
+    hip = run_hip(wl, outputs=ALL_OUT)
+    assert hip["stats"]["kernel"] == "mfma"
+    compare(hip, wl, rows=stratified_rows(wl, n_random=64), label="rev-long_rollout")
+    del wl
+    torch.cuda.empty_cache()
+
+
 def test_student_only_token_logprobs():
     say("student only")
     wl = custom("ragged_v1000", **CASES["ragged_v1000"])
@@ -150,8 +183,9 @@ def test_identical_teacher_gives_exact_zero_kl():
                                vocab=spec.vocab, d_student=spec.d_student,
                                d_teacher=spec.d_student, logit_scale=spec.logit_scale)
     for simple in (False, True):
-        hip = run_hip(wl, simple=simple, region=O.REGION_ALL)
+        hip = run_hip(wl, simple=simple, region=O.REGION_ALL, outputs=ALL_OUT)
         assert np.all(hip["kl"] == 0.0)
+        assert np.all(hip["kl_rev"] == 0.0)
         np.testing.assert_array_equal(hip["logp_s"], hip["logp_t"])
         np.testing.assert_array_equal(hip["am_s"], hip["am_t"])
 
