@@ -39,26 +39,36 @@ import numpy as np
 REGION_TEACHER = 0   # t >= cut: the teacher continuation (Eq. 1's scored tokens)
 REGION_STUDENT = 1   # t <  cut: the student prefix (OPD's scored tokens)
 REGION_ALL = 2       # every valid position
+REGION_SPANS = 3     # the given scored spans of each sequence (multi-turn: teacher actions)
 
 
 def _f64(a) -> np.ndarray:
     return np.asarray(a, dtype=np.float64)
 
 
-def masks(cu_seqlens, cut, valid_len=None, region: int = REGION_TEACHER) -> dict:
-    """Position masks and counts (Sec. 3.1, Eq. 1 and the sentence after it).
+def masks(cu_seqlens, cut, valid_len=None, region: int = REGION_TEACHER, spans=None) -> dict:
+    """Position masks and counts (Sec. 3.1, Eq. 1 and the sentence after it;
+    Sec. 3.2 for span masks).
 
     Sequence b occupies packed rows [cu[b], cu[b+1]); local index t = row - cu[b].
     valid(t) = t < valid_len[b] (valid_len defaults to the sequence length);
     in-region(t) = valid(t) and (t >= cut[b] | t < cut[b] | true) for the
-    teacher / student / all regions.
+    teacher / student / all regions. With `spans` (REGION_SPANS; one list of
+    (start, end) pairs per sequence, local and half-open) in-region(t) = valid(t)
+    and t lies in one of the sequence's spans: in the multi-turn form of the method
+    only the teacher's action tokens are scored, while the student's turns and every
+    environment observation stay in the context.
     """
     cu = np.asarray(cu_seqlens, dtype=np.int64)
-    cut = np.asarray(cut, dtype=np.int64)
     B = len(cu) - 1
     T = int(cu[-1])
     lengths = cu[1:] - cu[:-1]
     vl = lengths.copy() if valid_len is None else np.asarray(valid_len, dtype=np.int64)
+    if region == REGION_SPANS:
+        if spans is None or len(spans) != B:
+            raise ValueError("REGION_SPANS needs one span list per sequence")
+    else:
+        cut = np.asarray(cut, dtype=np.int64)
     seq_id = np.empty(T, dtype=np.int64)
     local_t = np.empty(T, dtype=np.int64)
     valid = np.zeros(T, dtype=bool)
@@ -76,6 +86,10 @@ def masks(cu_seqlens, cut, valid_len=None, region: int = REGION_TEACHER) -> dict
             r = t < cut[b]
         elif region == REGION_ALL:
             r = np.ones_like(v)
+        elif region == REGION_SPANS:
+            r = np.zeros_like(v)
+            for (a, e) in spans[b]:
+                r |= (t >= a) & (t < e)
         else:
             raise ValueError("unknown region %r" % (region,))
         inreg[rows] = v & r
@@ -200,7 +214,7 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
 def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
           h_teacher=None, w_teacher=None, scale_student: float = 1.0,
           scale_teacher: float = 1.0, region: int = REGION_TEACHER,
-          rows=None) -> dict:
+          rows=None, spans=None) -> dict:
     """The whole scoring of a packed batch, masked.
 
     Outputs per packed position (length T): logp_s, logp_t, argmax_s, argmax_t,
@@ -213,7 +227,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
     rows: optional subset of packed rows to evaluate (the others are left at the
     masked values and reported in `evaluated`); masks and counts are always full.
     """
-    m = masks(cu_seqlens, cut, valid_len, region)
+    m = masks(cu_seqlens, cut, valid_len, region, spans)
     T = m["valid"].shape[0]
     B = len(np.asarray(cu_seqlens)) - 1
     has_t = h_teacher is not None

@@ -54,6 +54,11 @@ class WorkloadSpec:
     eos: bool                       # draw a valid length past the cut
     outlier_frac: float             # fraction of rows scaled by outlier_mul
     outlier_mul: float
+    # Multi-turn structure (Sec. 3.2), or None: (prompt_lo, prompt_hi, student_turns,
+    # teacher_turns, action_lo, action_hi, obs_lo, obs_hi). Each turn is an action
+    # followed by an environment observation; lengths are drawn per turn, the cut is
+    # the first teacher turn and the scored spans are the teacher's actions.
+    turns: Optional[tuple] = None
 
 
 # The five workloads the scoring path is measured and checked on.
@@ -68,12 +73,17 @@ WORKLOADS = {
                                  4.0, "student", ("abs", 256, 4096 - 256), True, 0.0, 1.0),
     "ragged": WorkloadSpec("ragged", 64, None, (128, 8192), 151936, 2048, 5120, "bf16", 1.0,
                            "teacher", ("frac", 0.1, 0.9), False, 0.0, 1.0),
+    # Agentic rollouts (Sec. 3.2, Sec. 4.2): 10 student turns then 5 teacher turns;
+    # only the teacher's action tokens are scored.
+    "multi_turn": WorkloadSpec("multi_turn", 8, None, None, 151936, 2048, 5120, "bf16", 1.0,
+                               "teacher", ("abs", 0, 0), False, 0.0, 1.0,
+                               turns=(128, 512, 10, 5, 32, 192, 32, 384)),
 }
-WORKLOAD_ORDER = ["tiny", "small", "large_vocab", "long_rollout", "ragged"]
+WORKLOAD_ORDER = ["tiny", "small", "large_vocab", "long_rollout", "ragged", "multi_turn"]
 
 # Fixed order of the per-tensor random streams spawned from the seed.
 _STREAMS = ["h_student", "h_teacher", "w_student", "w_teacher", "lengths", "cuts",
-            "eos", "outliers", "targets"]
+            "eos", "outliers", "targets", "turns"]
 
 
 def _streams(seed: int):
@@ -94,6 +104,8 @@ def draw_structure(spec: WorkloadSpec, seed: int = 0):
     """
     st = _streams(seed)
     B = spec.num_seqs
+    if spec.turns is not None:
+        return _draw_turns(spec, st)
     if spec.seq_len is not None:
         lengths = np.full(B, spec.seq_len, dtype=np.int64)
     else:
@@ -128,6 +140,45 @@ def draw_structure(spec: WorkloadSpec, seed: int = 0):
         valid_len=None if valid is None else valid.astype(np.int32),
         outlier_rows=outliers.astype(np.int64),
         total_positions=T,
+    )
+
+
+def _draw_turns(spec: WorkloadSpec, st: dict) -> dict:
+    """Multi-turn structure: prompt, student turns, teacher turns (action + observation
+    each); cut = start of the first teacher turn; spans = the teacher's actions."""
+    p_lo, p_hi, k, m, a_lo, a_hi, o_lo, o_hi = spec.turns
+    rng = np.random.default_rng(st["turns"])
+    B = spec.num_seqs
+    lengths = np.zeros(B, dtype=np.int64)
+    cuts = np.zeros(B, dtype=np.int64)
+    spans = []
+    for b in range(B):
+        t = int(rng.integers(p_lo, p_hi + 1))
+        seq_spans = []
+        for turn in range(k + m):
+            if turn == k:
+                cuts[b] = t
+            a = int(rng.integers(a_lo, a_hi + 1))
+            o = int(rng.integers(o_lo, o_hi + 1))
+            if turn >= k:
+                seq_spans.append((t, t + a))
+            t += a + o
+        lengths[b] = t
+        spans.append(seq_spans)
+    cu = np.zeros(B + 1, dtype=np.int64)
+    np.cumsum(lengths, out=cu[1:])
+    off = np.zeros(B + 1, dtype=np.int64)
+    np.cumsum([len(x) for x in spans], out=off[1:])
+    flat = np.array([list(x) for sp in spans for x in sp], dtype=np.int32).reshape(-1, 2)
+    return dict(
+        cu_seqlens=cu.astype(np.int32),
+        cut=cuts.astype(np.int32),
+        valid_len=None,
+        outlier_rows=np.zeros(0, dtype=np.int64),
+        total_positions=int(cu[-1]),
+        spans=spans,
+        span_offsets=off.astype(np.int32),
+        span_pairs=flat,
     )
 
 
@@ -236,16 +287,19 @@ def make_workload(name: str, seed: int = 0, device="cpu", spec: Optional[Workloa
         scale_student=spec.logit_scale,
         scale_teacher=spec.logit_scale,
         structure=s,
+        spans=s.get("spans"),
+        span_offsets=t32(s.get("span_offsets")),
+        span_pairs=t32(s.get("span_pairs")),
     )
 
 
 def custom_spec(num_seqs=2, seq_len=32, vocab=1000, d_student=64, d_teacher=96, dtype="bf16",
                 logit_scale=1.0, target_source="uniform", cut_rule=("abs", 1, 31), eos=False,
-                ragged_len=None, outlier_frac=0.0, outlier_mul=1.0, name="custom"):
+                ragged_len=None, outlier_frac=0.0, outlier_mul=1.0, name="custom", turns=None):
     """A workload spec of arbitrary size, for tests (same recipe as the named ones)."""
-    return WorkloadSpec(name, num_seqs, None if ragged_len else seq_len, ragged_len, vocab,
-                        d_student, d_teacher, dtype, logit_scale, target_source, cut_rule, eos,
-                        outlier_frac, outlier_mul)
+    return WorkloadSpec(name, num_seqs, None if (ragged_len or turns) else seq_len, ragged_len,
+                        vocab, d_student, d_teacher, dtype, logit_scale, target_source, cut_rule,
+                        eos, outlier_frac, outlier_mul, turns)
 
 
 def tensor_digest(t: torch.Tensor) -> str:

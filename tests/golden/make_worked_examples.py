@@ -76,8 +76,26 @@ cases.append(dict(
     derivation="Bernoulli: p(1) = sigmoid(z1 - z0); KL = p ln(p/q) + (1-p) ln((1-p)/(1-q)); "
                "the reverse exchanges p and q"))
 
+# 4. Multi-turn (Sec. 3.2): prompt [0,3), student action/observation turns [3,5)/[5,7)
+#    and [7,9)/[9,11), teacher turns [11,14)/[14,15) and [15,18)/[18,19); only the
+#    teacher actions are scored. EOS after local t = 16 (valid length 17) drops the
+#    last action's final token: 3 + 2 = 5 scored positions, each with logp = -ln 4
+#    under uniform logits over V = 4, so Eq. 1's loss is 5 ln 4.
+cases.append(dict(
+    name="multi_turn_teacher_actions",
+    d_student=1, d_teacher=1, vocab=4,
+    h_student=[[1.0]] * 19, w_student=[[0.5] * 4],
+    h_teacher=[[1.0]] * 19, w_teacher=[[0.5] * 4],
+    targets=[t % 4 for t in range(19)], cu_seqlens=[0, 19], cut=[11], valid_len=[17],
+    region="spans", spans=[[[11, 14], [15, 18]]],
+    expect=dict(
+        logp_s=[-math.log(4.0)] * 17 + [0.0, 0.0], kl=[0.0] * 19,
+        argmax_s=[0] * 17 + [-1, -1], n_scored=5, t_valid=17, ce=[5.0 * math.log(4.0)]),
+    derivation="scored = teacher action tokens inside the valid length: {11,12,13,15,16}"))
+
 out = dict(
-    source="closed forms of the scoring definitions (Sec. 3.1 Eq. 1; Sec. 6 KL; Sec. 1 reverse KL); "
+    source="closed forms of the scoring definitions (Sec. 3.1 Eq. 1; Sec. 3.2 multi-turn masks; "
+           "Sec. 6 KL; Sec. 1 reverse KL); "
            "the paper prints no numeric worked example",
     cases=cases)
 path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "worked_examples.json")

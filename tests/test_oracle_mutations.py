@@ -62,12 +62,19 @@ def klr_dropped_cross_term(z_s, lse_s, z_t, lse_t):
     return a - ent, b - ent
 
 
-def masks_off_by_one(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER):
-    return _orig_masks(cu_seqlens, np.asarray(cut) + 1, valid_len, region)
+def masks_off_by_one(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER, spans=None):
+    return _orig_masks(cu_seqlens, np.asarray(cut) + 1, valid_len, region, spans)
 
 
-def masks_ignore_valid(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER):
-    return _orig_masks(cu_seqlens, cut, None, region)
+def masks_ignore_valid(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER, spans=None):
+    return _orig_masks(cu_seqlens, cut, None, region, spans)
+
+
+def masks_span_end_inclusive(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER,
+                             spans=None):
+    if spans is not None:
+        spans = [[(a, e + 1) for (a, e) in sp] for sp in spans]
+    return _orig_masks(cu_seqlens, cut, valid_len, region, spans)
 
 
 def project_no_scale(h_rows, w, scale=1.0):
@@ -91,6 +98,7 @@ MUTANTS = [
     ("kl_student_teacher", klr_dropped_cross_term),
     ("masks", masks_off_by_one),
     ("masks", masks_ignore_valid),
+    ("masks", masks_span_end_inclusive),
     ("project", project_no_scale),
     ("project", project_dropped_last_k),
 ]
@@ -108,6 +116,7 @@ PINS = [
     P.test_argmax_exact_ties_take_lowest_index,
     P.test_mask_counts_enumerated,
     P.test_eq1_masks_prefix_and_scores_continuation,
+    P.test_span_masks_reduce_to_the_cut_regions_and_add_up,
     P.test_masked_outputs_exact_values,
 ]
 

@@ -82,16 +82,20 @@ def test_golden_worked_examples():
     with open(os.path.join(GOLDEN, "worked_examples.json")) as f:
         data = json.load(f)
     for c in data["cases"]:
+        region = O.REGION_SPANS if c.get("region") == "spans" else O.REGION_TEACHER
+        spans = [[tuple(x) for x in sp] for sp in c["spans"]] if "spans" in c else None
         out = O.score(np.array(c["h_student"]), np.array(c["w_student"]), np.array(c["targets"]),
                       np.array(c["cu_seqlens"]), np.array(c["cut"]),
                       None if c["valid_len"] is None else np.array(c["valid_len"]),
-                      np.array(c["h_teacher"]), np.array(c["w_teacher"]))
+                      np.array(c["h_teacher"]), np.array(c["w_teacher"]), region=region,
+                      spans=spans)
         e = c["expect"]
         for k in ("logp_s", "logp_t", "kl", "kl_rev", "ce", "lse_s", "lse_t"):
             if k in e:
                 np.testing.assert_allclose(out[k], e[k], rtol=0, atol=1e-14, err_msg=c["name"] + k)
         for k in ("argmax_s", "argmax_t"):
-            np.testing.assert_array_equal(out[k], e[k], err_msg=c["name"] + k)
+            if k in e:
+                np.testing.assert_array_equal(out[k], e[k], err_msg=c["name"] + k)
         assert out["n_scored"] == e["n_scored"] and out["t_valid"] == e["t_valid"]
 
 
@@ -273,6 +277,31 @@ def test_mask_counts_enumerated():
                 # the scored teacher positions are exactly local t in [cut, vl)
                 np.testing.assert_array_equal(np.nonzero(mt["in_region"])[0],
                                               np.arange(cut, max(cut, vl)))
+
+
+def test_span_masks_reduce_to_the_cut_regions_and_add_up():
+    """Span masks (Sec. 3.2): a single span [cut, len) is the teacher region, [0, cut)
+    the student region, [0, len) every valid position, no span scores nothing; the
+    count of two disjoint span sets is the sum of their counts."""
+    for L in range(0, 9):
+        for c in range(0, L + 1):
+            for vl in range(0, L + 1):
+                cu, cut, v = [0, L], [c], [vl]
+                for spans, region in (([(c, L)], O.REGION_TEACHER), ([(0, c)], O.REGION_STUDENT),
+                                      ([(0, L)], O.REGION_ALL)):
+                    a = O.masks(cu, cut, v, O.REGION_SPANS, [spans])
+                    b = O.masks(cu, cut, v, region)
+                    np.testing.assert_array_equal(a["in_region"], b["in_region"])
+                    assert a["n_scored"] == b["n_scored"]
+                e = O.masks(cu, cut, v, O.REGION_SPANS, [[]])
+                assert e["n_scored"] == 0 and e["t_valid"] == vl
+                # disjoint split of [0, L) at every point
+                for x in range(0, L + 1):
+                    s1 = O.masks(cu, cut, v, O.REGION_SPANS, [[(0, x)]])["n_scored"]
+                    s2 = O.masks(cu, cut, v, O.REGION_SPANS, [[(x, L)]])["n_scored"]
+                    assert s1 + s2 == min(L, vl)
+                    both = O.masks(cu, cut, v, O.REGION_SPANS, [[(0, x), (x, L)]])["n_scored"]
+                    assert both == s1 + s2
 
 
 def test_eq1_masks_prefix_and_scores_continuation():

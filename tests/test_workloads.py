@@ -21,7 +21,9 @@ def test_structure_ranges_all_workloads():
         lengths = np.diff(cu)
         assert cu[0] == 0 and np.all(lengths >= 0) and len(cut) == spec.num_seqs
         kind, lo, hi = spec.cut_rule
-        if kind == "abs":
+        if spec.turns is not None:
+            check_turns(spec, s)
+        elif kind == "abs":
             assert np.all(cut >= lo) and np.all(cut <= hi)
             assert np.all(lengths == spec.seq_len)
         else:
@@ -36,6 +38,27 @@ def test_structure_ranges_all_workloads():
         # same seed, same structure
         s2 = W.draw_structure(spec, 0)
         np.testing.assert_array_equal(s2["cut"], cut)
+
+
+def check_turns(spec, s):
+    """Multi-turn structure: the cut is the first teacher turn, one span per teacher
+    action, spans inside the sequence, increasing and disjoint, lengths within the
+    per-turn ranges."""
+    p_lo, p_hi, k, m, a_lo, a_hi, o_lo, o_hi = spec.turns
+    lengths = np.diff(s["cu_seqlens"].astype(np.int64))
+    off = s["span_offsets"]
+    assert off[0] == 0 and off[-1] == len(s["span_pairs"])
+    for b, sp in enumerate(s["spans"]):
+        assert len(sp) == m and off[b + 1] - off[b] == m
+        np.testing.assert_array_equal(s["span_pairs"][off[b]:off[b + 1]], np.array(sp))
+        assert sp[0][0] == s["cut"][b]
+        assert p_lo + k * (a_lo + o_lo) <= s["cut"][b] <= p_hi + k * (a_hi + o_hi)
+        prev = 0
+        for (a, e) in sp:
+            assert prev <= a and a_lo <= e - a <= a_hi
+            prev = e + o_lo
+        assert prev - o_lo + o_lo <= lengths[b] <= sp[-1][1] + o_hi
+    assert s["valid_len"] is None
 
 
 def test_ragged_total_positions_near_expectation():
