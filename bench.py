@@ -130,11 +130,16 @@ def main():
     outs = L.make_outputs(kl=kl, kl_reverse=klr, counts=counts, logp_student=lps,
                           logp_teacher=lpt, argmax_student=ams, argmax_teacher=amt,
                           ce_per_seq=ce)
-    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
-                         wl["h_teacher"], wl["valid_len"], L.OLIVE_REGION_TEACHER)
+    use_spans = wl.get("spans") is not None       # multi-turn: teacher actions scored
+    batch = L.make_batch(wl["cu_seqlens"], None if use_spans else wl["cut"], wl["targets"],
+                         wl["h_student"], wl["h_teacher"], wl["valid_len"],
+                         L.OLIVE_REGION_SPANS if use_spans else L.OLIVE_REGION_TEACHER)
+    spans = L.make_spans(wl["span_offsets"], wl["span_pairs"]) if use_spans else None
 
     def step():
-        if args.reverse_kl:
+        if use_spans:
+            L.olive_score_batch_spans(ctx, batch, spans, outs, stream)
+        elif args.reverse_kl:
             L.olive_score_batch(ctx, batch, outs, stream)
         else:
             L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
@@ -181,6 +186,7 @@ def main():
             "d_student": spec.d_student, "d_teacher": spec.d_teacher,
             "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
             "reverse_kl": bool(args.reverse_kl),
+            "region": "spans" if use_spans else "teacher",
             "near_tie_rows": stats["flagged"], "grid": stats["grid"],
             "step_tflops": flops / (ms_step * 1e-3) / 1e12,
             "pct_bf16_peak_step": 100.0 * flops / (ms_step * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,

@@ -65,7 +65,9 @@ typedef enum {
 typedef enum {
     OLIVE_REGION_TEACHER = 0, /* local t >= cut: the teacher continuation, Eq. 1's scored tokens */
     OLIVE_REGION_STUDENT = 1, /* local t <  cut: the student prefix (OPD scores these, Sec. 1) */
-    OLIVE_REGION_ALL = 2      /* every valid position */
+    OLIVE_REGION_ALL = 2,     /* every valid position */
+    OLIVE_REGION_SPANS = 3    /* the scored spans given to olive_score_batch_spans: the
+                                 teacher's actions of a multi-turn rollout (Sec. 3.2) */
 } olive_region;
 
 /* Fixed at init. */
@@ -175,6 +177,21 @@ typedef struct {
 } olive_score_outputs;
 
 /*
+ * Scored spans of a multi-turn batch (Sec. 3.2): the student's turns and every
+ * environment observation stay in the context, only the teacher's actions are
+ * scored. Spans are local, half-open [start, end), per sequence increasing and
+ * disjoint, 0 <= start <= end <= len_b; a position is scored when it lies in one
+ * of its sequence's spans and before the sequence's valid length.
+ */
+typedef struct {
+    int32_t size;                /* host: sizeof(olive_spans) (checked) */
+    int32_t num_spans;           /* S >= 0: spans over the whole batch */
+    const int32_t *span_offsets; /* device [B+1]: sequence b's spans are entries
+                                    [off[b], off[b+1]); off[0] = 0, nondecreasing, off[B] = S */
+    const int32_t *spans;        /* device [S][2]: (start, end) pairs; may be NULL when S = 0 */
+} olive_spans;
+
+/*
  * Every per-position output of one batch in one fused pass over the vocabulary:
  * olive_kl_masked's outputs plus the reverse KL. Teacher outputs (kl, kl_reverse,
  * logp_teacher, argmax_teacher) need a teacher context and b->h_teacher.
@@ -183,6 +200,19 @@ typedef struct {
  */
 olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
                                const olive_score_outputs *out, void *hip_stream);
+
+/*
+ * olive_score_batch with a span region: b->region must be OLIVE_REGION_SPANS and
+ * b->cut may be NULL (it is not read). kl, kl_reverse and ce_per_seq are taken over
+ * the spans; log-probs and greedy tokens at every valid position as usual.
+ * Errors: as olive_score_batch, plus E_NULL (spans, or its arrays while S > 0),
+ * E_RANGE (spans->size wrong, S < 0, or b->region not OLIVE_REGION_SPANS). Malformed
+ * offsets or spans found on the device set bit 16 of the device error word and make
+ * the affected sequences' outputs NaN (all of them for bad offsets).
+ */
+olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
+                                     const olive_spans *spans, const olive_score_outputs *out,
+                                     void *hip_stream);
 
 /* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
 olive_status olive_score_free(olive_score_ctx *ctx);
@@ -194,7 +224,8 @@ const char *olive_status_string(olive_status s);
  * Read and clear the context's device error word (synchronises the device).
  *   device_code host: receives a bit set, 0 when no content error occurred:
  *   1 = target out of [0, V), 2 = cut out of [0, len], 4 = valid_len out of [0, len],
- *   8 = cu_seqlens not nondecreasing from 0 or cu[B] != T.
+ *   8 = cu_seqlens not nondecreasing from 0 or cu[B] != T, 16 = span offsets or spans
+ *   malformed (olive_score_batch_spans).
  */
 olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
 

@@ -32,6 +32,7 @@ OLIVE_W_VD = 1
 OLIVE_REGION_TEACHER = 0
 OLIVE_REGION_STUDENT = 1
 OLIVE_REGION_ALL = 2
+OLIVE_REGION_SPANS = 3
 OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
 
@@ -58,6 +59,11 @@ class olive_score_outputs(ctypes.Structure):
                 ("counts", ctypes.c_void_p), ("logp_student", ctypes.c_void_p),
                 ("logp_teacher", ctypes.c_void_p), ("argmax_student", ctypes.c_void_p),
                 ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p)]
+
+
+class olive_spans(ctypes.Structure):
+    _fields_ = [("size", ctypes.c_int32), ("num_spans", ctypes.c_int32),
+                ("span_offsets", ctypes.c_void_p), ("spans", ctypes.c_void_p)]
 
 
 class OliveError(RuntimeError):
@@ -92,6 +98,10 @@ def load() -> ctypes.CDLL:
     lib.olive_score_batch.argtypes = [vp, ctypes.POINTER(olive_batch),
                                       ctypes.POINTER(olive_score_outputs), vp]
     lib.olive_score_batch.restype = st
+    lib.olive_score_batch_spans.argtypes = [vp, ctypes.POINTER(olive_batch),
+                                            ctypes.POINTER(olive_spans),
+                                            ctypes.POINTER(olive_score_outputs), vp]
+    lib.olive_score_batch_spans.restype = st
     lib.olive_score_free.argtypes = [vp]
     lib.olive_score_free.restype = st
     lib.olive_status_string.argtypes = [st]
@@ -203,6 +213,25 @@ def olive_score_batch(ctx, batch: olive_batch, outputs: olive_score_outputs, str
                                  _stream(stream))
     if check:
         _check(s, "olive_score_batch")
+    return s
+
+
+def make_spans(span_offsets, span_pairs, num_spans: Optional[int] = None) -> olive_spans:
+    """An olive_spans over device tensors: offsets [B+1] int32, pairs [S, 2] int32."""
+    sp = olive_spans()
+    sp.size = ctypes.sizeof(olive_spans)
+    sp.num_spans = int(num_spans if num_spans is not None else span_pairs.shape[0])
+    sp.span_offsets = _ptr(span_offsets)
+    sp.spans = _ptr(span_pairs) if sp.num_spans > 0 else None
+    return sp
+
+
+def olive_score_batch_spans(ctx, batch: olive_batch, spans: olive_spans,
+                            outputs: olive_score_outputs, stream=None, check: bool = True) -> int:
+    s = load().olive_score_batch_spans(ctx, ctypes.byref(batch), ctypes.byref(spans),
+                                       ctypes.byref(outputs), _stream(stream))
+    if check:
+        _check(s, "olive_score_batch_spans")
     return s
 
 

@@ -64,14 +64,22 @@ olive_status dev_alloc(T **p, size_t bytes) {
 olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP; }
 
 // The scoring of one batch, shared by every scoring entry point.
-olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, float *kl_rev,
-                 int64_t *counts, float *logp_s, float *logp_t, int32_t *am_s, int32_t *am_t,
-                 float *ce, hipStream_t st) {
+olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
+                 float *kl, float *kl_rev, int64_t *counts, float *logp_s, float *logp_t,
+                 int32_t *am_s, int32_t *am_t, float *ce, hipStream_t st) {
     const olive_score_desc &d = ctx->desc;
-    if (!b->cu_seqlens || !b->cut || !b->targets || !b->h_student) return OLIVE_E_NULL;
+    if (!b->cu_seqlens || !b->targets || !b->h_student) return OLIVE_E_NULL;
+    if (!spans && !b->cut) return OLIVE_E_NULL;
     if (b->num_seqs < 1 || b->num_seqs > d.max_seqs) return OLIVE_E_SHAPE;
     if (b->total_positions < 1 || b->total_positions > d.max_positions) return OLIVE_E_SHAPE;
-    if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) return OLIVE_E_RANGE;
+    if (spans) {
+        if (b->region != OLIVE_REGION_SPANS) return OLIVE_E_RANGE;
+        if (spans->size != (int32_t)sizeof(olive_spans) || spans->num_spans < 0)
+            return OLIVE_E_RANGE;
+        if (!spans->span_offsets || (spans->num_spans > 0 && !spans->spans)) return OLIVE_E_NULL;
+    } else if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) {
+        return OLIVE_E_RANGE;
+    }
     const bool want_t = kl || kl_rev || logp_t || am_t;
     if (want_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
     const bool has_t = want_t;
@@ -97,11 +105,12 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, float *k
         fixed_splits = (int)(want < 1 ? 1 : (want > lim ? lim : want));
         max_units = pt * fixed_splits;
     }
-    s = check_hip(launch_prep(*b, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
+    s = check_hip(launch_prep(*b, spans, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
                               mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
                               fixed_splits, st));
     if (s) return s;
-    s = check_hip(launch_rowmap(*b, V, ctx->seqbuf, ctx->sched, ctx->rowmap, ctx->err, logp_s,
+    s = check_hip(launch_rowmap(*b, spans, V, ctx->seqbuf, ctx->sched, ctx->rowmap, ctx->err,
+                                logp_s,
                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
                                 has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, st));
     if (s) return s;
@@ -149,8 +158,8 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, float *kl, float *k
         if (s) return s;
     }
     if (ce) {
-        s = check_hip(launch_ce(*b, ctx->seqbuf, ctx->sched, logp_s ? logp_s : ctx->logp_tmp,
-                                ce, st));
+        s = check_hip(launch_ce(*b, spans, ctx->seqbuf, ctx->sched,
+                                logp_s ? logp_s : ctx->logp_tmp, ce, st));
         if (s) return s;
     }
     return OLIVE_OK;
@@ -268,8 +277,8 @@ olive_status olive_token_logprobs(olive_score_ctx *ctx, const olive_batch *b, fl
                                   float *logp_teacher, int32_t *argmax_student,
                                   int32_t *argmax_teacher, void *hip_stream) {
     if (!ctx || !b || !logp_student) return OLIVE_E_NULL;
-    return run(ctx, b, nullptr, nullptr, nullptr, logp_student, logp_teacher, argmax_student,
-               argmax_teacher, nullptr, (hipStream_t)hip_stream);
+    return run(ctx, b, nullptr, nullptr, nullptr, nullptr, logp_student, logp_teacher,
+               argmax_student, argmax_teacher, nullptr, (hipStream_t)hip_stream);
 }
 
 olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *kl,
@@ -278,18 +287,34 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
                              void *hip_stream) {
     if (!ctx || !b || !kl) return OLIVE_E_NULL;
     if (!ctx->has_t) return OLIVE_E_UNSUPPORTED;
-    return run(ctx, b, kl, nullptr, counts, logp_student, logp_teacher, argmax_student,
+    return run(ctx, b, nullptr, kl, nullptr, counts, logp_student, logp_teacher, argmax_student,
                argmax_teacher, ce_per_seq, (hipStream_t)hip_stream);
 }
 
-olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
-                               const olive_score_outputs *out, void *hip_stream) {
-    if (!ctx || !b || !out) return OLIVE_E_NULL;
+static olive_status check_outputs(const olive_score_outputs *out) {
+    if (!out) return OLIVE_E_NULL;
     if (out->size != (int32_t)sizeof(olive_score_outputs)) return OLIVE_E_RANGE;
     if (!out->kl && !out->kl_reverse && !out->counts && !out->logp_student &&
         !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq)
         return OLIVE_E_NULL;
-    return run(ctx, b, out->kl, out->kl_reverse, out->counts, out->logp_student,
+    return OLIVE_OK;
+}
+
+olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
+                               const olive_score_outputs *out, void *hip_stream) {
+    if (!ctx || !b) return OLIVE_E_NULL;
+    if (olive_status e = check_outputs(out)) return e;
+    return run(ctx, b, nullptr, out->kl, out->kl_reverse, out->counts, out->logp_student,
+               out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
+               (hipStream_t)hip_stream);
+}
+
+olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
+                                     const olive_spans *spans, const olive_score_outputs *out,
+                                     void *hip_stream) {
+    if (!ctx || !b || !spans) return OLIVE_E_NULL;
+    if (olive_status e = check_outputs(out)) return e;
+    return run(ctx, b, spans, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
                (hipStream_t)hip_stream);
 }

@@ -42,6 +42,7 @@ enum {
     ERR_CUT = 2,
     ERR_VALID = 4,
     ERR_CU = 8,
+    ERR_SPAN = 16,
 };
 
 constexpr int MFMA_BV = 256;     // vocabulary rows per tile (MFMA M)
@@ -66,10 +67,11 @@ struct ScoreArgs {
 // Host-side launchers (each defined beside its kernel).
 hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int elem_bytes,
                          hipStream_t st);
-hipError_t launch_prep(const olive_batch &b, int64_t V, int32_t *seqbuf, Sched *sched,
-                       int32_t *err, int64_t *counts, int tile_rows, int policy,
+hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, int64_t V, int32_t *seqbuf,
+                       Sched *sched, int32_t *err, int64_t *counts, int tile_rows, int policy,
                        int n_vtiles, int grid, int fixed_splits, hipStream_t st);
-hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
+hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, int64_t V,
+                         const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
                          float *logp_tmp, hipStream_t st);
@@ -88,8 +90,8 @@ hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *o
                             hipStream_t st);
 int fixup_chunks(int64_t V);
 size_t fixup_result_bytes();
-hipError_t launch_ce(const olive_batch &b, const int32_t *seqbuf, const Sched *sched,
-                     const float *logp_s, float *ce, hipStream_t st);
+hipError_t launch_ce(const olive_batch &b, const olive_spans *spans, const int32_t *seqbuf,
+                     const Sched *sched, const float *logp_s, float *ce, hipStream_t st);
 
 // Layout of the per-sequence workspace (int32, 4 * (max_seqs + 1) entries).
 //   [0, B+1)          exclusive prefix sum of valid lengths (compacted row offsets)

@@ -3,7 +3,9 @@
 // Masks follow Sec. 3.1 (Eq. 1 and the sentence after it): each packed sequence
 // is a student prefix (local t < cut) followed by a teacher continuation (t >= cut);
 // positions at or past the sequence's valid length (an end-of-sequence) are not
-// scored at all. The teacher region is what Eq. 1 sums over.
+// scored at all. The teacher region is what Eq. 1 sums over. In the multi-turn form
+// (Sec. 3.2) the scored region is instead a list of spans per sequence (the
+// teacher's actions), the student's turns and the observations staying as context.
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -11,10 +13,28 @@
 
 namespace olive {
 
+// Scored spans of a batch in the span region (null otherwise).
+struct SpanArgs {
+    const int32_t *off;     // [B+1]: spans of sequence b are [off[b], off[b+1])
+    const int32_t *pairs;   // [S][2]: local [start, end)
+    int32_t n;              // S
+};
+
 __device__ __forceinline__ bool in_region(int region, int t, int cut) {
     return region == OLIVE_REGION_TEACHER ? (t >= cut)
            : region == OLIVE_REGION_STUDENT ? (t < cut)
                                              : true;
+}
+
+// t inside one of spans [i0, i1) (validated: increasing, disjoint): the last span
+// starting at or before t must end after it.
+__device__ __forceinline__ bool in_spans(const int32_t *pairs, int i0, int i1, int t) {
+    int lo = i0, hi = i1;   // first span with start > t
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (pairs[2 * mid] <= t) lo = mid + 1; else hi = mid;
+    }
+    return lo > i0 && t < pairs[2 * (lo - 1) + 1];
 }
 
 __device__ __forceinline__ int region_count(int region, int vl, int cut) {
@@ -31,15 +51,23 @@ constexpr int PREP_THREADS = 1024;
 __global__ void __launch_bounds__(PREP_THREADS)
 prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             const int32_t *__restrict__ vlen, int32_t B, int64_t T, int32_t region,
-            int32_t *__restrict__ seqbuf, Sched *__restrict__ sched, int32_t *__restrict__ err,
-            int64_t *__restrict__ counts, int32_t tile_rows, int32_t policy, int32_t n_vtiles,
-            int32_t grid, int32_t fixed_splits) {
-    __shared__ int s_bad;
+            SpanArgs sp, int32_t *__restrict__ seqbuf, Sched *__restrict__ sched,
+            int32_t *__restrict__ err, int64_t *__restrict__ counts, int32_t tile_rows,
+            int32_t policy, int32_t n_vtiles, int32_t grid, int32_t fixed_splits) {
+    __shared__ int s_bad, s_badoff;
     __shared__ int s_scan[PREP_THREADS];
     __shared__ long long s_red[PREP_THREADS];
     const int tid = threadIdx.x;
-    if (tid == 0) s_bad = 0;
+    const bool span_mode = region == OLIVE_REGION_SPANS;
+    if (tid == 0) { s_bad = 0; s_badoff = 0; }
     __syncthreads();
+    if (span_mode) {   // span offsets: 0 = off[0] <= off[1] <= ... <= off[B] = S
+        for (int b = tid; b <= B; b += PREP_THREADS) {
+            const int o = sp.off[b];
+            bool bad = (b == 0 && o != 0) || (b == B && o != sp.n) || (b > 0 && o < sp.off[b - 1]);
+            if (bad) atomicOr(&s_badoff, 1);
+        }
+    }
     for (int b = tid; b <= B; b += PREP_THREADS) {
         int c = cu[b];
         bool bad = (b == 0 && c != 0) || (b == B && (int64_t)c != T) || (b > 0 && c < cu[b - 1]);
@@ -71,18 +99,33 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
         long long sc = 0;
         if (b < B) {
             int len = cu[b + 1] - cu[b];
-            int c = cut[b];
+            int c = span_mode ? 0 : cut[b];
             int vl = vlen ? vlen[b] : len;
             int e = 0;
             if (c < 0 || c > len) e |= ERR_CUT;
             if (vl < 0 || vl > len) e |= ERR_VALID;
+            long long span_sc = 0;
+            if (span_mode) {
+                if (s_badoff) {
+                    e |= ERR_SPAN;
+                } else {
+                    int prev = 0;
+                    for (int i = sp.off[b]; i < sp.off[b + 1]; ++i) {
+                        const int a = sp.pairs[2 * i], z = sp.pairs[2 * i + 1];
+                        if (a < prev || a > z || z > len) { e |= ERR_SPAN; break; }
+                        prev = z;
+                        const int zz = z < vl ? z : vl;
+                        span_sc += zz > a ? zz - a : 0;
+                    }
+                }
+            }
             if (e) {
                 atomicOr(err, e);
                 vl_eff[b] = 0; cut_eff[b] = 0; badseq[b] = 1;
             } else {
                 vl_eff[b] = vl; cut_eff[b] = c; badseq[b] = 0;
                 v = vl;
-                sc = region_count(region, vl, c);
+                sc = span_mode ? span_sc : region_count(region, vl, c);
             }
         }
         s_scan[tid] = v;
@@ -139,7 +182,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
 // rows of malformed sequences (NaN, argmax -1).
 __global__ void __launch_bounds__(256)
 rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t region,
-              const int32_t *__restrict__ seqbuf, const Sched *__restrict__ sched,
+              SpanArgs sp, const int32_t *__restrict__ seqbuf, const Sched *__restrict__ sched,
               uint32_t *__restrict__ rowmap, float *__restrict__ logp_s,
               float *__restrict__ logp_t, int32_t *__restrict__ am_s, int32_t *__restrict__ am_t,
               float *__restrict__ kl, float *__restrict__ kl_rev,
@@ -175,7 +218,10 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             continue;
         }
         if (t < vl_eff[b]) {
-            uint32_t inr = in_region(region, t, cut_eff[b]) ? 1u : 0u;
+            const bool r = region == OLIVE_REGION_SPANS
+                               ? in_spans(sp.pairs, sp.off[b], sp.off[b + 1], t)
+                               : in_region(region, t, cut_eff[b]);
+            uint32_t inr = r ? 1u : 0u;
             rowmap[cvalid[b] + t] = (uint32_t)g | (inr << 31);
         } else {
             if (logp_s) logp_s[g] = 0.f;
@@ -192,7 +238,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
 // Eq. 1 per sequence: ce_b = - sum over the in-region valid positions of logp_S,
 // accumulated in fp64 in a fixed order (deterministic).
 __global__ void __launch_bounds__(256)
-ce_kernel(const int32_t *__restrict__ cu, int32_t B, int32_t region,
+ce_kernel(const int32_t *__restrict__ cu, int32_t B, int32_t region, SpanArgs sp,
           const int32_t *__restrict__ seqbuf, const Sched *__restrict__ sched,
           const float *__restrict__ logp_s, float *__restrict__ ce) {
     __shared__ double red[256];
@@ -206,12 +252,20 @@ ce_kernel(const int32_t *__restrict__ cu, int32_t B, int32_t region,
         return;
     }
     int vl = vl_eff[b], c = cut_eff[b];
-    int lo = 0, hi = vl;
-    if (region == OLIVE_REGION_TEACHER) lo = c < vl ? c : vl;
-    else if (region == OLIVE_REGION_STUDENT) hi = c < vl ? c : vl;
     const int64_t base = cu[b];
     double acc = 0.0;
-    for (int t = lo + threadIdx.x; t < hi; t += 256) acc -= (double)logp_s[base + t];
+    if (region == OLIVE_REGION_SPANS) {
+        for (int i = sp.off[b]; i < sp.off[b + 1]; ++i) {
+            const int lo = sp.pairs[2 * i];
+            const int hi = sp.pairs[2 * i + 1] < vl ? sp.pairs[2 * i + 1] : vl;
+            for (int t = lo + threadIdx.x; t < hi; t += 256) acc -= (double)logp_s[base + t];
+        }
+    } else {
+        int lo = 0, hi = vl;
+        if (region == OLIVE_REGION_TEACHER) lo = c < vl ? c : vl;
+        else if (region == OLIVE_REGION_STUDENT) hi = c < vl ? c : vl;
+        for (int t = lo + threadIdx.x; t < hi; t += 256) acc -= (double)logp_s[base + t];
+    }
     red[threadIdx.x] = acc;
     __syncthreads();
     for (int off = 128; off > 0; off >>= 1) {
@@ -250,18 +304,27 @@ hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int
     return hipGetLastError();
 }
 
-hipError_t launch_prep(const olive_batch &b, int64_t V, int32_t *seqbuf, Sched *sched,
-                       int32_t *err, int64_t *counts, int tile_rows, int policy, int n_vtiles,
-                       int grid, int fixed_splits, hipStream_t st) {
+static SpanArgs span_args(const olive_spans *s) {
+    SpanArgs a;
+    a.off = s ? s->span_offsets : nullptr;
+    a.pairs = s ? s->spans : nullptr;
+    a.n = s ? s->num_spans : 0;
+    return a;
+}
+
+hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, int64_t V, int32_t *seqbuf,
+                       Sched *sched, int32_t *err, int64_t *counts, int tile_rows, int policy,
+                       int n_vtiles, int grid, int fixed_splits, hipStream_t st) {
     (void)V;
     prep_kernel<<<1, PREP_THREADS, 0, st>>>(b.cu_seqlens, b.cut, b.valid_len, b.num_seqs,
-                                            b.total_positions, b.region, seqbuf, sched, err,
-                                            counts, tile_rows, policy, n_vtiles, grid,
+                                            b.total_positions, b.region, span_args(spans), seqbuf,
+                                            sched, err, counts, tile_rows, policy, n_vtiles, grid,
                                             fixed_splits);
     return hipGetLastError();
 }
 
-hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
+hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, int64_t V,
+                         const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
                          float *logp_tmp, hipStream_t st) {
@@ -271,15 +334,16 @@ hipError_t launch_rowmap(const olive_batch &b, int64_t V, const int32_t *seqbuf,
     if (blocks > 4096) blocks = 4096;
     if (blocks < 1) blocks = 1;
     rowmap_kernel<<<(unsigned)blocks, 256, 0, st>>>(b.cu_seqlens, b.num_seqs, T, b.region,
-                                                    seqbuf, sched, rowmap, logp_s, logp_t, am_s,
+                                                    span_args(spans), seqbuf, sched, rowmap,
+                                                    logp_s, logp_t, am_s,
                                                     am_t, kl, kl_rev, logp_tmp);
     return hipGetLastError();
 }
 
-hipError_t launch_ce(const olive_batch &b, const int32_t *seqbuf, const Sched *sched,
-                     const float *logp_s, float *ce, hipStream_t st) {
-    ce_kernel<<<(unsigned)b.num_seqs, 256, 0, st>>>(b.cu_seqlens, b.num_seqs, b.region, seqbuf,
-                                                    sched, logp_s, ce);
+hipError_t launch_ce(const olive_batch &b, const olive_spans *spans, const int32_t *seqbuf,
+                     const Sched *sched, const float *logp_s, float *ce, hipStream_t st) {
+    ce_kernel<<<(unsigned)b.num_seqs, 256, 0, st>>>(b.cu_seqlens, b.num_seqs, b.region,
+                                                    span_args(spans), seqbuf, sched, logp_s, ce);
     return hipGetLastError();
 }
 

@@ -71,10 +71,19 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
     out["am_t"] = i32() if "am_t" in outputs and not student_only else None
     out["ce"] = torch.full((B,), fill, dtype=torch.float32, device=dev) \
         if "ce" in outputs and not student_only else None
-    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
+    spans = wl.get("spans") if region == L.OLIVE_REGION_SPANS else None
+    batch = L.make_batch(wl["cu_seqlens"], None if spans is not None else wl["cut"],
+                         wl["targets"], wl["h_student"],
                          None if student_only else wl["h_teacher"], wl["valid_len"], region)
     for _ in range(repeat):
-        if out["kl_rev"] is not None:
+        if spans is not None:
+            o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
+                               logp_student=out["logp_s"], logp_teacher=out["logp_t"],
+                               argmax_student=out["am_s"], argmax_teacher=out["am_t"],
+                               ce_per_seq=out["ce"])
+            sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
+            L.olive_score_batch_spans(ctx, batch, sp, o)
+        elif out["kl_rev"] is not None:
             o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
                                logp_student=out["logp_s"], logp_teacher=out["logp_t"],
                                argmax_student=out["am_s"], argmax_teacher=out["am_t"],
@@ -117,6 +126,11 @@ def structure_np(wl):
             None if wl["valid_len"] is None else to_np(wl["valid_len"]))
 
 
+def masks_of(wl, region):
+    cu, cut, vl = structure_np(wl)
+    return O.masks(cu, cut, vl, region, wl.get("spans") if region == O.REGION_SPANS else None)
+
+
 def stratified_rows(wl, n_random=128, seed=1):
     """Rows of a large workload the oracle evaluates: around every cut and end of
     sequence, first/last rows, every outlier row, and random rows."""
@@ -131,6 +145,11 @@ def stratified_rows(wl, n_random=128, seed=1):
                 picks.add(int(cu[b] + t))
     for r in wl.get("outlier_rows", []):
         picks.add(int(r))
+    for b, sp in enumerate(wl.get("spans") or []):
+        for (a0, e0) in sp:
+            for t in (a0 - 1, a0, e0 - 1, e0):
+                if 0 <= t < lengths[b]:
+                    picks.add(int(cu[b] + t))
     rng = np.random.default_rng(seed)
     T = int(cu[-1])
     picks.update(int(x) for x in rng.choice(T, size=min(n_random, T), replace=False))
@@ -141,7 +160,7 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
             label=""):
     """Compare HIP outputs with the oracle, element by element, at the acceptance bar."""
     cu, cut, vl = structure_np(wl)
-    m = O.masks(cu, cut, vl, region)
+    m = masks_of(wl, region)
     T = len(m["valid"])
     if "counts" in hip:
         assert int(hip["counts"][0]) == m["n_scored"], (label, hip["counts"], m["n_scored"])

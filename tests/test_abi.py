@@ -34,7 +34,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for n in ("olive_score_init", "olive_token_logprobs", "olive_kl_masked",
               "olive_score_free", "olive_status_string", "olive_score_last_error",
-              "olive_score_last_stats", "olive_score_kernel_times", "olive_score_batch"):
+              "olive_score_last_stats", "olive_score_kernel_times", "olive_score_batch",
+              "olive_score_batch_spans"):
         assert n in names
 
 
@@ -61,6 +62,8 @@ def test_struct_layouts_match_header():
     assert ctypes.sizeof(L.olive_score_outputs) == 72
     assert L.olive_score_outputs.kl.offset == 8
     assert L.olive_score_outputs.ce_per_seq.offset == 64
+    assert ctypes.sizeof(L.olive_spans) == 24
+    assert L.olive_spans.spans.offset == 16
 
 
 def _init(desc, ws=1, wt=1):
@@ -114,6 +117,9 @@ def test_calls_on_null_context(lib):
     assert lib.olive_score_kernel_times(None, f, 1) == L.OLIVE_E_NULL
     o = L.make_outputs()
     assert lib.olive_score_batch(None, ctypes.byref(b), ctypes.byref(o), None) == L.OLIVE_E_NULL
+    sp = L.olive_spans()
+    assert lib.olive_score_batch_spans(None, ctypes.byref(b), ctypes.byref(sp), ctypes.byref(o),
+                                       None) == L.OLIVE_E_NULL
 
 
 def test_binding_refuses_to_run_without_the_library(monkeypatch, tmp_path):

@@ -135,6 +135,83 @@ def test_reverse_kl_on_long_rollout_sampled():
     torch.cuda.empty_cache()
 
 
+# ----------------------------------------------------------------------------- span masks
+TURNS_CASE = dict(num_seqs=3, vocab=1000, d_student=128, d_teacher=256, target_source="teacher",
+                  turns=(4, 16, 3, 2, 4, 24, 4, 40))
+
+
+@pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
+def test_span_masks_full(simple):
+    say("span masks", "generic" if simple else "mfma")
+    wl = custom("turns", **TURNS_CASE)
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, simple=simple, outputs=ALL_OUT)
+    assert hip["err"] == 0
+    compare(hip, wl, region=O.REGION_SPANS, label="spans")
+
+
+def test_spans_equal_to_the_cut_region_reproduce_it():
+    say("spans [cut, len) == teacher region")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    cu = wl["cu_seqlens"].cpu().numpy()
+    cut = wl["cut"].cpu().numpy()
+    lens = np.diff(cu)
+    wl["spans"] = [[(int(c), int(n))] for c, n in zip(cut, lens)]
+    wl["span_offsets"] = torch.arange(len(lens) + 1, dtype=torch.int32, device="cuda")
+    wl["span_pairs"] = torch.tensor([[int(c), int(n)] for c, n in zip(cut, lens)],
+                                    dtype=torch.int32, device="cuda")
+    a = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    b = run_hip(wl, region=L.OLIVE_REGION_TEACHER, outputs=ALL_OUT)
+    for k in ("kl", "kl_rev", "ce", "logp_s", "logp_t", "am_s", "am_t", "counts"):
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+def test_empty_spans_score_nothing():
+    say("no spans")
+    wl = custom("turns", **TURNS_CASE)
+    B = wl["cu_seqlens"].shape[0] - 1
+    wl["spans"] = [[] for _ in range(B)]
+    wl["span_offsets"] = torch.zeros(B + 1, dtype=torch.int32, device="cuda")
+    wl["span_pairs"] = torch.zeros((0, 2), dtype=torch.int32, device="cuda")
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    assert int(hip["counts"][0]) == 0 and hip["err"] == 0
+    assert np.all(hip["kl"] == 0.0) and np.all(hip["kl_rev"] == 0.0) and np.all(hip["ce"] == 0.0)
+    compare(hip, wl, region=O.REGION_SPANS, label="no-spans")
+
+
+def test_malformed_spans_set_the_error_word():
+    say("malformed spans")
+    wl = custom("turns", **TURNS_CASE)
+    pairs = wl["span_pairs"].clone()
+    # overlap the first two spans of sequence 1 (entries 2 and 3)
+    pairs[3, 0] = pairs[2, 1] - 1
+    wl["span_pairs"] = pairs
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    assert hip["err"] & 16
+    cu = wl["cu_seqlens"].cpu().numpy()
+    assert np.all(np.isnan(hip["logp_s"][cu[1]:cu[2]]))
+    assert np.isnan(hip["ce"][1]) and not np.isnan(hip["ce"][0]) and not np.isnan(hip["ce"][2])
+    assert not np.any(np.isnan(hip["logp_s"][cu[0]:cu[1]]))
+    # offsets that do not end at S: every sequence is rejected
+    wl2 = custom("turns", **TURNS_CASE)
+    off = wl2["span_offsets"].clone()
+    off[-1] += 1
+    wl2["span_offsets"] = off
+    hip2 = run_hip(wl2, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    assert hip2["err"] & 16 and np.all(np.isnan(hip2["logp_s"]))
+
+
+def test_multi_turn_workload_sampled():
+    say("multi_turn workload sampled")
+    wl = W.make_workload("multi_turn", 0, device="cuda")
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    say("multi_turn stats", hip["stats"])
+    assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    compare(hip, wl, region=O.REGION_SPANS, rows=stratified_rows(wl, n_random=48),
+            label="multi_turn")
+    del wl
+    torch.cuda.empty_cache()
+
+
 def test_student_only_token_logprobs():
     say("student only")
     wl = custom("ragged_v1000", **CASES["ragged_v1000"])
