@@ -78,6 +78,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--reverse-kl", action="store_true",
                     help="also form KL(student || teacher) in the same pass (olive_score_batch)")
+    ap.add_argument("--region-only", action="store_true",
+                    help="score only the region's positions (OLIVE_OUT_REGION_ONLY): the rate "
+                         "and the roofline then count scored positions")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 3 plain device copies of BYTES bytes (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -129,7 +132,8 @@ def main():
     klr = torch.empty(T, dtype=torch.float32, device=dev) if args.reverse_kl else None
     outs = L.make_outputs(kl=kl, kl_reverse=klr, counts=counts, logp_student=lps,
                           logp_teacher=lpt, argmax_student=ams, argmax_teacher=amt,
-                          ce_per_seq=ce)
+                          ce_per_seq=ce,
+                          flags=L.OLIVE_OUT_REGION_ONLY if args.region_only else 0)
     use_spans = wl.get("spans") is not None       # multi-turn: teacher actions scored
     batch = L.make_batch(wl["cu_seqlens"], None if use_spans else wl["cut"], wl["targets"],
                          wl["h_student"], wl["h_teacher"], wl["valid_len"],
@@ -139,7 +143,7 @@ def main():
     def step():
         if use_spans:
             L.olive_score_batch_spans(ctx, batch, spans, outs, stream)
-        elif args.reverse_kl:
+        elif args.reverse_kl or args.region_only:
             L.olive_score_batch(ctx, batch, outs, stream)
         else:
             L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
@@ -162,14 +166,15 @@ def main():
     stats = L.olive_score_last_stats(ctx)
     err = L.olive_score_last_error(ctx)
     n_scored, t_valid = [int(x) for x in counts.cpu().tolist()]
+    rows = n_scored if args.region_only else t_valid     # positions the pass scores
     log("timed %d steps: %.3f ms/step, scoring kernel %.3f ms, stats %s, err %d"
         % (args.steps, ms_step, kernel_ms, stats, err))
-    flops = 2.0 * t_valid * spec.vocab * (spec.d_student + spec.d_teacher)
+    flops = 2.0 * rows * spec.vocab * (spec.d_student + spec.d_teacher)
     achieved = flops / (kernel_ms * 1e-3) / 1e12
-    traffic = None if args.reverse_kl else measured_traffic(args.workload)
+    traffic = None if (args.reverse_kl or args.region_only) else measured_traffic(args.workload)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
-        "value": t_valid / (ms_step * 1e-3),
+        "value": rows / (ms_step * 1e-3),
         "unit": "positions/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -185,7 +190,7 @@ def main():
             "valid_positions": t_valid, "scored_positions": n_scored, "vocab": spec.vocab,
             "d_student": spec.d_student, "d_teacher": spec.d_teacher,
             "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
-            "reverse_kl": bool(args.reverse_kl),
+            "reverse_kl": bool(args.reverse_kl), "region_only": bool(args.region_only),
             "region": "spans" if use_spans else "teacher",
             "near_tie_rows": stats["flagged"], "grid": stats["grid"],
             "step_tflops": flops / (ms_step * 1e-3) / 1e12,

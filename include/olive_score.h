@@ -156,6 +156,12 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
                              int32_t *argmax_student, int32_t *argmax_teacher,
                              float *ce_per_seq, void *hip_stream);
 
+/* Score only the region's positions: log-probs and greedy tokens outside the region
+ * get the fixed values of positions past the valid length (0 and -1), and the
+ * vocabulary pass covers the scored positions only, so its cost scales with the
+ * scored count instead of the valid count (Eq. 1 needs the region alone). */
+#define OLIVE_OUT_REGION_ONLY 1
+
 /*
  * Output set of olive_score_batch. Every pointer may be NULL (that output is not
  * formed); at least one must be set. Device buffers, caller-owned, as in
@@ -163,7 +169,7 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
  */
 typedef struct {
     int32_t size;                /* host: sizeof(olive_score_outputs) (checked) */
-    int32_t reserved;            /* 0 */
+    int32_t flags;               /* bit set of OLIVE_OUT_* (0 = defaults) */
     float *kl;                   /* [T] fp32: KL(teacher || student) in the region, +0.0
                                     elsewhere (the divergence distillation minimises, Sec. 6) */
     float *kl_reverse;           /* [T] fp32: KL(student || teacher), masked the same way (the
@@ -195,8 +201,8 @@ typedef struct {
  * Every per-position output of one batch in one fused pass over the vocabulary:
  * olive_kl_masked's outputs plus the reverse KL. Teacher outputs (kl, kl_reverse,
  * logp_teacher, argmax_teacher) need a teacher context and b->h_teacher.
- * Errors: E_NULL (out, or every output pointer, NULL), E_RANGE (out->size wrong),
- * and as olive_kl_masked.
+ * Errors: E_NULL (out, or every output pointer, NULL), E_RANGE (out->size wrong or
+ * unknown flags), and as olive_kl_masked.
  */
 olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
                                const olive_score_outputs *out, void *hip_stream);

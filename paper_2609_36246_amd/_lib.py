@@ -35,6 +35,7 @@ OLIVE_REGION_ALL = 2
 OLIVE_REGION_SPANS = 3
 OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
+OLIVE_OUT_REGION_ONLY = 1
 
 
 class olive_score_desc(ctypes.Structure):
@@ -54,7 +55,7 @@ class olive_batch(ctypes.Structure):
 
 
 class olive_score_outputs(ctypes.Structure):
-    _fields_ = [("size", ctypes.c_int32), ("reserved", ctypes.c_int32),
+    _fields_ = [("size", ctypes.c_int32), ("flags", ctypes.c_int32),
                 ("kl", ctypes.c_void_p), ("kl_reverse", ctypes.c_void_p),
                 ("counts", ctypes.c_void_p), ("logp_student", ctypes.c_void_p),
                 ("logp_teacher", ctypes.c_void_p), ("argmax_student", ctypes.c_void_p),
@@ -196,10 +197,11 @@ def olive_kl_masked(ctx, batch: olive_batch, kl, counts=None, logp_student=None,
 
 
 def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_teacher=None,
-                 argmax_student=None, argmax_teacher=None, ce_per_seq=None) -> olive_score_outputs:
+                 argmax_student=None, argmax_teacher=None, ce_per_seq=None,
+                 flags: int = 0) -> olive_score_outputs:
     o = olive_score_outputs()
     o.size = ctypes.sizeof(olive_score_outputs)
-    o.reserved = 0
+    o.flags = int(flags)
     o.kl, o.kl_reverse, o.counts = _ptr(kl), _ptr(kl_reverse), _ptr(counts)
     o.logp_student, o.logp_teacher = _ptr(logp_student), _ptr(logp_teacher)
     o.argmax_student, o.argmax_teacher = _ptr(argmax_student), _ptr(argmax_teacher)

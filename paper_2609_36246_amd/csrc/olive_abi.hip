@@ -66,7 +66,8 @@ olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE
 // The scoring of one batch, shared by every scoring entry point.
 olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
                  float *kl, float *kl_rev, int64_t *counts, float *logp_s, float *logp_t,
-                 int32_t *am_s, int32_t *am_t, float *ce, hipStream_t st) {
+                 int32_t *am_s, int32_t *am_t, float *ce, hipStream_t st,
+                 bool region_only = false) {
     const olive_score_desc &d = ctx->desc;
     if (!b->cu_seqlens || !b->targets || !b->h_student) return OLIVE_E_NULL;
     if (!spans && !b->cut) return OLIVE_E_NULL;
@@ -105,11 +106,12 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
         fixed_splits = (int)(want < 1 ? 1 : (want > lim ? lim : want));
         max_units = pt * fixed_splits;
     }
-    s = check_hip(launch_prep(*b, spans, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
+    s = check_hip(launch_prep(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
                               mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
                               fixed_splits, st));
     if (s) return s;
-    s = check_hip(launch_rowmap(*b, spans, V, ctx->seqbuf, ctx->sched, ctx->rowmap, ctx->err,
+    s = check_hip(launch_rowmap(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
+                                ctx->err,
                                 logp_s,
                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
                                 has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, st));
@@ -294,6 +296,7 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
 static olive_status check_outputs(const olive_score_outputs *out) {
     if (!out) return OLIVE_E_NULL;
     if (out->size != (int32_t)sizeof(olive_score_outputs)) return OLIVE_E_RANGE;
+    if (out->flags & ~OLIVE_OUT_REGION_ONLY) return OLIVE_E_RANGE;
     if (!out->kl && !out->kl_reverse && !out->counts && !out->logp_student &&
         !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq)
         return OLIVE_E_NULL;
@@ -306,7 +309,7 @@ olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
     if (olive_status e = check_outputs(out)) return e;
     return run(ctx, b, nullptr, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
-               (hipStream_t)hip_stream);
+               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0);
 }
 
 olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
@@ -316,7 +319,7 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
     if (olive_status e = check_outputs(out)) return e;
     return run(ctx, b, spans, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
-               (hipStream_t)hip_stream);
+               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0);
 }
 
 olive_status olive_score_free(olive_score_ctx *ctx) {

@@ -27,7 +27,8 @@ enum Field {
 
 // Device-side schedule of one call, written by the preparation kernel.
 struct Sched {
-    int32_t t_valid;    // valid (scored or context) positions = compacted rows
+    int32_t t_valid;    // compacted rows: valid positions, or only the in-region ones when
+                        // the call restricts every output to the region
     int32_t n_ptiles;   // ceil(t_valid / tile_rows) for the kernel in use
     int32_t n_splits;   // vocabulary splits
     int32_t n_units;    // n_ptiles * n_splits
@@ -67,11 +68,12 @@ struct ScoreArgs {
 // Host-side launchers (each defined beside its kernel).
 hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int elem_bytes,
                          hipStream_t st);
-hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, int64_t V, int32_t *seqbuf,
-                       Sched *sched, int32_t *err, int64_t *counts, int tile_rows, int policy,
-                       int n_vtiles, int grid, int fixed_splits, hipStream_t st);
-hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, int64_t V,
-                         const int32_t *seqbuf,
+hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, bool region_only,
+                       int64_t V, int32_t *seqbuf, Sched *sched, int32_t *err, int64_t *counts,
+                       int tile_rows, int policy, int n_vtiles, int grid, int fixed_splits,
+                       hipStream_t st);
+hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool region_only,
+                         int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
                          float *logp_tmp, hipStream_t st);

@@ -27,14 +27,28 @@ __device__ __forceinline__ bool in_region(int region, int t, int cut) {
 }
 
 // t inside one of spans [i0, i1) (validated: increasing, disjoint): the last span
-// starting at or before t must end after it.
-__device__ __forceinline__ bool in_spans(const int32_t *pairs, int i0, int i1, int t) {
+// starting at or before t must end after it. Returns that span's index or -1.
+__device__ __forceinline__ int span_of(const int32_t *pairs, int i0, int i1, int t) {
     int lo = i0, hi = i1;   // first span with start > t
     while (lo < hi) {
         const int mid = (lo + hi) >> 1;
         if (pairs[2 * mid] <= t) lo = mid + 1; else hi = mid;
     }
-    return lo > i0 && t < pairs[2 * (lo - 1) + 1];
+    return (lo > i0 && t < pairs[2 * (lo - 1) + 1]) ? lo - 1 : -1;
+}
+
+// Rank of in-region position t among the sequence's in-region positions (its
+// compacted index when only the region is scored).
+__device__ __forceinline__ int region_rank(int region, const SpanArgs &sp, int b, int span,
+                                           int t, int cut, int vl) {
+    if (region == OLIVE_REGION_TEACHER) return t - cut;
+    if (region != OLIVE_REGION_SPANS) return t;
+    int r = 0;
+    for (int i = sp.off[b]; i < span; ++i) {
+        const int a = sp.pairs[2 * i], e = sp.pairs[2 * i + 1] < vl ? sp.pairs[2 * i + 1] : vl;
+        r += e > a ? e - a : 0;
+    }
+    return r + (t - sp.pairs[2 * span]);
 }
 
 __device__ __forceinline__ int region_count(int region, int vl, int cut) {
@@ -51,12 +65,14 @@ constexpr int PREP_THREADS = 1024;
 __global__ void __launch_bounds__(PREP_THREADS)
 prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             const int32_t *__restrict__ vlen, int32_t B, int64_t T, int32_t region,
-            SpanArgs sp, int32_t *__restrict__ seqbuf, Sched *__restrict__ sched,
-            int32_t *__restrict__ err, int64_t *__restrict__ counts, int32_t tile_rows,
-            int32_t policy, int32_t n_vtiles, int32_t grid, int32_t fixed_splits) {
+            SpanArgs sp, int32_t region_only, int32_t *__restrict__ seqbuf,
+            Sched *__restrict__ sched, int32_t *__restrict__ err, int64_t *__restrict__ counts,
+            int32_t tile_rows, int32_t policy, int32_t n_vtiles, int32_t grid,
+            int32_t fixed_splits) {
     __shared__ int s_bad, s_badoff;
     __shared__ int s_scan[PREP_THREADS];
     __shared__ long long s_red[PREP_THREADS];
+    __shared__ long long s_val[PREP_THREADS];
     const int tid = threadIdx.x;
     const bool span_mode = region == OLIVE_REGION_SPANS;
     if (tid == 0) { s_bad = 0; s_badoff = 0; }
@@ -92,11 +108,12 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
         return;
     }
     int carry = 0;
-    long long scored = 0;
+    long long scored = 0, valid = 0;
     for (int base = 0; base < B; base += PREP_THREADS) {
         int b = base + tid;
-        int v = 0;
-        long long sc = 0;
+        int v = 0;            // compacted rows of this sequence
+        long long sc = 0;     // its scored positions
+        long long vv = 0;     // its valid positions
         if (b < B) {
             int len = cu[b + 1] - cu[b];
             int c = span_mode ? 0 : cut[b];
@@ -124,12 +141,14 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
                 vl_eff[b] = 0; cut_eff[b] = 0; badseq[b] = 1;
             } else {
                 vl_eff[b] = vl; cut_eff[b] = c; badseq[b] = 0;
-                v = vl;
                 sc = span_mode ? span_sc : region_count(region, vl, c);
+                vv = vl;
+                v = region_only ? (int)sc : vl;
             }
         }
         s_scan[tid] = v;
         s_red[tid] = sc;
+        s_val[tid] = vv;
         __syncthreads();
         for (int off = 1; off < PREP_THREADS; off <<= 1) {   // inclusive scan
             int add = tid >= off ? s_scan[tid - off] : 0;
@@ -137,18 +156,22 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             s_scan[tid] += add;
             __syncthreads();
         }
-        for (int off = PREP_THREADS / 2; off > 0; off >>= 1) {  // fixed-order sum
-            if (tid < off) s_red[tid] += s_red[tid + off];
+        for (int off = PREP_THREADS / 2; off > 0; off >>= 1) {  // fixed-order sums
+            if (tid < off) {
+                s_red[tid] += s_red[tid + off];
+                s_val[tid] += s_val[tid + off];
+            }
             __syncthreads();
         }
         if (b < B) cvalid[b] = carry + s_scan[tid] - v;
         carry += s_scan[PREP_THREADS - 1];
         scored += s_red[0];
+        valid += s_val[0];
         __syncthreads();
     }
     if (tid == 0) {
         cvalid[B] = carry;
-        int t_valid = carry;
+        int t_valid = carry;   // compacted rows: valid, or in-region when region-only
         int n_p = (t_valid + tile_rows - 1) / tile_rows;
         int ns = 1;
         if (policy == 0) {
@@ -173,16 +196,17 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
         sched->n_scored = scored;
         sched->n_flagged = 0;
         sched->cu_bad = 0;
-        if (counts) { counts[0] = scored; counts[1] = t_valid; }
+        if (counts) { counts[0] = scored; counts[1] = valid; }
     }
 }
 
-// Maps every packed row to its compacted index (valid rows only) and writes the
-// fixed outputs of rows past the valid length (logp 0, argmax -1, kl +0) and of
-// rows of malformed sequences (NaN, argmax -1).
+// Maps every packed row to its compacted index (valid rows, or with region_only
+// in-region rows only) and writes the fixed outputs of rows that are not scored
+// (logp 0, argmax -1, kl +0) and of rows of malformed sequences (NaN, argmax -1).
 __global__ void __launch_bounds__(256)
 rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t region,
-              SpanArgs sp, const int32_t *__restrict__ seqbuf, const Sched *__restrict__ sched,
+              SpanArgs sp, int32_t region_only, const int32_t *__restrict__ seqbuf,
+              const Sched *__restrict__ sched,
               uint32_t *__restrict__ rowmap, float *__restrict__ logp_s,
               float *__restrict__ logp_t, int32_t *__restrict__ am_s, int32_t *__restrict__ am_t,
               float *__restrict__ kl, float *__restrict__ kl_rev,
@@ -217,12 +241,22 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (logp_tmp) logp_tmp[g] = qnan;
             continue;
         }
-        if (t < vl_eff[b]) {
-            const bool r = region == OLIVE_REGION_SPANS
-                               ? in_spans(sp.pairs, sp.off[b], sp.off[b + 1], t)
-                               : in_region(region, t, cut_eff[b]);
-            uint32_t inr = r ? 1u : 0u;
-            rowmap[cvalid[b] + t] = (uint32_t)g | (inr << 31);
+        const int vl = vl_eff[b];
+        int span = -1;
+        bool r = false;
+        if (t < vl) {
+            if (region == OLIVE_REGION_SPANS) {
+                span = span_of(sp.pairs, sp.off[b], sp.off[b + 1], t);
+                r = span >= 0;
+            } else {
+                r = in_region(region, t, cut_eff[b]);
+            }
+        }
+        if (t < vl && !region_only) {
+            rowmap[cvalid[b] + t] = (uint32_t)g | ((r ? 1u : 0u) << 31);
+        } else if (t < vl && r) {
+            rowmap[cvalid[b] + region_rank(region, sp, b, span, t, cut_eff[b], vl)] =
+                (uint32_t)g | (1u << 31);
         } else {
             if (logp_s) logp_s[g] = 0.f;
             if (logp_t) logp_t[g] = 0.f;
@@ -312,19 +346,20 @@ static SpanArgs span_args(const olive_spans *s) {
     return a;
 }
 
-hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, int64_t V, int32_t *seqbuf,
-                       Sched *sched, int32_t *err, int64_t *counts, int tile_rows, int policy,
-                       int n_vtiles, int grid, int fixed_splits, hipStream_t st) {
+hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, bool region_only,
+                       int64_t V, int32_t *seqbuf, Sched *sched, int32_t *err, int64_t *counts,
+                       int tile_rows, int policy, int n_vtiles, int grid, int fixed_splits,
+                       hipStream_t st) {
     (void)V;
     prep_kernel<<<1, PREP_THREADS, 0, st>>>(b.cu_seqlens, b.cut, b.valid_len, b.num_seqs,
-                                            b.total_positions, b.region, span_args(spans), seqbuf,
-                                            sched, err, counts, tile_rows, policy, n_vtiles, grid,
-                                            fixed_splits);
+                                            b.total_positions, b.region, span_args(spans),
+                                            region_only ? 1 : 0, seqbuf, sched, err, counts,
+                                            tile_rows, policy, n_vtiles, grid, fixed_splits);
     return hipGetLastError();
 }
 
-hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, int64_t V,
-                         const int32_t *seqbuf,
+hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool region_only,
+                         int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
                          float *logp_tmp, hipStream_t st) {
@@ -334,7 +369,8 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, int64_t
     if (blocks > 4096) blocks = 4096;
     if (blocks < 1) blocks = 1;
     rowmap_kernel<<<(unsigned)blocks, 256, 0, st>>>(b.cu_seqlens, b.num_seqs, T, b.region,
-                                                    span_args(spans), seqbuf, sched, rowmap,
+                                                    span_args(spans), region_only ? 1 : 0, seqbuf,
+                                                    sched, rowmap,
                                                     logp_s, logp_t, am_s,
                                                     am_t, kl, kl_rev, logp_tmp);
     return hipGetLastError();

@@ -37,7 +37,7 @@ def to_np(t):
 
 def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
             outputs=("kl", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
-            poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1):
+            poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1, out_flags=0):
     """Score a workload on the GPU; returns numpy outputs (and stats)."""
     dev = wl["h_student"].device
     spec = wl["spec"]
@@ -76,19 +76,16 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
                          wl["targets"], wl["h_student"],
                          None if student_only else wl["h_teacher"], wl["valid_len"], region)
     for _ in range(repeat):
-        if spans is not None:
+        if spans is not None or out["kl_rev"] is not None or out_flags:
             o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
                                logp_student=out["logp_s"], logp_teacher=out["logp_t"],
                                argmax_student=out["am_s"], argmax_teacher=out["am_t"],
-                               ce_per_seq=out["ce"])
-            sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
-            L.olive_score_batch_spans(ctx, batch, sp, o)
-        elif out["kl_rev"] is not None:
-            o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
-                               logp_student=out["logp_s"], logp_teacher=out["logp_t"],
-                               argmax_student=out["am_s"], argmax_teacher=out["am_t"],
-                               ce_per_seq=out["ce"])
-            L.olive_score_batch(ctx, batch, o)
+                               ce_per_seq=out["ce"], flags=out_flags)
+            if spans is not None:
+                sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
+                L.olive_score_batch_spans(ctx, batch, sp, o)
+            else:
+                L.olive_score_batch(ctx, batch, o)
         elif student_only or out["kl"] is None:
             L.olive_token_logprobs(ctx, batch, out["logp_s"], out["logp_t"], out["am_s"],
                                    out["am_t"])
@@ -157,14 +154,22 @@ def stratified_rows(wl, n_random=128, seed=1):
 
 
 def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, check_ce=True,
-            label=""):
-    """Compare HIP outputs with the oracle, element by element, at the acceptance bar."""
+            label="", region_only=False):
+    """Compare HIP outputs with the oracle, element by element, at the acceptance bar.
+
+    region_only: the call scored only the region; every output outside it must hold
+    the fixed values of unscored positions, and the region is compared as usual."""
     cu, cut, vl = structure_np(wl)
     m = masks_of(wl, region)
     T = len(m["valid"])
+    if region_only:
+        m = dict(m)
+        m["valid"] = m["in_region"].copy()
     if "counts" in hip:
         assert int(hip["counts"][0]) == m["n_scored"], (label, hip["counts"], m["n_scored"])
         assert int(hip["counts"][1]) == m["t_valid"], (label, hip["counts"], m["t_valid"])
+    if region_only:
+        m["t_valid"] = int(m["valid"].sum())
     valid, inr = m["valid"], m["in_region"]
     # fixed values outside the valid prefix, bit-exact
     inval = ~valid

@@ -200,6 +200,23 @@ def test_malformed_spans_set_the_error_word():
     assert hip2["err"] & 16 and np.all(np.isnan(hip2["logp_s"]))
 
 
+@pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
+@pytest.mark.parametrize("case", ["ragged_v1000", "turns"])
+def test_region_only_scores_just_the_region(case, simple):
+    say("region only", case, "generic" if simple else "mfma")
+    if case == "turns":
+        wl, region = custom("turns", **TURNS_CASE), O.REGION_SPANS
+    else:
+        wl, region = custom(case, **CASES[case]), O.REGION_TEACHER
+    hip = run_hip(wl, region=region, simple=simple, outputs=ALL_OUT,
+                  out_flags=L.OLIVE_OUT_REGION_ONLY)
+    assert hip["err"] == 0
+    compare(hip, wl, region=region, region_only=True, label="region-only-" + case)
+    # the compacted rows are the scored ones
+    full = run_hip(wl, region=region, simple=simple, outputs=ALL_OUT)
+    np.testing.assert_array_equal(hip["counts"], full["counts"])
+
+
 def test_multi_turn_workload_sampled():
     say("multi_turn workload sampled")
     wl = W.make_workload("multi_turn", 0, device="cuda")
