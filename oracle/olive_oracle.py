@@ -20,6 +20,10 @@ What it computes (for every packed position of a batch of stitched rollouts):
     direction, the per-token objective of on-policy distillation (Sec. 1);
   * argmax_X = lowest v attaining M_X   -- the greedy token (the K = 1 case of the
     top-K overlap statistic of Sec. 4.1);
+  * TopK_X = the K largest logits of model X, ties broken towards the lower index;
+    overlap = |TopK_S & TopK_T| / K (the top-K overlap ratio of Sec. 4.1) and the
+    top-K KL approximation sum_{v in TopK_T} p_T[v] (log p_T[v] - log p_S[v]) with
+    full-vocabulary normalisers (OPD's LogProb top-K = 16, App. A Table 3);
   * masks: a position is valid when it precedes the sequence's valid length, and
     in-region (scored) for the teacher region when it is at or past the cut, the
     prompt and student prefix being masked out of Eq. 1's loss (Sec. 3.1).
@@ -152,6 +156,35 @@ def kl_student_teacher(z_s, lse_s: float, z_t, lse_t: float) -> tuple:
     return kl_teacher_student(z_s, lse_s, z_t, lse_t)
 
 
+TOPK = 16   # LogProb top-K of the OPD baseline (App. A, Table 3)
+
+
+def topk_set(z_row, k: int) -> np.ndarray:
+    """Indices of the k largest entries, ordered by (value descending, index
+    ascending): ties at the boundary go to the lower vocabulary indices. One library
+    sort on the key (value descending, index ascending)."""
+    z = _f64(z_row)
+    order = np.lexsort((np.arange(len(z)), -z))
+    return order[:k].astype(np.int64)
+
+
+def topk_overlap(set_s, set_t, k: int = TOPK) -> float:
+    """|TopK(student) & TopK(teacher)| / k (Sec. 4.1's top-K overlap ratio), from
+    the two index sets."""
+    return len(set(np.asarray(set_s).tolist()) & set(np.asarray(set_t).tolist())) / float(k)
+
+
+def kl_topk(z_t, lse_t: float, z_s, lse_s: float, set_t) -> float:
+    """KL(teacher || student) restricted to the teacher's top-k tokens (set_t), with
+    the full-vocabulary normalisers (not renormalised): the top-K approximation of
+    the OPD baseline (abstract; App. A, Table 3: LogProb top-K = 16)."""
+    zt, zs = _f64(z_t), _f64(z_s)
+    idx = np.asarray(set_t, dtype=np.int64)
+    lp_t = zt[idx] - lse_t
+    lp_s = zs[idx] - lse_s
+    return math.fsum((np.exp(lp_t) * (lp_t - lp_s)).tolist())
+
+
 def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1.0,
                h_teacher_rows=None, w_teacher=None, scale_teacher: float = 1.0,
                chunk: Optional[int] = None) -> dict:
@@ -160,7 +193,8 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     Returns float64 / int64 arrays of length n: z_y_s, lse_s, logp_s, argmax_s,
     gap_s, max_s, and with a teacher the same for t plus kl (direct) and
     kl_nonneg (KL(teacher || student)), kl_rev and kl_rev_nonneg (KL(student ||
-    teacher)).
+    teacher)), overlap and kl_topk (top-K statistics, K = TOPK) and the top-K index
+    sets topk_s / topk_t ([n, TOPK]).
     """
     hs = _f64(h_student_rows)
     n = hs.shape[0]
@@ -178,8 +212,10 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     out["argmax_s"] = np.zeros(n, dtype=np.int64)
     if has_t:
         for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg", "kl_rev",
-                  "kl_rev_nonneg"):
+                  "kl_rev_nonneg", "overlap", "kl_topk"):
             out[k] = np.zeros(n)
+        out["topk_s"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
+        out["topk_t"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
         out["argmax_t"] = np.zeros(n, dtype=np.int64)
     for r0 in range(0, n, chunk):
         r1 = min(n, r0 + chunk)
@@ -208,6 +244,12 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
                 klr, klrp = kl_student_teacher(zs[i], st["lse"], zt[i], tt["lse"])
                 out["kl_rev"][g] = klr
                 out["kl_rev_nonneg"][g] = klrp
+                kk = min(TOPK, V)
+                set_s, set_t = topk_set(zs[i], kk), topk_set(zt[i], kk)
+                out["overlap"][g] = topk_overlap(set_s, set_t, kk)
+                out["kl_topk"][g] = kl_topk(zt[i], tt["lse"], zs[i], st["lse"], set_t)
+                out["topk_s"][g] = set_s
+                out["topk_t"][g] = set_t
     return out
 
 
@@ -240,7 +282,8 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
                        scale_teacher)
     out = dict(logp_s=np.zeros(T), argmax_s=np.full(T, -1, dtype=np.int64),
                lse_s=np.zeros(T), gap_s=np.full(T, math.inf), kl=np.zeros(T),
-               kl_nonneg=np.zeros(T), kl_rev=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
+               kl_nonneg=np.zeros(T), kl_rev=np.zeros(T), overlap=np.zeros(T),
+               kl_topk=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
     if has_t:
         out.update(logp_t=np.zeros(T), argmax_t=np.full(T, -1, dtype=np.int64),
                    lse_t=np.zeros(T), gap_t=np.full(T, math.inf))
@@ -255,6 +298,8 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
             out["kl"][sel[inr]] = r["kl"][inr]
             out["kl_nonneg"][sel[inr]] = r["kl_nonneg"][inr]
             out["kl_rev"][sel[inr]] = r["kl_rev"][inr]
+            out["overlap"][sel[inr]] = r["overlap"][inr]
+            out["kl_topk"][sel[inr]] = r["kl_topk"][inr]
     # Eq. 1: the loss of sequence b is minus the sum of the student's log-probs of
     # its in-region tokens; an empty region gives 0.
     ce = np.zeros(B)

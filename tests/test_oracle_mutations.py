@@ -16,6 +16,8 @@ from tests import test_oracle_pins as P
 _orig_lss = O.log_softmax_stats
 _orig_kl = O.kl_teacher_student
 _orig_klr = O.kl_student_teacher
+_orig_topk = O.topk_set
+_orig_kltk = O.kl_topk
 _orig_masks = O.masks
 _orig_project = O.project
 
@@ -62,6 +64,26 @@ def klr_dropped_cross_term(z_s, lse_s, z_t, lse_t):
     return a - ent, b - ent
 
 
+def topk_ties_high_index(z_row, k):
+    z = np.asarray(z_row, dtype=np.float64)
+    order = np.lexsort((-np.arange(len(z)), -z))
+    return order[:k].astype(np.int64)
+
+
+def kl_topk_renormalised(z_t, lse_t, z_s, lse_s, set_t):
+    idx = np.asarray(set_t, dtype=np.int64)
+    zt = np.asarray(z_t, dtype=np.float64)[idx]
+    zs = np.asarray(z_s, dtype=np.float64)[idx]
+    lt = zt - (zt.max() + math.log(np.exp(zt - zt.max()).sum()))
+    ls = zs - (zs.max() + math.log(np.exp(zs - zs.max()).sum()))
+    return math.fsum((np.exp(lt) * (lt - ls)).tolist())
+
+
+def overlap_jaccard(set_s, set_t, k=O.TOPK):
+    a, b = set(np.asarray(set_s).tolist()), set(np.asarray(set_t).tolist())
+    return len(a & b) / float(len(a | b))
+
+
 def masks_off_by_one(cu_seqlens, cut, valid_len=None, region=O.REGION_TEACHER, spans=None):
     return _orig_masks(cu_seqlens, np.asarray(cut) + 1, valid_len, region, spans)
 
@@ -99,6 +121,9 @@ MUTANTS = [
     ("masks", masks_off_by_one),
     ("masks", masks_ignore_valid),
     ("masks", masks_span_end_inclusive),
+    ("topk_set", topk_ties_high_index),
+    ("kl_topk", kl_topk_renormalised),
+    ("topk_overlap", overlap_jaccard),
     ("project", project_no_scale),
     ("project", project_dropped_last_k),
 ]
@@ -117,6 +142,9 @@ PINS = [
     P.test_mask_counts_enumerated,
     P.test_eq1_masks_prefix_and_scores_continuation,
     P.test_span_masks_reduce_to_the_cut_regions_and_add_up,
+    P.test_topk_set_ties_take_lower_indices,
+    P.test_topk_worked_example,
+    P.test_topk_reduces_to_argmax_and_to_the_full_kl,
     P.test_masked_outputs_exact_values,
 ]
 

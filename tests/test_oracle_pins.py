@@ -279,6 +279,68 @@ def test_mask_counts_enumerated():
                                               np.arange(cut, max(cut, vl)))
 
 
+# ----------------------------------------------------------------------------- top-K statistics
+def test_topk_set_ties_take_lower_indices():
+    z = [1.0, 3.0, 3.0, 2.0, 3.0, -1.0]
+    np.testing.assert_array_equal(O.topk_set(z, 2), [1, 2])
+    np.testing.assert_array_equal(O.topk_set(z, 4), [1, 2, 4, 3])
+    np.testing.assert_array_equal(O.topk_set([0.0] * 7, 3), [0, 1, 2])
+    # brute force: every k-subset ordered by (value desc, index asc)
+    rng = np.random.default_rng(21)
+    for _ in range(50):
+        V = int(rng.integers(1, 12))
+        z = rng.integers(-3, 4, size=V).astype(np.float64)   # many ties
+        k = int(rng.integers(1, V + 1))
+        want = [v for _, v in sorted((-z[v], v) for v in range(V))][:k]
+        np.testing.assert_array_equal(O.topk_set(z, k), want)
+
+
+def test_topk_worked_example():
+    """Teacher logits ln(1, 4, 2, 8, 1), student ln(4, 1, 2, 1, 8), K = 2:
+    TopK_T = {3, 1}, TopK_S = {4, 0}: overlap 0; with Z_T = 16 and Z_S = 16,
+    KL_top2 = (8/16) ln(8/1) + (4/16) ln(4/1)."""
+    zt = np.log([1.0, 4.0, 2.0, 8.0, 1.0])
+    zs = np.log([4.0, 1.0, 2.0, 1.0, 8.0])
+    lse_t = lse_s = math.log(16.0)
+    st, ss = O.topk_set(zt, 2), O.topk_set(zs, 2)
+    np.testing.assert_array_equal(st, [3, 1])
+    np.testing.assert_array_equal(ss, [4, 0])
+    assert O.topk_overlap(ss, st, 2) == 0.0
+    want = 0.5 * math.log(8.0) + 0.25 * math.log(4.0)
+    assert abs(O.kl_topk(zt, lse_t, zs, lse_s, st) - want) <= 1e-14
+    # a student sharing one of the two: ln(1, 2, 4, 8, 1) -> TopK_S = {3, 2}, overlap 1/2
+    s2 = O.topk_set(np.log([1.0, 2.0, 4.0, 8.0, 1.0]), 2)
+    np.testing.assert_array_equal(s2, [3, 2])
+    assert O.topk_overlap(s2, st, 2) == 0.5
+
+
+def test_topk_reduces_to_argmax_and_to_the_full_kl():
+    rng = np.random.default_rng(22)
+    hs, ht = bf16_values((6, 8), rng), bf16_values((6, 8), rng)
+    for V in (5, 16, 40):
+        ws, wt = bf16_values((8, V), rng), bf16_values((8, V), rng)
+        r = O.row_scores(hs, ws, np.zeros(6, dtype=np.int64), 1.0, ht, wt, 2.0)
+        zs, zt = O.project(hs, ws, 1.0), O.project(ht, wt, 2.0)
+        for i in range(6):
+            # K = 1: the greedy tokens
+            s1, t1 = O.topk_set(zs[i], 1), O.topk_set(zt[i], 1)
+            assert s1[0] == r["argmax_s"][i] and t1[0] == r["argmax_t"][i]
+            a = t1[0]
+            lp_t, lp_s = zt[i, a] - r["lse_t"][i], zs[i, a] - r["lse_s"][i]
+            assert abs(O.kl_topk(zt[i], r["lse_t"][i], zs[i], r["lse_s"][i], t1)
+                       - math.exp(lp_t) * (lp_t - lp_s)) <= 1e-14
+            # K = V: every token, the full KL and overlap 1
+            if V <= O.TOPK:
+                assert r["overlap"][i] == 1.0
+                assert abs(r["kl_topk"][i] - r["kl"][i]) <= 1e-12
+            else:
+                assert r["kl_topk"][i] != r["kl"][i]
+    # identical models: overlap 1 and zero divergence
+    ws = bf16_values((8, 300), rng)
+    r = O.row_scores(hs, ws, np.zeros(6, dtype=np.int64), 1.0, hs, ws, 1.0)
+    assert np.all(r["overlap"] == 1.0) and np.all(r["kl_topk"] == 0.0)
+
+
 def test_span_masks_reduce_to_the_cut_regions_and_add_up():
     """Span masks (Sec. 3.2): a single span [cut, len) is the teacher region, [0, cut)
     the student region, [0, len) every valid position, no span scores nothing; the
