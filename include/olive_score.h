@@ -92,6 +92,11 @@ typedef struct {
 /* Record HIP events around the vocabulary-scoring kernel of every call (for
  * olive_score_kernel_times); costs two event records per call. */
 #define OLIVE_FLAG_KERNEL_TIMING 2
+/* Reserve the workspace of the top-K statistics (olive_score_outputs' topk_* and
+ * kl_topk fields). Needs a bf16 teacher context on which the MFMA kernel applies and
+ * V >= 512 (else init returns E_UNSUPPORTED). The workspace holds about
+ * (max_positions x (2.9 KB + 2.3 KB x ceil(V / 4096))) of device memory. */
+#define OLIVE_FLAG_TOPK 4
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */
 typedef struct {
@@ -180,6 +185,17 @@ typedef struct {
     int32_t *argmax_student;     /* [T] int32 */
     int32_t *argmax_teacher;     /* [T] int32 */
     float *ce_per_seq;           /* [B] fp32: Eq. 1's loss per sequence */
+    /* Top-K statistics, K = 16 (need OLIVE_FLAG_TOPK at init and a teacher). TopK_X is
+     * the set of model X's 16 largest logits, larger value first and the lower
+     * vocabulary index first among equal values. At scored positions: */
+    float *topk_overlap;         /* [T] fp32: |TopK_S & TopK_T| / 16 (Sec. 4.1's top-K
+                                    overlap ratio), +0.0 at other valid positions */
+    float *kl_topk;              /* [T] fp32: sum over v in TopK_T of
+                                    p_T(v) (log p_T(v) - log p_S(v)) with the full-vocabulary
+                                    normalisers: the top-16 approximation of KL(teacher ||
+                                    student) (App. A, Table 3), +0.0 elsewhere */
+    int32_t *topk_student;       /* [T][16] int32: TopK_S in rank order, -1 elsewhere */
+    int32_t *topk_teacher;       /* [T][16] int32: TopK_T in rank order, -1 elsewhere */
 } olive_score_outputs;
 
 /*
@@ -199,10 +215,13 @@ typedef struct {
 
 /*
  * Every per-position output of one batch in one fused pass over the vocabulary:
- * olive_kl_masked's outputs plus the reverse KL. Teacher outputs (kl, kl_reverse,
- * logp_teacher, argmax_teacher) need a teacher context and b->h_teacher.
+ * olive_kl_masked's outputs plus the reverse KL and the top-K statistics. Teacher
+ * outputs (kl, kl_reverse, logp_teacher, argmax_teacher and every top-K output) need
+ * a teacher context and b->h_teacher. Malformed sequences give NaN (top-K indices -1)
+ * as for the other outputs.
  * Errors: E_NULL (out, or every output pointer, NULL), E_RANGE (out->size wrong or
- * unknown flags), and as olive_kl_masked.
+ * unknown flags), E_UNSUPPORTED (a top-K output without OLIVE_FLAG_TOPK at init, or
+ * with hidden states that are not 16-byte aligned), and as olive_kl_masked.
  */
 olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
                                const olive_score_outputs *out, void *hip_stream);
@@ -237,9 +256,11 @@ olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
 
 /*
  * Diagnostics of the last scoring call (synchronises the device).
- *   out host [4] int64: [0] vocabulary splits used, [1] rows whose greedy token was
+ *   out host [5] int64: [0] vocabulary splits used, [1] rows whose greedy token was
  *   re-decided in fp64 because its top-2 logit gap was within the fp32 error window,
- *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched.
+ *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched,
+ *   [4] rows whose top-K sets were recomputed by the exact rescan (0 without top-K
+ *   outputs).
  */
 olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out);
 

@@ -35,6 +35,8 @@ OLIVE_REGION_ALL = 2
 OLIVE_REGION_SPANS = 3
 OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
+OLIVE_FLAG_TOPK = 4
+OLIVE_TOPK = 16
 OLIVE_OUT_REGION_ONLY = 1
 
 
@@ -59,7 +61,9 @@ class olive_score_outputs(ctypes.Structure):
                 ("kl", ctypes.c_void_p), ("kl_reverse", ctypes.c_void_p),
                 ("counts", ctypes.c_void_p), ("logp_student", ctypes.c_void_p),
                 ("logp_teacher", ctypes.c_void_p), ("argmax_student", ctypes.c_void_p),
-                ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p)]
+                ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p),
+                ("topk_overlap", ctypes.c_void_p), ("kl_topk", ctypes.c_void_p),
+                ("topk_student", ctypes.c_void_p), ("topk_teacher", ctypes.c_void_p)]
 
 
 class olive_spans(ctypes.Structure):
@@ -198,6 +202,7 @@ def olive_kl_masked(ctx, batch: olive_batch, kl, counts=None, logp_student=None,
 
 def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_teacher=None,
                  argmax_student=None, argmax_teacher=None, ce_per_seq=None,
+                 topk_overlap=None, kl_topk=None, topk_student=None, topk_teacher=None,
                  flags: int = 0) -> olive_score_outputs:
     o = olive_score_outputs()
     o.size = ctypes.sizeof(olive_score_outputs)
@@ -206,6 +211,8 @@ def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_
     o.logp_student, o.logp_teacher = _ptr(logp_student), _ptr(logp_teacher)
     o.argmax_student, o.argmax_teacher = _ptr(argmax_student), _ptr(argmax_teacher)
     o.ce_per_seq = _ptr(ce_per_seq)
+    o.topk_overlap, o.kl_topk = _ptr(topk_overlap), _ptr(kl_topk)
+    o.topk_student, o.topk_teacher = _ptr(topk_student), _ptr(topk_teacher)
     return o
 
 
@@ -248,10 +255,10 @@ def olive_score_last_error(ctx) -> int:
 
 
 def olive_score_last_stats(ctx) -> dict:
-    out = (ctypes.c_int64 * 4)()
+    out = (ctypes.c_int64 * 5)()
     _check(load().olive_score_last_stats(ctx, out), "olive_score_last_stats")
     return dict(splits=out[0], flagged=out[1], kernel=("mfma", "generic")[out[2]]
-                if out[2] in (0, 1) else None, grid=out[3])
+                if out[2] in (0, 1) else None, grid=out[3], topk_rescanned=out[4])
 
 
 def olive_score_kernel_times(ctx, n: int) -> list:

@@ -98,7 +98,7 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
                int32_t *__restrict__ err, float *__restrict__ logp_s, float *__restrict__ logp_t,
                int32_t *__restrict__ am_s, int32_t *__restrict__ am_t, float *__restrict__ kl,
                float *__restrict__ kl_rev, float *__restrict__ logp_tmp,
-               int32_t *__restrict__ flagged, int flag_cap) {
+               float *__restrict__ lse_out, int32_t *__restrict__ flagged, int flag_cap) {
     const int lane = threadIdx.x & 63;
     const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     Sched *sched = const_cast<Sched *>(a.sched);
@@ -162,12 +162,14 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
     }
     if (lane != 0) return;
     const float lse_s = a.sS * ss.best + fast_log2(ss.z) * kLn2;
+    if (lse_out) lse_out[j * 2] = lse_s;
     const float lp_s = a.sS * zy_s - lse_s;
     if (logp_s) logp_s[g] = lp_s;
     if (logp_tmp) logp_tmp[g] = lp_s;
     if (am_s) am_s[g] = ss.idx;
     if (HAS_T) {
         const float lse_t = a.sT * st.best + fast_log2(st.z) * kLn2;
+        if (lse_out) lse_out[j * 2 + 1] = lse_t;
         if (logp_t) logp_t[g] = a.sT * zy_t - lse_t;
         if (am_t) am_t[g] = st.idx;
         if (kl) {
@@ -196,13 +198,15 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,
-                          int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st) {
+                          float *lse_out, int32_t *flagged, int flag_cap, int64_t max_rows,
+                          hipStream_t st) {
     if (max_rows <= 0) return hipSuccess;
     dim3 grid((unsigned)((max_rows + 3) / 4));
     int same = same_scale ? 1 : 0;
 #define OLIVE_COMBINE(E_, T_)                                                                \
     combine_kernel<E_, T_><<<grid, 256, 0, st>>>(a, same, targets, err, logp_s, logp_t, am_s, \
-                                                 am_t, kl, kl_rev, logp_tmp, flagged, flag_cap)
+                                                 am_t, kl, kl_rev, logp_tmp, lse_out, flagged,   \
+                                                 flag_cap)
     if (bf16) {
         if (has_t) OLIVE_COMBINE(uint16_t, true);
         else OLIVE_COMBINE(uint16_t, false);

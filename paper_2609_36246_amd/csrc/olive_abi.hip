@@ -1,6 +1,6 @@
 // Host side of the C ABI declared in include/olive_score.h: argument validation,
 // workspace ownership, and the per-call launch sequence
-//   prep -> rowmap -> score (MFMA or generic) -> combine -> [fixup] -> [ce].
+//   prep -> rowmap -> score (MFMA or generic) -> combine -> [fixup] -> [top-K] -> [ce].
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -28,7 +28,12 @@ struct olive_score_ctx {
     void *fx_scratch = nullptr;
     float *wn_s = nullptr, *wn_t = nullptr;     // weight-row L2 norms (rounding bounds)
     int32_t *err = nullptr;
-    bool bf16 = false, has_t = false, mfma_ok = false;
+    // top-K workspace (OLIVE_FLAG_TOPK): normalisers [P][2], merged lists [P][2][16],
+    // the rescan queue [P] and the per-chunk lists of queued rows
+    float *tk_lse = nullptr, *tk_list_v = nullptr;
+    int32_t *tk_list_i = nullptr, *tk_queue = nullptr;
+    void *tk_rescan = nullptr;
+    bool bf16 = false, has_t = false, mfma_ok = false, topk = false;
     int last_kernel = -1, last_grid = 0;
     bool timing = false;
     hipEvent_t ev[2][64] = {};     // start / end of the scoring kernel, ring of 64 calls
@@ -45,7 +50,8 @@ void release(olive_score_ctx *c) {
         for (int i = 0; i < 64; ++i)
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
-                    c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err};
+                    c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
+                    c->tk_lse, c->tk_list_v, c->tk_list_i, c->tk_queue, c->tk_rescan};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -67,7 +73,7 @@ olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE
 olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
                  float *kl, float *kl_rev, int64_t *counts, float *logp_s, float *logp_t,
                  int32_t *am_s, int32_t *am_t, float *ce, hipStream_t st,
-                 bool region_only = false) {
+                 bool region_only = false, TopkOut tk = TopkOut{}) {
     const olive_score_desc &d = ctx->desc;
     if (!b->cu_seqlens || !b->targets || !b->h_student) return OLIVE_E_NULL;
     if (!spans && !b->cut) return OLIVE_E_NULL;
@@ -81,7 +87,9 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     } else if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) {
         return OLIVE_E_RANGE;
     }
-    const bool want_t = kl || kl_rev || logp_t || am_t;
+    const bool topk = tk.any();
+    if (topk && !ctx->topk) return OLIVE_E_UNSUPPORTED;
+    const bool want_t = kl || kl_rev || logp_t || am_t || topk;
     if (want_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
     const bool has_t = want_t;
     const int64_t T = b->total_positions;
@@ -91,6 +99,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     // hidden-state buffers; others take the generic kernel.
     const bool mfma = ctx->mfma_ok && ((uintptr_t)b->h_student & 15) == 0 &&
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
+    if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
 
     olive_status s;
@@ -108,13 +117,14 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     }
     s = check_hip(launch_prep(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
                               mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
-                              fixed_splits, st));
+                              fixed_splits, topk ? 2 : 1, st));
     if (s) return s;
     s = check_hip(launch_rowmap(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
                                 ctx->err,
                                 logp_s,
                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
-                                has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, st));
+                                has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, tk,
+                                st));
     if (s) return s;
 
     ScoreArgs a;
@@ -139,7 +149,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     const int slot = (int)(ctx->n_calls % 64);
     if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
     if (mfma)
-        s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, grid, st));
+        s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, topk, grid, st));
     else
         s = check_hip(launch_score_simple(a, ctx->bf16, has_t, max_units, st));
     if (s) return s;
@@ -151,12 +161,18 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     int32_t *flagged = (am_s || (has_t && am_t)) ? ctx->flagged : nullptr;
     s = check_hip(launch_combine(a, ctx->bf16, has_t, same_scale, b->targets, ctx->err, logp_s,
                                  has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
-                                 has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, flagged,
-                                 ctx->flag_cap, T, st));
+                                 has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp,
+                                 topk ? ctx->tk_lse : nullptr, flagged, ctx->flag_cap, T, st));
     if (s) return s;
     if (flagged) {
         s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
                                         ctx->wn_s, ctx->wn_t, am_s, has_t ? am_t : nullptr, st));
+        if (s) return s;
+    }
+    if (topk) {
+        s = check_hip(launch_topk(a, ctx->bf16, ctx->tk_lse, ctx->tk_list_v, ctx->tk_list_i,
+                                  ctx->tk_queue, (int)ctx->desc.max_positions, ctx->tk_rescan,
+                                  tk.overlap, tk.kl, tk.idx_s, tk.idx_t, T, st));
         if (s) return s;
     }
     if (ce) {
@@ -199,7 +215,8 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (d.d_student > 12288 || d.d_teacher > 12288) return OLIVE_E_UNSUPPORTED;
     if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
     if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
-    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING)) return OLIVE_E_RANGE;
+    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK))
+        return OLIVE_E_RANGE;
     if (!w_student) return OLIVE_E_NULL;
     if (d.d_teacher > 0 && !w_teacher) return OLIVE_E_NULL;
 
@@ -220,6 +237,11 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
                  (d.w_layout == OLIVE_W_DV ||      // borrowed weights: 16-byte rows
                   (((uintptr_t)w_student & 15) == 0 &&
                    (!c->has_t || ((uintptr_t)w_teacher & 15) == 0)));
+    c->topk = (d.flags & OLIVE_FLAG_TOPK) != 0;
+    if (c->topk && (!c->mfma_ok || !c->has_t || d.vocab < 512)) {
+        release(c);
+        return OLIVE_E_UNSUPPORTED;
+    }
     const int esz = c->bf16 ? 2 : 4;
     const int64_t V = d.vocab;
     olive_status s = OLIVE_OK;
@@ -244,7 +266,14 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (!s) s = dev_alloc(&c->rowmap, (size_t)P * sizeof(uint32_t));
     if (!s) s = dev_alloc(&c->seqbuf, (size_t)seqbuf_entries(d.max_seqs) * sizeof(int32_t));
     if (!s) s = dev_alloc(&c->sched, sizeof(Sched));
-    if (!s) s = dev_alloc(&c->part, (size_t)NFIELDS * MAX_SPLITS * c->pstride * sizeof(float));
+    if (!s)
+        s = dev_alloc(&c->part, (size_t)(c->topk ? NFIELDS_TOPK : NFIELDS) * MAX_SPLITS *
+                                    c->pstride * sizeof(float));
+    if (!s && c->topk) s = dev_alloc(&c->tk_lse, (size_t)P * 2 * sizeof(float));
+    if (!s && c->topk) s = dev_alloc(&c->tk_list_v, (size_t)P * 2 * TOPK_K * sizeof(float));
+    if (!s && c->topk) s = dev_alloc(&c->tk_list_i, (size_t)P * 2 * TOPK_K * sizeof(int32_t));
+    if (!s && c->topk) s = dev_alloc(&c->tk_queue, (size_t)P * sizeof(int32_t));
+    if (!s && c->topk) s = dev_alloc(&c->tk_rescan, topk_rescan_bytes(V, (int)P));
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
     if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
     if (!s)
@@ -293,12 +322,17 @@ olive_status olive_kl_masked(olive_score_ctx *ctx, const olive_batch *b, float *
                argmax_teacher, ce_per_seq, (hipStream_t)hip_stream);
 }
 
+static TopkOut topk_of(const olive_score_outputs *out) {
+    return TopkOut{out->topk_overlap, out->kl_topk, out->topk_student, out->topk_teacher};
+}
+
 static olive_status check_outputs(const olive_score_outputs *out) {
     if (!out) return OLIVE_E_NULL;
     if (out->size != (int32_t)sizeof(olive_score_outputs)) return OLIVE_E_RANGE;
     if (out->flags & ~OLIVE_OUT_REGION_ONLY) return OLIVE_E_RANGE;
     if (!out->kl && !out->kl_reverse && !out->counts && !out->logp_student &&
-        !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq)
+        !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq &&
+        !out->topk_overlap && !out->kl_topk && !out->topk_student && !out->topk_teacher)
         return OLIVE_E_NULL;
     return OLIVE_OK;
 }
@@ -309,7 +343,8 @@ olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
     if (olive_status e = check_outputs(out)) return e;
     return run(ctx, b, nullptr, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
-               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0);
+               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0,
+               topk_of(out));
 }
 
 olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
@@ -319,7 +354,8 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
     if (olive_status e = check_outputs(out)) return e;
     return run(ctx, b, spans, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
-               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0);
+               (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0,
+               topk_of(out));
 }
 
 olive_status olive_score_free(olive_score_ctx *ctx) {
@@ -348,6 +384,7 @@ olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out) {
     out[1] = s.n_flagged;
     out[2] = ctx->last_kernel;
     out[3] = ctx->last_grid;
+    out[4] = s.n_topk_queued;
     return OLIVE_OK;
 }
 

@@ -24,6 +24,15 @@ enum Field {
     F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8, F_B = 9,
     NFIELDS = 10
 };
+// Top-K planes (contexts built with OLIVE_FLAG_TOPK only), per model m (0 = S, 1 = T)
+// from F_TK + m * TK_FIELDS: the split's 8 largest raw logits (descending, lower
+// index first among equals), their indices (int32 bits), and a floor that bounds
+// every logit of the split not in the list.
+constexpr int TK_LIST = 8;
+constexpr int TK_FIELDS = 2 * TK_LIST + 1;
+constexpr int F_TK = NFIELDS;
+constexpr int NFIELDS_TOPK = NFIELDS + 2 * TK_FIELDS;
+constexpr int TOPK_K = 16;   // LogProb top-K of the OPD baseline (App. A, Table 3)
 
 // Device-side schedule of one call, written by the preparation kernel.
 struct Sched {
@@ -35,6 +44,17 @@ struct Sched {
     int64_t n_scored;   // in-region valid positions
     int32_t n_flagged;  // rows queued for the near-tie argmax re-decision
     int32_t cu_bad;     // cu_seqlens malformed: nothing is scored
+    int32_t n_topk_queued;  // rows queued for the exact top-K rescan
+    int32_t pad;
+};
+
+// Top-K outputs of a call (null pointers: not requested).
+struct TopkOut {
+    float *overlap;
+    float *kl;
+    int32_t *idx_s;     // [T][TOPK_K]
+    int32_t *idx_t;
+    bool any() const { return overlap || kl || idx_s || idx_t; }
 };
 
 // Bits of the device error word.
@@ -71,20 +91,26 @@ hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int
 hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, bool region_only,
                        int64_t V, int32_t *seqbuf, Sched *sched, int32_t *err, int64_t *counts,
                        int tile_rows, int policy, int n_vtiles, int grid, int fixed_splits,
-                       hipStream_t st);
+                       int min_splits, hipStream_t st);
 hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool region_only,
                          int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
-                         float *logp_tmp, hipStream_t st);
+                         float *logp_tmp, const TopkOut &tk, hipStream_t st);
 hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_t max_units,
                                hipStream_t st);
-hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev, int grid,
-                             hipStream_t st);
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
+                             bool topk, int grid, hipStream_t st);
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,
-                          int32_t *flagged, int flag_cap, int64_t max_rows, hipStream_t st);
+                          float *lse_out, int32_t *flagged, int flag_cap, int64_t max_rows,
+                          hipStream_t st);
+size_t topk_rescan_bytes(int64_t V, int cap);
+hipError_t launch_topk(const ScoreArgs &a, bool bf16, const float *lse, float *list_v,
+                       int32_t *list_i, int32_t *queue, int cap, void *rescan_buf,
+                       float *overlap, float *kl_topk, int32_t *idx_s, int32_t *idx_t,
+                       int64_t max_rows, hipStream_t st);
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
                              void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
                              int32_t *am_t, hipStream_t st);

@@ -68,7 +68,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             SpanArgs sp, int32_t region_only, int32_t *__restrict__ seqbuf,
             Sched *__restrict__ sched, int32_t *__restrict__ err, int64_t *__restrict__ counts,
             int32_t tile_rows, int32_t policy, int32_t n_vtiles, int32_t grid,
-            int32_t fixed_splits) {
+            int32_t fixed_splits, int32_t min_splits) {
     __shared__ int s_bad, s_badoff;
     __shared__ int s_scan[PREP_THREADS];
     __shared__ long long s_red[PREP_THREADS];
@@ -103,6 +103,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             atomicOr(err, ERR_CU);
             sched->t_valid = 0; sched->n_ptiles = 0; sched->n_splits = 1; sched->n_units = 0;
             sched->n_scored = 0; sched->n_flagged = 0; sched->cu_bad = 1;
+            sched->n_topk_queued = 0;
             if (counts) { counts[0] = 0; counts[1] = 0; }
         }
         return;
@@ -178,7 +179,8 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             // Minimise (rounds of the persistent grid) x (vocabulary tiles per split).
             long long best = -1;
             int smax = n_vtiles < MAX_SPLITS ? n_vtiles : MAX_SPLITS;
-            for (int s = 1; s <= smax; ++s) {
+            const int smin = min_splits < smax ? min_splits : smax;
+            for (int s = smin; s <= smax; ++s) {
                 long long units = (long long)n_p * s;
                 long long rounds = (units + grid - 1) / grid;
                 long long per = (n_vtiles + s - 1) / s;
@@ -195,6 +197,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
         sched->n_units = n_p * ns;
         sched->n_scored = scored;
         sched->n_flagged = 0;
+        sched->n_topk_queued = 0;
         sched->cu_bad = 0;
         if (counts) { counts[0] = scored; counts[1] = valid; }
     }
@@ -210,7 +213,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
               uint32_t *__restrict__ rowmap, float *__restrict__ logp_s,
               float *__restrict__ logp_t, int32_t *__restrict__ am_s, int32_t *__restrict__ am_t,
               float *__restrict__ kl, float *__restrict__ kl_rev,
-              float *__restrict__ logp_tmp) {
+              float *__restrict__ logp_tmp, TopkOut tk) {
     const int32_t *cvalid = seqbuf;
     const int32_t *vl_eff = seqbuf + (B + 1);
     const int32_t *cut_eff = seqbuf + 2 * (B + 1);
@@ -239,6 +242,12 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (kl) kl[g] = qnan;
             if (kl_rev) kl_rev[g] = qnan;
             if (logp_tmp) logp_tmp[g] = qnan;
+            if (tk.overlap) tk.overlap[g] = qnan;
+            if (tk.kl) tk.kl[g] = qnan;
+            for (int e = 0; e < TOPK_K; ++e) {
+                if (tk.idx_s) tk.idx_s[g * TOPK_K + e] = -1;
+                if (tk.idx_t) tk.idx_t[g * TOPK_K + e] = -1;
+            }
             continue;
         }
         const int vl = vl_eff[b];
@@ -265,6 +274,12 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (kl) kl[g] = 0.f;
             if (kl_rev) kl_rev[g] = 0.f;
             if (logp_tmp) logp_tmp[g] = 0.f;
+            if (tk.overlap) tk.overlap[g] = 0.f;
+            if (tk.kl) tk.kl[g] = 0.f;
+            for (int e = 0; e < TOPK_K; ++e) {
+                if (tk.idx_s) tk.idx_s[g * TOPK_K + e] = -1;
+                if (tk.idx_t) tk.idx_t[g * TOPK_K + e] = -1;
+            }
         }
     }
 }
@@ -349,12 +364,13 @@ static SpanArgs span_args(const olive_spans *s) {
 hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, bool region_only,
                        int64_t V, int32_t *seqbuf, Sched *sched, int32_t *err, int64_t *counts,
                        int tile_rows, int policy, int n_vtiles, int grid, int fixed_splits,
-                       hipStream_t st) {
+                       int min_splits, hipStream_t st) {
     (void)V;
     prep_kernel<<<1, PREP_THREADS, 0, st>>>(b.cu_seqlens, b.cut, b.valid_len, b.num_seqs,
                                             b.total_positions, b.region, span_args(spans),
                                             region_only ? 1 : 0, seqbuf, sched, err, counts,
-                                            tile_rows, policy, n_vtiles, grid, fixed_splits);
+                                            tile_rows, policy, n_vtiles, grid, fixed_splits,
+                                            min_splits);
     return hipGetLastError();
 }
 
@@ -362,7 +378,7 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool re
                          int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
-                         float *logp_tmp, hipStream_t st) {
+                         float *logp_tmp, const TopkOut &tk, hipStream_t st) {
     (void)V; (void)err;
     int64_t T = b.total_positions;
     int64_t blocks = (T + 255) / 256;
@@ -372,7 +388,7 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool re
                                                     span_args(spans), region_only ? 1 : 0, seqbuf,
                                                     sched, rowmap,
                                                     logp_s, logp_t, am_s,
-                                                    am_t, kl, kl_rev, logp_tmp);
+                                                    am_t, kl, kl_rev, logp_tmp, tk);
     return hipGetLastError();
 }
 

@@ -95,6 +95,9 @@ __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory")
 // with lgkmcnt(0)); completion is ordered by the explicit vmcnt waits and barriers of
 // the pipeline. m0 is written here only: the kernel has no other m0 user.
 __device__ __forceinline__ void dma16(const char *g, uint32_t la) {
+    // The address is wave-uniform by construction; readfirstlane makes that explicit
+    // when register pressure has moved it to a VGPR.
+    la = __builtin_amdgcn_readfirstlane(la);
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
     // s_nop: one wait state between the m0 write and the DMA that reads it.
@@ -117,7 +120,15 @@ struct Run {                // running statistics of one position column
     int idx;
 };
 
-template <bool HAS_T, bool SAME, bool REV>
+// The 4 largest logits (and indices) a lane has seen of one position column, in
+// (value descending, index ascending) order; kMasked marks empty slots. Everything
+// the lane has dropped is <= v[3].
+struct Top4 {
+    float v[4];
+    int i[4];
+};
+
+template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 struct Kernel {
     // Addresses of the 12 DMAs of one step (8 W, 4 H) of model `m`, K step kk,
     // vocabulary tile vt, into ring stage `st`. DMA i of a wave fills stage rows
@@ -350,7 +361,8 @@ struct Kernel {
     static __device__ __forceinline__ void fold(const floatx16 (&accS)[4][2],
                                                 const floatx16 (&accT)[4][2], Run (&RS)[2],
                                                 Run (&RT)[2], float (&A)[2], float (&Bq)[2],
-                                                const ScoreArgs &a, int vbase) {
+                                                Top4 (&KS)[2], Top4 (&KT)[2], const ScoreArgs &a,
+                                                int vbase) {
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -366,7 +378,60 @@ struct Kernel {
                 fold_block<HAS_T && REV>(zs, RS[cb], Bq[cb], zt, a.cS, a.sS, a.sT, vbase + vb * 32);
                 if (HAS_T)
                     fold_block<true>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
+                if (TOPK) {
+                    topk_block(zs, KS[cb], vbase + vb * 32);
+                    topk_block(zt, KT[cb], vbase + vb * 32);
+                }
             }
+    }
+
+    // Insert (x, xi) into a descending top list; strict comparisons keep the earlier
+    // (lower-index) entry first among equal values, as entries arrive in index order.
+    template <int N>
+    static __device__ __forceinline__ void topk_insert(float (&v)[N], int (&ix)[N], float x,
+                                                       int xi) {
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            const bool gt = x > v[j];
+            const float nv = gt ? x : v[j];
+            const int ni = gt ? xi : ix[j];
+            x = gt ? v[j] : x;
+            xi = gt ? ix[j] : xi;
+            v[j] = nv;
+            ix[j] = ni;
+        }
+    }
+
+    // The same for entries of other lanes: (value descending, index ascending) order by
+    // comparison. Returns the value pushed off the end.
+    template <int N>
+    static __device__ __forceinline__ float topk_insert_lex(float (&v)[N], int (&ix)[N], float x,
+                                                           int xi) {
+#pragma unroll
+        for (int j = 0; j < N; ++j) {
+            const bool gt = x > v[j] || (x == v[j] && xi < ix[j]);
+            const float nv = gt ? x : v[j];
+            const int ni = gt ? xi : ix[j];
+            x = gt ? v[j] : x;
+            xi = gt ? ix[j] : xi;
+            v[j] = nv;
+            ix[j] = ni;
+        }
+        return x;
+    }
+
+    // Offer one 32-row block (16 values per lane, rows in increasing index order) to a
+    // lane's top-4; skipped when no value of the block beats the current 4th.
+    static __device__ __forceinline__ void topk_block(const float (&z)[16], Top4 &K,
+                                                      int vcode0) {
+        float bm = z[0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) bm = max2(bm, z[r]);
+        if (bm > K.v[3]) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                topk_insert<4>(K.v, K.i, z[r], vcode0 + 8 * (r >> 2) + (r & 3));
+        }
     }
 
     static __device__ __forceinline__ void zero_acc(floatx16 (&accS)[4][2],
@@ -387,7 +452,7 @@ struct Kernel {
         x.best = a.best; x.sec = a.sec; x.idx = a.idx; x.z = a.z;
     }
 
-    static __device__ void run(ScoreArgs a) {
+    static __device__ __forceinline__ void run(ScoreArgs a) {
         const int t_valid = a.sched->t_valid;
         const int n_p = a.sched->n_ptiles;
         const int ns = a.sched->n_splits;
@@ -446,6 +511,14 @@ struct Kernel {
 
             Run RS[2], RT[2];
             float AA[2] = {0.f, 0.f}, BB[2] = {0.f, 0.f};
+            Top4 KS[2], KT[2];
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    KS[cb].v[e] = kMasked; KS[cb].i[e] = 0x7fffffff;
+                    KT[cb].v[e] = kMasked; KT[cb].i[e] = 0x7fffffff;
+                }
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 RS[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
@@ -515,7 +588,7 @@ struct Kernel {
                 OLIVE_STEPS(accS, nS)
                 if (HAS_T) OLIVE_STEPS(accT, nT)
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
-                fold(accS, accT, RS, RT, AA, BB, a, vbase);
+                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, vbase);
             }
 #undef OLIVE_STEPS
 
@@ -533,9 +606,32 @@ struct Kernel {
                     merge_run(RT[cb], AA[cb], q2, qa, a.cT);
                 }
             }
+            // Top-K: lanes l and l+32 combine their top-4 lists into a top-8 (nothing is
+            // dropped); the floor bounds everything either lane dropped.
+            float Q8v[2][2][8], Qfl[2][2];
+            int Q8i[2][2][8];
+            if (TOPK) {
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+#pragma unroll
+                    for (int cb = 0; cb < 2; ++cb) {
+                        const Top4 &K = m ? KT[cb] : KS[cb];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            Q8v[m][cb][e] = K.v[e]; Q8i[m][cb][e] = K.i[e];
+                            Q8v[m][cb][4 + e] = kMasked; Q8i[m][cb][4 + e] = 0x7fffffff;
+                        }
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb], __shfl_xor(K.v[e], 32),
+                                               __shfl_xor(K.i[e], 32));
+                        Qfl[m][cb] = max2(K.v[3], __shfl_xor(K.v[3], 32));
+                    }
+            }
             // Merge the two vocabulary halves (wv = 1 into wv = 0) through LDS, once
             // the trailing prefetches into the stages have landed.
             float *xs = (float *)g_ring;   // [wt][cb][l32][10]
+            float *xk = xs + 2 * 2 * 32 * 10;   // top-K: [wt][cb][l32][model][17]
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
             compiler_fence();
             __builtin_amdgcn_s_barrier();
@@ -548,6 +644,18 @@ struct Kernel {
                     o[3] = RS[cb].z;
                     o[4] = RT[cb].best; o[5] = RT[cb].sec; o[6] = __int_as_float(RT[cb].idx);
                     o[7] = RT[cb].z; o[8] = AA[cb]; o[9] = BB[cb];
+                    if (TOPK) {
+#pragma unroll
+                        for (int m = 0; m < 2; ++m) {
+                            float *q = xk + (((L.wt * 2 + cb) * 32 + L.l32) * 2 + m) * 17;
+#pragma unroll
+                            for (int e = 0; e < 8; ++e) {
+                                q[e] = Q8v[m][cb][e];
+                                q[8 + e] = __int_as_float(Q8i[m][cb][e]);
+                            }
+                            q[16] = Qfl[m][cb];
+                        }
+                    }
                 }
             }
             compiler_fence();
@@ -577,6 +685,29 @@ struct Kernel {
                             P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT[cb].z;
                             P[(F_A * MAX_SPLITS + s) * ps + j] = AA[cb];
                             if (REV) P[(F_B * MAX_SPLITS + s) * ps + j] = BB[cb];
+                            if (TOPK) {
+                                // the other half's top-8 into this one's: the 8 dropped
+                                // raise the floor
+#pragma unroll
+                                for (int m = 0; m < 2; ++m) {
+                                    const float *q =
+                                        xk + (((L.wt * 2 + cb) * 32 + L.l32) * 2 + m) * 17;
+                                    float fl = max2(Qfl[m][cb], q[16]);
+#pragma unroll
+                                    for (int e = 0; e < 8; ++e)
+                                        fl = max2(fl, topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb],
+                                                                        q[e],
+                                                                        __float_as_int(q[8 + e])));
+#pragma unroll
+                                    for (int e = 0; e < 8; ++e) {
+                                        P[((F_TK + m * TK_FIELDS + e) * MAX_SPLITS + s) * ps + j] =
+                                            Q8v[m][cb][e];
+                                        P[((F_TK + m * TK_FIELDS + 8 + e) * MAX_SPLITS + s) * ps +
+                                          j] = __int_as_float(Q8i[m][cb][e]);
+                                    }
+                                    P[((F_TK + m * TK_FIELDS + 16) * MAX_SPLITS + s) * ps + j] = fl;
+                                }
+                            }
                         }
                     }
                 }
@@ -587,26 +718,28 @@ struct Kernel {
     }
 };
 
-template <bool HAS_T, bool SAME, bool REV>
+template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_mfma_kernel(ScoreArgs a) {
-    Kernel<HAS_T, SAME, REV>::run(a);
+    Kernel<HAS_T, SAME, REV, TOPK>::run(a);
 }
 
-hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev, int grid,
-                             hipStream_t st) {
+hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
+                             bool topk, int grid, hipStream_t st) {
     if (grid <= 0) return hipSuccess;
+#define OLIVE_SCORE(S_, R_, K_) score_mfma_kernel<true, S_, R_, K_><<<grid, 256, 0, st>>>(a)
     if (has_t) {
         if (same_scale) {
-            if (rev) score_mfma_kernel<true, true, true><<<grid, 256, 0, st>>>(a);
-            else score_mfma_kernel<true, true, false><<<grid, 256, 0, st>>>(a);
+            if (topk) { if (rev) OLIVE_SCORE(true, true, true); else OLIVE_SCORE(true, false, true); }
+            else { if (rev) OLIVE_SCORE(true, true, false); else OLIVE_SCORE(true, false, false); }
         } else {
-            if (rev) score_mfma_kernel<true, false, true><<<grid, 256, 0, st>>>(a);
-            else score_mfma_kernel<true, false, false><<<grid, 256, 0, st>>>(a);
+            if (topk) { if (rev) OLIVE_SCORE(false, true, true); else OLIVE_SCORE(false, false, true); }
+            else { if (rev) OLIVE_SCORE(false, true, false); else OLIVE_SCORE(false, false, false); }
         }
     } else {
-        score_mfma_kernel<false, true, false><<<grid, 256, 0, st>>>(a);
+        score_mfma_kernel<false, true, false, false><<<grid, 256, 0, st>>>(a);
     }
+#undef OLIVE_SCORE
     return hipGetLastError();
 }
 

@@ -2,9 +2,12 @@
 oracle on the same seeded workload, and compare them at the acceptance tolerances.
 
 Tolerances: per-token log-prob within 2e-3 absolute; per-position KL (either
-direction) within 1e-3 + 1e-3 |KL|; masked counts, valid counts and greedy argmax
-bit-exact; Eq. 1's
-per-sequence loss within 1e-3 relative (plus 1e-3 absolute for tiny sums).
+direction, and the top-K KL) within 1e-3 + 1e-3 |KL|; masked counts, valid counts and
+greedy argmax bit-exact; Eq. 1's per-sequence loss within 1e-3 relative (plus 1e-3
+absolute for tiny sums). Top-K sets: equal to the oracle's wherever the fp64 logits
+separate the 16th from the 17th entry by more than twice the fp32 rounding bound
+of a logit, and otherwise a valid top-16 under logits moved by at most that bound;
+the overlap ratio exact on the returned sets.
 """
 import math
 import sys
@@ -35,18 +38,28 @@ def to_np(t):
     return t.detach().cpu().numpy()
 
 
+TOPK_OUTPUTS = ("overlap", "kl_topk", "tk_s", "tk_t")
+
+
 def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
             outputs=("kl", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
-            poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1, out_flags=0):
-    """Score a workload on the GPU; returns numpy outputs (and stats)."""
+            poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1, out_flags=0,
+            topk_ctx=None):
+    """Score a workload on the GPU; returns numpy outputs (and stats).
+
+    Top-K outputs ("overlap", "kl_topk", "tk_s", "tk_t") make the context reserve
+    the top-K workspace (topk_ctx overrides that choice)."""
     dev = wl["h_student"].device
     spec = wl["spec"]
     T = wl["total_positions"]
     B = wl["cu_seqlens"].shape[0] - 1
     own = ctx is None
     if own:
+        if topk_ctx is None:
+            topk_ctx = any(k in outputs for k in TOPK_OUTPUTS)
         flags = (L.OLIVE_FLAG_SIMPLE_KERNEL if simple else 0) | \
-                (L.OLIVE_FLAG_KERNEL_TIMING if timing else 0)
+                (L.OLIVE_FLAG_KERNEL_TIMING if timing else 0) | \
+                (L.OLIVE_FLAG_TOPK if topk_ctx else 0)
         desc = L.make_desc(spec.vocab, spec.d_student, 0 if student_only else spec.d_teacher,
                            L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
                            wl["scale_student"], wl["scale_teacher"], max_positions=T,
@@ -71,16 +84,24 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
     out["am_t"] = i32() if "am_t" in outputs and not student_only else None
     out["ce"] = torch.full((B,), fill, dtype=torch.float32, device=dev) \
         if "ce" in outputs and not student_only else None
+    out["overlap"] = f32() if "overlap" in outputs else None
+    out["kl_topk"] = f32() if "kl_topk" in outputs else None
+    for k in ("tk_s", "tk_t"):
+        out[k] = torch.full((T, L.OLIVE_TOPK), -7, dtype=torch.int32, device=dev) \
+            if k in outputs else None
+    any_topk = any(out[k] is not None for k in TOPK_OUTPUTS)
     spans = wl.get("spans") if region == L.OLIVE_REGION_SPANS else None
     batch = L.make_batch(wl["cu_seqlens"], None if spans is not None else wl["cut"],
                          wl["targets"], wl["h_student"],
                          None if student_only else wl["h_teacher"], wl["valid_len"], region)
     for _ in range(repeat):
-        if spans is not None or out["kl_rev"] is not None or out_flags:
+        if spans is not None or out["kl_rev"] is not None or out_flags or any_topk:
             o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
                                logp_student=out["logp_s"], logp_teacher=out["logp_t"],
                                argmax_student=out["am_s"], argmax_teacher=out["am_t"],
-                               ce_per_seq=out["ce"], flags=out_flags)
+                               ce_per_seq=out["ce"], topk_overlap=out["overlap"],
+                               kl_topk=out["kl_topk"], topk_student=out["tk_s"],
+                               topk_teacher=out["tk_t"], flags=out_flags)
             if spans is not None:
                 sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
                 L.olive_score_batch_spans(ctx, batch, sp, o)
@@ -220,3 +241,113 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
     say("%s parity ok on %d rows; worst %s" % (label, sel.size,
                                                 {k: "%.2e" % v for k, v in worst.items()}))
     return r
+
+
+def logit_error_bound(h_rows, w, scale):
+    """Per row, a bound on |fp32 logit - exact logit| over the vocabulary: products of
+    bf16 values are exact in fp32 and a d-term fp32 sum errs by at most
+    d 2^-24 sum |h_k w_k| <= d 2^-24 |h| |w_v| (taken with a 2x margin)."""
+    h = np.asarray(h_rows, dtype=np.float64)
+    wn = np.sqrt((np.asarray(w, dtype=np.float64) ** 2).sum(axis=0)).max()
+    d = h.shape[1]
+    return scale * d * 2.0 ** -23 * np.sqrt((h ** 2).sum(axis=1)) * wn
+
+
+def check_topk_set(got, z, delta, label):
+    """got: 16 vocabulary indices in rank order; z: exact (fp64) logits of the row;
+    delta: the rounding bound of one logit. Returns True when the oracle's set is
+    unique at this resolution (then got must equal it in rank order wherever the
+    ranking is unique); else checks got is a valid top-16 of logits moved by <= delta."""
+    K = len(got)
+    want = O.topk_set(z, K)
+    zs = z[want]
+    rest = np.ones(len(z), dtype=bool)
+    rest[want] = False
+    z17 = z[rest].max() if rest.any() else -np.inf
+    assert len(set(got.tolist())) == K and got.min() >= 0 and got.max() < len(z), \
+        (label, got)
+    gz = z[got]
+    # every returned entry at least as large as every other, up to 2 delta
+    others = np.ones(len(z), dtype=bool)
+    others[got] = False
+    top_other = z[others].max() if others.any() else -np.inf
+    assert gz.min() >= top_other - 2 * delta, (label, gz.min(), top_other, delta)
+    # rank order: non-increasing up to 2 delta, ties (within 2 delta) in any order
+    assert np.all(gz[:-1] >= gz[1:] - 2 * delta), (label, gz)
+    unique = (zs[-1] - z17) > 2 * delta
+    if unique:
+        assert set(got.tolist()) == set(want.tolist()), (label, got, want)
+        # where neighbouring values are separated, the order is the oracle's
+        sep = np.diff(zs) < -2 * delta
+        for k in range(K):
+            lo_ok = k == 0 or sep[k - 1]
+            hi_ok = k == K - 1 or sep[k]
+            if lo_ok and hi_ok:
+                assert got[k] == want[k], (label, k, got, want)
+    return unique
+
+
+def compare_topk(hip, wl, region=O.REGION_TEACHER, rows=None, label="", region_only=False,
+                 max_ambiguous_frac=0.3):
+    """Top-K outputs against the oracle: fixed values at unscored positions, sets
+    valid under the logit rounding bound (equal to the oracle's where unique),
+    overlap exact on the sets and equal to the oracle's where both sets are unique,
+    kl_topk at the KL tolerance against the oracle's (on the returned teacher set
+    where the oracle's is not unique)."""
+    m = masks_of(wl, region)
+    valid, inr = m["valid"], m["in_region"]
+    T = len(valid)
+    K = L.OLIVE_TOPK
+    uns = ~inr
+    if "overlap" in hip:
+        assert np.all(hip["overlap"][uns] == 0.0) and not np.any(np.signbit(hip["overlap"][uns]))
+    if "kl_topk" in hip:
+        assert np.all(hip["kl_topk"][uns] == 0.0) and not np.any(np.signbit(hip["kl_topk"][uns]))
+    for k in ("tk_s", "tk_t"):
+        if k in hip:
+            assert np.all(hip[k][uns] == -1), (label, k)
+    sel = np.nonzero(inr)[0] if rows is None else np.asarray(rows)
+    sel = sel[inr[sel]]
+    if sel.size == 0:
+        return
+    idx = torch.from_numpy(sel).to(wl["h_student"].device)
+    hs, ht = to_np(wl["h_student"][idx]), to_np(wl["h_teacher"][idx])
+    ws = to_np(wl["w_student"]).astype(np.float64)
+    wt = to_np(wl["w_teacher"]).astype(np.float64)
+    sS, sT = wl["scale_student"], wl["scale_teacher"]
+    ds = logit_error_bound(hs, ws, sS)
+    dt = logit_error_bound(ht, wt, sT)
+    n_amb = 0
+    worst = 0.0
+    t0 = time.time()
+    for r0 in range(0, sel.size, 64):
+        zs_all = O.project(hs[r0:r0 + 64], ws, sS)
+        zt_all = O.project(ht[r0:r0 + 64], wt, sT)
+        for i in range(zs_all.shape[0]):
+            g = int(sel[r0 + i])
+            zs, zt = zs_all[i], zt_all[i]
+            tag = "%s row %d" % (label, g)
+            us = check_topk_set(hip["tk_s"][g], zs, ds[r0 + i], tag + " S") \
+                if "tk_s" in hip else True
+            ut = check_topk_set(hip["tk_t"][g], zt, dt[r0 + i], tag + " T") \
+                if "tk_t" in hip else True
+            n_amb += (not us) or (not ut)
+            set_s = hip["tk_s"][g] if "tk_s" in hip else None
+            set_t = hip["tk_t"][g] if "tk_t" in hip else None
+            if "overlap" in hip:
+                if us and ut:
+                    want = O.topk_overlap(O.topk_set(zs, K), O.topk_set(zt, K), K)
+                    assert hip["overlap"][g] == want, (tag, hip["overlap"][g], want)
+                if set_s is not None and set_t is not None:
+                    own = len(set(set_s.tolist()) & set(set_t.tolist())) / K
+                    assert hip["overlap"][g] == own, (tag, hip["overlap"][g], own)
+            if "kl_topk" in hip:
+                st, tt = O.log_softmax_stats(zs), O.log_softmax_stats(zt)
+                tset = O.topk_set(zt, K) if ut or set_t is None else set_t
+                want = O.kl_topk(zt, tt["lse"], zs, st["lse"], tset)
+                err = abs(hip["kl_topk"][g] - want)
+                worst = max(worst, err)
+                assert err <= KL_ATOL + KL_RTOL * abs(want), (tag, hip["kl_topk"][g], want)
+    assert n_amb <= max_ambiguous_frac * sel.size + 1, (label, n_amb, sel.size)
+    say("%s top-K ok on %d rows (%d with a near-tie at the 16th entry); worst kl_topk err "
+        "%.2e; oracle %.1fs" % (label, sel.size, n_amb, worst, time.time() - t0))

@@ -54,16 +54,42 @@ def test_status_strings(lib):
     assert "unknown" in L.olive_status_string(99)
 
 
-def test_struct_layouts_match_header():
-    assert ctypes.sizeof(L.olive_score_desc) == 48
-    assert L.olive_score_desc.max_positions.offset == 32
-    assert ctypes.sizeof(L.olive_batch) == 64
-    assert L.olive_batch.h_teacher.offset == 56
-    assert ctypes.sizeof(L.olive_score_outputs) == 72
-    assert L.olive_score_outputs.kl.offset == 8
-    assert L.olive_score_outputs.ce_per_seq.offset == 64
-    assert ctypes.sizeof(L.olive_spans) == 24
-    assert L.olive_spans.spans.offset == 16
+STRUCTS = ("olive_score_desc", "olive_batch", "olive_score_outputs", "olive_spans")
+
+
+def header_layouts(tmp_path):
+    """sizeof and offsetof of every field of the public structs, from the header
+    itself compiled by the host C compiler."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "olive_score.h"',
+             "int main(void) {"]
+    for name in STRUCTS:
+        lines.append('printf("%s __sizeof__ %%zu\\n", sizeof(%s));' % (name, name))
+        for f, _ in getattr(L, name)._fields_:
+            lines.append('printf("%s %s %%zu\\n", offsetof(%s, %s));' % (name, f, name, f))
+    lines += ["return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o",
+                    str(exe)], check=True)
+    out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout
+    return {tuple(l.split()[:2]): int(l.split()[2]) for l in out.splitlines()}
+
+
+def test_struct_layouts_match_header(tmp_path):
+    got = header_layouts(tmp_path)
+    for name in STRUCTS:
+        st = getattr(L, name)
+        assert got[(name, "__sizeof__")] == ctypes.sizeof(st), name
+        for f, _ in st._fields_:
+            assert got[(name, f)] == getattr(st, f).offset, (name, f)
+    assert ctypes.sizeof(L.olive_score_outputs) == 104
+    assert L.olive_score_outputs.topk_teacher.offset == 96
 
 
 def _init(desc, ws=1, wt=1):

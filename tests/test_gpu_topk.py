@@ -1,0 +1,194 @@
+"""GPU parity of the top-K statistics (K = 16) against the fp64 oracle: the top-K
+overlap ratio of Sec. 4.1, the top-16 KL of App. A (Table 3) and the two index sets.
+
+The sets come from the scoring pass's per-split lists; rows whose lists cannot
+prove their set go through an exact rescan. Crafted weights drive every row through
+that rescan and through exact ties at the 16th entry; the usual outputs of a call
+are checked unchanged by the top-K requests.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import olive_oracle as O
+from paper_2609_36246_amd import _lib as L
+from paper_2609_36246_amd import workloads as W
+from tests.gpu_harness import compare, compare_topk, run_hip, say, stratified_rows
+
+pytestmark = pytest.mark.gpu
+
+BASE = ("kl", "kl_rev", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce")
+TOPK = ("overlap", "kl_topk", "tk_s", "tk_t")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def gpu():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    L.load()
+
+
+def custom(name, seed=0, **kw):
+    spec = W.custom_spec(name=name, **kw)
+    return W.make_workload(name, seed, device="cuda", spec=spec)
+
+
+CASES = {
+    "ragged_v1000": dict(num_seqs=3, ragged_len=(40, 300), vocab=1000, d_student=128,
+                         d_teacher=256, cut_rule=("frac", 0.1, 0.9), eos=True),
+    "multi_tile": dict(num_seqs=5, ragged_len=(700, 1300), vocab=5000, d_student=256,
+                       d_teacher=128, logit_scale=4.0, target_source="student",
+                       cut_rule=("frac", 0.1, 0.9)),
+    "narrow_k": dict(num_seqs=2, ragged_len=(100, 250), vocab=700, d_student=64,
+                     d_teacher=192, cut_rule=("frac", 0.2, 0.8)),
+    "even_v": dict(num_seqs=2, seq_len=200, vocab=2048, d_student=384, d_teacher=512,
+                   target_source="teacher", cut_rule=("abs", 1, 199), outlier_frac=0.05,
+                   outlier_mul=8.0),
+    # five vocabulary tiles: the split count leaves a short last split
+    "v1200": dict(num_seqs=2, seq_len=130, vocab=1200, d_student=128, d_teacher=128,
+                  logit_scale=2.0, cut_rule=("abs", 1, 129)),
+}
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_topk_full(case):
+    say("top-K full", case)
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl, outputs=BASE + TOPK)
+    assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    assert hip["stats"]["splits"] >= 2
+    say(case, "stats", hip["stats"])
+    compare(hip, wl, label="topk-" + case)
+    compare_topk(hip, wl, label="topk-" + case)
+
+
+def test_topk_requests_leave_the_other_outputs_unchanged():
+    say("top-K variant vs plain variant")
+    wl = custom("multi_tile", **CASES["multi_tile"])
+    a = run_hip(wl, outputs=BASE)
+    b = run_hip(wl, outputs=BASE + TOPK)
+    for k in ("kl", "kl_rev", "logp_s", "logp_t", "am_s", "am_t", "ce", "counts"):
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+
+
+@pytest.mark.parametrize("region", [O.REGION_STUDENT, O.REGION_ALL])
+def test_topk_regions(region):
+    say("top-K region", region)
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    hip = run_hip(wl, region=region, outputs=BASE + TOPK)
+    compare(hip, wl, region=region, label="topk-region%d" % region)
+    compare_topk(hip, wl, region=region, label="topk-region%d" % region)
+
+
+def test_topk_region_only_and_spans():
+    say("top-K with region-only outputs and span masks")
+    wl = custom("turns", num_seqs=3, vocab=1000, d_student=128, d_teacher=256,
+                target_source="teacher", turns=(4, 16, 3, 2, 4, 24, 4, 40))
+    for flags in (0, L.OLIVE_OUT_REGION_ONLY):
+        hip = run_hip(wl, region=O.REGION_SPANS, outputs=BASE + TOPK, out_flags=flags)
+        assert hip["err"] == 0
+        compare(hip, wl, region=O.REGION_SPANS, label="topk-turns-%d" % flags,
+                region_only=bool(flags))
+        compare_topk(hip, wl, region=O.REGION_SPANS, label="topk-turns-%d" % flags)
+
+
+def test_topk_partial_requests():
+    say("top-K outputs one at a time")
+    wl = custom("narrow_k", **CASES["narrow_k"])
+    full = run_hip(wl, outputs=("counts", "logp_s") + TOPK)
+    for k in TOPK:
+        one = run_hip(wl, outputs=("logp_s", k))
+        np.testing.assert_array_equal(one[k], full[k], err_msg=k)
+
+
+def test_ties_and_clustered_sets_go_through_the_exact_rescan():
+    """Teacher: 32 identical weight columns far above the rest, so the top-16 is a
+    tie broken by the lower index (columns 40..55). Student: 41 columns in one
+    vocabulary tile with distinct, increasing multiples of one direction, so one
+    split holds the whole top-16 and every row needs the rescan. V = 9000 spans
+    three rescan chunks with a ragged last one."""
+    say("top-K ties and rescan")
+    wl = custom("tie", num_seqs=2, seq_len=90, vocab=9000, d_student=128, d_teacher=128,
+                cut_rule=("abs", 1, 89))
+    ws, wt = wl["w_student"], wl["w_teacher"]      # [d, V]
+    hs, ht = wl["h_student"], wl["h_teacher"]      # [T, d]
+    wt[0, :] = 0
+    wt[:, 40:72] = 0
+    wt[0, 40:72] = 1.0
+    ht[:, 0] = 1024.0
+    ws[0, :] = 0
+    ws[:, 300:341] = 0
+    mult = torch.tensor([1.0 + j / 64.0 for j in range(41)], dtype=torch.float32)
+    ws[0, 300:341] = mult.to(ws.dtype).to(ws.device)
+    hs[:, 0] = 1024.0
+    hip = run_hip(wl, outputs=BASE + TOPK)
+    say("tie stats", hip["stats"])
+    m = O.masks(*[t.cpu().numpy() if t is not None else None
+                  for t in (wl["cu_seqlens"], wl["cut"], wl["valid_len"])],
+                O.REGION_TEACHER)
+    rows = np.nonzero(m["in_region"])[0]
+    assert hip["stats"]["topk_rescanned"] == rows.size
+    want_t = np.arange(40, 56)
+    want_s = 340 - np.arange(16)
+    for g in rows:
+        np.testing.assert_array_equal(hip["tk_t"][g], want_t)
+        np.testing.assert_array_equal(hip["tk_s"][g], want_s)
+    assert np.all(hip["overlap"][rows] == 0.0)
+    compare(hip, wl, label="tie")
+    compare_topk(hip, wl, label="tie", max_ambiguous_frac=1.0)
+
+
+def test_topk_on_long_rollout_sampled():
+    say("top-K, long_rollout sampled")
+    wl = W.make_workload("long_rollout", 0, device="cuda")
+    hip = run_hip(wl, outputs=BASE + TOPK)
+    say("long_rollout stats", hip["stats"])
+    assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    rows = stratified_rows(wl, n_random=64)
+    compare(hip, wl, rows=rows, label="topk-long_rollout")
+    compare_topk(hip, wl, rows=rows, label="topk-long_rollout")
+    del wl
+    torch.cuda.empty_cache()
+
+
+def test_topk_needs_the_flag_and_the_mfma_path():
+    say("top-K argument errors")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    dev = wl["h_student"].device
+    T = wl["total_positions"]
+    ov = torch.zeros(T, dtype=torch.float32, device=dev)
+    # a context without the top-K workspace refuses top-K outputs
+    res = run_hip(wl, outputs=("logp_s",), keep_ctx=True, topk_ctx=False)
+    ctx = res["ctx"]
+    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
+                         wl["h_teacher"], wl["valid_len"], L.OLIVE_REGION_TEACHER)
+    o = L.make_outputs(topk_overlap=ov)
+    assert L.olive_score_batch(ctx, batch, o, check=False) == L.OLIVE_E_UNSUPPORTED
+    L.olive_score_free(ctx)
+    # hidden states off 16-byte alignment cannot take the MFMA path the lists come from
+    res = run_hip(wl, outputs=("logp_s", "overlap"), keep_ctx=True)
+    ctx = res["ctx"]
+    d = wl["spec"].d_student
+    hs_off = torch.empty(T * d + 8, dtype=wl["h_student"].dtype, device=dev)[1:1 + T * d]
+    hs_off = hs_off.view(T, d)
+    hs_off.copy_(wl["h_student"])
+    batch = L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], hs_off,
+                         wl["h_teacher"], wl["valid_len"], L.OLIVE_REGION_TEACHER)
+    assert L.olive_score_batch(ctx, batch, o, check=False) == L.OLIVE_E_UNSUPPORTED
+    L.olive_score_free(ctx)
+    # contexts the MFMA kernel does not apply to, or with V < 512, refuse the flag
+    spec = wl["spec"]
+    for kw in (dict(dtype=L.OLIVE_F32), dict(vocab=300), dict(flags=L.OLIVE_FLAG_TOPK |
+                                                               L.OLIVE_FLAG_SIMPLE_KERNEL)):
+        args = dict(vocab=spec.vocab, dtype=L.OLIVE_BF16, flags=L.OLIVE_FLAG_TOPK)
+        args.update(kw)
+        desc = L.make_desc(args["vocab"], spec.d_student, spec.d_teacher, args["dtype"],
+                           L.OLIVE_W_DV, 1.0, 1.0, max_positions=T, max_seqs=4,
+                           flags=args["flags"])
+        w = torch.zeros(spec.d_teacher * spec.vocab, dtype=torch.float32, device=dev)
+        status, handle = L.olive_score_init(desc, w, w, check=False)
+        assert status == L.OLIVE_E_UNSUPPORTED and handle is None, kw
+    # a student-only context refuses it too (the overlap needs the teacher)
+    desc = L.make_desc(spec.vocab, spec.d_student, 0, L.OLIVE_BF16, L.OLIVE_W_DV, 1.0, 1.0,
+                       max_positions=T, max_seqs=4, flags=L.OLIVE_FLAG_TOPK)
+    status, handle = L.olive_score_init(desc, wl["w_student"], None, check=False)
+    assert status == L.OLIVE_E_UNSUPPORTED and handle is None
