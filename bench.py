@@ -81,6 +81,9 @@ def main():
     ap.add_argument("--region-only", action="store_true",
                     help="score only the region's positions (OLIVE_OUT_REGION_ONLY): the rate "
                          "and the roofline then count scored positions")
+    ap.add_argument("--topk", action="store_true",
+                    help="also form the top-16 statistics (overlap ratio, top-16 KL and both "
+                         "index sets; OLIVE_FLAG_TOPK)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 3 plain device copies of BYTES bytes (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -118,7 +121,8 @@ def main():
     desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher,
                        L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
                        wl["scale_student"], wl["scale_teacher"], max_positions=T, max_seqs=B,
-                       flags=L.OLIVE_FLAG_KERNEL_TIMING)
+                       flags=L.OLIVE_FLAG_KERNEL_TIMING |
+                       (L.OLIVE_FLAG_TOPK if args.topk else 0))
     stream = torch.cuda.current_stream()
     ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"], stream)
     dev = wl["h_student"].device
@@ -130,10 +134,15 @@ def main():
     amt = torch.empty(T, dtype=torch.int32, device=dev)
     ce = torch.empty(B, dtype=torch.float32, device=dev)
     klr = torch.empty(T, dtype=torch.float32, device=dev) if args.reverse_kl else None
+    tk = dict(topk_overlap=torch.empty(T, dtype=torch.float32, device=dev),
+              kl_topk=torch.empty(T, dtype=torch.float32, device=dev),
+              topk_student=torch.empty(T, L.OLIVE_TOPK, dtype=torch.int32, device=dev),
+              topk_teacher=torch.empty(T, L.OLIVE_TOPK, dtype=torch.int32, device=dev)) \
+        if args.topk else {}
     outs = L.make_outputs(kl=kl, kl_reverse=klr, counts=counts, logp_student=lps,
                           logp_teacher=lpt, argmax_student=ams, argmax_teacher=amt,
                           ce_per_seq=ce,
-                          flags=L.OLIVE_OUT_REGION_ONLY if args.region_only else 0)
+                          flags=L.OLIVE_OUT_REGION_ONLY if args.region_only else 0, **tk)
     use_spans = wl.get("spans") is not None       # multi-turn: teacher actions scored
     batch = L.make_batch(wl["cu_seqlens"], None if use_spans else wl["cut"], wl["targets"],
                          wl["h_student"], wl["h_teacher"], wl["valid_len"],
@@ -143,7 +152,7 @@ def main():
     def step():
         if use_spans:
             L.olive_score_batch_spans(ctx, batch, spans, outs, stream)
-        elif args.reverse_kl or args.region_only:
+        elif args.reverse_kl or args.region_only or args.topk:
             L.olive_score_batch(ctx, batch, outs, stream)
         else:
             L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
@@ -171,7 +180,8 @@ def main():
         % (args.steps, ms_step, kernel_ms, stats, err))
     flops = 2.0 * rows * spec.vocab * (spec.d_student + spec.d_teacher)
     achieved = flops / (kernel_ms * 1e-3) / 1e12
-    traffic = None if (args.reverse_kl or args.region_only) else measured_traffic(args.workload)
+    traffic = None if (args.reverse_kl or args.region_only or args.topk) \
+        else measured_traffic(args.workload)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
         "value": rows / (ms_step * 1e-3),
@@ -191,6 +201,8 @@ def main():
             "d_student": spec.d_student, "d_teacher": spec.d_teacher,
             "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
             "reverse_kl": bool(args.reverse_kl), "region_only": bool(args.region_only),
+            "topk": bool(args.topk), "topk_filtered_pairs": stats["topk_filtered"],
+            "topk_scanned_pairs": stats["topk_scanned"],
             "region": "spans" if use_spans else "teacher",
             "near_tie_rows": stats["flagged"], "grid": stats["grid"],
             "step_tflops": flops / (ms_step * 1e-3) / 1e12,

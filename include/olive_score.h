@@ -94,8 +94,8 @@ typedef struct {
 #define OLIVE_FLAG_KERNEL_TIMING 2
 /* Reserve the workspace of the top-K statistics (olive_score_outputs' topk_* and
  * kl_topk fields). Needs a bf16 teacher context on which the MFMA kernel applies and
- * V >= 512 (else init returns E_UNSUPPORTED). The workspace holds about
- * (max_positions x (2.9 KB + 2.3 KB x ceil(V / 4096))) of device memory. */
+ * 512 <= V <= 2^23 (else init returns E_UNSUPPORTED). The workspace holds about
+ * max_positions x 6.7 KB of device memory. */
 #define OLIVE_FLAG_TOPK 4
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */
@@ -256,11 +256,12 @@ olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
 
 /*
  * Diagnostics of the last scoring call (synchronises the device).
- *   out host [5] int64: [0] vocabulary splits used, [1] rows whose greedy token was
+ *   out host [6] int64: [0] vocabulary splits used, [1] rows whose greedy token was
  *   re-decided in fp64 because its top-2 logit gap was within the fp32 error window,
  *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched,
- *   [4] rows whose top-K sets were recomputed by the exact rescan (0 without top-K
- *   outputs).
+ *   [4] (position, model) pairs whose top-K set needed a filter pass over the
+ *   vocabulary, [5] pairs of those that needed an exhaustive exact scan (more than
+ *   256 near-tied candidates); [4] and [5] are 0 without top-K outputs.
  */
 olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out);
 

@@ -255,10 +255,11 @@ def olive_score_last_error(ctx) -> int:
 
 
 def olive_score_last_stats(ctx) -> dict:
-    out = (ctypes.c_int64 * 5)()
+    out = (ctypes.c_int64 * 6)()
     _check(load().olive_score_last_stats(ctx, out), "olive_score_last_stats")
     return dict(splits=out[0], flagged=out[1], kernel=("mfma", "generic")[out[2]]
-                if out[2] in (0, 1) else None, grid=out[3], topk_rescanned=out[4])
+                if out[2] in (0, 1) else None, grid=out[3], topk_filtered=out[4],
+                topk_scanned=out[5])
 
 
 def olive_score_kernel_times(ctx, n: int) -> list:

@@ -6,6 +6,7 @@
 #include <cmath>
 #include <cstring>
 #include <new>
+#include <vector>
 
 #include "olive_internal.hpp"
 
@@ -27,12 +28,10 @@ struct olive_score_ctx {
     int flag_cap = 0;
     void *fx_scratch = nullptr;
     float *wn_s = nullptr, *wn_t = nullptr;     // weight-row L2 norms (rounding bounds)
+    float wmax_s = 0.f, wmax_t = 0.f;           // their maxima
     int32_t *err = nullptr;
-    // top-K workspace (OLIVE_FLAG_TOPK): normalisers [P][2], merged lists [P][2][16],
-    // the rescan queue [P] and the per-chunk lists of queued rows
-    float *tk_lse = nullptr, *tk_list_v = nullptr;
-    int32_t *tk_list_i = nullptr, *tk_queue = nullptr;
-    void *tk_rescan = nullptr;
+    void *tk_buf = nullptr;                     // top-K workspace (OLIVE_FLAG_TOPK)
+    TopkWork tkw = {};
     bool bf16 = false, has_t = false, mfma_ok = false, topk = false;
     int last_kernel = -1, last_grid = 0;
     bool timing = false;
@@ -51,7 +50,7 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_lse, c->tk_list_v, c->tk_list_i, c->tk_queue, c->tk_rescan};
+                    c->tk_buf};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -68,6 +67,13 @@ olive_status dev_alloc(T **p, size_t bytes) {
 }
 
 olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP; }
+
+// Top-K lists need two splits at least (16 listed entries) and at most 1024
+// vocabulary tiles per split (the 16-bit row ordinal of a list key).
+int topk_min_splits(int n_vtiles) {
+    const int s = (n_vtiles + 1023) / 1024;
+    return s > 2 ? s : 2;
+}
 
 // The scoring of one batch, shared by every scoring entry point.
 olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
@@ -117,7 +123,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     }
     s = check_hip(launch_prep(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
                               mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
-                              fixed_splits, topk ? 2 : 1, st));
+                              fixed_splits, topk ? topk_min_splits(n_vtiles) : 1, st));
     if (s) return s;
     s = check_hip(launch_rowmap(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
                                 ctx->err,
@@ -144,6 +150,8 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     a.sT = has_t ? d.logit_scale_teacher : 1.f;
     a.cS = a.sS * 1.4426950408889634f;
     a.cT = a.sT * 1.4426950408889634f;
+    a.wmax_s = ctx->wmax_s;
+    a.wmax_t = ctx->wmax_t;
     const bool same_scale = has_t && (a.sS == a.sT);
 
     const int slot = (int)(ctx->n_calls % 64);
@@ -162,7 +170,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     s = check_hip(launch_combine(a, ctx->bf16, has_t, same_scale, b->targets, ctx->err, logp_s,
                                  has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
                                  has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp,
-                                 topk ? ctx->tk_lse : nullptr, flagged, ctx->flag_cap, T, st));
+                                 topk ? ctx->tkw.lse : nullptr, flagged, ctx->flag_cap, T, st));
     if (s) return s;
     if (flagged) {
         s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
@@ -170,9 +178,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
         if (s) return s;
     }
     if (topk) {
-        s = check_hip(launch_topk(a, ctx->bf16, ctx->tk_lse, ctx->tk_list_v, ctx->tk_list_i,
-                                  ctx->tk_queue, (int)ctx->desc.max_positions, ctx->tk_rescan,
-                                  tk.overlap, tk.kl, tk.idx_s, tk.idx_t, T, st));
+        s = check_hip(launch_topk(a, ctx->tkw, tk, T, st));
         if (s) return s;
     }
     if (ce) {
@@ -238,7 +244,8 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
                   (((uintptr_t)w_student & 15) == 0 &&
                    (!c->has_t || ((uintptr_t)w_teacher & 15) == 0)));
     c->topk = (d.flags & OLIVE_FLAG_TOPK) != 0;
-    if (c->topk && (!c->mfma_ok || !c->has_t || d.vocab < 512)) {
+    if (c->topk && (!c->mfma_ok || !c->has_t || d.vocab < 512 ||
+                    d.vocab > (int64_t)MAX_SPLITS * 1024 * MFMA_BV)) {
         release(c);
         return OLIVE_E_UNSUPPORTED;
     }
@@ -269,11 +276,10 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (!s)
         s = dev_alloc(&c->part, (size_t)(c->topk ? NFIELDS_TOPK : NFIELDS) * MAX_SPLITS *
                                     c->pstride * sizeof(float));
-    if (!s && c->topk) s = dev_alloc(&c->tk_lse, (size_t)P * 2 * sizeof(float));
-    if (!s && c->topk) s = dev_alloc(&c->tk_list_v, (size_t)P * 2 * TOPK_K * sizeof(float));
-    if (!s && c->topk) s = dev_alloc(&c->tk_list_i, (size_t)P * 2 * TOPK_K * sizeof(int32_t));
-    if (!s && c->topk) s = dev_alloc(&c->tk_queue, (size_t)P * sizeof(int32_t));
-    if (!s && c->topk) s = dev_alloc(&c->tk_rescan, topk_rescan_bytes(V, (int)P));
+    if (!s && c->topk) {
+        s = dev_alloc(&c->tk_buf, topk_work_bytes(P));
+        if (!s) c->tkw = topk_carve(c->tk_buf, P);
+    }
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
     if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
     if (!s)
@@ -287,6 +293,23 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         (c->has_t && launch_row_norms(c->wt, V, d.d_teacher, c->bf16, c->wn_t, st) != hipSuccess)) {
         release(c);
         return OLIVE_E_HIP;
+    }
+    if (c->topk) {   // the largest row norms bound the rounding of any logit
+        if (hipStreamSynchronize(st) != hipSuccess) {
+            release(c);
+            return OLIVE_E_HIP;
+        }
+        std::vector<float> wn((size_t)V);
+        for (int m = 0; m < 2; ++m) {
+            if (hipMemcpy(wn.data(), m ? c->wn_t : c->wn_s, (size_t)V * sizeof(float),
+                          hipMemcpyDeviceToHost) != hipSuccess) {
+                release(c);
+                return OLIVE_E_HIP;
+            }
+            float mx = 0.f;
+            for (float x : wn) mx = x > mx ? x : mx;
+            (m ? c->wmax_t : c->wmax_s) = mx * (1.0f + 0x1p-10f);
+        }
     }
     c->timing = (d.flags & OLIVE_FLAG_KERNEL_TIMING) != 0;
     if (c->timing) {
@@ -384,7 +407,8 @@ olive_status olive_score_last_stats(olive_score_ctx *ctx, int64_t *out) {
     out[1] = s.n_flagged;
     out[2] = ctx->last_kernel;
     out[3] = ctx->last_grid;
-    out[4] = s.n_topk_queued;
+    out[4] = s.n_tkq[0] + s.n_tkq[1];
+    out[5] = s.n_tk_fb;
     return OLIVE_OK;
 }
 

@@ -21,6 +21,26 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t bits16) {
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 
+// Order-preserving image of a float (a larger float maps to a larger unsigned).
+__device__ __forceinline__ uint32_t f2ord(float z) {
+    const uint32_t b = __float_as_uint(z);
+    return b ^ ((uint32_t)((int32_t)b >> 31) | 0x80000000u);
+}
+__device__ __forceinline__ float ord2f(uint32_t u) {
+    return __uint_as_float((u & 0x80000000u) ? (u & 0x7fffffffu) : ~u);
+}
+// Top-K list keys: the high 16 bits of f2ord(z) (the logit rounded toward -inf to a
+// bucket [lb(code), lb(code + 1))) above a 16-bit tie part. Lower and (exclusive)
+// upper end of the bucket of a key's code.
+__device__ __forceinline__ float key_lb(uint32_t key) { return ord2f(key & 0xFFFF0000u); }
+__device__ __forceinline__ float key_ub(uint32_t key) {
+    const uint32_t c = key >> 16;
+    return c >= 0xFFFFu ? __builtin_inff() : ord2f((c + 1) << 16);
+}
+
+// Exclusive upper end of the bucket of a value that is a bucket's lower end.
+__device__ __forceinline__ float bucket_ub(float lb) { return key_ub(f2ord(lb)); }
+
 template <typename T>
 __device__ __forceinline__ float load_elem(const T *p, int64_t i);
 template <>

@@ -33,6 +33,23 @@ constexpr int TK_FIELDS = 2 * TK_LIST + 1;
 constexpr int F_TK = NFIELDS;
 constexpr int NFIELDS_TOPK = NFIELDS + 2 * TK_FIELDS;
 constexpr int TOPK_K = 16;   // LogProb top-K of the OPD baseline (App. A, Table 3)
+constexpr int TK_CAP = 256;  // candidates kept per (row, model) by the vocabulary filter
+
+// Device workspace of the top-K statistics, carved from one allocation (topk_carve):
+// cap = max_positions compacted rows.
+struct TopkWork {
+    float *lse;        // [cap][2] full-vocabulary log-normalisers (combine)
+    float *list_v;     // [cap][2][16] the sets: exact logits (fp32) in rank order
+    int32_t *list_i;   //               and their vocabulary indices
+    int32_t *qj;       // [2][cap] queued compacted rows per model
+    float *qthr;       // [2][cap] their fp32 candidate thresholds
+    int32_t *qcnt;     // [2][cap] candidates the filter found
+    int32_t *cand;     // [2][cap][TK_CAP] their vocabulary indices
+    int32_t *fb;       // [2 cap] pairs (model * cap + queue slot) for the exhaustive scan
+    int cap;
+};
+size_t topk_work_bytes(int64_t cap);
+TopkWork topk_carve(void *base, int64_t cap);
 
 // Device-side schedule of one call, written by the preparation kernel.
 struct Sched {
@@ -44,7 +61,8 @@ struct Sched {
     int64_t n_scored;   // in-region valid positions
     int32_t n_flagged;  // rows queued for the near-tie argmax re-decision
     int32_t cu_bad;     // cu_seqlens malformed: nothing is scored
-    int32_t n_topk_queued;  // rows queued for the exact top-K rescan
+    int32_t n_tkq[2];   // (row, model) pairs whose top-K field needs the vocabulary filter
+    int32_t n_tk_fb;    // pairs of those that need the exhaustive exact scan
     int32_t pad;
 };
 
@@ -83,6 +101,7 @@ struct ScoreArgs {
     int32_t n_vtiles;            // vocabulary tiles (MFMA) or chunks (generic)
     float cS, cT;                // s * log2(e)
     float sS, sT;                // logit scales
+    float wmax_s, wmax_t;        // largest weight-row L2 norm (top-K rounding bounds)
 };
 
 // Host-side launchers (each defined beside its kernel).
@@ -106,10 +125,7 @@ hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_s
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,
                           float *lse_out, int32_t *flagged, int flag_cap, int64_t max_rows,
                           hipStream_t st);
-size_t topk_rescan_bytes(int64_t V, int cap);
-hipError_t launch_topk(const ScoreArgs &a, bool bf16, const float *lse, float *list_v,
-                       int32_t *list_i, int32_t *queue, int cap, void *rescan_buf,
-                       float *overlap, float *kl_topk, int32_t *idx_s, int32_t *idx_t,
+hipError_t launch_topk(const ScoreArgs &a, const TopkWork &w, const TopkOut &out,
                        int64_t max_rows, hipStream_t st);
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
                              void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,

@@ -120,12 +120,15 @@ struct Run {                // running statistics of one position column
     int idx;
 };
 
-// The 4 largest logits (and indices) a lane has seen of one position column, in
-// (value descending, index ascending) order; kMasked marks empty slots. Everything
-// the lane has dropped is <= v[3].
+// The 4 largest logits a lane has seen of one position column, as packed keys in
+// descending order (0 = empty): the high 16 bits are the logit's order-preserving
+// code rounded toward -inf (the logit lies in [lb(code), lb(code + 1))), the low 16
+// bits 0xFFFF minus the lane's ordinal of the row (vocabulary tile of the split x 64 +
+// 32-row block x 16 + row of the block), so that among equal codes the lower
+// vocabulary index ranks first. Every logit the lane dropped is below lb(code_3 + 1).
+// The lists only narrow the field: the top-K sets are decided on exact logits later.
 struct Top4 {
-    float v[4];
-    int i[4];
+    uint32_t k[4];
 };
 
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
@@ -362,7 +365,7 @@ struct Kernel {
                                                 const floatx16 (&accT)[4][2], Run (&RS)[2],
                                                 Run (&RT)[2], float (&A)[2], float (&Bq)[2],
                                                 Top4 (&KS)[2], Top4 (&KT)[2], const ScoreArgs &a,
-                                                int vbase) {
+                                                int vbase, int lvt) {
 #pragma unroll
         for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -379,27 +382,11 @@ struct Kernel {
                 if (HAS_T)
                     fold_block<true>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
                 if (TOPK) {
-                    topk_block(zs, KS[cb], vbase + vb * 32);
-                    topk_block(zt, KT[cb], vbase + vb * 32);
+                    const uint32_t tie0 = 0xFFFFu - (uint32_t)(lvt * 64 + vb * 16);
+                    topk_block(zs, KS[cb], tie0);
+                    topk_block(zt, KT[cb], tie0);
                 }
             }
-    }
-
-    // Insert (x, xi) into a descending top list; strict comparisons keep the earlier
-    // (lower-index) entry first among equal values, as entries arrive in index order.
-    template <int N>
-    static __device__ __forceinline__ void topk_insert(float (&v)[N], int (&ix)[N], float x,
-                                                       int xi) {
-#pragma unroll
-        for (int j = 0; j < N; ++j) {
-            const bool gt = x > v[j];
-            const float nv = gt ? x : v[j];
-            const int ni = gt ? xi : ix[j];
-            x = gt ? v[j] : x;
-            xi = gt ? ix[j] : xi;
-            v[j] = nv;
-            ix[j] = ni;
-        }
     }
 
     // The same for entries of other lanes: (value descending, index ascending) order by
@@ -420,17 +407,26 @@ struct Kernel {
         return x;
     }
 
-    // Offer one 32-row block (16 values per lane, rows in increasing index order) to a
-    // lane's top-4; skipped when no value of the block beats the current 4th.
+    // Offer one 32-row block (16 values per lane) to a lane's top-4; skipped when no
+    // key of the block can beat the current 4th. tie0 = 0xFFFF minus the ordinal of
+    // the block's first row.
     static __device__ __forceinline__ void topk_block(const float (&z)[16], Top4 &K,
-                                                      int vcode0) {
+                                                      uint32_t tie0) {
         float bm = z[0];
 #pragma unroll
         for (int r = 1; r < 16; ++r) bm = max2(bm, z[r]);
-        if (bm > K.v[3]) {
+        // wave-uniform: inserting keys that do not beat the 4th leaves a list unchanged
+        if (__builtin_amdgcn_ballot_w64(((f2ord(bm) & 0xFFFF0000u) | 0xFFFFu) > K.k[3]) != 0) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                topk_insert<4>(K.v, K.i, z[r], vcode0 + 8 * (r >> 2) + (r & 3));
+            for (int r = 0; r < 16; ++r) {
+                uint32_t x = (f2ord(z[r]) & 0xFFFF0000u) | (tie0 - (uint32_t)r);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const uint32_t hi = x > K.k[j] ? x : K.k[j];
+                    x = x > K.k[j] ? K.k[j] : x;
+                    K.k[j] = hi;
+                }
+            }
         }
     }
 
@@ -515,10 +511,7 @@ struct Kernel {
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    KS[cb].v[e] = kMasked; KS[cb].i[e] = 0x7fffffff;
-                    KT[cb].v[e] = kMasked; KT[cb].i[e] = 0x7fffffff;
-                }
+                for (int e = 0; e < 4; ++e) { KS[cb].k[e] = 0u; KT[cb].k[e] = 0u; }
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 RS[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
@@ -588,7 +581,7 @@ struct Kernel {
                 OLIVE_STEPS(accS, nS)
                 if (HAS_T) OLIVE_STEPS(accT, nT)
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
-                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, vbase);
+                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, vbase, vt - vt0);
             }
 #undef OLIVE_STEPS
 
@@ -606,8 +599,9 @@ struct Kernel {
                     merge_run(RT[cb], AA[cb], q2, qa, a.cT);
                 }
             }
-            // Top-K: lanes l and l+32 combine their top-4 lists into a top-8 (nothing is
-            // dropped); the floor bounds everything either lane dropped.
+            // Top-K: each lane decodes its keys to (lower end of the value's bucket,
+            // vocabulary index); lanes l and l+32 combine their top-4 lists into a top-8
+            // (nothing is dropped); the floor bounds everything either lane dropped.
             float Q8v[2][2][8], Qfl[2][2];
             int Q8i[2][2][8];
             if (TOPK) {
@@ -616,16 +610,28 @@ struct Kernel {
 #pragma unroll
                     for (int cb = 0; cb < 2; ++cb) {
                         const Top4 &K = m ? KT[cb] : KS[cb];
+                        float kv[4];
+                        int ki[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            Q8v[m][cb][e] = K.v[e]; Q8i[m][cb][e] = K.i[e];
+                            const uint32_t key = K.k[e];
+                            const uint32_t ord = 0xFFFFu - (key & 0xFFFFu);
+                            const int vt = vt0 + (int)(ord >> 6);
+                            const int r = (int)(ord & 15u);
+                            const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+                            kv[e] = key ? key_lb(key) : kMasked;
+                            ki[e] = key ? row0 + L.wv * 128 + 4 * L.h + (int)((ord >> 4) & 3u) * 32 +
+                                              8 * (r >> 2) + (r & 3)
+                                        : 0x7fffffff;
+                            Q8v[m][cb][e] = kv[e]; Q8i[m][cb][e] = ki[e];
                             Q8v[m][cb][4 + e] = kMasked; Q8i[m][cb][4 + e] = 0x7fffffff;
                         }
 #pragma unroll
                         for (int e = 0; e < 4; ++e)
-                            topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb], __shfl_xor(K.v[e], 32),
-                                               __shfl_xor(K.i[e], 32));
-                        Qfl[m][cb] = max2(K.v[3], __shfl_xor(K.v[3], 32));
+                            topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb], __shfl_xor(kv[e], 32),
+                                               __shfl_xor(ki[e], 32));
+                        const float f = K.k[3] ? key_ub(K.k[3]) : kMasked;
+                        Qfl[m][cb] = max2(f, __shfl_xor(f, 32));
                     }
             }
             // Merge the two vocabulary halves (wv = 1 into wv = 0) through LDS, once
@@ -694,10 +700,12 @@ struct Kernel {
                                         xk + (((L.wt * 2 + cb) * 32 + L.l32) * 2 + m) * 17;
                                     float fl = max2(Qfl[m][cb], q[16]);
 #pragma unroll
-                                    for (int e = 0; e < 8; ++e)
-                                        fl = max2(fl, topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb],
-                                                                        q[e],
-                                                                        __float_as_int(q[8 + e])));
+                                    for (int e = 0; e < 8; ++e) {
+                                        // a dropped entry's value lies below its bucket's end
+                                        const float x = topk_insert_lex<8>(
+                                            Q8v[m][cb], Q8i[m][cb], q[e], __float_as_int(q[8 + e]));
+                                        fl = max2(fl, x == kMasked ? x : key_ub(f2ord(x)));
+                                    }
 #pragma unroll
                                     for (int e = 0; e < 8; ++e) {
                                         P[((F_TK + m * TK_FIELDS + e) * MAX_SPLITS + s) * ps + j] =

@@ -6,15 +6,24 @@
 //   kl_topk = sum over v in TopK_T of p_T[v] (log p_T[v] - log p_S[v]),
 // with the full-vocabulary normalisers of the scoring pass.
 //
-// The scoring kernel leaves per (split, row, model) the split's 8 largest logits and a
-// floor above everything else of the split. Here:
-//   select  - merges the lists of every split into the row's 16 largest; when some
-//             split's floor reaches the 16th value an entry it dropped could belong to
-//             the set, and the row is queued for an exact rescan;
-//   rescan  - recomputes every logit of a queued row (fp32, per vocabulary chunk) and
-//             keeps each chunk's 16 largest; merge picks the row's 16 from the chunks;
-//   outputs - forms the overlap, gathers the student logits at the teacher's tokens
-//             and sums the top-K KL in a fixed order.
+// The sets are decided on exact logits, as the greedy token is: fp32 logits only
+// narrow the field. Exact logits are bf16 products (exact in fp32) summed in fp64.
+// delta = d 2^-23 |h| max_v |w_v| bounds the rounding of any fp32 logit of a row.
+// The scoring kernel leaves per (split, row, model) the split's 8 largest fp32 logits,
+// each as the lower end of a bucket that holds it (one 2^-7 relative step), and a
+// floor above every other fp32 logit of the split. Stages:
+//   select  - z16 = the 16th largest listed value. A logit whose exact value can reach
+//             the exact top-16 has an fp32 value >= thr = z16 - 2 delta. When no split
+//             floor reaches thr, every such logit is listed: their exact values are
+//             formed and ranked. Otherwise the (row, model) pair is queued with thr;
+//   filter  - for the queued pairs, every fp32 logit of the vocabulary (MFMA, 64
+//             queued rows x 128 vocabulary rows per work item); the indices of those
+//             >= thr are kept (at most TK_CAP per pair);
+//   exact   - exact values of a pair's kept indices, ranked; a pair with more than
+//             TK_CAP goes to
+//   scan    - every exact logit of the pair's row (one workgroup, fp64 sums);
+//   outputs - the overlap, the exact student logits at the teacher's tokens and the
+//             top-K KL summed in a fixed order.
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -22,37 +31,37 @@
 
 namespace olive {
 
-constexpr int TKR_CHUNK = 4096;     // vocabulary rows per rescan work item
-constexpr int TKR_THREADS = 256;
-constexpr int TKR_GROUPS = TKR_THREADS / 8;
-constexpr float kTkEmpty = -0x1p99f;   // empty list slot (never a real logit)
+constexpr int TK_CAND = MAX_SPLITS * TK_LIST;   // listed entries of one (row, model)
+constexpr int TKF_QB = 64;                      // queued rows per filter work item
+constexpr int TKF_VR = 128;                     // vocabulary rows per filter work item
+constexpr int TKS_THREADS = 256;                // exhaustive scan
+constexpr int TKS_GROUPS = TKS_THREADS / 8;
+constexpr double kTkEmpty = -0x1p1000;          // empty slot (below every finite logit)
+constexpr int kTkNoIdx = 0x7fffffff;
 
-struct TkEntry {
-    float v;
-    int i;
-};
+typedef __bf16 tk_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float tk_floatx16 __attribute__((ext_vector_type(16)));
 
 // (v, i) ranks before (w, j): larger value first, lower index among equals.
-__device__ __forceinline__ bool tk_before(float v, int i, float w, int j) {
+__device__ __forceinline__ bool tk_before(double v, int i, double w, int j) {
     return v > w || (v == w && i < j);
 }
 
 // Wave-wide best (value, index) of one candidate per lane.
-__device__ __forceinline__ TkEntry wave_best(float v, int i) {
+__device__ __forceinline__ void wave_best(double &v, int &i) {
     for (int off = 32; off > 0; off >>= 1) {
-        const float ov = __shfl_xor(v, off);
+        const double ov = __shfl_xor(v, off);
         const int oi = __shfl_xor(i, off);
         if (tk_before(ov, oi, v, i)) { v = ov; i = oi; }
     }
-    return TkEntry{v, i};
 }
 
 template <int N>
-__device__ __forceinline__ void tk_insert(float (&v)[N], int (&ix)[N], float x, int xi) {
+__device__ __forceinline__ void tk_insert(double (&v)[N], int (&ix)[N], double x, int xi) {
 #pragma unroll
     for (int j = 0; j < N; ++j) {
         const bool b = tk_before(x, xi, v[j], ix[j]);
-        const float nv = b ? x : v[j];
+        const double nv = b ? x : v[j];
         const int ni = b ? xi : ix[j];
         x = b ? v[j] : x;
         xi = b ? ix[j] : xi;
@@ -61,192 +70,343 @@ __device__ __forceinline__ void tk_insert(float (&v)[N], int (&ix)[N], float x, 
     }
 }
 
-template <int N>
-__device__ __forceinline__ void tk_pop(float (&v)[N], int (&ix)[N]) {
+// Sum of the exact products of 8 bf16 pairs, accumulated in fp64.
+__device__ __forceinline__ double dot8_f64(const uint4 &p, const uint4 &q, double acc) {
+    const uint32_t a[4] = {p.x, p.y, p.z, p.w}, b[4] = {q.x, q.y, q.z, q.w};
 #pragma unroll
-    for (int j = 0; j + 1 < N; ++j) { v[j] = v[j + 1]; ix[j] = ix[j + 1]; }
-    v[N - 1] = kTkEmpty;
-    ix[N - 1] = 0x7fffffff;
+    for (int t = 0; t < 4; ++t) {
+        acc += (double)(bf16_bits_to_f32(a[t] & 0xffffu) * bf16_bits_to_f32(b[t] & 0xffffu));
+        acc += (double)(bf16_bits_to_f32(a[t] >> 16) * bf16_bits_to_f32(b[t] >> 16));
+    }
+    return acc;
 }
 
-// One wavefront per compacted in-region row: the row's 16 largest logits of each
-// model from the split lists (raw, unscaled logits: the order is the same as of the
-// scaled ones). Lane l < n_splits walks split l's list, staged in LDS.
+// Exact logit h . w of one vocabulary row by one wavefront (d a multiple of 8, rows
+// 16-byte aligned); every lane returns the sum.
+__device__ __forceinline__ double wave_dot_exact(const uint16_t *h, const uint16_t *w, int d,
+                                                 int lane) {
+    double acc = 0.0;
+    for (int k = lane * 8; k < d; k += 512)
+        acc = dot8_f64(*(const uint4 *)(h + k), *(const uint4 *)(w + k), acc);
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+// |h|^2 in fp32 by one wavefront.
+__device__ __forceinline__ float wave_sumsq(const uint16_t *h, int d, int lane) {
+    float acc = 0.f;
+    for (int k = lane; k < d; k += 64) {
+        const float x = bf16_bits_to_f32(h[k]);
+        acc = fmaf(x, x, acc);
+    }
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    return acc;
+}
+
+// Rank n <= TK_CAND candidates (exact values cx, indices ci in LDS; kTkEmpty marks a
+// skipped slot) and write the 16 best of row j, model m.
+__device__ __forceinline__ void rank_and_write(const double *cx, const int *ci, int n, int lane,
+                                               int64_t j, int m, float *list_v,
+                                               int32_t *list_i) {
+    double kv[4];
+    int ki[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        const int c = lane + 64 * t;
+        const bool ok = c < n && cx[c] != kTkEmpty;
+        kv[t] = ok ? cx[c] : kTkEmpty;
+        ki[t] = ok ? ci[c] : kTkNoIdx;
+    }
+    for (int r = 0; r < TOPK_K; ++r) {
+        double bv = kv[0];
+        int bi = ki[0], bt = 0;
+#pragma unroll
+        for (int t = 1; t < 4; ++t)
+            if (tk_before(kv[t], ki[t], bv, bi)) { bv = kv[t]; bi = ki[t]; bt = t; }
+        double wv = bv;
+        int wi = bi;
+        wave_best(wv, wi);
+        if (bv == wv && bi == wi) {             // candidate indices are unique
+#pragma unroll
+            for (int t = 0; t < 4; ++t)
+                if (t == bt) { kv[t] = kTkEmpty; ki[t] = kTkNoIdx; }
+        }
+        if (lane == 0) {
+            list_v[(j * 2 + m) * TOPK_K + r] = (float)wv;
+            list_i[(j * 2 + m) * TOPK_K + r] = wi;
+        }
+    }
+}
+
+// One wavefront per compacted in-region row, for each model in turn.
 __global__ void __launch_bounds__(256)
-topk_select_kernel(ScoreArgs a, float *__restrict__ list_v, int32_t *__restrict__ list_i,
-                   int32_t *__restrict__ queue, int cap) {
-    __shared__ float sv[4][MAX_SPLITS][TK_LIST + 1];
-    __shared__ int si[4][MAX_SPLITS][TK_LIST + 1];
+topk_select_kernel(ScoreArgs a, TopkWork w) {
+    __shared__ float cv[4][TK_CAND];
+    __shared__ int ci[4][TK_CAND];
+    __shared__ double cx[4][TK_CAND];
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
     const int64_t j = (int64_t)blockIdx.x * 4 + wid;
     Sched *sched = const_cast<Sched *>(a.sched);
     if (j >= sched->t_valid) return;
-    if (!(a.rowmap[j] >> 31)) return;            // not scored
+    const uint32_t rm = a.rowmap[j];
+    if (!(rm >> 31)) return;                     // not scored
+    const int64_t g = rm & 0x7fffffffu;
     const int ns = sched->n_splits;
+    const int nc = ns * TK_LIST;
     const int64_t ps = a.pstride;
-    bool overflow = false;
     for (int m = 0; m < 2; ++m) {
-        float fl = kTkEmpty;
+        const int d = m ? a.dt : a.ds;
+        const uint16_t *h = (const uint16_t *)(m ? a.ht : a.hs) + g * d;
+        const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
+        const float hh = wave_sumsq(h, d, lane);
+        if (hh == 0.f) {   // h = 0: every exact logit is 0, the set is 0..15
+            if (lane < TOPK_K) {
+                w.list_v[(j * 2 + m) * TOPK_K + lane] = 0.f;
+                w.list_i[(j * 2 + m) * TOPK_K + lane] = lane;
+            }
+            continue;
+        }
+        float fl = -__builtin_inff();
         if (lane < ns) {
             for (int e = 0; e < TK_LIST; ++e) {
-                sv[wid][lane][e] = a.part[((F_TK + m * TK_FIELDS + e) * MAX_SPLITS + lane) * ps + j];
-                si[wid][lane][e] = __float_as_int(
+                cv[wid][lane * TK_LIST + e] =
+                    a.part[((F_TK + m * TK_FIELDS + e) * MAX_SPLITS + lane) * ps + j];
+                ci[wid][lane * TK_LIST + e] = __float_as_int(
                     a.part[((F_TK + m * TK_FIELDS + TK_LIST + e) * MAX_SPLITS + lane) * ps + j]);
             }
-            sv[wid][lane][TK_LIST] = kTkEmpty;   // end of the list
-            si[wid][lane][TK_LIST] = 0x7fffffff;
             fl = a.part[((F_TK + m * TK_FIELDS + 2 * TK_LIST) * MAX_SPLITS + lane) * ps + j];
         }
         __builtin_amdgcn_wave_barrier();
+        // z16: the 16th largest listed value (lane l < ns walks split l's sorted list)
         int ptr = 0;
-        float mine_v = kTkEmpty;
-        int mine_i = 0x7fffffff;
+        double z16 = kTkEmpty;
         for (int r = 0; r < TOPK_K; ++r) {
-            const float hv = lane < ns ? sv[wid][lane][ptr] : kTkEmpty;
-            const int hi = lane < ns ? si[wid][lane][ptr] : 0x7fffffff;
-            const TkEntry b = wave_best(hv, hi);
-            if (lane < ns && hv == b.v && hi == b.i && ptr < TK_LIST) ++ptr;   // unique indices
-            if (lane == r) { mine_v = b.v; mine_i = b.i; }
+            double hv = kTkEmpty;
+            int hi = kTkNoIdx;
+            if (lane < ns && ptr < TK_LIST) {
+                hv = cv[wid][lane * TK_LIST + ptr];
+                hi = ci[wid][lane * TK_LIST + ptr];
+            }
+            double bv = hv;
+            int bi = hi;
+            wave_best(bv, bi);
+            if (lane < ns && ptr < TK_LIST && hv == bv && hi == bi) ++ptr;
+            z16 = bv;
         }
-        const float tau = __shfl(mine_v, TOPK_K - 1);
-        overflow |= __any(lane < ns && fl >= tau);
-        if (lane < TOPK_K) {
-            list_v[(j * 2 + m) * TOPK_K + lane] = mine_v;
-            list_i[(j * 2 + m) * TOPK_K + lane] = mine_i;
+        const float delta = (float)d * 0x1p-23f * (sqrtf(hh) * (1.0f + 0x1p-10f)) *
+                            (m ? a.wmax_t : a.wmax_s);
+        const float thr = (float)z16 - 2.f * delta;
+        // every logit that can reach the exact top-16 is listed unless a floor reaches
+        // thr (a floor or threshold that is not finite queues the pair as well)
+        if (__any(lane < ns && !(fl < thr))) {
+            if (lane == 0) {
+                const int q = atomicAdd(&sched->n_tkq[m], 1);
+                if (q < w.cap) {
+                    w.qj[m * w.cap + q] = (int32_t)j;
+                    w.qthr[m * w.cap + q] = thr;
+                    w.qcnt[m * w.cap + q] = 0;
+                }
+            }
+            continue;
+        }
+        // exact values of the listed entries whose bucket reaches thr (an empty slot,
+        // index outside [0, V), never does)
+        for (int c = 0; c < nc; ++c) {
+            double x = kTkEmpty;
+            const int v = ci[wid][c];
+            if (bucket_ub(cv[wid][c]) >= thr && (unsigned)v < (unsigned)a.V)
+                x = wave_dot_exact(h, W + (int64_t)v * d, d, lane);
+            if (lane == 0) cx[wid][c] = x;
         }
         __builtin_amdgcn_wave_barrier();
-    }
-    if (overflow && lane == 0) {
-        const int q = atomicAdd(&sched->n_topk_queued, 1);
-        if (q < cap) queue[q] = (int32_t)j;
+        rank_and_write(cx[wid], ci[wid], nc, lane, j, m, w.list_v, w.list_i);
+        __builtin_amdgcn_wave_barrier();
     }
 }
 
-// 8 consecutive bf16 of two rows: sum of products into acc (v_dot2, exact products).
-typedef __bf16 tk_bf16x2 __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ float tk_dot8(const uint4 &p, const uint4 &q, float acc) {
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(tk_bf16x2, p.x),
-                                          __builtin_bit_cast(tk_bf16x2, q.x), acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(tk_bf16x2, p.y),
-                                          __builtin_bit_cast(tk_bf16x2, q.y), acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(tk_bf16x2, p.z),
-                                          __builtin_bit_cast(tk_bf16x2, q.z), acc, false);
-    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(tk_bf16x2, p.w),
-                                          __builtin_bit_cast(tk_bf16x2, q.w), acc, false);
-    return acc;
-}
-
-// Work item (queued row, model, vocabulary chunk): every logit of the chunk in fp32
-// (8 lanes per weight row), the chunk's 16 largest kept per 8-lane group and merged
-// over the workgroup. The queued row varies fastest over the items, so workgroups
-// running side by side read the same weight chunk.
-__global__ void __launch_bounds__(TKR_THREADS)
-topk_rescan_kernel(ScoreArgs a, const int32_t *__restrict__ queue, int cap, int n_chunks,
-                   TkEntry *__restrict__ out) {
-    extern __shared__ __attribute__((aligned(16))) uint16_t tk_h[];   // [d] bf16
-    __shared__ float red_v[TKR_GROUPS][TOPK_K];
-    __shared__ int red_i[TKR_GROUPS][TOPK_K];
-    const int nq_all = a.sched->n_topk_queued;
-    const int nq = nq_all < cap ? nq_all : cap;
-    const int64_t n_items = (int64_t)nq * 2 * n_chunks;
-    const int tid = threadIdx.x, g8 = tid & 7, grp = tid >> 3;
-    for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
-        const int q = (int)(item % nq);
-        const int c = (int)((item / nq) % n_chunks);
-        const int m = (int)(item / ((int64_t)nq * n_chunks));
+// Work item (model, 64 queued rows, 128 vocabulary rows): the fp32 logits by MFMA
+// (32x32x16 bf16; vocabulary rows are the A operand, queued rows the B operand, both
+// read straight from memory), the indices of those >= the pair's threshold kept. The
+// K order inside a 64-wide step is permuted the same way for both operands: lane
+// half hf takes k in [32 hf + 8 s, 32 hf + 8 s + 8) at sub-step s, so each lane reads
+// 64 contiguous bytes of its row per step.
+__global__ void __launch_bounds__(256)
+topk_filter_kernel(ScoreArgs a, TopkWork w) {
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    const int hf = lane >> 5, c32 = lane & 31;
+    const int n_vt = (a.V + TKF_VR - 1) / TKF_VR;
+    int nq[2], nqb[2];
+    for (int m = 0; m < 2; ++m) {
+        const int n = a.sched->n_tkq[m];
+        nq[m] = n < w.cap ? n : w.cap;
+        nqb[m] = (nq[m] + TKF_QB - 1) / TKF_QB;
+    }
+    const int64_t items0 = (int64_t)nqb[0] * n_vt;
+    const int64_t items = items0 + (int64_t)nqb[1] * n_vt;
+    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
+        const int m = it < items0 ? 0 : 1;
+        const int64_t rel = m ? it - items0 : it;
+        const int qb = (int)(rel % nqb[m]);      // queued batch fastest: a vocabulary
+        const int vt = (int)(rel / nqb[m]);      // tile is read by neighbouring items
         const int d = m ? a.dt : a.ds;
         const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
-        const int64_t g = a.rowmap[queue[q]] & 0x7fffffffu;
+        const uint16_t *H = (const uint16_t *)(m ? a.ht : a.hs);
+        const int r0 = vt * TKF_VR + wid * 32;
+        const int vrow = r0 + c32 < a.V ? r0 + c32 : a.V - 1;
+        const uint16_t *wr = W + (int64_t)vrow * d + 32 * hf;
+        const uint16_t *hr[2];
+        for (int cb = 0; cb < 2; ++cb) {
+            int q = qb * TKF_QB + cb * 32 + c32;
+            q = q < nq[m] ? q : nq[m] - 1;
+            const int64_t g = a.rowmap[w.qj[m * w.cap + q]] & 0x7fffffffu;
+            hr[cb] = H + g * d + 32 * hf;
+        }
+        tk_floatx16 acc[2];
+        acc[0] = tk_floatx16{0.f};
+        acc[1] = tk_floatx16{0.f};
+        for (int k0 = 0; k0 < d; k0 += 64) {
+            uint4 A[4], B0[4], B1[4];
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                A[s] = *(const uint4 *)(wr + k0 + 8 * s);
+                B0[s] = *(const uint4 *)(hr[0] + k0 + 8 * s);
+                B1[s] = *(const uint4 *)(hr[1] + k0 + 8 * s);
+            }
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const tk_bf16x8 av = __builtin_bit_cast(tk_bf16x8, A[s]);
+                acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    av, __builtin_bit_cast(tk_bf16x8, B0[s]), acc[0], 0, 0, 0);
+                acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    av, __builtin_bit_cast(tk_bf16x8, B1[s]), acc[1], 0, 0, 0);
+            }
+        }
+        // lane holds column c32 (a queued row) and rows 8 (r / 4) + 4 hf + r % 4
+        for (int cb = 0; cb < 2; ++cb) {
+            const int q = qb * TKF_QB + cb * 32 + c32;
+            if (q >= nq[m]) continue;
+            const float thr = w.qthr[m * w.cap + q];
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int v = r0 + 8 * (r >> 2) + 4 * hf + (r & 3);
+                if (v < a.V && acc[cb][r] >= thr) {
+                    const int n = atomicAdd(&w.qcnt[m * w.cap + q], 1);
+                    if (n < TK_CAP) w.cand[((int64_t)m * w.cap + q) * TK_CAP + n] = v;
+                }
+            }
+        }
+    }
+}
+
+// One wavefront per queued pair: exact values of its kept indices, ranked. A pair
+// with more indices than were kept goes to the exhaustive scan.
+__global__ void __launch_bounds__(256)
+topk_exact_kernel(ScoreArgs a, TopkWork w) {
+    __shared__ double cx[4][TK_CAP];
+    __shared__ int ci[4][TK_CAP];
+    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+    Sched *sched = const_cast<Sched *>(a.sched);
+    int nq[2];
+    for (int m = 0; m < 2; ++m) {
+        const int n = sched->n_tkq[m];
+        nq[m] = n < w.cap ? n : w.cap;
+    }
+    for (int64_t p = (int64_t)blockIdx.x * 4 + wid; p < nq[0] + nq[1];
+         p += (int64_t)gridDim.x * 4) {
+        const int m = p < nq[0] ? 0 : 1;
+        const int q = (int)(m ? p - nq[0] : p);
+        const int n = w.qcnt[m * w.cap + q];
+        const int64_t j = w.qj[m * w.cap + q];
+        if (n > TK_CAP) {
+            if (lane == 0) {
+                const int f = atomicAdd(&sched->n_tk_fb, 1);
+                w.fb[f] = m * w.cap + q;
+            }
+            continue;
+        }
+        const int d = m ? a.dt : a.ds;
+        const int64_t g = a.rowmap[j] & 0x7fffffffu;
+        const uint16_t *h = (const uint16_t *)(m ? a.ht : a.hs) + g * d;
+        const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
+        const int32_t *cd = w.cand + ((int64_t)m * w.cap + q) * TK_CAP;
+        for (int c = 0; c < n; ++c) {
+            const int v = cd[c];
+            const double x = wave_dot_exact(h, W + (int64_t)v * d, d, lane);
+            if (lane == 0) { cx[wid][c] = x; ci[wid][c] = v; }
+        }
+        __builtin_amdgcn_wave_barrier();
+        rank_and_write(cx[wid], ci[wid], n, lane, j, m, w.list_v, w.list_i);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// One workgroup per pair of the exhaustive scan: every exact logit of the row (8 lanes
+// per vocabulary row, fp64 sums), a top-16 per 8-lane group, merged over the group.
+__global__ void __launch_bounds__(TKS_THREADS)
+topk_scan_kernel(ScoreArgs a, TopkWork w) {
+    extern __shared__ __attribute__((aligned(16))) uint16_t tk_h[];   // [d] bf16
+    __shared__ double red_v[TKS_GROUPS][TOPK_K];
+    __shared__ int red_i[TKS_GROUPS][TOPK_K];
+    const int nfb = a.sched->n_tk_fb;
+    const int tid = threadIdx.x, g8 = tid & 7, grp = tid >> 3;
+    for (int e = blockIdx.x; e < nfb; e += gridDim.x) {
+        const int code = w.fb[e];
+        const int m = code >= w.cap ? 1 : 0;
+        const int q = code - m * w.cap;
+        const int64_t j = w.qj[m * w.cap + q];
+        const int d = m ? a.dt : a.ds;
+        const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
+        const int64_t g = a.rowmap[j] & 0x7fffffffu;
         const uint16_t *h = (const uint16_t *)(m ? a.ht : a.hs) + g * d;
         __syncthreads();
-        for (int k = tid; k < d; k += TKR_THREADS) tk_h[k] = h[k];
+        for (int k = tid * 8; k < d; k += TKS_THREADS * 8)
+            *(uint4 *)(tk_h + k) = *(const uint4 *)(h + k);
         __syncthreads();
-        float lv[TOPK_K];
+        double lv[TOPK_K];
         int li[TOPK_K];
 #pragma unroll
-        for (int e = 0; e < TOPK_K; ++e) { lv[e] = kTkEmpty; li[e] = 0x7fffffff; }
-        const int v_end = (c + 1) * TKR_CHUNK < a.V ? (c + 1) * TKR_CHUNK : a.V;
-        for (int v0 = c * TKR_CHUNK; v0 < v_end; v0 += TKR_GROUPS) {
+        for (int t = 0; t < TOPK_K; ++t) { lv[t] = kTkEmpty; li[t] = kTkNoIdx; }
+        for (int v0 = 0; v0 < a.V; v0 += TKS_GROUPS) {
             const int v = v0 + grp;
-            const bool ok = v < v_end;
-            const uint16_t *wr = W + (int64_t)(ok ? v : v_end - 1) * d;
-            float z = 0.f;
+            const bool ok = v < a.V;
+            const uint16_t *wr = W + (int64_t)(ok ? v : a.V - 1) * d;
+            double z = 0.0;
             for (int k = g8 * 8; k < d; k += 64)
-                z = tk_dot8(*(const uint4 *)(tk_h + k), *(const uint4 *)(wr + k), z);
+                z = dot8_f64(*(const uint4 *)(tk_h + k), *(const uint4 *)(wr + k), z);
             z += __shfl_xor(z, 1);
             z += __shfl_xor(z, 2);
             z += __shfl_xor(z, 4);
-            if (ok && z > lv[TOPK_K - 1]) tk_insert<TOPK_K>(lv, li, z, v);   // v increasing
+            if (ok && tk_before(z, v, lv[TOPK_K - 1], li[TOPK_K - 1]))
+                tk_insert<TOPK_K>(lv, li, z, v);
         }
         if (g8 == 0) {
 #pragma unroll
-            for (int e = 0; e < TOPK_K; ++e) { red_v[grp][e] = lv[e]; red_i[grp][e] = li[e]; }
+            for (int t = 0; t < TOPK_K; ++t) { red_v[grp][t] = lv[t]; red_i[grp][t] = li[t]; }
         }
         __syncthreads();
         if (tid < 64) {   // merge the 32 group lists: lane l < 32 owns group l's list
             int ptr = 0;
-            float cur_v = tid < TKR_GROUPS ? red_v[tid][0] : kTkEmpty;
-            int cur_i = tid < TKR_GROUPS ? red_i[tid][0] : 0x7fffffff;
             for (int r = 0; r < TOPK_K; ++r) {
-                const TkEntry b = wave_best(cur_v, cur_i);
-                if (tid < TKR_GROUPS && cur_v == b.v && cur_i == b.i) {
-                    ++ptr;
-                    cur_v = ptr < TOPK_K ? red_v[tid][ptr] : kTkEmpty;
-                    cur_i = ptr < TOPK_K ? red_i[tid][ptr] : 0x7fffffff;
+                double hv = kTkEmpty;
+                int hi = kTkNoIdx;
+                if (tid < TKS_GROUPS && ptr < TOPK_K) { hv = red_v[tid][ptr]; hi = red_i[tid][ptr]; }
+                double bv = hv;
+                int bi = hi;
+                wave_best(bv, bi);
+                if (tid < TKS_GROUPS && ptr < TOPK_K && hv == bv && hi == bi) ++ptr;
+                if (tid == 0) {
+                    w.list_v[(j * 2 + m) * TOPK_K + r] = (float)bv;
+                    w.list_i[(j * 2 + m) * TOPK_K + r] = bi;
                 }
-                if (tid == 0) out[((int64_t)q * 2 + m) * n_chunks * TOPK_K + (int64_t)c * TOPK_K + r] = b;
             }
         }
-        __syncthreads();
-    }
-}
-
-// One wavefront per (queued row, model): the 16 largest over the chunks' lists.
-__global__ void __launch_bounds__(256)
-topk_rescan_merge_kernel(ScoreArgs a, const int32_t *__restrict__ queue, int cap, int n_chunks,
-                         const TkEntry *__restrict__ res, float *__restrict__ list_v,
-                         int32_t *__restrict__ list_i) {
-    const int lane = threadIdx.x & 63;
-    const int nq_all = a.sched->n_topk_queued;
-    const int nq = nq_all < cap ? nq_all : cap;
-    const int64_t w = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (w >= (int64_t)nq * 2) return;
-    const int q = (int)(w >> 1), m = (int)(w & 1);
-    const TkEntry *r = res + w * n_chunks * TOPK_K;
-    // each lane keeps the 16 best of its chunks (lane, lane + 64, ...); every chunk
-    // list is sorted, so a chunk is read only while its entries still rank in
-    float lv[TOPK_K];
-    int li[TOPK_K];
-#pragma unroll
-    for (int e = 0; e < TOPK_K; ++e) { lv[e] = kTkEmpty; li[e] = 0x7fffffff; }
-    for (int c = lane; c < n_chunks; c += 64)
-        for (int e = 0; e < TOPK_K; ++e) {
-            const TkEntry x = r[(int64_t)c * TOPK_K + e];
-            if (!tk_before(x.v, x.i, lv[TOPK_K - 1], li[TOPK_K - 1])) break;
-            tk_insert<TOPK_K>(lv, li, x.v, x.i);
-        }
-    float mine_v = kTkEmpty;
-    int mine_i = 0x7fffffff;
-    for (int k = 0; k < TOPK_K; ++k) {   // vocabulary indices are unique across chunks
-        const TkEntry b = wave_best(lv[0], li[0]);
-        if (lv[0] == b.v && li[0] == b.i) tk_pop<TOPK_K>(lv, li);
-        if (lane == k) { mine_v = b.v; mine_i = b.i; }
-    }
-    const int64_t j = queue[q];
-    if (lane < TOPK_K) {
-        list_v[(j * 2 + m) * TOPK_K + lane] = mine_v;
-        list_i[(j * 2 + m) * TOPK_K + lane] = mine_i;
     }
 }
 
 // One wavefront per compacted row: the outputs. Rows outside the region get the
 // fixed values of unscored positions (overlap 0, kl_topk +0, indices -1).
-template <typename E>
 __global__ void __launch_bounds__(256)
-topk_output_kernel(ScoreArgs a, const float *__restrict__ lse, const float *__restrict__ list_v,
-                   const int32_t *__restrict__ list_i, float *__restrict__ overlap,
-                   float *__restrict__ kl_topk, int32_t *__restrict__ idx_s,
-                   int32_t *__restrict__ idx_t) {
+topk_output_kernel(ScoreArgs a, TopkWork w, TopkOut o) {
     const int lane = threadIdx.x & 63;
     const int64_t j = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (j >= a.sched->t_valid) return;
@@ -254,85 +414,97 @@ topk_output_kernel(ScoreArgs a, const float *__restrict__ lse, const float *__re
     const int64_t g = rm & 0x7fffffffu;
     if (!(rm >> 31)) {
         if (lane == 0) {
-            if (overlap) overlap[g] = 0.f;
-            if (kl_topk) kl_topk[g] = 0.f;
+            if (o.overlap) o.overlap[g] = 0.f;
+            if (o.kl) o.kl[g] = 0.f;
         }
         if (lane < TOPK_K) {
-            if (idx_s) idx_s[g * TOPK_K + lane] = -1;
-            if (idx_t) idx_t[g * TOPK_K + lane] = -1;
+            if (o.idx_s) o.idx_s[g * TOPK_K + lane] = -1;
+            if (o.idx_t) o.idx_t[g * TOPK_K + lane] = -1;
         }
         return;
     }
-    // An entry outside [0, V) is a list's empty slot: with finite logits every list
-    // fills from real rows; NaN logits (malformed inputs) leave slots empty.
-    int is = lane < TOPK_K ? list_i[(j * 2 + 0) * TOPK_K + lane] : -1;
-    int it = lane < TOPK_K ? list_i[(j * 2 + 1) * TOPK_K + lane] : -1;
+    // An entry outside [0, V) is an empty slot: with finite logits every list fills
+    // from real rows; NaN logits (malformed inputs) leave slots empty.
+    int is = lane < TOPK_K ? w.list_i[(j * 2 + 0) * TOPK_K + lane] : -1;
+    int it = lane < TOPK_K ? w.list_i[(j * 2 + 1) * TOPK_K + lane] : -1;
     if ((unsigned)is >= (unsigned)a.V) is = -1;
     if ((unsigned)it >= (unsigned)a.V) it = -1;
-    const float vt = lane < TOPK_K ? list_v[(j * 2 + 1) * TOPK_K + lane] : 0.f;
+    const float vt = lane < TOPK_K ? w.list_v[(j * 2 + 1) * TOPK_K + lane] : 0.f;
     if (lane < TOPK_K) {
-        if (idx_s) idx_s[g * TOPK_K + lane] = is;
-        if (idx_t) idx_t[g * TOPK_K + lane] = it;
+        if (o.idx_s) o.idx_s[g * TOPK_K + lane] = is;
+        if (o.idx_t) o.idx_t[g * TOPK_K + lane] = it;
     }
-    if (overlap) {
+    if (o.overlap) {
         // lane k < 16 tests whether the teacher's k-th token is among the student's 16
         bool hit = false;
-        for (int k = 0; k < TOPK_K; ++k) hit |= (lane < TOPK_K) && it >= 0 && (__shfl(is, k) == it);
+        for (int k = 0; k < TOPK_K; ++k)
+            hit |= (lane < TOPK_K) && it >= 0 && (__shfl(is, k) == it);
         const int cnt = __popcll(__ballot(hit));
-        if (lane == 0) overlap[g] = (float)cnt / (float)TOPK_K;
+        if (lane == 0) o.overlap[g] = (float)cnt / (float)TOPK_K;
     }
-    if (kl_topk) {
-        const float lse_s = lse[j * 2 + 0], lse_t = lse[j * 2 + 1];
-        const E *hs = (const E *)a.hs + g * a.ds;
-        const E *ws = (const E *)a.ws;
+    if (o.kl) {
+        const float lse_s = w.lse[j * 2 + 0], lse_t = w.lse[j * 2 + 1];
+        const uint16_t *hs = (const uint16_t *)a.hs + g * a.ds;
+        const uint16_t *ws = (const uint16_t *)a.ws;
         float sum = 0.f;
         for (int k = 0; k < TOPK_K; ++k) {       // fixed order: the teacher's ranking
             const int v = __shfl(it, k);
             const float zt = __shfl(vt, k);
-            float zs = 0.f;
-            if (v >= 0) {
-                const E *wr = ws + (int64_t)v * a.ds;
-                for (int e = lane; e < a.ds; e += 64)
-                    zs = fmaf(load_elem(hs, e), load_elem(wr, e), zs);
-                for (int off = 32; off > 0; off >>= 1) zs += __shfl_xor(zs, off);
-            } else {
-                zs = __builtin_nanf("");
-            }
+            const float zs = v >= 0
+                ? (float)wave_dot_exact(hs, ws + (int64_t)v * a.ds, a.ds, lane)
+                : __builtin_nanf("");
             const float lpt = a.sT * zt - lse_t;
             const float lps = a.sS * zs - lse_s;
-            sum = fmaf(fast_exp2(lpt * 1.4426950408889634f), lpt - lps, sum);
+            sum = fmaf(fast_exp2(lpt * kLog2e), lpt - lps, sum);
         }
-        if (lane == 0) kl_topk[g] = sum;
+        if (lane == 0) o.kl[g] = sum;
     }
 }
 
-size_t topk_rescan_bytes(int64_t V, int cap) {
-    const int n_chunks = (int)((V + TKR_CHUNK - 1) / TKR_CHUNK);
-    return (size_t)cap * 2 * n_chunks * TOPK_K * sizeof(TkEntry);
+namespace {
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 }
 
-hipError_t launch_topk(const ScoreArgs &a, bool bf16, const float *lse, float *list_v,
-                       int32_t *list_i, int32_t *queue, int cap, void *rescan_buf,
-                       float *overlap, float *kl_topk, int32_t *idx_s, int32_t *idx_t,
+size_t topk_work_bytes(int64_t cap) {
+    const size_t c = (size_t)cap;
+    return align256(c * 2 * 4) + 2 * align256(c * 2 * TOPK_K * 4) + 3 * align256(c * 2 * 4) +
+           align256(c * 2 * TK_CAP * 4) + align256(c * 2 * 4);
+}
+
+TopkWork topk_carve(void *base, int64_t cap) {
+    const size_t c = (size_t)cap;
+    char *p = (char *)base;
+    TopkWork w;
+    w.cap = (int)cap;
+    w.lse = (float *)p;        p += align256(c * 2 * 4);
+    w.list_v = (float *)p;     p += align256(c * 2 * TOPK_K * 4);
+    w.list_i = (int32_t *)p;   p += align256(c * 2 * TOPK_K * 4);
+    w.qj = (int32_t *)p;       p += align256(c * 2 * 4);
+    w.qthr = (float *)p;       p += align256(c * 2 * 4);
+    w.qcnt = (int32_t *)p;     p += align256(c * 2 * 4);
+    w.cand = (int32_t *)p;     p += align256(c * 2 * TK_CAP * 4);
+    w.fb = (int32_t *)p;
+    return w;
+}
+
+hipError_t launch_topk(const ScoreArgs &a, const TopkWork &w, const TopkOut &out,
                        int64_t max_rows, hipStream_t st) {
     if (max_rows <= 0) return hipSuccess;
-    if (!bf16) return hipErrorInvalidValue;   // the MFMA path only
-    dim3 grid((unsigned)((max_rows + 3) / 4));
-    topk_select_kernel<<<grid, 256, 0, st>>>(a, list_v, list_i, queue, cap);
+    const dim3 rows((unsigned)((max_rows + 3) / 4));
+    topk_select_kernel<<<rows, 256, 0, st>>>(a, w);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const int n_chunks = (int)((a.V + TKR_CHUNK - 1) / TKR_CHUNK);
+    topk_filter_kernel<<<1024, 256, 0, st>>>(a, w);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    topk_exact_kernel<<<256, 256, 0, st>>>(a, w);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     const int dmax = a.ds > a.dt ? a.ds : a.dt;
-    topk_rescan_kernel<<<512, TKR_THREADS, (size_t)dmax * 2, st>>>(a, queue, cap, n_chunks,
-                                                                   (TkEntry *)rescan_buf);
+    topk_scan_kernel<<<256, TKS_THREADS, (size_t)dmax * 2, st>>>(a, w);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    topk_rescan_merge_kernel<<<(unsigned)((2 * (int64_t)cap + 3) / 4), 256, 0, st>>>(
-        a, queue, cap, n_chunks, (const TkEntry *)rescan_buf, list_v, list_i);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    topk_output_kernel<uint16_t><<<grid, 256, 0, st>>>(a, lse, list_v, list_i, overlap, kl_topk,
-                                                       idx_s, idx_t);
+    topk_output_kernel<<<rows, 256, 0, st>>>(a, w, out);
     return hipGetLastError();
 }
 

@@ -100,12 +100,12 @@ def test_topk_partial_requests():
         np.testing.assert_array_equal(one[k], full[k], err_msg=k)
 
 
-def test_ties_and_clustered_sets_go_through_the_exact_rescan():
+def test_ties_and_clustered_sets_go_through_the_vocabulary_filter():
     """Teacher: 32 identical weight columns far above the rest, so the top-16 is a
     tie broken by the lower index (columns 40..55). Student: 41 columns in one
     vocabulary tile with distinct, increasing multiples of one direction, so one
-    split holds the whole top-16 and every row needs the rescan. V = 9000 spans
-    three rescan chunks with a ragged last one."""
+    split holds the whole top-16. Both models of every row need the filter pass
+    over the vocabulary (V = 9000: a ragged last filter tile)."""
     say("top-K ties and rescan")
     wl = custom("tie", num_seqs=2, seq_len=90, vocab=9000, d_student=128, d_teacher=128,
                 cut_rule=("abs", 1, 89))
@@ -126,7 +126,8 @@ def test_ties_and_clustered_sets_go_through_the_exact_rescan():
                   for t in (wl["cu_seqlens"], wl["cut"], wl["valid_len"])],
                 O.REGION_TEACHER)
     rows = np.nonzero(m["in_region"])[0]
-    assert hip["stats"]["topk_rescanned"] == rows.size
+    assert hip["stats"]["topk_filtered"] == 2 * rows.size
+    assert hip["stats"]["topk_scanned"] == 0
     want_t = np.arange(40, 56)
     want_s = 340 - np.arange(16)
     for g in rows:
@@ -135,6 +136,37 @@ def test_ties_and_clustered_sets_go_through_the_exact_rescan():
     assert np.all(hip["overlap"][rows] == 0.0)
     compare(hip, wl, label="tie")
     compare_topk(hip, wl, label="tie", max_ambiguous_frac=1.0)
+
+
+def test_mass_ties_take_the_exhaustive_scan_and_zero_rows_the_fixed_set():
+    """Teacher: 300 identical columns (100..399) far above the rest: more near-tied
+    candidates than the filter keeps, so every row takes the exhaustive exact scan
+    and the set is 100..115. Student: rows with h = 0, whose logits are all exactly 0
+    (set 0..15)."""
+    say("top-K mass ties and zero rows")
+    wl = custom("mass", num_seqs=2, seq_len=40, vocab=2000, d_student=128, d_teacher=128,
+                cut_rule=("abs", 1, 39))
+    wt, ht, hs = wl["w_teacher"], wl["h_teacher"], wl["h_student"]
+    wt[0, :] = 0
+    wt[:, 100:400] = 0
+    wt[0, 100:400] = 1.0
+    ht[:, 0] = 1024.0
+    zero_rows = [3, 4, 5, 50, 51]
+    hs[zero_rows, :] = 0
+    hip = run_hip(wl, outputs=BASE + TOPK)
+    say("mass stats", hip["stats"])
+    m = O.masks(*[t.cpu().numpy() if t is not None else None
+                  for t in (wl["cu_seqlens"], wl["cut"], wl["valid_len"])],
+                O.REGION_TEACHER)
+    rows = np.nonzero(m["in_region"])[0]
+    assert hip["stats"]["topk_scanned"] == rows.size
+    for g in rows:
+        np.testing.assert_array_equal(hip["tk_t"][g], np.arange(100, 116))
+    for g in zero_rows:
+        if m["in_region"][g]:
+            np.testing.assert_array_equal(hip["tk_s"][g], np.arange(16))
+    compare(hip, wl, label="mass")
+    compare_topk(hip, wl, label="mass", max_ambiguous_frac=1.0)
 
 
 def test_topk_on_long_rollout_sampled():
