@@ -24,6 +24,13 @@ What it computes (for every packed position of a batch of stitched rollouts):
     overlap = |TopK_S & TopK_T| / K (the top-K overlap ratio of Sec. 4.1) and the
     top-K KL approximation sum_{v in TopK_T} p_T[v] (log p_T[v] - log p_S[v]) with
     full-vocabulary normalisers (OPD's LogProb top-K = 16, App. A Table 3);
+  * the gradient of L = w_ce * sum_b CE_b + w_kl * sum_t KL(p_T || p_S)[t] (Eq. 1's
+    loss, and the distillation divergence, over the in-region positions) with respect
+    to the student's hidden states and LM-head weight, for the backward pass the
+    student's training step needs after its masked CE (Sec. 3.1; the optimisation of
+    Sec. 3.3): per in-region position, dL/dz_S = w_ce (p_S - onehot(y)) +
+    w_kl (p_S - p_T) for the scaled logits z_S, then dh = s_S W dL/dz_S and
+    dW = s_S sum_t h_t (dL/dz_S)_t^T;
   * masks: a position is valid when it precedes the sequence's valid length, and
     in-region (scored) for the teacher region when it is at or past the cut, the
     prompt and student prefix being masked out of Eq. 1's loss (Sec. 3.1).
@@ -313,3 +320,80 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
     out["valid"] = m["valid"]
     out["in_region"] = m["in_region"]
     return out
+
+
+def grad_logits(z_s, lse_s: float, y: int, w_ce: float = 1.0, z_t=None, lse_t=None,
+                w_kl: float = 0.0) -> np.ndarray:
+    """dL/dz_S of one in-region row, for L = w_ce (-log p_S[y]) + w_kl KL(p_T || p_S)
+    and the scaled student logits z_S: the derivative of -log p_S[y] is
+    p_S - onehot(y); that of KL(p_T || p_S) = sum p_T log p_T - sum p_T log p_S is
+    p_S - p_T (sum p_T = 1)."""
+    p_s = np.exp(_f64(z_s) - lse_s)
+    g = (w_ce + w_kl) * p_s
+    g[int(y)] -= w_ce
+    if w_kl != 0.0:
+        g -= w_kl * np.exp(_f64(z_t) - lse_t)
+    return g
+
+
+def backward(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
+             h_teacher=None, w_teacher=None, scale_student: float = 1.0,
+             scale_teacher: float = 1.0, region: int = REGION_TEACHER, spans=None,
+             w_ce: float = 1.0, w_kl: float = 0.0, rows=None) -> dict:
+    """Gradient of L = w_ce * sum_b CE_b + w_kl * sum_{t in region} KL(p_T || p_S)[t]
+    (CE_b: Eq. 1's loss of sequence b) with respect to the student's hidden states
+    h_S [T, d] and LM-head weight W_S [d, V] (the layout of the workloads).
+
+    z_S = s_S h W, so dL/dh_t = s_S W g_t and dL/dW = s_S sum_t h_t g_t^T with
+    g_t = dL/dz_S at row t (grad_logits) for in-region t and 0 elsewhere.
+
+    Returns grad_h [T, d] (rows outside the region are 0), grad_w [d, V] and the
+    per-row g for the evaluated rows. rows: optional subset of packed rows whose
+    grad_h is formed (grad_w is then None: it needs every in-region row).
+    """
+    m = masks(cu_seqlens, cut, valid_len, region, spans)
+    T = m["valid"].shape[0]
+    hs = _f64(h_student)
+    ws = _f64(w_student)
+    d, V = ws.shape
+    y = np.asarray(targets, dtype=np.int64)
+    inr = np.nonzero(m["in_region"])[0]
+    sel = inr if rows is None else np.intersect1d(np.asarray(rows, dtype=np.int64), inr)
+    grad_h = np.zeros((T, d))
+    grad_w = np.zeros((d, V)) if rows is None else None
+    g_rows = np.zeros((len(sel), V))
+    if w_kl != 0.0:
+        ht, wt = _f64(h_teacher), _f64(w_teacher)
+    chunk = max(1, min(256, (1 << 22) // max(V, 1)))
+    for r0 in range(0, len(sel), chunk):
+        idx = sel[r0:r0 + chunk]
+        zs = project(hs[idx], ws, scale_student)
+        zt = project(ht[idx], wt, scale_teacher) if w_kl != 0.0 else None
+        for i, t in enumerate(idx):
+            lse_s = log_softmax_stats(zs[i])["lse"]
+            if w_kl != 0.0:
+                lse_t = log_softmax_stats(zt[i])["lse"]
+                g = grad_logits(zs[i], lse_s, y[t], w_ce, zt[i], lse_t, w_kl)
+            else:
+                g = grad_logits(zs[i], lse_s, y[t], w_ce)
+            g_rows[r0 + i] = g
+        gb = g_rows[r0:r0 + len(idx)]
+        grad_h[idx] = scale_student * (gb @ ws.T)
+        if grad_w is not None:
+            grad_w += scale_student * (hs[idx].T @ gb)
+    return dict(grad_h=grad_h, grad_w=grad_w, g=g_rows, rows=sel, in_region=m["in_region"])
+
+
+def loss(h_student, w_student, targets, cu_seqlens, cut, valid_len=None, h_teacher=None,
+         w_teacher=None, scale_student: float = 1.0, scale_teacher: float = 1.0,
+         region: int = REGION_TEACHER, spans=None, w_ce: float = 1.0,
+         w_kl: float = 0.0) -> float:
+    """L = w_ce * sum_b CE_b + w_kl * sum_t KL(p_T || p_S)[t] from the forward scoring
+    (the function whose gradient `backward` forms)."""
+    r = score(h_student, w_student, targets, cu_seqlens, cut, valid_len,
+              h_teacher if w_kl != 0.0 else None, w_teacher if w_kl != 0.0 else None,
+              scale_student, scale_teacher, region, spans=spans)
+    total = w_ce * math.fsum(r["ce"].tolist())
+    if w_kl != 0.0:
+        total += w_kl * math.fsum(r["kl"].tolist())
+    return total

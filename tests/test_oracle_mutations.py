@@ -20,6 +20,8 @@ _orig_topk = O.topk_set
 _orig_kltk = O.kl_topk
 _orig_masks = O.masks
 _orig_project = O.project
+_orig_glog = O.grad_logits
+_orig_backward = O.backward
 
 
 def lss_dropped_max(z_row):
@@ -110,6 +112,41 @@ def project_dropped_last_k(h_rows, w, scale=1.0):
     return _orig_project(h, w, scale)
 
 
+def glog_kl_sign(z_s, lse_s, y, w_ce=1.0, z_t=None, lse_t=None, w_kl=0.0):
+    # the KL part as p_T - p_S
+    g = _orig_glog(z_s, lse_s, y, w_ce, z_t, lse_t, 0.0)
+    if w_kl != 0.0:
+        g -= w_kl * (np.exp(np.asarray(z_s, dtype=np.float64) - lse_s) -
+                     np.exp(np.asarray(z_t, dtype=np.float64) - lse_t))
+    return g
+
+
+def glog_target_off_by_one(z_s, lse_s, y, w_ce=1.0, z_t=None, lse_t=None, w_kl=0.0):
+    V = len(z_s)
+    return _orig_glog(z_s, lse_s, (int(y) + 1) % V, w_ce, z_t, lse_t, w_kl)
+
+
+def glog_ce_weight_on_softmax_dropped(z_s, lse_s, y, w_ce=1.0, z_t=None, lse_t=None, w_kl=0.0):
+    g = _orig_glog(z_s, lse_s, y, w_ce, z_t, lse_t, w_kl)
+    return g - w_ce * np.exp(np.asarray(z_s, dtype=np.float64) - lse_s)
+
+
+def backward_no_scale(*args, **kw):
+    r = _orig_backward(*args, **kw)
+    s = kw.get("scale_student", args[8] if len(args) > 8 else 1.0)
+    r["grad_h"] = r["grad_h"] / s
+    return r
+
+
+def backward_grad_w_unscaled_rows(*args, **kw):
+    # dW formed from the logit gradient without the hidden states' scale
+    r = _orig_backward(*args, **kw)
+    if r["grad_w"] is not None:
+        s = kw.get("scale_student", args[8] if len(args) > 8 else 1.0)
+        r["grad_w"] = r["grad_w"] / s
+    return r
+
+
 MUTANTS = [
     ("log_softmax_stats", lss_dropped_max),
     ("log_softmax_stats", lss_last_index),
@@ -126,6 +163,11 @@ MUTANTS = [
     ("topk_overlap", overlap_jaccard),
     ("project", project_no_scale),
     ("project", project_dropped_last_k),
+    ("grad_logits", glog_kl_sign),
+    ("grad_logits", glog_target_off_by_one),
+    ("grad_logits", glog_ce_weight_on_softmax_dropped),
+    ("backward", backward_no_scale),
+    ("backward", backward_grad_w_unscaled_rows),
 ]
 
 PINS = [
@@ -146,6 +188,9 @@ PINS = [
     P.test_topk_worked_example,
     P.test_topk_reduces_to_argmax_and_to_the_full_kl,
     P.test_masked_outputs_exact_values,
+    lambda: [P.test_backward_matches_finite_differences(r, sp) for r, sp in
+             ((O.REGION_TEACHER, None), (O.REGION_SPANS, [[(0, 2), (3, 5)], [(1, 4)]]))],
+    P.test_backward_invariants,
 ]
 
 

@@ -414,3 +414,72 @@ def test_masked_outputs_exact_values():
     assert not np.any(np.signbit(out["kl"][outside]))
     assert out["t_valid"] == 8 + 0 + 13 and out["n_scored"] == 4 + 0 + 6
     assert out["ce"][1] == 0.0
+
+
+# ------------------------------------------------------------------ backward (grad)
+def _tiny_batch(seed, V=11, d_s=4, d_t=3, lens=(5, 7)):
+    rng = np.random.default_rng(seed)
+    T = sum(lens)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int64)
+    return dict(h_s=rng.standard_normal((T, d_s)), w_s=rng.standard_normal((d_s, V)),
+                h_t=rng.standard_normal((T, d_t)), w_t=rng.standard_normal((d_t, V)),
+                y=rng.integers(0, V, T), cu=cu, cut=np.array([2, 3]),
+                vl=np.array([lens[0], lens[1] - 1]))
+
+
+def _loss(b, h_s, w_s, region, spans, w_ce, w_kl, s_s, s_t):
+    return O.loss(h_s, w_s, b["y"], b["cu"], b["cut"], b["vl"], b["h_t"], b["w_t"], s_s, s_t,
+                  region, spans, w_ce, w_kl)
+
+
+@pytest.mark.parametrize("region,spans", [(O.REGION_TEACHER, None), (O.REGION_ALL, None),
+                                          (O.REGION_SPANS, [[(0, 2), (3, 5)], [(1, 4)]])])
+def test_backward_matches_finite_differences(region, spans):
+    """dL/dh_S and dL/dW_S against central differences of the oracle's forward loss
+    L = w_ce sum_b CE_b + w_kl sum_t KL(p_T || p_S)[t] (Eq. 1 and the distillation
+    divergence), with two different logit scales."""
+    b = _tiny_batch(3)
+    w_ce, w_kl, s_s, s_t = 1.0, 0.7, 2.0, 1.5
+    g = O.backward(b["h_s"], b["w_s"], b["y"], b["cu"], b["cut"], b["vl"], b["h_t"], b["w_t"],
+                   s_s, s_t, region, spans, w_ce, w_kl)
+    eps = 1e-6
+    for arr, grad in (("h", g["grad_h"]), ("w", g["grad_w"])):
+        base = b["h_s"] if arr == "h" else b["w_s"]
+        num = np.zeros_like(base)
+        for idx in np.ndindex(base.shape):
+            plus, minus = base.copy(), base.copy()
+            plus[idx] += eps
+            minus[idx] -= eps
+            hp, wp = (plus, b["w_s"]) if arr == "h" else (b["h_s"], plus)
+            hm, wm = (minus, b["w_s"]) if arr == "h" else (b["h_s"], minus)
+            num[idx] = (_loss(b, hp, wp, region, spans, w_ce, w_kl, s_s, s_t) -
+                        _loss(b, hm, wm, region, spans, w_ce, w_kl, s_s, s_t)) / (2 * eps)
+        np.testing.assert_allclose(grad, num, rtol=1e-6, atol=1e-7, err_msg=arr)
+    # positions outside the region get no gradient
+    out = ~g["in_region"]
+    assert np.all(g["grad_h"][out] == 0.0)
+
+
+def test_backward_invariants():
+    """Every row's dL/dz sums to 0 over the vocabulary (both distributions sum to 1),
+    so dW's rows sum to 0; the KL part vanishes for identical models and the whole
+    gradient for an empty region."""
+    b = _tiny_batch(5)
+    g = O.backward(b["h_s"], b["w_s"], b["y"], b["cu"], b["cut"], b["vl"], b["h_t"], b["w_t"],
+                   1.5, 1.0, O.REGION_TEACHER, None, 0.8, 0.3)
+    np.testing.assert_allclose(g["g"].sum(axis=1), 0.0, atol=1e-12)
+    np.testing.assert_allclose(g["grad_w"].sum(axis=1), 0.0, atol=1e-12)
+    # CE part alone: the target entry is p_S[y] - 1 < 0, every other entry p_S > 0
+    g1 = O.backward(b["h_s"], b["w_s"], b["y"], b["cu"], b["cut"], b["vl"], scale_student=1.5,
+                    w_ce=1.0, w_kl=0.0)
+    for i, t in enumerate(g1["rows"]):
+        row = g1["g"][i]
+        assert row[b["y"][t]] < 0 and np.all(np.delete(row, b["y"][t]) > 0)
+    # teacher == student (same hidden states, weights and scale), KL only: no gradient
+    g2 = O.backward(b["h_s"], b["w_s"], b["y"], b["cu"], b["cut"], b["vl"], b["h_s"], b["w_s"],
+                    1.5, 1.5, O.REGION_ALL, None, 0.0, 1.0)
+    assert np.abs(g2["grad_h"]).max() < 1e-14 and np.abs(g2["grad_w"]).max() < 1e-14
+    # empty region: cut at the end of every sequence
+    g3 = O.backward(b["h_s"], b["w_s"], b["y"], b["cu"], np.array([5, 7]), b["vl"],
+                    scale_student=1.0)
+    assert not g3["grad_h"].any() and not g3["grad_w"].any()
