@@ -84,6 +84,11 @@ def main():
     ap.add_argument("--topk", action="store_true",
                     help="also form the top-16 statistics (overlap ratio, top-16 KL and both "
                          "index sets; OLIVE_FLAG_TOPK)")
+    ap.add_argument("--backward", action="store_true",
+                    help="time olive_score_backward instead (dL/dh_S and dL/dW_S of Eq. 1's "
+                         "summed loss, plus --backward-kl times the summed KL)")
+    ap.add_argument("--backward-kl", type=float, default=0.0, metavar="W",
+                    help="KL weight of the --backward loss (default 0: Eq. 1 alone)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 3 plain device copies of BYTES bytes (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -118,6 +123,9 @@ def main():
     T = wl["total_positions"]
     B = spec.num_seqs
     log("workload ready in %.1fs: T=%d" % (time.time() - t0, T))
+    if args.backward:
+        bench_backward(args, wl, L)
+        return
     desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher,
                        L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
                        wl["scale_student"], wl["scale_teacher"], max_positions=T, max_seqs=B,
@@ -218,6 +226,68 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) on a bounded sample ...")
         out["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def bench_backward(args, wl, L):
+    """One olive_score_backward call per step: the forward normalisers of the scored
+    rows, the logit gradient and the two products, both gradients requested."""
+    import torch
+    spec = wl["spec"]
+    T = wl["total_positions"]
+    B = spec.num_seqs
+    desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher, L.OLIVE_BF16, L.OLIVE_W_DV,
+                       wl["scale_student"], wl["scale_teacher"], max_positions=T, max_seqs=B,
+                       flags=L.OLIVE_FLAG_BACKWARD)
+    stream = torch.cuda.current_stream()
+    ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"], stream)
+    dev = wl["h_student"].device
+    gh = torch.empty((T, spec.d_student), dtype=torch.float32, device=dev)
+    gw = torch.empty((spec.d_student, spec.vocab), dtype=torch.float32, device=dev)
+    use_spans = wl.get("spans") is not None
+    batch = L.make_batch(wl["cu_seqlens"], None if use_spans else wl["cut"], wl["targets"],
+                         wl["h_student"], wl["h_teacher"], wl["valid_len"],
+                         L.OLIVE_REGION_SPANS if use_spans else L.OLIVE_REGION_TEACHER)
+    spans = L.make_spans(wl["span_offsets"], wl["span_pairs"]) if use_spans else None
+    counts = torch.zeros(2, dtype=torch.int64, device=dev)
+    g = L.make_grad_outputs(1.0, args.backward_kl, gh, gw, counts)
+
+    def step():
+        L.olive_score_backward(ctx, batch, g, spans=spans, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log("warmup done")
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / args.steps
+    err = L.olive_score_last_error(ctx)
+    L.olive_score_free(ctx)
+    R = int(counts[0].item())
+    dt = spec.d_teacher if args.backward_kl else 0
+    # forward normalisers and the logit-gradient pass each project both models; the
+    # two products are 2 R V d_S each
+    flops = 2.0 * R * spec.vocab * (2 * (spec.d_student + dt) + 2 * spec.d_student)
+    log("timed %d backward steps: %.3f ms/step, err %d" % (args.steps, ms_step, err))
+    out = {
+        "metric": "scored positions/sec, backward (dL/dh_S, dL/dW_S) of the masked CE",
+        "value": R / (ms_step * 1e-3), "unit": "positions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; random hidden states and weights of the workload's shapes)",
+        "config": {"workload": args.workload, "scored_positions": R, "vocab": spec.vocab,
+                   "d_student": spec.d_student, "d_teacher": spec.d_teacher,
+                   "w_ce": 1.0, "w_kl": args.backward_kl,
+                   "step_tflops": flops / (ms_step * 1e-3) / 1e12,
+                   "pct_bf16_peak_step": 100.0 * flops / (ms_step * 1e-3) / 1e12 /
+                   PEAK_BF16_TFLOPS},
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -97,6 +97,11 @@ typedef struct {
  * 512 <= V <= 2^23 (else init returns E_UNSUPPORTED). The workspace holds about
  * max_positions x 6.7 KB of device memory. */
 #define OLIVE_FLAG_TOPK 4
+/* Reserve the workspace of olive_score_backward. Needs a bf16 context on which the
+ * MFMA kernel applies (else init returns E_UNSUPPORTED). The workspace holds about
+ * 4 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
+ * (5.6 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
+#define OLIVE_FLAG_BACKWARD 8
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */
 typedef struct {
@@ -238,6 +243,44 @@ olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
 olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
                                      const olive_spans *spans, const olive_score_outputs *out,
                                      void *hip_stream);
+
+/*
+ * Gradient outputs of olive_score_backward. L = w_ce * sum_b CE_b (Eq. 1's loss, summed
+ * over the sequences) + w_kl * sum over the region's positions of KL(p_T || p_S), the
+ * loss of the student's training step after its masked CE (Sec. 3.1; the optimisation
+ * of Sec. 3.3). Device buffers, caller-owned, overwritten.
+ */
+typedef struct {
+    int32_t size;                /* host: sizeof(olive_grad_outputs) (checked) */
+    int32_t flags;               /* 0 */
+    float w_ce;                  /* weight of the CE sum, finite */
+    float w_kl;                  /* weight of the KL sum, finite; 0 leaves the teacher out
+                                    (its hidden states may then be NULL) */
+    float *grad_h_student;       /* [T][d_S] fp32 or NULL: dL/dh_S, +0.0 at positions
+                                    outside the region or past the valid length */
+    float *grad_w_student;       /* fp32 or NULL: dL/dW_S in the context's weight layout,
+                                    [d_S][V] (OLIVE_W_DV) or [V][d_S] (OLIVE_W_VD) */
+    int64_t *counts;             /* [2] int64 or NULL: scored and valid positions */
+} olive_grad_outputs;
+
+/*
+ * Backward pass of the student's loss: dL/dh_S and dL/dW_S for the scaled logits
+ * z_S = s_S h_S W_S. Per scored position the logit gradient is
+ * w_ce (p_S - onehot(y)) + w_kl (p_S - p_T); it is formed in one fused pass over the
+ * vocabulary (recomputing both models' logits from the forward normalisers) and held
+ * in bf16 (round to nearest even) as the operand of the two products
+ * dL/dh = s_S g W^T and dL/dW = s_S h^T g, which accumulate in fp32.
+ * spans: NULL, or the scored spans when b->region is OLIVE_REGION_SPANS.
+ * Errors: E_NULL (g, or both gradient pointers, NULL; a required batch pointer NULL),
+ * E_RANGE (g->size or flags wrong, a weight not finite, region / spans as for
+ * olive_score_batch_spans), E_UNSUPPORTED (no OLIVE_FLAG_BACKWARD at init; w_kl != 0
+ * without a teacher; hidden states not 16-byte aligned), E_SHAPE as olive_kl_masked.
+ * Content errors on the device set the error word as in the forward calls and make
+ * the gradients of the affected rows (and so dL/dW) NaN.
+ */
+olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,
+                                  const olive_spans *spans, const olive_grad_outputs *g,
+                                  void *hip_stream);
 
 /* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
 olive_status olive_score_free(olive_score_ctx *ctx);

@@ -339,7 +339,8 @@ def grad_logits(z_s, lse_s: float, y: int, w_ce: float = 1.0, z_t=None, lse_t=No
 def backward(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
              h_teacher=None, w_teacher=None, scale_student: float = 1.0,
              scale_teacher: float = 1.0, region: int = REGION_TEACHER, spans=None,
-             w_ce: float = 1.0, w_kl: float = 0.0, rows=None) -> dict:
+             w_ce: float = 1.0, w_kl: float = 0.0, rows=None, cols=None,
+             keep_g: bool = True) -> dict:
     """Gradient of L = w_ce * sum_b CE_b + w_kl * sum_{t in region} KL(p_T || p_S)[t]
     (CE_b: Eq. 1's loss of sequence b) with respect to the student's hidden states
     h_S [T, d] and LM-head weight W_S [d, V] (the layout of the workloads).
@@ -349,7 +350,9 @@ def backward(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
 
     Returns grad_h [T, d] (rows outside the region are 0), grad_w [d, V] and the
     per-row g for the evaluated rows. rows: optional subset of packed rows whose
-    grad_h is formed (grad_w is then None: it needs every in-region row).
+    grad_h is formed (grad_w is then None: it needs every in-region row). cols:
+    optional vocabulary columns of grad_w to keep (grad_w is then [d, len(cols)]).
+    keep_g: keep the per-row g (off for large batches).
     """
     m = masks(cu_seqlens, cut, valid_len, region, spans)
     T = m["valid"].shape[0]
@@ -360,8 +363,9 @@ def backward(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
     inr = np.nonzero(m["in_region"])[0]
     sel = inr if rows is None else np.intersect1d(np.asarray(rows, dtype=np.int64), inr)
     grad_h = np.zeros((T, d))
-    grad_w = np.zeros((d, V)) if rows is None else None
-    g_rows = np.zeros((len(sel), V))
+    cols = None if cols is None else np.asarray(cols, dtype=np.int64)
+    grad_w = None if rows is not None else np.zeros((d, V if cols is None else len(cols)))
+    g_rows = np.zeros((len(sel), V)) if keep_g else None
     if w_kl != 0.0:
         ht, wt = _f64(h_teacher), _f64(w_teacher)
     chunk = max(1, min(256, (1 << 22) // max(V, 1)))
@@ -369,18 +373,19 @@ def backward(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
         idx = sel[r0:r0 + chunk]
         zs = project(hs[idx], ws, scale_student)
         zt = project(ht[idx], wt, scale_teacher) if w_kl != 0.0 else None
+        gb = np.zeros((len(idx), V))
         for i, t in enumerate(idx):
             lse_s = log_softmax_stats(zs[i])["lse"]
             if w_kl != 0.0:
                 lse_t = log_softmax_stats(zt[i])["lse"]
-                g = grad_logits(zs[i], lse_s, y[t], w_ce, zt[i], lse_t, w_kl)
+                gb[i] = grad_logits(zs[i], lse_s, y[t], w_ce, zt[i], lse_t, w_kl)
             else:
-                g = grad_logits(zs[i], lse_s, y[t], w_ce)
-            g_rows[r0 + i] = g
-        gb = g_rows[r0:r0 + len(idx)]
+                gb[i] = grad_logits(zs[i], lse_s, y[t], w_ce)
+        if g_rows is not None:
+            g_rows[r0:r0 + len(idx)] = gb
         grad_h[idx] = scale_student * (gb @ ws.T)
         if grad_w is not None:
-            grad_w += scale_student * (hs[idx].T @ gb)
+            grad_w += scale_student * (hs[idx].T @ (gb if cols is None else gb[:, cols]))
     return dict(grad_h=grad_h, grad_w=grad_w, g=g_rows, rows=sel, in_region=m["in_region"])
 
 

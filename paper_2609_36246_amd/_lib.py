@@ -36,6 +36,7 @@ OLIVE_REGION_SPANS = 3
 OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
 OLIVE_FLAG_TOPK = 4
+OLIVE_FLAG_BACKWARD = 8
 OLIVE_TOPK = 16
 OLIVE_OUT_REGION_ONLY = 1
 
@@ -64,6 +65,13 @@ class olive_score_outputs(ctypes.Structure):
                 ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p),
                 ("topk_overlap", ctypes.c_void_p), ("kl_topk", ctypes.c_void_p),
                 ("topk_student", ctypes.c_void_p), ("topk_teacher", ctypes.c_void_p)]
+
+
+class olive_grad_outputs(ctypes.Structure):
+    _fields_ = [("size", ctypes.c_int32), ("flags", ctypes.c_int32),
+                ("w_ce", ctypes.c_float), ("w_kl", ctypes.c_float),
+                ("grad_h_student", ctypes.c_void_p), ("grad_w_student", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p)]
 
 
 class olive_spans(ctypes.Structure):
@@ -107,6 +115,10 @@ def load() -> ctypes.CDLL:
                                             ctypes.POINTER(olive_spans),
                                             ctypes.POINTER(olive_score_outputs), vp]
     lib.olive_score_batch_spans.restype = st
+    lib.olive_score_backward.argtypes = [vp, ctypes.POINTER(olive_batch),
+                                         ctypes.POINTER(olive_spans),
+                                         ctypes.POINTER(olive_grad_outputs), vp]
+    lib.olive_score_backward.restype = st
     lib.olive_score_free.argtypes = [vp]
     lib.olive_score_free.restype = st
     lib.olive_status_string.argtypes = [st]
@@ -233,6 +245,27 @@ def make_spans(span_offsets, span_pairs, num_spans: Optional[int] = None) -> oli
     sp.span_offsets = _ptr(span_offsets)
     sp.spans = _ptr(span_pairs) if sp.num_spans > 0 else None
     return sp
+
+
+def make_grad_outputs(w_ce=1.0, w_kl=0.0, grad_h=None, grad_w=None,
+                      counts=None) -> olive_grad_outputs:
+    o = olive_grad_outputs()
+    o.size = ctypes.sizeof(olive_grad_outputs)
+    o.flags = 0
+    o.w_ce, o.w_kl = float(w_ce), float(w_kl)
+    o.grad_h_student, o.grad_w_student = _ptr(grad_h), _ptr(grad_w)
+    o.counts = _ptr(counts)
+    return o
+
+
+def olive_score_backward(ctx, batch: olive_batch, grads: olive_grad_outputs, spans=None,
+                         stream=None, check: bool = True) -> int:
+    s = load().olive_score_backward(ctx, ctypes.byref(batch),
+                                    ctypes.byref(spans) if spans is not None else None,
+                                    ctypes.byref(grads), _stream(stream))
+    if check:
+        _check(s, "olive_score_backward")
+    return s
 
 
 def olive_score_batch_spans(ctx, batch: olive_batch, spans: olive_spans,

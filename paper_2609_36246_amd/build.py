@@ -12,7 +12,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libolive_score.so")
 SOURCES = ["olive_abi.hip", "prep.hip", "score_simple.hip", "score_mfma.hip", "combine.hip",
-           "fixup.hip", "topk.hip"]
+           "fixup.hip", "topk.hip", "gemm_mfma.hip", "backward.hip"]
 ARCH = "gfx950"
 
 

@@ -1,0 +1,74 @@
+// Data movement of the backward pass: the scored hidden rows of a chunk gathered
+// and transposed into the K-contiguous operand of the dL/dW product, and a zero fill.
+#include <hip/hip_runtime.h>
+
+#include "olive_internal.hpp"
+
+namespace olive {
+
+// out[k][t] = h[row(c0 + t)][k] for t < the chunk's scored rows, 0 for the rest of
+// the pitch. One 64 (rows) x 64 (k) tile per workgroup, transposed through LDS.
+__global__ void __launch_bounds__(256)
+gather_t_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restrict__ rowmap,
+                const Sched *__restrict__ sched, int c0, int chunk, int pitch,
+                uint16_t *__restrict__ out) {
+    __shared__ uint16_t tile[64][64 + 8];
+    const int t_all = sched->t_valid - c0;
+    const int t_rows = t_all < 0 ? 0 : (t_all < chunk ? t_all : chunk);
+    const int t0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+    const int tid = threadIdx.x;
+    {
+        const int tl = tid >> 2, kl = (tid & 3) * 16;
+        const int t = t0 + tl;
+        uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
+        if (t < t_rows) {
+            const int64_t g = rowmap[c0 + t] & 0x7fffffffu;
+            const uint4 *src = (const uint4 *)(h + g * d + k0 + kl);
+            a = src[0];
+            b = src[1];
+        }
+        const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            tile[tl][kl + 2 * e] = (uint16_t)(w[e] & 0xffffu);
+            tile[tl][kl + 2 * e + 1] = (uint16_t)(w[e] >> 16);
+        }
+    }
+    __syncthreads();
+    {
+        const int kl = tid >> 2, tl = (tid & 3) * 16;
+        uint32_t w[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            w[e] = (uint32_t)tile[tl + 2 * e][kl] | ((uint32_t)tile[tl + 2 * e + 1][kl] << 16);
+        uint4 *dst = (uint4 *)(out + (int64_t)(k0 + kl) * pitch + t0 + tl);
+        dst[0] = make_uint4(w[0], w[1], w[2], w[3]);
+        dst[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    }
+}
+
+__global__ void __launch_bounds__(256) fill_zero_kernel(float4 *__restrict__ p, int64_t n4) {
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4;
+         i += (int64_t)gridDim.x * 256)
+        p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+hipError_t launch_gather_t(const void *h, int d, const uint32_t *rowmap, const Sched *sched,
+                           int c0, int chunk, int pitch, uint16_t *out, hipStream_t st) {
+    // d and pitch are multiples of 64 (the MFMA path's widths, the chunk pitch)
+    dim3 grid((unsigned)(pitch / 64), (unsigned)(d / 64));
+    gather_t_kernel<<<grid, 256, 0, st>>>((const uint16_t *)h, d, rowmap, sched, c0, chunk,
+                                          pitch, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill(float *p, int64_t n, hipStream_t st) {
+    // n is a multiple of 4 (whole rows of a width that is a multiple of 64)
+    const int64_t n4 = n / 4;
+    const int64_t blocks = (n4 + 255) / 256 < 4096 ? (n4 + 255) / 256 : 4096;
+    if (blocks <= 0) return hipSuccess;
+    fill_zero_kernel<<<(unsigned)blocks, 256, 0, st>>>((float4 *)p, n4);
+    return hipGetLastError();
+}
+
+}  // namespace olive

@@ -118,6 +118,7 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
             if (HAS_T && am_t) am_t[g] = -1;
             if (HAS_T && kl) kl[g] = inr ? qnan : 0.f;
             if (HAS_T && kl_rev) kl_rev[g] = inr ? qnan : 0.f;
+            if (lse_out) { lse_out[j * 2] = qnan; lse_out[j * 2 + 1] = qnan; }
         }
         return;
     }

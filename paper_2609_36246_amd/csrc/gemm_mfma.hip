@@ -1,0 +1,262 @@
+// bf16 GEMM for gfx950 with fp32 accumulation and output:
+//   C (+)= alpha * A * B^T,   A [M][K], B [N][K] bf16, rows K-contiguous,
+// the two GEMMs of the backward pass (dL/dh and dL/dW from the logit gradient).
+//
+// The operand pipeline is the scoring kernel's: a workgroup (4 wavefronts, 2 x 2)
+// owns a 256 x 128 output tile, K advances 64 elements per step, each step's A tile
+// (256 rows x 128 B) and B tile (128 rows x 128 B) land in a 3-stage LDS ring through
+// global->LDS DMAs issued two steps ahead, and v_mfma_f32_32x32x16_bf16 accumulates
+// 128 x 64 per wavefront in AGPRs. Here every lane holds its own row pointers for
+// both operands, so ragged M and N read clamped rows (whose results are dropped).
+//
+// N and K may be read on the device (the scored-row count of a call is known only
+// there); the grid is persistent and every workgroup derives the tile count itself.
+#include <hip/hip_runtime.h>
+
+#include "mfma_pipe.hpp"
+#include "olive_internal.hpp"
+
+namespace olive {
+
+namespace {
+
+struct GLane {
+    int lane, wid, wv, wt, h, l32;
+    int ldsoff[4];
+    const char *ap[W_DMA];   // A row chunk of each of the wave's 8 A DMAs
+    const char *bp[H_DMA];   // B row chunk of each of its 4 B DMAs
+};
+
+struct GFrag {
+    bf16x8 A[4], B[2];
+};
+
+__device__ __forceinline__ void g_issue(const GLane &L, int st, int kk) {
+    const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;
+    const uint32_t la = base + (uint32_t)L.wid * (W_DMA * 1024u);
+    const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
+    const int off = kk * ROWB;
+#pragma unroll
+    for (int i = 0; i < W_DMA; ++i) dma16(L.ap[i] + off, la + i * 1024);
+#pragma unroll
+    for (int i = 0; i < H_DMA; ++i) dma16(L.bp[i] + off, lb + i * 1024);
+}
+
+template <int SUB>
+__device__ __forceinline__ void g_read(const GLane &L, int st, GFrag &F) {
+    const char *stage = g_ring + st * STAGE_BYTES;
+    const char *ab = stage + L.wv * 128 * ROWB + L.ldsoff[SUB];
+    const char *bb = stage + WT_BYTES + L.wt * 64 * ROWB + L.ldsoff[SUB];
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb) F.A[vb] = *(const bf16x8 *)(ab + vb * 32 * ROWB);
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) F.B[cb] = *(const bf16x8 *)(bb + cb * 32 * ROWB);
+}
+
+__device__ __forceinline__ void g_mma(const GFrag &F, floatx16 (&acc)[4][2]) {
+#pragma unroll
+    for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            __builtin_amdgcn_sched_barrier(0);
+            acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[vb], F.B[cb], acc[vb][cb],
+                                                                  0, 0, 0);
+        }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// The 8 MFMAs of one sub-step with the DMAs of one third of the next refill
+// interleaved (4 of the step's 12).
+template <int Q0>
+__device__ __forceinline__ void g_mma_issue(const GFrag &F, floatx16 (&acc)[4][2],
+                                            const GLane &L, uint32_t la, uint32_t lb, int off) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        __builtin_amdgcn_sched_barrier(0);
+        acc[j >> 1][j & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[j >> 1], F.B[j & 1],
+                                                                     acc[j >> 1][j & 1], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);
+        if ((j & 1) == 1) {
+            const int q = Q0 + (j >> 1);   // DMA index 0..11 of the refill
+            if (q < W_DMA) dma16(L.ap[q] + off, la + q * 1024);
+            else dma16(L.bp[q - W_DMA] + off, lb + (q - W_DMA) * 1024);
+        }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+__device__ __forceinline__ void g_arrive() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_imm(DMA_PER_STEP));
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+}
+
+// One step in stage st: barrier, refill the stage of step n-1 with step pk (n+2,
+// saturated at the last step), run the four k16 sub-steps; the last one's fragments
+// stay pending in P.
+template <bool PEND>
+__device__ __forceinline__ void g_step(const GLane &L, int st, int pk, floatx16 (&acc)[4][2],
+                                       GFrag &P) {
+    const int pv = st == 0 ? NST - 1 : st - 1;
+    g_arrive();
+    const uint32_t base = ring_addr() + (uint32_t)pv * STAGE_BYTES;
+    const uint32_t la = base + (uint32_t)L.wid * (W_DMA * 1024u);
+    const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
+    const int off = pk * ROWB;
+    GFrag F0, F1, F2;
+    g_read<0>(L, st, F0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PEND) {
+        g_mma_issue<0>(P, acc, L, la, lb, off);
+        g_read<1>(L, st, F1);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma_issue<4>(F0, acc, L, la, lb, off);
+        g_read<2>(L, st, F2);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma_issue<8>(F1, acc, L, la, lb, off);
+        g_read<3>(L, st, P);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma(F2, acc);
+    } else {
+        g_read<1>(L, st, F1);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma_issue<0>(F0, acc, L, la, lb, off);
+        g_read<2>(L, st, F2);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma_issue<4>(F1, acc, L, la, lb, off);
+        g_read<3>(L, st, P);
+        __builtin_amdgcn_sched_barrier(0);
+        g_mma_issue<8>(F2, acc, L, la, lb, off);
+    }
+}
+
+__device__ __forceinline__ int dev_count(const int32_t *p, int off, int cap, int host) {
+    if (!p) return host;
+    int n = *p - off;
+    n = n < 0 ? 0 : n;
+    return n < cap ? n : cap;
+}
+
+}  // namespace
+
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+gemm_mfma_kernel(GemmArgs g) {
+    const int M = g.M;
+    const int N = dev_count(g.n_dev, g.n_off, g.n_cap, g.N);
+    const int krows = dev_count(g.k_dev, g.k_off, g.k_cap, g.K);
+    const int ksteps = (krows + BK - 1) / BK;
+    if (ksteps == 0 && g.accumulate) return;     // nothing to add
+    const int tm = (M + BV - 1) / BV, tn = (N + BT - 1) / BT;
+    const int64_t n_tiles = (int64_t)tm * tn;
+    GLane L;
+    L.lane = threadIdx.x & 63;
+    L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    L.wv = L.wid & 1;
+    L.wt = L.wid >> 1;
+    L.h = L.lane >> 5;
+    L.l32 = L.lane & 31;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+    const int G = gridDim.x;
+    const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+    const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+
+    for (int64_t q = my; q < n_tiles; q += G) {
+        const int mi = g.m_fast ? (int)(q % tm) : (int)(q / tn);
+        const int ni = g.m_fast ? (int)(q / tm) : (int)(q % tn);
+        const int m0 = mi * BV, n0 = ni * BT;
+        // A DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7
+        // with chunk (lane&7) ^ swz(R); B DMA i rows R = wid*32 + 8i + lane/8.
+#pragma unroll
+        for (int i = 0; i < W_DMA; ++i) {
+            const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
+            const int ch = (L.lane & 7) ^ swz(R);
+            const int r = m0 + R < M ? m0 + R : M - 1;
+            L.ap[i] = g.A + (int64_t)r * g.lda + ch * 16;
+        }
+#pragma unroll
+        for (int i = 0; i < H_DMA; ++i) {
+            const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
+            const int ch = (L.lane & 7) ^ swz(R);
+            const int r = n0 + R < N ? n0 + R : N - 1;
+            L.bp[i] = g.B + (int64_t)r * g.ldb + ch * 16;
+        }
+        floatx16 acc[4][2];
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) acc[vb][cb] = floatx16{0.f};
+
+        if (ksteps > 0) {
+            // prologue: steps 0 and 1 (saturated) into stages 0 and 1
+            g_issue(L, 0, 0);
+            g_issue(L, 1, ksteps > 1 ? 1 : 0);
+            int st = 0;
+            GFrag P;
+            g_step<false>(L, st, 2 < ksteps ? 2 : ksteps - 1, acc, P);
+            st = 1;
+            for (int n = 1; n < ksteps; ++n) {
+                const int pk = n + 2 < ksteps ? n + 2 : ksteps - 1;
+                g_step<true>(L, st, pk, acc, P);
+                st = st + 1 == NST ? 0 : st + 1;
+            }
+            g_mma(P, acc);
+            // every DMA landed (trailing refills included) and every wave is done with
+            // the ring before the next tile's prologue refills it
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __builtin_amdgcn_s_barrier();
+            compiler_fence();
+        }
+
+        // lane holds column n = n0 + wt*64 + cb*32 + l32 and rows
+        // m = m0 + wv*128 + vb*32 + 8*(r/4) + 4*h + r%4
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb) {
+            const int n = n0 + L.wt * 64 + cb * 32 + L.l32;
+            if (n >= N) continue;
+            int64_t orow = n;
+            if (g.rowmap) orow = g.rowmap[g.rowmap_off + n] & 0x7fffffffu;
+#pragma unroll
+            for (int vb = 0; vb < 4; ++vb)
+#pragma unroll
+                for (int rq = 0; rq < 4; ++rq) {
+                    const int mb = m0 + L.wv * 128 + vb * 32 + 8 * rq + 4 * L.h;
+                    float v[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) v[e] = g.alpha * agpr_read(acc[vb][cb][4 * rq + e]);
+                    if (g.trans_out) {
+                        float *c = g.C + orow * g.ldc + mb;
+                        if (mb + 3 < M && ((g.ldc & 3) == 0)) {
+                            float4 o = make_float4(v[0], v[1], v[2], v[3]);
+                            if (g.accumulate) {
+                                const float4 p = *(const float4 *)c;
+                                o.x += p.x; o.y += p.y; o.z += p.z; o.w += p.w;
+                            }
+                            *(float4 *)c = o;
+                        } else {
+                            for (int e = 0; e < 4; ++e)
+                                if (mb + e < M) c[e] = g.accumulate ? c[e] + v[e] : v[e];
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            if (mb + e >= M) continue;
+                            float *c = g.C + (int64_t)(mb + e) * g.ldc + orow;
+                            *c = g.accumulate ? *c + v[e] : v[e];
+                        }
+                    }
+                }
+        }
+    }
+}
+
+hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st) {
+    if (grid <= 0 || g.M <= 0) return hipSuccess;
+    gemm_mfma_kernel<<<grid, 256, 0, st>>>(g);
+    return hipGetLastError();
+}
+
+}  // namespace olive

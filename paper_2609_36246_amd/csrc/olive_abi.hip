@@ -32,6 +32,15 @@ struct olive_score_ctx {
     int32_t *err = nullptr;
     void *tk_buf = nullptr;                     // top-K workspace (OLIVE_FLAG_TOPK)
     TopkWork tkw = {};
+    // backward workspace (OLIVE_FLAG_BACKWARD)
+    bool bw = false;
+    int bw_chunk = 0;                           // scored rows per logit-gradient chunk
+    int64_t bw_vp = 0;                          // V rounded up to 64
+    float *bw_lse = nullptr;                    // [P][2]
+    uint16_t *bw_wt = nullptr;                  // W_S^T [d_S][bw_vp] bf16 (zero padded)
+    uint16_t *bw_dzt = nullptr;                 // [chunk][bw_vp]
+    uint16_t *bw_dzv = nullptr;                 // [V][chunk]
+    uint16_t *bw_hrt = nullptr;                 // [d_S][chunk]
     bool bf16 = false, has_t = false, mfma_ok = false, topk = false;
     int last_kernel = -1, last_grid = 0;
     bool timing = false;
@@ -50,7 +59,7 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_buf};
+                    c->tk_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_dzv, c->bw_hrt};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -67,6 +76,29 @@ olive_status dev_alloc(T **p, size_t bytes) {
 }
 
 olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE_E_HIP; }
+
+constexpr int64_t kBackwardChunk = 8192;   // scored rows per logit-gradient chunk
+
+// W_S^T [d_S][V] with rows padded to bw_vp (zeros), from the [V][d_S] weights the
+// kernels use; the padded columns of the [chunk][bw_vp] gradient buffer are zeroed
+// once (no pass writes them).
+olive_status backward_init(olive_score_ctx *c, hipStream_t st) {
+    const int64_t V = c->desc.vocab, ds = c->desc.d_student;
+    void *tmp = nullptr;
+    olive_status s = dev_alloc(&tmp, (size_t)ds * V * 2);
+    if (s) return s;
+    // repack reads [rows][cols] and writes [cols][rows]: the [V][d_S] weights as rows
+    bool ok = launch_repack(c->ws, tmp, V, ds, 2, st) == hipSuccess &&
+              hipMemsetAsync(c->bw_wt, 0, (size_t)ds * c->bw_vp * 2, st) == hipSuccess &&
+              hipMemcpy2DAsync(c->bw_wt, (size_t)c->bw_vp * 2, tmp, (size_t)V * 2,
+                               (size_t)V * 2, (size_t)ds, hipMemcpyDeviceToDevice,
+                               st) == hipSuccess &&
+              hipMemsetAsync(c->bw_dzt, 0, (size_t)c->bw_chunk * c->bw_vp * 2, st) ==
+                  hipSuccess &&
+              hipStreamSynchronize(st) == hipSuccess;
+    (void)hipFree(tmp);
+    return ok ? OLIVE_OK : OLIVE_E_HIP;
+}
 
 // Top-K lists need two splits at least (16 listed entries) and at most 1024
 // vocabulary tiles per split (the 16-bit row ordinal of a list key).
@@ -189,6 +221,134 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     return OLIVE_OK;
 }
 
+// The backward pass: forward normalisers of the scored rows (region-only forward),
+// then per chunk of scored rows the logit gradient and the two products.
+olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
+                          const olive_grad_outputs *go, hipStream_t st) {
+    const olive_score_desc &d = ctx->desc;
+    if (!b->cu_seqlens || !b->targets || !b->h_student) return OLIVE_E_NULL;
+    if (!spans && !b->cut) return OLIVE_E_NULL;
+    if (b->num_seqs < 1 || b->num_seqs > d.max_seqs) return OLIVE_E_SHAPE;
+    if (b->total_positions < 1 || b->total_positions > d.max_positions) return OLIVE_E_SHAPE;
+    if (spans) {
+        if (b->region != OLIVE_REGION_SPANS) return OLIVE_E_RANGE;
+        if (spans->size != (int32_t)sizeof(olive_spans) || spans->num_spans < 0)
+            return OLIVE_E_RANGE;
+        if (!spans->span_offsets || (spans->num_spans > 0 && !spans->spans)) return OLIVE_E_NULL;
+    } else if (b->region < OLIVE_REGION_TEACHER || b->region > OLIVE_REGION_ALL) {
+        return OLIVE_E_RANGE;
+    }
+    const bool has_t = go->w_kl != 0.f;
+    if (has_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
+    if (((uintptr_t)b->h_student & 15) != 0 || (has_t && ((uintptr_t)b->h_teacher & 15) != 0))
+        return OLIVE_E_UNSUPPORTED;
+    const int64_t T = b->total_positions;
+    const int64_t V = d.vocab;
+    const int n_vtiles = (int)((V + 255) / 256);
+    const int grid = ctx->n_cu;
+    olive_status s = check_hip(launch_prep(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->err,
+                                           go->counts, MFMA_BT, 0, n_vtiles, grid, 1, 1, st));
+    if (s) return s;
+    s = check_hip(launch_rowmap(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
+                                ctx->err, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                nullptr, TopkOut{}, st));
+    if (s) return s;
+    ScoreArgs a;
+    a.hs = b->h_student;
+    a.ht = has_t ? b->h_teacher : nullptr;
+    a.ws = ctx->ws;
+    a.wt = has_t ? ctx->wt : nullptr;
+    a.rowmap = ctx->rowmap;
+    a.sched = ctx->sched;
+    a.part = ctx->part;
+    a.pstride = ctx->pstride;
+    a.V = (int32_t)V;
+    a.ds = d.d_student;
+    a.dt = has_t ? d.d_teacher : 0;
+    a.n_vtiles = n_vtiles;
+    a.sS = d.logit_scale_student;
+    a.sT = has_t ? d.logit_scale_teacher : 1.f;
+    a.cS = a.sS * 1.4426950408889634f;
+    a.cT = a.sT * 1.4426950408889634f;
+    a.wmax_s = ctx->wmax_s;
+    a.wmax_t = ctx->wmax_t;
+    const bool same_scale = has_t && (a.sS == a.sT);
+    s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
+    if (s) return s;
+    s = check_hip(launch_combine(a, true, has_t, same_scale, b->targets, ctx->err, nullptr,
+                                 nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                 ctx->bw_lse, nullptr, 0, T, st));
+    if (s) return s;
+    const int ds = d.d_student;
+    if (go->grad_h_student) {
+        s = check_hip(launch_fill(go->grad_h_student, T * ds, st));
+        if (s) return s;
+    }
+    const int ch = ctx->bw_chunk;
+    for (int64_t c0 = 0; c0 < d.max_positions; c0 += ch) {
+        DzArgs z;
+        z.c0 = (int)c0;
+        z.chunk = ch;
+        z.pitch = ch;
+        z.vp = ctx->bw_vp;
+        z.lse = ctx->bw_lse;
+        z.targets = b->targets;
+        z.w_ce = go->w_ce;
+        z.w_kl = go->w_kl;
+        z.dz_t = ctx->bw_dzt;
+        z.dz_v = ctx->bw_dzv;
+        s = check_hip(launch_score_dz(a, z, has_t, grid, st));
+        if (s) return s;
+        if (go->grad_w_student) {
+            s = check_hip(launch_gather_t(b->h_student, ds, ctx->rowmap, ctx->sched, (int)c0, ch,
+                                          ch, ctx->bw_hrt, st));
+            if (s) return s;
+            GemmArgs g = {};
+            g.A = (const char *)ctx->bw_dzv;        // [V][chunk]: rows v, K = scored rows
+            g.lda = (int64_t)ch * 2;
+            g.B = (const char *)ctx->bw_hrt;        // [d_S][chunk]
+            g.ldb = (int64_t)ch * 2;
+            g.M = (int)V;
+            g.N = ds;
+            g.k_dev = &ctx->sched->t_valid;
+            g.k_off = (int)c0;
+            g.k_cap = ch;
+            g.C = go->grad_w_student;
+            const bool dv = d.w_layout == OLIVE_W_DV;
+            g.trans_out = dv;                       // [d_S][V]: C[k][v]
+            g.ldc = dv ? V : ds;
+            g.alpha = a.sS;
+            g.accumulate = c0 > 0;
+            g.m_fast = false;
+            s = check_hip(launch_gemm(g, grid, st));
+            if (s) return s;
+        }
+        if (go->grad_h_student) {
+            GemmArgs g = {};
+            g.A = (const char *)ctx->bw_wt;         // W_S^T [d_S][vp]: rows k, K = vocabulary
+            g.lda = ctx->bw_vp * 2;
+            g.B = (const char *)ctx->bw_dzt;        // [chunk][vp]
+            g.ldb = ctx->bw_vp * 2;
+            g.M = ds;
+            g.K = (int)ctx->bw_vp;
+            g.n_dev = &ctx->sched->t_valid;
+            g.n_off = (int)c0;
+            g.n_cap = ch;
+            g.C = go->grad_h_student;               // row of scored row n: rowmap[c0 + n]
+            g.ldc = ds;
+            g.rowmap = ctx->rowmap;
+            g.rowmap_off = (int)c0;
+            g.trans_out = true;
+            g.alpha = a.sS;
+            g.accumulate = false;
+            g.m_fast = true;
+            s = check_hip(launch_gemm(g, grid, st));
+            if (s) return s;
+        }
+    }
+    return OLIVE_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -221,7 +381,8 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (d.d_student > 12288 || d.d_teacher > 12288) return OLIVE_E_UNSUPPORTED;
     if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
     if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
-    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK))
+    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK |
+                    OLIVE_FLAG_BACKWARD))
         return OLIVE_E_RANGE;
     if (!w_student) return OLIVE_E_NULL;
     if (d.d_teacher > 0 && !w_teacher) return OLIVE_E_NULL;
@@ -246,6 +407,11 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     c->topk = (d.flags & OLIVE_FLAG_TOPK) != 0;
     if (c->topk && (!c->mfma_ok || !c->has_t || d.vocab < 512 ||
                     d.vocab > (int64_t)MAX_SPLITS * 1024 * MFMA_BV)) {
+        release(c);
+        return OLIVE_E_UNSUPPORTED;
+    }
+    c->bw = (d.flags & OLIVE_FLAG_BACKWARD) != 0;
+    if (c->bw && !c->mfma_ok) {
         release(c);
         return OLIVE_E_UNSUPPORTED;
     }
@@ -279,6 +445,18 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (!s && c->topk) {
         s = dev_alloc(&c->tk_buf, topk_work_bytes(P));
         if (!s) c->tkw = topk_carve(c->tk_buf, P);
+    }
+    if (!s && c->bw) {
+        const int64_t ch = (P + 127) / 128 * 128;
+        c->bw_chunk = (int)(ch < kBackwardChunk ? ch : kBackwardChunk);
+        c->bw_vp = (V + 63) / 64 * 64;
+        const int64_t ds = d.d_student;
+        s = dev_alloc(&c->bw_lse, (size_t)P * 2 * sizeof(float));
+        if (!s) s = dev_alloc(&c->bw_wt, (size_t)ds * c->bw_vp * 2);
+        if (!s) s = dev_alloc(&c->bw_dzt, (size_t)c->bw_chunk * c->bw_vp * 2);
+        if (!s) s = dev_alloc(&c->bw_dzv, (size_t)V * c->bw_chunk * 2);
+        if (!s) s = dev_alloc(&c->bw_hrt, (size_t)ds * c->bw_chunk * 2);
+        if (!s) s = backward_init(c, st);
     }
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
     if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
@@ -379,6 +557,17 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
                (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0,
                topk_of(out));
+}
+
+olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,
+                                  const olive_spans *spans, const olive_grad_outputs *g,
+                                  void *hip_stream) {
+    if (!ctx || !b || !g) return OLIVE_E_NULL;
+    if (g->size != (int32_t)sizeof(olive_grad_outputs) || g->flags != 0) return OLIVE_E_RANGE;
+    if (!std::isfinite(g->w_ce) || !std::isfinite(g->w_kl)) return OLIVE_E_RANGE;
+    if (!g->grad_h_student && !g->grad_w_student) return OLIVE_E_NULL;
+    if (!ctx->bw) return OLIVE_E_UNSUPPORTED;
+    return run_backward(ctx, b, spans, g, (hipStream_t)hip_stream);
 }
 
 olive_status olive_score_free(olive_score_ctx *ctx) {

@@ -104,6 +104,40 @@ struct ScoreArgs {
     float wmax_s, wmax_t;        // largest weight-row L2 norm (top-K rounding bounds)
 };
 
+// Logit-gradient pass of the backward (scored rows [c0, c0 + chunk) of a call).
+struct DzArgs {
+    int c0, chunk;               // first compacted scored row, rows per chunk
+    int pitch;                   // dz_v row pitch in elements (>= chunk rounded up to 64)
+    int64_t vp;                  // dz_t row pitch: V rounded up to 64
+    const float *lse;            // [rows][2] forward log-normalisers per compacted row
+    const int32_t *targets;      // packed realised tokens
+    float w_ce, w_kl;            // loss weights
+    uint16_t *dz_t;              // [chunk][vp] bf16 logit gradient
+    uint16_t *dz_v;              // [V][pitch] the same, transposed
+};
+
+// C (+)= alpha * A * B^T on bf16 rows (K contiguous), fp32 C. N and K are read on the
+// device when their pointers are set: clamp(*p - off, 0, cap).
+struct GemmArgs {
+    const char *A;
+    int64_t lda;                 // bytes between A rows
+    const char *B;
+    int64_t ldb;
+    int M, N, K;
+    const int32_t *n_dev;
+    int n_off, n_cap;
+    const int32_t *k_dev;
+    int k_off, k_cap;
+    float *C;
+    int64_t ldc;                 // elements
+    const uint32_t *rowmap;      // output row of column n: rowmap[rowmap_off + n] (low 31 bits)
+    int rowmap_off;
+    float alpha;
+    bool trans_out;              // C[n][m] instead of C[m][n]
+    bool accumulate;             // C += instead of C =
+    bool m_fast;                 // tile order: M index fastest
+};
+
 // Host-side launchers (each defined beside its kernel).
 hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int elem_bytes,
                          hipStream_t st);
@@ -120,6 +154,12 @@ hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_
                                hipStream_t st);
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
                              bool topk, int grid, hipStream_t st);
+hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,
+                           hipStream_t st);
+hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st);
+hipError_t launch_gather_t(const void *h, int d, const uint32_t *rowmap, const Sched *sched,
+                           int c0, int chunk, int pitch, uint16_t *out, hipStream_t st);
+hipError_t launch_fill(float *p, int64_t n, hipStream_t st);
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,

@@ -29,83 +29,21 @@
 // across position tiles through L2 and the infinity cache, H tiles across splits.
 #include <hip/hip_runtime.h>
 
+#include "mfma_pipe.hpp"
 #include "olive_device.hpp"
 #include "olive_internal.hpp"
 
 namespace olive {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float floatx16 __attribute__((ext_vector_type(16)));
-typedef __attribute__((address_space(3))) void lds_void;
-
-constexpr int BV = MFMA_BV;              // 256
-constexpr int BT = MFMA_BT;              // 128
-constexpr int BK = 64;                   // K elements per pipeline step
-constexpr int ROWB = BK * 2;             // bytes per row per step: one 128-byte line
-constexpr int WT_BYTES = BV * ROWB;      // 32 KB
-constexpr int HT_BYTES = BT * ROWB;      // 16 KB
 // Logit of vocabulary rows outside the tile range: -2^99. A power of two, so that
 // kMasked * c is exact and a block whose running max is kMasked folds to exp2(0) = 1
 // rather than to the rounding residual of the product; z + kMasked rounds back to
 // exactly kMasked for any |z| < 2^74, in both models (their difference is 0).
 constexpr float kMasked = -0x1p99f;
 
-// Ring of NST LDS stages; stage i holds the W tile [256 rows x 128 B] followed by
-// the H tile [128 rows x 128 B] of one K step.
-constexpr int NST = 3;
-constexpr int STAGE_BYTES = WT_BYTES + HT_BYTES;     // 48 KB; 3 stages = 144 KB
-constexpr int W_DMA = WT_BYTES / 1024 / 4;           // 16-byte-per-lane DMAs per wave: 8
-constexpr int H_DMA = HT_BYTES / 1024 / 4;           // 4
-constexpr int DMA_PER_STEP = W_DMA + H_DMA;          // 12
-__shared__ __attribute__((aligned(1024))) char g_ring[NST * STAGE_BYTES];
-
-__device__ __forceinline__ uint32_t ring_addr() {
-    return (uint32_t)(uintptr_t)(lds_void *)g_ring;
-}
-
-// s_waitcnt immediates (gfx9 encoding: vmcnt bits [3:0] and [15:14], expcnt [6:4],
-// lgkmcnt [11:8]): "vmcnt <= n" alone, and together with "lgkmcnt = 0".
-constexpr int vmcnt_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (0xF << 8) | (7 << 4); }
-constexpr int vmcnt_lgkm0_imm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
-
 // max(a, b) for non-NaN operands as one v_med3_f32 (no NaN canonicalisation).
 __device__ __forceinline__ float max2(float a, float b) {
     return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
-}
-
-// 16-byte slot swizzle of a 128-byte stage row: slot = chunk ^ ((row >> 1) & 7).
-// Measured on gfx950 to keep the ds_read_b128 operand fetches (32 rows x 2 chunks
-// per instruction, any of the 4 sub-steps) free of bank conflicts.
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
-
-// Read one accumulator element where it lives (an AGPR). Issuing the read at the
-// point of use keeps the register allocator from copying whole accumulator tuples
-// into VGPRs ahead of the epilogue.
-__device__ __forceinline__ float agpr_read(float x) {
-    float y;
-    asm volatile("v_accvgpr_read_b32 %0, %1" : "=v"(y) : "a"(x));
-    return y;
-}
-
-__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
-
-// One global -> LDS DMA of 16 bytes per lane: lane i's bytes land at the wave-uniform
-// LDS address `l` + 16 i. Issued as inline assembly so that the compiler's wait-count
-// analysis does not see an LDS write in flight (it would then wait for every LDS read
-// with lgkmcnt(0)); completion is ordered by the explicit vmcnt waits and barriers of
-// the pipeline. m0 is written here only: the kernel has no other m0 user.
-__device__ __forceinline__ void dma16(const char *g, uint32_t la) {
-    // The address is wave-uniform by construction; readfirstlane makes that explicit
-    // when register pressure has moved it to a VGPR.
-    la = __builtin_amdgcn_readfirstlane(la);
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-    // s_nop: one wait state between the m0 write and the DMA that reads it.
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(la), "v"(g)
-                 : "memory", "m0");
-#pragma clang diagnostic pop
 }
 
 struct Lane {
@@ -724,12 +662,186 @@ struct Kernel {
             __syncthreads();
         }
     }
+
+    // Logit-gradient pass of the backward: the same units and steps over the scored
+    // rows [c0, c0 + chunk) of the call (compacted, region only), with the fold
+    // replaced by g = (w_ce + w_kl) p_S - w_ce onehot(y) - w_kl p_T, p_X = exp(s_X z_X -
+    // lse_X) with the forward pass's normalisers, stored as bf16 (round to nearest
+    // even) into dz_t [row][v] and dz_v [v][row]. dz_v columns from the chunk's row
+    // count up to its pitch are written as zeros (the K padding of the dW product).
+    static __device__ __forceinline__ void run_dz(ScoreArgs a, DzArgs z) {
+        const int t_all = a.sched->t_valid - z.c0;
+        const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
+        const int n_p = (t_rows + BT - 1) / BT;
+        const int G = gridDim.x;
+        // splits: minimise (rounds of the persistent grid) x (vocabulary tiles per split)
+        const int smax = a.n_vtiles < MAX_SPLITS ? a.n_vtiles : MAX_SPLITS;
+        int ns = 1;
+        int64_t best = -1;
+        for (int sc = 1; sc <= smax; ++sc) {
+            const int64_t cost = (((int64_t)n_p * sc + G - 1) / G) * ((a.n_vtiles + sc - 1) / sc);
+            if (best < 0 || cost < best) { best = cost; ns = sc; }
+        }
+        const int64_t n_units = (int64_t)n_p * ns;
+        Lane L;
+        L.lane = threadIdx.x & 63;
+        L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        L.wv = L.wid & 1;
+        L.wt = L.wid >> 1;
+        L.h = L.lane >> 5;
+        L.l32 = L.lane & 31;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+        const int nS = a.ds / BK, nT = HAS_T ? a.dt / BK : 0;
+        const int spv = nS + nT;
+#pragma unroll
+        for (int par = 0; par < 2; ++par) {
+            const int R0 = L.wid * 8 * W_DMA + (L.lane >> 3);
+            const int ch = (L.lane & 7) ^ swz(R0 + 8 * par);
+            L.wvoff[0][par] = (uint32_t)(R0 * a.ds * 2 + ch * 16);
+            L.wvoff[1][par] = HAS_T ? (uint32_t)(R0 * a.dt * 2 + ch * 16) : 0u;
+        }
+        const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+        const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+        const float wsum = z.w_ce + z.w_kl;
+
+        for (int64_t q = my; q < n_units; q += G) {
+            const int p = (int)(q % n_p), s = (int)(q / n_p);
+#pragma unroll
+            for (int i = 0; i < H_DMA; ++i) {
+                const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
+                const int ch = (L.lane & 7) ^ swz(R);
+                int t = p * BT + R;
+                t = t < t_rows ? t : t_rows - 1;
+                const int64_t g = a.rowmap[z.c0 + t] & 0x7fffffffu;
+                L.hp[0][i] = (const char *)a.hs + g * a.ds * 2 + ch * 16;
+                L.hp[1][i] = HAS_T ? (const char *)a.ht + g * a.dt * 2 + ch * 16 : nullptr;
+            }
+            // the lane's two columns: scored row, normalisers (log2 domain), target
+            int tcol[2];
+            bool ok[2];
+            float l2s[2], l2t[2];
+            int ycol[2];
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                tcol[cb] = p * BT + L.wt * 64 + cb * 32 + L.l32;
+                ok[cb] = tcol[cb] < t_rows;
+                const int j = z.c0 + (ok[cb] ? tcol[cb] : 0);
+                const int64_t g = a.rowmap[j] & 0x7fffffffu;
+                l2s[cb] = ok[cb] ? z.lse[2 * (int64_t)j] * kLog2e : 0.f;
+                l2t[cb] = ok[cb] && HAS_T ? z.lse[2 * (int64_t)j + 1] * kLog2e : 0.f;
+                ycol[cb] = ok[cb] ? z.targets[g] : -1;
+            }
+            const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
+            const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
+            const int total = (vt1 - vt0) * spv;
+            floatx16 accS[4][2], accT[4][2];
+            zero_acc(accS, accT);
+            int ivt = vt0, ir = 0;
+            auto adv_if = [&](bool go) {
+                ir += go ? 1 : 0;
+                const bool wrap = ir == spv;
+                ir = wrap ? 0 : ir;
+                ivt += wrap ? 1 : 0;
+            };
+            auto im = [&]() { return ir < nS ? 0 : 1; };
+            auto ik = [&]() { return ir < nS ? ir : ir - nS; };
+#pragma unroll
+            for (int i = 0; i < NST - 1; ++i) {
+                issue(a, L, i, im(), ik(), ivt);
+                adv_if(i + 1 < total);
+            }
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+            int n = 0, st = 0;
+#define OLIVE_STEPS(ACC_, COUNT_)                                                        \
+            {                                                                            \
+                Frag P;                                                                  \
+                step<false>(a, L, st, im(), ik(), ivt, ACC_, P);                         \
+                adv_if(n + NST < total);                                                 \
+                ++n;                                                                     \
+                st = st + 1 == NST ? 0 : st + 1;                                         \
+                for (int k = 1; k < (COUNT_); ++k) {                                     \
+                    step<true>(a, L, st, im(), ik(), ivt, ACC_, P);                      \
+                    adv_if(n + NST < total);                                             \
+                    ++n;                                                                 \
+                    st = st + 1 == NST ? 0 : st + 1;                                     \
+                }                                                                        \
+                mma(P, ACC_);                                                            \
+                __builtin_amdgcn_sched_barrier(0);                                       \
+            }
+            for (int vt = vt0; vt < vt1; ++vt) {
+                const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+                const int vlo = vt * BV;   // rows below vlo of a shifted last tile: done
+                zero_acc(accS, accT);
+                OLIVE_STEPS(accS, nS)
+                if (HAS_T) OLIVE_STEPS(accT, nT)
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int vb = 0; vb < 4; ++vb) {
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int rq = 0; rq < 4; ++rq) {
+                            const int v0 = row0 + L.wv * 128 + vb * 32 + 8 * rq + 4 * L.h;
+                            uint32_t b[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e) {
+                                const float zs = agpr_read(accS[vb][cb][4 * rq + e]);
+                                float gr = wsum * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
+                                if (HAS_T) {
+                                    const float zt = agpr_read(accT[vb][cb][4 * rq + e]);
+                                    gr = fmaf(-z.w_kl, fast_exp2(fmaf(zt, a.cT, -l2t[cb])), gr);
+                                }
+                                gr -= (v0 + e == ycol[cb]) ? z.w_ce : 0.f;
+                                b[e] = ok[cb] ? f32_to_bf16_rne(gr) : 0u;
+                            }
+                            if (v0 >= vlo) {   // the 4 rows share the test (vlo % 4 == 0)
+                                const int t = tcol[cb];
+#pragma unroll
+                                for (int e = 0; e < 4; ++e)
+                                    if (t < z.pitch)
+                                        z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = (uint16_t)b[e];
+                                if (ok[cb]) {
+                                    uint2 w;
+                                    w.x = b[0] | (b[1] << 16);
+                                    w.y = b[2] | (b[3] << 16);
+                                    *(uint2 *)(z.dz_t + (int64_t)t * z.vp + v0) = w;
+                                }
+                            }
+                        }
+                    }
+            }
+#undef OLIVE_STEPS
+            // every DMA landed and every wave is done with the ring before the next
+            // unit's prologue refills it
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __builtin_amdgcn_s_barrier();
+            compiler_fence();
+        }
+    }
 };
 
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_mfma_kernel(ScoreArgs a) {
     Kernel<HAS_T, SAME, REV, TOPK>::run(a);
+}
+
+template <bool HAS_T>
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+score_dz_kernel(ScoreArgs a, DzArgs z) {
+    Kernel<HAS_T, true, false, false>::run_dz(a, z);
+}
+
+hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,
+                           hipStream_t st) {
+    if (grid <= 0) return hipSuccess;
+    if (has_t)
+        score_dz_kernel<true><<<grid, 256, 0, st>>>(a, z);
+    else
+        score_dz_kernel<false><<<grid, 256, 0, st>>>(a, z);
+    return hipGetLastError();
 }
 
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,

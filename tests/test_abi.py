@@ -35,7 +35,7 @@ def test_header_declares_the_boundary():
     for n in ("olive_score_init", "olive_token_logprobs", "olive_kl_masked",
               "olive_score_free", "olive_status_string", "olive_score_last_error",
               "olive_score_last_stats", "olive_score_kernel_times", "olive_score_batch",
-              "olive_score_batch_spans"):
+              "olive_score_batch_spans", "olive_score_backward"):
         assert n in names
 
 
@@ -54,7 +54,8 @@ def test_status_strings(lib):
     assert "unknown" in L.olive_status_string(99)
 
 
-STRUCTS = ("olive_score_desc", "olive_batch", "olive_score_outputs", "olive_spans")
+STRUCTS = ("olive_score_desc", "olive_batch", "olive_score_outputs", "olive_spans",
+           "olive_grad_outputs")
 
 
 def header_layouts(tmp_path):
@@ -143,6 +144,9 @@ def test_calls_on_null_context(lib):
     assert lib.olive_score_kernel_times(None, f, 1) == L.OLIVE_E_NULL
     o = L.make_outputs()
     assert lib.olive_score_batch(None, ctypes.byref(b), ctypes.byref(o), None) == L.OLIVE_E_NULL
+    gr = L.make_grad_outputs()
+    assert lib.olive_score_backward(None, ctypes.byref(b), None, ctypes.byref(gr),
+                                    None) == L.OLIVE_E_NULL
     sp = L.olive_spans()
     assert lib.olive_score_batch_spans(None, ctypes.byref(b), ctypes.byref(sp), ctypes.byref(o),
                                        None) == L.OLIVE_E_NULL
