@@ -11,6 +11,9 @@
 //
 // N and K may be read on the device (the scored-row count of a call is known only
 // there); the grid is persistent and every workgroup derives the tile count itself.
+// With ksplit = 2 each tile's K range is halved over two work units that add into C
+// with atomics: C must hold zeros (or the value to add to) beforehand, and the sum
+// is still deterministic, as two fp32 additions into the same start value commute.
 #include <hip/hip_runtime.h>
 
 #include "mfma_pipe.hpp"
@@ -150,6 +153,8 @@ gemm_mfma_kernel(GemmArgs g) {
     if (ksteps == 0 && g.accumulate) return;     // nothing to add
     const int tm = (M + BV - 1) / BV, tn = (N + BT - 1) / BT;
     const int64_t n_tiles = (int64_t)tm * tn;
+    const int ksplit = g.ksplit == 2 ? 2 : 1;
+    const int kper = (ksteps + ksplit - 1) / ksplit;
     GLane L;
     L.lane = threadIdx.x & 63;
     L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -163,7 +168,10 @@ gemm_mfma_kernel(GemmArgs g) {
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
     const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
 
-    for (int64_t q = my; q < n_tiles; q += G) {
+    for (int64_t u = my; u < n_tiles * ksplit; u += G) {
+        const int64_t q = u % n_tiles;
+        const int kb = (int)(u / n_tiles) * kper;
+        const int kn = ksteps - kb < kper ? ksteps - kb : kper;   // this unit's steps
         const int mi = g.m_fast ? (int)(q % tm) : (int)(q / tn);
         const int ni = g.m_fast ? (int)(q / tm) : (int)(q % tn);
         const int m0 = mi * BV, n0 = ni * BT;
@@ -189,16 +197,16 @@ gemm_mfma_kernel(GemmArgs g) {
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) acc[vb][cb] = floatx16{0.f};
 
-        if (ksteps > 0) {
+        if (kn > 0) {
             // prologue: steps 0 and 1 (saturated) into stages 0 and 1
-            g_issue(L, 0, 0);
-            g_issue(L, 1, ksteps > 1 ? 1 : 0);
+            g_issue(L, 0, kb);
+            g_issue(L, 1, kb + (kn > 1 ? 1 : 0));
             int st = 0;
             GFrag P;
-            g_step<false>(L, st, 2 < ksteps ? 2 : ksteps - 1, acc, P);
+            g_step<false>(L, st, kb + (2 < kn ? 2 : kn - 1), acc, P);
             st = 1;
-            for (int n = 1; n < ksteps; ++n) {
-                const int pk = n + 2 < ksteps ? n + 2 : ksteps - 1;
+            for (int n = 1; n < kn; ++n) {
+                const int pk = kb + (n + 2 < kn ? n + 2 : kn - 1);
                 g_step<true>(L, st, pk, acc, P);
                 st = st + 1 == NST ? 0 : st + 1;
             }
@@ -227,7 +235,14 @@ gemm_mfma_kernel(GemmArgs g) {
                     float v[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) v[e] = g.alpha * agpr_read(acc[vb][cb][4 * rq + e]);
-                    if (g.trans_out) {
+                    if (ksplit > 1) {
+                        for (int e = 0; e < 4; ++e) {
+                            if (mb + e >= M) continue;
+                            float *c = g.trans_out ? g.C + orow * g.ldc + mb + e
+                                                   : g.C + (int64_t)(mb + e) * g.ldc + orow;
+                            atomicAdd(c, v[e]);
+                        }
+                    } else if (g.trans_out) {
                         float *c = g.C + orow * g.ldc + mb;
                         if (mb + 3 < M && ((g.ldc & 3) == 0)) {
                             float4 o = make_float4(v[0], v[1], v[2], v[3]);

@@ -342,6 +342,9 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
             g.alpha = a.sS;
             g.accumulate = false;
             g.m_fast = true;
+            // d_S / 256 x rows / 128 tiles rarely fill the grid: halve K over two units
+            // (the rows of dL/dh were zero-filled above)
+            g.ksplit = 2;
             s = check_hip(launch_gemm(g, grid, st));
             if (s) return s;
         }

@@ -35,6 +35,12 @@
 
 namespace olive {
 
+// Vocabulary splits that consecutive work units cycle through: the 32 workgroups of an
+// XCD then share 32 / OLIVE_SPLIT_GROUP position tiles x OLIVE_SPLIT_GROUP splits.
+#ifndef OLIVE_SPLIT_GROUP
+#define OLIVE_SPLIT_GROUP 4
+#endif
+
 // Logit of vocabulary rows outside the tile range: -2^99. A power of two, so that
 // kMasked * c is exact and a block whose running max is kMasked folds to exp2(0) = 1
 // rather than to the rounding residual of the product; z + kMasked rounds back to
@@ -414,19 +420,20 @@ struct Kernel {
         const int G = gridDim.x;
         const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
         const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
-        const int nsb = ns >> 2, rem = ns & 3;
-        const int64_t full_units = (int64_t)nsb * 4 * n_p;
+        constexpr int SG = OLIVE_SPLIT_GROUP;
+        const int nsb = ns / SG, rem = ns % SG;
+        const int64_t full_units = (int64_t)nsb * SG * n_p;
 
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
             if (q < full_units) {
-                const int64_t w = q % (4 * (int64_t)n_p);
-                p = (int)(w >> 2);
-                s = (int)(q / (4 * (int64_t)n_p)) * 4 + (int)(w & 3);
+                const int64_t w = q % (SG * (int64_t)n_p);
+                p = (int)(w / SG);
+                s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
             } else {
                 const int64_t w = q - full_units;
                 p = (int)(w / rem);
-                s = nsb * 4 + (int)(w % rem);
+                s = nsb * SG + (int)(w % rem);
             }
             // H DMA i of wave wid fills stage rows R = wid*32 + 8i + lane/8.
 #pragma unroll
