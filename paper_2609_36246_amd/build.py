@@ -12,7 +12,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libolive_score.so")
 SOURCES = ["olive_abi.hip", "prep.hip", "score_simple.hip", "score_mfma.hip", "combine.hip",
-           "fixup.hip", "topk.hip", "gemm_mfma.hip", "backward.hip"]
+           "fixup.hip", "topk.hip", "gemm_mfma.hip", "backward.hip",
+           "filter.hip", "argmax.hip"]
 ARCH = "gfx950"
 
 

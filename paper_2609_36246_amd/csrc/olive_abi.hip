@@ -32,6 +32,8 @@ struct olive_score_ctx {
     int32_t *err = nullptr;
     void *tk_buf = nullptr;                     // top-K workspace (OLIVE_FLAG_TOPK)
     TopkWork tkw = {};
+    void *fx_buf = nullptr;                     // greedy re-decision queue (MFMA path)
+    FilterQueue fxq = {};
     // backward workspace (OLIVE_FLAG_BACKWARD)
     bool bw = false;
     int bw_chunk = 0;                           // scored rows per logit-gradient chunk
@@ -59,7 +61,7 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_dzv, c->bw_hrt};
+                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_dzv, c->bw_hrt};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -205,8 +207,13 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                                  topk ? ctx->tkw.lse : nullptr, flagged, ctx->flag_cap, T, st));
     if (s) return s;
     if (flagged) {
-        s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap, ctx->fx_scratch,
-                                        ctx->wn_s, ctx->wn_t, am_s, has_t ? am_t : nullptr, st));
+        if (mfma)
+            s = check_hip(launch_argmax_fix(a, flagged, ctx->flag_cap, ctx->fxq, am_s,
+                                            has_t ? am_t : nullptr, st));
+        else
+            s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap,
+                                            ctx->fx_scratch, ctx->wn_s, ctx->wn_t, am_s,
+                                            has_t ? am_t : nullptr, st));
         if (s) return s;
     }
     if (topk) {
@@ -447,7 +454,13 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
                                     c->pstride * sizeof(float));
     if (!s && c->topk) {
         s = dev_alloc(&c->tk_buf, topk_work_bytes(P));
-        if (!s) c->tkw = topk_carve(c->tk_buf, P);
+        if (!s) c->tkw = topk_carve(c->tk_buf, P, &c->sched->n_tkq[0], &c->sched->n_tk_fb);
+    }
+    if (!s && c->mfma_ok) {
+        s = dev_alloc(&c->fx_buf, filter_queue_bytes(c->flag_cap, FX_CCAP));
+        if (!s)
+            c->fxq = filter_queue_carve(c->fx_buf, c->flag_cap, FX_CCAP, &c->sched->n_fxq[0],
+                                        &c->sched->n_fx_fb);
     }
     if (!s && c->bw) {
         const int64_t ch = (P + 127) / 128 * 128;
@@ -475,13 +488,13 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         release(c);
         return OLIVE_E_HIP;
     }
-    if (c->topk) {   // the largest row norms bound the rounding of any logit
+    if (c->mfma_ok) {   // the largest row norms bound the rounding of any logit
         if (hipStreamSynchronize(st) != hipSuccess) {
             release(c);
             return OLIVE_E_HIP;
         }
         std::vector<float> wn((size_t)V);
-        for (int m = 0; m < 2; ++m) {
+        for (int m = 0; m < (c->has_t ? 2 : 1); ++m) {
             if (hipMemcpy(wn.data(), m ? c->wn_t : c->wn_s, (size_t)V * sizeof(float),
                           hipMemcpyDeviceToHost) != hipSuccess) {
                 release(c);

@@ -34,22 +34,34 @@ constexpr int F_TK = NFIELDS;
 constexpr int NFIELDS_TOPK = NFIELDS + 2 * TK_FIELDS;
 constexpr int TOPK_K = 16;   // LogProb top-K of the OPD baseline (App. A, Table 3)
 constexpr int TK_CAP = 256;  // candidates kept per (row, model) by the vocabulary filter
+constexpr int FX_CCAP = 64;  // candidates kept per near-tie pair of the greedy re-decision
 
-// Device workspace of the top-K statistics, carved from one allocation (topk_carve):
-// cap = max_positions compacted rows.
+// Queue of (compacted row, model) pairs whose decision needs every vocabulary entry
+// with an fp32 logit at or above a threshold: the MFMA filter fills in their
+// candidates (launch_filter). Carved from one allocation (filter_queue_carve).
+struct FilterQueue {
+    int32_t *n;          // device [2]: queued pairs per model (Sched fields)
+    int32_t *nfb;        // device: pairs sent to the exhaustive scan (a Sched field)
+    int32_t *qj;         // [2][cap] compacted row
+    float *qthr;         // [2][cap] fp32 threshold on the raw logit h . w
+    int32_t *qcnt;       // [2][cap] candidates found (may exceed ccap)
+    int32_t *cand;       // [2][cap][ccap] their vocabulary indices
+    int32_t *fb;         // [2 cap] (model * cap + slot) of the pairs for the exhaustive scan
+    int cap, ccap;
+};
+size_t filter_queue_bytes(int64_t cap, int ccap);
+FilterQueue filter_queue_carve(void *base, int64_t cap, int ccap, int32_t *n, int32_t *nfb);
+
+// Device workspace of the top-K statistics (topk_carve): cap = max_positions rows.
 struct TopkWork {
     float *lse;        // [cap][2] full-vocabulary log-normalisers (combine)
     float *list_v;     // [cap][2][16] the sets: exact logits (fp32) in rank order
     int32_t *list_i;   //               and their vocabulary indices
-    int32_t *qj;       // [2][cap] queued compacted rows per model
-    float *qthr;       // [2][cap] their fp32 candidate thresholds
-    int32_t *qcnt;     // [2][cap] candidates the filter found
-    int32_t *cand;     // [2][cap][TK_CAP] their vocabulary indices
-    int32_t *fb;       // [2 cap] pairs (model * cap + queue slot) for the exhaustive scan
+    FilterQueue fq;    // pairs whose listed candidates do not settle the set
     int cap;
 };
 size_t topk_work_bytes(int64_t cap);
-TopkWork topk_carve(void *base, int64_t cap);
+TopkWork topk_carve(void *base, int64_t cap, int32_t *n, int32_t *nfb);
 
 // Device-side schedule of one call, written by the preparation kernel.
 struct Sched {
@@ -63,7 +75,8 @@ struct Sched {
     int32_t cu_bad;     // cu_seqlens malformed: nothing is scored
     int32_t n_tkq[2];   // (row, model) pairs whose top-K field needs the vocabulary filter
     int32_t n_tk_fb;    // pairs of those that need the exhaustive exact scan
-    int32_t pad;
+    int32_t n_fxq[2];   // near-tie (row, model) pairs of the greedy re-decision (MFMA path)
+    int32_t n_fx_fb;    // pairs of those that need the exhaustive exact scan
 };
 
 // Top-K outputs of a call (null pointers: not requested).
@@ -140,6 +153,7 @@ struct GemmArgs {
 };
 
 // Host-side launchers (each defined beside its kernel).
+hipError_t launch_filter(const ScoreArgs &a, const FilterQueue &q, hipStream_t st);
 hipError_t launch_repack(const void *w_dv, void *w_vd, int64_t d, int64_t V, int elem_bytes,
                          hipStream_t st);
 hipError_t launch_prep(const olive_batch &b, const olive_spans *spans, bool region_only,
@@ -168,6 +182,9 @@ hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_s
                           hipStream_t st);
 hipError_t launch_topk(const ScoreArgs &a, const TopkWork &w, const TopkOut &out,
                        int64_t max_rows, hipStream_t st);
+hipError_t launch_argmax_fix(const ScoreArgs &a, const int32_t *flagged, int flag_cap,
+                             const FilterQueue &q, int32_t *am_s, int32_t *am_t,
+                             hipStream_t st);
 hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
                              void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
                              int32_t *am_t, hipStream_t st);

@@ -17,8 +17,8 @@
 //             floor reaches thr, every such logit is listed: their exact values are
 //             formed and ranked. Otherwise the (row, model) pair is queued with thr;
 //   filter  - for the queued pairs, every fp32 logit of the vocabulary (MFMA, 64
-//             queued rows x 128 vocabulary rows per work item); the indices of those
-//             >= thr are kept (at most TK_CAP per pair);
+//             queued rows x 128 vocabulary rows per work item; filter.hip); the
+//             indices of those >= thr are kept (at most TK_CAP per pair);
 //   exact   - exact values of a pair's kept indices, ranked; a pair with more than
 //             TK_CAP goes to
 //   scan    - every exact logit of the pair's row (one workgroup, fp64 sums);
@@ -26,83 +26,13 @@
 //             top-K KL summed in a fixed order.
 #include <hip/hip_runtime.h>
 
+#include "exact.hpp"
 #include "olive_device.hpp"
 #include "olive_internal.hpp"
 
 namespace olive {
 
 constexpr int TK_CAND = MAX_SPLITS * TK_LIST;   // listed entries of one (row, model)
-constexpr int TKF_QB = 64;                      // queued rows per filter work item
-constexpr int TKF_VR = 128;                     // vocabulary rows per filter work item
-constexpr int TKS_THREADS = 256;                // exhaustive scan
-constexpr int TKS_GROUPS = TKS_THREADS / 8;
-constexpr double kTkEmpty = -0x1p1000;          // empty slot (below every finite logit)
-constexpr int kTkNoIdx = 0x7fffffff;
-
-typedef __bf16 tk_bf16x8 __attribute__((ext_vector_type(8)));
-typedef float tk_floatx16 __attribute__((ext_vector_type(16)));
-
-// (v, i) ranks before (w, j): larger value first, lower index among equals.
-__device__ __forceinline__ bool tk_before(double v, int i, double w, int j) {
-    return v > w || (v == w && i < j);
-}
-
-// Wave-wide best (value, index) of one candidate per lane.
-__device__ __forceinline__ void wave_best(double &v, int &i) {
-    for (int off = 32; off > 0; off >>= 1) {
-        const double ov = __shfl_xor(v, off);
-        const int oi = __shfl_xor(i, off);
-        if (tk_before(ov, oi, v, i)) { v = ov; i = oi; }
-    }
-}
-
-template <int N>
-__device__ __forceinline__ void tk_insert(double (&v)[N], int (&ix)[N], double x, int xi) {
-#pragma unroll
-    for (int j = 0; j < N; ++j) {
-        const bool b = tk_before(x, xi, v[j], ix[j]);
-        const double nv = b ? x : v[j];
-        const int ni = b ? xi : ix[j];
-        x = b ? v[j] : x;
-        xi = b ? ix[j] : xi;
-        v[j] = nv;
-        ix[j] = ni;
-    }
-}
-
-// Sum of the exact products of 8 bf16 pairs, accumulated in fp64.
-__device__ __forceinline__ double dot8_f64(const uint4 &p, const uint4 &q, double acc) {
-    const uint32_t a[4] = {p.x, p.y, p.z, p.w}, b[4] = {q.x, q.y, q.z, q.w};
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        acc += (double)(bf16_bits_to_f32(a[t] & 0xffffu) * bf16_bits_to_f32(b[t] & 0xffffu));
-        acc += (double)(bf16_bits_to_f32(a[t] >> 16) * bf16_bits_to_f32(b[t] >> 16));
-    }
-    return acc;
-}
-
-// Exact logit h . w of one vocabulary row by one wavefront (d a multiple of 8, rows
-// 16-byte aligned); every lane returns the sum.
-__device__ __forceinline__ double wave_dot_exact(const uint16_t *h, const uint16_t *w, int d,
-                                                 int lane) {
-    double acc = 0.0;
-    for (int k = lane * 8; k < d; k += 512)
-        acc = dot8_f64(*(const uint4 *)(h + k), *(const uint4 *)(w + k), acc);
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    return acc;
-}
-
-// |h|^2 in fp32 by one wavefront.
-__device__ __forceinline__ float wave_sumsq(const uint16_t *h, int d, int lane) {
-    float acc = 0.f;
-    for (int k = lane; k < d; k += 64) {
-        const float x = bf16_bits_to_f32(h[k]);
-        acc = fmaf(x, x, acc);
-    }
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-    return acc;
-}
-
 // Rank n <= TK_CAND candidates (exact values cx, indices ci in LDS; kTkEmpty marks a
 // skipped slot) and write the 16 best of row j, model m.
 __device__ __forceinline__ void rank_and_write(const double *cx, const int *ci, int n, int lane,
@@ -200,11 +130,12 @@ topk_select_kernel(ScoreArgs a, TopkWork w) {
         // thr (a floor or threshold that is not finite queues the pair as well)
         if (__any(lane < ns && !(fl < thr))) {
             if (lane == 0) {
-                const int q = atomicAdd(&sched->n_tkq[m], 1);
-                if (q < w.cap) {
-                    w.qj[m * w.cap + q] = (int32_t)j;
-                    w.qthr[m * w.cap + q] = thr;
-                    w.qcnt[m * w.cap + q] = 0;
+                const FilterQueue &f = w.fq;
+                const int q = atomicAdd(&f.n[m], 1);
+                if (q < f.cap) {
+                    f.qj[m * f.cap + q] = (int32_t)j;
+                    f.qthr[m * f.cap + q] = thr;
+                    f.qcnt[m * f.cap + q] = 0;
                 }
             }
             continue;
@@ -224,80 +155,6 @@ topk_select_kernel(ScoreArgs a, TopkWork w) {
     }
 }
 
-// Work item (model, 64 queued rows, 128 vocabulary rows): the fp32 logits by MFMA
-// (32x32x16 bf16; vocabulary rows are the A operand, queued rows the B operand, both
-// read straight from memory), the indices of those >= the pair's threshold kept. The
-// K order inside a 64-wide step is permuted the same way for both operands: lane
-// half hf takes k in [32 hf + 8 s, 32 hf + 8 s + 8) at sub-step s, so each lane reads
-// 64 contiguous bytes of its row per step.
-__global__ void __launch_bounds__(256)
-topk_filter_kernel(ScoreArgs a, TopkWork w) {
-    const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    const int hf = lane >> 5, c32 = lane & 31;
-    const int n_vt = (a.V + TKF_VR - 1) / TKF_VR;
-    int nq[2], nqb[2];
-    for (int m = 0; m < 2; ++m) {
-        const int n = a.sched->n_tkq[m];
-        nq[m] = n < w.cap ? n : w.cap;
-        nqb[m] = (nq[m] + TKF_QB - 1) / TKF_QB;
-    }
-    const int64_t items0 = (int64_t)nqb[0] * n_vt;
-    const int64_t items = items0 + (int64_t)nqb[1] * n_vt;
-    for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
-        const int m = it < items0 ? 0 : 1;
-        const int64_t rel = m ? it - items0 : it;
-        const int qb = (int)(rel % nqb[m]);      // queued batch fastest: a vocabulary
-        const int vt = (int)(rel / nqb[m]);      // tile is read by neighbouring items
-        const int d = m ? a.dt : a.ds;
-        const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
-        const uint16_t *H = (const uint16_t *)(m ? a.ht : a.hs);
-        const int r0 = vt * TKF_VR + wid * 32;
-        const int vrow = r0 + c32 < a.V ? r0 + c32 : a.V - 1;
-        const uint16_t *wr = W + (int64_t)vrow * d + 32 * hf;
-        const uint16_t *hr[2];
-        for (int cb = 0; cb < 2; ++cb) {
-            int q = qb * TKF_QB + cb * 32 + c32;
-            q = q < nq[m] ? q : nq[m] - 1;
-            const int64_t g = a.rowmap[w.qj[m * w.cap + q]] & 0x7fffffffu;
-            hr[cb] = H + g * d + 32 * hf;
-        }
-        tk_floatx16 acc[2];
-        acc[0] = tk_floatx16{0.f};
-        acc[1] = tk_floatx16{0.f};
-        for (int k0 = 0; k0 < d; k0 += 64) {
-            uint4 A[4], B0[4], B1[4];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                A[s] = *(const uint4 *)(wr + k0 + 8 * s);
-                B0[s] = *(const uint4 *)(hr[0] + k0 + 8 * s);
-                B1[s] = *(const uint4 *)(hr[1] + k0 + 8 * s);
-            }
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const tk_bf16x8 av = __builtin_bit_cast(tk_bf16x8, A[s]);
-                acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    av, __builtin_bit_cast(tk_bf16x8, B0[s]), acc[0], 0, 0, 0);
-                acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    av, __builtin_bit_cast(tk_bf16x8, B1[s]), acc[1], 0, 0, 0);
-            }
-        }
-        // lane holds column c32 (a queued row) and rows 8 (r / 4) + 4 hf + r % 4
-        for (int cb = 0; cb < 2; ++cb) {
-            const int q = qb * TKF_QB + cb * 32 + c32;
-            if (q >= nq[m]) continue;
-            const float thr = w.qthr[m * w.cap + q];
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int v = r0 + 8 * (r >> 2) + 4 * hf + (r & 3);
-                if (v < a.V && acc[cb][r] >= thr) {
-                    const int n = atomicAdd(&w.qcnt[m * w.cap + q], 1);
-                    if (n < TK_CAP) w.cand[((int64_t)m * w.cap + q) * TK_CAP + n] = v;
-                }
-            }
-        }
-    }
-}
-
 // One wavefront per queued pair: exact values of its kept indices, ranked. A pair
 // with more indices than were kept goes to the exhaustive scan.
 __global__ void __launch_bounds__(256)
@@ -305,30 +162,27 @@ topk_exact_kernel(ScoreArgs a, TopkWork w) {
     __shared__ double cx[4][TK_CAP];
     __shared__ int ci[4][TK_CAP];
     const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-    Sched *sched = const_cast<Sched *>(a.sched);
+    const FilterQueue &f = w.fq;
     int nq[2];
     for (int m = 0; m < 2; ++m) {
-        const int n = sched->n_tkq[m];
-        nq[m] = n < w.cap ? n : w.cap;
+        const int n = f.n[m];
+        nq[m] = n < f.cap ? n : f.cap;
     }
     for (int64_t p = (int64_t)blockIdx.x * 4 + wid; p < nq[0] + nq[1];
          p += (int64_t)gridDim.x * 4) {
         const int m = p < nq[0] ? 0 : 1;
         const int q = (int)(m ? p - nq[0] : p);
-        const int n = w.qcnt[m * w.cap + q];
-        const int64_t j = w.qj[m * w.cap + q];
-        if (n > TK_CAP) {
-            if (lane == 0) {
-                const int f = atomicAdd(&sched->n_tk_fb, 1);
-                w.fb[f] = m * w.cap + q;
-            }
+        const int n = f.qcnt[m * f.cap + q];
+        const int64_t j = f.qj[m * f.cap + q];
+        if (n > f.ccap) {
+            if (lane == 0) f.fb[atomicAdd(f.nfb, 1)] = m * f.cap + q;
             continue;
         }
         const int d = m ? a.dt : a.ds;
         const int64_t g = a.rowmap[j] & 0x7fffffffu;
         const uint16_t *h = (const uint16_t *)(m ? a.ht : a.hs) + g * d;
         const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
-        const int32_t *cd = w.cand + ((int64_t)m * w.cap + q) * TK_CAP;
+        const int32_t *cd = f.cand + ((int64_t)m * f.cap + q) * f.ccap;
         for (int c = 0; c < n; ++c) {
             const int v = cd[c];
             const double x = wave_dot_exact(h, W + (int64_t)v * d, d, lane);
@@ -340,65 +194,30 @@ topk_exact_kernel(ScoreArgs a, TopkWork w) {
     }
 }
 
-// One workgroup per pair of the exhaustive scan: every exact logit of the row (8 lanes
-// per vocabulary row, fp64 sums), a top-16 per 8-lane group, merged over the group.
-__global__ void __launch_bounds__(TKS_THREADS)
+// One workgroup per pair of the exhaustive scan: the row's 16 best of every exact
+// logit of the vocabulary.
+__global__ void __launch_bounds__(SCAN_THREADS)
 topk_scan_kernel(ScoreArgs a, TopkWork w) {
     extern __shared__ __attribute__((aligned(16))) uint16_t tk_h[];   // [d] bf16
-    __shared__ double red_v[TKS_GROUPS][TOPK_K];
-    __shared__ int red_i[TKS_GROUPS][TOPK_K];
-    const int nfb = a.sched->n_tk_fb;
-    const int tid = threadIdx.x, g8 = tid & 7, grp = tid >> 3;
+    __shared__ double red_v[SCAN_GROUPS][TOPK_K];
+    __shared__ int red_i[SCAN_GROUPS][TOPK_K];
+    const FilterQueue &f = w.fq;
+    const int nfb = *f.nfb;
     for (int e = blockIdx.x; e < nfb; e += gridDim.x) {
-        const int code = w.fb[e];
-        const int m = code >= w.cap ? 1 : 0;
-        const int q = code - m * w.cap;
-        const int64_t j = w.qj[m * w.cap + q];
+        const int code = f.fb[e];
+        const int m = code >= f.cap ? 1 : 0;
+        const int q = code - m * f.cap;
+        const int64_t j = f.qj[m * f.cap + q];
         const int d = m ? a.dt : a.ds;
         const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
         const int64_t g = a.rowmap[j] & 0x7fffffffu;
         const uint16_t *h = (const uint16_t *)(m ? a.ht : a.hs) + g * d;
-        __syncthreads();
-        for (int k = tid * 8; k < d; k += TKS_THREADS * 8)
-            *(uint4 *)(tk_h + k) = *(const uint4 *)(h + k);
-        __syncthreads();
-        double lv[TOPK_K];
-        int li[TOPK_K];
-#pragma unroll
-        for (int t = 0; t < TOPK_K; ++t) { lv[t] = kTkEmpty; li[t] = kTkNoIdx; }
-        for (int v0 = 0; v0 < a.V; v0 += TKS_GROUPS) {
-            const int v = v0 + grp;
-            const bool ok = v < a.V;
-            const uint16_t *wr = W + (int64_t)(ok ? v : a.V - 1) * d;
-            double z = 0.0;
-            for (int k = g8 * 8; k < d; k += 64)
-                z = dot8_f64(*(const uint4 *)(tk_h + k), *(const uint4 *)(wr + k), z);
-            z += __shfl_xor(z, 1);
-            z += __shfl_xor(z, 2);
-            z += __shfl_xor(z, 4);
-            if (ok && tk_before(z, v, lv[TOPK_K - 1], li[TOPK_K - 1]))
-                tk_insert<TOPK_K>(lv, li, z, v);
-        }
-        if (g8 == 0) {
-#pragma unroll
-            for (int t = 0; t < TOPK_K; ++t) { red_v[grp][t] = lv[t]; red_i[grp][t] = li[t]; }
-        }
-        __syncthreads();
-        if (tid < 64) {   // merge the 32 group lists: lane l < 32 owns group l's list
-            int ptr = 0;
-            for (int r = 0; r < TOPK_K; ++r) {
-                double hv = kTkEmpty;
-                int hi = kTkNoIdx;
-                if (tid < TKS_GROUPS && ptr < TOPK_K) { hv = red_v[tid][ptr]; hi = red_i[tid][ptr]; }
-                double bv = hv;
-                int bi = hi;
-                wave_best(bv, bi);
-                if (tid < TKS_GROUPS && ptr < TOPK_K && hv == bv && hi == bi) ++ptr;
-                if (tid == 0) {
-                    w.list_v[(j * 2 + m) * TOPK_K + r] = (float)bv;
-                    w.list_i[(j * 2 + m) * TOPK_K + r] = bi;
-                }
-            }
+        double bv;
+        int bi;
+        scan_row_top16(h, W, d, a.V, tk_h, red_v, red_i, bv, bi);
+        if (threadIdx.x < TOPK_K) {
+            w.list_v[(j * 2 + m) * TOPK_K + threadIdx.x] = (float)bv;
+            w.list_i[(j * 2 + m) * TOPK_K + threadIdx.x] = bi;
         }
     }
 }
@@ -467,11 +286,11 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 size_t topk_work_bytes(int64_t cap) {
     const size_t c = (size_t)cap;
-    return align256(c * 2 * 4) + 2 * align256(c * 2 * TOPK_K * 4) + 3 * align256(c * 2 * 4) +
-           align256(c * 2 * TK_CAP * 4) + align256(c * 2 * 4);
+    return align256(c * 2 * 4) + 2 * align256(c * 2 * TOPK_K * 4) +
+           filter_queue_bytes(cap, TK_CAP);
 }
 
-TopkWork topk_carve(void *base, int64_t cap) {
+TopkWork topk_carve(void *base, int64_t cap, int32_t *n, int32_t *nfb) {
     const size_t c = (size_t)cap;
     char *p = (char *)base;
     TopkWork w;
@@ -479,11 +298,7 @@ TopkWork topk_carve(void *base, int64_t cap) {
     w.lse = (float *)p;        p += align256(c * 2 * 4);
     w.list_v = (float *)p;     p += align256(c * 2 * TOPK_K * 4);
     w.list_i = (int32_t *)p;   p += align256(c * 2 * TOPK_K * 4);
-    w.qj = (int32_t *)p;       p += align256(c * 2 * 4);
-    w.qthr = (float *)p;       p += align256(c * 2 * 4);
-    w.qcnt = (int32_t *)p;     p += align256(c * 2 * 4);
-    w.cand = (int32_t *)p;     p += align256(c * 2 * TK_CAP * 4);
-    w.fb = (int32_t *)p;
+    w.fq = filter_queue_carve(p, cap, TK_CAP, n, nfb);
     return w;
 }
 
@@ -494,14 +309,13 @@ hipError_t launch_topk(const ScoreArgs &a, const TopkWork &w, const TopkOut &out
     topk_select_kernel<<<rows, 256, 0, st>>>(a, w);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    topk_filter_kernel<<<1024, 256, 0, st>>>(a, w);
-    e = hipGetLastError();
+    e = launch_filter(a, w.fq, st);
     if (e != hipSuccess) return e;
     topk_exact_kernel<<<256, 256, 0, st>>>(a, w);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int dmax = a.ds > a.dt ? a.ds : a.dt;
-    topk_scan_kernel<<<256, TKS_THREADS, (size_t)dmax * 2, st>>>(a, w);
+    topk_scan_kernel<<<256, SCAN_THREADS, (size_t)dmax * 2, st>>>(a, w);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     topk_output_kernel<<<rows, 256, 0, st>>>(a, w, out);
