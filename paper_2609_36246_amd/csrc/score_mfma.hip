@@ -64,16 +64,25 @@ struct Run {                // running statistics of one position column
     int idx;
 };
 
-// The 4 largest logits a lane has seen of one position column, as packed keys in
+// The largest logits a lane keeps of one position column (4), as packed keys in
 // descending order (0 = empty): the high 16 bits are the logit's order-preserving
 // code rounded toward -inf (the logit lies in [lb(code), lb(code + 1))), the low 16
 // bits 0xFFFF minus the lane's ordinal of the row (vocabulary tile of the split x 64 +
 // 32-row block x 16 + row of the block), so that among equal codes the lower
-// vocabulary index ranks first. Every logit the lane dropped is below lb(code_3 + 1).
-// The lists only narrow the field: the top-K sets are decided on exact logits later.
+// vocabulary index ranks first. Every logit the lane dropped is below lb(c + 1) for c
+// the larger code of the 4th key and of the floor key. The lists only narrow the
+// field: the top-K sets are decided on exact logits later.
 struct Top4 {
     uint32_t k[4];
+    uint32_t f;      // floor key: the largest key a block dropped outright (0 = none)
 };
+
+// Middle of three unsigned values (one v_med3_u32).
+__device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
+    const uint32_t lo = a < b ? a : b, hi = a < b ? b : a;
+    const uint32_t m = hi < c ? hi : c;
+    return lo > m ? lo : m;
+}
 
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 struct Kernel {
@@ -351,25 +360,30 @@ struct Kernel {
         return x;
     }
 
-    // Offer one 32-row block (16 values per lane) to a lane's top-4; skipped when no
-    // key of the block can beat the current 4th. tie0 = 0xFFFF minus the ordinal of
-    // the block's first row.
+    // Offer one 32-row block (16 values per lane) to a lane's list: the block's three
+    // largest keys by a running v_med3_u32 network, the two largest inserted, the
+    // third raising the floor key. Every key the lane drops is then at most the list's
+    // 4th or some block's third, so the floor bounds it. tie0 = 0xFFFF minus the
+    // ordinal of the block's first row.
     static __device__ __forceinline__ void topk_block(const float (&z)[16], Top4 &K,
                                                       uint32_t tie0) {
-        float bm = z[0];
+        uint32_t b1 = 0u, b2 = 0u, b3 = 0u;
 #pragma unroll
-        for (int r = 1; r < 16; ++r) bm = max2(bm, z[r]);
-        // wave-uniform: inserting keys that do not beat the 4th leaves a list unchanged
-        if (__builtin_amdgcn_ballot_w64(((f2ord(bm) & 0xFFFF0000u) | 0xFFFFu) > K.k[3]) != 0) {
+        for (int r = 0; r < 16; ++r) {
+            const uint32_t x = (f2ord(z[r]) & 0xFFFF0000u) | (tie0 - (uint32_t)r);
+            b3 = umed3(x, b2, b3);
+            b2 = umed3(x, b1, b2);
+            b1 = b1 > x ? b1 : x;
+        }
+        K.f = K.f > b3 ? K.f : b3;
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                uint32_t x = (f2ord(z[r]) & 0xFFFF0000u) | (tie0 - (uint32_t)r);
+        for (int t = 0; t < 2; ++t) {
+            uint32_t x = t ? b2 : b1;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const uint32_t hi = x > K.k[j] ? x : K.k[j];
-                    x = x > K.k[j] ? K.k[j] : x;
-                    K.k[j] = hi;
-                }
+            for (int j = 0; j < 4; ++j) {
+                const uint32_t hi = x > K.k[j] ? x : K.k[j];
+                x = x > K.k[j] ? K.k[j] : x;
+                K.k[j] = hi;
             }
         }
     }
@@ -457,6 +471,8 @@ struct Kernel {
             for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
                 for (int e = 0; e < 4; ++e) { KS[cb].k[e] = 0u; KT[cb].k[e] = 0u; }
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) { KS[cb].f = 0u; KT[cb].f = 0u; }
 #pragma unroll
             for (int cb = 0; cb < 2; ++cb) {
                 RS[cb] = Run{kNegInf, kNegInf, 0.f, 0x7fffffff};
@@ -575,7 +591,8 @@ struct Kernel {
                         for (int e = 0; e < 4; ++e)
                             topk_insert_lex<8>(Q8v[m][cb], Q8i[m][cb], __shfl_xor(kv[e], 32),
                                                __shfl_xor(ki[e], 32));
-                        const float f = K.k[3] ? key_ub(K.k[3]) : kMasked;
+                        const uint32_t fk = K.k[3] > K.f ? K.k[3] : K.f;
+                        const float f = fk ? key_ub(fk) : kMasked;
                         Qfl[m][cb] = max2(f, __shfl_xor(f, 32));
                     }
             }
