@@ -96,6 +96,11 @@ def load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError("libolive_score.so is not built (run: python -m "
                           "paper_2609_36246_amd.build); there is no fallback")
+    # torch's HIP runtime must be resident first: the library's libamdhip64.so.7 then
+    # resolves to it by soname.  Loaded the other way round, torch (which asks for the
+    # file libamdhip64.so) brings a second runtime into the process and the library's
+    # calls see no device and cannot use torch's streams or allocations.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32p, i64p, f32p = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p
     st = ctypes.c_int

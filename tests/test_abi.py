@@ -157,3 +157,23 @@ def test_binding_refuses_to_run_without_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(L, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         L.load()
+
+
+def test_library_and_torch_share_one_hip_runtime(lib):
+    """Loading the binding before torch must still leave a single HIP runtime mapped."""
+    import subprocess
+    import sys
+    code = ("from paper_2609_36246_amd import _lib as L\n"
+            "L.load()\n"
+            "import torch\n"
+            "paths = set()\n"
+            "for line in open('/proc/self/maps'):\n"
+            "    f = line.split()[-1]\n"
+            "    if 'libamdhip64' in f:\n"
+            "        paths.add(__import__('os').path.realpath(f))\n"
+            "print(len(paths), sorted(paths))\n")
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, capture_output=True, text=True,
+                       timeout=300)
+    assert r.returncode == 0, r.stderr
+    n = int(r.stdout.split()[0])
+    assert n == 1, r.stdout
