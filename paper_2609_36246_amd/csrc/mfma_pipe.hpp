@@ -73,4 +73,31 @@ __device__ __forceinline__ void dma16(const char *g, uint32_t la) {
 #pragma clang diagnostic pop
 }
 
+// The same DMA with the LDS address `la` + OFF formed in m0 by one scalar add, from a
+// 64-bit lane address (dma16_at) or from a wave-uniform base in SGPRs plus a 32-bit
+// lane offset (dma16_sv: the address add happens in the load, not in a VALU op).
+template <int OFF>
+__device__ __forceinline__ void dma16_at(const char *g, uint32_t la) {
+    la = __builtin_amdgcn_readfirstlane(la);
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+    asm volatile("s_add_u32 m0, %0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(la), "v"(g), "i"(OFF)
+                 : "memory", "m0", "scc");
+#pragma clang diagnostic pop
+}
+
+template <int OFF>
+__device__ __forceinline__ void dma16_sv(const char *base, uint32_t voff, uint32_t la) {
+    la = __builtin_amdgcn_readfirstlane(la);
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+    asm volatile("s_add_u32 m0, %0, %3\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(la), "v"(voff), "s"(base), "i"(OFF)
+                 : "memory", "m0", "scc");
+#pragma clang diagnostic pop
+}
+
 }  // namespace olive

@@ -86,48 +86,86 @@ __device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
 
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 struct Kernel {
-    // Addresses of the 12 DMAs of one step (8 W, 4 H) of model `m`, K step kk,
-    // vocabulary tile vt, into ring stage `st`. DMA i of a wave fills stage rows
-    // 8i .. 8i+7 of the wave's slice: every 8 lanes read one full 128-byte line of a row.
-    struct Issue {
-        const char *wt;         // W tile row 0 at K step kk (wave-uniform)
-        int64_t wstep;          // 8 rows of W (wave-uniform)
-        uint32_t wo0, wo1;      // lane offsets for even / odd W DMAs
-        int hoff;               // K step offset into the H rows
-        int m;
-        uint32_t lwp, lhp;      // LDS targets (wave-uniform)
+    // Issue cursor: the next step to prefetch. Wave-uniform: its model block (vocabulary
+    // tile vt, model m, step kk of the block's cnt), the W tile pointer at the step's K
+    // offset and the K offset into the hidden rows; per lane: the W row offsets of the 8
+    // W DMAs and the hidden-row pointers of the 4 H DMAs, both for model m. A step only
+    // adds `inc` (one 128-byte line) to the two offsets; the lane parts change with the
+    // model block, twice per vocabulary tile. Past the unit's last step `inc` is 0 and
+    // the trailing prefetches repeat an in-bounds step of the last tile.
+    struct Cursor {
+        const char *w;
+        int64_t hoff, inc;
+        int vt, m, kk, cnt;
+        int vt1, nS, nT;
+        uint32_t wq[W_DMA];
+        const char *hq[H_DMA];
     };
-    static __device__ __forceinline__ Issue plan(const ScoreArgs &a, const Lane &L, int st, int m,
-                                                 int kk, int vt) {
-        Issue I;
-        const int d = m ? a.dt : a.ds;
-        const int64_t rowbytes = (int64_t)d * 2;
-        const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
-        I.wt = (const char *)(m ? a.wt : a.ws) + (int64_t)row0 * rowbytes + kk * ROWB;
-        I.wstep = 8 * rowbytes;
-        I.wo0 = m ? L.wvoff[1][0] : L.wvoff[0][0];
-        I.wo1 = m ? L.wvoff[1][1] : L.wvoff[0][1];
-        I.hoff = kk * ROWB;
-        I.m = m;
-        const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;   // wave-uniform
-        I.lwp = base + (uint32_t)L.wid * (W_DMA * 1024u);
-        I.lhp = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
-        return I;
+
+    // Point the cursor at step 0 of block (vt, M); a tile at or past vt1 is clamped to
+    // the unit's last one and the cursor stops there.
+    template <int M>
+    static __device__ __forceinline__ void enter(Cursor &C, const ScoreArgs &a, const Lane &L,
+                                                 int vt) {
+        const bool live = vt < C.vt1;
+        const int v = live ? vt : C.vt1 - 1;
+        const int rb = M ? 2 * a.dt : 2 * a.ds;   // bytes per weight row
+        int row0 = v * BV < a.V - BV ? v * BV : a.V - BV;
+        row0 = row0 > 0 ? row0 : 0;
+        C.vt = v;
+        C.m = M;
+        C.kk = 0;
+        C.cnt = live ? (M ? C.nT : C.nS) : 0x7fffffff;
+        C.inc = live ? ROWB : 0;
+        C.w = (const char *)(M ? a.wt : a.ws) + (int64_t)row0 * rb;
+        C.hoff = 0;
+#pragma unroll
+        for (int q = 0; q < W_DMA; ++q) C.wq[q] = L.wvoff[M][q & 1] + (uint32_t)(q * 8 * rb);
+#pragma unroll
+        for (int i = 0; i < H_DMA; ++i) C.hq[i] = L.hp[M][i];
     }
+
+    // Move to the next model block once the current one is fully issued: the teacher
+    // block of the same tile after a student block, else the next tile's student block.
+    static __device__ __forceinline__ void turn(Cursor &C, const ScoreArgs &a, const Lane &L) {
+        if (C.kk == C.cnt) {
+            if (HAS_T && C.m == 0) enter<1>(C, a, L, C.vt);
+            else enter<0>(C, a, L, C.vt + 1);
+        }
+    }
+
+    static __device__ __forceinline__ void advance(Cursor &C) {
+        C.w += C.inc;
+        C.hoff += C.inc;
+        C.kk += 1;
+    }
+
+    // DMA Q of a step (Q < 8: W rows 8Q .. 8Q+7 of the wave's slice; else H DMA Q-8)
+    // into the stage whose wave parts start at lw (W) and lh (H).
     template <int Q>
-    static __device__ __forceinline__ void dma_q(const Lane &L, const Issue &I) {
-        if (Q < W_DMA)
-            dma16(I.wt + Q * I.wstep + ((Q & 1) ? I.wo1 : I.wo0), I.lwp + Q * 1024);
+    static __device__ __forceinline__ void dma_q(const Cursor &C, uint32_t lw, uint32_t lh) {
+        if constexpr (Q < W_DMA)
+            dma16_sv<Q * 1024>(C.w, C.wq[Q], lw);
         else
-            dma16((I.m ? L.hp[1][Q - W_DMA] : L.hp[0][Q - W_DMA]) + I.hoff,
-                  I.lhp + (Q - W_DMA) * 1024);
+            dma16_at<(Q - W_DMA) * 1024>(C.hq[Q - W_DMA] + C.hoff, lh);
     }
-    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, int st, int m,
-                                                 int kk, int vt) {
-        const Issue I = plan(a, L, st, m, kk, vt);
-        dma_q<0>(L, I); dma_q<1>(L, I); dma_q<2>(L, I); dma_q<3>(L, I);
-        dma_q<4>(L, I); dma_q<5>(L, I); dma_q<6>(L, I); dma_q<7>(L, I);
-        dma_q<8>(L, I); dma_q<9>(L, I); dma_q<10>(L, I); dma_q<11>(L, I);
+
+    // LDS targets of this wave's DMAs into ring stage st.
+    static __device__ __forceinline__ uint32_t stage_w(const Lane &L, int st) {
+        return ring_addr() + (uint32_t)st * STAGE_BYTES + (uint32_t)L.wid * (W_DMA * 1024u);
+    }
+    static __device__ __forceinline__ uint32_t stage_h(const Lane &L, int st) {
+        return ring_addr() + (uint32_t)st * STAGE_BYTES + WT_BYTES +
+               (uint32_t)L.wid * (H_DMA * 1024u);
+    }
+
+    // All 12 DMAs of the cursor's step into stage st (the pipeline prologue).
+    static __device__ __forceinline__ void issue(const ScoreArgs &a, const Lane &L, Cursor &C,
+                                                 int st) {
+        turn(C, a, L);
+        const uint32_t lw = stage_w(L, st), lh = stage_h(L, st);
+        dmas<0, DMA_PER_STEP>(C, lw, lh);
+        advance(C);
     }
 
     // Operand fragments of one k16 sub-step: 4 W row blocks, 2 H column blocks.
@@ -156,10 +194,10 @@ struct Kernel {
     }
 
     template <int QB, int QE>
-    static __device__ __forceinline__ void dmas(const Lane &L, const Issue &I) {
+    static __device__ __forceinline__ void dmas(const Cursor &C, uint32_t lw, uint32_t lh) {
         if constexpr (QB < QE) {
-            dma_q<QB>(L, I);
-            dmas<QB + 1, QE>(L, I);
+            dma_q<QB>(C, lw, lh);
+            dmas<QB + 1, QE>(C, lw, lh);
         }
     }
 
@@ -169,13 +207,13 @@ struct Kernel {
     // and stall the wave in front of its next MFMA.
     template <int Q0, int NQ>
     static __device__ __forceinline__ void mma_issue(const Frag &F, floatx16 (&acc)[4][2],
-                                                     const Lane &L, const Issue &I) {
+                                                     const Cursor &C, uint32_t lw, uint32_t lh) {
 #define OLIVE_MI(J_, VB_, CB_)                                                             \
         __builtin_amdgcn_sched_barrier(0);                                               \
         acc[VB_][CB_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[VB_], F.B[CB_],        \
                                                                 acc[VB_][CB_], 0, 0, 0); \
         __builtin_amdgcn_sched_barrier(0);                                               \
-        dmas<Q0 + ((J_) * NQ + 7) / 8, Q0 + ((J_) * NQ + NQ + 7) / 8>(L, I);
+        dmas<Q0 + ((J_) * NQ + 7) / 8, Q0 + ((J_) * NQ + NQ + 7) / 8>(C, lw, lh);
         OLIVE_MI(0, 0, 0)
         OLIVE_MI(1, 0, 1)
         OLIVE_MI(2, 1, 0)
@@ -200,44 +238,93 @@ struct Kernel {
         compiler_fence();
     }
 
-    // One pipeline step n in stage `st`: meet the stage barrier, prefetch step n+2 into
-    // the stage of step n-1, then run the step's four k16 sub-steps, each one's LDS
-    // reads issued under the previous one's MFMAs. With PEND, the last sub-step of
-    // step n-1 (fragments in P) runs under the first reads. On return P holds this
-    // step's last sub-step, still to be run. Past the end of a unit the prefetch
-    // repeats the last step's in-bounds addresses, so no DMA sits under a branch.
+    // One pipeline step n in stage `st`: meet the stage barrier, prefetch the cursor's
+    // step (n+2) into the stage of step n-1, then run the step's four k16 sub-steps,
+    // each one's LDS reads issued under the previous one's MFMAs. With PEND, the last
+    // sub-step of step n-1 (fragments in P) runs under the first reads. On return P
+    // holds this step's last sub-step, still to be run. Every step issues its 12 DMAs
+    // (past the end of a unit, of an in-bounds step), so no DMA sits under a branch.
     template <bool PEND>
-    static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, int st, int pm,
-                                                int pk, int pvt, floatx16 (&acc)[4][2],
-                                                Frag &P) {
+    static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, Cursor &C,
+                                                int st, floatx16 (&acc)[4][2], Frag &P) {
         const int pv = st == 0 ? NST - 1 : st - 1;
+        turn(C, a, L);
         arrive();
-        const Issue I = plan(a, L, pv, pm, pk, pvt);
+        const uint32_t lw = stage_w(L, pv), lh = stage_h(L, pv);
         Frag F0, F1, F2;
         read_frag<0>(L, st, F0);
         __builtin_amdgcn_sched_barrier(0);
         if (PEND) {
-            mma_issue<0, 3>(P, acc, L, I);
+            mma_issue<0, 3>(P, acc, C, lw, lh);
             read_frag<1>(L, st, F1);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<3, 3>(F0, acc, L, I);
+            mma_issue<3, 3>(F0, acc, C, lw, lh);
             read_frag<2>(L, st, F2);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<6, 3>(F1, acc, L, I);
+            mma_issue<6, 3>(F1, acc, C, lw, lh);
             read_frag<3>(L, st, P);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<9, 3>(F2, acc, L, I);
+            mma_issue<9, 3>(F2, acc, C, lw, lh);
         } else {
             read_frag<1>(L, st, F1);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<0, 4>(F0, acc, L, I);
+            mma_issue<0, 4>(F0, acc, C, lw, lh);
             read_frag<2>(L, st, F2);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<4, 4>(F1, acc, L, I);
+            mma_issue<4, 4>(F1, acc, C, lw, lh);
             read_frag<3>(L, st, P);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<8, 4>(F2, acc, L, I);
+            mma_issue<8, 4>(F2, acc, C, lw, lh);
         }
+        advance(C);
+    }
+
+    // The K sweep of one work unit: for every vocabulary tile vt0 .. vt1-1 the student
+    // block (nS steps into accS), then the teacher block (nT steps into accT), then
+    // tile_end(vt, row0) on the finished accumulators. Prefetch runs two steps ahead
+    // through the cursor, across block and tile ends.
+    template <class TileEnd>
+    static __device__ __forceinline__ void sweep(const ScoreArgs &a, const Lane &L, int vt0,
+                                                 int vt1, int nS, int nT,
+                                                 floatx16 (&accS)[4][2], floatx16 (&accT)[4][2],
+                                                 TileEnd &&tile_end) {
+        Cursor C;
+        C.vt1 = vt1;
+        C.nS = nS;
+        C.nT = nT;
+        enter<0>(C, a, L, vt0);
+        // Prologue: steps 0 .. NST-2 into stages 0 .. NST-2; the first step's barrier
+        // waits for step 0.
+#pragma unroll
+        for (int i = 0; i < NST - 1; ++i) issue(a, L, C, i);
+        // Drain scalar loads before the loops: an SMEM load still pending at a loop
+        // header would force lgkmcnt(0) (full LDS waits) inside every step.
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        int st = 0;   // ring stage of the current step
+        // A model block of COUNT_ steps: the first step has no pending sub-step, the
+        // block's last sub-step runs after the loop.
+#define OLIVE_STEPS(ACC_, COUNT_)                                                        \
+        {                                                                                \
+            Frag P;                                                                      \
+            step<false>(a, L, C, st, ACC_, P);                                           \
+            st = st + 1 == NST ? 0 : st + 1;                                             \
+            for (int k = 1; k < (COUNT_); ++k) {                                         \
+                step<true>(a, L, C, st, ACC_, P);                                        \
+                st = st + 1 == NST ? 0 : st + 1;                                         \
+            }                                                                            \
+            mma(P, ACC_);                                                                \
+            __builtin_amdgcn_sched_barrier(0);                                           \
+        }
+        for (int vt = vt0; vt < vt1; ++vt) {
+            // The last tile, when V is not a multiple of 256, is shifted back to end at
+            // V; its rows below vt*BV were covered by the previous tile.
+            const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+            zero_acc(accS, accT);
+            OLIVE_STEPS(accS, nS)
+            if (HAS_T) OLIVE_STEPS(accT, nT)
+            tile_end(vt, row0);
+        }
+#undef OLIVE_STEPS
     }
 
     // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
@@ -421,7 +508,6 @@ struct Kernel {
 #pragma unroll
         for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
         const int nS = a.ds / BK, nT = HAS_T ? a.dt / BK : 0;
-        const int spv = nS + nT;
         // W DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7 with
         // chunk (lane&7) ^ swz(R); swz(R) depends on i only through its parity.
 #pragma unroll
@@ -462,7 +548,6 @@ struct Kernel {
             }
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
-            const int total = (vt1 - vt0) * spv;
 
             Run RS[2], RT[2];
             float AA[2] = {0.f, 0.f}, BB[2] = {0.f, 0.f};
@@ -487,64 +572,15 @@ struct Kernel {
                     accT[vb][cb] = floatx16{0.f};
                 }
 
-            // Issue cursor: (vtile, position within the vtile's steps) of the next step
-            // to prefetch, saturating at the unit's last step.
-            int ivt = vt0, ir = 0;
-            // Branch-free advance: control flow between steps would make the compiler
-            // merge its LDS wait state conservatively (lgkmcnt(0)) at every join.
-            auto adv_if = [&](bool go) {
-                ir += go ? 1 : 0;
-                const bool wrap = ir == spv;
-                ir = wrap ? 0 : ir;
-                ivt += wrap ? 1 : 0;
-            };
-            auto im = [&]() { return ir < nS ? 0 : 1; };
-            auto ik = [&]() { return ir < nS ? ir : ir - nS; };
-            // Prologue: steps 0 .. NST-2 into stages 0 .. NST-2; the first step's barrier
-            // waits for step 0.
-#pragma unroll
-            for (int i = 0; i < NST - 1; ++i) {
-                issue(a, L, i, im(), ik(), ivt);
-                adv_if(i + 1 < total);
-            }
-            // Drain scalar loads before the loops: an SMEM load still pending at a loop
-            // header would force lgkmcnt(0) (full LDS waits) inside every step.
-            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-
-            int n = 0;    // global step index within the unit
-            int st = 0;   // ring stage of step n
-            // A model block of COUNT_ steps: the first step has no pending sub-step, the
-            // block's last sub-step runs after the loop.
-#define OLIVE_STEPS(ACC_, COUNT_)                                                        \
-            {                                                                            \
-                Frag P;                                                                  \
-                step<false>(a, L, st, im(), ik(), ivt, ACC_, P);                         \
-                adv_if(n + NST < total);                                                 \
-                ++n;                                                                     \
-                st = st + 1 == NST ? 0 : st + 1;                                         \
-                for (int k = 1; k < (COUNT_); ++k) {                                     \
-                    step<true>(a, L, st, im(), ik(), ivt, ACC_, P);                      \
-                    adv_if(n + NST < total);                                             \
-                    ++n;                                                                 \
-                    st = st + 1 == NST ? 0 : st + 1;                                     \
-                }                                                                        \
-                mma(P, ACC_);                                                            \
-                __builtin_amdgcn_sched_barrier(0);                                       \
-            }
-            for (int vt = vt0; vt < vt1; ++vt) {
-                // The last tile, when V is not a multiple of 256, is shifted back to end
-                // at V; its rows below vt*BV were covered by the previous tile. One more
-                // MFMA adds kMasked to those rows (the logit is absorbed), so they drop
-                // out of every statistic and the fold needs no masking.
-                const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
-                const int vbase = row0 + L.wv * 128 + 4 * L.h;
-                zero_acc(accS, accT);
-                OLIVE_STEPS(accS, nS)
-                if (HAS_T) OLIVE_STEPS(accT, nT)
+            // After each tile: the last tile, when V is not a multiple of 256, is shifted
+            // back to end at V, and one more MFMA adds kMasked to its rows below vt*BV
+            // (the logit is absorbed), so they drop out of every statistic and the fold
+            // needs no masking.
+            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
-                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, vbase, vt - vt0);
-            }
-#undef OLIVE_STEPS
+                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, row0 + L.wv * 128 + 4 * L.h,
+                     vt - vt0);
+            });
 
             // Merge lanes l and l+32 (same columns, interleaved vocabulary rows).
 #pragma unroll
@@ -717,7 +753,6 @@ struct Kernel {
 #pragma unroll
         for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
         const int nS = a.ds / BK, nT = HAS_T ? a.dt / BK : 0;
-        const int spv = nS + nT;
 #pragma unroll
         for (int par = 0; par < 2; ++par) {
             const int R0 = L.wid * 8 * W_DMA + (L.lane >> 3);
@@ -758,47 +793,9 @@ struct Kernel {
             }
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
-            const int total = (vt1 - vt0) * spv;
             floatx16 accS[4][2], accT[4][2];
-            zero_acc(accS, accT);
-            int ivt = vt0, ir = 0;
-            auto adv_if = [&](bool go) {
-                ir += go ? 1 : 0;
-                const bool wrap = ir == spv;
-                ir = wrap ? 0 : ir;
-                ivt += wrap ? 1 : 0;
-            };
-            auto im = [&]() { return ir < nS ? 0 : 1; };
-            auto ik = [&]() { return ir < nS ? ir : ir - nS; };
-#pragma unroll
-            for (int i = 0; i < NST - 1; ++i) {
-                issue(a, L, i, im(), ik(), ivt);
-                adv_if(i + 1 < total);
-            }
-            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
-            int n = 0, st = 0;
-#define OLIVE_STEPS(ACC_, COUNT_)                                                        \
-            {                                                                            \
-                Frag P;                                                                  \
-                step<false>(a, L, st, im(), ik(), ivt, ACC_, P);                         \
-                adv_if(n + NST < total);                                                 \
-                ++n;                                                                     \
-                st = st + 1 == NST ? 0 : st + 1;                                         \
-                for (int k = 1; k < (COUNT_); ++k) {                                     \
-                    step<true>(a, L, st, im(), ik(), ivt, ACC_, P);                      \
-                    adv_if(n + NST < total);                                             \
-                    ++n;                                                                 \
-                    st = st + 1 == NST ? 0 : st + 1;                                     \
-                }                                                                        \
-                mma(P, ACC_);                                                            \
-                __builtin_amdgcn_sched_barrier(0);                                       \
-            }
-            for (int vt = vt0; vt < vt1; ++vt) {
-                const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
+            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                 const int vlo = vt * BV;   // rows below vlo of a shifted last tile: done
-                zero_acc(accS, accT);
-                OLIVE_STEPS(accS, nS)
-                if (HAS_T) OLIVE_STEPS(accT, nT)
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -834,8 +831,7 @@ struct Kernel {
                             }
                         }
                     }
-            }
-#undef OLIVE_STEPS
+            });
             // every DMA landed and every wave is done with the ring before the next
             // unit's prologue refills it
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
