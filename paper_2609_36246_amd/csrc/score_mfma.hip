@@ -92,7 +92,7 @@ struct Kernel {
     // W DMAs and the hidden-row pointers of the 4 H DMAs, both for model m. A step only
     // adds `inc` (one 128-byte line) to the two offsets; the lane parts change with the
     // model block, twice per vocabulary tile. Past the unit's last step `inc` is 0 and
-    // the trailing prefetches repeat an in-bounds step of the last tile.
+    // the trailing prefetches repeat the last issued step.
     struct Cursor {
         const char *w;
         int64_t hoff, inc;
@@ -102,21 +102,17 @@ struct Kernel {
         const char *hq[H_DMA];
     };
 
-    // Point the cursor at step 0 of block (vt, M); a tile at or past vt1 is clamped to
-    // the unit's last one and the cursor stops there.
+    // Point the cursor at step 0 of block (vt, M).
     template <int M>
     static __device__ __forceinline__ void enter(Cursor &C, const ScoreArgs &a, const Lane &L,
                                                  int vt) {
-        const bool live = vt < C.vt1;
-        const int v = live ? vt : C.vt1 - 1;
         const int rb = M ? 2 * a.dt : 2 * a.ds;   // bytes per weight row
-        int row0 = v * BV < a.V - BV ? v * BV : a.V - BV;
-        row0 = row0 > 0 ? row0 : 0;
-        C.vt = v;
+        const int row0 = vt * BV < a.V - BV ? vt * BV : a.V - BV;
+        C.vt = vt;
         C.m = M;
         C.kk = 0;
-        C.cnt = live ? (M ? C.nT : C.nS) : 0x7fffffff;
-        C.inc = live ? ROWB : 0;
+        C.cnt = M ? C.nT : C.nS;
+        C.inc = ROWB;
         C.w = (const char *)(M ? a.wt : a.ws) + (int64_t)row0 * rb;
         C.hoff = 0;
 #pragma unroll
@@ -125,12 +121,21 @@ struct Kernel {
         for (int i = 0; i < H_DMA; ++i) C.hq[i] = L.hp[M][i];
     }
 
-    // Move to the next model block once the current one is fully issued: the teacher
-    // block of the same tile after a student block, else the next tile's student block.
+    // Once the current model block is fully issued, move to the next one: the teacher
+    // block of the same tile after a student block, else the next tile's student
+    // block; past the unit's last tile, stay on the last issued step (still in L2).
     static __device__ __forceinline__ void turn(Cursor &C, const ScoreArgs &a, const Lane &L) {
         if (C.kk == C.cnt) {
-            if (HAS_T && C.m == 0) enter<1>(C, a, L, C.vt);
-            else enter<0>(C, a, L, C.vt + 1);
+            if (HAS_T && C.m == 0) {
+                enter<1>(C, a, L, C.vt);
+            } else if (C.vt + 1 < C.vt1) {
+                enter<0>(C, a, L, C.vt + 1);
+            } else {
+                C.w -= ROWB;
+                C.hoff -= ROWB;
+                C.inc = 0;
+                C.cnt = 0x7fffffff;
+            }
         }
     }
 
@@ -243,7 +248,8 @@ struct Kernel {
     // each one's LDS reads issued under the previous one's MFMAs. With PEND, the last
     // sub-step of step n-1 (fragments in P) runs under the first reads. On return P
     // holds this step's last sub-step, still to be run. Every step issues its 12 DMAs
-    // (past the end of a unit, of an in-bounds step), so no DMA sits under a branch.
+    // (past the end of a unit, those of its last step again), so no DMA sits under a
+    // branch.
     template <bool PEND>
     static __device__ __forceinline__ void step(const ScoreArgs &a, const Lane &L, Cursor &C,
                                                 int st, floatx16 (&acc)[4][2], Frag &P) {
