@@ -34,15 +34,29 @@ struct GFrag {
     bf16x8 A[4], B[2];
 };
 
+// DMA q of a step (q < 8: A rows 8q .. 8q+7 of the wave's slice; else B DMA q-8) at K
+// byte offset off into the stage whose wave parts start at la (A) and lb (B).
+template <int Q>
+__device__ __forceinline__ void g_dma(const GLane &L, uint32_t la, uint32_t lb, int off) {
+    if constexpr (Q < W_DMA)
+        dma16_at<Q * 1024>(L.ap[Q] + off, la);
+    else
+        dma16_at<(Q - W_DMA) * 1024>(L.bp[Q - W_DMA] + off, lb);
+}
+
+template <int QB, int QE>
+__device__ __forceinline__ void g_dmas(const GLane &L, uint32_t la, uint32_t lb, int off) {
+    if constexpr (QB < QE) {
+        g_dma<QB>(L, la, lb, off);
+        g_dmas<QB + 1, QE>(L, la, lb, off);
+    }
+}
+
 __device__ __forceinline__ void g_issue(const GLane &L, int st, int kk) {
     const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;
     const uint32_t la = base + (uint32_t)L.wid * (W_DMA * 1024u);
     const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
-    const int off = kk * ROWB;
-#pragma unroll
-    for (int i = 0; i < W_DMA; ++i) dma16(L.ap[i] + off, la + i * 1024);
-#pragma unroll
-    for (int i = 0; i < H_DMA; ++i) dma16(L.bp[i] + off, lb + i * 1024);
+    g_dmas<0, DMA_PER_STEP>(L, la, lb, kk * ROWB);
 }
 
 template <int SUB>
@@ -73,18 +87,21 @@ __device__ __forceinline__ void g_mma(const GFrag &F, floatx16 (&acc)[4][2]) {
 template <int Q0>
 __device__ __forceinline__ void g_mma_issue(const GFrag &F, floatx16 (&acc)[4][2],
                                             const GLane &L, uint32_t la, uint32_t lb, int off) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        __builtin_amdgcn_sched_barrier(0);
-        acc[j >> 1][j & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[j >> 1], F.B[j & 1],
-                                                                     acc[j >> 1][j & 1], 0, 0, 0);
-        __builtin_amdgcn_sched_barrier(0);
-        if ((j & 1) == 1) {
-            const int q = Q0 + (j >> 1);   // DMA index 0..11 of the refill
-            if (q < W_DMA) dma16(L.ap[q] + off, la + q * 1024);
-            else dma16(L.bp[q - W_DMA] + off, lb + (q - W_DMA) * 1024);
-        }
-    }
+#define OLIVE_GMI(J_)                                                                     \
+    __builtin_amdgcn_sched_barrier(0);                                                    \
+    acc[(J_) >> 1][(J_) & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                   \
+        F.A[(J_) >> 1], F.B[(J_) & 1], acc[(J_) >> 1][(J_) & 1], 0, 0, 0);                \
+    __builtin_amdgcn_sched_barrier(0);                                                    \
+    if constexpr (((J_) & 1) == 1) g_dma<Q0 + ((J_) >> 1)>(L, la, lb, off);
+    OLIVE_GMI(0)
+    OLIVE_GMI(1)
+    OLIVE_GMI(2)
+    OLIVE_GMI(3)
+    OLIVE_GMI(4)
+    OLIVE_GMI(5)
+    OLIVE_GMI(6)
+    OLIVE_GMI(7)
+#undef OLIVE_GMI
     __builtin_amdgcn_sched_barrier(0);
 }
 

@@ -810,30 +810,32 @@ struct Kernel {
 #pragma unroll
                         for (int rq = 0; rq < 4; ++rq) {
                             const int v0 = row0 + L.wv * 128 + vb * 32 + 8 * rq + 4 * L.h;
-                            uint32_t b[4];
+                            float gr[4];
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
                                 const float zs = agpr_read(accS[vb][cb][4 * rq + e]);
-                                float gr = wsum * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
+                                gr[e] = wsum * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
                                 if (HAS_T) {
                                     const float zt = agpr_read(accT[vb][cb][4 * rq + e]);
-                                    gr = fmaf(-z.w_kl, fast_exp2(fmaf(zt, a.cT, -l2t[cb])), gr);
+                                    gr[e] = fmaf(-z.w_kl, fast_exp2(fmaf(zt, a.cT, -l2t[cb])),
+                                                 gr[e]);
                                 }
-                                gr -= (v0 + e == ycol[cb]) ? z.w_ce : 0.f;
-                                b[e] = ok[cb] ? f32_to_bf16_rne(gr) : 0u;
+                                gr[e] -= (v0 + e == ycol[cb]) ? z.w_ce : 0.f;
                             }
+                            // rows v0, v0+1 and v0+2, v0+3 as packed bf16 pairs
+                            uint2 w;
+                            w.x = ok[cb] ? pack_bf16x2(gr[0], gr[1]) : 0u;
+                            w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
                             if (v0 >= vlo) {   // the 4 rows share the test (vlo % 4 == 0)
                                 const int t = tcol[cb];
-#pragma unroll
-                                for (int e = 0; e < 4; ++e)
-                                    if (t < z.pitch)
-                                        z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = (uint16_t)b[e];
-                                if (ok[cb]) {
-                                    uint2 w;
-                                    w.x = b[0] | (b[1] << 16);
-                                    w.y = b[2] | (b[3] << 16);
-                                    *(uint2 *)(z.dz_t + (int64_t)t * z.vp + v0) = w;
+                                if (t < z.pitch) {
+                                    uint16_t *col = z.dz_v + (int64_t)v0 * z.pitch + t;
+                                    col[0] = (uint16_t)w.x;
+                                    col[z.pitch] = (uint16_t)(w.x >> 16);
+                                    col[2 * (int64_t)z.pitch] = (uint16_t)w.y;
+                                    col[3 * (int64_t)z.pitch] = (uint16_t)(w.y >> 16);
                                 }
+                                if (ok[cb]) *(uint2 *)(z.dz_t + (int64_t)t * z.vp + v0) = w;
                             }
                         }
                     }
