@@ -14,6 +14,29 @@ constexpr int FL_VR = 128;   // vocabulary rows per work item (4 wavefronts x 32
 typedef __bf16 fl_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float fl_floatx16 __attribute__((ext_vector_type(16)));
 
+// One 64-wide K step of a lane's operands: its vocabulary row (A) and its two queued
+// rows (B0, B1), 4 x 16 bytes each.
+__device__ __forceinline__ void fl_load(uint4 (&R)[12], const uint16_t *wr,
+                                        const uint16_t *const (&hr)[2], int k0) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        R[s] = *(const uint4 *)(wr + k0 + 8 * s);
+        R[4 + s] = *(const uint4 *)(hr[0] + k0 + 8 * s);
+        R[8 + s] = *(const uint4 *)(hr[1] + k0 + 8 * s);
+    }
+}
+
+__device__ __forceinline__ void fl_mma(const uint4 (&R)[12], fl_floatx16 (&acc)[2]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+        const fl_bf16x8 av = __builtin_bit_cast(fl_bf16x8, R[s]);
+        acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            av, __builtin_bit_cast(fl_bf16x8, R[4 + s]), acc[0], 0, 0, 0);
+        acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            av, __builtin_bit_cast(fl_bf16x8, R[8 + s]), acc[1], 0, 0, 0);
+    }
+}
+
 // Work item (model, 64 queued rows, 128 vocabulary rows): the fp32 logits by MFMA
 // (32x32x16 bf16; vocabulary rows are the A operand, queued rows the B operand, both
 // read straight from memory), the indices of those >= the pair's threshold kept. The
@@ -31,11 +54,13 @@ filter_kernel(ScoreArgs a, FilterQueue w) {
         nq[m] = n < w.cap ? n : w.cap;
         nqb[m] = (nq[m] + FL_QB - 1) / FL_QB;
     }
-    const int64_t items0 = (int64_t)nqb[0] * n_vt;
-    const int64_t items = items0 + (int64_t)nqb[1] * n_vt;
+    // Teacher items first: the wider rows take longer, and the dispatcher hands the
+    // cheaper student items to whichever CUs finish early.
+    const int64_t items1 = (int64_t)nqb[1] * n_vt;
+    const int64_t items = items1 + (int64_t)nqb[0] * n_vt;
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
-        const int m = it < items0 ? 0 : 1;
-        const int64_t rel = m ? it - items0 : it;
+        const int m = it < items1 ? 1 : 0;
+        const int64_t rel = m ? it : it - items1;
         const int qb = (int)(rel % nqb[m]);      // queued batch fastest: a vocabulary
         const int vt = (int)(rel / nqb[m]);      // tile is read by neighbouring items
         const int d = m ? a.dt : a.ds;
@@ -54,23 +79,22 @@ filter_kernel(ScoreArgs a, FilterQueue w) {
         fl_floatx16 acc[2];
         acc[0] = fl_floatx16{0.f};
         acc[1] = fl_floatx16{0.f};
-        for (int k0 = 0; k0 < d; k0 += 64) {
-            uint4 A[4], B0[4], B1[4];
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                A[s] = *(const uint4 *)(wr + k0 + 8 * s);
-                B0[s] = *(const uint4 *)(hr[0] + k0 + 8 * s);
-                B1[s] = *(const uint4 *)(hr[1] + k0 + 8 * s);
-            }
-#pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const fl_bf16x8 av = __builtin_bit_cast(fl_bf16x8, A[s]);
-                acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    av, __builtin_bit_cast(fl_bf16x8, B0[s]), acc[0], 0, 0, 0);
-                acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                    av, __builtin_bit_cast(fl_bf16x8, B1[s]), acc[1], 0, 0, 0);
-            }
+        // Two register buffers: the loads of step i+1 are in flight under the MFMAs of
+        // step i. Pairs of steps, then an odd last step; after the last pair X reloads
+        // the last step (unused when the count is even).
+        const int nst = d / 64;
+        uint4 X[12], Y[12];
+        fl_load(X, wr, hr, 0);
+        int i = 0;
+        for (; i + 1 < nst; i += 2) {
+            fl_load(Y, wr, hr, (i + 1) * 64);
+            __builtin_amdgcn_sched_barrier(0);
+            fl_mma(X, acc);
+            fl_load(X, wr, hr, (i + 2 < nst ? i + 2 : nst - 1) * 64);
+            __builtin_amdgcn_sched_barrier(0);
+            fl_mma(Y, acc);
         }
+        if (i < nst) fl_mma(X, acc);
         // lane holds column c32 (a queued row) and rows 8 (r / 4) + 4 hf + r % 4
         for (int cb = 0; cb < 2; ++cb) {
             const int q = qb * FL_QB + cb * 32 + c32;
@@ -114,7 +138,11 @@ FilterQueue filter_queue_carve(void *base, int64_t cap, int ccap, int32_t *n, in
 }
 
 hipError_t launch_filter(const ScoreArgs &a, const FilterQueue &q, hipStream_t st) {
-    filter_kernel<<<1024, 256, 0, st>>>(a, q);
+    // One work item per workgroup for up to 64 queued rows per model (the queue sizes
+    // live on the device); larger queues stride.
+    const int64_t n_vt = (a.V + FL_VR - 1) / FL_VR;
+    const int64_t grid = 2 * n_vt < 65536 ? 2 * n_vt : 65536;
+    filter_kernel<<<(unsigned)grid, 256, 0, st>>>(a, q);
     return hipGetLastError();
 }
 
