@@ -229,11 +229,15 @@ def test_multi_turn_workload_sampled():
     torch.cuda.empty_cache()
 
 
-def test_student_only_token_logprobs():
-    say("student only")
-    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+# student-only contexts: every block of a unit is a student block (one K step each in
+# narrow_k and v257), so each block end moves to the next vocabulary tile
+@pytest.mark.parametrize("case", ["ragged_v1000", "multi_tile", "narrow_k", "v257"])
+def test_student_only_token_logprobs(case):
+    say("student only", case)
+    wl = custom(case, **CASES[case])
     hip = run_hip(wl, student_only=True, outputs=("logp_s", "am_s"))
-    compare(hip, wl, student_only=True, label="student-only")
+    assert hip["stats"]["kernel"] == "mfma"
+    compare(hip, wl, student_only=True, label="student-only-" + case)
 
 
 def test_tiny_workload_full():
