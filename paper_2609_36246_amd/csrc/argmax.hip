@@ -2,12 +2,15 @@
 // pairs whose fp32 top-2 logit gap fell inside the fp32 error window (flagged by the
 // combine pass with theta, a lower bound of the exact value of the fp32 winner).
 //
-// The exact maximum is >= theta, and every fp32 logit lies within
-// delta = d 2^-23 |h| max_v |w_v| of its exact value, so every entry that can be the
-// exact maximum has an fp32 logit >= theta - delta. The vocabulary filter (MFMA, up to
-// 64 queued rows per read of W) keeps those entries, their exact values (bf16
-// products summed in fp64) are formed and the largest wins, lower index first. A
-// pair with more than FX_CCAP such entries takes the exhaustive exact scan.
+// The exact maximum is >= theta, and every fp32 logit (in any summation order) lies
+// within delta = d 2^-23 |h| max_v |w_v| of its exact value, so every entry that can
+// be the exact maximum has an fp32 logit >= thr = theta - delta. The scoring pass left
+// per vocabulary split the fp32 maximum, second value (ties counted twice) and argmax
+// of the row: a split whose maximum is below thr holds no such entry, one whose second
+// value is below thr exactly one, at its argmax. Only splits whose second value reaches
+// thr are read again, by the vocabulary filter (MFMA, up to 64 queued rows per read).
+// The exact values of all these entries (bf16 products summed in fp64) decide, lower
+// index first. A pair with more than FX_CCAP entries takes the exhaustive exact scan.
 #include <hip/hip_runtime.h>
 
 #include "exact.hpp"
@@ -16,9 +19,10 @@
 
 namespace olive {
 
-// One wavefront per flagged row: queue each flagged model with its threshold.
-// Rows whose hidden state is zero need nothing: every logit is exactly 0 and the
-// scoring pass already took index 0.
+// One wavefront per flagged row: queue each flagged model with its threshold, its
+// candidates from the splits that hold at most one, and mark the other splits for the
+// filter. Rows whose hidden state is zero need nothing: every logit is exactly 0 and
+// the scoring pass already took index 0.
 __global__ void __launch_bounds__(256)
 fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
                 FilterQueue q) {
@@ -27,6 +31,7 @@ fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
     const int nf_all = a.sched->n_flagged;
     const int nf = nf_all < flag_cap ? nf_all : flag_cap;
     if (f >= nf) return;
+    const int ns = a.sched->n_splits;
     const int32_t j = flagged[4 * f];
     const int fl = flagged[4 * f + 1];
     const int64_t g = a.rowmap[j] & 0x7fffffffu;
@@ -39,13 +44,30 @@ fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
         const float theta = __int_as_float(flagged[4 * f + 2 + m]);
         const float delta =
             (float)d * 0x1p-23f * (sqrtf(hh) * (1.0f + 0x1p-10f)) * (m ? a.wmax_t : a.wmax_s);
+        const float thr = theta - delta;
+        // lane s < ns: split s's maximum, second value and argmax for this row
+        const int fb = m ? F_BEST_T : F_BEST_S;
+        float best = kNegInf, sec = kNegInf;
+        int idx = 0;
+        if (lane < ns) {
+            best = a.part[((fb + 0) * MAX_SPLITS + lane) * a.pstride + j];
+            sec = a.part[((fb + 1) * MAX_SPLITS + lane) * a.pstride + j];
+            idx = __float_as_int(a.part[((fb + 2) * MAX_SPLITS + lane) * a.pstride + j]);
+        }
+        const bool scan = sec >= thr;
+        const bool one = best >= thr && !scan;
+        const uint64_t one_mask = __ballot(one);
+        const uint64_t scan_mask = __ballot(scan);
+        int slot = lane == 0 ? atomicAdd(&q.n[m], 1) : 0;
+        slot = __shfl(slot, 0);
+        if (slot >= q.cap) continue;
+        int32_t *cd = q.cand + ((int64_t)m * q.cap + slot) * q.ccap;
+        if (one) cd[__popcll(one_mask & ((1ull << lane) - 1ull))] = idx;
         if (lane == 0) {
-            const int s = atomicAdd(&q.n[m], 1);
-            if (s < q.cap) {
-                q.qj[m * q.cap + s] = j;
-                q.qthr[m * q.cap + s] = theta - delta;
-                q.qcnt[m * q.cap + s] = 0;
-            }
+            q.qj[m * q.cap + slot] = j;
+            q.qthr[m * q.cap + slot] = thr;
+            q.qcnt[m * q.cap + slot] = __popcll(one_mask);
+            if (scan_mask) atomicOr(&q.smask[m], (uint32_t)scan_mask);
         }
     }
 }

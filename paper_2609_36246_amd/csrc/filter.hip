@@ -10,6 +10,7 @@ namespace olive {
 
 constexpr int FL_QB = 64;    // queued rows per work item (two 32-column MFMA blocks)
 constexpr int FL_VR = 128;   // vocabulary rows per work item (4 wavefronts x 32)
+static_assert(2 * FL_VR == MFMA_BV, "two work-item tiles per tile of the scoring pass");
 
 typedef __bf16 fl_bf16x8 __attribute__((ext_vector_type(8)));
 typedef float fl_floatx16 __attribute__((ext_vector_type(16)));
@@ -58,11 +59,25 @@ filter_kernel(ScoreArgs a, FilterQueue w) {
     // cheaper student items to whichever CUs finish early.
     const int64_t items1 = (int64_t)nqb[1] * n_vt;
     const int64_t items = items1 + (int64_t)nqb[0] * n_vt;
+    // With a split mask, only the vocabulary tiles of the marked splits of the scoring
+    // pass (split s: its 256-row tiles [n_vtiles s / ns, n_vtiles (s + 1) / ns)).
+    uint32_t sm[2] = {0xFFFFFFFFu, 0xFFFFFFFFu};
+    if (w.smask) {
+        sm[0] = w.smask[0];
+        sm[1] = w.smask[1];
+        if ((sm[0] | sm[1]) == 0u) return;
+    }
+    const int ns = a.sched->n_splits;
     for (int64_t it = blockIdx.x; it < items; it += gridDim.x) {
         const int m = it < items1 ? 1 : 0;
         const int64_t rel = m ? it : it - items1;
         const int qb = (int)(rel % nqb[m]);      // queued batch fastest: a vocabulary
         const int vt = (int)(rel / nqb[m]);      // tile is read by neighbouring items
+        if (w.smask) {
+            const int64_t t = vt >> 1;           // the scoring pass's 256-row tile
+            const int split = (int)(((t + 1) * ns - 1) / a.n_vtiles);
+            if (!((sm[m] >> split) & 1u)) continue;
+        }
         const int d = m ? a.dt : a.ds;
         const uint16_t *W = (const uint16_t *)(m ? a.wt : a.ws);
         const uint16_t *H = (const uint16_t *)(m ? a.ht : a.hs);
@@ -134,6 +149,7 @@ FilterQueue filter_queue_carve(void *base, int64_t cap, int ccap, int32_t *n, in
     q.qcnt = (int32_t *)p;   p += align256(c * 2 * 4);
     q.cand = (int32_t *)p;   p += align256(c * 2 * (size_t)ccap * 4);
     q.fb = (int32_t *)p;
+    q.smask = nullptr;
     return q;
 }
 

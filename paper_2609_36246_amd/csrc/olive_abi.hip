@@ -458,9 +458,11 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     }
     if (!s && c->mfma_ok) {
         s = dev_alloc(&c->fx_buf, filter_queue_bytes(c->flag_cap, FX_CCAP));
-        if (!s)
+        if (!s) {
             c->fxq = filter_queue_carve(c->fx_buf, c->flag_cap, FX_CCAP, &c->sched->n_fxq[0],
                                         &c->sched->n_fx_fb);
+            c->fxq.smask = &c->sched->fx_smask[0];   // the greedy filter reads marked splits
+        }
     }
     if (!s && c->bw) {
         const int64_t ch = (P + 127) / 128 * 128;

@@ -47,6 +47,8 @@ struct FilterQueue {
     int32_t *qcnt;       // [2][cap] candidates found (may exceed ccap)
     int32_t *cand;       // [2][cap][ccap] their vocabulary indices
     int32_t *fb;         // [2 cap] (model * cap + slot) of the pairs for the exhaustive scan
+    uint32_t *smask;     // device [2] or null: per model, the vocabulary splits (bit s) the
+                         // filter reads; null: every split
     int cap, ccap;
 };
 size_t filter_queue_bytes(int64_t cap, int ccap);
@@ -77,6 +79,8 @@ struct Sched {
     int32_t n_tk_fb;    // pairs of those that need the exhaustive exact scan
     int32_t n_fxq[2];   // near-tie (row, model) pairs of the greedy re-decision (MFMA path)
     int32_t n_fx_fb;    // pairs of those that need the exhaustive exact scan
+    uint32_t fx_smask[2];   // per model: vocabulary splits (bit s) the re-decision's filter
+                            // must read
 };
 
 // Top-K outputs of a call (null pointers: not requested).

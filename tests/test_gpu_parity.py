@@ -304,6 +304,31 @@ def test_duplicate_best_column_takes_lowest_index():
     compare(hip2, wl, label="dup-column")
 
 
+# Exact greedy ties placed in the winner's own 256-row tile (its split must be read
+# again) and/or in another split (decided from the per-split maximum and argmax alone).
+@pytest.mark.parametrize("partner", ["same_tile", "other_split", "both"])
+@pytest.mark.parametrize("case", ["even_v", "multi_tile"])
+def test_greedy_ties_within_and_across_splits(case, partner):
+    say("greedy ties", case, partner)
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl)
+    V = wl["spec"].vocab
+    for key, am in (("w_student", hip["am_s"]), ("w_teacher", hip["am_t"])):
+        j = int(am[am >= 0][0])
+        near = j ^ 1 if (j ^ 1) < V else j - 1
+        far = (j + V // 2) % V
+        partners = {"same_tile": [near], "other_split": [far], "both": [near, far]}[partner]
+        for p in partners:
+            wl[key][:, p] = wl[key][:, j]
+        tied = am == j
+        assert tied.any()
+        expect = min([j] + partners)
+        hip2 = run_hip(wl)
+        got = hip2["am_s"] if key == "w_student" else hip2["am_t"]
+        assert np.all(got[tied] == expect), (key, j, partners)
+    compare(hip2, wl, label="ties-%s-%s" % (case, partner))
+
+
 def test_deterministic_and_fully_written():
     say("determinism / poisoned outputs")
     wl = custom("multi_tile", **CASES["multi_tile"])
