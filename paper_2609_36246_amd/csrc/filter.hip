@@ -1,7 +1,9 @@
 // The vocabulary filter of the exact decisions on the bf16 MFMA path: for every
 // queued (row, model) pair, the indices of the vocabulary entries whose fp32 logit
 // reaches the pair's threshold. The threshold is set so that every entry that can
-// win the exact decision is among them; the exact values are formed afterwards.
+// win the exact decision is among them; the exact values are formed afterwards. With
+// a split mask (the greedy re-decision), only the vocabulary splits it marks are read;
+// the candidates of the other splits are already queued.
 #include <hip/hip_runtime.h>
 
 #include "olive_internal.hpp"
