@@ -306,8 +306,9 @@ def test_duplicate_best_column_takes_lowest_index():
 
 # Exact greedy ties placed in the winner's own 256-row tile (its split must be read
 # again) and/or in another split (decided from the per-split maximum and argmax alone).
+# narrow_k's widths (64 and 192: one and three K steps) take the filter's odd tail.
 @pytest.mark.parametrize("partner", ["same_tile", "other_split", "both"])
-@pytest.mark.parametrize("case", ["even_v", "multi_tile"])
+@pytest.mark.parametrize("case", ["even_v", "multi_tile", "narrow_k"])
 def test_greedy_ties_within_and_across_splits(case, partner):
     say("greedy ties", case, partner)
     wl = custom(case, **CASES[case])
