@@ -330,6 +330,37 @@ def test_greedy_ties_within_and_across_splits(case, partner):
     compare(hip2, wl, label="ties-%s-%s" % (case, partner))
 
 
+def test_one_context_across_batches_of_different_sizes():
+    """Per-call state (counts, near-tie lists, filter queues and split masks) starts
+    afresh on every call: one context scores a batch with a planted greedy tie, a
+    smaller batch of the same weights, and the first batch again."""
+    say("one context, three calls")
+    big = custom("multi_tile", **CASES["multi_tile"])
+    kw = dict(CASES["multi_tile"])
+    kw.update(num_seqs=2, ragged_len=(60, 200))
+    small = custom("multi_tile_small", **kw)
+    assert torch.equal(small["w_student"], big["w_student"])
+    assert torch.equal(small["w_teacher"], big["w_teacher"])
+    # a tie in the winner's own tile: the greedy filter must read that split again
+    am = run_hip(big)["am_s"]
+    j = int(am[am >= 0][0])
+    p = j ^ 1 if (j ^ 1) < big["spec"].vocab else j - 1
+    for w in (big, small):
+        w["w_student"][:, p] = w["w_student"][:, j]
+    first = run_hip(big, outputs=ALL_OUT, keep_ctx=True)
+    ctx = first["ctx"]
+    try:
+        compare(first, big, label="ctx-call1")
+        second = run_hip(small, outputs=ALL_OUT, ctx=ctx)
+        compare(second, small, label="ctx-call2")
+        third = run_hip(big, outputs=ALL_OUT, ctx=ctx)
+        compare(third, big, label="ctx-call3")
+        for k in ("kl", "kl_rev", "logp_s", "logp_t", "am_s", "am_t", "ce", "counts"):
+            np.testing.assert_array_equal(first[k], third[k], err_msg=k)
+    finally:
+        L.olive_score_free(ctx)
+
+
 def test_deterministic_and_fully_written():
     say("determinism / poisoned outputs")
     wl = custom("multi_tile", **CASES["multi_tile"])
