@@ -199,11 +199,13 @@ size_t fixup_result_bytes();
 hipError_t launch_ce(const olive_batch &b, const olive_spans *spans, const int32_t *seqbuf,
                      const Sched *sched, const float *logp_s, float *ce, hipStream_t st);
 
-// Layout of the per-sequence workspace (int32, 4 * (max_seqs + 1) entries).
-//   [0, B+1)          exclusive prefix sum of valid lengths (compacted row offsets)
+// Layout of the per-sequence workspace (int32, 5 * (max_seqs + 1) entries).
+//   [0, B+1)          exclusive prefix sum of compacted rows per sequence (valid, or
+//                     in-region when only the region is compacted)
 //   [B+1, 2B+2)       effective valid length per sequence (0 for a bad sequence)
 //   [2B+2, 3B+3)      effective cut per sequence
 //   [3B+3, 4B+4)      1 when the sequence's cut / valid length was out of range
-inline int64_t seqbuf_entries(int64_t max_seqs) { return 4 * (max_seqs + 1); }
+//   [4B+4, 5B+5)      exclusive prefix sum of in-region valid rows per sequence
+inline int64_t seqbuf_entries(int64_t max_seqs) { return 5 * (max_seqs + 1); }
 
 }  // namespace olive

@@ -57,6 +57,23 @@ __device__ __forceinline__ int region_count(int region, int vl, int cut) {
     return vl;
 }
 
+// Rank of valid position t outside the region among the sequence's valid positions
+// outside it. In the span region t lies in no span, so every span that starts before
+// t also ends at or before it.
+__device__ __forceinline__ int outside_rank(int region, const SpanArgs &sp, int b, int t, int cut,
+                                            int vl) {
+    if (region == OLIVE_REGION_TEACHER) return t;         // t < cut
+    if (region == OLIVE_REGION_STUDENT) return t - cut;   // cut <= t < vl
+    int r = 0;
+    for (int i = sp.off[b]; i < sp.off[b + 1]; ++i) {
+        const int a = sp.pairs[2 * i];
+        if (a >= t) break;
+        const int e = sp.pairs[2 * i + 1] < vl ? sp.pairs[2 * i + 1] : vl;
+        r += e > a ? e - a : 0;
+    }
+    return t - r;
+}
+
 constexpr int PREP_THREADS = 1024;
 
 // One workgroup: validates the batch structure, derives per-sequence effective
@@ -71,6 +88,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             int32_t fixed_splits, int32_t min_splits) {
     __shared__ int s_bad, s_badoff;
     __shared__ int s_scan[PREP_THREADS];
+    __shared__ int s_scan_sc[PREP_THREADS];
     __shared__ long long s_red[PREP_THREADS];
     __shared__ long long s_val[PREP_THREADS];
     const int tid = threadIdx.x;
@@ -94,9 +112,11 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
     int32_t *vl_eff = seqbuf + (B + 1);
     int32_t *cut_eff = seqbuf + 2 * (B + 1);
     int32_t *badseq = seqbuf + 3 * (B + 1);
+    int32_t *cscored = seqbuf + 4 * (B + 1);
     if (s_bad) {
         for (int b = tid; b <= B; b += PREP_THREADS) {
             cvalid[b] = 0;
+            cscored[b] = 0;
             if (b < B) { vl_eff[b] = 0; cut_eff[b] = 0; badseq[b] = 1; }
         }
         if (tid == 0) {
@@ -110,7 +130,7 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
         }
         return;
     }
-    int carry = 0;
+    int carry = 0, carry_sc = 0;
     long long scored = 0, valid = 0;
     for (int base = 0; base < B; base += PREP_THREADS) {
         int b = base + tid;
@@ -150,13 +170,16 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             }
         }
         s_scan[tid] = v;
+        s_scan_sc[tid] = (int)sc;
         s_red[tid] = sc;
         s_val[tid] = vv;
         __syncthreads();
-        for (int off = 1; off < PREP_THREADS; off <<= 1) {   // inclusive scan
+        for (int off = 1; off < PREP_THREADS; off <<= 1) {   // inclusive scans
             int add = tid >= off ? s_scan[tid - off] : 0;
+            int add_sc = tid >= off ? s_scan_sc[tid - off] : 0;
             __syncthreads();
             s_scan[tid] += add;
+            s_scan_sc[tid] += add_sc;
             __syncthreads();
         }
         for (int off = PREP_THREADS / 2; off > 0; off >>= 1) {  // fixed-order sums
@@ -166,14 +189,19 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             }
             __syncthreads();
         }
-        if (b < B) cvalid[b] = carry + s_scan[tid] - v;
+        if (b < B) {
+            cvalid[b] = carry + s_scan[tid] - v;
+            cscored[b] = carry_sc + s_scan_sc[tid] - (int)sc;
+        }
         carry += s_scan[PREP_THREADS - 1];
+        carry_sc += s_scan_sc[PREP_THREADS - 1];
         scored += s_red[0];
         valid += s_val[0];
         __syncthreads();
     }
     if (tid == 0) {
         cvalid[B] = carry;
+        cscored[B] = carry_sc;
         int t_valid = carry;   // compacted rows: valid, or in-region when region-only
         int n_p = (t_valid + tile_rows - 1) / tile_rows;
         int ns = 1;
@@ -207,9 +235,12 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
     }
 }
 
-// Maps every packed row to its compacted index (valid rows, or with region_only
-// in-region rows only) and writes the fixed outputs of rows that are not scored
-// (logp 0, argmax -1, kl +0) and of rows of malformed sequences (NaN, argmax -1).
+// Maps every packed row to its compacted index and writes the fixed outputs of rows
+// that are not scored (logp 0, argmax -1, kl +0) and of rows of malformed sequences
+// (NaN, argmax -1). With region_only only in-region rows are compacted; otherwise the
+// valid rows are, the in-region ones first ([0, n_scored), by sequence and position)
+// and then the others, so that work needed only for scored rows covers the leading
+// position tiles.
 __global__ void __launch_bounds__(256)
 rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t region,
               SpanArgs sp, int32_t region_only, const int32_t *__restrict__ seqbuf,
@@ -222,7 +253,9 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
     const int32_t *vl_eff = seqbuf + (B + 1);
     const int32_t *cut_eff = seqbuf + 2 * (B + 1);
     const int32_t *badseq = seqbuf + 3 * (B + 1);
+    const int32_t *cscored = seqbuf + 4 * (B + 1);
     const bool cu_bad = sched->cu_bad != 0;
+    const int32_t n_scored = (int32_t)sched->n_scored;
     const float qnan = __builtin_nanf("");
     for (int64_t g = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; g < T;
          g += (int64_t)gridDim.x * blockDim.x) {
@@ -266,7 +299,11 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             }
         }
         if (t < vl && !region_only) {
-            rowmap[cvalid[b] + t] = (uint32_t)g | ((r ? 1u : 0u) << 31);
+            const int idx =
+                r ? cscored[b] + region_rank(region, sp, b, span, t, cut_eff[b], vl)
+                  : n_scored + (cvalid[b] - cscored[b]) +
+                        outside_rank(region, sp, b, t, cut_eff[b], vl);
+            rowmap[idx] = (uint32_t)g | ((r ? 1u : 0u) << 31);
         } else if (t < vl && r) {
             rowmap[cvalid[b] + region_rank(region, sp, b, span, t, cut_eff[b], vl)] =
                 (uint32_t)g | (1u << 31);

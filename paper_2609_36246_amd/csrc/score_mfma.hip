@@ -407,6 +407,8 @@ struct Kernel {
     }
 
     // Fold the lane's 2 columns x 64 rows of both models, block by block.
+    // LISTS: also offer the blocks to the lanes' top-K lists.
+    template <bool LISTS>
     static __device__ __forceinline__ void fold(const floatx16 (&accS)[4][2],
                                                 const floatx16 (&accT)[4][2], Run (&RS)[2],
                                                 Run (&RT)[2], float (&A)[2], float (&Bq)[2],
@@ -427,7 +429,7 @@ struct Kernel {
                 fold_block<HAS_T && REV>(zs, RS[cb], Bq[cb], zt, a.cS, a.sS, a.sT, vbase + vb * 32);
                 if (HAS_T)
                     fold_block<true>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
-                if (TOPK) {
+                if (LISTS) {
                     const uint32_t tie0 = 0xFFFFu - (uint32_t)(lvt * 64 + vb * 16);
                     topk_block(zs, KS[cb], tie0);
                     topk_block(zt, KT[cb], tie0);
@@ -501,6 +503,7 @@ struct Kernel {
 
     static __device__ __forceinline__ void run(ScoreArgs a) {
         const int t_valid = a.sched->t_valid;
+        const int64_t n_scored = TOPK ? a.sched->n_scored : 0;
         const int n_p = a.sched->n_ptiles;
         const int ns = a.sched->n_splits;
         const int n_units = a.sched->n_units;
@@ -582,11 +585,22 @@ struct Kernel {
             // back to end at V, and one more MFMA adds kMasked to its rows below vt*BV
             // (the logit is absorbed), so they drop out of every statistic and the fold
             // needs no masking.
-            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
-                if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
-                fold(accS, accT, RS, RT, AA, BB, KS, KT, a, row0 + L.wv * 128 + 4 * L.h,
-                     vt - vt0);
-            });
+            // Top-K lists only where they are used: the scored rows are compacted first,
+            // so only position tiles starting below n_scored hold any.
+            const bool lists = TOPK && (int64_t)p * BT < n_scored;
+            if (lists) {
+                sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+                    if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
+                    fold<true>(accS, accT, RS, RT, AA, BB, KS, KT, a,
+                               row0 + L.wv * 128 + 4 * L.h, vt - vt0);
+                });
+            } else {
+                sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+                    if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
+                    fold<false>(accS, accT, RS, RT, AA, BB, KS, KT, a,
+                                row0 + L.wv * 128 + 4 * L.h, vt - vt0);
+                });
+            }
 
             // Merge lanes l and l+32 (same columns, interleaved vocabulary rows).
 #pragma unroll
@@ -607,7 +621,7 @@ struct Kernel {
             // (nothing is dropped); the floor bounds everything either lane dropped.
             float Q8v[2][2][8], Qfl[2][2];
             int Q8i[2][2][8];
-            if (TOPK) {
+            if (lists) {
 #pragma unroll
                 for (int m = 0; m < 2; ++m)
 #pragma unroll
@@ -654,7 +668,7 @@ struct Kernel {
                     o[3] = RS[cb].z;
                     o[4] = RT[cb].best; o[5] = RT[cb].sec; o[6] = __int_as_float(RT[cb].idx);
                     o[7] = RT[cb].z; o[8] = AA[cb]; o[9] = BB[cb];
-                    if (TOPK) {
+                    if (lists) {
 #pragma unroll
                         for (int m = 0; m < 2; ++m) {
                             float *q = xk + (((L.wt * 2 + cb) * 32 + L.l32) * 2 + m) * 17;
@@ -695,7 +709,7 @@ struct Kernel {
                             P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT[cb].z;
                             P[(F_A * MAX_SPLITS + s) * ps + j] = AA[cb];
                             if (REV) P[(F_B * MAX_SPLITS + s) * ps + j] = BB[cb];
-                            if (TOPK) {
+                            if (lists) {
                                 // the other half's top-8 into this one's: the 8 dropped
                                 // raise the floor
 #pragma unroll
