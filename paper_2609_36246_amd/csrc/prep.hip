@@ -124,8 +124,8 @@ prep_kernel(const int32_t *__restrict__ cu, const int32_t *__restrict__ cut,
             sched->t_valid = 0; sched->n_ptiles = 0; sched->n_splits = 1; sched->n_units = 0;
             sched->n_scored = 0; sched->n_flagged = 0; sched->cu_bad = 1;
             sched->n_tkq[0] = 0; sched->n_tkq[1] = 0; sched->n_tk_fb = 0;
-        sched->n_fxq[0] = 0; sched->n_fxq[1] = 0; sched->n_fx_fb = 0;
-        sched->fx_smask[0] = 0u; sched->fx_smask[1] = 0u;
+            sched->n_fxq[0] = 0; sched->n_fxq[1] = 0; sched->n_fx_fb = 0;
+            sched->fx_smask[0] = 0u; sched->fx_smask[1] = 0u;
             if (counts) { counts[0] = 0; counts[1] = 0; }
         }
         return;
