@@ -815,7 +815,12 @@ struct Kernel {
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
             floatx16 accS[4][2], accT[4][2];
             sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
-                const int vlo = vt * BV;   // rows below vlo of a shifted last tile: done
+                // A shifted last tile (V not a multiple of 256) starts at V - 256, which
+                // may be any row: its rows below vlo were stored by the previous tile,
+                // and its 4-row groups may straddle vlo and sit off 8-byte alignment in
+                // dz_t, so it stores row by row.
+                const int vlo = vt * BV;
+                const bool shifted = row0 != vlo;
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -840,8 +845,8 @@ struct Kernel {
                             uint2 w;
                             w.x = ok[cb] ? pack_bf16x2(gr[0], gr[1]) : 0u;
                             w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
-                            if (v0 >= vlo) {   // the 4 rows share the test (vlo % 4 == 0)
-                                const int t = tcol[cb];
+                            const int t = tcol[cb];
+                            if (!shifted) {
                                 if (t < z.pitch) {
                                     uint16_t *col = z.dz_v + (int64_t)v0 * z.pitch + t;
                                     col[0] = (uint16_t)w.x;
@@ -850,6 +855,15 @@ struct Kernel {
                                     col[3 * (int64_t)z.pitch] = (uint16_t)(w.y >> 16);
                                 }
                                 if (ok[cb]) *(uint2 *)(z.dz_t + (int64_t)t * z.vp + v0) = w;
+                            } else {
+                                const uint16_t q[4] = {(uint16_t)w.x, (uint16_t)(w.x >> 16),
+                                                       (uint16_t)w.y, (uint16_t)(w.y >> 16)};
+#pragma unroll
+                                for (int e = 0; e < 4; ++e) {
+                                    if (v0 + e < vlo) continue;
+                                    if (t < z.pitch) z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = q[e];
+                                    if (ok[cb]) z.dz_t[(int64_t)t * z.vp + v0 + e] = q[e];
+                                }
                             }
                         }
                     }

@@ -132,6 +132,12 @@ CASES = {
     "even_v": dict(num_seqs=2, seq_len=200, vocab=2048, d_student=384, d_teacher=512,
                    target_source="teacher", cut_rule=("abs", 1, 199), outlier_frac=0.05,
                    outlier_mul=8.0),
+    # V % 4 != 0: the shifted last vocabulary tile starts off 4-row alignment (at 1 and
+    # at 745), so its first new row sits inside a 4-row group of the tile's lanes
+    "v257": dict(num_seqs=2, seq_len=150, vocab=257, d_student=64, d_teacher=64,
+                 logit_scale=2.0, cut_rule=("abs", 1, 149)),
+    "v1001": dict(num_seqs=3, ragged_len=(60, 200), vocab=1001, d_student=128,
+                  d_teacher=64, target_source="student", cut_rule=("frac", 0.1, 0.9)),
 }
 
 
