@@ -84,6 +84,11 @@ __device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
     return lo > m ? lo : m;
 }
 
+// Per-wave LDS staging of the logit-gradient pass's dz_v blocks (32 rows x 64
+// columns of bf16 per wave), beside the ring: only that pass's kernel allocates it.
+constexpr int DZV_STAGE = 32 * 64 * 2;
+__shared__ __attribute__((aligned(16))) char g_dzv[4 * DZV_STAGE];
+
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 struct Kernel {
     // Issue cursor: the next step to prefetch. Wave-uniform: its model block (vocabulary
@@ -814,13 +819,87 @@ struct Kernel {
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
             floatx16 accS[4][2], accT[4][2];
+            // g of rows v0 .. v0+3 (v0 = the lane's row of 32-row block vb, quad rq) at
+            // column cb, as two packed bf16 pairs (zero for columns past the scored rows)
+            auto grad4 = [&](int vb, int cb, int rq, int v0) {
+                float gr[4];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const float zs = agpr_read(accS[vb][cb][4 * rq + e]);
+                    gr[e] = wsum * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
+                    if (HAS_T) {
+                        const float zt = agpr_read(accT[vb][cb][4 * rq + e]);
+                        gr[e] = fmaf(-z.w_kl, fast_exp2(fmaf(zt, a.cT, -l2t[cb])), gr[e]);
+                    }
+                    gr[e] -= (v0 + e == ycol[cb]) ? z.w_ce : 0.f;
+                }
+                uint2 w;
+                w.x = ok[cb] ? pack_bf16x2(gr[0], gr[1]) : 0u;
+                w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
+                return w;
+            };
+            // the wave's 4 KB staging area for dz_v: [32 rows][64 columns] bf16, 16-byte
+            // chunk c of row r at slot c ^ (4 * bit 2 of r), so that the two 4-row halves
+            // of a store instruction land in different banks
+            char *stg = g_dzv + L.wid * DZV_STAGE;
+            const int tw0 = p * BT + L.wt * 64;   // the wave's first column
             sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
-                // A shifted last tile (V not a multiple of 256) starts at V - 256, which
-                // may be any row: its rows below vlo were stored by the previous tile,
-                // and its 4-row groups may straddle vlo and sit off 8-byte alignment in
-                // dz_t, so it stores row by row.
                 const int vlo = vt * BV;
-                const bool shifted = row0 != vlo;
+                const int vw0 = row0 + L.wv * 128;   // the wave's first row
+                if (row0 == vlo) {
+                    // Whole 16-byte pieces. dz_t: lanes l and l+32 hold rows 8q .. 8q+3
+                    // and 8q+4 .. 8q+7 of one column for quads q = 2k, 2k+1; one swap of
+                    // their upper and lower halves gives each 8 consecutive rows. dz_v:
+                    // the 32 x 64 block of each vb goes through LDS and leaves as whole
+                    // 128-byte rows.
+#pragma unroll
+                    for (int vb = 0; vb < 4; ++vb) {
+#pragma unroll
+                        for (int cb = 0; cb < 2; ++cb) {
+                            __builtin_amdgcn_sched_barrier(0);
+                            uint2 w[4];
+#pragma unroll
+                            for (int rq = 0; rq < 4; ++rq)
+                                w[rq] = grad4(vb, cb, rq, vw0 + vb * 32 + 8 * rq + 4 * L.h);
+#pragma unroll
+                            for (int k = 0; k < 2; ++k) {
+                                const auto X = __builtin_amdgcn_permlane32_swap(
+                                    w[2 * k].x, w[2 * k + 1].x, false, false);
+                                const auto Y = __builtin_amdgcn_permlane32_swap(
+                                    w[2 * k].y, w[2 * k + 1].y, false, false);
+                                if (ok[cb])
+                                    *(uint4 *)(z.dz_t + (int64_t)tcol[cb] * z.vp + vw0 + vb * 32 +
+                                               16 * k + 8 * L.h) =
+                                        make_uint4(X[0], Y[0], X[1], Y[1]);
+                            }
+                            const int cc = cb * 32 + L.l32;   // column in the wave's 64
+#pragma unroll
+                            for (int rq = 0; rq < 4; ++rq) {
+                                const int r = 8 * rq + 4 * L.h;
+                                const int sl = ((cc >> 3) ^ (4 * L.h)) << 4;
+                                char *q = stg + r * 128 + sl + (cc & 7) * 2;
+                                *(uint16_t *)(q) = (uint16_t)w[rq].x;
+                                *(uint16_t *)(q + 128) = (uint16_t)(w[rq].x >> 16);
+                                *(uint16_t *)(q + 256) = (uint16_t)w[rq].y;
+                                *(uint16_t *)(q + 384) = (uint16_t)(w[rq].y >> 16);
+                            }
+                        }
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const int r = 8 * i + (L.lane >> 3), c = L.lane & 7;
+                            const uint4 q =
+                                *(const uint4 *)(stg + r * 128 + ((c ^ (4 * ((r >> 2) & 1))) << 4));
+                            const int t = tw0 + 8 * c;
+                            if (t + 8 <= z.pitch)
+                                *(uint4 *)(z.dz_v + (int64_t)(vw0 + vb * 32 + r) * z.pitch + t) = q;
+                        }
+                    }
+                    return;
+                }
+                // A shifted last tile (V not a multiple of 256) starts at V - 256, which
+                // may be any row: its rows below vlo were stored by the previous tile, and
+                // its 4-row groups may straddle vlo and sit off 8-byte alignment in dz_t,
+                // so it stores row by row.
 #pragma unroll
                 for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
@@ -828,42 +907,16 @@ struct Kernel {
                         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                         for (int rq = 0; rq < 4; ++rq) {
-                            const int v0 = row0 + L.wv * 128 + vb * 32 + 8 * rq + 4 * L.h;
-                            float gr[4];
+                            const int v0 = vw0 + vb * 32 + 8 * rq + 4 * L.h;
+                            const uint2 w = grad4(vb, cb, rq, v0);
+                            const uint16_t q[4] = {(uint16_t)w.x, (uint16_t)(w.x >> 16),
+                                                   (uint16_t)w.y, (uint16_t)(w.y >> 16)};
+                            const int t = tcol[cb];
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
-                                const float zs = agpr_read(accS[vb][cb][4 * rq + e]);
-                                gr[e] = wsum * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
-                                if (HAS_T) {
-                                    const float zt = agpr_read(accT[vb][cb][4 * rq + e]);
-                                    gr[e] = fmaf(-z.w_kl, fast_exp2(fmaf(zt, a.cT, -l2t[cb])),
-                                                 gr[e]);
-                                }
-                                gr[e] -= (v0 + e == ycol[cb]) ? z.w_ce : 0.f;
-                            }
-                            // rows v0, v0+1 and v0+2, v0+3 as packed bf16 pairs
-                            uint2 w;
-                            w.x = ok[cb] ? pack_bf16x2(gr[0], gr[1]) : 0u;
-                            w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
-                            const int t = tcol[cb];
-                            if (!shifted) {
-                                if (t < z.pitch) {
-                                    uint16_t *col = z.dz_v + (int64_t)v0 * z.pitch + t;
-                                    col[0] = (uint16_t)w.x;
-                                    col[z.pitch] = (uint16_t)(w.x >> 16);
-                                    col[2 * (int64_t)z.pitch] = (uint16_t)w.y;
-                                    col[3 * (int64_t)z.pitch] = (uint16_t)(w.y >> 16);
-                                }
-                                if (ok[cb]) *(uint2 *)(z.dz_t + (int64_t)t * z.vp + v0) = w;
-                            } else {
-                                const uint16_t q[4] = {(uint16_t)w.x, (uint16_t)(w.x >> 16),
-                                                       (uint16_t)w.y, (uint16_t)(w.y >> 16)};
-#pragma unroll
-                                for (int e = 0; e < 4; ++e) {
-                                    if (v0 + e < vlo) continue;
-                                    if (t < z.pitch) z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = q[e];
-                                    if (ok[cb]) z.dz_t[(int64_t)t * z.vp + v0 + e] = q[e];
-                                }
+                                if (v0 + e < vlo) continue;
+                                if (t < z.pitch) z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = q[e];
+                                if (ok[cb]) z.dz_t[(int64_t)t * z.vp + v0 + e] = q[e];
                             }
                         }
                     }
