@@ -89,6 +89,10 @@ def main():
                          "summed loss, plus --backward-kl times the summed KL)")
     ap.add_argument("--backward-kl", type=float, default=0.0, metavar="W",
                     help="KL weight of the --backward loss (default 0: Eq. 1 alone)")
+    ap.add_argument("--train-step", action="store_true",
+                    help="with --backward: each step is a forward call (KL, both models' "
+                         "log-probs, per-sequence CE) and a backward that reuses its "
+                         "normalisers (OLIVE_GRAD_REUSE_FORWARD)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 3 plain device copies of BYTES bytes (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -109,6 +113,9 @@ def main():
         sys.exit(2)
     if not 1 <= args.steps <= 64:
         print("--steps must be in [1, 64]", file=sys.stderr)
+        sys.exit(2)
+    if args.train_step and not args.backward:
+        print("--train-step applies to --backward", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -231,7 +238,8 @@ def main():
 
 def bench_backward(args, wl, L):
     """One olive_score_backward call per step: the forward normalisers of the scored
-    rows, the logit gradient and the two products, both gradients requested."""
+    rows, the logit gradient and the two products, both gradients requested. With
+    --train-step, a forward call first, whose normalisers the backward reuses."""
     import torch
     spec = wl["spec"]
     T = wl["total_positions"]
@@ -250,9 +258,20 @@ def bench_backward(args, wl, L):
                          L.OLIVE_REGION_SPANS if use_spans else L.OLIVE_REGION_TEACHER)
     spans = L.make_spans(wl["span_offsets"], wl["span_pairs"]) if use_spans else None
     counts = torch.zeros(2, dtype=torch.int64, device=dev)
-    g = L.make_grad_outputs(1.0, args.backward_kl, gh, gw, counts)
+    train = args.train_step
+    g = L.make_grad_outputs(1.0, args.backward_kl, gh, gw, counts, reuse_forward=train)
+    if train:
+        f32 = dict(dtype=torch.float32, device=dev)
+        fo = L.make_outputs(kl=torch.empty(T, **f32), logp_student=torch.empty(T, **f32),
+                            logp_teacher=torch.empty(T, **f32),
+                            ce_per_seq=torch.empty(B, **f32))
 
     def step():
+        if train:
+            if spans is not None:
+                L.olive_score_batch_spans(ctx, batch, spans, fo, stream=stream)
+            else:
+                L.olive_score_batch(ctx, batch, fo, stream=stream)
         L.olive_score_backward(ctx, batch, g, spans=spans, stream=stream)
 
     for _ in range(args.warmup):
@@ -270,20 +289,31 @@ def bench_backward(args, wl, L):
     err = L.olive_score_last_error(ctx)
     L.olive_score_free(ctx)
     R = int(counts[0].item())
+    Tv = int(counts[1].item())
     dt = spec.d_teacher if args.backward_kl else 0
-    # forward normalisers and the logit-gradient pass each project both models; the
-    # two products are 2 R V d_S each
-    flops = 2.0 * R * spec.vocab * (2 * (spec.d_student + dt) + 2 * spec.d_student)
-    log("timed %d backward steps: %.3f ms/step, err %d" % (args.steps, ms_step, err))
+    if train:
+        # the forward projects both models over the valid rows; the backward's
+        # logit-gradient pass and its two products
+        flops = 2.0 * spec.vocab * (Tv * (spec.d_student + spec.d_teacher) +
+                                    R * (spec.d_student + dt + 2 * spec.d_student))
+    else:
+        # forward normalisers and the logit-gradient pass each project both models;
+        # the two products are 2 R V d_S each
+        flops = 2.0 * R * spec.vocab * (2 * (spec.d_student + dt) + 2 * spec.d_student)
+    log("timed %d %s steps: %.3f ms/step, err %d"
+        % (args.steps, "training" if train else "backward", ms_step, err))
     out = {
-        "metric": "scored positions/sec, backward (dL/dh_S, dL/dW_S) of the masked CE",
+        "metric": ("scored positions/sec, training step (forward outputs + backward reusing "
+                   "its normalisers) of the masked CE" if train else
+                   "scored positions/sec, backward (dL/dh_S, dL/dW_S) of the masked CE"),
         "value": R / (ms_step * 1e-3), "unit": "positions/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; random hidden states and weights of the workload's shapes)",
         "config": {"workload": args.workload, "scored_positions": R, "vocab": spec.vocab,
                    "d_student": spec.d_student, "d_teacher": spec.d_teacher,
-                   "w_ce": 1.0, "w_kl": args.backward_kl,
+                   "w_ce": 1.0, "w_kl": args.backward_kl, "train_step": train,
+                   "valid_positions": Tv,
                    "step_tflops": flops / (ms_step * 1e-3) / 1e12,
                    "pct_bf16_peak_step": 100.0 * flops / (ms_step * 1e-3) / 1e12 /
                    PEAK_BF16_TFLOPS},

@@ -252,7 +252,7 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
  */
 typedef struct {
     int32_t size;                /* host: sizeof(olive_grad_outputs) (checked) */
-    int32_t flags;               /* 0 */
+    int32_t flags;               /* 0 or OLIVE_GRAD_REUSE_FORWARD */
     float w_ce;                  /* weight of the CE sum, finite */
     float w_kl;                  /* weight of the KL sum, finite; 0 leaves the teacher out
                                     (its hidden states may then be NULL) */
@@ -263,6 +263,17 @@ typedef struct {
     int64_t *counts;             /* [2] int64 or NULL: scored and valid positions */
 } olive_grad_outputs;
 
+/* olive_grad_outputs.flags: take the log-normalisers (lse_S, and lse_T when w_kl != 0)
+ * from the last forward call on this context (olive_score_batch, _spans, olive_kl_masked,
+ * olive_token_logprobs) instead of recomputing them, which saves one MFMA pass over the
+ * student's (and teacher's) vocabulary. That call must have run on the MFMA path with
+ * the same batch: the same sizes, region, spans and device pointers, holding the same
+ * data (the caller's part: contents are not compared), and must be ordered before the
+ * backward (the same stream, or the caller's synchronisation). Otherwise, or after a
+ * backward without this flag has replaced the normalisers, or when w_kl != 0 and that
+ * call scored the student only, the backward returns E_RANGE. */
+#define OLIVE_GRAD_REUSE_FORWARD 1
+
 /*
  * Backward pass of the student's loss: dL/dh_S and dL/dW_S for the scaled logits
  * z_S = s_S h_S W_S. Per scored position the logit gradient is
@@ -272,7 +283,8 @@ typedef struct {
  * dL/dh = s_S g W^T and dL/dW = s_S h^T g, which accumulate in fp32.
  * spans: NULL, or the scored spans when b->region is OLIVE_REGION_SPANS.
  * Errors: E_NULL (g, or both gradient pointers, NULL; a required batch pointer NULL),
- * E_RANGE (g->size or flags wrong, a weight not finite, region / spans as for
+ * E_RANGE (g->size or flags wrong, OLIVE_GRAD_REUSE_FORWARD without a matching forward
+ * call, a weight not finite, region / spans as for
  * olive_score_batch_spans), E_UNSUPPORTED (no OLIVE_FLAG_BACKWARD at init; w_kl != 0
  * without a teacher; hidden states not 16-byte aligned), E_SHAPE as olive_kl_masked.
  * Content errors on the device set the error word as in the forward calls and make
@@ -281,6 +293,8 @@ typedef struct {
 olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,
                                   const olive_spans *spans, const olive_grad_outputs *g,
                                   void *hip_stream);
+/* With OLIVE_GRAD_REUSE_FORWARD the backward is the logit-gradient pass and the two
+ * products only: a training step's forward call supplies the normalisers. */
 
 /* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
 olive_status olive_score_free(olive_score_ctx *ctx);

@@ -37,6 +37,7 @@ OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
 OLIVE_FLAG_TOPK = 4
 OLIVE_FLAG_BACKWARD = 8
+OLIVE_GRAD_REUSE_FORWARD = 1
 OLIVE_TOPK = 16
 OLIVE_OUT_REGION_ONLY = 1
 
@@ -253,10 +254,10 @@ def make_spans(span_offsets, span_pairs, num_spans: Optional[int] = None) -> oli
 
 
 def make_grad_outputs(w_ce=1.0, w_kl=0.0, grad_h=None, grad_w=None,
-                      counts=None) -> olive_grad_outputs:
+                      counts=None, reuse_forward=False) -> olive_grad_outputs:
     o = olive_grad_outputs()
     o.size = ctypes.sizeof(olive_grad_outputs)
-    o.flags = 0
+    o.flags = OLIVE_GRAD_REUSE_FORWARD if reuse_forward else 0
     o.w_ce, o.w_kl = float(w_ce), float(w_kl)
     o.grad_h_student, o.grad_w_student = _ptr(grad_h), _ptr(grad_w)
     o.counts = _ptr(counts)

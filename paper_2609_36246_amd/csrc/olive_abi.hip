@@ -43,6 +43,15 @@ struct olive_score_ctx {
     uint16_t *bw_dzt = nullptr;                 // [chunk][bw_vp]
     uint16_t *bw_dzv = nullptr;                 // [V][chunk]
     uint16_t *bw_hrt = nullptr;                 // [d_S][chunk]
+    // Normalisers of the last forward call on the MFMA path and the batch they belong
+    // to, for a backward on that batch (OLIVE_GRAD_REUSE_FORWARD). Scored rows take the
+    // same compacted index in every pass (scored-first compaction), so the forward's
+    // rows [0, n_scored) are the backward's.
+    const float *fwd_lse = nullptr;             // bw_lse, or the top-K workspace's
+    bool fwd_lse_ok = false, fwd_lse_t = false; // valid; holds lse_T too
+    olive_batch fwd_batch = {};
+    bool fwd_spans = false;
+    olive_spans fwd_sp = {};
     bool bf16 = false, has_t = false, mfma_ok = false, topk = false;
     int last_kernel = -1, last_grid = 0;
     bool timing = false;
@@ -68,6 +77,20 @@ void release(olive_score_ctx *c) {
 }
 
 bool finite_positive(float x) { return std::isfinite(x) && x > 0.f; }
+
+// The batch (and spans) a call was given are those of the recorded forward call: the same
+// sizes, region and device pointers.
+bool same_batch(const olive_score_ctx *c, const olive_batch *b, const olive_spans *sp) {
+    const olive_batch &f = c->fwd_batch;
+    if (f.num_seqs != b->num_seqs || f.region != b->region ||
+        f.total_positions != b->total_positions || f.cu_seqlens != b->cu_seqlens ||
+        f.cut != b->cut || f.valid_len != b->valid_len || f.targets != b->targets ||
+        f.h_student != b->h_student || f.h_teacher != b->h_teacher)
+        return false;
+    if (c->fwd_spans != (sp != nullptr)) return false;
+    return !sp || (c->fwd_sp.num_spans == sp->num_spans &&
+                   c->fwd_sp.span_offsets == sp->span_offsets && c->fwd_sp.spans == sp->spans);
+}
 
 template <typename T>
 olive_status dev_alloc(T **p, size_t bytes) {
@@ -141,6 +164,9 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
+    // normalisers kept for a backward on this batch (MFMA path, backward contexts)
+    float *lse_out = topk ? ctx->tkw.lse : ((mfma && ctx->bw) ? ctx->bw_lse : nullptr);
+    ctx->fwd_lse_ok = false;
 
     olive_status s;
     int grid = 0;
@@ -204,8 +230,16 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     s = check_hip(launch_combine(a, ctx->bf16, has_t, same_scale, b->targets, ctx->err, logp_s,
                                  has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
                                  has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp,
-                                 topk ? ctx->tkw.lse : nullptr, flagged, ctx->flag_cap, T, st));
+                                 lse_out, flagged, ctx->flag_cap, T, st));
     if (s) return s;
+    if (mfma && ctx->bw && lse_out) {
+        ctx->fwd_lse = lse_out;
+        ctx->fwd_lse_ok = true;
+        ctx->fwd_lse_t = has_t;
+        ctx->fwd_batch = *b;
+        ctx->fwd_spans = spans != nullptr;
+        if (spans) ctx->fwd_sp = *spans;
+    }
     if (flagged) {
         if (mfma)
             s = check_hip(launch_argmax_fix(a, flagged, ctx->flag_cap, ctx->fxq, am_s,
@@ -249,6 +283,9 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     if (has_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
     if (((uintptr_t)b->h_student & 15) != 0 || (has_t && ((uintptr_t)b->h_teacher & 15) != 0))
         return OLIVE_E_UNSUPPORTED;
+    const bool reuse = (go->flags & OLIVE_GRAD_REUSE_FORWARD) != 0;
+    if (reuse && !(ctx->fwd_lse_ok && (!has_t || ctx->fwd_lse_t) && same_batch(ctx, b, spans)))
+        return OLIVE_E_RANGE;
     const int64_t T = b->total_positions;
     const int64_t V = d.vocab;
     const int n_vtiles = (int)((V + 255) / 256);
@@ -280,12 +317,19 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     a.wmax_s = ctx->wmax_s;
     a.wmax_t = ctx->wmax_t;
     const bool same_scale = has_t && (a.sS == a.sT);
-    s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
-    if (s) return s;
-    s = check_hip(launch_combine(a, true, has_t, same_scale, b->targets, ctx->err, nullptr,
-                                 nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                 ctx->bw_lse, nullptr, 0, T, st));
-    if (s) return s;
+    const float *lse = ctx->fwd_lse;
+    if (!reuse) {
+        // the forward normalisers of the scored rows; they replace a forward call's for
+        // reuse (always, wherever that call's are kept: one rule for every output set)
+        ctx->fwd_lse_ok = false;
+        s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
+        if (s) return s;
+        s = check_hip(launch_combine(a, true, has_t, same_scale, b->targets, ctx->err, nullptr,
+                                     nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                     ctx->bw_lse, nullptr, 0, T, st));
+        if (s) return s;
+        lse = ctx->bw_lse;
+    }
     const int ds = d.d_student;
     if (go->grad_h_student) {
         s = check_hip(launch_fill(go->grad_h_student, T * ds, st));
@@ -298,7 +342,7 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         z.chunk = ch;
         z.pitch = ch;
         z.vp = ctx->bw_vp;
-        z.lse = ctx->bw_lse;
+        z.lse = lse;
         z.targets = b->targets;
         z.w_ce = go->w_ce;
         z.w_kl = go->w_kl;
@@ -581,7 +625,8 @@ olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,
                                   const olive_spans *spans, const olive_grad_outputs *g,
                                   void *hip_stream) {
     if (!ctx || !b || !g) return OLIVE_E_NULL;
-    if (g->size != (int32_t)sizeof(olive_grad_outputs) || g->flags != 0) return OLIVE_E_RANGE;
+    if (g->size != (int32_t)sizeof(olive_grad_outputs) || (g->flags & ~OLIVE_GRAD_REUSE_FORWARD))
+        return OLIVE_E_RANGE;
     if (!std::isfinite(g->w_ce) || !std::isfinite(g->w_kl)) return OLIVE_E_RANGE;
     if (!g->grad_h_student && !g->grad_w_student) return OLIVE_E_NULL;
     if (!ctx->bw) return OLIVE_E_UNSUPPORTED;

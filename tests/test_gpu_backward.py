@@ -238,6 +238,68 @@ def test_backward_on_long_rollout_sampled():
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("mode", ["ce", "ce+kl", "ce+kl-topk"])
+def test_backward_reuses_forward_normalisers(mode):
+    """OLIVE_GRAD_REUSE_FORWARD: the normalisers of the preceding forward call on the same
+    batch stand in for the backward's own pass (from the top-K workspace when that call
+    asked for top-K outputs). The gradients meet the same bar and repeat bit for bit; the
+    flag is refused once no matching forward call holds them."""
+    say("backward reusing the forward normalisers", mode)
+    w_kl = 0.0 if mode == "ce" else 0.5
+    topk = mode.endswith("topk")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    spec = wl["spec"]
+    T = wl["total_positions"]
+    B = wl["cu_seqlens"].shape[0] - 1
+    dev = wl["h_student"].device
+    flags = L.OLIVE_FLAG_BACKWARD | (L.OLIVE_FLAG_TOPK if topk else 0)
+    desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher, L.OLIVE_BF16, L.OLIVE_W_DV,
+                       wl["scale_student"], wl["scale_teacher"], max_positions=T,
+                       max_seqs=B, flags=flags)
+    ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"])
+
+    def batch_of(region):
+        return L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"], wl["h_student"],
+                            wl["h_teacher"], wl["valid_len"], region)
+
+    def forward(batch):
+        kl = torch.empty(T, dtype=torch.float32, device=dev)
+        ov = torch.empty(T, dtype=torch.float32, device=dev) if topk else None
+        L.olive_score_batch(ctx, batch, L.make_outputs(kl=kl, topk_overlap=ov))
+
+    def backward(batch, reuse, check=True):
+        gh = torch.full((T, spec.d_student), float("nan"), dtype=torch.float32, device=dev)
+        gw = torch.full((spec.d_student * spec.vocab,), float("nan"), dtype=torch.float32,
+                        device=dev)
+        g = L.make_grad_outputs(1.0, w_kl, gh, gw, reuse_forward=reuse)
+        st = L.olive_score_backward(ctx, batch, g, check=check)
+        torch.cuda.synchronize()
+        return st, {"h": to_np(gh), "w": to_np(gw).reshape(spec.d_student, spec.vocab)}
+
+    batch = batch_of(L.OLIVE_REGION_TEACHER)
+    forward(batch)
+    _, a = backward(batch, True)
+    _, b = backward(batch, True)
+    np.testing.assert_array_equal(a["h"], b["h"])
+    np.testing.assert_array_equal(a["w"], b["w"])
+    ref = oracle_backward(wl, 1.0, w_kl, O.REGION_TEACHER)
+    check_grads(a, ref, wl, "reuse-" + mode)
+    # a backward without the flag replaces the normalisers
+    backward(batch, False)
+    assert backward(batch, True, check=False)[0] == L.OLIVE_E_RANGE
+    # the last forward call was on another batch (another region)
+    forward(batch)
+    forward(batch_of(L.OLIVE_REGION_ALL))
+    assert backward(batch, True, check=False)[0] == L.OLIVE_E_RANGE
+    if w_kl:
+        # a student-only forward call holds no teacher normalisers
+        lp = torch.empty(T, dtype=torch.float32, device=dev)
+        L.olive_token_logprobs(ctx, batch, lp)
+        assert backward(batch, True, check=False)[0] == L.OLIVE_E_RANGE
+    assert L.olive_score_last_error(ctx) == 0
+    L.olive_score_free(ctx)
+
+
 def test_backward_argument_errors():
     say("backward argument errors")
     wl = custom("narrow_k", **CASES["narrow_k"])
