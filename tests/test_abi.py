@@ -93,6 +93,15 @@ def test_struct_layouts_match_header(tmp_path):
     assert L.olive_score_outputs.topk_teacher.offset == 96
 
 
+def test_header_constants_match_the_binding():
+    """Every numeric #define of the header has the same value in the Python binding."""
+    text = open(HEADER).read()
+    defs = re.findall(r"^#define\s+(OLIVE_[A-Z0-9_]+)\s+(\d+)\s*$", text, re.M)
+    assert len(defs) >= 6
+    for name, value in defs:
+        assert getattr(L, name) == int(value), name
+
+
 def _init(desc, ws=1, wt=1):
     return L.olive_score_init(desc, ws, wt, stream=None, check=False)
 
