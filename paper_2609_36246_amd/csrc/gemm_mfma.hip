@@ -152,6 +152,23 @@ __device__ __forceinline__ void g_step(const GLane &L, int st, int pk, floatx16 
     }
 }
 
+// Tile (mi, ni) of the q-th tile in blocks of GM x GN tiles (bands of GM row tiles, each
+// cut into blocks of GN column tiles; the last band and block may be narrower), n
+// fastest inside a block. The 32 units one XCD runs together then share 4 A strips and
+// 8 B strips: 4 x 32 + 8 x 16 KB fetched per step, the fewest for a 256 x 128 tile.
+constexpr int GM = 4, GN = 8;
+__device__ __forceinline__ void tile_of(int64_t q, int tm, int tn, int &mi, int &ni) {
+    const int64_t per_band = (int64_t)GM * tn;
+    const int band = (int)(q / per_band);
+    const int hm = tm - GM * band < GM ? tm - GM * band : GM;   // rows of this band
+    const int r = (int)(q - band * per_band);
+    const int blk = r / (hm * GN);
+    const int w = tn - GN * blk < GN ? tn - GN * blk : GN;      // columns of this block
+    const int rr = r - blk * hm * GN;
+    mi = band * GM + rr / w;
+    ni = blk * GN + rr % w;
+}
+
 __device__ __forceinline__ int dev_count(const int32_t *p, int off, int cap, int host) {
     if (!p) return host;
     int n = *p - off;
@@ -189,8 +206,8 @@ gemm_mfma_kernel(GemmArgs g) {
         const int64_t q = u % n_tiles;
         const int kb = (int)(u / n_tiles) * kper;
         const int kn = ksteps - kb < kper ? ksteps - kb : kper;   // this unit's steps
-        const int mi = g.m_fast ? (int)(q % tm) : (int)(q / tn);
-        const int ni = g.m_fast ? (int)(q / tm) : (int)(q % tn);
+        int mi, ni;
+        tile_of(q, tm, tn, mi, ni);
         const int m0 = mi * BV, n0 = ni * BT;
         // A DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7
         // with chunk (lane&7) ^ swz(R); B DMA i rows R = wid*32 + 8i + lane/8.

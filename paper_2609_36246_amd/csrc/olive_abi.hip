@@ -370,7 +370,6 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
             g.ldc = dv ? V : ds;
             g.alpha = a.sS;
             g.accumulate = c0 > 0;
-            g.m_fast = false;
             s = check_hip(launch_gemm(g, grid, st));
             if (s) return s;
         }
@@ -392,7 +391,6 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
             g.trans_out = true;
             g.alpha = a.sS;
             g.accumulate = false;
-            g.m_fast = true;
             // d_S / 256 x rows / 128 tiles rarely fill the grid: halve K over two units
             // (the rows of dL/dh were zero-filled above)
             g.ksplit = 2;

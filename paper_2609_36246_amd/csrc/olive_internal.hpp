@@ -152,7 +152,6 @@ struct GemmArgs {
     float alpha;
     bool trans_out;              // C[n][m] instead of C[m][n]
     bool accumulate;             // C += instead of C =
-    bool m_fast;                 // tile order: M index fastest
     int ksplit;                  // 1, or 2: halves of K added into C with atomics
 };
 
