@@ -26,8 +26,12 @@ namespace {
 struct GLane {
     int lane, wid, wv, wt, h, l32;
     int ldsoff[4];
-    const char *ap[W_DMA];   // A row chunk of each of the wave's 8 A DMAs
-    const char *bp[H_DMA];   // B row chunk of each of its 4 B DMAs
+    // the tile's first A and B rows (wave-uniform) and, per DMA, the lane's row chunk
+    // as a 32-bit offset from them: the K offset is added to the bases in scalar
+    // registers, the lane part inside the load
+    const char *abase, *bbase;
+    uint32_t aoff[W_DMA];    // 8 A DMAs
+    uint32_t boff[H_DMA];    // 4 B DMAs
 };
 
 struct GFrag {
@@ -39,9 +43,9 @@ struct GFrag {
 template <int Q>
 __device__ __forceinline__ void g_dma(const GLane &L, uint32_t la, uint32_t lb, int off) {
     if constexpr (Q < W_DMA)
-        dma16_at<Q * 1024>(L.ap[Q] + off, la);
+        dma16_sv<Q * 1024>(L.abase + off, L.aoff[Q], la);
     else
-        dma16_at<(Q - W_DMA) * 1024>(L.bp[Q - W_DMA] + off, lb);
+        dma16_sv<(Q - W_DMA) * 1024>(L.bbase + off, L.boff[Q - W_DMA], lb);
 }
 
 template <int QB, int QE>
@@ -210,20 +214,23 @@ gemm_mfma_kernel(GemmArgs g) {
         tile_of(q, tm, tn, mi, ni);
         const int m0 = mi * BV, n0 = ni * BT;
         // A DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7
-        // with chunk (lane&7) ^ swz(R); B DMA i rows R = wid*32 + 8i + lane/8.
+        // with chunk (lane&7) ^ swz(R); B DMA i rows R = wid*32 + 8i + lane/8. Rows
+        // past M (N) read the last one; offsets stay below 256 row pitches.
+        L.abase = g.A + (int64_t)m0 * g.lda;
+        L.bbase = g.B + (int64_t)n0 * g.ldb;
 #pragma unroll
         for (int i = 0; i < W_DMA; ++i) {
             const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
             const int ch = (L.lane & 7) ^ swz(R);
-            const int r = m0 + R < M ? m0 + R : M - 1;
-            L.ap[i] = g.A + (int64_t)r * g.lda + ch * 16;
+            const int r = m0 + R < M ? R : M - 1 - m0;
+            L.aoff[i] = (uint32_t)((int64_t)r * g.lda + ch * 16);
         }
 #pragma unroll
         for (int i = 0; i < H_DMA; ++i) {
             const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
             const int ch = (L.lane & 7) ^ swz(R);
-            const int r = n0 + R < N ? n0 + R : N - 1;
-            L.bp[i] = g.B + (int64_t)r * g.ldb + ch * 16;
+            const int r = n0 + R < N ? R : N - 1 - n0;
+            L.boff[i] = (uint32_t)((int64_t)r * g.ldb + ch * 16);
         }
         floatx16 acc[4][2];
 #pragma unroll
@@ -304,6 +311,9 @@ gemm_mfma_kernel(GemmArgs g) {
 
 hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st) {
     if (grid <= 0 || g.M <= 0) return hipSuccess;
+    // lane offsets within a tile are 32-bit: 256 rows of either operand
+    if (g.lda <= 0 || g.ldb <= 0 || g.lda >= ((int64_t)1 << 24) || g.ldb >= ((int64_t)1 << 24))
+        return hipErrorInvalidValue;
     gemm_mfma_kernel<<<grid, 256, 0, st>>>(g);
     return hipGetLastError();
 }
