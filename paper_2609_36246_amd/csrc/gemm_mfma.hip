@@ -6,8 +6,9 @@
 // owns a 256 x 128 output tile, K advances 64 elements per step, each step's A tile
 // (256 rows x 128 B) and B tile (128 rows x 128 B) land in a 3-stage LDS ring through
 // global->LDS DMAs issued two steps ahead, and v_mfma_f32_32x32x16_bf16 accumulates
-// 128 x 64 per wavefront in AGPRs. Here every lane holds its own row pointers for
-// both operands, so ragged M and N read clamped rows (whose results are dropped).
+// 128 x 64 per wavefront in AGPRs. Here every lane holds its own row offsets (from the
+// tile's first rows) for both operands, so ragged M and N read clamped rows (whose
+// results are dropped).
 //
 // N and K may be read on the device (the scored-row count of a call is known only
 // there); the grid is persistent and every workgroup derives the tile count itself.
