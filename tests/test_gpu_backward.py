@@ -300,6 +300,41 @@ def test_backward_reuses_forward_normalisers(mode):
     L.olive_score_free(ctx)
 
 
+def test_backward_reuse_after_a_region_only_span_forward():
+    """OLIVE_GRAD_REUSE_FORWARD after a region-only forward call with span masks, weights
+    in the [V][d] layout: the region-only compaction gives the scored rows the indices the
+    backward uses."""
+    say("backward reusing a region-only span forward, [V][d] weights")
+    wl = custom("turns", num_seqs=3, vocab=1000, d_student=128, d_teacher=256,
+                target_source="teacher", turns=(4, 16, 3, 2, 4, 24, 4, 40))
+    spec = wl["spec"]
+    T = wl["total_positions"]
+    B = wl["cu_seqlens"].shape[0] - 1
+    dev = wl["h_student"].device
+    desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher, L.OLIVE_BF16, L.OLIVE_W_VD,
+                       wl["scale_student"], wl["scale_teacher"], max_positions=T,
+                       max_seqs=B, flags=L.OLIVE_FLAG_BACKWARD)
+    ctx = L.olive_score_init(desc, wl["w_student"].t().contiguous(),
+                             wl["w_teacher"].t().contiguous())
+    batch = L.make_batch(wl["cu_seqlens"], None, wl["targets"], wl["h_student"],
+                         wl["h_teacher"], wl["valid_len"], L.OLIVE_REGION_SPANS)
+    sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
+    kl = torch.empty(T, dtype=torch.float32, device=dev)
+    L.olive_score_batch_spans(ctx, batch, sp,
+                              L.make_outputs(kl=kl, flags=L.OLIVE_OUT_REGION_ONLY))
+    gh = torch.full((T, spec.d_student), float("nan"), dtype=torch.float32, device=dev)
+    gw = torch.full((spec.vocab * spec.d_student,), float("nan"), dtype=torch.float32,
+                    device=dev)
+    g = L.make_grad_outputs(1.0, 0.25, gh, gw, reuse_forward=True)
+    L.olive_score_backward(ctx, batch, g, spans=sp)
+    torch.cuda.synchronize()
+    assert L.olive_score_last_error(ctx) == 0
+    L.olive_score_free(ctx)
+    hip = {"h": to_np(gh), "w": to_np(gw).reshape(spec.vocab, spec.d_student).T}
+    ref = oracle_backward(wl, 1.0, 0.25, O.REGION_SPANS)
+    check_grads(hip, ref, wl, "reuse-spans-vd")
+
+
 def test_backward_argument_errors():
     say("backward argument errors")
     wl = custom("narrow_k", **CASES["narrow_k"])
