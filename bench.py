@@ -108,7 +108,7 @@ def main():
         print(json.dumps({"copy_bytes": n * 4, "copies": 3}), flush=True)
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
               "(--gpus %d requested)" % args.gpus, file=sys.stderr)
         sys.exit(2)
     if not 1 <= args.steps <= 64:
