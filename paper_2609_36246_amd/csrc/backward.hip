@@ -1,5 +1,6 @@
 // Data movement of the backward pass: the scored hidden rows of a chunk gathered
-// and transposed into the K-contiguous operand of the dL/dW product, and a zero fill.
+// and transposed into the K-contiguous operand of the dL/dW product, the student's
+// weights transposed into K-blocked panels for the dL/dh product, and a zero fill.
 #include <hip/hip_runtime.h>
 
 #include "olive_internal.hpp"
@@ -51,6 +52,33 @@ __global__ void __launch_bounds__(256) fill_zero_kernel(float4 *__restrict__ p, 
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4;
          i += (int64_t)gridDim.x * 256)
         p[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// out[p][k][j] = W[64 p + j][k] (0 for rows past V): W^T [d][V] cut into panels of 64
+// vocabulary columns, [vp/64][d][64], so that one K step of the dL/dh product reads 256
+// contiguous 128-byte rows. One 64 (rows) x 64 (k) tile per workgroup through LDS.
+__global__ void __launch_bounds__(256)
+panel_t_kernel(const uint16_t *__restrict__ w, int64_t V, int d, uint16_t *__restrict__ out) {
+    __shared__ uint16_t tile[64][64 + 2];
+    const int64_t v0 = (int64_t)blockIdx.x * 64;
+    const int k0 = blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int r = ty; r < 64; r += 4) {
+        const int64_t v = v0 + r;
+        tile[r][tx] = v < V ? w[v * d + k0 + tx] : (uint16_t)0;
+    }
+    __syncthreads();
+    for (int r = ty; r < 64; r += 4)
+        out[((int64_t)blockIdx.x * d + k0 + r) * 64 + tx] = tile[tx][r];
+}
+
+hipError_t launch_panel_t(const void *w, int64_t V, int d, int64_t vp, void *out,
+                          hipStream_t st) {
+    // d and vp are multiples of 64 (the MFMA path's widths, the padded vocabulary)
+    if (d % 64 != 0 || vp % 64 != 0 || vp < V) return hipErrorInvalidValue;
+    dim3 grid((unsigned)(vp / 64), (unsigned)(d / 64));
+    panel_t_kernel<<<grid, 256, 0, st>>>((const uint16_t *)w, V, d, (uint16_t *)out);
+    return hipGetLastError();
 }
 
 hipError_t launch_gather_t(const void *h, int d, const uint32_t *rowmap, const Sched *sched,

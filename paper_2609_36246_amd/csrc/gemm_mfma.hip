@@ -31,6 +31,7 @@ struct GLane {
     // as a 32-bit offset from them: the K offset is added to the bases in scalar
     // registers, the lane part inside the load
     const char *abase, *bbase;
+    int64_t ak, bk;          // bytes from one K step of 64 elements to the next
     uint32_t aoff[W_DMA];    // 8 A DMAs
     uint32_t boff[H_DMA];    // 4 B DMAs
 };
@@ -39,21 +40,21 @@ struct GFrag {
     bf16x8 A[4], B[2];
 };
 
-// DMA q of a step (q < 8: A rows 8q .. 8q+7 of the wave's slice; else B DMA q-8) at K
-// byte offset off into the stage whose wave parts start at la (A) and lb (B).
+// DMA q of K step kk (q < 8: A rows 8q .. 8q+7 of the wave's slice; else B DMA q-8)
+// into the stage whose wave parts start at la (A) and lb (B).
 template <int Q>
-__device__ __forceinline__ void g_dma(const GLane &L, uint32_t la, uint32_t lb, int off) {
+__device__ __forceinline__ void g_dma(const GLane &L, uint32_t la, uint32_t lb, int kk) {
     if constexpr (Q < W_DMA)
-        dma16_sv<Q * 1024>(L.abase + off, L.aoff[Q], la);
+        dma16_sv<Q * 1024>(L.abase + kk * L.ak, L.aoff[Q], la);
     else
-        dma16_sv<(Q - W_DMA) * 1024>(L.bbase + off, L.boff[Q - W_DMA], lb);
+        dma16_sv<(Q - W_DMA) * 1024>(L.bbase + kk * L.bk, L.boff[Q - W_DMA], lb);
 }
 
 template <int QB, int QE>
-__device__ __forceinline__ void g_dmas(const GLane &L, uint32_t la, uint32_t lb, int off) {
+__device__ __forceinline__ void g_dmas(const GLane &L, uint32_t la, uint32_t lb, int kk) {
     if constexpr (QB < QE) {
-        g_dma<QB>(L, la, lb, off);
-        g_dmas<QB + 1, QE>(L, la, lb, off);
+        g_dma<QB>(L, la, lb, kk);
+        g_dmas<QB + 1, QE>(L, la, lb, kk);
     }
 }
 
@@ -61,7 +62,7 @@ __device__ __forceinline__ void g_issue(const GLane &L, int st, int kk) {
     const uint32_t base = ring_addr() + (uint32_t)st * STAGE_BYTES;
     const uint32_t la = base + (uint32_t)L.wid * (W_DMA * 1024u);
     const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
-    g_dmas<0, DMA_PER_STEP>(L, la, lb, kk * ROWB);
+    g_dmas<0, DMA_PER_STEP>(L, la, lb, kk);
 }
 
 template <int SUB>
@@ -91,13 +92,13 @@ __device__ __forceinline__ void g_mma(const GFrag &F, floatx16 (&acc)[4][2]) {
 // interleaved (4 of the step's 12).
 template <int Q0>
 __device__ __forceinline__ void g_mma_issue(const GFrag &F, floatx16 (&acc)[4][2],
-                                            const GLane &L, uint32_t la, uint32_t lb, int off) {
+                                            const GLane &L, uint32_t la, uint32_t lb, int kk) {
 #define OLIVE_GMI(J_)                                                                     \
     __builtin_amdgcn_sched_barrier(0);                                                    \
     acc[(J_) >> 1][(J_) & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                   \
         F.A[(J_) >> 1], F.B[(J_) & 1], acc[(J_) >> 1][(J_) & 1], 0, 0, 0);                \
     __builtin_amdgcn_sched_barrier(0);                                                    \
-    if constexpr (((J_) & 1) == 1) g_dma<Q0 + ((J_) >> 1)>(L, la, lb, off);
+    if constexpr (((J_) & 1) == 1) g_dma<Q0 + ((J_) >> 1)>(L, la, lb, kk);
     OLIVE_GMI(0)
     OLIVE_GMI(1)
     OLIVE_GMI(2)
@@ -129,7 +130,7 @@ __device__ __forceinline__ void g_step(const GLane &L, int st, int pk, floatx16 
     const uint32_t base = ring_addr() + (uint32_t)pv * STAGE_BYTES;
     const uint32_t la = base + (uint32_t)L.wid * (W_DMA * 1024u);
     const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
-    const int off = pk * ROWB;
+    const int off = pk;   // K step of the refill
     GFrag F0, F1, F2;
     g_read<0>(L, st, F0);
     __builtin_amdgcn_sched_barrier(0);
@@ -219,6 +220,8 @@ gemm_mfma_kernel(GemmArgs g) {
         // past M (N) read the last one; offsets stay below 256 row pitches.
         L.abase = g.A + (int64_t)m0 * g.lda;
         L.bbase = g.B + (int64_t)n0 * g.ldb;
+        L.ak = g.akstep;
+        L.bk = g.bkstep;
 #pragma unroll
         for (int i = 0; i < W_DMA; ++i) {
             const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
@@ -315,6 +318,7 @@ hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st) {
     // lane offsets within a tile are 32-bit: 256 rows of either operand
     if (g.lda <= 0 || g.ldb <= 0 || g.lda >= ((int64_t)1 << 24) || g.ldb >= ((int64_t)1 << 24))
         return hipErrorInvalidValue;
+    if (g.akstep <= 0 || g.bkstep <= 0) return hipErrorInvalidValue;
     gemm_mfma_kernel<<<grid, 256, 0, st>>>(g);
     return hipGetLastError();
 }

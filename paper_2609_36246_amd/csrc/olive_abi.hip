@@ -39,8 +39,8 @@ struct olive_score_ctx {
     int bw_chunk = 0;                           // scored rows per logit-gradient chunk
     int64_t bw_vp = 0;                          // V rounded up to 64
     float *bw_lse = nullptr;                    // [P][2]
-    uint16_t *bw_wt = nullptr;                  // W_S^T [d_S][bw_vp] bf16 (zero padded)
-    uint16_t *bw_dzt = nullptr;                 // [chunk][bw_vp]
+    uint16_t *bw_wt = nullptr;                  // W_S^T panels [bw_vp/64][d_S][64] bf16
+    uint16_t *bw_dzt = nullptr;                 // panels [bw_vp/64][chunk][64]
     uint16_t *bw_dzv = nullptr;                 // [V][chunk]
     uint16_t *bw_hrt = nullptr;                 // [d_S][chunk]
     // Normalisers of the last forward call on the MFMA path and the batch they belong
@@ -104,24 +104,15 @@ olive_status check_hip(hipError_t e) { return e == hipSuccess ? OLIVE_OK : OLIVE
 
 constexpr int64_t kBackwardChunk = 8192;   // scored rows per logit-gradient chunk
 
-// W_S^T [d_S][V] with rows padded to bw_vp (zeros), from the [V][d_S] weights the
-// kernels use; the padded columns of the [chunk][bw_vp] gradient buffer are zeroed
-// once (no pass writes them).
+// W_S^T in K-blocked panels [bw_vp/64][d_S][64] (zeros past V), from the [V][d_S]
+// weights the kernels use; the gradient panels' columns past V are zeroed once (no
+// pass writes them).
 olive_status backward_init(olive_score_ctx *c, hipStream_t st) {
     const int64_t V = c->desc.vocab, ds = c->desc.d_student;
-    void *tmp = nullptr;
-    olive_status s = dev_alloc(&tmp, (size_t)ds * V * 2);
-    if (s) return s;
-    // repack reads [rows][cols] and writes [cols][rows]: the [V][d_S] weights as rows
-    bool ok = launch_repack(c->ws, tmp, V, ds, 2, st) == hipSuccess &&
-              hipMemsetAsync(c->bw_wt, 0, (size_t)ds * c->bw_vp * 2, st) == hipSuccess &&
-              hipMemcpy2DAsync(c->bw_wt, (size_t)c->bw_vp * 2, tmp, (size_t)V * 2,
-                               (size_t)V * 2, (size_t)ds, hipMemcpyDeviceToDevice,
-                               st) == hipSuccess &&
+    bool ok = launch_panel_t(c->ws, V, (int)ds, c->bw_vp, c->bw_wt, st) == hipSuccess &&
               hipMemsetAsync(c->bw_dzt, 0, (size_t)c->bw_chunk * c->bw_vp * 2, st) ==
                   hipSuccess &&
               hipStreamSynchronize(st) == hipSuccess;
-    (void)hipFree(tmp);
     return ok ? OLIVE_OK : OLIVE_E_HIP;
 }
 
@@ -357,8 +348,10 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
             GemmArgs g = {};
             g.A = (const char *)ctx->bw_dzv;        // [V][chunk]: rows v, K = scored rows
             g.lda = (int64_t)ch * 2;
+            g.akstep = 128;
             g.B = (const char *)ctx->bw_hrt;        // [d_S][chunk]
             g.ldb = (int64_t)ch * 2;
+            g.bkstep = 128;
             g.M = (int)V;
             g.N = ds;
             g.k_dev = &ctx->sched->t_valid;
@@ -375,10 +368,13 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         }
         if (go->grad_h_student) {
             GemmArgs g = {};
-            g.A = (const char *)ctx->bw_wt;         // W_S^T [d_S][vp]: rows k, K = vocabulary
-            g.lda = ctx->bw_vp * 2;
-            g.B = (const char *)ctx->bw_dzt;        // [chunk][vp]
-            g.ldb = ctx->bw_vp * 2;
+            // K-blocked panels: one K step of either operand is a contiguous block
+            g.A = (const char *)ctx->bw_wt;         // W_S^T [vp/64][d_S][64]: rows k, K = v
+            g.lda = 128;
+            g.akstep = (int64_t)ds * 128;
+            g.B = (const char *)ctx->bw_dzt;        // [vp/64][chunk][64]
+            g.ldb = 128;
+            g.bkstep = (int64_t)ch * 128;
             g.M = ds;
             g.K = (int)ctx->bw_vp;
             g.n_dev = &ctx->sched->t_valid;

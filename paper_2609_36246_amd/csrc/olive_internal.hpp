@@ -125,21 +125,25 @@ struct ScoreArgs {
 struct DzArgs {
     int c0, chunk;               // first compacted scored row, rows per chunk
     int pitch;                   // dz_v row pitch in elements (>= chunk rounded up to 64)
-    int64_t vp;                  // dz_t row pitch: V rounded up to 64
+    int64_t vp;                  // V rounded up to 64
     const float *lse;            // [rows][2] forward log-normalisers per compacted row
     const int32_t *targets;      // packed realised tokens
     float w_ce, w_kl;            // loss weights
-    uint16_t *dz_t;              // [chunk][vp] bf16 logit gradient
+    uint16_t *dz_t;              // [vp/64][chunk][64] bf16 logit gradient (K-blocked panels)
     uint16_t *dz_v;              // [V][pitch] the same, transposed
 };
 
-// C (+)= alpha * A * B^T on bf16 rows (K contiguous), fp32 C. N and K are read on the
-// device when their pointers are set: clamp(*p - off, 0, cap).
+// C (+)= alpha * A * B^T on bf16 rows, fp32 C. Each operand is read in K steps of 64
+// elements: step kk of row r at base + kk * kstep + r * ld (row-major: kstep = 128,
+// ld = the row pitch; K-blocked panels [K/64][rows][64]: ld = 128, kstep = rows * 128).
+// N and K are read on the device when their pointers are set: clamp(*p - off, 0, cap).
 struct GemmArgs {
     const char *A;
     int64_t lda;                 // bytes between A rows
+    int64_t akstep;              // bytes between A's K steps
     const char *B;
     int64_t ldb;
+    int64_t bkstep;
     int M, N, K;
     const int32_t *n_dev;
     int n_off, n_cap;
@@ -175,6 +179,8 @@ hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bo
 hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,
                            hipStream_t st);
 hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st);
+hipError_t launch_panel_t(const void *w, int64_t V, int d, int64_t vp, void *out,
+                          hipStream_t st);
 hipError_t launch_gather_t(const void *h, int d, const uint32_t *rowmap, const Sched *sched,
                            int c0, int chunk, int pitch, uint16_t *out, hipStream_t st);
 hipError_t launch_fill(float *p, int64_t n, hipStream_t st);

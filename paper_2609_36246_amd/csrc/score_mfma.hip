@@ -748,12 +748,18 @@ struct Kernel {
         }
     }
 
+    // Element (t, v) of the K-blocked dz_t panels [vp/64][chunk][64].
+    static __device__ __forceinline__ int64_t dzt_at(const DzArgs &z, int t, int v) {
+        return ((int64_t)(v >> 6) * z.chunk + t) * 64 + (v & 63);
+    }
+
     // Logit-gradient pass of the backward: the same units and steps over the scored
     // rows [c0, c0 + chunk) of the call (compacted, region only), with the fold
     // replaced by g = (w_ce + w_kl) p_S - w_ce onehot(y) - w_kl p_T, p_X = exp(s_X z_X -
     // lse_X) with the forward pass's normalisers, stored as bf16 (round to nearest
-    // even) into dz_t [row][v] and dz_v [v][row]. dz_v columns from the chunk's row
-    // count up to its pitch are written as zeros (the K padding of the dW product).
+    // even) into dz_t (K-blocked panels [v/64][row][64]) and dz_v [v][row]. dz_v
+    // columns from the chunk's row count up to its pitch are written as zeros (the K
+    // padding of the dW product).
     static __device__ __forceinline__ void run_dz(ScoreArgs a, DzArgs z) {
         const int t_all = a.sched->t_valid - z.c0;
         const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
@@ -867,9 +873,9 @@ struct Kernel {
                                     w[2 * k].x, w[2 * k + 1].x, false, false);
                                 const auto Y = __builtin_amdgcn_permlane32_swap(
                                     w[2 * k].y, w[2 * k + 1].y, false, false);
+                                const int v = vw0 + vb * 32 + 16 * k + 8 * L.h;
                                 if (ok[cb])
-                                    *(uint4 *)(z.dz_t + (int64_t)tcol[cb] * z.vp + vw0 + vb * 32 +
-                                               16 * k + 8 * L.h) =
+                                    *(uint4 *)(z.dz_t + dzt_at(z, tcol[cb], v)) =
                                         make_uint4(X[0], Y[0], X[1], Y[1]);
                             }
                             const int cc = cb * 32 + L.l32;   // column in the wave's 64
@@ -916,7 +922,7 @@ struct Kernel {
                             for (int e = 0; e < 4; ++e) {
                                 if (v0 + e < vlo) continue;
                                 if (t < z.pitch) z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = q[e];
-                                if (ok[cb]) z.dz_t[(int64_t)t * z.vp + v0 + e] = q[e];
+                                if (ok[cb]) z.dz_t[dzt_at(z, t, v0 + e)] = q[e];
                             }
                         }
                     }
