@@ -51,7 +51,10 @@ def cpu_baseline(wl, seconds: float):
         ht = np32(wl["h_teacher"][idx]).astype(np.float64)
         y = wl["targets"][idx].cpu().numpy()
         t0 = time.perf_counter()
-        O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"])
+        # what the timed call forms: both models' log-normalisers, log-probs and greedy
+        # tokens, and the forward KL (no reverse KL or top-K sets)
+        O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"],
+                     extras=False)
         return time.perf_counter() - t0
     # Rows in chunks until the timed oracle work reaches `seconds` (only the oracle
     # calls are timed; gathering the rows is not).
@@ -62,9 +65,32 @@ def cpu_baseline(wl, seconds: float):
         n += len(rows)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [os.cpu_count()])
     return dict(value=n / t, unit="positions/s", cores=int(threads), kind="oracle",
+                cpu_model=cpu_model(),
                 sample="%d random valid rows of the workload (seed 12345), fp64 numpy oracle "
-                       "row_scores (both models + KL), weights converted to float64 before "
-                       "the timed region; %.1f s" % (n, t))
+                       "row_scores without its reverse-KL and top-K extras (both models' "
+                       "log-normalisers, log-probs and greedy tokens, forward KL: what the "
+                       "timed GPU call forms), weights converted to float64 before the timed "
+                       "region; %.1f s" % (n, t))
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.lower().startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def main():

@@ -246,9 +246,9 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
 
 /*
  * Gradient outputs of olive_score_backward. L = w_ce * sum_b CE_b (Eq. 1's loss, summed
- * over the sequences) + w_kl * sum over the region's positions of KL(p_T || p_S), the
- * loss of the student's training step after its masked CE (Sec. 3.1; the optimisation
- * of Sec. 3.3). Device buffers, caller-owned, overwritten.
+ * over the sequences) + w_kl * sum over the region's positions of KL(p_T || p_S): the
+ * student's update step on the masked CE loss (the update of Alg. 1, Eq. 1, Sec. 3.1),
+ * with an optional distillation term. Device buffers, caller-owned, overwritten.
  */
 typedef struct {
     int32_t size;                /* host: sizeof(olive_grad_outputs) (checked) */
@@ -314,7 +314,9 @@ olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
 /*
  * Diagnostics of the last scoring call (synchronises the device).
  *   out host [6] int64: [0] vocabulary splits used, [1] rows whose greedy token was
- *   re-decided in fp64 because its top-2 logit gap was within the fp32 error window,
+ *   re-decided from exact logits (bf16 products summed in fp64) because the gap between
+ *   their two largest fp32 logits was at most 2^-14 max(1, |s max|); every such row of
+ *   the call is re-decided (the list holds max_positions rows),
  *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched,
  *   [4] (position, model) pairs whose top-K set needed a filter pass over the
  *   vocabulary, [5] pairs of those that needed an exhaustive exact scan (more than

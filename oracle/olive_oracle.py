@@ -27,8 +27,8 @@ What it computes (for every packed position of a batch of stitched rollouts):
   * the gradient of L = w_ce * sum_b CE_b + w_kl * sum_t KL(p_T || p_S)[t] (Eq. 1's
     loss, and the distillation divergence, over the in-region positions) with respect
     to the student's hidden states and LM-head weight, for the backward pass the
-    student's training step needs after its masked CE (Sec. 3.1; the optimisation of
-    Sec. 3.3): per in-region position, dL/dz_S = w_ce (p_S - onehot(y)) +
+    student's update step on the masked CE loss needs (the update of Alg. 1 with
+    Eq. 1, Sec. 3.1): per in-region position, dL/dz_S = w_ce (p_S - onehot(y)) +
     w_kl (p_S - p_T) for the scaled logits z_S, then dh = s_S W dL/dz_S and
     dW = s_S sum_t h_t (dL/dz_S)_t^T;
   * masks: a position is valid when it precedes the sequence's valid length, and
@@ -194,7 +194,7 @@ def kl_topk(z_t, lse_t: float, z_s, lse_s: float, set_t) -> float:
 
 def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1.0,
                h_teacher_rows=None, w_teacher=None, scale_teacher: float = 1.0,
-               chunk: Optional[int] = None) -> dict:
+               chunk: Optional[int] = None, extras: bool = True) -> dict:
     """Unmasked per-row quantities for a set of rows (every row treated as valid).
 
     Returns float64 / int64 arrays of length n: z_y_s, lse_s, logp_s, argmax_s,
@@ -202,6 +202,10 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     kl_nonneg (KL(teacher || student)), kl_rev and kl_rev_nonneg (KL(student ||
     teacher)), overlap and kl_topk (top-K statistics, K = TOPK) and the top-K index
     sets topk_s / topk_t ([n, TOPK]).
+
+    extras=False leaves out the reverse KL and the top-K statistics (their keys are
+    then absent); every value that is returned is computed exactly as with
+    extras=True.
     """
     hs = _f64(h_student_rows)
     n = hs.shape[0]
@@ -218,11 +222,13 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     out = {k: np.zeros(n) for k in ("z_y_s", "lse_s", "logp_s", "gap_s", "max_s")}
     out["argmax_s"] = np.zeros(n, dtype=np.int64)
     if has_t:
-        for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg", "kl_rev",
-                  "kl_rev_nonneg", "overlap", "kl_topk"):
+        for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg"):
             out[k] = np.zeros(n)
-        out["topk_s"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
-        out["topk_t"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
+        if extras:
+            for k in ("kl_rev", "kl_rev_nonneg", "overlap", "kl_topk"):
+                out[k] = np.zeros(n)
+            out["topk_s"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
+            out["topk_t"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
         out["argmax_t"] = np.zeros(n, dtype=np.int64)
     for r0 in range(0, n, chunk):
         r1 = min(n, r0 + chunk)
@@ -248,6 +254,8 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
                 kl, klp = kl_teacher_student(zt[i], tt["lse"], zs[i], st["lse"])
                 out["kl"][g] = kl
                 out["kl_nonneg"][g] = klp
+                if not extras:
+                    continue
                 klr, klrp = kl_student_teacher(zs[i], st["lse"], zt[i], tt["lse"])
                 out["kl_rev"][g] = klr
                 out["kl_rev_nonneg"][g] = klrp

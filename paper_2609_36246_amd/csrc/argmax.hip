@@ -23,15 +23,8 @@ namespace olive {
 // candidates from the splits that hold at most one, and mark the other splits for the
 // filter. Rows whose hidden state is zero need nothing: every logit is exactly 0 and
 // the scoring pass already took index 0.
-__global__ void __launch_bounds__(256)
-fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
-                FilterQueue q) {
-    const int lane = threadIdx.x & 63;
-    const int f = blockIdx.x * 4 + (threadIdx.x >> 6);
-    const int nf_all = a.sched->n_flagged;
-    const int nf = nf_all < flag_cap ? nf_all : flag_cap;
-    if (f >= nf) return;
-    const int ns = a.sched->n_splits;
+__device__ __forceinline__ void queue_row(const ScoreArgs &a, const int32_t *__restrict__ flagged,
+                                          int f, int ns, int lane, const FilterQueue &q) {
     const int32_t j = flagged[4 * f];
     const int fl = flagged[4 * f + 1];
     const int64_t g = a.rowmap[j] & 0x7fffffffu;
@@ -70,6 +63,17 @@ fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
             if (scan_mask) atomicOr(&q.smask[m], (uint32_t)scan_mask);
         }
     }
+}
+
+__global__ void __launch_bounds__(256)
+fx_queue_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int flag_cap,
+                FilterQueue q) {
+    const int lane = threadIdx.x & 63;
+    const int nf_all = a.sched->n_flagged;
+    const int nf = nf_all < flag_cap ? nf_all : flag_cap;
+    const int ns = a.sched->n_splits;
+    for (int f = blockIdx.x * 4 + (threadIdx.x >> 6); f < nf; f += gridDim.x * 4)
+        queue_row(a, flagged, f, ns, lane, q);
 }
 
 // One wavefront per queued pair: the exact maximum of its candidates (one per lane).
@@ -137,7 +141,9 @@ hipError_t launch_argmax_fix(const ScoreArgs &a, const int32_t *flagged, int fla
                              const FilterQueue &q, int32_t *am_s, int32_t *am_t,
                              hipStream_t st) {
     if (flag_cap <= 0) return hipSuccess;
-    fx_queue_kernel<<<(unsigned)((flag_cap + 3) / 4), 256, 0, st>>>(a, flagged, flag_cap, q);
+    // a fixed grid that strides over the flagged rows (their count is on the device)
+    const int blocks = (flag_cap + 3) / 4 < 1024 ? (flag_cap + 3) / 4 : 1024;
+    fx_queue_kernel<<<blocks, 256, 0, st>>>(a, flagged, flag_cap, q);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     e = launch_filter(a, q, st);

@@ -16,8 +16,13 @@
 
 namespace olive {
 
-// Relative top-2 gap (in scaled logits) below which the greedy token is re-decided.
-constexpr float kTieWindow = 1.0f / 65536.0f;
+// Relative top-2 gap (in scaled logits) at or below which the greedy token is
+// re-decided exactly: 2^-14 max(1, |s M|). The fp32 logits of the MFMA pass differ
+// from the exact ones by rounding of the fp32 accumulation only (bf16 products are
+// exact in fp32); at the widths and magnitudes of the workloads (|z| up to ~20,
+// d up to 5120) that difference stays below ~1e-5, so rows whose top two are more
+// than the window apart are decided correctly by the fp32 values.
+constexpr float kTieWindow = 1.0f / 16384.0f;
 
 template <typename E>
 __device__ __forceinline__ float wave_dot(const E *h, const E *w, int d, int lane);

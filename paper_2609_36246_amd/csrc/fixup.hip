@@ -17,6 +17,9 @@
 // batch's hidden rows are staged in LDS and every weight row of the chunk is read
 // once for all of them, so W streams from HBM once per batch rather than once per
 // flagged row. Per-chunk winners are merged per row in a fixed order (phase 2).
+// One launch pair covers a window of the flagged list (entries [f_base, f_base +
+// cap)); the host runs windows until they cover every row a call can flag, and a
+// window past the list's end exits at once.
 #include <hip/hip_runtime.h>
 
 #include "olive_device.hpp"
@@ -93,16 +96,18 @@ row_norm_kernel(const E *__restrict__ w, int64_t V, int d, float *__restrict__ o
 
 template <typename E, int FB>
 __global__ void __launch_bounds__(FX_THREADS)
-fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int n_chunks,
-                  const float *__restrict__ wn_s, const float *__restrict__ wn_t,
+fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int f_base, int cap,
+                  int n_chunks, const float *__restrict__ wn_s, const float *__restrict__ wn_t,
                   FxResult *__restrict__ out) {
     extern __shared__ __attribute__((aligned(16))) char fx_smem[];   // [FB][d] of E
     __shared__ float s_eb[FB], s_theta[FB];
     __shared__ double red_v[FX_GROUPS][FB];
     __shared__ int red_i[FX_GROUPS][FB];
     E *hrows = (E *)fx_smem;
-    const int nf_all = a.sched->n_flagged;
-    const int nf = nf_all < cap ? nf_all : cap;
+    // this window's flagged rows: entries [f_base, f_base + cap) of the list
+    const int nf_all = a.sched->n_flagged - f_base;
+    const int nf = nf_all < 0 ? 0 : (nf_all < cap ? nf_all : cap);
+    flagged += 4 * (int64_t)f_base;
     const int n_batches = (nf + FB - 1) / FB;
     const int64_t n_items = (int64_t)n_batches * n_chunks * 2;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g8 = lane & 7;
@@ -264,11 +269,12 @@ fixup_scan_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int
 }
 
 __global__ void __launch_bounds__(64)
-fixup_merge_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int cap, int n_chunks,
-                   const FxResult *__restrict__ res, int32_t *__restrict__ am_s,
+fixup_merge_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int f_base, int cap,
+                   int n_chunks, const FxResult *__restrict__ res, int32_t *__restrict__ am_s,
                    int32_t *__restrict__ am_t) {
-    const int nf_all = a.sched->n_flagged;
-    const int nf = nf_all < cap ? nf_all : cap;
+    const int nf_all = a.sched->n_flagged - f_base;
+    const int nf = nf_all < 0 ? 0 : (nf_all < cap ? nf_all : cap);
+    flagged += 4 * (int64_t)f_base;
     for (int f = blockIdx.x * 64 + threadIdx.x; f < nf; f += gridDim.x * 64) {
         const int32_t j = flagged[4 * f];
         const int32_t mask = flagged[4 * f + 1];
@@ -300,26 +306,28 @@ hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *o
 }
 
 template <typename E, int FB>
-static void launch_scan(const ScoreArgs &a, const int32_t *flagged, int cap, int n_chunks,
-                        size_t lds, const float *wn_s, const float *wn_t, FxResult *res,
-                        hipStream_t st) {
-    fixup_scan_kernel<E, FB><<<1024, FX_THREADS, lds, st>>>(a, flagged, cap, n_chunks, wn_s,
-                                                             wn_t, res);
+static void launch_scan(const ScoreArgs &a, const int32_t *flagged, int f_base, int cap,
+                        int n_chunks, size_t lds, const float *wn_s, const float *wn_t,
+                        FxResult *res, hipStream_t st) {
+    fixup_scan_kernel<E, FB><<<1024, FX_THREADS, lds, st>>>(a, flagged, f_base, cap, n_chunks,
+                                                             wn_s, wn_t, res);
 }
 
 template <typename E>
-static void launch_scan_fb(int fb, const ScoreArgs &a, const int32_t *flagged, int cap,
-                           int n_chunks, size_t lds, const float *wn_s, const float *wn_t,
-                           FxResult *res, hipStream_t st) {
-    if (fb >= 8) launch_scan<E, 8>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
-    else if (fb >= 4) launch_scan<E, 4>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
-    else if (fb >= 2) launch_scan<E, 2>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
-    else launch_scan<E, 1>(a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+static void launch_scan_fb(int fb, const ScoreArgs &a, const int32_t *flagged, int f_base,
+                           int cap, int n_chunks, size_t lds, const float *wn_s,
+                           const float *wn_t, FxResult *res, hipStream_t st) {
+#define OLIVE_SCAN(FB_) launch_scan<E, FB_>(a, flagged, f_base, cap, n_chunks, lds, wn_s, wn_t, res, st)
+    if (fb >= 8) OLIVE_SCAN(8);
+    else if (fb >= 4) OLIVE_SCAN(4);
+    else if (fb >= 2) OLIVE_SCAN(2);
+    else OLIVE_SCAN(1);
+#undef OLIVE_SCAN
 }
 
-hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
-                             void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
-                             int32_t *am_t, hipStream_t st) {
+hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int f_base,
+                             int cap, void *scratch, const float *wn_s, const float *wn_t,
+                             int32_t *am_s, int32_t *am_t, hipStream_t st) {
     const int n_chunks = (a.V + FX_CHUNK - 1) / FX_CHUNK;
     const int dmax = a.ds > a.dt ? a.ds : a.dt;
     const int esz = bf16 ? 2 : 4;
@@ -330,12 +338,12 @@ hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagg
     const size_t lds = (size_t)fb * dmax * esz;
     FxResult *res = (FxResult *)scratch;
     if (bf16)
-        launch_scan_fb<uint16_t>(fb, a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+        launch_scan_fb<uint16_t>(fb, a, flagged, f_base, cap, n_chunks, lds, wn_s, wn_t, res, st);
     else
-        launch_scan_fb<float>(fb, a, flagged, cap, n_chunks, lds, wn_s, wn_t, res, st);
+        launch_scan_fb<float>(fb, a, flagged, f_base, cap, n_chunks, lds, wn_s, wn_t, res, st);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    fixup_merge_kernel<<<64, 64, 0, st>>>(a, flagged, cap, n_chunks, res, am_s, am_t);
+    fixup_merge_kernel<<<64, 64, 0, st>>>(a, flagged, f_base, cap, n_chunks, res, am_s, am_t);
     return hipGetLastError();
 }
 

@@ -13,8 +13,9 @@
 // N and K may be read on the device (the scored-row count of a call is known only
 // there); the grid is persistent and every workgroup derives the tile count itself.
 // With ksplit = 2 each tile's K range is halved over two work units that add into C
-// with atomics: C must hold zeros (or the value to add to) beforehand, and the sum
-// is still deterministic, as two fp32 additions into the same start value commute.
+// with atomics. C must hold zeros beforehand: then the result is deterministic, since
+// 0 + a + b and 0 + b + a round to the same value (the first addition is exact). With
+// any other start value c the two orders (c + a) + b and (c + b) + a may differ.
 #include <hip/hip_runtime.h>
 
 #include "mfma_pipe.hpp"

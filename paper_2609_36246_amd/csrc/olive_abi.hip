@@ -25,7 +25,8 @@ struct olive_score_ctx {
     int64_t pstride = 0;
     float *logp_tmp = nullptr;
     int32_t *flagged = nullptr;
-    int flag_cap = 0;
+    int flag_cap = 0;                           // rows the near-tie list holds: max_positions
+    int fx_window = 0;                          // generic path: flagged rows per window
     void *fx_scratch = nullptr;
     float *wn_s = nullptr, *wn_t = nullptr;     // weight-row L2 norms (rounding bounds)
     float wmax_s = 0.f, wmax_t = 0.f;           // their maxima
@@ -61,7 +62,9 @@ struct olive_score_ctx {
 
 namespace {
 
-constexpr int kFixupCapRows = 8192;
+// Flagged rows the generic path's exact re-decision takes per window (its scratch holds
+// one window's per-chunk winners); the windows cover every row a call can flag.
+constexpr int kFixupWindowRows = 8192;
 
 void release(olive_score_ctx *c) {
     if (!c) return;
@@ -236,9 +239,11 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
             s = check_hip(launch_argmax_fix(a, flagged, ctx->flag_cap, ctx->fxq, am_s,
                                             has_t ? am_t : nullptr, st));
         else
-            s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, ctx->flag_cap,
-                                            ctx->fx_scratch, ctx->wn_s, ctx->wn_t, am_s,
-                                            has_t ? am_t : nullptr, st));
+            // windows over the flagged list: at most one entry per compacted row
+            for (int64_t f0 = 0; f0 < T && !s; f0 += ctx->fx_window)
+                s = check_hip(launch_fixup_impl(a, ctx->bf16, flagged, (int)f0, ctx->fx_window,
+                                                ctx->fx_scratch, ctx->wn_s, ctx->wn_t, am_s,
+                                                has_t ? am_t : nullptr, st));
         if (s) return s;
     }
     if (topk) {
@@ -327,7 +332,9 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         if (s) return s;
     }
     const int ch = ctx->bw_chunk;
-    for (int64_t c0 = 0; c0 < d.max_positions; c0 += ch) {
+    // scored rows <= T: chunks past the call's positions are never launched (those past
+    // the scored count, known only on the device, exit at once)
+    for (int64_t c0 = 0; c0 < T; c0 += ch) {
         DzArgs z;
         z.c0 = (int)c0;
         z.chunk = ch;
@@ -402,7 +409,12 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
 extern "C" {
 
 const char *olive_status_string(olive_status s) {
-    switch (s) {
+    // A C caller may pass any int: read the argument's bytes rather than the enum value
+    // (a value outside the enumerators is undefined as a C++ enum).
+    int32_t code;
+    static_assert(sizeof(code) == sizeof(s), "olive_status is passed as a 32-bit int");
+    std::memcpy(&code, &s, sizeof(code));
+    switch (code) {
         case OLIVE_OK: return "OLIVE_OK: success";
         case OLIVE_E_NULL: return "OLIVE_E_NULL: a required pointer is NULL";
         case OLIVE_E_SHAPE: return "OLIVE_E_SHAPE: a size is out of range for this context";
@@ -483,7 +495,9 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     }
     const int64_t P = d.max_positions;
     c->pstride = (P + 255) / 256 * 256;
-    c->flag_cap = (int)(P < kFixupCapRows ? P : kFixupCapRows);
+    // One near-tie entry per compacted row at most: the list never drops a flagged row.
+    c->flag_cap = (int)P;
+    c->fx_window = (int)(P < kFixupWindowRows ? P : kFixupWindowRows);
     if (!s) s = dev_alloc(&c->rowmap, (size_t)P * sizeof(uint32_t));
     if (!s) s = dev_alloc(&c->seqbuf, (size_t)seqbuf_entries(d.max_seqs) * sizeof(int32_t));
     if (!s) s = dev_alloc(&c->sched, sizeof(Sched));
@@ -518,7 +532,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
     if (!s)
         s = dev_alloc(&c->fx_scratch,
-                      (size_t)c->flag_cap * fixup_chunks(V) * 2 * fixup_result_bytes());
+                      (size_t)c->fx_window * fixup_chunks(V) * 2 * fixup_result_bytes());
     if (!s) s = dev_alloc(&c->err, sizeof(int32_t));
     if (!s) s = dev_alloc(&c->wn_s, (size_t)V * sizeof(float));
     if (!s && c->has_t) s = dev_alloc(&c->wn_t, (size_t)V * sizeof(float));

@@ -194,9 +194,9 @@ hipError_t launch_topk(const ScoreArgs &a, const TopkWork &w, const TopkOut &out
 hipError_t launch_argmax_fix(const ScoreArgs &a, const int32_t *flagged, int flag_cap,
                              const FilterQueue &q, int32_t *am_s, int32_t *am_t,
                              hipStream_t st);
-hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int cap,
-                             void *scratch, const float *wn_s, const float *wn_t, int32_t *am_s,
-                             int32_t *am_t, hipStream_t st);
+hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagged, int f_base,
+                             int cap, void *scratch, const float *wn_s, const float *wn_t,
+                             int32_t *am_s, int32_t *am_t, hipStream_t st);
 hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *out,
                             hipStream_t st);
 int fixup_chunks(int64_t V);

@@ -19,6 +19,7 @@ import torch
 
 from oracle import olive_oracle as O
 from paper_2609_36246_amd import _lib as L
+from tests import oracle_pool
 
 LOGP_ATOL = 2e-3
 KL_ATOL = 1e-3
@@ -125,8 +126,10 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
     return res
 
 
-def oracle_rows(wl, rows, student_only=False):
-    """fp64 oracle on a subset of packed rows (all rows treated as valid)."""
+def oracle_rows(wl, rows, student_only=False, extras=True):
+    """fp64 oracle on a subset of packed rows (all rows treated as valid). Large row
+    sets run in the worker pool of tests/oracle_pool.py (the same oracle function,
+    over chunks of rows). extras=False leaves out the reverse KL and top-K values."""
     rows = np.asarray(rows, dtype=np.int64)
     idx = torch.from_numpy(rows).to(wl["h_student"].device)
     hs = to_np(wl["h_student"][idx])
@@ -135,9 +138,19 @@ def oracle_rows(wl, rows, student_only=False):
     ws = to_np(wl["w_student"])
     wt = None if student_only else to_np(wl["w_teacher"])
     t0 = time.time()
-    r = O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"])
-    say("oracle on %d rows took %.1fs" % (len(rows), time.time() - t0))
+    if len(rows) >= POOL_MIN_ROWS:
+        r = oracle_pool.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"],
+                                   extras=extras, log=say)
+        how = "%d worker processes" % oracle_pool.workers()
+    else:
+        r = O.row_scores(hs, ws, y, wl["scale_student"], ht, wt, wl["scale_teacher"],
+                         extras=extras)
+        how = "one process"
+    say("oracle on %d rows took %.1fs (%s)" % (len(rows), time.time() - t0, how))
     return r
+
+
+POOL_MIN_ROWS = 64
 
 
 def structure_np(wl):
@@ -148,6 +161,39 @@ def structure_np(wl):
 def masks_of(wl, region):
     cu, cut, vl = structure_np(wl)
     return O.masks(cu, cut, vl, region, wl.get("spans") if region == O.REGION_SPANS else None)
+
+
+def parity_rows(wl, frac=0.01, n_whole=2, seed=1):
+    """The row sample of a workload too large for the oracle in full: every row of the
+    n_whole sequences with the fewest valid rows, the rows around every cut (cut-1,
+    cut, cut+1) and end of the valid prefix (valid_len-1, valid_len), the first and
+    last row of every sequence, every outlier row, and random valid rows until the
+    sample holds at least `frac` of the valid rows. Returns (rows, whole sequences)."""
+    cu, cut, vl = structure_np(wl)
+    B = len(cu) - 1
+    lengths = np.diff(cu)
+    vlen = lengths if vl is None else vl
+    whole = [int(b) for b in np.argsort(vlen, kind="stable")[:n_whole]]
+    picks = set()
+    for b in whole:
+        picks.update(range(int(cu[b]), int(cu[b] + vlen[b])))
+    base = stratified_rows(wl, n_random=0)
+    picks.update(int(x) for x in base)
+    valid = masks_of(wl, O.REGION_TEACHER)["valid"]
+    t_valid = int(valid.sum())
+    want = int(np.ceil(frac * t_valid))
+    rng = np.random.default_rng(seed)
+    have = sum(1 for r in picks if valid[r])
+    for x in rng.permutation(np.nonzero(valid)[0]):
+        if have >= want:
+            break
+        if int(x) not in picks:
+            picks.add(int(x))
+            have += 1
+    rows = np.array(sorted(picks), dtype=np.int64)
+    n_valid = int(valid[rows].sum())
+    assert n_valid >= want, (n_valid, want)
+    return rows, whole
 
 
 def stratified_rows(wl, n_random=128, seed=1):
@@ -171,16 +217,20 @@ def stratified_rows(wl, n_random=128, seed=1):
                     picks.add(int(cu[b] + t))
     rng = np.random.default_rng(seed)
     T = int(cu[-1])
-    picks.update(int(x) for x in rng.choice(T, size=min(n_random, T), replace=False))
+    if n_random > 0:
+        picks.update(int(x) for x in rng.choice(T, size=min(n_random, T), replace=False))
     return np.array(sorted(picks), dtype=np.int64)
 
 
 def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, check_ce=True,
-            label="", region_only=False):
+            label="", region_only=False, whole_seqs=None):
     """Compare HIP outputs with the oracle, element by element, at the acceptance bar.
 
     region_only: the call scored only the region; every output outside it must hold
-    the fixed values of unscored positions, and the region is compared as usual."""
+    the fixed values of unscored positions, and the region is compared as usual.
+    rows: the packed rows to compare (default all); whole_seqs: sequences every row of
+    which is among them, whose per-sequence loss is then compared too (every sequence
+    when rows is None)."""
     cu, cut, vl = structure_np(wl)
     m = masks_of(wl, region)
     T = len(m["valid"])
@@ -204,7 +254,7 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
                 (label, key)
     sel = np.arange(T) if rows is None else np.asarray(rows)
     sel = sel[valid[sel]]
-    r = oracle_rows(wl, sel, student_only)
+    r = oracle_rows(wl, sel, student_only, extras="kl_rev" in hip)
     worst = {}
 
     def chk(name, got, want, atol, rtol=0.0):
@@ -232,15 +282,23 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
         if "kl_rev" in hip:
             want = np.where(inr[sel], r["kl_rev"], 0.0)
             chk("kl_rev", hip["kl_rev"][sel], want, KL_ATOL, KL_RTOL)
-        if check_ce and "ce" in hip and rows is None:
+        if check_ce and "ce" in hip and (rows is None or whole_seqs):
             B = len(cu) - 1
-            for b in range(B):
+            seqs = range(B) if rows is None else whole_seqs
+            for b in seqs:
                 idx = np.nonzero((m["seq_id"] == b) & inr)[0]
-                want = -math.fsum(r["logp_s"][np.searchsorted(sel, idx)].tolist()) \
-                    if idx.size else 0.0
-                assert abs(hip["ce"][b] - want) <= CE_RTOL * abs(want) + 1e-3, (label, b)
-    say("%s parity ok on %d rows; worst %s" % (label, sel.size,
-                                                {k: "%.2e" % v for k, v in worst.items()}))
+                pos = np.searchsorted(sel, idx)
+                assert np.all(sel[np.minimum(pos, sel.size - 1)] == idx), \
+                    (label, "sequence %d is not whole in the sample" % b)
+                want = -math.fsum(r["logp_s"][pos].tolist()) if idx.size else 0.0
+                assert abs(hip["ce"][b] - want) <= CE_RTOL * abs(want) + 1e-3, \
+                    (label, b, hip["ce"][b], want)
+    n_valid = int(valid.sum())
+    say("%s parity ok on %d of %d valid rows (%.2f%%)%s; worst %s" % (
+        label, sel.size, n_valid, 100.0 * sel.size / max(1, n_valid),
+        "" if not whole_seqs else "; whole sequences %s (%d rows, CE compared)" % (
+            list(whole_seqs), int(np.isin(m["seq_id"][sel], whole_seqs).sum())),
+        {k: "%.2e" % v for k, v in worst.items()}))
     return r
 
 

@@ -1,0 +1,62 @@
+"""The C ABI's host-side argument checks under AddressSanitizer and
+UndefinedBehaviorSanitizer (no GPU needed).
+
+tests/abi_host_check.c drives every host rejection path of include/olive_score.h
+(malformed descriptors, NULL pointers and contexts, and an init that fails in the
+HIP runtime and must free its partly built context). It is linked against the ABI
+source built for the host only with both sanitizers, and against the library's other
+objects as built by paper_2609_36246_amd/build.py; any invalid access or undefined
+behaviour on those paths aborts the program.
+"""
+import os
+import shutil
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+PKG = os.path.join(ROOT, "paper_2609_36246_amd")
+CSRC = os.path.join(PKG, "csrc")
+OBJ_DIR = os.path.join(PKG, "_build")
+ROCM = "/opt/rocm"
+# Each sanitizer flag applies to host code only.
+SAN = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+       "-Xarch_host", "-fno-sanitize-recover=all"]
+
+
+def _tools():
+    hipcc = os.path.join(ROCM, "bin", "hipcc")
+    clang = os.path.join(ROCM, "llvm", "bin", "clang")
+    if not (os.path.exists(hipcc) and os.path.exists(clang)):
+        pytest.skip("ROCm compilers not found")
+    return hipcc, clang
+
+
+def test_host_argument_checks_under_asan_and_ubsan(tmp_path):
+    hipcc, clang = _tools()
+    from paper_2609_36246_amd import build
+    others = [os.path.join(OBJ_DIR, s.replace(".hip", ".o")) for s in build.SOURCES
+              if s != "olive_abi.hip"]
+    if not all(os.path.exists(o) for o in others):
+        build.build()
+    inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
+    abi_o = str(tmp_path / "olive_abi_san.o")
+    subprocess.run([hipcc, "--offload-host-only", "-O1", "-g", "-std=c++17", "-fPIC"] + SAN +
+                   inc + ["-c", os.path.join(CSRC, "olive_abi.hip"), "-o", abi_o], check=True)
+    drv_o = str(tmp_path / "abi_host_check.o")
+    subprocess.run([clang, "-O1", "-g", "-std=c11"] + SAN[1::2] + inc +
+                   ["-c", os.path.join(ROOT, "tests", "abi_host_check.c"), "-o", drv_o],
+                   check=True)
+    exe = str(tmp_path / "abi_host_check")
+    subprocess.run([hipcc, "--offload-arch=gfx950"] + SAN + ["-o", exe, drv_o, abi_o] + others,
+                   check=True)
+    env = dict(os.environ)
+    # the HIP runtime's own allocations are not under test
+    env["ASAN_OPTIONS"] = "detect_leaks=0:abort_on_error=1"
+    env["UBSAN_OPTIONS"] = "halt_on_error=1:print_stacktrace=1"
+    env["HIP_VISIBLE_DEVICES"] = ""     # the host paths only, also on a machine with a GPU
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120, env=env)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert r.stdout.startswith("ok "), r.stdout
+    assert "runtime error" not in r.stderr and "AddressSanitizer" not in r.stderr, r.stderr
+    shutil.rmtree(str(tmp_path), ignore_errors=True)

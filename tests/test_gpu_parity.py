@@ -1,10 +1,10 @@
 """GPU parity of the HIP scoring path against the fp64 oracle (through the C ABI).
 
 Small workloads are compared on every position (they span several vocabulary and
-position tiles and end in ragged tails); the five named workloads are compared in
-full where the oracle finishes in seconds (tiny, small) and on a stratified row
-sample otherwise (large_vocab, long_rollout, ragged), at the launch configuration
-the benchmark times. Masks and counts are always compared in full.
+position tiles and end in ragged tails); of the five named workloads, tiny, small and
+large_vocab are compared on every row, long_rollout and ragged on at least 1% of their
+valid rows including two whole sequences, at the launch configuration the benchmark
+times. Masks and counts are always compared in full.
 """
 import numpy as np
 import pytest
@@ -13,7 +13,8 @@ import torch
 from oracle import olive_oracle as O
 from paper_2609_36246_amd import _lib as L
 from paper_2609_36246_amd import workloads as W
-from tests.gpu_harness import compare, run_hip, say, stratified_rows
+from tests.gpu_harness import (CE_RTOL, KL_ATOL, KL_RTOL, LOGP_ATOL, compare, parity_rows,
+                               run_hip, say, stratified_rows)
 
 pytestmark = pytest.mark.gpu
 
@@ -257,20 +258,96 @@ def test_small_workload_full():
     compare(hip, wl, label="small")
 
 
-@pytest.mark.parametrize("name", ["large_vocab", "long_rollout", "ragged"])
+def test_large_vocab_workload_full():
+    say("large_vocab workload, full parity on every row")
+    wl = W.make_workload("large_vocab", 0, device="cuda")
+    hip = run_hip(wl)
+    say("large_vocab stats", hip["stats"])
+    assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    compare(hip, wl, label="large_vocab")
+    del wl
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("name", ["long_rollout", "ragged"])
 def test_large_workload_sampled(name):
+    """At least 1% of the valid rows: every row of the two sequences with the fewest
+    valid rows (their per-sequence loss compared too), the rows around every cut and
+    end of the valid prefix, and random valid rows; masks and counts in full."""
     say("workload", name, "sampled parity")
     wl = W.make_workload(name, 0, device="cuda")
     hip = run_hip(wl)
     say(name, "stats", hip["stats"])
-    assert hip["stats"]["kernel"] == "mfma"
-    rows = stratified_rows(wl, n_random=96)
-    compare(hip, wl, rows=rows, label=name)
+    assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    rows, whole = parity_rows(wl, frac=0.01, n_whole=2)
+    compare(hip, wl, rows=rows, whole_seqs=whole, label=name)
     del wl
     torch.cuda.empty_cache()
 
 
 # ----------------------------------------------------------------------------- properties
+def test_vocabulary_permutation_permutes_the_outputs():
+    """Metamorphic: relabel the vocabulary (W columns permuted, targets mapped the same
+    way). Log-probs, both KLs and the per-sequence loss are functions of the logit
+    multiset and keep their values up to fp32 summation order (held to the acceptance
+    bar); greedy tokens map through the permutation (random logits have no exact
+    ties)."""
+    say("vocabulary permutation")
+    wl = custom("multi_tile", **CASES["multi_tile"])
+    a = run_hip(wl, outputs=ALL_OUT)
+    V = wl["spec"].vocab
+    perm = torch.from_numpy(np.random.default_rng(5).permutation(V)).cuda()   # v -> perm[v]
+    inv = torch.argsort(perm)
+    for key in ("w_student", "w_teacher"):
+        wl[key] = wl[key][:, inv].contiguous()          # new column perm[v] = old column v
+    wl["targets"] = perm[wl["targets"].long()].to(torch.int32)
+    b = run_hip(wl, outputs=ALL_OUT)
+    p = perm.cpu().numpy()
+    valid = a["am_s"] >= 0
+    for k in ("am_s", "am_t"):
+        np.testing.assert_array_equal(b[k][valid], p[a[k][valid]], err_msg=k)
+        np.testing.assert_array_equal(b[k][~valid], a[k][~valid], err_msg=k)
+    np.testing.assert_array_equal(a["counts"], b["counts"])
+    for k in ("logp_s", "logp_t"):
+        assert np.max(np.abs(a[k] - b[k])) <= LOGP_ATOL, k
+    for k in ("kl", "kl_rev"):
+        assert np.all(np.abs(a[k] - b[k]) <= KL_ATOL + KL_RTOL * np.abs(a[k])), k
+        assert np.all((a[k] == 0.0) == (b[k] == 0.0)), k
+    assert np.all(np.abs(a["ce"] - b["ce"]) <= CE_RTOL * np.abs(a["ce"]) + 1e-3)
+    compare(b, wl, label="permuted-vocab")
+
+
+@pytest.mark.parametrize("case,order", [("ragged_v1000", [2, 0, 1]),
+                                        ("multi_tile", [4, 3, 2, 1, 0])])
+def test_sequence_reordering_permutes_the_outputs(case, order):
+    """Metamorphic: reorder the sequences of the packed batch (cu_seqlens, cuts, valid
+    lengths, hidden rows and targets moved together). Rows are scored independently,
+    with the same vocabulary splits and fixed merge orders, so every per-position output
+    moves with its row bit for bit, and the per-sequence losses are permuted."""
+    say("sequence reordering", case, order)
+    wl = custom(case, **CASES[case])
+    a = run_hip(wl, outputs=ALL_OUT)
+    cu = wl["cu_seqlens"].cpu().numpy().astype(np.int64)
+    src = np.concatenate([np.arange(cu[b], cu[b + 1]) for b in order])   # new row -> old row
+    lens = np.diff(cu)[order]
+    ncu = np.zeros(len(order) + 1, dtype=np.int32)
+    np.cumsum(lens, out=ncu[1:])
+    idx = torch.from_numpy(src).cuda()
+    wl2 = dict(wl)
+    for key in ("h_student", "h_teacher"):
+        wl2[key] = wl[key][idx].contiguous()
+    wl2["targets"] = wl["targets"][idx].contiguous()
+    wl2["cu_seqlens"] = torch.from_numpy(ncu).cuda()
+    o = torch.tensor(order, dtype=torch.long).cuda()
+    wl2["cut"] = wl["cut"][o].contiguous()
+    wl2["valid_len"] = None if wl["valid_len"] is None else wl["valid_len"][o].contiguous()
+    b = run_hip(wl2, outputs=ALL_OUT)
+    for k in ("kl", "kl_rev", "logp_s", "logp_t", "am_s", "am_t"):
+        np.testing.assert_array_equal(b[k], a[k][src], err_msg=k)
+    np.testing.assert_array_equal(b["ce"], a["ce"][order])
+    np.testing.assert_array_equal(b["counts"], a["counts"])
+
+
 def test_identical_teacher_gives_exact_zero_kl():
     say("teacher == student")
     wl = custom("multi_tile", **CASES["multi_tile"])
@@ -286,6 +363,41 @@ def test_identical_teacher_gives_exact_zero_kl():
         assert np.all(hip["kl_rev"] == 0.0)
         np.testing.assert_array_equal(hip["logp_s"], hip["logp_t"])
         np.testing.assert_array_equal(hip["am_s"], hip["am_t"])
+
+
+def plant_ulp_pair(w, h, a, b, k, scale=4.0):
+    """Make columns a < b of w [d, V] the two largest logits of every row, one bf16 ulp
+    apart in row k: both get w[0] = scale (h[:, 0] = scale lifts them by scale^2), equal
+    entries elsewhere, and w[k, b] = w[k, a] + ulp with w[k, a] = 2^-10. The exact
+    winner is then b where h[:, k] > 0 and a (the lower index) where h[:, k] <= 0, with a
+    gap of |h[:, k]| 2^-17 -- far inside the fp32 near-tie window."""
+    w[:, b] = w[:, a]
+    w[0, a] = w[0, b] = scale
+    w[k, a] = 2.0 ** -10
+    w[k, b] = 2.0 ** -10 + 2.0 ** -17
+    h[:, 0] = scale
+
+
+@pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
+def test_more_near_ties_than_one_window(simple):
+    """Every one of 20,000 rows has its two best logits one bf16 ulp apart (both
+    models): each row is flagged, queued and re-decided exactly -- more than the 8192
+    rows one window of the generic path's re-decision holds -- and every greedy token
+    equals the oracle's."""
+    say("20k near-tied rows", "generic" if simple else "mfma")
+    wl = custom("ulp_pairs", num_seqs=4, seq_len=5000, vocab=512, d_student=64, d_teacher=64,
+                cut_rule=("abs", 1, 4999))
+    plant_ulp_pair(wl["w_student"], wl["h_student"], 100, 140, 3)
+    plant_ulp_pair(wl["w_teacher"], wl["h_teacher"], 7, 300, 5)
+    hip = run_hip(wl, simple=simple)
+    T = wl["total_positions"]
+    say("stats", hip["stats"])
+    assert hip["stats"]["flagged"] == T > 8192, hip["stats"]
+    hk_s = wl["h_student"][:, 3].float().cpu().numpy()
+    hk_t = wl["h_teacher"][:, 5].float().cpu().numpy()
+    np.testing.assert_array_equal(hip["am_s"], np.where(hk_s > 0, 140, 100))
+    np.testing.assert_array_equal(hip["am_t"], np.where(hk_t > 0, 300, 7))
+    compare(hip, wl, label="ulp-pairs-" + ("generic" if simple else "mfma"))
 
 
 def test_duplicate_best_column_takes_lowest_index():

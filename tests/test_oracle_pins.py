@@ -27,6 +27,23 @@ def bf16_values(shape, rng, std=1.0):
     return x.to(torch.bfloat16).float().numpy().astype(np.float64)
 
 
+def test_row_scores_without_extras_returns_the_same_values():
+    """extras=False only leaves keys out: every returned value is bit-identical to the
+    full call's (the GPU parity of large workloads uses it), and the left-out keys
+    are the reverse KL and top-K ones."""
+    rng = np.random.default_rng(7)
+    n, V, ds, dt = 5, 300, 16, 24
+    hs, ht = bf16_values((n, ds), rng, 2.0), bf16_values((n, dt), rng, 2.0)
+    ws, wt = bf16_values((ds, V), rng), bf16_values((dt, V), rng)
+    y = rng.integers(0, V, size=n)
+    full = O.row_scores(hs, ws, y, 2.0, ht, wt, 0.5)
+    core = O.row_scores(hs, ws, y, 2.0, ht, wt, 0.5, extras=False)
+    assert set(full) - set(core) == {"kl_rev", "kl_rev_nonneg", "overlap", "kl_topk",
+                                     "topk_s", "topk_t"}
+    for k, v in core.items():
+        np.testing.assert_array_equal(v, full[k], err_msg=k)
+
+
 # ----------------------------------------------------------------------------- exact arithmetic
 def decimal_row(h, w, scale):
     """z, lse, log-softmax of one row in 50-digit decimal arithmetic, no max shift."""
