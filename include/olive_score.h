@@ -201,6 +201,15 @@ typedef struct {
                                     student) (App. A, Table 3), +0.0 elsewhere */
     int32_t *topk_student;       /* [T][16] int32: TopK_S in rank order, -1 elsewhere */
     int32_t *topk_teacher;       /* [T][16] int32: TopK_T in rank order, -1 elsewhere */
+    /* Appended field: a caller built against the layout without it passes the smaller
+     * size (offsetof(olive_score_outputs, jsd)) and is served as before. */
+    float *jsd;                  /* [T] fp32: the Jensen-Shannon divergence
+                                    1/2 KL(p_S || m) + 1/2 KL(p_T || m), m = (p_S + p_T) / 2,
+                                    in the region, +0.0 elsewhere: the symmetric companion
+                                    of the reverse KL of on-policy distillation (Sec. 1).
+                                    Formed by a second pass over the vocabulary for the
+                                    scored positions; needs the MFMA path (E_UNSUPPORTED
+                                    otherwise) */
 } olive_score_outputs;
 
 /*
@@ -220,13 +229,15 @@ typedef struct {
 
 /*
  * Every per-position output of one batch in one fused pass over the vocabulary:
- * olive_kl_masked's outputs plus the reverse KL and the top-K statistics. Teacher
- * outputs (kl, kl_reverse, logp_teacher, argmax_teacher and every top-K output) need
- * a teacher context and b->h_teacher. Malformed sequences give NaN (top-K indices -1)
+ * olive_kl_masked's outputs plus the reverse KL and the top-K statistics (and, in a
+ * second pass over the scored positions, the Jensen-Shannon divergence). Teacher
+ * outputs (kl, kl_reverse, jsd, logp_teacher, argmax_teacher and every top-K output)
+ * need a teacher context and b->h_teacher. Malformed sequences give NaN (top-K indices -1)
  * as for the other outputs.
  * Errors: E_NULL (out, or every output pointer, NULL), E_RANGE (out->size wrong or
- * unknown flags), E_UNSUPPORTED (a top-K output without OLIVE_FLAG_TOPK at init, or
- * with hidden states that are not 16-byte aligned), and as olive_kl_masked.
+ * unknown flags), E_UNSUPPORTED (a top-K output without OLIVE_FLAG_TOPK at init, a
+ * top-K output or jsd where the MFMA kernel does not apply, e.g. hidden states that
+ * are not 16-byte aligned), and as olive_kl_masked.
  */
 olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
                                const olive_score_outputs *out, void *hip_stream);

@@ -18,6 +18,9 @@ What it computes (for every packed position of a batch of stitched rollouts):
     minimises it, Sec. 6; OPD scores student tokens with the teacher, Sec. 1);
   * KL(p_S || p_T) = sum_v p_S[v] (log p_S[v] - log p_T[v])   -- the reverse
     direction, the per-token objective of on-policy distillation (Sec. 1);
+  * JSD(p_S, p_T) = 1/2 KL(p_S || m) + 1/2 KL(p_T || m), m = (p_S + p_T) / 2  -- the
+    symmetric divergence between the two, bounded by ln 2 (the paper names only the
+    reverse KL for OPD; the Jensen-Shannon form is offered beside it);
   * argmax_X = lowest v attaining M_X   -- the greedy token (the K = 1 case of the
     top-K overlap statistic of Sec. 4.1);
   * TopK_X = the K largest logits of model X, ties broken towards the lower index;
@@ -163,6 +166,19 @@ def kl_student_teacher(z_s, lse_s: float, z_t, lse_t: float) -> tuple:
     return kl_teacher_student(z_s, lse_s, z_t, lse_t)
 
 
+def jsd(z_s, lse_s: float, z_t, lse_t: float) -> float:
+    """Jensen-Shannon divergence of one row's two distributions (fp64, exactly rounded
+    sums): 1/2 sum_v p_S (log p_S - log m) + 1/2 sum_v p_T (log p_T - log m) with the
+    mixture m = (p_S + p_T) / 2, whose log is formed as logaddexp(log p_S, log p_T) -
+    ln 2 so that it stays finite where one probability underflows."""
+    lp_s = _f64(z_s) - lse_s
+    lp_t = _f64(z_t) - lse_t
+    log_m = np.logaddexp(lp_s, lp_t) - math.log(2.0)
+    a = math.fsum((np.exp(lp_s) * (lp_s - log_m)).tolist())
+    b = math.fsum((np.exp(lp_t) * (lp_t - log_m)).tolist())
+    return 0.5 * a + 0.5 * b
+
+
 TOPK = 16   # LogProb top-K of the OPD baseline (App. A, Table 3)
 
 
@@ -200,12 +216,12 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
     Returns float64 / int64 arrays of length n: z_y_s, lse_s, logp_s, argmax_s,
     gap_s, max_s, and with a teacher the same for t plus kl (direct) and
     kl_nonneg (KL(teacher || student)), kl_rev and kl_rev_nonneg (KL(student ||
-    teacher)), overlap and kl_topk (top-K statistics, K = TOPK) and the top-K index
-    sets topk_s / topk_t ([n, TOPK]).
+    teacher)), jsd (Jensen-Shannon), overlap and kl_topk (top-K statistics, K = TOPK)
+    and the top-K index sets topk_s / topk_t ([n, TOPK]).
 
-    extras=False leaves out the reverse KL and the top-K statistics (their keys are
-    then absent); every value that is returned is computed exactly as with
-    extras=True.
+    extras=False leaves out the reverse KL, the Jensen-Shannon divergence and the top-K
+    statistics (their keys are then absent); every value that is returned is computed
+    exactly as with extras=True.
     """
     hs = _f64(h_student_rows)
     n = hs.shape[0]
@@ -225,7 +241,7 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
         for k in ("z_y_t", "lse_t", "logp_t", "gap_t", "max_t", "kl", "kl_nonneg"):
             out[k] = np.zeros(n)
         if extras:
-            for k in ("kl_rev", "kl_rev_nonneg", "overlap", "kl_topk"):
+            for k in ("kl_rev", "kl_rev_nonneg", "jsd", "overlap", "kl_topk"):
                 out[k] = np.zeros(n)
             out["topk_s"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
             out["topk_t"] = np.zeros((n, min(TOPK, V)), dtype=np.int64)
@@ -259,6 +275,7 @@ def row_scores(h_student_rows, w_student, targets_rows, scale_student: float = 1
                 klr, klrp = kl_student_teacher(zs[i], st["lse"], zt[i], tt["lse"])
                 out["kl_rev"][g] = klr
                 out["kl_rev_nonneg"][g] = klrp
+                out["jsd"][g] = jsd(zs[i], st["lse"], zt[i], tt["lse"])
                 kk = min(TOPK, V)
                 set_s, set_t = topk_set(zs[i], kk), topk_set(zt[i], kk)
                 out["overlap"][g] = topk_overlap(set_s, set_t, kk)
@@ -276,7 +293,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
 
     Outputs per packed position (length T): logp_s, logp_t, argmax_s, argmax_t,
     kl (KL(teacher || student) in-region, exactly +0.0 elsewhere), kl_rev
-    (KL(student || teacher), masked the same way); at positions
+    (KL(student || teacher)) and jsd (Jensen-Shannon), masked the same way; at positions
     past the valid length logp = 0 and argmax = -1. Per sequence: ce (Eq. 1's
     loss, minus the sum of the student's log-probs over the in-region positions).
     Counts: n_scored (in-region positions) and t_valid (valid positions).
@@ -297,7 +314,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
                        scale_teacher)
     out = dict(logp_s=np.zeros(T), argmax_s=np.full(T, -1, dtype=np.int64),
                lse_s=np.zeros(T), gap_s=np.full(T, math.inf), kl=np.zeros(T),
-               kl_nonneg=np.zeros(T), kl_rev=np.zeros(T), overlap=np.zeros(T),
+               kl_nonneg=np.zeros(T), kl_rev=np.zeros(T), jsd=np.zeros(T), overlap=np.zeros(T),
                kl_topk=np.zeros(T), evaluated=np.zeros(T, dtype=bool))
     if has_t:
         out.update(logp_t=np.zeros(T), argmax_t=np.full(T, -1, dtype=np.int64),
@@ -313,6 +330,7 @@ def score(h_student, w_student, targets, cu_seqlens, cut, valid_len=None,
             out["kl"][sel[inr]] = r["kl"][inr]
             out["kl_nonneg"][sel[inr]] = r["kl_nonneg"][inr]
             out["kl_rev"][sel[inr]] = r["kl_rev"][inr]
+            out["jsd"][sel[inr]] = r["jsd"][inr]
             out["overlap"][sel[inr]] = r["overlap"][inr]
             out["kl_topk"][sel[inr]] = r["kl_topk"][inr]
     # Eq. 1: the loss of sequence b is minus the sum of the student's log-probs of

@@ -65,7 +65,8 @@ class olive_score_outputs(ctypes.Structure):
                 ("logp_teacher", ctypes.c_void_p), ("argmax_student", ctypes.c_void_p),
                 ("argmax_teacher", ctypes.c_void_p), ("ce_per_seq", ctypes.c_void_p),
                 ("topk_overlap", ctypes.c_void_p), ("kl_topk", ctypes.c_void_p),
-                ("topk_student", ctypes.c_void_p), ("topk_teacher", ctypes.c_void_p)]
+                ("topk_student", ctypes.c_void_p), ("topk_teacher", ctypes.c_void_p),
+                ("jsd", ctypes.c_void_p)]
 
 
 class olive_grad_outputs(ctypes.Structure):
@@ -221,7 +222,7 @@ def olive_kl_masked(ctx, batch: olive_batch, kl, counts=None, logp_student=None,
 def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_teacher=None,
                  argmax_student=None, argmax_teacher=None, ce_per_seq=None,
                  topk_overlap=None, kl_topk=None, topk_student=None, topk_teacher=None,
-                 flags: int = 0) -> olive_score_outputs:
+                 jsd=None, flags: int = 0) -> olive_score_outputs:
     o = olive_score_outputs()
     o.size = ctypes.sizeof(olive_score_outputs)
     o.flags = int(flags)
@@ -231,6 +232,7 @@ def make_outputs(kl=None, kl_reverse=None, counts=None, logp_student=None, logp_
     o.ce_per_seq = _ptr(ce_per_seq)
     o.topk_overlap, o.kl_topk = _ptr(topk_overlap), _ptr(kl_topk)
     o.topk_student, o.topk_teacher = _ptr(topk_student), _ptr(topk_teacher)
+    o.jsd = _ptr(jsd)
     return o
 
 

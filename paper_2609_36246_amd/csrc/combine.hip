@@ -201,6 +201,35 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
     }
 }
 
+// Jensen-Shannon outputs (one thread per compacted row): the scored rows [0, n_scored)
+// sum their split partials in split order and scale by ln(2)/2; other valid rows get
+// +0.0. A scored row whose normalisers are NaN (bad target) stays NaN.
+__global__ void __launch_bounds__(256)
+jsd_combine_kernel(ScoreArgs a, int grid, float *__restrict__ jsd) {
+    const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const Sched *sched = a.sched;
+    const int t_valid = sched->t_valid;
+    if (j >= t_valid) return;
+    const int64_t n_sc = sched->n_scored;
+    const int rows = (int)(n_sc < t_valid ? n_sc : t_valid);
+    const int64_t g = a.rowmap[j] & 0x7fffffffu;
+    if (j >= rows) {
+        jsd[g] = 0.f;
+        return;
+    }
+    const int ns = pass_splits((rows + MFMA_BT - 1) / MFMA_BT, a.n_vtiles, grid);
+    float sum = 0.f;
+    for (int s = 0; s < ns; ++s) sum += a.part[(F_J * MAX_SPLITS + s) * a.pstride + j];
+    jsd[g] = 0.5f * kLn2 * sum;
+}
+
+hipError_t launch_jsd_combine(const ScoreArgs &a, float *jsd, int grid, int64_t max_rows,
+                              hipStream_t st) {
+    if (max_rows <= 0) return hipSuccess;
+    jsd_combine_kernel<<<(unsigned)((max_rows + 255) / 256), 256, 0, st>>>(a, grid, jsd);
+    return hipGetLastError();
+}
+
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,

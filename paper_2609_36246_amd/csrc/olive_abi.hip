@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cmath>
+#include <cstddef>
 #include <cstring>
 #include <new>
 #include <vector>
@@ -24,6 +25,7 @@ struct olive_score_ctx {
     float *part = nullptr;
     int64_t pstride = 0;
     float *logp_tmp = nullptr;
+    float *lse_buf = nullptr;                   // [P][2] normalisers for the JSD pass
     int32_t *flagged = nullptr;
     int flag_cap = 0;                           // rows the near-tie list holds: max_positions
     int fx_window = 0;                          // generic path: flagged rows per window
@@ -72,7 +74,7 @@ void release(olive_score_ctx *c) {
         for (int i = 0; i < 64; ++i)
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
-                    c->logp_tmp, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
+                    c->logp_tmp, c->lse_buf, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
                     c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_dzv, c->bw_hrt};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -130,7 +132,7 @@ int topk_min_splits(int n_vtiles) {
 olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *spans,
                  float *kl, float *kl_rev, int64_t *counts, float *logp_s, float *logp_t,
                  int32_t *am_s, int32_t *am_t, float *ce, hipStream_t st,
-                 bool region_only = false, TopkOut tk = TopkOut{}) {
+                 bool region_only = false, TopkOut tk = TopkOut{}, float *jsd = nullptr) {
     const olive_score_desc &d = ctx->desc;
     if (!b->cu_seqlens || !b->targets || !b->h_student) return OLIVE_E_NULL;
     if (!spans && !b->cut) return OLIVE_E_NULL;
@@ -146,7 +148,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     }
     const bool topk = tk.any();
     if (topk && !ctx->topk) return OLIVE_E_UNSUPPORTED;
-    const bool want_t = kl || kl_rev || logp_t || am_t || topk;
+    const bool want_t = kl || kl_rev || jsd || logp_t || am_t || topk;
     if (want_t && (!ctx->has_t || !b->h_teacher)) return OLIVE_E_UNSUPPORTED;
     const bool has_t = want_t;
     const int64_t T = b->total_positions;
@@ -157,9 +159,12 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     const bool mfma = ctx->mfma_ok && ((uintptr_t)b->h_student & 15) == 0 &&
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
+    if (jsd && !mfma) return OLIVE_E_UNSUPPORTED;    // the JSD pass is an MFMA pass
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
-    // normalisers kept for a backward on this batch (MFMA path, backward contexts)
-    float *lse_out = topk ? ctx->tkw.lse : ((mfma && ctx->bw) ? ctx->bw_lse : nullptr);
+    // normalisers kept for a backward on this batch (MFMA path, backward contexts), and
+    // read by the top-K stages and the JSD pass
+    float *lse_out = topk ? ctx->tkw.lse
+                          : ((mfma && ctx->bw) ? ctx->bw_lse : (jsd ? ctx->lse_buf : nullptr));
     ctx->fwd_lse_ok = false;
 
     olive_status s;
@@ -183,8 +188,8 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                                 ctx->err,
                                 logp_s,
                                 has_t ? logp_t : nullptr, am_s, has_t ? am_t : nullptr,
-                                has_t ? kl : nullptr, has_t ? kl_rev : nullptr, logp_tmp, tk,
-                                st));
+                                has_t ? kl : nullptr, has_t ? kl_rev : nullptr,
+                                has_t ? jsd : nullptr, logp_tmp, tk, st));
     if (s) return s;
 
     ScoreArgs a;
@@ -250,6 +255,15 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
         s = check_hip(launch_topk(a, ctx->tkw, tk, T, st));
         if (s) return s;
     }
+    if (jsd) {
+        // second pass over the scored rows (compacted first), from the normalisers
+        JsdArgs z;
+        z.lse = lse_out;
+        s = check_hip(launch_score_jsd(a, z, grid, st));
+        if (s) return s;
+        s = check_hip(launch_jsd_combine(a, jsd, grid, T, st));
+        if (s) return s;
+    }
     if (ce) {
         s = check_hip(launch_ce(*b, spans, ctx->seqbuf, ctx->sched,
                                 logp_s ? logp_s : ctx->logp_tmp, ce, st));
@@ -291,7 +305,7 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     if (s) return s;
     s = check_hip(launch_rowmap(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
                                 ctx->err, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                nullptr, TopkOut{}, st));
+                                nullptr, nullptr, TopkOut{}, st));
     if (s) return s;
     ScoreArgs a;
     a.hs = b->h_student;
@@ -529,6 +543,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         if (!s) s = backward_init(c, st);
     }
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
+    if (!s && c->mfma_ok && c->has_t) s = dev_alloc(&c->lse_buf, (size_t)P * 2 * sizeof(float));
     if (!s) s = dev_alloc(&c->flagged, (size_t)4 * c->flag_cap * sizeof(int32_t));
     if (!s)
         s = dev_alloc(&c->fx_scratch,
@@ -597,13 +612,22 @@ static TopkOut topk_of(const olive_score_outputs *out) {
     return TopkOut{out->topk_overlap, out->kl_topk, out->topk_student, out->topk_teacher};
 }
 
+// The JSD output of an output set, or NULL when the caller's struct predates the field
+// (it then passes the smaller size).
+static float *jsd_of(const olive_score_outputs *out) {
+    return out->size == (int32_t)sizeof(olive_score_outputs) ? out->jsd : nullptr;
+}
+
 static olive_status check_outputs(const olive_score_outputs *out) {
     if (!out) return OLIVE_E_NULL;
-    if (out->size != (int32_t)sizeof(olive_score_outputs)) return OLIVE_E_RANGE;
+    if (out->size != (int32_t)sizeof(olive_score_outputs) &&
+        out->size != (int32_t)offsetof(olive_score_outputs, jsd))
+        return OLIVE_E_RANGE;
     if (out->flags & ~OLIVE_OUT_REGION_ONLY) return OLIVE_E_RANGE;
     if (!out->kl && !out->kl_reverse && !out->counts && !out->logp_student &&
         !out->logp_teacher && !out->argmax_student && !out->argmax_teacher && !out->ce_per_seq &&
-        !out->topk_overlap && !out->kl_topk && !out->topk_student && !out->topk_teacher)
+        !out->topk_overlap && !out->kl_topk && !out->topk_student && !out->topk_teacher &&
+        !jsd_of(out))
         return OLIVE_E_NULL;
     return OLIVE_OK;
 }
@@ -615,7 +639,7 @@ olive_status olive_score_batch(olive_score_ctx *ctx, const olive_batch *b,
     return run(ctx, b, nullptr, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
                (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0,
-               topk_of(out));
+               topk_of(out), jsd_of(out));
 }
 
 olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
@@ -626,7 +650,7 @@ olive_status olive_score_batch_spans(olive_score_ctx *ctx, const olive_batch *b,
     return run(ctx, b, spans, out->kl, out->kl_reverse, out->counts, out->logp_student,
                out->logp_teacher, out->argmax_student, out->argmax_teacher, out->ce_per_seq,
                (hipStream_t)hip_stream, (out->flags & OLIVE_OUT_REGION_ONLY) != 0,
-               topk_of(out));
+               topk_of(out), jsd_of(out));
 }
 
 olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,

@@ -59,6 +59,21 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, int64_t 
     return bf16_bits_to_f32(p[i]);
 }
 
+// Vocabulary splits of a pass over n_p position tiles on a persistent grid of G
+// workgroups: the count minimising (rounds of the grid) x (vocabulary tiles per
+// split), the smallest among equals. The passes over the scored rows (logit gradient,
+// Jensen-Shannon) and the combine of the latter use it alike.
+__device__ __forceinline__ int pass_splits(int n_p, int n_vtiles, int G) {
+    const int smax = n_vtiles < MAX_SPLITS ? n_vtiles : MAX_SPLITS;
+    int ns = 1;
+    int64_t best = -1;
+    for (int sc = 1; sc <= smax; ++sc) {
+        const int64_t cost = (((int64_t)n_p * sc + G - 1) / G) * ((n_vtiles + sc - 1) / sc);
+        if (best < 0 || cost < best) { best = cost; ns = sc; }
+    }
+    return ns;
+}
+
 // Running max / second max / lowest argmax / rescaled exp-sum of one model, and
 // the teacher-weighted difference accumulator A (teacher only).
 struct Stat {

@@ -19,10 +19,12 @@ namespace olive {
 //             end) or s_T zT_v - s_S zS_v (different scales);
 //   B:        sum_v exp(s_S * (zS_v - BEST_S)) * (-D_v), the student-weighted
 //             difference (reverse KL; written only when it is requested).
+//   J:        the Jensen-Shannon pass's sum over the split of p_hi g(p_lo / p_hi)
+//             (log2 units; see the pass), for scored rows only.
 enum Field {
     F_BEST_S = 0, F_SEC_S = 1, F_IDX_S = 2, F_Z_S = 3,
-    F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8, F_B = 9,
-    NFIELDS = 10
+    F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8, F_B = 9, F_J = 10,
+    NFIELDS = 11
 };
 // Top-K planes (contexts built with OLIVE_FLAG_TOPK only), per model m (0 = S, 1 = T)
 // from F_TK + m * TK_FIELDS: the split's 8 largest raw logits (descending, lower
@@ -133,6 +135,12 @@ struct DzArgs {
     uint16_t *dz_v;              // [V][pitch] the same, transposed
 };
 
+// Jensen-Shannon pass over the scored rows [0, n_scored) of a forward call (the
+// scored rows are compacted first), from that call's log-normalisers.
+struct JsdArgs {
+    const float *lse;            // [rows][2] log-normalisers per compacted row (combine)
+};
+
 // C (+)= alpha * A * B^T on bf16 rows, fp32 C. Each operand is read in K steps of 64
 // elements: step kk of row r at base + kk * kstep + r * ld (row-major: kstep = 128,
 // ld = the row pitch; K-blocked panels [K/64][rows][64]: ld = 128, kstep = rows * 128).
@@ -171,13 +179,16 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool re
                          int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
-                         float *logp_tmp, const TopkOut &tk, hipStream_t st);
+                         float *jsd, float *logp_tmp, const TopkOut &tk, hipStream_t st);
 hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_t max_units,
                                hipStream_t st);
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
                              bool topk, int grid, hipStream_t st);
 hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,
                            hipStream_t st);
+hipError_t launch_score_jsd(const ScoreArgs &a, const JsdArgs &z, int grid, hipStream_t st);
+hipError_t launch_jsd_combine(const ScoreArgs &a, float *jsd, int grid, int64_t max_rows,
+                              hipStream_t st);
 hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st);
 hipError_t launch_panel_t(const void *w, int64_t V, int d, int64_t vp, void *out,
                           hipStream_t st);

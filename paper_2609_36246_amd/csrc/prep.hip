@@ -247,7 +247,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
               const Sched *__restrict__ sched,
               uint32_t *__restrict__ rowmap, float *__restrict__ logp_s,
               float *__restrict__ logp_t, int32_t *__restrict__ am_s, int32_t *__restrict__ am_t,
-              float *__restrict__ kl, float *__restrict__ kl_rev,
+              float *__restrict__ kl, float *__restrict__ kl_rev, float *__restrict__ jsd,
               float *__restrict__ logp_tmp, TopkOut tk) {
     const int32_t *cvalid = seqbuf;
     const int32_t *vl_eff = seqbuf + (B + 1);
@@ -278,6 +278,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (am_t) am_t[g] = -1;
             if (kl) kl[g] = qnan;
             if (kl_rev) kl_rev[g] = qnan;
+            if (jsd) jsd[g] = qnan;
             if (logp_tmp) logp_tmp[g] = qnan;
             if (tk.overlap) tk.overlap[g] = qnan;
             if (tk.kl) tk.kl[g] = qnan;
@@ -314,6 +315,7 @@ rowmap_kernel(const int32_t *__restrict__ cu, int32_t B, int64_t T, int32_t regi
             if (am_t) am_t[g] = -1;
             if (kl) kl[g] = 0.f;
             if (kl_rev) kl_rev[g] = 0.f;
+            if (jsd) jsd[g] = 0.f;
             if (logp_tmp) logp_tmp[g] = 0.f;
             if (tk.overlap) tk.overlap[g] = 0.f;
             if (tk.kl) tk.kl[g] = 0.f;
@@ -419,7 +421,7 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool re
                          int64_t V, const int32_t *seqbuf,
                          const Sched *sched, uint32_t *rowmap, int32_t *err, float *logp_s,
                          float *logp_t, int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev,
-                         float *logp_tmp, const TopkOut &tk, hipStream_t st) {
+                         float *jsd, float *logp_tmp, const TopkOut &tk, hipStream_t st) {
     (void)V; (void)err;
     int64_t T = b.total_positions;
     int64_t blocks = (T + 255) / 256;
@@ -429,7 +431,7 @@ hipError_t launch_rowmap(const olive_batch &b, const olive_spans *spans, bool re
                                                     span_args(spans), region_only ? 1 : 0, seqbuf,
                                                     sched, rowmap,
                                                     logp_s, logp_t, am_s,
-                                                    am_t, kl, kl_rev, logp_tmp, tk);
+                                                    am_t, kl, kl_rev, jsd, logp_tmp, tk);
     return hipGetLastError();
 }
 

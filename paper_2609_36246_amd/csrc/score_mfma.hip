@@ -765,14 +765,7 @@ struct Kernel {
         const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
         const int n_p = (t_rows + BT - 1) / BT;
         const int G = gridDim.x;
-        // splits: minimise (rounds of the persistent grid) x (vocabulary tiles per split)
-        const int smax = a.n_vtiles < MAX_SPLITS ? a.n_vtiles : MAX_SPLITS;
-        int ns = 1;
-        int64_t best = -1;
-        for (int sc = 1; sc <= smax; ++sc) {
-            const int64_t cost = (((int64_t)n_p * sc + G - 1) / G) * ((a.n_vtiles + sc - 1) / sc);
-            if (best < 0 || cost < best) { best = cost; ns = sc; }
-        }
+        const int ns = pass_splits(n_p, a.n_vtiles, G);
         const int64_t n_units = (int64_t)n_p * ns;
         Lane L;
         L.lane = threadIdx.x & 63;
@@ -935,6 +928,123 @@ struct Kernel {
             compiler_fence();
         }
     }
+
+    // Jensen-Shannon pass over the scored rows [0, n_scored) (compacted first by every
+    // forward call), from the forward pass's log-normalisers. With log2 probabilities
+    // l_S = z_S s_S log2(e) - lse_S log2(e) and l_T likewise, the divergence of a row is
+    //   JSD = 1/2 sum_v [p_S log p_S + p_T log p_T - (p_S + p_T) log((p_S + p_T) / 2)]
+    //       = ln(2)/2 sum_v p_hi g(r),   p_hi = 2^max(l_S, l_T),  r = 2^-|l_S - l_T|,
+    //   g(r) = (1 + r)(1 - log2(1 + r)) + r log2(r)   (0 at r = 1, 1 at r = 0),
+    // a sum of non-negative terms with no rescaling (the normalisers are known). The
+    // same units and K sweep as the scoring kernel recompute both models' logits; per
+    // lane and column the terms add in vocabulary order, lanes l / l+32 and the two
+    // vocabulary halves merge in a fixed order, and each (split, row) partial goes to
+    // plane F_J for the combine.
+    static __device__ __forceinline__ void run_jsd(ScoreArgs a, JsdArgs z) {
+        const int64_t n_sc = a.sched->n_scored;
+        const int t_valid = a.sched->t_valid;
+        const int rows = (int)(n_sc < t_valid ? n_sc : t_valid);
+        const int n_p = (rows + BT - 1) / BT;
+        const int G = gridDim.x;
+        const int ns = pass_splits(n_p, a.n_vtiles, G);
+        const int64_t n_units = (int64_t)n_p * ns;
+        Lane L;
+        L.lane = threadIdx.x & 63;
+        L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        L.wv = L.wid & 1;
+        L.wt = L.wid >> 1;
+        L.h = L.lane >> 5;
+        L.l32 = L.lane & 31;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+        const int nS = a.ds / BK, nT = a.dt / BK;
+#pragma unroll
+        for (int par = 0; par < 2; ++par) {
+            const int R0 = L.wid * 8 * W_DMA + (L.lane >> 3);
+            const int ch = (L.lane & 7) ^ swz(R0 + 8 * par);
+            L.wvoff[0][par] = (uint32_t)(R0 * a.ds * 2 + ch * 16);
+            L.wvoff[1][par] = (uint32_t)(R0 * a.dt * 2 + ch * 16);
+        }
+        const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+        const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+
+        for (int64_t q = my; q < n_units; q += G) {
+            const int p = (int)(q % n_p), s = (int)(q / n_p);
+#pragma unroll
+            for (int i = 0; i < H_DMA; ++i) {
+                const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
+                const int ch = (L.lane & 7) ^ swz(R);
+                int t = p * BT + R;
+                t = t < rows ? t : rows - 1;
+                const int64_t g = a.rowmap[t] & 0x7fffffffu;
+                L.hp[0][i] = (const char *)a.hs + g * a.ds * 2 + ch * 16;
+                L.hp[1][i] = (const char *)a.ht + g * a.dt * 2 + ch * 16;
+            }
+            // the lane's two columns: scored row and its normalisers in log2 units
+            int tcol[2];
+            bool ok[2];
+            float l2s[2], l2t[2], acc[2] = {0.f, 0.f};
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) {
+                tcol[cb] = p * BT + L.wt * 64 + cb * 32 + L.l32;
+                ok[cb] = tcol[cb] < rows;
+                const int64_t j = ok[cb] ? tcol[cb] : 0;
+                l2s[cb] = ok[cb] ? z.lse[2 * j] * kLog2e : 0.f;
+                l2t[cb] = ok[cb] ? z.lse[2 * j + 1] * kLog2e : 0.f;
+            }
+            const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
+            const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
+            floatx16 accS[4][2], accT[4][2];
+            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+                // rows of a shifted last tile below vt * BV get -2^99 in both models:
+                // p_hi = 0 there, and r stays finite
+                if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+                    for (int vb = 0; vb < 4; ++vb) {
+                        __builtin_amdgcn_sched_barrier(0);
+                        float part = 0.f;
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) {
+                            const float ls = fmaf(agpr_read(accS[vb][cb][r]), a.cS, -l2s[cb]);
+                            const float lt = fmaf(agpr_read(accT[vb][cb][r]), a.cT, -l2t[cb]);
+                            const float ad = fabsf(ls - lt);
+                            const float ph = fast_exp2(max2(ls, lt));
+                            const float rr = fast_exp2(-ad);
+                            const float one_r = 1.0f + rr;
+                            const float gv = fmaf(one_r, 1.0f - fast_log2(one_r), -rr * ad);
+                            part = fmaf(ph, gv, part);
+                        }
+                        acc[cb] += part;
+                    }
+            });
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb) acc[cb] += __shfl_xor(acc[cb], 32);
+            // the two vocabulary halves (wv = 1 into wv = 0) through LDS, once the
+            // trailing prefetches into the stages have landed
+            float *xs = (float *)g_ring;   // [wt][cb][l32]
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __builtin_amdgcn_s_barrier();
+            compiler_fence();
+            if (L.wv == 1 && L.h == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) xs[(L.wt * 2 + cb) * 32 + L.l32] = acc[cb];
+            }
+            compiler_fence();
+            __syncthreads();
+            if (L.wv == 0 && L.h == 0) {
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb)
+                    if (ok[cb])
+                        a.part[(F_J * MAX_SPLITS + s) * a.pstride + tcol[cb]] =
+                            acc[cb] + xs[(L.wt * 2 + cb) * 32 + L.l32];
+            }
+            compiler_fence();
+            __syncthreads();
+        }
+    }
 };
 
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
@@ -947,6 +1057,17 @@ template <bool HAS_T>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_dz_kernel(ScoreArgs a, DzArgs z) {
     Kernel<HAS_T, true, false, false>::run_dz(a, z);
+}
+
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+score_jsd_kernel(ScoreArgs a, JsdArgs z) {
+    Kernel<true, true, false, false>::run_jsd(a, z);
+}
+
+hipError_t launch_score_jsd(const ScoreArgs &a, const JsdArgs &z, int grid, hipStream_t st) {
+    if (grid <= 0) return hipSuccess;
+    score_jsd_kernel<<<grid, 256, 0, st>>>(a, z);
+    return hipGetLastError();
 }
 
 hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,

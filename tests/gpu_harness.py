@@ -78,6 +78,7 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
     out = {}
     out["kl"] = f32() if "kl" in outputs and not student_only else None
     out["kl_rev"] = f32() if "kl_rev" in outputs and not student_only else None
+    out["jsd"] = f32() if "jsd" in outputs and not student_only else None
     out["counts"] = torch.full((2,), -1, dtype=torch.int64, device=dev) \
         if "counts" in outputs else None
     out["logp_s"] = f32() if "logp_s" in outputs else None
@@ -97,13 +98,14 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
                          wl["targets"], wl["h_student"],
                          None if student_only else wl["h_teacher"], wl["valid_len"], region)
     for _ in range(repeat):
-        if spans is not None or out["kl_rev"] is not None or out_flags or any_topk:
+        if spans is not None or out["kl_rev"] is not None or out["jsd"] is not None or \
+                out_flags or any_topk:
             o = L.make_outputs(kl=out["kl"], kl_reverse=out["kl_rev"], counts=out["counts"],
                                logp_student=out["logp_s"], logp_teacher=out["logp_t"],
                                argmax_student=out["am_s"], argmax_teacher=out["am_t"],
                                ce_per_seq=out["ce"], topk_overlap=out["overlap"],
                                kl_topk=out["kl_topk"], topk_student=out["tk_s"],
-                               topk_teacher=out["tk_t"], flags=out_flags)
+                               topk_teacher=out["tk_t"], jsd=out["jsd"], flags=out_flags)
             if spans is not None:
                 sp = L.make_spans(wl["span_offsets"], wl["span_pairs"])
                 L.olive_score_batch_spans(ctx, batch, sp, o)
@@ -248,13 +250,13 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
     assert np.all(hip["logp_s"][inval] == 0.0), label
     if "am_s" in hip:
         assert np.all(hip["am_s"][inval] == -1), label
-    for key in ("kl", "kl_rev"):
+    for key in ("kl", "kl_rev", "jsd"):
         if not student_only and key in hip:
             assert np.all(hip[key][~inr] == 0.0) and not np.any(np.signbit(hip[key][~inr])), \
                 (label, key)
     sel = np.arange(T) if rows is None else np.asarray(rows)
     sel = sel[valid[sel]]
-    r = oracle_rows(wl, sel, student_only, extras="kl_rev" in hip)
+    r = oracle_rows(wl, sel, student_only, extras="kl_rev" in hip or "jsd" in hip)
     worst = {}
 
     def chk(name, got, want, atol, rtol=0.0):
@@ -282,6 +284,9 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
         if "kl_rev" in hip:
             want = np.where(inr[sel], r["kl_rev"], 0.0)
             chk("kl_rev", hip["kl_rev"][sel], want, KL_ATOL, KL_RTOL)
+        if "jsd" in hip:
+            want = np.where(inr[sel], r["jsd"], 0.0)
+            chk("jsd", hip["jsd"][sel], want, KL_ATOL, KL_RTOL)
         if check_ce and "ce" in hip and (rows is None or whole_seqs):
             B = len(cu) - 1
             seqs = range(B) if rows is None else whole_seqs
@@ -294,12 +299,20 @@ def compare(hip, wl, region=O.REGION_TEACHER, rows=None, student_only=False, che
                 assert abs(hip["ce"][b] - want) <= CE_RTOL * abs(want) + 1e-3, \
                     (label, b, hip["ce"][b], want)
     n_valid = int(valid.sum())
-    say("%s parity ok on %d of %d valid rows (%.2f%%)%s; worst %s" % (
+    line = "%s parity ok on %d of %d valid rows (%.2f%%)%s; worst %s" % (
         label, sel.size, n_valid, 100.0 * sel.size / max(1, n_valid),
         "" if not whole_seqs else "; whole sequences %s (%d rows, CE compared)" % (
             list(whole_seqs), int(np.isin(m["seq_id"][sel], whole_seqs).sum())),
-        {k: "%.2e" % v for k, v in worst.items()}))
+        {k: "%.2e" % v for k, v in worst.items()})
+    say(line)
+    if label in COVERAGE_LABELS:
+        COVERAGE.append(line)
     return r
+
+
+# Parity lines of the named workloads, printed in the run's terminal summary.
+COVERAGE = []
+COVERAGE_LABELS = ("tiny", "small", "large_vocab", "long_rollout", "ragged", "multi_turn")
 
 
 def exact_logit_bound(h_rows, w, scale):

@@ -89,8 +89,9 @@ def test_struct_layouts_match_header(tmp_path):
         assert got[(name, "__sizeof__")] == ctypes.sizeof(st), name
         for f, _ in st._fields_:
             assert got[(name, f)] == getattr(st, f).offset, (name, f)
-    assert ctypes.sizeof(L.olive_score_outputs) == 104
+    assert ctypes.sizeof(L.olive_score_outputs) == 112
     assert L.olive_score_outputs.topk_teacher.offset == 96
+    assert L.olive_score_outputs.jsd.offset == 104
 
 
 def test_header_constants_match_the_binding():

@@ -22,6 +22,40 @@ _orig_masks = O.masks
 _orig_project = O.project
 _orig_glog = O.grad_logits
 _orig_backward = O.backward
+_orig_jsd = O.jsd
+
+
+def _jsd_parts(z_s, lse_s, z_t, lse_t):
+    lp_s = np.asarray(z_s, dtype=np.float64) - lse_s
+    lp_t = np.asarray(z_t, dtype=np.float64) - lse_t
+    return lp_s, lp_t
+
+
+def jsd_geometric_mixture(z_s, lse_s, z_t, lse_t):
+    # the mixture taken as the geometric mean of the two distributions
+    lp_s, lp_t = _jsd_parts(z_s, lse_s, z_t, lse_t)
+    log_m = 0.5 * (lp_s + lp_t)
+    return 0.5 * math.fsum((np.exp(lp_s) * (lp_s - log_m)).tolist()) + \
+        0.5 * math.fsum((np.exp(lp_t) * (lp_t - log_m)).tolist())
+
+
+def jsd_mixture_not_halved(z_s, lse_s, z_t, lse_t):
+    # log(p_S + p_T) in place of log((p_S + p_T) / 2)
+    lp_s, lp_t = _jsd_parts(z_s, lse_s, z_t, lse_t)
+    log_m = np.logaddexp(lp_s, lp_t)
+    return 0.5 * math.fsum((np.exp(lp_s) * (lp_s - log_m)).tolist()) + \
+        0.5 * math.fsum((np.exp(lp_t) * (lp_t - log_m)).tolist())
+
+
+def jsd_one_sided(z_s, lse_s, z_t, lse_t):
+    # KL(p_S || m) alone
+    lp_s, lp_t = _jsd_parts(z_s, lse_s, z_t, lse_t)
+    log_m = np.logaddexp(lp_s, lp_t) - math.log(2.0)
+    return math.fsum((np.exp(lp_s) * (lp_s - log_m)).tolist())
+
+
+def jsd_not_halved(z_s, lse_s, z_t, lse_t):
+    return 2.0 * _orig_jsd(z_s, lse_s, z_t, lse_t)
 
 
 def lss_dropped_max(z_row):
@@ -168,6 +202,10 @@ MUTANTS = [
     ("grad_logits", glog_ce_weight_on_softmax_dropped),
     ("backward", backward_no_scale),
     ("backward", backward_grad_w_unscaled_rows),
+    ("jsd", jsd_geometric_mixture),
+    ("jsd", jsd_mixture_not_halved),
+    ("jsd", jsd_one_sided),
+    ("jsd", jsd_not_halved),
 ]
 
 PINS = [
@@ -191,6 +229,9 @@ PINS = [
     lambda: [P.test_backward_matches_finite_differences(r, sp) for r, sp in
              ((O.REGION_TEACHER, None), (O.REGION_SPANS, [[(0, 2), (3, 5)], [(1, 4)]]))],
     P.test_backward_invariants,
+    lambda: [P.test_jsd_decimal_entropy_form(s) for s in range(4)],
+    P.test_jsd_bounds_symmetry_and_limits,
+    P.test_jsd_two_tokens_closed_form,
 ]
 
 

@@ -38,7 +38,7 @@ def test_row_scores_without_extras_returns_the_same_values():
     y = rng.integers(0, V, size=n)
     full = O.row_scores(hs, ws, y, 2.0, ht, wt, 0.5)
     core = O.row_scores(hs, ws, y, 2.0, ht, wt, 0.5, extras=False)
-    assert set(full) - set(core) == {"kl_rev", "kl_rev_nonneg", "overlap", "kl_topk",
+    assert set(full) - set(core) == {"kl_rev", "kl_rev_nonneg", "jsd", "overlap", "kl_topk",
                                      "topk_s", "topk_t"}
     for k, v in core.items():
         np.testing.assert_array_equal(v, full[k], err_msg=k)
@@ -249,6 +249,76 @@ def test_peaked_student_limit_of_reverse_kl():
         rr = O.row_scores(hs, ws, r["argmax_s"], s, ht, wt, 1.0)
         np.testing.assert_allclose(rr["kl_rev"], -rr["logp_t"], rtol=0,
                                    atol=1e-6 * (64.0 / s) + 1e-9)
+
+
+def _decimal_entropy(logp):
+    """-sum p log p of a row given as exact decimal log-probs."""
+    return -sum((lp.exp() * lp for lp in logp), Decimal(0))
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_jsd_decimal_entropy_form(seed):
+    """JSD(p, q) = H((p + q) / 2) - (H(p) + H(q)) / 2: the entropy form of the
+    Jensen-Shannon divergence, evaluated at 50 digits from decimal logits, against the
+    oracle's sum of the two KLs to the mixture."""
+    rng = np.random.default_rng(300 + seed)
+    V = int(rng.integers(2, 17))
+    ds, dt = int(rng.integers(1, 9)), int(rng.integers(1, 9))
+    n = 3
+    hs, ht = bf16_values((n, ds), rng, 2.0), bf16_values((n, dt), rng, 2.0)
+    ws, wt = bf16_values((ds, V), rng), bf16_values((dt, V), rng)
+    sS, sT = [1.0, 4.0, 0.5, 2.0][seed], [1.0, 0.5, 4.0, 2.0][seed]
+    r = O.row_scores(hs, ws, np.zeros(n, dtype=np.int64), sS, ht, wt, sT)
+    getcontext().prec = 50
+    for i in range(n):
+        _, _, lps = decimal_row(hs[i], ws, sS)
+        _, _, lpt = decimal_row(ht[i], wt, sT)
+        m = [(a.exp() + b.exp()) / 2 for a, b in zip(lps, lpt)]
+        h_m = -sum((x * x.ln() for x in m if x > 0), Decimal(0))
+        want = h_m - (_decimal_entropy(lps) + _decimal_entropy(lpt)) / 2
+        assert abs(r["jsd"][i] - float(want)) <= 1e-13, (r["jsd"][i], float(want))
+
+
+def test_jsd_bounds_symmetry_and_limits():
+    """0 <= JSD <= ln 2; symmetric in the two models; 0 for identical models; ln 2 in
+    the limit of one-hot distributions on different tokens; and at most a quarter of
+    the symmetrised KL (each KL to the mixture is at most half the KL to the other
+    distribution, by convexity of KL in its second argument)."""
+    rng = np.random.default_rng(21)
+    n, V = 6, 400
+    hs, ht = bf16_values((n, 12), rng, 1.5), bf16_values((n, 20), rng, 1.5)
+    ws, wt = bf16_values((12, V), rng), bf16_values((20, V), rng)
+    y = np.zeros(n, dtype=np.int64)
+    r = O.row_scores(hs, ws, y, 1.0, ht, wt, 2.0)
+    assert np.all(r["jsd"] >= -1e-15) and np.all(r["jsd"] <= math.log(2.0) + 1e-15)
+    assert np.all(r["jsd"] <= 0.25 * (r["kl"] + r["kl_rev"]) + 1e-12)
+    swapped = O.row_scores(ht, wt, y, 2.0, hs, ws, 1.0)
+    np.testing.assert_allclose(swapped["jsd"], r["jsd"], rtol=1e-12, atol=1e-15)
+    same = O.row_scores(hs, ws, y, 1.0, hs, ws, 1.0)
+    assert np.all(np.abs(same["jsd"]) <= 1e-15)
+    # one-hot on different tokens: JSD -> ln 2
+    w1 = np.zeros((1, V))
+    w2 = np.zeros((1, V))
+    w1[0, 3] = 1.0
+    w2[0, 7] = 1.0
+    h = np.ones((1, 1))
+    for s, tol in ((40.0, 1e-12), (80.0, 1e-15)):
+        rr = O.row_scores(h, w1, [0], s, h, w2, s)
+        assert abs(rr["jsd"][0] - math.log(2.0)) <= tol + V * math.exp(-s) * 4, rr["jsd"][0]
+
+
+def test_jsd_two_tokens_closed_form():
+    """V = 2: with p = (a, 1 - a), q = (b, 1 - b) and the binary entropy h,
+    JSD = h((a + b) / 2) - (h(a) + h(b)) / 2."""
+    def hb(x):
+        return -(x * math.log(x) + (1 - x) * math.log(1 - x))
+    for zs, zt in ((0.3, -1.2), (2.5, 2.5), (-4.0, 1.0), (0.0, 7.0)):
+        a = 1.0 / (1.0 + math.exp(-zs))
+        b = 1.0 / (1.0 + math.exp(-zt))
+        want = hb((a + b) / 2) - 0.5 * (hb(a) + hb(b))
+        r = O.row_scores(np.ones((1, 1)), np.array([[zs, 0.0]]), [0], 1.0,
+                         np.ones((1, 1)), np.array([[zt, 0.0]]), 1.0)
+        assert abs(r["jsd"][0] - want) <= 1e-14, (zs, zt, r["jsd"][0], want)
 
 
 def test_lse_of_iid_gaussian_logits():
