@@ -52,7 +52,8 @@ typedef enum {
     OLIVE_E_RANGE = 4,       /* a value is out of range (logit scale not finite and > 0, region) */
     OLIVE_E_HIP = 5,         /* a HIP runtime call failed */
     OLIVE_E_NOMEM = 6,       /* device allocation failed at init */
-    OLIVE_E_UNSUPPORTED = 7  /* valid but not supported by this build (see each field) */
+    OLIVE_E_UNSUPPORTED = 7, /* valid but not supported by this build (see each field) */
+    OLIVE_E_LIMIT = 8        /* beyond the fixed limits of olive_kl_masked_static */
 } olive_status;
 
 typedef enum { OLIVE_F32 = 0, OLIVE_BF16 = 1 } olive_dtype;   /* of h and W; accumulate fp32 */
@@ -306,6 +307,34 @@ olive_status olive_score_backward(olive_score_ctx *ctx, const olive_batch *b,
                                   void *hip_stream);
 /* With OLIVE_GRAD_REUSE_FORWARD the backward is the logit-gradient pass and the two
  * products only: a training step's forward call supplies the normalisers. */
+
+/*
+ * olive_kl_masked without a context, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the call allocates nothing. Its per-call workspace lives in a fixed
+ * device array of 24 MiB that the library holds on each GPU it runs on until the process
+ * ends; the weights are read in place.
+ *   desc       host: as for olive_score_init, with w_layout = OLIVE_W_VD (the weights are
+ *              borrowed, not repacked), a teacher (d_teacher > 0), flags 0 or
+ *              OLIVE_FLAG_SIMPLE_KERNEL (else E_UNSUPPORTED), and the limits
+ *              max_positions <= 8192, max_seqs <= 256, vocab <= 262144 (else E_LIMIT).
+ *   w_student, w_teacher  device: [V][d_S] and [V][d_T] row-major, desc.dtype.
+ *   b and every output as in olive_kl_masked (the same values, within the same
+ *   acceptance bars: the kernels are those of olive_kl_masked).
+ * Every call on one GPU uses that GPU's one array and leaves its contents behind (each
+ * call writes what it reads, nothing needs clearing): calls that overlap on one GPU
+ * (several streams or host threads) race and must not be issued. The device error word
+ * is not reported: content errors make the affected outputs NaN as in olive_kl_masked.
+ * Each call first forms the weight-row norms that bound the rounding of the exact
+ * greedy decisions (one read of both weight matrices).
+ * Errors: E_NULL, E_DTYPE, E_SHAPE, E_RANGE, E_UNSUPPORTED, E_LIMIT, E_HIP, and the
+ * checks of olive_kl_masked on the batch.
+ */
+olive_status olive_kl_masked_static(const olive_score_desc *desc, const void *w_student,
+                                    const void *w_teacher, const olive_batch *b, float *kl,
+                                    int64_t *counts, float *logp_student, float *logp_teacher,
+                                    int32_t *argmax_student, int32_t *argmax_teacher,
+                                    float *ce_per_seq, void *hip_stream);
 
 /* Release a context and everything it owns (NULL is accepted). Synchronises the device. */
 olive_status olive_score_free(olive_score_ctx *ctx);

@@ -23,7 +23,8 @@ OLIVE_E_RANGE = 4
 OLIVE_E_HIP = 5
 OLIVE_E_NOMEM = 6
 OLIVE_E_UNSUPPORTED = 7
-STATUS_CODES = list(range(8))
+OLIVE_E_LIMIT = 8
+STATUS_CODES = list(range(9))
 
 OLIVE_F32 = 0
 OLIVE_BF16 = 1
@@ -115,6 +116,10 @@ def load() -> ctypes.CDLL:
     lib.olive_kl_masked.argtypes = [vp, ctypes.POINTER(olive_batch), f32p, i64p, f32p, f32p,
                                     i32p, i32p, f32p, vp]
     lib.olive_kl_masked.restype = st
+    lib.olive_kl_masked_static.argtypes = [ctypes.POINTER(olive_score_desc), vp, vp,
+                                           ctypes.POINTER(olive_batch), f32p, i64p, f32p, f32p,
+                                           i32p, i32p, f32p, vp]
+    lib.olive_kl_masked_static.restype = st
     lib.olive_score_batch.argtypes = [vp, ctypes.POINTER(olive_batch),
                                       ctypes.POINTER(olive_score_outputs), vp]
     lib.olive_score_batch.restype = st
@@ -216,6 +221,22 @@ def olive_kl_masked(ctx, batch: olive_batch, kl, counts=None, logp_student=None,
                                _ptr(argmax_teacher), _ptr(ce_per_seq), _stream(stream))
     if check:
         _check(s, "olive_kl_masked")
+    return s
+
+
+def olive_kl_masked_static(desc: olive_score_desc, w_student, w_teacher, batch: olive_batch,
+                           kl, counts=None, logp_student=None, logp_teacher=None,
+                           argmax_student=None, argmax_teacher=None, ce_per_seq=None,
+                           stream=None, check: bool = True) -> int:
+    """olive_kl_masked without a context ([V][d] weights read in place; nothing is
+    allocated: the library's fixed per-GPU scratch array holds the workspace)."""
+    s = load().olive_kl_masked_static(ctypes.byref(desc), _ptr(w_student), _ptr(w_teacher),
+                                      ctypes.byref(batch), _ptr(kl), _ptr(counts),
+                                      _ptr(logp_student), _ptr(logp_teacher),
+                                      _ptr(argmax_student), _ptr(argmax_teacher),
+                                      _ptr(ce_per_seq), _stream(stream))
+    if check:
+        _check(s, "olive_kl_masked_static")
     return s
 
 

@@ -36,7 +36,8 @@ __device__ __forceinline__ void queue_row(const ScoreArgs &a, const int32_t *__r
         if (hh == 0.f) continue;
         const float theta = __int_as_float(flagged[4 * f + 2 + m]);
         const float delta =
-            (float)d * 0x1p-23f * (sqrtf(hh) * (1.0f + 0x1p-10f)) * (m ? a.wmax_t : a.wmax_s);
+            (float)d * 0x1p-23f * (sqrtf(hh) * (1.0f + 0x1p-10f)) *
+            (a.wmax_dev ? a.wmax_dev[m] : (m ? a.wmax_t : a.wmax_s));
         const float thr = theta - delta;
         // lane s < ns: split s's maximum, second value and argmax for this row
         const int fb = m ? F_BEST_T : F_BEST_S;

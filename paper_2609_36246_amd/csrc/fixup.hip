@@ -295,6 +295,27 @@ fixup_merge_kernel(ScoreArgs a, const int32_t *__restrict__ flagged, int f_base,
     }
 }
 
+// out[0] = (1 + 2^-10) max_v wn[v]: the largest weight-row norm with the margin the
+// rounding bounds use (one workgroup; max is exact in any order).
+__global__ void __launch_bounds__(1024)
+max_norm_kernel(const float *__restrict__ wn, int64_t V, float *__restrict__ out) {
+    __shared__ float red[1024];
+    float m = 0.f;
+    for (int64_t v = threadIdx.x; v < V; v += 1024) m = fmaxf(m, wn[v]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    for (int off = 512; off > 0; off >>= 1) {
+        if ((int)threadIdx.x < off) red[threadIdx.x] = fmaxf(red[threadIdx.x], red[threadIdx.x + off]);
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) out[0] = red[0] * (1.0f + 0x1p-10f);
+}
+
+hipError_t launch_max_norm(const float *wn, int64_t V, float *out, hipStream_t st) {
+    max_norm_kernel<<<1, 1024, 0, st>>>(wn, V, out);
+    return hipGetLastError();
+}
+
 hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *out,
                             hipStream_t st) {
     const int64_t blocks = (V + 3) / 4 < 4096 ? (V + 3) / 4 : 4096;

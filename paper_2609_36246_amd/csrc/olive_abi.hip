@@ -6,12 +6,19 @@
 #include <cmath>
 #include <cstddef>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
 #include "olive_internal.hpp"
 
 using namespace olive;
+
+// Scratch of olive_kl_masked_static (one copy per GPU, held until the process ends). In
+// host code this name is a host-side stand-in, not a device address: each GPU's copy is
+// reached through the address hipGetSymbolAddress returns for it.
+constexpr size_t kStaticScratchBytes = (size_t)24 << 20;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
 
 struct olive_score_ctx {
     olive_score_desc desc;
@@ -32,6 +39,7 @@ struct olive_score_ctx {
     void *fx_scratch = nullptr;
     float *wn_s = nullptr, *wn_t = nullptr;     // weight-row L2 norms (rounding bounds)
     float wmax_s = 0.f, wmax_t = 0.f;           // their maxima
+    const float *wmax_dev = nullptr;            // or the maxima in device memory
     int32_t *err = nullptr;
     void *tk_buf = nullptr;                     // top-K workspace (OLIVE_FLAG_TOPK)
     TopkWork tkw = {};
@@ -82,6 +90,32 @@ void release(olive_score_ctx *c) {
 }
 
 bool finite_positive(float x) { return std::isfinite(x) && x > 0.f; }
+
+// Host checks of a descriptor (init and the no-allocation entry point).
+olive_status check_desc(const olive_score_desc &d) {
+    if (d.dtype != OLIVE_F32 && d.dtype != OLIVE_BF16) return OLIVE_E_DTYPE;
+    if (d.w_layout != OLIVE_W_DV && d.w_layout != OLIVE_W_VD) return OLIVE_E_DTYPE;
+    if (d.vocab < 1 || d.vocab >= (int64_t)1 << 31) return OLIVE_E_SHAPE;
+    if (d.d_student < 1 || d.d_teacher < 0) return OLIVE_E_SHAPE;
+    if (d.max_positions < 1 || d.max_positions >= ((int64_t)1 << 31) - 1) return OLIVE_E_SHAPE;
+    if (d.max_seqs < 1) return OLIVE_E_SHAPE;
+    if (d.d_student > 12288 || d.d_teacher > 12288) return OLIVE_E_UNSUPPORTED;
+    if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
+    if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
+    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK |
+                    OLIVE_FLAG_BACKWARD))
+        return OLIVE_E_RANGE;
+    return OLIVE_OK;
+}
+
+// Whether the bf16 MFMA kernel applies to a context of this descriptor and weights.
+bool mfma_applies(const olive_score_desc &d, const void *w_student, const void *w_teacher) {
+    const bool has_t = d.d_teacher > 0;
+    return d.dtype == OLIVE_BF16 && (d.d_student % 64 == 0) && (d.d_teacher % 64 == 0) &&
+           d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL) &&
+           (d.w_layout == OLIVE_W_DV ||      // borrowed weights: 16-byte rows
+            (((uintptr_t)w_student & 15) == 0 && (!has_t || ((uintptr_t)w_teacher & 15) == 0)));
+}
 
 // The batch (and spans) a call was given are those of the recorded forward call: the same
 // sizes, region and device pointers.
@@ -211,6 +245,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     a.cT = a.sT * 1.4426950408889634f;
     a.wmax_s = ctx->wmax_s;
     a.wmax_t = ctx->wmax_t;
+    a.wmax_dev = ctx->wmax_dev;
     const bool same_scale = has_t && (a.sS == a.sT);
 
     const int slot = (int)(ctx->n_calls % 64);
@@ -326,6 +361,7 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     a.cT = a.sT * 1.4426950408889634f;
     a.wmax_s = ctx->wmax_s;
     a.wmax_t = ctx->wmax_t;
+    a.wmax_dev = ctx->wmax_dev;
     const bool same_scale = has_t && (a.sS == a.sT);
     const float *lse = ctx->fwd_lse;
     if (!reuse) {
@@ -418,9 +454,124 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     return OLIVE_OK;
 }
 
+// ---------------------------------------------------------------------------------
+// Scratch of olive_kl_masked_static: one fixed device array per GPU, so that the call
+// allocates nothing. Limits: positions, sequences and vocabulary of a call.
+constexpr int64_t kStaticMaxPositions = 8192;
+constexpr int32_t kStaticMaxSeqs = 256;
+constexpr int64_t kStaticMaxVocab = 262144;
+constexpr int kStaticFxWindow = 512;              // generic path: flagged rows per window
+
+struct StaticDevice {
+    bool ready = false;
+    char *base = nullptr;      // this device's copy of `scratch`
+    int n_cu = 0;
+};
+constexpr int kStaticDevices = 64;
+StaticDevice g_static[kStaticDevices];
+std::mutex g_static_mu;
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+// Once per device, with that device current: the address of its copy of the scratch
+// array and its compute-unit count.
+olive_status static_setup(int dev, StaticDevice **out) {
+    if (dev < 0 || dev >= kStaticDevices) return OLIVE_E_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    StaticDevice &s = g_static[dev];
+    if (!s.ready) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return OLIVE_E_HIP;
+        int n_cu = 0;
+        if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) !=
+                hipSuccess || n_cu < 1)
+            return OLIVE_E_HIP;
+        s.base = (char *)p;
+        s.n_cu = n_cu;
+        s.ready = true;
+    }
+    *out = &s;
+    return OLIVE_OK;
+}
+
+// Lays the per-call workspace of a context out in a device's scratch array (the limits'
+// sizes); false when it would not fit.
+bool static_carve(olive_score_ctx *c, char *base) {
+    const int64_t P = kStaticMaxPositions;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        char *p = base + off;
+        off += align256(bytes);
+        return p;
+    };
+    c->sched = (Sched *)take(sizeof(Sched));
+    c->err = (int32_t *)take(sizeof(int32_t));
+    c->wmax_dev = (const float *)take(2 * sizeof(float));
+    c->seqbuf = (int32_t *)take((size_t)seqbuf_entries(kStaticMaxSeqs) * sizeof(int32_t));
+    c->rowmap = (uint32_t *)take((size_t)P * sizeof(uint32_t));
+    c->pstride = (P + 255) / 256 * 256;
+    c->part = (float *)take((size_t)NFIELDS * MAX_SPLITS * c->pstride * sizeof(float));
+    c->logp_tmp = (float *)take((size_t)P * sizeof(float));
+    c->flag_cap = (int)P;
+    c->flagged = (int32_t *)take((size_t)4 * P * sizeof(int32_t));
+    c->fx_buf = take(filter_queue_bytes(P, FX_CCAP));
+    c->fx_window = kStaticFxWindow;
+    c->fx_scratch = take((size_t)kStaticFxWindow * fixup_chunks(kStaticMaxVocab) * 2 *
+                         fixup_result_bytes());
+    c->wn_s = (float *)take((size_t)kStaticMaxVocab * sizeof(float));
+    c->wn_t = (float *)take((size_t)kStaticMaxVocab * sizeof(float));
+    if (off > kStaticScratchBytes) return false;
+    c->fxq = filter_queue_carve(c->fx_buf, c->flag_cap, FX_CCAP, &c->sched->n_fxq[0],
+                                &c->sched->n_fx_fb);
+    c->fxq.smask = &c->sched->fx_smask[0];
+    return true;
+}
+
 }  // namespace
 
 extern "C" {
+
+olive_status olive_kl_masked_static(const olive_score_desc *desc, const void *w_student,
+                                    const void *w_teacher, const olive_batch *b, float *kl,
+                                    int64_t *counts, float *logp_student, float *logp_teacher,
+                                    int32_t *argmax_student, int32_t *argmax_teacher,
+                                    float *ce_per_seq, void *hip_stream) {
+    if (!desc || !b || !kl) return OLIVE_E_NULL;
+    const olive_score_desc &d = *desc;
+    if (olive_status e = check_desc(d)) return e;
+    // borrowed [V][d] weights only (a repacked copy would need memory); no per-context
+    // options (timing, top-K, backward workspaces)
+    if (d.w_layout != OLIVE_W_VD || (d.flags & ~OLIVE_FLAG_SIMPLE_KERNEL) || d.d_teacher == 0)
+        return OLIVE_E_UNSUPPORTED;
+    if (!w_student || !w_teacher) return OLIVE_E_NULL;
+    if (d.max_positions > kStaticMaxPositions || d.max_seqs > kStaticMaxSeqs ||
+        d.vocab > kStaticMaxVocab)
+        return OLIVE_E_LIMIT;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return OLIVE_E_HIP;
+    StaticDevice *sd = nullptr;
+    if (olive_status e = static_setup(dev, &sd)) return e;
+    olive_score_ctx c;   // host-side description of this call only (nothing is allocated)
+    c.desc = d;
+    c.device = dev;
+    c.n_cu = sd->n_cu;
+    c.ws = w_student;
+    c.wt = w_teacher;
+    c.bf16 = d.dtype == OLIVE_BF16;
+    c.has_t = true;
+    c.mfma_ok = mfma_applies(d, w_student, w_teacher);
+    if (!static_carve(&c, sd->base)) return OLIVE_E_LIMIT;
+    hipStream_t st = (hipStream_t)hip_stream;
+    // the weight-row norms and their maxima bound the rounding of the near-tie decisions
+    float *wmax = const_cast<float *>(c.wmax_dev);
+    if (launch_row_norms(c.ws, d.vocab, d.d_student, c.bf16, c.wn_s, st) != hipSuccess ||
+        launch_row_norms(c.wt, d.vocab, d.d_teacher, c.bf16, c.wn_t, st) != hipSuccess ||
+        launch_max_norm(c.wn_s, d.vocab, wmax, st) != hipSuccess ||
+        launch_max_norm(c.wn_t, d.vocab, wmax + 1, st) != hipSuccess)
+        return OLIVE_E_HIP;
+    return run(&c, b, nullptr, kl, nullptr, counts, logp_student, logp_teacher, argmax_student,
+               argmax_teacher, ce_per_seq, st);
+}
 
 const char *olive_status_string(olive_status s) {
     // A C caller may pass any int: read the argument's bytes rather than the enum value
@@ -437,6 +588,9 @@ const char *olive_status_string(olive_status s) {
         case OLIVE_E_HIP: return "OLIVE_E_HIP: a HIP runtime call failed";
         case OLIVE_E_NOMEM: return "OLIVE_E_NOMEM: device allocation failed";
         case OLIVE_E_UNSUPPORTED: return "OLIVE_E_UNSUPPORTED: not supported by this context";
+        case OLIVE_E_LIMIT:
+            return "OLIVE_E_LIMIT: beyond the fixed limits of olive_kl_masked_static "
+                   "(positions, sequences or vocabulary)";
     }
     return "OLIVE: unknown status";
 }
@@ -446,18 +600,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
     if (!out || !desc) return OLIVE_E_NULL;
     *out = nullptr;
     const olive_score_desc &d = *desc;
-    if (d.dtype != OLIVE_F32 && d.dtype != OLIVE_BF16) return OLIVE_E_DTYPE;
-    if (d.w_layout != OLIVE_W_DV && d.w_layout != OLIVE_W_VD) return OLIVE_E_DTYPE;
-    if (d.vocab < 1 || d.vocab >= (int64_t)1 << 31) return OLIVE_E_SHAPE;
-    if (d.d_student < 1 || d.d_teacher < 0) return OLIVE_E_SHAPE;
-    if (d.max_positions < 1 || d.max_positions >= ((int64_t)1 << 31) - 1) return OLIVE_E_SHAPE;
-    if (d.max_seqs < 1) return OLIVE_E_SHAPE;
-    if (d.d_student > 12288 || d.d_teacher > 12288) return OLIVE_E_UNSUPPORTED;
-    if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
-    if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
-    if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK |
-                    OLIVE_FLAG_BACKWARD))
-        return OLIVE_E_RANGE;
+    if (olive_status e = check_desc(d)) return e;
     if (!w_student) return OLIVE_E_NULL;
     if (d.d_teacher > 0 && !w_teacher) return OLIVE_E_NULL;
 
@@ -473,11 +616,7 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         release(c);
         return OLIVE_E_HIP;
     }
-    c->mfma_ok = c->bf16 && (d.d_student % 64 == 0) && (d.d_teacher % 64 == 0) &&
-                 d.vocab >= 256 && !(d.flags & OLIVE_FLAG_SIMPLE_KERNEL) &&
-                 (d.w_layout == OLIVE_W_DV ||      // borrowed weights: 16-byte rows
-                  (((uintptr_t)w_student & 15) == 0 &&
-                   (!c->has_t || ((uintptr_t)w_teacher & 15) == 0)));
+    c->mfma_ok = mfma_applies(d, w_student, w_teacher);
     c->topk = (d.flags & OLIVE_FLAG_TOPK) != 0;
     if (c->topk && (!c->mfma_ok || !c->has_t || d.vocab < 512 ||
                     d.vocab > (int64_t)MAX_SPLITS * 1024 * MFMA_BV)) {

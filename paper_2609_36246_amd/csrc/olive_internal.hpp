@@ -121,6 +121,8 @@ struct ScoreArgs {
     float cS, cT;                // s * log2(e)
     float sS, sT;                // logit scales
     float wmax_s, wmax_t;        // largest weight-row L2 norm (top-K rounding bounds)
+    const float *wmax_dev;       // device [2]: the same two values formed on the device
+                                 // (used instead of wmax_s / wmax_t when set)
 };
 
 // Logit-gradient pass of the backward (scored rows [c0, c0 + chunk) of a call).
@@ -210,6 +212,7 @@ hipError_t launch_fixup_impl(const ScoreArgs &a, bool bf16, const int32_t *flagg
                              int32_t *am_s, int32_t *am_t, hipStream_t st);
 hipError_t launch_row_norms(const void *w, int64_t V, int d, bool bf16, float *out,
                             hipStream_t st);
+hipError_t launch_max_norm(const float *wn, int64_t V, float *out, hipStream_t st);
 int fixup_chunks(int64_t V);
 size_t fixup_result_bytes();
 hipError_t launch_ce(const olive_batch &b, const olive_spans *spans, const int32_t *seqbuf,

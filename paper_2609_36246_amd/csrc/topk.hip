@@ -124,7 +124,7 @@ topk_select_kernel(ScoreArgs a, TopkWork w) {
             z16 = bv;
         }
         const float delta = (float)d * 0x1p-23f * (sqrtf(hh) * (1.0f + 0x1p-10f)) *
-                            (m ? a.wmax_t : a.wmax_s);
+                            (a.wmax_dev ? a.wmax_dev[m] : (m ? a.wmax_t : a.wmax_s));
         const float thr = (float)z16 - 2.f * delta;
         // every logit that can reach the exact top-16 is listed unless a floor reaches
         // thr (a floor or threshold that is not finite queues the pair as well)

@@ -55,7 +55,7 @@ static olive_status init_with(const olive_score_desc *d) {
 
 int main(void) {
     /* status strings: every code, and an unknown one */
-    for (int c = OLIVE_OK; c <= OLIVE_E_UNSUPPORTED; ++c) {
+    for (int c = OLIVE_OK; c <= OLIVE_E_LIMIT; ++c) {
         const char *s = olive_status_string((olive_status)c);
         CHECK(s != NULL && strncmp(s, "OLIVE_", 6) == 0);
     }
@@ -124,6 +124,42 @@ int main(void) {
     CHECK(olive_score_last_stats(NULL, stats) == OLIVE_E_NULL);
     CHECK(olive_score_kernel_times(NULL, f, 1) == OLIVE_E_NULL);
     CHECK(olive_score_free(NULL) == OLIVE_OK);
+
+    /* the no-allocation entry point: host checks before any device call */
+    d = good_desc();
+    d.w_layout = OLIVE_W_VD;
+    CHECK(olive_kl_masked_static(NULL, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                 NULL) == OLIVE_E_NULL);
+    CHECK(olive_kl_masked_static(&d, dev_w, dev_w, &b, NULL, NULL, NULL, NULL, NULL, NULL, NULL,
+                                 NULL) == OLIVE_E_NULL);
+    CHECK(olive_kl_masked_static(&d, NULL, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                 NULL) == OLIVE_E_NULL);
+    {
+        olive_score_desc e = d; e.w_layout = OLIVE_W_DV;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_UNSUPPORTED);
+        e = d; e.flags = OLIVE_FLAG_KERNEL_TIMING;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_UNSUPPORTED);
+        e = d; e.d_teacher = 0;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_UNSUPPORTED);
+        e = d; e.max_positions = 8193;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_LIMIT);
+        e = d; e.vocab = 262145;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_LIMIT);
+        e = d; e.max_seqs = 257;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_LIMIT);
+        e = d; e.dtype = 9;
+        CHECK(olive_kl_masked_static(&e, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                     NULL) == OLIVE_E_DTYPE);
+    }
+    /* within every limit: without a device the call fails in the HIP runtime */
+    CHECK(olive_kl_masked_static(&d, dev_w, dev_w, &b, f, NULL, NULL, NULL, NULL, NULL, NULL,
+                                 NULL) == OLIVE_E_HIP);
 
     if (n_failed) {
         fprintf(stderr, "%d of %d checks failed\n", n_failed, n_checks);

@@ -2,9 +2,10 @@
 UndefinedBehaviorSanitizer (no GPU needed).
 
 tests/abi_host_check.c drives every host rejection path of include/olive_score.h
-(malformed descriptors, NULL pointers and contexts, and an init that fails in the
-HIP runtime and must free its partly built context). It is linked against the ABI
-source built for the host only with both sanitizers, and against the library's other
+(malformed descriptors, NULL pointers and contexts, the limits of the no-allocation
+entry point, and an init that fails in the HIP runtime and must free its partly built
+context). It is linked against the ABI source built with both sanitizers on its host
+code, and against the library's other
 objects as built by paper_2609_36246_amd/build.py; any invalid access or undefined
 behaviour on those paths aborts the program.
 """
@@ -41,7 +42,7 @@ def test_host_argument_checks_under_asan_and_ubsan(tmp_path):
         build.build()
     inc = ["-I", os.path.join(ROOT, "include"), "-I", CSRC]
     abi_o = str(tmp_path / "olive_abi_san.o")
-    subprocess.run([hipcc, "--offload-host-only", "-O1", "-g", "-std=c++17", "-fPIC"] + SAN +
+    subprocess.run([hipcc, "--offload-arch=gfx950", "-O1", "-g", "-std=c++17", "-fPIC"] + SAN +
                    inc + ["-c", os.path.join(CSRC, "olive_abi.hip"), "-o", abi_o], check=True)
     drv_o = str(tmp_path / "abi_host_check.o")
     subprocess.run([clang, "-O1", "-g", "-std=c11"] + SAN[1::2] + inc +
