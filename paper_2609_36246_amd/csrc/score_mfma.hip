@@ -29,6 +29,7 @@
 // across position tiles through L2 and the infinity cache, H tiles across splits.
 #include <hip/hip_runtime.h>
 
+#include "fold.hpp"
 #include "mfma_pipe.hpp"
 #include "olive_device.hpp"
 #include "olive_internal.hpp"
@@ -41,27 +42,11 @@ namespace olive {
 #define OLIVE_SPLIT_GROUP 4
 #endif
 
-// Logit of vocabulary rows outside the tile range: -2^99. A power of two, so that
-// kMasked * c is exact and a block whose running max is kMasked folds to exp2(0) = 1
-// rather than to the rounding residual of the product; z + kMasked rounds back to
-// exactly kMasked for any |z| < 2^74, in both models (their difference is 0).
-constexpr float kMasked = -0x1p99f;
-
-// max(a, b) for non-NaN operands as one v_med3_f32 (no NaN canonicalisation).
-__device__ __forceinline__ float max2(float a, float b) {
-    return __builtin_amdgcn_fmed3f(a, b, __builtin_inff());
-}
-
 struct Lane {
     int lane, wid, wv, wt, h, l32;
     int ldsoff[4];          // operand fetch offsets for the four k16 sub-steps
     uint32_t wvoff[2][2];   // per model, per W DMA parity: lane part of row * rowbytes + chunk * 16
     const char *hp[2][H_DMA];   // per model, per H DMA: pointer to the row chunk
-};
-
-struct Run {                // running statistics of one position column
-    float best, sec, z;
-    int idx;
 };
 
 // The largest logits a lane keeps of one position column (4), as packed keys in
@@ -338,52 +323,6 @@ struct Kernel {
 #undef OLIVE_STEPS
     }
 
-    // Fold one 32-row block (16 values per lane: rows 8*(r/4) + 4*h + r%4 of block
-    // vb, column cb) into a model's running statistics. With DIFF, also the sum of
-    // the block's exp weights times the logit difference to the other model
-    // (z - o with equal scales, s_self z - s_other o otherwise) into Aacc: the
-    // teacher's forms the forward KL, the student's the reverse one.
-    template <bool DIFF>
-    static __device__ __forceinline__ void fold_block(const float (&z)[16], Run &R, float &Aacc,
-                                                      const float (&o)[16], float c, float s_self,
-                                                      float s_other, int vcode0) {
-        float tm = R.best, ts = R.sec;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            ts = __builtin_amdgcn_fmed3f(z[r], tm, ts);
-            tm = max2(tm, z[r]);
-        }
-        // Branch-free: lowest row of this block equal to the new max (used only when
-        // the block raised the max), and the rescale of the running sums (1 when not).
-        int code = 0;
-#pragma unroll
-        for (int r = 15; r >= 0; --r) code = (z[r] == tm) ? 8 * (r >> 2) + (r & 3) : code;
-        const bool up = tm > R.best;
-        const float resc = fast_exp2((R.best - tm) * c);
-        R.z *= resc;
-        if (DIFF) Aacc *= resc;
-        R.idx = up ? vcode0 + code : R.idx;
-        R.best = tm;
-        R.sec = ts;
-        const float mneg = -tm * c;
-        float zsum = 0.f, asum = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            const float e = fast_exp2(fmaf(z[r], c, mneg));
-            zsum += e;
-            if (DIFF) {
-                float dlt;
-                {
-#pragma clang fp contract(off)
-                    dlt = SAME ? (z[r] - o[r]) : (s_self * z[r] - s_other * o[r]);
-                }
-                asum = fmaf(e, dlt, asum);
-            }
-        }
-        R.z += zsum;
-        if (DIFF) Aacc += asum;
-    }
-
     // Add kMasked to the rows of a shifted last tile whose vocabulary index is below
     // vlo, with one MFMA per block (A: kMasked in k = 0 of masked rows, B: ones), so the
     // accumulators are only ever touched by MFMAs.
@@ -431,9 +370,10 @@ struct Kernel {
                     zs[r] = agpr_read(accS[vb][cb][r]);
                     if (HAS_T) zt[r] = agpr_read(accT[vb][cb][r]);
                 }
-                fold_block<HAS_T && REV>(zs, RS[cb], Bq[cb], zt, a.cS, a.sS, a.sT, vbase + vb * 32);
+                fold_block<HAS_T && REV, SAME>(zs, RS[cb], Bq[cb], zt, a.cS, a.sS, a.sT,
+                                                 vbase + vb * 32);
                 if (HAS_T)
-                    fold_block<true>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
+                    fold_block<true, SAME>(zt, RT[cb], A[cb], zs, a.cT, a.sT, a.sS, vbase + vb * 32);
                 if (LISTS) {
                     const uint32_t tie0 = 0xFFFFu - (uint32_t)(lvt * 64 + vb * 16);
                     topk_block(zs, KS[cb], tie0);
@@ -497,13 +437,6 @@ struct Kernel {
                 accS[vb][cb] = floatx16{0.f};
                 if (HAS_T) accT[vb][cb] = floatx16{0.f};
             }
-    }
-
-    static __device__ __forceinline__ void merge_run(Run &x, float &xa, const Run &y, float ya,
-                                                     float c) {
-        Stat a{x.best, x.sec, x.idx, x.z}, b{y.best, y.sec, y.idx, y.z};
-        stat_merge(a, xa, b, ya, c);
-        x.best = a.best; x.sec = a.sec; x.idx = a.idx; x.z = a.z;
     }
 
     static __device__ __forceinline__ void run(ScoreArgs a) {
