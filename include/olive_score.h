@@ -100,8 +100,8 @@ typedef struct {
 #define OLIVE_FLAG_TOPK 4
 /* Reserve the workspace of olive_score_backward. Needs a bf16 context on which the
  * MFMA kernel applies (else init returns E_UNSUPPORTED). The workspace holds about
- * 4 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
- * (5.6 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
+ * 2 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
+ * (3.1 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
 #define OLIVE_FLAG_BACKWARD 8
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */

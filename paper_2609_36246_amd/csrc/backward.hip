@@ -48,6 +48,33 @@ gather_t_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restric
     }
 }
 
+// Zeros in rows [rows, rows rounded up to 64) of every panel of dz_t ([np][chunk][64]
+// bf16), rows = the chunk's scored rows (on the device): the K padding the dL/dW product
+// reads in its last K step. One 16-byte piece per lane.
+__global__ void __launch_bounds__(256)
+zero_tail_kernel(uint16_t *__restrict__ dzt, int np, int chunk, const Sched *__restrict__ sched,
+                 int c0) {
+    const int t_all = sched->t_valid - c0;
+    const int rows = t_all < 0 ? 0 : (t_all < chunk ? t_all : chunk);
+    const int pad = ((rows + 63) / 64) * 64 - rows;   // rows to clear per panel
+    const int64_t n = (int64_t)np * pad * 8;           // 16-byte pieces
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * 256) {
+        const int64_t p = i / (pad * 8);
+        const int r = rows + (int)((i / 8) % pad), c = (int)(i % 8);
+        *(uint4 *)(dzt + ((p * chunk + r) * 64 + c * 8)) = make_uint4(0, 0, 0, 0);
+    }
+}
+
+hipError_t launch_zero_tail(uint16_t *dzt, int64_t vp, int chunk, const Sched *sched, int c0,
+                            hipStream_t st) {
+    const int np = (int)(vp / 64);
+    const int64_t most = (int64_t)np * 63 * 8;         // pieces for the widest padding
+    const int64_t blocks = (most + 255) / 256 < 2048 ? (most + 255) / 256 : 2048;
+    zero_tail_kernel<<<(unsigned)blocks, 256, 0, st>>>(dzt, np, chunk, sched, c0);
+    return hipGetLastError();
+}
+
 __global__ void __launch_bounds__(256) fill_zero_kernel(float4 *__restrict__ p, int64_t n4) {
     for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n4;
          i += (int64_t)gridDim.x * 256)

@@ -28,6 +28,10 @@ namespace {
 struct GLane {
     int lane, wid, wv, wt, h, l32;
     int ldsoff[4];
+    // K-major A (transposed panels): per lane, the byte offsets of its transpose reads
+    // within a stage, for the read of K rows 0..3 or 4..7 of its half (r) and for even or
+    // odd 32-row blocks (parity); the block pair and the sub-step add constants
+    uint32_t troff[2][2];
     // the tile's first A and B rows (wave-uniform) and, per DMA, the lane's row chunk
     // as a 32-bit offset from them: the K offset is added to the bases in scalar
     // registers, the lane part inside the load
@@ -66,13 +70,39 @@ __device__ __forceinline__ void g_issue(const GLane &L, int st, int kk) {
     g_dmas<0, DMA_PER_STEP>(L, la, lb, kk);
 }
 
-template <int SUB>
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// One ds_read_b64_tr_b16 at byte offset off of the ring. In each group of 16 lanes, lane
+// j supplies 4 consecutive 16-bit values M[j][0..3] (8 bytes at its address) and lane i
+// receives M[i/4][i%4], M[i/4 + 4][i%4], M[i/4 + 8][i%4], M[i/4 + 12][i%4].
+__device__ __forceinline__ i16x4 tr_read(uint32_t off) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_i16x4 *)((__attribute__((address_space(3))) char *)(lds_void *)g_ring + off));
+}
+
+template <int SUB, bool ATR>
 __device__ __forceinline__ void g_read(const GLane &L, int st, GFrag &F) {
     const char *stage = g_ring + st * STAGE_BYTES;
-    const char *ab = stage + L.wv * 128 * ROWB + L.ldsoff[SUB];
     const char *bb = stage + WT_BYTES + L.wt * 64 * ROWB + L.ldsoff[SUB];
+    if constexpr (ATR) {
+        // 32-row block vb of the wave = panel 2 wv + vb / 2, columns 32 (vb % 2) ..: two
+        // transpose reads give the lane K rows 16 SUB + 8 h + 0..3 and + 4..7 of its row
+        const uint32_t sb = (uint32_t)st * STAGE_BYTES;
 #pragma unroll
-    for (int vb = 0; vb < 4; ++vb) F.A[vb] = *(const bf16x8 *)(ab + vb * 32 * ROWB);
+        for (int vb = 0; vb < 4; ++vb) {
+            constexpr int kq = SUB * 16 * ROWB;
+            const uint32_t bo = sb + (uint32_t)((vb >> 1) * 64 * ROWB + kq);
+            const i16x4 lo = tr_read(L.troff[0][vb & 1] + bo);
+            const i16x4 hi = tr_read(L.troff[1][vb & 1] + bo);
+            const i16x4 both[2] = {lo, hi};
+            F.A[vb] = __builtin_bit_cast(bf16x8, both);
+        }
+    } else {
+        const char *ab = stage + L.wv * 128 * ROWB + L.ldsoff[SUB];
+#pragma unroll
+        for (int vb = 0; vb < 4; ++vb) F.A[vb] = *(const bf16x8 *)(ab + vb * 32 * ROWB);
+    }
 #pragma unroll
     for (int cb = 0; cb < 2; ++cb) F.B[cb] = *(const bf16x8 *)(bb + cb * 32 * ROWB);
 }
@@ -123,7 +153,7 @@ __device__ __forceinline__ void g_arrive() {
 // One step in stage st: barrier, refill the stage of step n-1 with step pk (n+2,
 // saturated at the last step), run the four k16 sub-steps; the last one's fragments
 // stay pending in P.
-template <bool PEND>
+template <bool PEND, bool ATR>
 __device__ __forceinline__ void g_step(const GLane &L, int st, int pk, floatx16 (&acc)[4][2],
                                        GFrag &P) {
     const int pv = st == 0 ? NST - 1 : st - 1;
@@ -133,27 +163,27 @@ __device__ __forceinline__ void g_step(const GLane &L, int st, int pk, floatx16 
     const uint32_t lb = base + WT_BYTES + (uint32_t)L.wid * (H_DMA * 1024u);
     const int off = pk;   // K step of the refill
     GFrag F0, F1, F2;
-    g_read<0>(L, st, F0);
+    g_read<0, ATR>(L, st, F0);
     __builtin_amdgcn_sched_barrier(0);
     if (PEND) {
         g_mma_issue<0>(P, acc, L, la, lb, off);
-        g_read<1>(L, st, F1);
+        g_read<1, ATR>(L, st, F1);
         __builtin_amdgcn_sched_barrier(0);
         g_mma_issue<4>(F0, acc, L, la, lb, off);
-        g_read<2>(L, st, F2);
+        g_read<2, ATR>(L, st, F2);
         __builtin_amdgcn_sched_barrier(0);
         g_mma_issue<8>(F1, acc, L, la, lb, off);
-        g_read<3>(L, st, P);
+        g_read<3, ATR>(L, st, P);
         __builtin_amdgcn_sched_barrier(0);
         g_mma(F2, acc);
     } else {
-        g_read<1>(L, st, F1);
+        g_read<1, ATR>(L, st, F1);
         __builtin_amdgcn_sched_barrier(0);
         g_mma_issue<0>(F0, acc, L, la, lb, off);
-        g_read<2>(L, st, F2);
+        g_read<2, ATR>(L, st, F2);
         __builtin_amdgcn_sched_barrier(0);
         g_mma_issue<4>(F1, acc, L, la, lb, off);
-        g_read<3>(L, st, P);
+        g_read<3, ATR>(L, st, P);
         __builtin_amdgcn_sched_barrier(0);
         g_mma_issue<8>(F2, acc, L, la, lb, off);
     }
@@ -185,6 +215,7 @@ __device__ __forceinline__ int dev_count(const int32_t *p, int off, int cap, int
 
 }  // namespace
 
+template <bool ATR>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 gemm_mfma_kernel(GemmArgs g) {
     const int M = g.M;
@@ -205,6 +236,20 @@ gemm_mfma_kernel(GemmArgs g) {
     L.l32 = L.lane & 31;
 #pragma unroll
     for (int s = 0; s < 4; ++s) L.ldsoff[s] = L.l32 * ROWB + (((2 * s + L.h) ^ swz(L.l32)) << 4);
+    if (ATR) {
+        // stage row R = 64 (panel in tile) + K row; lane j of 16-lane group gq supplies
+        // K row 8 h + 4 r + j / 4 at columns 32 par + 16 (gq % 2) + 4 (j % 4) .. + 3, so
+        // that lane i of the group receives column 16 (gq % 2) + i, K rows +0 .. +3
+        const int gq = L.lane >> 4, j = L.lane & 15;
+#pragma unroll
+        for (int r = 0; r < 2; ++r)
+#pragma unroll
+            for (int par = 0; par < 2; ++par) {
+                const int R = 2 * L.wv * 64 + 8 * L.h + 4 * r + (j >> 2);
+                const int c = 32 * par + 16 * (gq & 1) + 4 * (j & 3);
+                L.troff[r][par] = (uint32_t)(R * ROWB + (((c >> 3) ^ swz(R)) << 4) + (c & 7) * 2);
+            }
+    }
     const int G = gridDim.x;
     const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
     const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
@@ -219,16 +264,32 @@ gemm_mfma_kernel(GemmArgs g) {
         // A DMA i of wave wid fills stage rows R = wid*64 + 8i + lane/8, slot lane&7
         // with chunk (lane&7) ^ swz(R); B DMA i rows R = wid*32 + 8i + lane/8. Rows
         // past M (N) read the last one; offsets stay below 256 row pitches.
-        L.abase = g.A + (int64_t)m0 * g.lda;
         L.bbase = g.B + (int64_t)n0 * g.ldb;
-        L.ak = g.akstep;
         L.bk = g.bkstep;
+        if (ATR) {
+            // wave wid loads panel m0 / 64 + wid (the last one for panels past M): its 64
+            // K rows of the step, 8 KB contiguous
+            const int p0 = m0 / 64;
+            const int pw = p0 + L.wid < g.a_panels ? L.wid : g.a_panels - 1 - p0;
+            L.abase = g.A + (int64_t)p0 * g.a_prows * ROWB;
+            L.ak = 64 * ROWB;
 #pragma unroll
-        for (int i = 0; i < W_DMA; ++i) {
-            const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
-            const int ch = (L.lane & 7) ^ swz(R);
-            const int r = m0 + R < M ? R : M - 1 - m0;
-            L.aoff[i] = (uint32_t)((int64_t)r * g.lda + ch * 16);
+            for (int i = 0; i < W_DMA; ++i) {
+                const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
+                const int ch = (L.lane & 7) ^ swz(R);
+                L.aoff[i] = (uint32_t)(((int64_t)pw * g.a_prows + 8 * i + (L.lane >> 3)) * ROWB +
+                                       ch * 16);
+            }
+        } else {
+            L.abase = g.A + (int64_t)m0 * g.lda;
+            L.ak = g.akstep;
+#pragma unroll
+            for (int i = 0; i < W_DMA; ++i) {
+                const int R = L.wid * 8 * W_DMA + 8 * i + (L.lane >> 3);
+                const int ch = (L.lane & 7) ^ swz(R);
+                const int r = m0 + R < M ? R : M - 1 - m0;
+                L.aoff[i] = (uint32_t)((int64_t)r * g.lda + ch * 16);
+            }
         }
 #pragma unroll
         for (int i = 0; i < H_DMA; ++i) {
@@ -249,11 +310,11 @@ gemm_mfma_kernel(GemmArgs g) {
             g_issue(L, 1, kb + (kn > 1 ? 1 : 0));
             int st = 0;
             GFrag P;
-            g_step<false>(L, st, kb + (2 < kn ? 2 : kn - 1), acc, P);
+            g_step<false, ATR>(L, st, kb + (2 < kn ? 2 : kn - 1), acc, P);
             st = 1;
             for (int n = 1; n < kn; ++n) {
                 const int pk = kb + (n + 2 < kn ? n + 2 : kn - 1);
-                g_step<true>(L, st, pk, acc, P);
+                g_step<true, ATR>(L, st, pk, acc, P);
                 st = st + 1 == NST ? 0 : st + 1;
             }
             g_mma(P, acc);
@@ -316,11 +377,18 @@ gemm_mfma_kernel(GemmArgs g) {
 
 hipError_t launch_gemm(const GemmArgs &g, int grid, hipStream_t st) {
     if (grid <= 0 || g.M <= 0) return hipSuccess;
-    // lane offsets within a tile are 32-bit: 256 rows of either operand
-    if (g.lda <= 0 || g.ldb <= 0 || g.lda >= ((int64_t)1 << 24) || g.ldb >= ((int64_t)1 << 24))
-        return hipErrorInvalidValue;
-    if (g.akstep <= 0 || g.bkstep <= 0) return hipErrorInvalidValue;
-    gemm_mfma_kernel<<<grid, 256, 0, st>>>(g);
+    // lane offsets within a tile are 32-bit: 256 rows of either operand (4 panels of A)
+    if (g.ldb <= 0 || g.ldb >= ((int64_t)1 << 24) || g.bkstep <= 0) return hipErrorInvalidValue;
+    if (g.a_panels > 0) {
+        if (g.a_prows <= 0 || (int64_t)g.a_prows * ROWB * 4 >= ((int64_t)1 << 32) ||
+            (int64_t)g.a_panels * 64 < g.M)
+            return hipErrorInvalidValue;
+        gemm_mfma_kernel<true><<<grid, 256, 0, st>>>(g);
+    } else {
+        if (g.lda <= 0 || g.lda >= ((int64_t)1 << 24) || g.akstep <= 0)
+            return hipErrorInvalidValue;
+        gemm_mfma_kernel<false><<<grid, 256, 0, st>>>(g);
+    }
     return hipGetLastError();
 }
 

@@ -52,7 +52,6 @@ struct olive_score_ctx {
     float *bw_lse = nullptr;                    // [P][2]
     uint16_t *bw_wt = nullptr;                  // W_S^T panels [bw_vp/64][d_S][64] bf16
     uint16_t *bw_dzt = nullptr;                 // panels [bw_vp/64][chunk][64]
-    uint16_t *bw_dzv = nullptr;                 // [V][chunk]
     uint16_t *bw_hrt = nullptr;                 // [d_S][chunk]
     // Normalisers of the last forward call on the MFMA path and the batch they belong
     // to, for a backward on that batch (OLIVE_GRAD_REUSE_FORWARD). Scored rows take the
@@ -83,7 +82,7 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->lse_buf, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_dzv, c->bw_hrt};
+                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_hrt};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -388,24 +387,25 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         DzArgs z;
         z.c0 = (int)c0;
         z.chunk = ch;
-        z.pitch = ch;
         z.vp = ctx->bw_vp;
         z.lse = lse;
         z.targets = b->targets;
         z.w_ce = go->w_ce;
         z.w_kl = go->w_kl;
         z.dz_t = ctx->bw_dzt;
-        z.dz_v = ctx->bw_dzv;
         s = check_hip(launch_score_dz(a, z, has_t, grid, st));
         if (s) return s;
         if (go->grad_w_student) {
+            s = check_hip(launch_zero_tail(ctx->bw_dzt, ctx->bw_vp, ch, ctx->sched, (int)c0, st));
+            if (s) return s;
             s = check_hip(launch_gather_t(b->h_student, ds, ctx->rowmap, ctx->sched, (int)c0, ch,
                                           ch, ctx->bw_hrt, st));
             if (s) return s;
             GemmArgs g = {};
-            g.A = (const char *)ctx->bw_dzv;        // [V][chunk]: rows v, K = scored rows
-            g.lda = (int64_t)ch * 2;
-            g.akstep = 128;
+            // dz_t panels [vp/64][chunk][64]: rows v, K = scored rows, read transposed
+            g.A = (const char *)ctx->bw_dzt;
+            g.a_panels = (int)(ctx->bw_vp / 64);
+            g.a_prows = ch;
             g.B = (const char *)ctx->bw_hrt;        // [d_S][chunk]
             g.ldb = (int64_t)ch * 2;
             g.bkstep = 128;
@@ -677,7 +677,6 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         s = dev_alloc(&c->bw_lse, (size_t)P * 2 * sizeof(float));
         if (!s) s = dev_alloc(&c->bw_wt, (size_t)ds * c->bw_vp * 2);
         if (!s) s = dev_alloc(&c->bw_dzt, (size_t)c->bw_chunk * c->bw_vp * 2);
-        if (!s) s = dev_alloc(&c->bw_dzv, (size_t)V * c->bw_chunk * 2);
         if (!s) s = dev_alloc(&c->bw_hrt, (size_t)ds * c->bw_chunk * 2);
         if (!s) s = backward_init(c, st);
     }

@@ -127,14 +127,13 @@ struct ScoreArgs {
 
 // Logit-gradient pass of the backward (scored rows [c0, c0 + chunk) of a call).
 struct DzArgs {
-    int c0, chunk;               // first compacted scored row, rows per chunk
-    int pitch;                   // dz_v row pitch in elements (>= chunk rounded up to 64)
+    int c0, chunk;               // first compacted scored row, rows per chunk (a multiple
+                                 // of the 128-row position tile)
     int64_t vp;                  // V rounded up to 64
     const float *lse;            // [rows][2] forward log-normalisers per compacted row
     const int32_t *targets;      // packed realised tokens
     float w_ce, w_kl;            // loss weights
     uint16_t *dz_t;              // [vp/64][chunk][64] bf16 logit gradient (K-blocked panels)
-    uint16_t *dz_v;              // [V][pitch] the same, transposed
 };
 
 // Jensen-Shannon pass over the scored rows [0, n_scored) of a forward call (the
@@ -167,6 +166,11 @@ struct GemmArgs {
     bool trans_out;              // C[n][m] instead of C[m][n]
     bool accumulate;             // C += instead of C =
     int ksplit;                  // 1, or 2: halves of K added into C with atomics
+    // A given K-major instead: a_panels > 0 panels of 64 rows m, panel p holding K rows
+    // of 128 bytes (64 m values each) at A + (p * a_prows + k) * 128 ([M/64][K][64]); the
+    // MFMA operand is formed with LDS transpose reads. lda and akstep are then unused.
+    int a_panels;
+    int a_prows;
 };
 
 // Host-side launchers (each defined beside its kernel).
@@ -197,6 +201,8 @@ hipError_t launch_panel_t(const void *w, int64_t V, int d, int64_t vp, void *out
 hipError_t launch_gather_t(const void *h, int d, const uint32_t *rowmap, const Sched *sched,
                            int c0, int chunk, int pitch, uint16_t *out, hipStream_t st);
 hipError_t launch_fill(float *p, int64_t n, hipStream_t st);
+hipError_t launch_zero_tail(uint16_t *dzt, int64_t vp, int chunk, const Sched *sched, int c0,
+                            hipStream_t st);
 hipError_t launch_combine(const ScoreArgs &a, bool bf16, bool has_t, bool same_scale,
                           const int32_t *targets, int32_t *err, float *logp_s, float *logp_t,
                           int32_t *am_s, int32_t *am_t, float *kl, float *kl_rev, float *logp_tmp,

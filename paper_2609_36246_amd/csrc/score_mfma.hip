@@ -69,11 +69,6 @@ __device__ __forceinline__ uint32_t umed3(uint32_t a, uint32_t b, uint32_t c) {
     return lo > m ? lo : m;
 }
 
-// Per-wave LDS staging of the logit-gradient pass's dz_v blocks (32 rows x 64
-// columns of bf16 per wave), beside the ring: only that pass's kernel allocates it.
-constexpr int DZV_STAGE = 32 * 64 * 2;
-__shared__ __attribute__((aligned(16))) char g_dzv[4 * DZV_STAGE];
-
 template <bool HAS_T, bool SAME, bool REV, bool TOPK>
 struct Kernel {
     // Issue cursor: the next step to prefetch. Wave-uniform: its model block (vocabulary
@@ -690,9 +685,8 @@ struct Kernel {
     // rows [c0, c0 + chunk) of the call (compacted, region only), with the fold
     // replaced by g = (w_ce + w_kl) p_S - w_ce onehot(y) - w_kl p_T, p_X = exp(s_X z_X -
     // lse_X) with the forward pass's normalisers, stored as bf16 (round to nearest
-    // even) into dz_t (K-blocked panels [v/64][row][64]) and dz_v [v][row]. dz_v
-    // columns from the chunk's row count up to its pitch are written as zeros (the K
-    // padding of the dW product).
+    // even) into dz_t (K-blocked panels [v/64][row][64]), the operand of both products
+    // (the dW product reads it transposed; launch_zero_tail clears its K padding).
     static __device__ __forceinline__ void run_dz(ScoreArgs a, DzArgs z) {
         const int t_all = a.sched->t_valid - z.c0;
         const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
@@ -770,20 +764,13 @@ struct Kernel {
                 w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
                 return w;
             };
-            // the wave's 4 KB staging area for dz_v: [32 rows][64 columns] bf16, 16-byte
-            // chunk c of row r at slot c ^ (4 * bit 2 of r), so that the two 4-row halves
-            // of a store instruction land in different banks
-            char *stg = g_dzv + L.wid * DZV_STAGE;
-            const int tw0 = p * BT + L.wt * 64;   // the wave's first column
             sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                 const int vlo = vt * BV;
                 const int vw0 = row0 + L.wv * 128;   // the wave's first row
                 if (row0 == vlo) {
-                    // Whole 16-byte pieces. dz_t: lanes l and l+32 hold rows 8q .. 8q+3
-                    // and 8q+4 .. 8q+7 of one column for quads q = 2k, 2k+1; one swap of
-                    // their upper and lower halves gives each 8 consecutive rows. dz_v:
-                    // the 32 x 64 block of each vb goes through LDS and leaves as whole
-                    // 128-byte rows.
+                    // Whole 16-byte pieces: lanes l and l+32 hold rows 8q .. 8q+3 and
+                    // 8q+4 .. 8q+7 of one column for quads q = 2k, 2k+1; one swap of
+                    // their upper and lower halves gives each 8 consecutive rows.
 #pragma unroll
                     for (int vb = 0; vb < 4; ++vb) {
 #pragma unroll
@@ -804,26 +791,6 @@ struct Kernel {
                                     *(uint4 *)(z.dz_t + dzt_at(z, tcol[cb], v)) =
                                         make_uint4(X[0], Y[0], X[1], Y[1]);
                             }
-                            const int cc = cb * 32 + L.l32;   // column in the wave's 64
-#pragma unroll
-                            for (int rq = 0; rq < 4; ++rq) {
-                                const int r = 8 * rq + 4 * L.h;
-                                const int sl = ((cc >> 3) ^ (4 * L.h)) << 4;
-                                char *q = stg + r * 128 + sl + (cc & 7) * 2;
-                                *(uint16_t *)(q) = (uint16_t)w[rq].x;
-                                *(uint16_t *)(q + 128) = (uint16_t)(w[rq].x >> 16);
-                                *(uint16_t *)(q + 256) = (uint16_t)w[rq].y;
-                                *(uint16_t *)(q + 384) = (uint16_t)(w[rq].y >> 16);
-                            }
-                        }
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const int r = 8 * i + (L.lane >> 3), c = L.lane & 7;
-                            const uint4 q =
-                                *(const uint4 *)(stg + r * 128 + ((c ^ (4 * ((r >> 2) & 1))) << 4));
-                            const int t = tw0 + 8 * c;
-                            if (t + 8 <= z.pitch)
-                                *(uint4 *)(z.dz_v + (int64_t)(vw0 + vb * 32 + r) * z.pitch + t) = q;
                         }
                     }
                     return;
@@ -847,7 +814,6 @@ struct Kernel {
 #pragma unroll
                             for (int e = 0; e < 4; ++e) {
                                 if (v0 + e < vlo) continue;
-                                if (t < z.pitch) z.dz_v[(int64_t)(v0 + e) * z.pitch + t] = q[e];
                                 if (ok[cb]) z.dz_t[dzt_at(z, t, v0 + e)] = q[e];
                             }
                         }
