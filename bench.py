@@ -73,6 +73,83 @@ def cpu_baseline(wl, seconds: float):
                        "region; %.1f s" % (n, t))
 
 
+def bench_library_gemm(args, wl):
+    """Plain library GEMMs of the workload's contractions (torch.mm -> hipBLASLt),
+    bf16 operands and bf16 results, for comparison with the fused kernels: the logits
+    z_X = h_X W_X of both models over the valid rows (what an unfused path computes
+    before its softmax and KL passes; it would also write and re-read the [T, V]
+    logits), and the backward's products dL/dh = g W^T and dL/dW = h^T g over the
+    scored rows with a bf16 logit gradient g."""
+    import torch
+
+    # Row selection only: packed rows below each sequence's valid length, and of those
+    # the scored ones (from the cut, or the spans of a multi-turn batch).
+    cu = wl["cu_seqlens"].tolist()
+    vl = None if wl["valid_len"] is None else wl["valid_len"].tolist()
+    cut = wl["cut"].tolist()
+    spans = wl.get("spans")                       # per-sequence (start, end) lists
+    valid_rows, scored_rows = [], []
+    for b in range(len(cu) - 1):
+        n = cu[b + 1] - cu[b] if vl is None else vl[b]
+        valid_rows += range(cu[b], cu[b] + n)
+        for lo, hi in (spans[b] if spans is not None else [(cut[b], n)]):
+            scored_rows += range(cu[b] + lo, cu[b] + min(hi, n))
+    dev = wl["h_student"].device
+    valid = torch.tensor(valid_rows, dtype=torch.int64, device=dev)
+    scored = torch.tensor(scored_rows, dtype=torch.int64, device=dev)
+    V = wl["spec"].vocab
+
+    def timed(fn, reps):
+        for _ in range(2):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    res = []
+
+    def add(name, ms, flop):
+        tf = flop / ms / 1e9
+        res.append(dict(gemm=name, ms=round(ms, 4), tflops=round(tf, 1),
+                        frac=round(tf / PEAK_BF16_TFLOPS, 4)))
+        log("%-28s %9.3f ms %8.1f TFLOP/s" % (name, ms, tf))
+
+    reps = max(1, min(args.steps, 10))
+    F = torch.nn.functional
+    # Each product in both operand layouts the library takes without a copy: "nn" =
+    # torch.mm(A, B) with both row-major, "nt" = F.linear(A, B^T-stored) = A B with B
+    # held transposed. The fused kernels read W as [V][d] (the "nt" form of z).
+    for tag, h, w in (("z_S = h_S W_S", wl["h_student"], wl["w_student"]),
+                      ("z_T = h_T W_T", wl["h_teacher"], wl["w_teacher"])):
+        hv = h.index_select(0, valid).contiguous()
+        flop = 2.0 * hv.shape[0] * V * hv.shape[1]
+        add(tag + " nn", timed(lambda: torch.mm(hv, w), reps), flop)
+        wvd = w.t().contiguous()                     # [V][d]
+        add(tag + " nt", timed(lambda: F.linear(hv, wvd), reps), flop)
+        del hv, wvd
+    w = wl["w_student"]                              # [d_S][V]
+    hr = wl["h_student"].index_select(0, scored).contiguous()
+    R, d = hr.shape
+    g = (torch.randn(R, V, device=dev) * 1e-3).to(torch.bfloat16)
+    flop = 2.0 * R * V * d
+    wvd = w.t().contiguous()                         # [V][d_S]
+    add("dh = g W^T nn", timed(lambda: torch.mm(g, wvd), reps), flop)
+    del wvd
+    add("dh = g W^T nt", timed(lambda: F.linear(g, w), reps), flop)
+    hrt = hr.t().contiguous()                        # [d_S][R]
+    add("dW = h^T g nn", timed(lambda: torch.mm(hrt, g), reps), flop)
+    gt = g.t().contiguous()                          # [V][R]
+    add("dW = h^T g nt", timed(lambda: F.linear(hrt, gt), reps), flop)
+    print(json.dumps(dict(library_gemm=res, workload=args.workload, valid_rows=int(valid.numel()),
+                          scored_rows=int(R), dtype="bf16", peak_tflops=PEAK_BF16_TFLOPS)),
+          flush=True)
+
+
 def cpu_model() -> str:
     """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
     import subprocess
@@ -119,6 +196,11 @@ def main():
                     help="with --backward: each step is a forward call (KL, both models' "
                          "log-probs, per-sequence CE) and a backward that reuses its "
                          "normalisers (OLIVE_GRAD_REUSE_FORWARD)")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="only time the plain library GEMMs (torch.mm, bf16 in and out) of "
+                         "the workload's contractions: each model's logits over the valid "
+                         "rows and the backward's two products over the scored rows, the "
+                         "unfused path's dominant cost; prints one JSON line and exits")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run 3 plain device copies of BYTES bytes (for scaling the "
                          "FETCH_SIZE / WRITE_SIZE counters) and exit")
@@ -158,6 +240,9 @@ def main():
     log("workload ready in %.1fs: T=%d" % (time.time() - t0, T))
     if args.backward:
         bench_backward(args, wl, L)
+        return
+    if args.library_gemm:
+        bench_library_gemm(args, wl)
         return
     desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher,
                        L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
@@ -368,12 +453,20 @@ def measured_traffic(workload: str):
         return None
 
 
+# The scoring kernel's source and the headers it includes.
+KERNEL_SOURCES = ("score_mfma.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
+                  "olive_internal.hpp")
+
+
 def kernel_source_sha() -> str:
     import hashlib
-    p = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36246_amd", "csrc",
-                     "score_mfma.hip")
-    with open(p, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36246_amd",
+                        "csrc")
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(name.encode() + b"\0" + f.read())
+    return h.hexdigest()[:16]
 
 
 if __name__ == "__main__":
