@@ -179,6 +179,9 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--narrow-tile", action="store_true",
+                    help="score with the 256 x 128 two-model kernel (OLIVE_FLAG_NARROW_TILE) "
+                         "instead of the 256 x 256 one")
     ap.add_argument("--reverse-kl", action="store_true",
                     help="also form KL(student || teacher) in the same pass (olive_score_batch)")
     ap.add_argument("--region-only", action="store_true",
@@ -248,7 +251,8 @@ def main():
                        L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
                        wl["scale_student"], wl["scale_teacher"], max_positions=T, max_seqs=B,
                        flags=L.OLIVE_FLAG_KERNEL_TIMING |
-                       (L.OLIVE_FLAG_TOPK if args.topk else 0))
+                       (L.OLIVE_FLAG_TOPK if args.topk else 0) |
+                       (L.OLIVE_FLAG_NARROW_TILE if args.narrow_tile else 0))
     stream = torch.cuda.current_stream()
     ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"], stream)
     dev = wl["h_student"].device

@@ -103,6 +103,18 @@ typedef struct {
  * 2 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
  * (3.1 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
 #define OLIVE_FLAG_BACKWARD 8
+/* Score forward-KL calls with the 256 x 128 two-model MFMA kernel instead of the
+ * 256 x 256 one. Without this flag a bf16 teacher context on which the MFMA kernel
+ * applies keeps K-blocked copies of both weights and a panel buffer for the hidden rows
+ * of a call (2 (V rounded up to 256 + max_positions rounded up to 256) (d_S + d_T) bytes
+ * of device memory: 1.9 GB + 0.4 GB for V = 151936, d_S + d_T = 6144 and 32768
+ * positions), and its forward-KL calls without reverse KL or top-K outputs run the
+ * 256 x 256 kernel. That kernel forms KL's cross term with the teacher's softmax weights
+ * held in fp16 and normalised by their own sum (Sec. 6's KL; the weights' rounding moves
+ * a KL value by at most 2^-11 (1 - 2^-11)^-1 times the mean absolute deviation of the
+ * logit difference under p_T, which is at most 2 (KL + TV)); every other output is
+ * formed as in the 256 x 128 kernel. */
+#define OLIVE_FLAG_NARROW_TILE 16
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */
 typedef struct {
@@ -357,7 +369,8 @@ olive_status olive_score_last_error(olive_score_ctx *ctx, int32_t *device_code);
  *   re-decided from exact logits (bf16 products summed in fp64) because the gap between
  *   their two largest fp32 logits was at most 2^-14 max(1, |s max|); every such row of
  *   the call is re-decided (the list holds max_positions rows),
- *   [2] kernel id (0 = MFMA bf16, 1 = generic), [3] persistent workgroups launched,
+ *   [2] kernel id (0 = MFMA bf16 256 x 128, 1 = generic, 2 = MFMA bf16 256 x 256),
+ *   [3] persistent workgroups launched,
  *   [4] (position, model) pairs whose top-K set needed a filter pass over the
  *   vocabulary, [5] pairs of those that needed an exhaustive exact scan (more than
  *   256 near-tied candidates); [4] and [5] are 0 without top-K outputs.

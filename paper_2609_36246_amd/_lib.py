@@ -38,6 +38,7 @@ OLIVE_FLAG_SIMPLE_KERNEL = 1
 OLIVE_FLAG_KERNEL_TIMING = 2
 OLIVE_FLAG_TOPK = 4
 OLIVE_FLAG_BACKWARD = 8
+OLIVE_FLAG_NARROW_TILE = 16
 OLIVE_GRAD_REUSE_FORWARD = 1
 OLIVE_TOPK = 16
 OLIVE_OUT_REGION_ONLY = 1
@@ -319,9 +320,11 @@ def olive_score_last_error(ctx) -> int:
 def olive_score_last_stats(ctx) -> dict:
     out = (ctypes.c_int64 * 6)()
     _check(load().olive_score_last_stats(ctx, out), "olive_score_last_stats")
-    return dict(splits=out[0], flagged=out[1], kernel=("mfma", "generic")[out[2]]
-                if out[2] in (0, 1) else None, grid=out[3], topk_filtered=out[4],
-                topk_scanned=out[5])
+    kid = out[2]
+    return dict(splits=out[0], flagged=out[1],
+                kernel={0: "mfma", 1: "generic", 2: "mfma"}.get(kid),
+                tile={0: "256x128", 2: "256x256"}.get(kid), grid=out[3],
+                topk_filtered=out[4], topk_scanned=out[5])
 
 
 def olive_score_kernel_times(ctx, n: int) -> list:

@@ -13,7 +13,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libolive_score.so")
 SOURCES = ["olive_abi.hip", "prep.hip", "score_simple.hip", "score_mfma.hip", "combine.hip",
            "fixup.hip", "topk.hip", "gemm_mfma.hip", "backward.hip",
-           "filter.hip", "argmax.hip"]
+           "filter.hip", "argmax.hip", "score_wide.hip"]
 ARCH = "gfx950"
 
 

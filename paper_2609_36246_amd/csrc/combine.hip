@@ -91,6 +91,25 @@ __device__ __forceinline__ void wave_merge(Stat &st, float &acc, float c) {
     }
 }
 
+// The same with a second accumulator rescaled like z (the 256 x 256 kernel's sum of
+// fp16 teacher weights).
+__device__ __forceinline__ void wave_merge2(Stat &st, float &acc, float &acc2, float c) {
+    for (int off = 32; off > 0; off >>= 1) {
+        Stat o;
+        o.best = __shfl_xor(st.best, off);
+        o.sec = __shfl_xor(st.sec, off);
+        o.idx = __shfl_xor(st.idx, off);
+        o.z = __shfl_xor(st.z, off);
+        const float oa = __shfl_xor(acc, off), ob = __shfl_xor(acc2, off);
+        // both accumulators follow z's rescale: merge (z, acc) and (z, acc2) alike
+        Stat s2 = st;
+        float a2 = acc2;
+        stat_merge(st, acc, o, oa, c);
+        stat_merge(s2, a2, o, ob, c);
+        acc2 = a2;
+    }
+}
+
 __device__ __forceinline__ bool near_tie(const Stat &st, float s) {
     float gap = s * (st.best - st.sec);
     float mag = fabsf(s * st.best);
@@ -138,17 +157,21 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
     }
     const int ns = sched->n_splits;
     Stat ss = stat_identity(), st = stat_identity();
-    float acc_a = 0.f, acc_b = 0.f;
+    float acc_a = 0.f, acc_b = 0.f, acc_zh = 0.f;
     if (lane < ns) {
         ss = load_stat(a.part, a.pstride, F_BEST_S, lane, j);
         if (HAS_T) {
             st = load_stat(a.part, a.pstride, F_BEST_T, lane, j);
             acc_a = a.part[(F_A * MAX_SPLITS + lane) * a.pstride + j];
             if (kl_rev) acc_b = a.part[(F_B * MAX_SPLITS + lane) * a.pstride + j];
+            if (a.wide) acc_zh = a.part[(F_ZH * MAX_SPLITS + lane) * a.pstride + j];
         }
     }
     wave_merge(ss, acc_b, a.cS);
-    if (HAS_T) wave_merge(st, acc_a, a.cT);
+    if (HAS_T) {
+        if (a.wide) wave_merge2(st, acc_a, acc_zh, a.cT);
+        else wave_merge(st, acc_a, a.cT);
+    }
     // Every lane now holds the merged statistics.
     int fl = (am_s && near_tie(ss, a.sS)) ? 1 : 0;
     if (HAS_T) fl |= (am_t && near_tie(st, a.sT)) ? 2 : 0;
@@ -179,8 +202,10 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
         if (logp_t) logp_t[g] = a.sT * zy_t - lse_t;
         if (am_t) am_t[g] = st.idx;
         if (kl) {
+            // the teacher-weighted mean of the logit difference: A / Z_T, or with the
+            // 256 x 256 kernel's fp16 weights A / (their sum)
             float an = same_scale ? a.sT * acc_a : acc_a;
-            float v = an / st.z - lse_t + lse_s;
+            float v = an / (a.wide ? acc_zh : st.z) - lse_t + lse_s;
             kl[g] = inr ? v : 0.f;
         }
         if (kl_rev) {

@@ -62,6 +62,12 @@ struct olive_score_ctx {
     olive_batch fwd_batch = {};
     bool fwd_spans = false;
     olive_spans fwd_sp = {};
+    // 256 x 256 kernel (forward KL calls with a teacher on the MFMA path): K-blocked
+    // panels of both weights (made at init) and of a call's compacted hidden rows
+    bool wide = false;
+    uint16_t *wp_s = nullptr, *wp_t = nullptr;  // [d/32][wp_rows][32]
+    uint16_t *hp_s = nullptr, *hp_t = nullptr;  // [d/32][hp_rows][32]
+    int64_t wp_rows = 0, hp_rows = 0;
     bool bf16 = false, has_t = false, mfma_ok = false, topk = false;
     int last_kernel = -1, last_grid = 0;
     bool timing = false;
@@ -82,7 +88,8 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->lse_buf, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_hrt};
+                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_hrt,
+                    c->wp_s, c->wp_t, c->hp_s, c->hp_t};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
     delete c;
@@ -102,7 +109,7 @@ olive_status check_desc(const olive_score_desc &d) {
     if (!finite_positive(d.logit_scale_student)) return OLIVE_E_RANGE;
     if (d.d_teacher > 0 && !finite_positive(d.logit_scale_teacher)) return OLIVE_E_RANGE;
     if (d.flags & ~(OLIVE_FLAG_SIMPLE_KERNEL | OLIVE_FLAG_KERNEL_TIMING | OLIVE_FLAG_TOPK |
-                    OLIVE_FLAG_BACKWARD))
+                    OLIVE_FLAG_BACKWARD | OLIVE_FLAG_NARROW_TILE))
         return OLIVE_E_RANGE;
     return OLIVE_OK;
 }
@@ -193,6 +200,9 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
     if (jsd && !mfma) return OLIVE_E_UNSUPPORTED;    // the JSD pass is an MFMA pass
+    // The 256 x 256 kernel takes forward-KL calls with a teacher; the reverse KL and the
+    // top-K lists need both models' logits side by side (the 256 x 128 kernel).
+    const bool wide = mfma && has_t && ctx->wide && !kl_rev && !topk;
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
     // normalisers kept for a backward on this batch (MFMA path, backward contexts), and
     // read by the top-K stages and the JSD pass
@@ -214,7 +224,8 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
         max_units = pt * fixed_splits;
     }
     s = check_hip(launch_prep(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->err, counts,
-                              mfma ? MFMA_BT : SIMPLE_BT, mfma ? 0 : 1, n_vtiles, grid,
+                              wide ? WIDE_BT : (mfma ? MFMA_BT : SIMPLE_BT), mfma ? 0 : 1,
+                              n_vtiles, grid,
                               fixed_splits, topk ? topk_min_splits(n_vtiles) : 1, st));
     if (s) return s;
     s = check_hip(launch_rowmap(*b, spans, region_only, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
@@ -245,18 +256,36 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     a.wmax_s = ctx->wmax_s;
     a.wmax_t = ctx->wmax_t;
     a.wmax_dev = ctx->wmax_dev;
+    a.wps = ctx->wp_s;
+    a.wpt = ctx->wp_t;
+    a.hps = ctx->hp_s;
+    a.hpt = ctx->hp_t;
+    a.vpad = ctx->wp_rows;
+    a.prow = ctx->hp_rows;
+    a.wide = wide ? 1 : 0;
     const bool same_scale = has_t && (a.sS == a.sT);
 
+    if (wide) {
+        // the call's compacted hidden rows into panels (zero past them, to the tile end)
+        s = check_hip(launch_panel_h(b->h_student, d.d_student, ctx->rowmap, ctx->sched,
+                                     ctx->hp_rows, ctx->hp_s, st));
+        if (!s)
+            s = check_hip(launch_panel_h(b->h_teacher, d.d_teacher, ctx->rowmap, ctx->sched,
+                                         ctx->hp_rows, ctx->hp_t, st));
+        if (s) return s;
+    }
     const int slot = (int)(ctx->n_calls % 64);
     if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
-    if (mfma)
+    if (wide)
+        s = check_hip(launch_score_wide(a, same_scale, grid, st));
+    else if (mfma)
         s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, topk, grid, st));
     else
         s = check_hip(launch_score_simple(a, ctx->bf16, has_t, max_units, st));
     if (s) return s;
     if (ctx->timing && hipEventRecord(ctx->ev[1][slot], st) != hipSuccess) return OLIVE_E_HIP;
     ctx->n_calls++;
-    ctx->last_kernel = mfma ? 0 : 1;
+    ctx->last_kernel = wide ? 2 : (mfma ? 0 : 1);
     ctx->last_grid = mfma ? grid : (int)max_units;
 
     int32_t *flagged = (am_s || (has_t && am_t)) ? ctx->flagged : nullptr;
@@ -679,6 +708,18 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         if (!s) s = dev_alloc(&c->bw_dzt, (size_t)c->bw_chunk * c->bw_vp * 2);
         if (!s) s = dev_alloc(&c->bw_hrt, (size_t)ds * c->bw_chunk * 2);
         if (!s) s = backward_init(c, st);
+    }
+    c->wide = c->mfma_ok && c->has_t && !(d.flags & OLIVE_FLAG_NARROW_TILE);
+    if (!s && c->wide) {
+        c->wp_rows = (V + MFMA_BV - 1) / MFMA_BV * MFMA_BV;
+        c->hp_rows = (P + WIDE_BT - 1) / WIDE_BT * WIDE_BT;
+        s = dev_alloc(&c->wp_s, (size_t)c->wp_rows * d.d_student * 2);
+        if (!s) s = dev_alloc(&c->wp_t, (size_t)c->wp_rows * d.d_teacher * 2);
+        if (!s) s = dev_alloc(&c->hp_s, (size_t)c->hp_rows * d.d_student * 2);
+        if (!s) s = dev_alloc(&c->hp_t, (size_t)c->hp_rows * d.d_teacher * 2);
+        if (!s && (launch_panel_w(c->ws, V, d.d_student, c->wp_rows, c->wp_s, st) != hipSuccess ||
+                   launch_panel_w(c->wt, V, d.d_teacher, c->wp_rows, c->wp_t, st) != hipSuccess))
+            s = OLIVE_E_HIP;
     }
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));
     if (!s && c->mfma_ok && c->has_t) s = dev_alloc(&c->lse_buf, (size_t)P * 2 * sizeof(float));

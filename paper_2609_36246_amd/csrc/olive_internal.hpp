@@ -21,10 +21,14 @@ namespace olive {
 //             difference (reverse KL; written only when it is requested).
 //   J:        the Jensen-Shannon pass's sum over the split of p_hi g(p_lo / p_hi)
 //             (log2 units; see the pass), for scored rows only.
+//   ZH:       the 256 x 256 kernel only: sum_v w^_v of the teacher weights it keeps in
+//             fp16 (w^_v = 2^15 exp(s_T (zT_v - BEST_T)) rounded), rescaled like Z; its A
+//             is sum_v w^_v D_v, so that KL's cross term is A / ZH.
 enum Field {
     F_BEST_S = 0, F_SEC_S = 1, F_IDX_S = 2, F_Z_S = 3,
     F_BEST_T = 4, F_SEC_T = 5, F_IDX_T = 6, F_Z_T = 7, F_A = 8, F_B = 9, F_J = 10,
-    NFIELDS = 11
+    F_ZH = 11,
+    NFIELDS = 12
 };
 // Top-K planes (contexts built with OLIVE_FLAG_TOPK only), per model m (0 = S, 1 = T)
 // from F_TK + m * TK_FIELDS: the split's 8 largest raw logits (descending, lower
@@ -105,6 +109,7 @@ enum {
 
 constexpr int MFMA_BV = 256;     // vocabulary rows per tile (MFMA M)
 constexpr int MFMA_BT = 128;     // positions per tile (MFMA N)
+constexpr int WIDE_BT = 256;     // positions per tile of the 256 x 256 kernel
 constexpr int SIMPLE_BT = 16;    // positions per tile of the generic kernel
 constexpr int SIMPLE_VC = 256;   // vocabulary chunk of the generic kernel
 constexpr int MAX_SPLITS = 32;   // vocabulary splits a call may use
@@ -123,6 +128,11 @@ struct ScoreArgs {
     float wmax_s, wmax_t;        // largest weight-row L2 norm (top-K rounding bounds)
     const float *wmax_dev;       // device [2]: the same two values formed on the device
                                  // (used instead of wmax_s / wmax_t when set)
+    // 256 x 256 kernel: K-blocked panels [d/32][rows][32] of the weights (rows = vpad,
+    // zero past V) and of the call's compacted hidden rows (rows = prow)
+    const void *wps, *wpt, *hps, *hpt;
+    int64_t vpad, prow;
+    int32_t wide;                // the partials come from that kernel (KL's cross term is A / ZH)
 };
 
 // Logit-gradient pass of the backward (scored rows [c0, c0 + chunk) of a call).
@@ -190,6 +200,11 @@ hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_
                                hipStream_t st);
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
                              bool topk, int grid, hipStream_t st);
+hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, int grid, hipStream_t st);
+hipError_t launch_panel_w(const void *w, int64_t V, int d, int64_t vpad, void *out,
+                          hipStream_t st);
+hipError_t launch_panel_h(const void *h, int d, const uint32_t *rowmap, const Sched *sched,
+                          int64_t prow, void *out, hipStream_t st);
 hipError_t launch_score_dz(const ScoreArgs &a, const DzArgs &z, bool has_t, int grid,
                            hipStream_t st);
 hipError_t launch_score_jsd(const ScoreArgs &a, const JsdArgs &z, int grid, hipStream_t st);

@@ -46,7 +46,7 @@ TOPK_OUTPUTS = ("overlap", "kl_topk", "tk_s", "tk_t")
 def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
             outputs=("kl", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
             poison=False, ctx=None, keep_ctx=False, timing=False, repeat=1, out_flags=0,
-            topk_ctx=None):
+            topk_ctx=None, narrow=False):
     """Score a workload on the GPU; returns numpy outputs (and stats).
 
     Top-K outputs ("overlap", "kl_topk", "tk_s", "tk_t") make the context reserve
@@ -61,7 +61,8 @@ def run_hip(wl, region=L.OLIVE_REGION_TEACHER, simple=False, student_only=False,
             topk_ctx = any(k in outputs for k in TOPK_OUTPUTS)
         flags = (L.OLIVE_FLAG_SIMPLE_KERNEL if simple else 0) | \
                 (L.OLIVE_FLAG_KERNEL_TIMING if timing else 0) | \
-                (L.OLIVE_FLAG_TOPK if topk_ctx else 0)
+                (L.OLIVE_FLAG_TOPK if topk_ctx else 0) | \
+                (L.OLIVE_FLAG_NARROW_TILE if narrow else 0)
         desc = L.make_desc(spec.vocab, spec.d_student, 0 if student_only else spec.d_teacher,
                            L.OLIVE_BF16 if spec.dtype == "bf16" else L.OLIVE_F32, L.OLIVE_W_DV,
                            wl["scale_student"], wl["scale_teacher"], max_positions=T,
