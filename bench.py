@@ -310,8 +310,11 @@ def main():
         % (args.steps, ms_step, kernel_ms, stats, err))
     flops = 2.0 * rows * spec.vocab * (spec.d_student + spec.d_teacher)
     achieved = flops / (kernel_ms * 1e-3) / 1e12
+    # the dominant kernel of the call: the 256 x 256 one, or the 256 x 128 one (reverse KL,
+    # top-K, OLIVE_FLAG_NARROW_TILE)
+    kernel = "score_wide" if stats.get("tile") == "256x256" else "score_mfma"
     traffic = None if (args.reverse_kl or args.region_only or args.topk) \
-        else measured_traffic(args.workload)
+        else measured_traffic(args.workload, kernel)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
         "value": rows / (ms_step * 1e-3),
@@ -341,7 +344,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
+            "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic, "kernel": kernel + "_kernel",
         },
     }
     L.olive_score_free(ctx)
@@ -436,11 +439,11 @@ def bench_backward(args, wl, L):
     print(json.dumps(out), flush=True)
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per launch of the scoring kernel from the committed rocprofv3 counter
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of a scoring kernel from the committed rocprofv3 counter
     summary of this workload (FETCH_SIZE and WRITE_SIZE, scaled by a plain copy's
     readings), or None when there is none for the current kernel source."""
-    path = os.path.join(PROFILES, "score_mfma_%s_traffic.txt" % workload)
+    path = os.path.join(PROFILES, "%s_%s_traffic.txt" % (kernel, workload))
     if not os.path.exists(path):
         return None
     fields = {}
@@ -449,7 +452,7 @@ def measured_traffic(workload: str):
             if ":" in line and not line.startswith((" ", "#", "$")):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
-    if fields.get("kernel_source_sha") != kernel_source_sha():
+    if fields.get("kernel_source_sha") != kernel_source_sha(kernel):
         return None
     try:
         return float(fields["hbm_bytes_per_launch"])
@@ -457,17 +460,21 @@ def measured_traffic(workload: str):
         return None
 
 
-# The scoring kernel's source and the headers it includes.
-KERNEL_SOURCES = ("score_mfma.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
-                  "olive_internal.hpp")
+# Each scoring kernel's source and the headers it includes.
+KERNEL_SOURCES = {
+    "score_mfma": ("score_mfma.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
+                   "olive_internal.hpp"),
+    "score_wide": ("score_wide.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
+                   "olive_internal.hpp"),
+}
 
 
-def kernel_source_sha() -> str:
+def kernel_source_sha(kernel: str = "score_wide") -> str:
     import hashlib
     csrc = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2609_36246_amd",
                         "csrc")
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in KERNEL_SOURCES[kernel]:
         with open(os.path.join(csrc, name), "rb") as f:
             h.update(name.encode() + b"\0" + f.read())
     return h.hexdigest()[:16]
