@@ -1,13 +1,16 @@
-// Fused bf16 scoring kernel for gfx950 with a 256 x 256 tile (MFMA 32x32x16, LDS ring
+// Fused bf16 scoring kernel for gfx950 with a 256 x 256 tile (MFMA 16x16x32, LDS ring
 // fed by direct global->LDS loads from K-blocked panels).
 //
-// A workgroup (4 wavefronts, 2 x 2) owns 256 vocabulary rows x 256 compacted positions
-// and sweeps the vocabulary tiles of one split for one position tile. Per vocabulary
-// tile it accumulates the teacher logits (K = d_T) and then the student logits
-// (K = d_S) of the same 256 x 256 block in the same 256 AGPRs per lane: one model's
-// fp32 accumulators at a time, where holding both models (the other kernel) limits
-// the tile to 256 x 128. Bytes moved from L2 into LDS per MFMA operation, and LDS reads
-// per MFMA, are then two thirds of that kernel's.
+// A workgroup (4 wavefronts) owns 256 vocabulary rows x 256 compacted positions and
+// sweeps the vocabulary tiles of one split for one position tile; wavefront w owns all
+// 256 rows of positions 64w .. 64w+63 (16 x 4 blocks of v_mfma_f32_16x16x32_bf16, 256
+// AGPRs). Per vocabulary tile it accumulates the teacher logits (K = d_T) and then the
+// student logits (K = d_S) of the same block in the same AGPRs: one model's fp32
+// accumulators at a time, where holding both models (the other kernel) limits the tile
+// to 256 x 128. The 16x16x32 shape moves half the accumulator bytes per MFMA operation
+// of the 32x32x16 one; under this load the chip is power-limited, and a pure-MFMA loop
+// of 16x16x32 on random bf16 operands held a 14 % higher clock than one of 32x32x16 at
+// the same pipe occupancy.
 //
 // KL(teacher || student) needs, per vocabulary entry, the teacher's softmax weight
 // next to the student's logit. The teacher fold keeps those weights, relative to the
@@ -25,12 +28,16 @@
 // Pipeline: K advances 32 elements per step. W and the hidden rows are read from
 // K-blocked panels ([d/32][rows][32] bf16, 64 bytes per row per panel), so one step of
 // a tile is a contiguous 16 KB for W (256 rows) and for H (256 positions): whole
-// 128-byte lines at half the K step of the row-major layout. The two 16 KB tiles land
-// in one of 4 LDS stages (32 KB each) through global_load_lds_dwordx4, issued three
-// steps ahead. Stage rows are 64 bytes; the 16-byte chunk c of row r sits in slot
-// c ^ ((r >> 2) & 3), which keeps the ds_read_b128 operand fetches (16 rows x one chunk
-// per 256 bytes of banks) free of bank conflicts. The swizzle is applied on the global
-// side of the DMA (each lane fetches the chunk that belongs at its LDS slot).
+// 128-byte lines. The two 16 KB tiles land in one of 4 LDS stages (32 KB each) through
+// global_load_lds_dwordx4, issued three steps ahead. A step's 64 MFMAs run in two
+// halves of 8 row blocks; the second half runs under the next step's operand reads.
+// Stage rows are 64 bytes; the 16-byte chunk c of row r sits in slot c ^ ((r >> 1) & 3).
+// A ds_read_b128 of a 16x16x32 operand reads 16 rows x 4 chunks; of the XOR swizzles on
+// 16-byte slots measured on gfx950 only this one left it free of bank conflicts (the
+// 32x32x16 operand's 32 rows x 2 chunks are conflict-free with c ^ ((r >> 2) & 3)
+// instead). The panels are written with the swizzle already applied (rows are tile
+// rows modulo 256), so each DMA copies 1 KB linearly: DMAs whose lanes fetched permuted
+// pieces made the L2 fetch 2.2 to 3 times the bytes from the fabric.
 //
 // The grid is persistent (one workgroup per CU); work units (position tile, split) are
 // ordered so that the 32 workgroups of one XCD share 8 position tiles x 4 splits.
@@ -130,20 +137,29 @@ __device__ __forceinline__ float f16_hi(uint32_t u) {
     return (float)__builtin_bit_cast(halfx2, u)[1];
 }
 
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
 struct XLane {
-    int lane, wid, wv, wt, h, l32;
-    uint32_t voff[XDMA]; // per DMA i of an operand: the lane's byte offset within a
-                         // 16 KB tile step (wave part and i * 1 KB included)
-    uint32_t lds_a[2];   // operand read offsets of sub-step j within a stage (W part)
-    uint32_t lds_b[2];   // (H part)
+    int lane, wid, l16, g;   // g = lane / 16: the lane's 4-row group of an output block
+                             // and its 8-element K chunk of an operand fragment
+    uint32_t voff[XDMA];     // per DMA i of an operand: the lane's byte offset within a
+                             // 16 KB tile step (wave part and i * 1 KB included)
+    uint32_t lds_a;          // operand read offset within a stage: W row l16 of block 0
+    uint32_t lds_b;          // H row (position) 64 wid + l16 of block 0
 };
 
-struct XFrag {
-    bf16x8 A[4], B[4];
+// Operand fragments: one half of a step's A blocks (8 of the 16 row blocks), and the
+// step's 4 B blocks (the wavefront's 64 positions).
+struct XFragA {
+    bf16x8 A[8];
+};
+struct XFragB {
+    bf16x8 B[4];
 };
 
-// Running max / second max / lowest argmax of one column over one 32-row block (R.z is
-// left alone). Returns the rescale factor exp2(c (old max - new max)) of the sums.
+// Running max / second max / lowest argmax of one column over 16 logits (R.z is left
+// alone): 4 output blocks of the column, element e at row vcode0 + 16 (e / 4) + e % 4.
+// Returns the rescale factor exp2(c (old max - new max)) of the sums.
 __device__ __forceinline__ float block_max(const float (&z)[16], Run &R, int vcode0,
                                            float c, float inf) {
     float tm = R.best, ts = R.sec;
@@ -154,7 +170,7 @@ __device__ __forceinline__ float block_max(const float (&z)[16], Run &R, int vco
     }
     int code = 0;
 #pragma unroll
-    for (int r = 15; r >= 0; --r) code = (z[r] == tm) ? 8 * (r >> 2) + (r & 3) : code;
+    for (int r = 15; r >= 0; --r) code = (z[r] == tm) ? 16 * (r >> 2) + (r & 3) : code;
     const bool up = tm > R.best;
     const float resc = fast_exp2((R.best - tm) * c);
     R.idx = up ? vcode0 + code : R.idx;
@@ -163,7 +179,7 @@ __device__ __forceinline__ float block_max(const float (&z)[16], Run &R, int vco
     return resc;
 }
 
-// Teacher, second pass over a column's blocks of the tile, once the column's running
+// Teacher, second pass over a column's logits of the tile, once the column's running
 // max over the tile is final (the first pass is block_max): mneg = 15 - c max. Adds
 // the weights 2^15 exp2(c (z - max)) in fp32 to zsum, keeps them as fp16 in eh, adds
 // the fp16 values to hsum and their products with the logits to asum. All weights of a
@@ -191,8 +207,8 @@ __device__ __forceinline__ void teacher_weights(const float (&z)[16], float c, f
     }
 }
 
-// Student block: running statistics, and the sum of the teacher's fp16 weights times
-// the student logits into as.
+// Student, 16 logits of a column: running statistics, and the sum of the teacher's fp16
+// weights times the student logits into as.
 __device__ __forceinline__ void fold_student(const float (&z)[16], Run &R, float &as,
                                              const uint32_t (&eh)[8], float c, int vcode0,
                                              float inf) {
@@ -306,55 +322,62 @@ struct Wide {
         advance(C);
     }
 
-    template <int J>
-    static __device__ __forceinline__ void read_frag(const XLane &L, int st, XFrag &F) {
+    // Half H of a step's A blocks (row blocks 8H .. 8H+7), and the step's B blocks.
+    template <int H>
+    static __device__ __forceinline__ void read_a(const XLane &L, int st, XFragA &F) {
         const char *stage = x_ring + st * XSTAGE;
 #pragma unroll
-        for (int vb = 0; vb < 4; ++vb)
-            F.A[vb] = *(const bf16x8 *)(stage + L.lds_a[J] + vb * 32 * XROW);
+        for (int i = 0; i < 8; ++i)
+            F.A[i] = *(const bf16x8 *)(stage + L.lds_a + (8 * H + i) * 1024);
+    }
+    static __device__ __forceinline__ void read_b(const XLane &L, int st, XFragB &F) {
+        const char *stage = x_ring + st * XSTAGE;
 #pragma unroll
         for (int cb = 0; cb < 4; ++cb)
-            F.B[cb] = *(const bf16x8 *)(stage + L.lds_b[J] + cb * 32 * XROW);
+            F.B[cb] = *(const bf16x8 *)(stage + L.lds_b + cb * 1024);
     }
 
-    static __device__ __forceinline__ void mma(const XFrag &F, floatx16 (&acc)[4][4]) {
-#pragma unroll
-        for (int vb = 0; vb < 4; ++vb)
-#pragma unroll
-            for (int cb = 0; cb < 4; ++cb)
-                acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(F.A[vb], F.B[cb],
-                                                                      acc[vb][cb], 0, 0, 0);
+    // Operand reads interleaved with a half's MFMAs (one read after each of its first
+    // MFMAs, so that the matrix pipe is fed from the step's first cycle on): RD 1 reads
+    // this step's first-half A blocks and its B blocks (12), RD 2 its second-half A
+    // blocks (8), RD 0 none.
+    template <int RD, int J>
+    static __device__ __forceinline__ void read_at(const XLane &L, const char *stage, XFragA &RA,
+                                                   XFragB &RB) {
+        if constexpr (RD == 1 && J < 8)
+            RA.A[J] = *(const bf16x8 *)(stage + L.lds_a + J * 1024);
+        else if constexpr (RD == 1 && J >= 8 && J < 12)
+            RB.B[J - 8] = *(const bf16x8 *)(stage + L.lds_b + (J - 8) * 1024);
+        else if constexpr (RD == 2 && J < 8)
+            RA.A[J] = *(const bf16x8 *)(stage + L.lds_a + (8 + J) * 1024);
     }
 
-    // The 16 MFMAs of one sub-step (ZERO: the block's first, onto zero accumulators)
-    // with DMAs Q0 .. Q0+NQ-1 of the refill spread between them.
-    template <bool ZERO, int Q0, int NQ>
-    static __device__ __forceinline__ void mma_issue(const XFrag &F, floatx16 (&acc)[4][4],
-                                                     const Cursor &C, const XLane &L,
-                                                     uint32_t lw) {
-#define OLIVE_XMI(J_, VB_, CB_)                                                             \
-        __builtin_amdgcn_sched_barrier(0);                                                \
-        acc[VB_][CB_] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(                            \
-            F.A[VB_], F.B[CB_], ZERO ? floatx16{0.f} : acc[VB_][CB_], 0, 0, 0);             \
-        __builtin_amdgcn_sched_barrier(0);                                                \
-        dmas<Q0 + ((J_) * NQ + 15) / 16, Q0 + ((J_) * NQ + NQ + 15) / 16>(C, L, lw);
-        OLIVE_XMI(0, 0, 0)
-        OLIVE_XMI(1, 0, 1)
-        OLIVE_XMI(2, 0, 2)
-        OLIVE_XMI(3, 0, 3)
-        OLIVE_XMI(4, 1, 0)
-        OLIVE_XMI(5, 1, 1)
-        OLIVE_XMI(6, 1, 2)
-        OLIVE_XMI(7, 1, 3)
-        OLIVE_XMI(8, 2, 0)
-        OLIVE_XMI(9, 2, 1)
-        OLIVE_XMI(10, 2, 2)
-        OLIVE_XMI(11, 2, 3)
-        OLIVE_XMI(12, 3, 0)
-        OLIVE_XMI(13, 3, 1)
-        OLIVE_XMI(14, 3, 2)
-        OLIVE_XMI(15, 3, 3)
-#undef OLIVE_XMI
+    // MFMA J (0..31) of half H of a step, then its share of the refill's DMAs Q0 ..
+    // Q0+NQ-1 (spread evenly over the 32) and of the interleaved reads, then MFMA J+1.
+    // ZERO: onto zero accumulators (the block's first K step).
+    template <int H, bool ZERO, int Q0, int NQ, int RD, int J>
+    static __device__ __forceinline__ void mma_from(const XFragA &FA, const XFragB &FB,
+                                                    floatx4 (&acc)[16][4], const Cursor &C,
+                                                    const XLane &L, uint32_t lw,
+                                                    const char *stage, XFragA &RA, XFragB &RB) {
+        if constexpr (J < 32) {
+            constexpr int i = J >> 2, cb = J & 3;
+            __builtin_amdgcn_sched_barrier(0);
+            acc[8 * H + i][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                FA.A[i], FB.B[cb], ZERO ? floatx4{0.f} : acc[8 * H + i][cb], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            read_at<RD, J>(L, stage, RA, RB);
+            __builtin_amdgcn_sched_barrier(0);
+            dmas<Q0 + (J * NQ + 31) / 32, Q0 + (J * NQ + NQ + 31) / 32>(C, L, lw);
+            mma_from<H, ZERO, Q0, NQ, RD, J + 1>(FA, FB, acc, C, L, lw, stage, RA, RB);
+        }
+    }
+    template <int H, bool ZERO, int Q0, int NQ, int RD = 0>
+    static __device__ __forceinline__ void mma_half(const XFragA &FA, const XFragB &FB,
+                                                    floatx4 (&acc)[16][4], const Cursor &C,
+                                                    const XLane &L, uint32_t lw,
+                                                    const char *stage, XFragA &RA, XFragB &RB) {
+        mma_from<H, ZERO, Q0, NQ, RD, 0>(FA, FB, acc, C, L, lw, stage, RA, RB);
         __builtin_amdgcn_sched_barrier(0);
     }
 
@@ -370,54 +393,67 @@ struct Wide {
         compiler_fence();
     }
 
-    // One step in stage st: meet the barrier, read sub-step 0's fragments, run the
-    // previous step's sub-step 1 (P) under those reads, read sub-step 1 into P, run
-    // sub-step 0. FIRST: the block's first step (no pending sub-step; sub-step 0 starts
-    // the accumulators at zero).
-    template <bool FIRST>
+    // One step in stage st: meet the barrier, read the first half's A blocks and the B
+    // blocks, run the previous step's second half (PA x PB) under those reads, read this
+    // step's second-half A blocks into PA, run the first half. KIND 0: the block's first
+    // step (no pending half; the first half starts its accumulators at zero); KIND 1:
+    // its second step (the pending half starts its accumulators at zero); KIND 2: later.
+    template <int KIND>
     static __device__ __forceinline__ void step(const ScoreArgs &a, const XLane &L, Cursor &C,
-                                                int st, floatx16 (&acc)[4][4], XFrag &P) {
+                                                int st, floatx4 (&acc)[16][4], XFragA &PA,
+                                                XFragB &PB) {
         const int pv = st == 0 ? XNST - 1 : st - 1;
         turn(C, a);
         arrive();
         const uint32_t lw = stage_w(L, pv);
-        XFrag F0;
-        read_frag<0>(L, st, F0);
-        __builtin_amdgcn_sched_barrier(0);
-        if (FIRST) {
-            read_frag<1>(L, st, P);
+        const char *stage = x_ring + st * XSTAGE;
+        XFragA F0;
+        XFragB FB;
+        if (KIND == 0) {
+            read_a<0>(L, st, F0);
+            read_b(L, st, FB);
+            read_a<1>(L, st, PA);
             __builtin_amdgcn_sched_barrier(0);
-            mma_issue<true, 0, 8>(F0, acc, C, L, lw);
+            mma_half<0, true, 0, 8>(F0, FB, acc, C, L, lw, stage, F0, FB);
         } else {
-            mma_issue<false, 0, 4>(P, acc, C, L, lw);
-            read_frag<1>(L, st, P);
-            __builtin_amdgcn_sched_barrier(0);
-            mma_issue<false, 4, 4>(F0, acc, C, L, lw);
+            // the previous step's second half, with this step's first reads in between
+            mma_half<1, KIND == 1, 0, 4, 1>(PA, PB, acc, C, L, lw, stage, F0, FB);
+            // this step's first half, with its second-half reads (into PA) in between
+            mma_half<0, false, 4, 4, 2>(F0, FB, acc, C, L, lw, stage, PA, FB);
         }
+        PB = FB;
         advance(C);
     }
 
     // Add kMasked to the rows at or past V of the padded last tile (one MFMA per block:
     // A holds kMasked in k = 0 of those rows, B ones), so they drop out of every
     // statistic while the accumulators stay MFMA-only.
-    static __device__ __forceinline__ void mask_tail(const XLane &L, floatx16 (&acc)[4][4],
+    static __device__ __forceinline__ void mask_tail(const XLane &L, floatx4 (&acc)[16][4],
                                                      int row0, int V) {
-        bf16x8 ones, bias[4];
+        bf16x8 ones;
 #pragma unroll
         for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
 #pragma unroll
-        for (int vb = 0; vb < 4; ++vb) {
-            const int v = row0 + L.wv * 128 + vb * 32 + L.l32;
+        for (int vb = 0; vb < 16; ++vb) {
+            const int v = row0 + vb * 16 + L.l16;   // A-operand row of this lane
+            bf16x8 bias;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) bias[vb][e] = (__bf16)0.0f;
-            if (L.h == 0 && v >= V) bias[vb][0] = (__bf16)kMasked;
-        }
-#pragma unroll
-        for (int vb = 0; vb < 4; ++vb)
+            for (int e = 0; e < 8; ++e) bias[e] = (__bf16)0.0f;
+            if (L.g == 0 && v >= V) bias[0] = (__bf16)kMasked;
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb)
-                acc[vb][cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bias[vb], ones,
-                                                                      acc[vb][cb], 0, 0, 0);
+                acc[vb][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(bias, ones, acc[vb][cb], 0,
+                                                                      0, 0);
+        }
+    }
+
+    // The 16 logits of column cb in row blocks 4q .. 4q+3.
+    static __device__ __forceinline__ void col16(const floatx4 (&acc)[16][4], int q, int cb,
+                                                 float (&z)[16]) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) z[4 * j + r] = agpr_read(acc[4 * q + j][cb][r]);
     }
 
     static __device__ __forceinline__ void run(ScoreArgs a) {
@@ -428,23 +464,18 @@ struct Wide {
         XLane L;
         L.lane = threadIdx.x & 63;
         L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-        L.wv = L.wid & 1;
-        L.wt = L.wid >> 1;
-        L.h = L.lane >> 5;
-        L.l32 = L.lane & 31;
-        // DMA lane: 16 rows x 64 bytes per DMA, row lane/4, LDS slot lane&3 holding the
-        // row's chunk (lane&3) ^ ((row >> 2) & 3) = (lane&3) ^ ((lane >> 4) & 3).
+        L.l16 = L.lane & 15;
+        L.g = L.lane >> 4;
+        // DMA lane: 16 bytes at 16 lane of a 1 KB piece of the step's tile. The panels
+        // hold every row's 16-byte chunks already in their swizzled slots (panel_w,
+        // panel_h), so the copy is linear and lands swizzled.
 #pragma unroll
         for (int i = 0; i < XDMA; ++i)
-            L.voff[i] = (uint32_t)(L.wid * XDMA * 1024 + i * 1024 + (L.lane >> 2) * XROW +
-                                   (((L.lane & 3) ^ ((L.lane >> 4) & 3)) << 4));
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const uint32_t lane_part =
-                (uint32_t)(L.l32 * XROW + (((2 * j + L.h) ^ ((L.l32 >> 2) & 3)) << 4));
-            L.lds_a[j] = (uint32_t)(L.wv * 128 * XROW) + lane_part;
-            L.lds_b[j] = (uint32_t)(XW_BYTES + L.wt * 128 * XROW) + lane_part;
-        }
+            L.voff[i] = (uint32_t)(L.wid * XDMA * 1024 + i * 1024 + L.lane * 16);
+        // operand fragment of a 16-row block: row l16, K chunk g, in slot g ^ ((l16 >> 1) & 3)
+        const uint32_t lane_part = (uint32_t)(L.l16 * XROW + ((L.g ^ ((L.l16 >> 1) & 3)) << 4));
+        L.lds_a = lane_part;
+        L.lds_b = (uint32_t)(XW_BYTES + L.wid * 4 * 1024) + lane_part;
         const int nS = a.ds / XK, nT = a.dt / XK;
         const int G = gridDim.x;
         const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
@@ -476,8 +507,8 @@ struct Wide {
                 AT[cb] = 0.f;
                 AS[cb] = 0.f;
             }
-            uint32_t eh[4][4][8];
-            floatx16 acc[4][4];
+            uint32_t eh[4][4][8];   // [row-block quarter][cb][pair]
+            floatx4 acc[16][4];
 
             Cursor C;
             C.vt1 = vt1;
@@ -491,19 +522,26 @@ struct Wide {
             int st = 0;
 #define OLIVE_XSTEPS(COUNT_)                                                              \
             {                                                                             \
-                XFrag P;                                                                  \
-                step<true>(a, L, C, st, acc, P);                                          \
+                XFragA PA;                                                                \
+                XFragB PB;                                                                \
+                step<0>(a, L, C, st, acc, PA, PB);                                        \
                 st = st + 1 == XNST ? 0 : st + 1;                                         \
-                for (int k = 1; k < (COUNT_); ++k) {                                      \
-                    step<false>(a, L, C, st, acc, P);                                     \
+                if ((COUNT_) > 1) {                                                       \
+                    step<1>(a, L, C, st, acc, PA, PB);                                    \
                     st = st + 1 == XNST ? 0 : st + 1;                                     \
+                    for (int k = 2; k < (COUNT_); ++k) {                                  \
+                        step<2>(a, L, C, st, acc, PA, PB);                                \
+                        st = st + 1 == XNST ? 0 : st + 1;                                 \
+                    }                                                                     \
+                    mma_half<1, false, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);      \
+                } else {                                                                  \
+                    mma_half<1, true, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);       \
                 }                                                                         \
-                mma(P, acc);                                                              \
                 __builtin_amdgcn_sched_barrier(0);                                        \
             }
             for (int vt = vt0; vt < vt1; ++vt) {
                 const int row0 = vt * XV;
-                const int vbase = row0 + L.wv * 128 + 4 * L.h;
+                const int vbase = row0 + 4 * L.g;
                 OLIVE_XSTEPS(nT)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
@@ -513,12 +551,11 @@ struct Wide {
                         Run R = stat_get(1, cb);
                         const float m0 = R.best;
 #pragma unroll
-                        for (int vb = 0; vb < 4; ++vb) {
+                        for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
-#pragma unroll
-                            for (int r = 0; r < 16; ++r) z[r] = agpr_read(acc[vb][cb][r]);
-                            (void)block_max(z, R, vbase + vb * 32, a.cT, inf);
+                            col16(acc, qq, cb, z);
+                            (void)block_max(z, R, vbase + qq * 64, a.cT, inf);
                         }
                         // one rescale per column and tile, to the tile's max
                         const float resc = fast_exp2((m0 - R.best) * a.cT);
@@ -526,12 +563,11 @@ struct Wide {
                         AS[cb] *= resc;
                         const float mneg = fmaf(-R.best, a.cT, 15.0f);
 #pragma unroll
-                        for (int vb = 0; vb < 4; ++vb) {
+                        for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
-#pragma unroll
-                            for (int r = 0; r < 16; ++r) z[r] = agpr_read(acc[vb][cb][r]);
-                            teacher_weights(z, a.cT, mneg, one, zsum, hsum, asum, eh[vb][cb]);
+                            col16(acc, qq, cb, z);
+                            teacher_weights(z, a.cT, mneg, one, zsum, hsum, asum, eh[qq][cb]);
                         }
                         R.z = zsum;
                         ZH[cb] = hsum;
@@ -551,12 +587,11 @@ struct Wide {
                     for (int cb = 0; cb < 4; ++cb) {
                         Run R = stat_get(0, cb);
 #pragma unroll
-                        for (int vb = 0; vb < 4; ++vb) {
+                        for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
-#pragma unroll
-                            for (int r = 0; r < 16; ++r) z[r] = agpr_read(acc[vb][cb][r]);
-                            fold_student(z, R, AS[cb], eh[vb][cb], a.cS, vbase + vb * 32, inf);
+                            col16(acc, qq, cb, z);
+                            fold_student(z, R, AS[cb], eh[qq][cb], a.cS, vbase + qq * 64, inf);
                         }
                         stat_put(0, cb, R);
                     }
@@ -565,69 +600,43 @@ struct Wide {
 #undef OLIVE_XSTEPS
 
             // The difference sums (unscaled with equal scales; the combine multiplies by
-            // s), then lanes l and l+32 (same columns, interleaved rows).
-            float AA[4];
-            Run RS[4], RT[4];
+            // s), then the 4 lanes of each column (row groups g = 0..3) merge.
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): trailing prefetches landed
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
-                RS[cb] = stat_get(0, cb);
-                RT[cb] = stat_get(1, cb);
-                AA[cb] = SAME ? AT[cb] - AS[cb] : a.sT * AT[cb] - a.sS * AS[cb];
-                Run o{__shfl_xor(RS[cb].best, 32), __shfl_xor(RS[cb].sec, 32),
-                      __shfl_xor(RS[cb].z, 32), __shfl_xor(RS[cb].idx, 32)};
-                float dummy = 0.f;
-                merge_run(RS[cb], dummy, o, 0.f, a.cS);
-                Run t{__shfl_xor(RT[cb].best, 32), __shfl_xor(RT[cb].sec, 32),
-                      __shfl_xor(RT[cb].z, 32), __shfl_xor(RT[cb].idx, 32)};
-                const float ta = __shfl_xor(AA[cb], 32), tz = __shfl_xor(ZH[cb], 32);
-                merge_teacher(RT[cb], AA[cb], ZH[cb], t, ta, tz, a.cT);
-            }
-            // The two vocabulary halves (wv = 1 into wv = 0) through LDS, once the
-            // trailing prefetches into the ring have landed.
-            float *xs = (float *)x_ring;   // [wt][cb][l32][10]
-            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
-            compiler_fence();
-            __builtin_amdgcn_s_barrier();
-            compiler_fence();
-            if (L.wv == 1 && L.h == 0) {
+                float aa = SAME ? AT[cb] - AS[cb] : a.sT * AT[cb] - a.sS * AS[cb];
+                float zh = ZH[cb];
+                Run RS = stat_get(0, cb), RT = stat_get(1, cb);
 #pragma unroll
-                for (int cb = 0; cb < 4; ++cb) {
-                    float *o = xs + ((L.wt * 4 + cb) * 32 + L.l32) * 10;
-                    o[0] = RS[cb].best; o[1] = RS[cb].sec; o[2] = __int_as_float(RS[cb].idx);
-                    o[3] = RS[cb].z;
-                    o[4] = RT[cb].best; o[5] = RT[cb].sec; o[6] = __int_as_float(RT[cb].idx);
-                    o[7] = RT[cb].z; o[8] = AA[cb]; o[9] = ZH[cb];
-                }
-            }
-            compiler_fence();
-            __syncthreads();
-            if (L.wv == 0 && L.h == 0) {
-#pragma unroll
-                for (int cb = 0; cb < 4; ++cb) {
-                    const float *o = xs + ((L.wt * 4 + cb) * 32 + L.l32) * 10;
+                for (int off = 16; off <= 32; off <<= 1) {
+                    Run o{__shfl_xor(RS.best, off), __shfl_xor(RS.sec, off),
+                          __shfl_xor(RS.z, off), __shfl_xor(RS.idx, off)};
                     float dummy = 0.f;
-                    merge_run(RS[cb], dummy, Run{o[0], o[1], o[3], __float_as_int(o[2])}, 0.f,
-                              a.cS);
-                    merge_teacher(RT[cb], AA[cb], ZH[cb],
-                                  Run{o[4], o[5], o[7], __float_as_int(o[6])}, o[8], o[9], a.cT);
-                    const int j = p * XT + L.wt * 128 + cb * 32 + L.l32;
-                    if (j < t_valid) {
-                        float *P = a.part;
-                        const int64_t ps = a.pstride;
-                        P[(F_BEST_S * MAX_SPLITS + s) * ps + j] = RS[cb].best;
-                        P[(F_SEC_S * MAX_SPLITS + s) * ps + j] = RS[cb].sec;
-                        P[(F_IDX_S * MAX_SPLITS + s) * ps + j] = __int_as_float(RS[cb].idx);
-                        P[(F_Z_S * MAX_SPLITS + s) * ps + j] = RS[cb].z;
-                        P[(F_BEST_T * MAX_SPLITS + s) * ps + j] = RT[cb].best;
-                        P[(F_SEC_T * MAX_SPLITS + s) * ps + j] = RT[cb].sec;
-                        P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT[cb].idx);
-                        // the teacher's exp-sum carries the weights' 2^15 (exact)
-                        P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT[cb].z * 0x1p-15f;
-                        P[(F_A * MAX_SPLITS + s) * ps + j] = AA[cb];
-                        P[(F_ZH * MAX_SPLITS + s) * ps + j] = ZH[cb];
-                    }
+                    merge_run(RS, dummy, o, 0.f, a.cS);
+                    Run t{__shfl_xor(RT.best, off), __shfl_xor(RT.sec, off),
+                          __shfl_xor(RT.z, off), __shfl_xor(RT.idx, off)};
+                    const float ta = __shfl_xor(aa, off), tz = __shfl_xor(zh, off);
+                    merge_teacher(RT, aa, zh, t, ta, tz, a.cT);
+                }
+                const int j = p * XT + L.wid * 64 + cb * 16 + L.l16;
+                if (L.g == 0 && j < t_valid) {
+                    float *P = a.part;
+                    const int64_t ps = a.pstride;
+                    P[(F_BEST_S * MAX_SPLITS + s) * ps + j] = RS.best;
+                    P[(F_SEC_S * MAX_SPLITS + s) * ps + j] = RS.sec;
+                    P[(F_IDX_S * MAX_SPLITS + s) * ps + j] = __int_as_float(RS.idx);
+                    P[(F_Z_S * MAX_SPLITS + s) * ps + j] = RS.z;
+                    P[(F_BEST_T * MAX_SPLITS + s) * ps + j] = RT.best;
+                    P[(F_SEC_T * MAX_SPLITS + s) * ps + j] = RT.sec;
+                    P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT.idx);
+                    // the teacher's exp-sum carries the weights' 2^15 (exact)
+                    P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT.z * 0x1p-15f;
+                    P[(F_A * MAX_SPLITS + s) * ps + j] = aa;
+                    P[(F_ZH * MAX_SPLITS + s) * ps + j] = zh;
                 }
             }
+            // every wave is past its last read of the ring before the next unit's
+            // prologue refills it
             compiler_fence();
             __syncthreads();
         }
@@ -640,8 +649,13 @@ score_wide_kernel(ScoreArgs a) {
     Wide<SAME>::run(a);
 }
 
-// [V][d] bf16 weights -> K-blocked panels [d/32][vpad][32] (rows V .. vpad-1 zero).
-// Block (64-row group, panel); thread: row t/4, 16-byte chunk t&3.
+// Slot of 16-byte chunk q (0..3) of panel row r: the LDS swizzle of the stages, applied
+// when the panels are written (tiles start at multiples of 256 rows).
+__device__ __forceinline__ int panel_slot(int64_t r, int q) { return q ^ (int)((r >> 1) & 3); }
+
+// [V][d] bf16 weights -> K-blocked panels [d/32][vpad][32] (rows V .. vpad-1 zero), each
+// row's chunks in their swizzled slots. Block (64-row group, panel); thread: row t/4,
+// 16-byte chunk t&3.
 __global__ void __launch_bounds__(256)
 panel_w_kernel(const uint16_t *__restrict__ w, int64_t V, int d, int64_t vpad,
                uint16_t *__restrict__ out) {
@@ -649,12 +663,12 @@ panel_w_kernel(const uint16_t *__restrict__ w, int64_t V, int d, int64_t vpad,
     const int pnl = blockIdx.y, q = threadIdx.x & 3;
     uint4 val = make_uint4(0u, 0u, 0u, 0u);
     if (v < V) val = *(const uint4 *)(w + v * d + pnl * XK + q * 8);
-    *(uint4 *)(out + ((int64_t)pnl * vpad + v) * XK + q * 8) = val;
+    *(uint4 *)(out + ((int64_t)pnl * vpad + v) * XK + panel_slot(v, q) * 8) = val;
 }
 
-// The compacted hidden rows of a call -> K-blocked panels [d/32][prow][32]: row j <
-// t_valid is hidden row rowmap[j]; rows t_valid .. up to the next multiple of 256 are
-// zero (the last position tile's columns past the rows).
+// The compacted hidden rows of a call -> K-blocked panels [d/32][prow][32], chunks in
+// their swizzled slots: row j < t_valid is hidden row rowmap[j]; rows t_valid .. up to
+// the next multiple of 256 are zero (the last position tile's columns past the rows).
 __global__ void __launch_bounds__(256)
 panel_h_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restrict__ rowmap,
                const Sched *__restrict__ sched, int64_t prow, uint16_t *__restrict__ out) {
@@ -668,7 +682,7 @@ panel_h_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restrict
         const int64_t g = rowmap[j] & 0x7fffffffu;
         val = *(const uint4 *)(h + g * d + pnl * XK + q * 8);
     }
-    *(uint4 *)(out + ((int64_t)pnl * prow + j) * XK + q * 8) = val;
+    *(uint4 *)(out + ((int64_t)pnl * prow + j) * XK + panel_slot(j, q) * 8) = val;
 }
 
 }  // namespace
