@@ -28,19 +28,20 @@
 // Pipeline: K advances 32 elements per step. W and the hidden rows are read from
 // K-blocked panels ([d/32][rows][32] bf16, 64 bytes per row per panel), so one step of
 // a tile is a contiguous 16 KB for W (256 rows) and for H (256 positions): whole
-// 128-byte lines. The two 16 KB tiles land in one of 4 LDS stages (32 KB each) through
-// global_load_lds_dwordx4, issued three steps ahead. A step's 64 MFMAs run in two
+// 128-byte lines. The two 16 KB tiles land in one of 3 LDS stages (32 KB each) through
+// global_load_lds_dwordx4, issued two steps ahead. A step's 64 MFMAs run in two
 // halves of 8 row blocks; the second half runs under the next step's operand reads.
 // Stage rows are 64 bytes; the 16-byte chunk c of row r sits in slot c ^ ((r >> 1) & 3).
 // A ds_read_b128 of a 16x16x32 operand reads 16 rows x 4 chunks; of the XOR swizzles on
 // 16-byte slots measured on gfx950 only this one left it free of bank conflicts (the
 // 32x32x16 operand's 32 rows x 2 chunks are conflict-free with c ^ ((r >> 2) & 3)
 // instead). The panels are written with the swizzle already applied (rows are tile
-// rows modulo 256), so each DMA copies 1 KB linearly: DMAs whose lanes fetched permuted
-// pieces made the L2 fetch 2.2 to 3 times the bytes from the fabric.
+// rows modulo 256), so each DMA copies 1 KB linearly, whole lines per 8 lanes.
 //
 // The grid is persistent (one workgroup per CU); work units (position tile, split) are
-// ordered so that the 32 workgroups of one XCD share 8 position tiles x 4 splits.
+// ordered so that the 32 workgroups of one XCD share 8 position tiles x 4 splits. They
+// share those panel steps through the XCD's L2 only while they stay within some 15 K
+// steps of one another; a phase lock (Wide::phase_lock) keeps them there.
 #include <hip/hip_runtime.h>
 
 #include "fold.hpp"
