@@ -31,6 +31,7 @@
 
 #include "fold.hpp"
 #include "mfma_pipe.hpp"
+#include "phase_lock.hpp"
 #include "olive_device.hpp"
 #include "olive_internal.hpp"
 
@@ -273,8 +274,10 @@ struct Kernel {
     // The K sweep of one work unit: for every vocabulary tile vt0 .. vt1-1 the student
     // block (nS steps into accS), then the teacher block (nT steps into accT), then
     // tile_end(vt, row0) on the finished accumulators. Prefetch runs two steps ahead
-    // through the cursor, across block and tile ends.
-    template <class TileEnd>
+    // through the cursor, across block and tile ends. LOCK: phase-lock the XCD's
+    // workgroups at tile starts (the scoring pass; the backward's passes, whose tile ends
+    // hold more live state, leave it off).
+    template <bool LOCK, class TileEnd>
     static __device__ __forceinline__ void sweep(const ScoreArgs &a, const Lane &L, int vt0,
                                                  int vt1, int nS, int nT,
                                                  floatx16 (&accS)[4][2], floatx16 (&accT)[4][2],
@@ -306,7 +309,13 @@ struct Kernel {
             mma(P, ACC_);                                                                \
             __builtin_amdgcn_sched_barrier(0);                                           \
         }
+        // Phase lock of the XCD's workgroups (phase_lock.hpp); the first two tiles of a
+        // unit only measure the period.
+        const int G = gridDim.x;
+        const bool lock = LOCK && phase_lock_on(G, 2 * (nS + nT));
+        PhaseClock PH{0u, 0u};
         for (int vt = vt0; vt < vt1; ++vt) {
+            if (lock && L.wid == 0) phase_lock<DMA_PER_STEP * (NST - 2)>(PH, G);
             // The last tile, when V is not a multiple of 256, is shifted back to end at
             // V; its rows below vt*BV were covered by the previous tile.
             const int row0 = (vt * BV < a.V - BV) ? vt * BV : a.V - BV;
@@ -522,13 +531,13 @@ struct Kernel {
             // so only position tiles starting below n_scored hold any.
             const bool lists = TOPK && (int64_t)p * BT < n_scored;
             if (lists) {
-                sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+                sweep<true>(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                     if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
                     fold<true>(accS, accT, RS, RT, AA, BB, KS, KT, a,
                                row0 + L.wv * 128 + 4 * L.h, vt - vt0);
                 });
             } else {
-                sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+                sweep<true>(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                     if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);
                     fold<false>(accS, accT, RS, RT, AA, BB, KS, KT, a,
                                 row0 + L.wv * 128 + 4 * L.h, vt - vt0);
@@ -764,7 +773,7 @@ struct Kernel {
                 w.y = ok[cb] ? pack_bf16x2(gr[2], gr[3]) : 0u;
                 return w;
             };
-            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+            sweep<false>(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                 const int vlo = vt * BV;
                 const int vw0 = row0 + L.wv * 128;   // the wave's first row
                 if (row0 == vlo) {
@@ -894,7 +903,7 @@ struct Kernel {
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
             floatx16 accS[4][2], accT[4][2];
-            sweep(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
+            sweep<false>(a, L, vt0, vt1, nS, nT, accS, accT, [&](int vt, int row0) {
                 // rows of a shifted last tile below vt * BV get -2^99 in both models:
                 // p_hi = 0 there, and r stays finite
                 if (row0 != vt * BV) mask_mma(L, accS, accT, row0, vt * BV);

@@ -41,13 +41,14 @@
 // The grid is persistent (one workgroup per CU); work units (position tile, split) are
 // ordered so that the 32 workgroups of one XCD share 8 position tiles x 4 splits. They
 // share those panel steps through the XCD's L2 only while they stay within some 15 K
-// steps of one another; a phase lock (Wide::phase_lock) keeps them there.
+// steps of one another; a phase lock (phase_lock.hpp) keeps them there.
 #include <hip/hip_runtime.h>
 
 #include "fold.hpp"
 #include "mfma_pipe.hpp"
 #include "olive_device.hpp"
 #include "olive_internal.hpp"
+#include "phase_lock.hpp"
 
 namespace olive {
 
@@ -82,15 +83,6 @@ __device__ __forceinline__ void stat_put(int m, int cb, const Run &R) {
     p[8 * 256] = R.z;
     p[12 * 256] = __int_as_float(R.idx);
 }
-
-// Phase lock of one XCD's workgroups (Wide::phase_lock). g_phase[b]: the s_memrealtime
-// tick at which workgroup b last started a vocabulary tile; x_phase: wavefront 0's copy
-// of its XCD peers' entries, landed by a DMA issued one tile earlier. The entries steer
-// timing only: stale or foreign values (another launch on the device) cost at most one
-// bounded wait per tile, never a result.
-constexpr int XPH_MAX_GRID = 2048;
-__device__ uint32_t g_phase[XPH_MAX_GRID];
-__shared__ uint32_t x_phase[64];
 
 __device__ __forceinline__ uint32_t xring_addr() {
     return (uint32_t)(uintptr_t)(lds_void *)x_ring;
@@ -435,76 +427,6 @@ struct Wide {
         advance(C);
     }
 
-    // Phase lock. The workgroups of one XCD share each W and H panel step through that
-    // XCD's L2 only while they run within some 15 K steps of one another; left alone
-    // they drift 20 to 40 steps apart, the bytes fetched from the fabric double and the
-    // clock drops. Every workgroup sweeps the same K steps in every vocabulary tile, so
-    // what matters is the phase: the start time modulo the tile period D. At a tile
-    // start wavefront 0 reads the start times its XCD peers had published one tile
-    // earlier; if the peer furthest behind trails it by more than D/32 (some 8 K steps),
-    // it sleeps the excess, at most D/64 per tile. The wait is bounded by the clock,
-    // never by another workgroup.
-    struct Phase {
-        uint32_t prev, d;   // this workgroup's last tile start; its tile period (0: unknown)
-    };
-
-    static __device__ __forceinline__ int phase_peer(int G) {
-        const int lane = (int)(threadIdx.x & 63), b = (int)blockIdx.x;
-        const int j = lane * 8 + (b & 7);
-        return (lane < 32 && j < G && j != b) ? j : -1;
-    }
-
-    static __device__ __forceinline__ void phase_lock(Phase &P, int G) {
-        // The copy issued at the previous tile start has landed: this wave has issued the
-        // DMAs of at least one K step since, and this is the ring's own wait level.
-        __builtin_amdgcn_s_waitcnt(vmcnt_lgkm0_imm(XDMA_STEP * (XNST - 2)));
-        compiler_fence();
-        const int j = phase_peer(G);
-        const uint32_t peer_t = x_phase[threadIdx.x & 63];
-        const uint32_t now = (uint32_t)__builtin_amdgcn_s_memrealtime();
-        const int D = (int)P.d;
-        int lag = 0;
-        if (D > 0 && j >= 0) {
-            // the peer's entry predates the copy, about one tile ago: dt ~ -2D .. -D
-            int dt = (int)(peer_t - now);
-            if (dt > -3 * D && dt <= 0) {
-                dt += D;
-                if (dt < 0) dt += D;
-                if (dt < 0) dt += D;
-                if (dt < D / 2) lag = dt;   // the peer reaches this phase dt ticks later
-            }
-        }
-        // the largest lag over the 32 peer lanes, in scalar registers
-        int lmax = 0;
-#pragma unroll
-        for (int i = 0; i < 32; ++i) lmax = max(lmax, __builtin_amdgcn_readlane(lag, i));
-        const int w = min(lmax - (D >> 5), D >> 6);
-        if (w > 0) {
-            for (int it = 0; it < 4096 &&
-                             (int)((uint32_t)__builtin_amdgcn_s_memrealtime() - now) < w;
-                 ++it)
-                __builtin_amdgcn_s_sleep(1);
-        }
-        const uint32_t t1 = (uint32_t)__builtin_amdgcn_s_memrealtime();
-        if (threadIdx.x == 0)
-            __hip_atomic_store(&g_phase[blockIdx.x], t1, __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        P.d = P.prev ? t1 - P.prev : 0u;
-        P.prev = t1;
-        // copy the peers' entries (lanes without a peer copy this workgroup's own) for the
-        // next tile start: 4 bytes per lane into x_phase
-        const uint32_t voff = (uint32_t)(j >= 0 ? j : (int)blockIdx.x) * 4u;
-        const uint32_t la =
-            __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(lds_void *)x_phase);
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dword %1, %2 sc1"
-                     :
-                     : "s"(la), "v"(voff), "s"((const void *)g_phase)
-                     : "memory", "m0");
-#pragma clang diagnostic pop
-    }
-
     // Add kMasked to the rows at or past V of the padded last tile (one MFMA per block:
     // A holds kMasked in k = 0 of those rows, B ones), so they drop out of every
     // statistic while the accumulators stay MFMA-only.
@@ -564,9 +486,7 @@ struct Wide {
         const int nsb = ns / SG, rem = ns % SG;
         const int64_t full_units = (int64_t)nsb * SG * n_p;
 
-        // phase lock where the grid maps onto the 8 XCDs and a tile spans enough K steps
-        const bool lock = (G & 7) == 0 && G <= XPH_MAX_GRID && nS + nT >= 32;
-        Phase PH{0u, 0u};
+        const bool lock = phase_lock_on(G, nS + nT);
 
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
@@ -625,12 +545,11 @@ struct Wide {
             }
             // the first two tiles of a unit only measure the period (it straddles the
             // unit change)
-            PH.prev = 0u;
-            PH.d = 0u;
+            PhaseClock PH{0u, 0u};
             for (int vt = vt0; vt < vt1; ++vt) {
                 const int row0 = vt * XV;
                 const int vbase = row0 + 4 * L.g;
-                if (lock && L.wid == 0) phase_lock(PH, G);
+                if (lock && L.wid == 0) phase_lock<XDMA_STEP * (XNST - 2)>(PH, G);
                 OLIVE_XSTEPS(nT)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
