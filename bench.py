@@ -463,9 +463,9 @@ def measured_traffic(workload: str, kernel: str):
 # Each scoring kernel's source and the headers it includes.
 KERNEL_SOURCES = {
     "score_mfma": ("score_mfma.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
-                   "olive_internal.hpp"),
+                   "olive_internal.hpp", "phase_lock.hpp"),
     "score_wide": ("score_wide.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
-                   "olive_internal.hpp"),
+                   "olive_internal.hpp", "phase_lock.hpp"),
 }
 
 
