@@ -103,13 +103,14 @@ typedef struct {
  * 2 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
  * (3.1 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
 #define OLIVE_FLAG_BACKWARD 8
-/* Score forward-KL calls with the 256 x 128 two-model MFMA kernel instead of the
- * 256 x 256 one. Without this flag a bf16 teacher context on which the MFMA kernel
- * applies keeps K-blocked copies of both weights and a panel buffer for the hidden rows
- * of a call (2 (V rounded up to 256 + max_positions rounded up to 256) (d_S + d_T) bytes
- * of device memory: 1.9 GB + 0.4 GB for V = 151936, d_S + d_T = 6144 and 32768
- * positions), and its forward-KL calls without reverse KL or top-K outputs run the
- * 256 x 256 kernel. That kernel forms KL's cross term with the teacher's softmax weights
+/* Score with the 256 x 128 two-model MFMA kernel instead of the 256 x 256 one. Without
+ * this flag a bf16 context on which the MFMA kernel applies keeps K-blocked copies of its
+ * weights and a panel buffer for the hidden rows of a call (2 (V rounded up to 256 +
+ * max_positions rounded up to 256) (d_S + d_T) bytes of device memory, d_T = 0 for a
+ * student-only context: 1.9 GB + 0.4 GB for V = 151936, d_S + d_T = 6144 and 32768
+ * positions), and its student-only calls, forward-KL calls without reverse KL or top-K
+ * outputs, and the normaliser pass of olive_score_backward run the 256 x 256 kernel.
+ * That kernel forms KL's cross term with the teacher's softmax weights
  * held in fp16 and normalised by their own sum (Sec. 6's KL; the weights' rounding moves
  * a KL value by at most 2^-11 (1 - 2^-11)^-1 times the mean absolute deviation of the
  * logit difference under p_T, which is at most 2 (KL + TV)); every other output is

@@ -200,9 +200,9 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
     if (jsd && !mfma) return OLIVE_E_UNSUPPORTED;    // the JSD pass is an MFMA pass
-    // The 256 x 256 kernel takes forward-KL calls with a teacher; the reverse KL and the
+    // The 256 x 256 kernel takes student-only and forward-KL calls; the reverse KL and the
     // top-K lists need both models' logits side by side (the 256 x 128 kernel).
-    const bool wide = mfma && has_t && ctx->wide && !kl_rev && !topk;
+    const bool wide = mfma && ctx->wide && !kl_rev && !topk;
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
     // normalisers kept for a backward on this batch (MFMA path, backward contexts), and
     // read by the top-K stages and the JSD pass
@@ -257,9 +257,9 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     a.wmax_t = ctx->wmax_t;
     a.wmax_dev = ctx->wmax_dev;
     a.wps = ctx->wp_s;
-    a.wpt = ctx->wp_t;
+    a.wpt = has_t ? ctx->wp_t : nullptr;
     a.hps = ctx->hp_s;
-    a.hpt = ctx->hp_t;
+    a.hpt = has_t ? ctx->hp_t : nullptr;
     a.vpad = ctx->wp_rows;
     a.prow = ctx->hp_rows;
     a.wide = wide ? 1 : 0;
@@ -269,7 +269,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
         // the call's compacted hidden rows into panels (zero past them, to the tile end)
         s = check_hip(launch_panel_h(b->h_student, d.d_student, ctx->rowmap, ctx->sched,
                                      ctx->hp_rows, ctx->hp_s, st));
-        if (!s)
+        if (!s && has_t)
             s = check_hip(launch_panel_h(b->h_teacher, d.d_teacher, ctx->rowmap, ctx->sched,
                                          ctx->hp_rows, ctx->hp_t, st));
         if (s) return s;
@@ -277,7 +277,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     const int slot = (int)(ctx->n_calls % 64);
     if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
     if (wide)
-        s = check_hip(launch_score_wide(a, same_scale, grid, st));
+        s = check_hip(launch_score_wide(a, same_scale, has_t, grid, st));
     else if (mfma)
         s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, topk, grid, st));
     else
@@ -363,12 +363,21 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     const int64_t V = d.vocab;
     const int n_vtiles = (int)((V + 255) / 256);
     const int grid = ctx->n_cu;
-    olive_status s = check_hip(launch_prep(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->err,
-                                           go->counts, MFMA_BT, 0, n_vtiles, grid, 1, 1, st));
-    if (s) return s;
-    s = check_hip(launch_rowmap(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
-                                ctx->err, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                nullptr, nullptr, TopkOut{}, st));
+    // The row compaction and schedule, for position tiles of tile_rows: the normaliser
+    // pass runs the 256 x 256 kernel where the context keeps its panels, the gradient
+    // passes take 128-row tiles.
+    auto schedule = [&](int tile_rows) {
+        olive_status e = check_hip(launch_prep(*b, spans, true, V, ctx->seqbuf, ctx->sched,
+                                               ctx->err, go->counts, tile_rows, 0, n_vtiles,
+                                               grid, 1, 1, st));
+        if (!e)
+            e = check_hip(launch_rowmap(*b, spans, true, V, ctx->seqbuf, ctx->sched, ctx->rowmap,
+                                        ctx->err, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                        nullptr, nullptr, nullptr, TopkOut{}, st));
+        return e;
+    };
+    const bool wide = !reuse && ctx->wide;
+    olive_status s = schedule(wide ? WIDE_BT : MFMA_BT);
     if (s) return s;
     ScoreArgs a;
     a.hs = b->h_student;
@@ -391,18 +400,40 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     a.wmax_t = ctx->wmax_t;
     a.wmax_dev = ctx->wmax_dev;
     const bool same_scale = has_t && (a.sS == a.sT);
+    a.wps = ctx->wp_s;
+    a.wpt = has_t ? ctx->wp_t : nullptr;
+    a.hps = ctx->hp_s;
+    a.hpt = has_t ? ctx->hp_t : nullptr;
+    a.vpad = ctx->wp_rows;
+    a.prow = ctx->hp_rows;
+    a.wide = wide ? 1 : 0;
     const float *lse = ctx->fwd_lse;
     if (!reuse) {
         // the forward normalisers of the scored rows; they replace a forward call's for
         // reuse (always, wherever that call's are kept: one rule for every output set)
         ctx->fwd_lse_ok = false;
-        s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
+        if (wide) {
+            s = check_hip(launch_panel_h(b->h_student, d.d_student, ctx->rowmap, ctx->sched,
+                                         ctx->hp_rows, ctx->hp_s, st));
+            if (!s && has_t)
+                s = check_hip(launch_panel_h(b->h_teacher, d.d_teacher, ctx->rowmap,
+                                             ctx->sched, ctx->hp_rows, ctx->hp_t, st));
+            if (!s) s = check_hip(launch_score_wide(a, same_scale, has_t, grid, st));
+        } else {
+            s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
+        }
         if (s) return s;
         s = check_hip(launch_combine(a, true, has_t, same_scale, b->targets, ctx->err, nullptr,
                                      nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                      ctx->bw_lse, nullptr, 0, T, st));
         if (s) return s;
         lse = ctx->bw_lse;
+        if (wide) {
+            // the gradient passes' 128-row position tiles
+            s = schedule(MFMA_BT);
+            if (s) return s;
+            a.wide = 0;
+        }
     }
     const int ds = d.d_student;
     if (go->grad_h_student) {
@@ -709,16 +740,17 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         if (!s) s = dev_alloc(&c->bw_hrt, (size_t)ds * c->bw_chunk * 2);
         if (!s) s = backward_init(c, st);
     }
-    c->wide = c->mfma_ok && c->has_t && !(d.flags & OLIVE_FLAG_NARROW_TILE);
+    c->wide = c->mfma_ok && !(d.flags & OLIVE_FLAG_NARROW_TILE);
     if (!s && c->wide) {
         c->wp_rows = (V + MFMA_BV - 1) / MFMA_BV * MFMA_BV;
         c->hp_rows = (P + WIDE_BT - 1) / WIDE_BT * WIDE_BT;
         s = dev_alloc(&c->wp_s, (size_t)c->wp_rows * d.d_student * 2);
-        if (!s) s = dev_alloc(&c->wp_t, (size_t)c->wp_rows * d.d_teacher * 2);
         if (!s) s = dev_alloc(&c->hp_s, (size_t)c->hp_rows * d.d_student * 2);
-        if (!s) s = dev_alloc(&c->hp_t, (size_t)c->hp_rows * d.d_teacher * 2);
+        if (!s && c->has_t) s = dev_alloc(&c->wp_t, (size_t)c->wp_rows * d.d_teacher * 2);
+        if (!s && c->has_t) s = dev_alloc(&c->hp_t, (size_t)c->hp_rows * d.d_teacher * 2);
         if (!s && (launch_panel_w(c->ws, V, d.d_student, c->wp_rows, c->wp_s, st) != hipSuccess ||
-                   launch_panel_w(c->wt, V, d.d_teacher, c->wp_rows, c->wp_t, st) != hipSuccess))
+                   (c->has_t &&
+                    launch_panel_w(c->wt, V, d.d_teacher, c->wp_rows, c->wp_t, st) != hipSuccess)))
             s = OLIVE_E_HIP;
     }
     if (!s) s = dev_alloc(&c->logp_tmp, (size_t)P * sizeof(float));

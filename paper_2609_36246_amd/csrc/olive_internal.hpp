@@ -200,7 +200,8 @@ hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_
                                hipStream_t st);
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
                              bool topk, int grid, hipStream_t st);
-hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, int grid, hipStream_t st);
+hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, int grid,
+                             hipStream_t st);
 hipError_t launch_panel_w(const void *w, int64_t V, int d, int64_t vpad, void *out,
                           hipStream_t st);
 hipError_t launch_panel_h(const void *h, int d, const uint32_t *rowmap, const Sched *sched,

@@ -228,6 +228,17 @@ __device__ __forceinline__ void fold_student(const float (&z)[16], Run &R, float
     as = asum;
 }
 
+// Student of a student-only call, 16 logits of a column: running statistics only.
+__device__ __forceinline__ void fold_student_only(const float (&z)[16], Run &R, float c,
+                                                  int vcode0, float inf) {
+    R.z *= block_max(z, R, vcode0, c, inf);
+    const float mneg = -R.best * c;
+    float zsum = R.z;
+#pragma unroll
+    for (int q = 0; q < 16; ++q) zsum += fast_exp2(fmaf(z[q], c, mneg));
+    R.z = zsum;
+}
+
 // Merge the teacher record y (with its difference sum ya and weight sum yz) into x.
 __device__ __forceinline__ void merge_teacher(Run &x, float &xa, float &xz, const Run &y,
                                               float ya, float yz, float c) {
@@ -251,7 +262,9 @@ __device__ __forceinline__ void merge_teacher(Run &x, float &xa, float &xz, cons
     xz = wz + lz * r;
 }
 
-template <bool SAME>
+// HAS_T: a teacher block and fold precede the student's in every tile; without it the
+// call is student-only (SAME is then unused).
+template <bool SAME, bool HAS_T>
 struct Wide {
     struct Cursor {
         const char *w, *h;       // W and H tile of the step to prefetch
@@ -279,7 +292,7 @@ struct Wide {
             if (C.m == 1) {
                 enter<0>(C, a, C.vt);
             } else if (C.vt + 1 < C.vt1) {
-                enter<1>(C, a, C.vt + 1);
+                enter<HAS_T ? 1 : 0>(C, a, C.vt + 1);
             } else {
                 C.w -= C.wstep;
                 C.h -= C.hstep;
@@ -519,7 +532,7 @@ struct Wide {
             C.nS = nS;
             C.nT = nT;
             C.p = p;
-            enter<1>(C, a, vt0);
+            enter<HAS_T ? 1 : 0>(C, a, vt0);
 #pragma unroll
             for (int i = 0; i < XNST - 1; ++i) issue(a, L, C, i);
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): no scalar load pending
@@ -550,6 +563,7 @@ struct Wide {
                 const int row0 = vt * XV;
                 const int vbase = row0 + 4 * L.g;
                 if (lock && L.wid == 0) phase_lock<XDMA_STEP * (XNST - 2)>(PH, G);
+                if constexpr (HAS_T) {
                 OLIVE_XSTEPS(nT)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
@@ -587,6 +601,7 @@ struct Wide {
                         stat_put(1, cb, R);
                     }
                 }
+                }
                 OLIVE_XSTEPS(nS)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
@@ -599,7 +614,11 @@ struct Wide {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
                             col16(acc, qq, cb, z);
-                            fold_student(z, R, AS[cb], eh[qq][cb], a.cS, vbase + qq * 64, inf);
+                            if constexpr (HAS_T)
+                                fold_student(z, R, AS[cb], eh[qq][cb], a.cS, vbase + qq * 64,
+                                             inf);
+                            else
+                                fold_student_only(z, R, a.cS, vbase + qq * 64, inf);
                         }
                         stat_put(0, cb, R);
                     }
@@ -621,10 +640,12 @@ struct Wide {
                           __shfl_xor(RS.z, off), __shfl_xor(RS.idx, off)};
                     float dummy = 0.f;
                     merge_run(RS, dummy, o, 0.f, a.cS);
-                    Run t{__shfl_xor(RT.best, off), __shfl_xor(RT.sec, off),
-                          __shfl_xor(RT.z, off), __shfl_xor(RT.idx, off)};
-                    const float ta = __shfl_xor(aa, off), tz = __shfl_xor(zh, off);
-                    merge_teacher(RT, aa, zh, t, ta, tz, a.cT);
+                    if constexpr (HAS_T) {
+                        Run t{__shfl_xor(RT.best, off), __shfl_xor(RT.sec, off),
+                              __shfl_xor(RT.z, off), __shfl_xor(RT.idx, off)};
+                        const float ta = __shfl_xor(aa, off), tz = __shfl_xor(zh, off);
+                        merge_teacher(RT, aa, zh, t, ta, tz, a.cT);
+                    }
                 }
                 const int j = p * XT + L.wid * 64 + cb * 16 + L.l16;
                 if (L.g == 0 && j < t_valid) {
@@ -634,6 +655,7 @@ struct Wide {
                     P[(F_SEC_S * MAX_SPLITS + s) * ps + j] = RS.sec;
                     P[(F_IDX_S * MAX_SPLITS + s) * ps + j] = __int_as_float(RS.idx);
                     P[(F_Z_S * MAX_SPLITS + s) * ps + j] = RS.z;
+                    if (!HAS_T) continue;
                     P[(F_BEST_T * MAX_SPLITS + s) * ps + j] = RT.best;
                     P[(F_SEC_T * MAX_SPLITS + s) * ps + j] = RT.sec;
                     P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT.idx);
@@ -651,10 +673,10 @@ struct Wide {
     }
 };
 
-template <bool SAME>
+template <bool SAME, bool HAS_T>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_wide_kernel(ScoreArgs a) {
-    Wide<SAME>::run(a);
+    Wide<SAME, HAS_T>::run(a);
 }
 
 // Slot of 16-byte chunk q (0..3) of panel row r: the LDS swizzle of the stages, applied
@@ -695,14 +717,19 @@ panel_h_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restrict
 
 }  // namespace
 
-hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, int grid, hipStream_t st) {
+hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, int grid,
+                             hipStream_t st) {
     if (grid <= 0) return hipSuccess;
-    if (a.ds % XK != 0 || a.dt % XK != 0 || a.dt <= 0 || a.vpad % XV != 0 || a.prow % XT != 0)
+    if (a.ds <= 0 || a.ds % XK != 0 || a.vpad % XV != 0 || a.prow % XT != 0 || !a.wps ||
+        !a.hps)
         return hipErrorInvalidValue;
-    if (same_scale)
-        score_wide_kernel<true><<<grid, 256, 0, st>>>(a);
+    if (has_t && (a.dt <= 0 || a.dt % XK != 0 || !a.wpt || !a.hpt)) return hipErrorInvalidValue;
+    if (!has_t)
+        score_wide_kernel<false, false><<<grid, 256, 0, st>>>(a);
+    else if (same_scale)
+        score_wide_kernel<true, true><<<grid, 256, 0, st>>>(a);
     else
-        score_wide_kernel<false><<<grid, 256, 0, st>>>(a);
+        score_wide_kernel<false, true><<<grid, 256, 0, st>>>(a);
     return hipGetLastError();
 }
 

@@ -276,13 +276,16 @@ def test_multi_turn_workload_sampled():
 
 
 # student-only contexts: every block of a unit is a student block (one K step each in
-# narrow_k and v257), so each block end moves to the next vocabulary tile
+# narrow_k and v257), so each block end moves to the next vocabulary tile; both MFMA
+# kernels take them (the 256 x 256 one by default)
+@pytest.mark.parametrize("narrow", [False, True], ids=["wide", "narrow"])
 @pytest.mark.parametrize("case", ["ragged_v1000", "multi_tile", "narrow_k", "v257"])
-def test_student_only_token_logprobs(case):
-    say("student only", case)
+def test_student_only_token_logprobs(case, narrow):
+    say("student only", case, "narrow" if narrow else "wide")
     wl = custom(case, **CASES[case])
-    hip = run_hip(wl, student_only=True, outputs=("logp_s", "am_s"))
+    hip = run_hip(wl, student_only=True, outputs=("logp_s", "am_s"), narrow=narrow)
     assert hip["stats"]["kernel"] == "mfma"
+    assert hip["stats"]["tile"] == ("256x128" if narrow else "256x256")
     compare(hip, wl, student_only=True, label="student-only-" + case)
 
 
