@@ -43,6 +43,23 @@ namespace olive {
 #define OLIVE_SPLIT_GROUP 4
 #endif
 
+// Work unit q -> (position tile p, vocabulary split s) of n_p tiles x ns splits: units
+// cycle through groups of OLIVE_SPLIT_GROUP splits (the remainder last).
+__device__ __forceinline__ void unit_tile_split(int64_t q, int n_p, int ns, int &p, int &s) {
+    constexpr int SG = OLIVE_SPLIT_GROUP;
+    const int nsb = ns / SG, rem = ns % SG;
+    const int64_t full_units = (int64_t)nsb * SG * n_p;
+    if (q < full_units) {
+        const int64_t w = q % (SG * (int64_t)n_p);
+        p = (int)(w / SG);
+        s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
+    } else {
+        const int64_t w = q - full_units;
+        p = (int)(w / rem);
+        s = nsb * SG + (int)(w % rem);
+    }
+}
+
 struct Lane {
     int lane, wid, wv, wt, h, l32;
     int ldsoff[4];          // operand fetch offsets for the four k16 sub-steps
@@ -471,21 +488,9 @@ struct Kernel {
         const int G = gridDim.x;
         const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
         const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
-        constexpr int SG = OLIVE_SPLIT_GROUP;
-        const int nsb = ns / SG, rem = ns % SG;
-        const int64_t full_units = (int64_t)nsb * SG * n_p;
-
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
-            if (q < full_units) {
-                const int64_t w = q % (SG * (int64_t)n_p);
-                p = (int)(w / SG);
-                s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
-            } else {
-                const int64_t w = q - full_units;
-                p = (int)(w / rem);
-                s = nsb * SG + (int)(w % rem);
-            }
+            unit_tile_split(q, n_p, ns, p, s);
             // H DMA i of wave wid fills stage rows R = wid*32 + 8i + lane/8.
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
@@ -725,7 +730,8 @@ struct Kernel {
         const float wsum = z.w_ce + z.w_kl;
 
         for (int64_t q = my; q < n_units; q += G) {
-            const int p = (int)(q % n_p), s = (int)(q / n_p);
+            int p, s;
+            unit_tile_split(q, n_p, ns, p, s);
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
                 const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
@@ -877,7 +883,8 @@ struct Kernel {
         const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
 
         for (int64_t q = my; q < n_units; q += G) {
-            const int p = (int)(q % n_p), s = (int)(q / n_p);
+            int p, s;
+            unit_tile_split(q, n_p, ns, p, s);
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
                 const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
