@@ -441,6 +441,16 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         if (s) return s;
     }
     const int ch = ctx->bw_chunk;
+    // The cross-entropy's logit gradient runs on the 256 x 256 kernel where the context
+    // keeps its panels: its hidden-row panels hold every scored row (built by the
+    // normaliser pass, or here when that pass was skipped). Chunks start at multiples of
+    // 8192 rows (or at 0), so at tile boundaries of the panels.
+    const bool wide_dz = ctx->wide && !has_t && (ch % WIDE_BT == 0 || T <= ch);
+    if (wide_dz && !wide) {
+        s = check_hip(launch_panel_h(b->h_student, d.d_student, ctx->rowmap, ctx->sched,
+                                     ctx->hp_rows, ctx->hp_s, st));
+        if (s) return s;
+    }
     // scored rows <= T: chunks past the call's positions are never launched (those past
     // the scored count, known only on the device, exit at once)
     for (int64_t c0 = 0; c0 < T; c0 += ch) {
@@ -453,7 +463,16 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         z.w_ce = go->w_ce;
         z.w_kl = go->w_kl;
         z.dz_t = ctx->bw_dzt;
-        s = check_hip(launch_score_dz(a, z, has_t, grid, st));
+        if (wide_dz) {
+            ScoreArgs aw = a;
+            aw.wps = ctx->wp_s;
+            aw.hps = (const char *)ctx->hp_s + c0 * 64;   // panel row c0 (32 bf16 per row)
+            aw.vpad = ctx->wp_rows;
+            aw.prow = ctx->hp_rows;
+            s = check_hip(launch_score_wide_dz(aw, z, grid, st));
+        } else {
+            s = check_hip(launch_score_dz(a, z, has_t, grid, st));
+        }
         if (s) return s;
         if (go->grad_w_student) {
             s = check_hip(launch_zero_tail(ctx->bw_dzt, ctx->bw_vp, ch, ctx->sched, (int)c0, st));

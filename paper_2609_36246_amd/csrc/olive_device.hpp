@@ -63,6 +63,24 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, int64_t 
 // workgroups: the count minimising (rounds of the grid) x (vocabulary tiles per
 // split), the smallest among equals. The passes over the scored rows (logit gradient,
 // Jensen-Shannon) and the combine of the latter use it alike.
+// Work unit q -> (position tile p, vocabulary split s) of n_p tiles x ns splits: units
+// cycle through groups of SG splits (the remainder last), so that the 32 workgroups of
+// an XCD, which take consecutive units, share 32 / SG position tiles x SG splits.
+__device__ __forceinline__ void unit_tile_split(int64_t q, int n_p, int ns, int SG, int &p,
+                                                int &s) {
+    const int nsb = ns / SG, rem = ns % SG;
+    const int64_t full_units = (int64_t)nsb * SG * n_p;
+    if (q < full_units) {
+        const int64_t w = q % (SG * (int64_t)n_p);
+        p = (int)(w / SG);
+        s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
+    } else {
+        const int64_t w = q - full_units;
+        p = (int)(w / rem);
+        s = nsb * SG + (int)(w % rem);
+    }
+}
+
 __device__ __forceinline__ int pass_splits(int n_p, int n_vtiles, int G) {
     const int smax = n_vtiles < MAX_SPLITS ? n_vtiles : MAX_SPLITS;
     int ns = 1;

@@ -202,6 +202,7 @@ hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bo
                              bool topk, int grid, hipStream_t st);
 hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, int grid,
                              hipStream_t st);
+hipError_t launch_score_wide_dz(const ScoreArgs &a, const DzArgs &z, int grid, hipStream_t st);
 hipError_t launch_panel_w(const void *w, int64_t V, int d, int64_t vpad, void *out,
                           hipStream_t st);
 hipError_t launch_panel_h(const void *h, int d, const uint32_t *rowmap, const Sched *sched,

@@ -43,23 +43,6 @@ namespace olive {
 #define OLIVE_SPLIT_GROUP 4
 #endif
 
-// Work unit q -> (position tile p, vocabulary split s) of n_p tiles x ns splits: units
-// cycle through groups of OLIVE_SPLIT_GROUP splits (the remainder last).
-__device__ __forceinline__ void unit_tile_split(int64_t q, int n_p, int ns, int &p, int &s) {
-    constexpr int SG = OLIVE_SPLIT_GROUP;
-    const int nsb = ns / SG, rem = ns % SG;
-    const int64_t full_units = (int64_t)nsb * SG * n_p;
-    if (q < full_units) {
-        const int64_t w = q % (SG * (int64_t)n_p);
-        p = (int)(w / SG);
-        s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
-    } else {
-        const int64_t w = q - full_units;
-        p = (int)(w / rem);
-        s = nsb * SG + (int)(w % rem);
-    }
-}
-
 struct Lane {
     int lane, wid, wv, wt, h, l32;
     int ldsoff[4];          // operand fetch offsets for the four k16 sub-steps
@@ -490,7 +473,7 @@ struct Kernel {
         const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
-            unit_tile_split(q, n_p, ns, p, s);
+            unit_tile_split(q, n_p, ns, OLIVE_SPLIT_GROUP, p, s);
             // H DMA i of wave wid fills stage rows R = wid*32 + 8i + lane/8.
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
@@ -731,7 +714,7 @@ struct Kernel {
 
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
-            unit_tile_split(q, n_p, ns, p, s);
+            unit_tile_split(q, n_p, ns, OLIVE_SPLIT_GROUP, p, s);
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
                 const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);
@@ -884,7 +867,7 @@ struct Kernel {
 
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
-            unit_tile_split(q, n_p, ns, p, s);
+            unit_tile_split(q, n_p, ns, OLIVE_SPLIT_GROUP, p, s);
 #pragma unroll
             for (int i = 0; i < H_DMA; ++i) {
                 const int R = (L.wid * H_DMA + i) * 8 + (L.lane >> 3);

@@ -471,11 +471,7 @@ struct Wide {
             for (int r = 0; r < 4; ++r) z[4 * j + r] = agpr_read(acc[4 * q + j][cb][r]);
     }
 
-    static __device__ __forceinline__ void run(ScoreArgs a) {
-        const int t_valid = a.sched->t_valid;
-        const int n_p = a.sched->n_ptiles;
-        const int ns = a.sched->n_splits;
-        const int n_units = a.sched->n_units;
+    static __device__ __forceinline__ XLane make_lane() {
         XLane L;
         L.lane = threadIdx.x & 63;
         L.wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -491,27 +487,46 @@ struct Wide {
         const uint32_t lane_part = (uint32_t)(L.l16 * XROW + ((L.g ^ ((L.l16 >> 1) & 3)) << 4));
         L.lds_a = lane_part;
         L.lds_b = (uint32_t)(XW_BYTES + L.wid * 4 * 1024) + lane_part;
+        return L;
+    }
+
+    // One model block of COUNT_ K steps into acc: the first step has no pending half, the
+    // block's last half runs after the loop.
+#define OLIVE_XSTEPS(COUNT_)                                                              \
+            {                                                                             \
+                XFragA PA;                                                                \
+                XFragB PB;                                                                \
+                step<0>(a, L, C, st, acc, PA, PB);                                        \
+                st = st + 1 == XNST ? 0 : st + 1;                                         \
+                if ((COUNT_) > 1) {                                                       \
+                    step<1>(a, L, C, st, acc, PA, PB);                                    \
+                    st = st + 1 == XNST ? 0 : st + 1;                                     \
+                    for (int k = 2; k < (COUNT_); ++k) {                                  \
+                        step<2>(a, L, C, st, acc, PA, PB);                                \
+                        st = st + 1 == XNST ? 0 : st + 1;                                 \
+                    }                                                                     \
+                    mma_half<1, false, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);      \
+                } else {                                                                  \
+                    mma_half<1, true, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);       \
+                }                                                                         \
+                __builtin_amdgcn_sched_barrier(0);                                        \
+            }
+
+    static __device__ __forceinline__ void run(ScoreArgs a) {
+        const int t_valid = a.sched->t_valid;
+        const int n_p = a.sched->n_ptiles;
+        const int ns = a.sched->n_splits;
+        const int n_units = a.sched->n_units;
+        const XLane L = make_lane();
         const int nS = a.ds / XK, nT = a.dt / XK;
         const int G = gridDim.x;
         const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
         const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
-        constexpr int SG = XSPLIT_GROUP;
-        const int nsb = ns / SG, rem = ns % SG;
-        const int64_t full_units = (int64_t)nsb * SG * n_p;
-
         const bool lock = phase_lock_on(G, nS + nT);
 
         for (int64_t q = my; q < n_units; q += G) {
             int p, s;
-            if (q < full_units) {
-                const int64_t w = q % (SG * (int64_t)n_p);
-                p = (int)(w / SG);
-                s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
-            } else {
-                const int64_t w = q - full_units;
-                p = (int)(w / rem);
-                s = nsb * SG + (int)(w % rem);
-            }
+            unit_tile_split(q, n_p, ns, XSPLIT_GROUP, p, s);
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
 
@@ -537,25 +552,6 @@ struct Wide {
             for (int i = 0; i < XNST - 1; ++i) issue(a, L, C, i);
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): no scalar load pending
             int st = 0;
-#define OLIVE_XSTEPS(COUNT_)                                                              \
-            {                                                                             \
-                XFragA PA;                                                                \
-                XFragB PB;                                                                \
-                step<0>(a, L, C, st, acc, PA, PB);                                        \
-                st = st + 1 == XNST ? 0 : st + 1;                                         \
-                if ((COUNT_) > 1) {                                                       \
-                    step<1>(a, L, C, st, acc, PA, PB);                                    \
-                    st = st + 1 == XNST ? 0 : st + 1;                                     \
-                    for (int k = 2; k < (COUNT_); ++k) {                                  \
-                        step<2>(a, L, C, st, acc, PA, PB);                                \
-                        st = st + 1 == XNST ? 0 : st + 1;                                 \
-                    }                                                                     \
-                    mma_half<1, false, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);      \
-                } else {                                                                  \
-                    mma_half<1, true, 0, 0>(PA, PB, acc, C, L, 0u, x_ring, PA, PB);       \
-                }                                                                         \
-                __builtin_amdgcn_sched_barrier(0);                                        \
-            }
             // the first two tiles of a unit only measure the period (it straddles the
             // unit change)
             PhaseClock PH{0u, 0u};
@@ -624,7 +620,6 @@ struct Wide {
                     }
                 }
             }
-#undef OLIVE_XSTEPS
 
             // The difference sums (unscaled with equal scales; the combine multiplies by
             // s), then the 4 lanes of each column (row groups g = 0..3) merge.
@@ -671,12 +666,112 @@ struct Wide {
             __syncthreads();
         }
     }
+
+    // Logit-gradient pass of the backward's cross-entropy (student only) over the scored
+    // rows [c0, c0 + chunk) of the call, from the forward pass's normalisers: per tile,
+    // g = w_ce (p_S - onehot(y)), p_S = exp(s_S z_S - lse_S), stored as bf16 (round to
+    // nearest even) into dz_t, K-blocked panels [v/64][row][64] of the chunk's rows.
+    // a.hps points at the panel row of compacted row c0; the position tiles are 256 rows
+    // and c0 a multiple of 256.
+    static __device__ __forceinline__ void run_dz(ScoreArgs a, DzArgs z) {
+        const int t_all = a.sched->t_valid - z.c0;
+        const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
+        const int n_p = (t_rows + XT - 1) / XT;
+        const int G = gridDim.x;
+        const int ns = pass_splits(n_p, a.n_vtiles, G);
+        const int64_t n_units = (int64_t)n_p * ns;
+        const XLane L = make_lane();
+        const int nS = a.ds / XK, nT = 0;
+        const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+        const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+        const bool lock = phase_lock_on(G, nS);
+        const float wce = z.w_ce;
+
+        for (int64_t q = my; q < n_units; q += G) {
+            int p, s;
+            unit_tile_split(q, n_p, ns, XSPLIT_GROUP, p, s);
+            const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
+            const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
+            // the lane's 4 columns: chunk row, normaliser (log2 domain), target
+            int tcol[4], ycol[4];
+            float l2s[4];
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                tcol[cb] = p * XT + L.wid * 64 + cb * 16 + L.l16;
+                const bool ok = tcol[cb] < t_rows;
+                const int j = z.c0 + (ok ? tcol[cb] : 0);
+                l2s[cb] = ok ? z.lse[2 * (int64_t)j] * kLog2e : 0.f;
+                ycol[cb] = ok ? z.targets[a.rowmap[j] & 0x7fffffffu] : -1;
+                tcol[cb] = ok ? tcol[cb] : -1;
+            }
+            floatx4 acc[16][4];
+            Cursor C;
+            C.vt1 = vt1;
+            C.nS = nS;
+            C.nT = nT;
+            C.p = p;
+            enter<0>(C, a, vt0);
+#pragma unroll
+            for (int i = 0; i < XNST - 1; ++i) issue(a, L, C, i);
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): no scalar load pending
+            int st = 0;
+            PhaseClock PH{0u, 0u};
+            for (int vt = vt0; vt < vt1; ++vt) {
+                const int row0 = vt * XV;
+                if (lock && L.wid == 0) phase_lock<XDMA_STEP * (XNST - 2)>(PH, G);
+                OLIVE_XSTEPS(nS)
+                // Rows at or past V are not stored (dz_t's rows V .. vp-1 stay zero).
+                // Lane (l16, g) holds rows 16 vb + 4 g .. +3 of column cb: 8 bytes of one
+                // panel row.
+#pragma unroll
+                for (int vb = 0; vb < 16; ++vb) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    const int v0 = row0 + vb * 16 + 4 * L.g;
+#pragma unroll
+                    for (int cb = 0; cb < 4; ++cb) {
+                        float gr[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const float zs = agpr_read(acc[vb][cb][e]);
+                            gr[e] = wce * fast_exp2(fmaf(zs, a.cS, -l2s[cb]));
+                            gr[e] -= (v0 + e == ycol[cb]) ? wce : 0.f;
+                        }
+                        const int t = tcol[cb];
+                        if (t < 0 || v0 >= a.V) continue;
+                        uint16_t *dst = z.dz_t + (((int64_t)(v0 >> 6) * z.chunk + t) * 64 +
+                                                  (v0 & 63));
+                        if (v0 + 4 <= a.V) {
+                            *(uint2 *)dst = make_uint2(pack_bf16x2(gr[0], gr[1]),
+                                                       pack_bf16x2(gr[2], gr[3]));
+                        } else {
+                            const uint32_t w0 = pack_bf16x2(gr[0], gr[1]);
+                            const uint32_t w1 = pack_bf16x2(gr[2], gr[3]);
+                            const uint16_t h4[4] = {(uint16_t)w0, (uint16_t)(w0 >> 16),
+                                                    (uint16_t)w1, (uint16_t)(w1 >> 16)};
+                            for (int e = 0; e < 4 && v0 + e < a.V; ++e) dst[e] = h4[e];
+                        }
+                    }
+                }
+            }
+            // every DMA landed and every wave is done with the ring before the next
+            // unit's prologue refills it
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __syncthreads();
+        }
+    }
+#undef OLIVE_XSTEPS
 };
 
 template <bool SAME, bool HAS_T>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_wide_kernel(ScoreArgs a) {
     Wide<SAME, HAS_T>::run(a);
+}
+
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+score_wide_dz_kernel(ScoreArgs a, DzArgs z) {
+    Wide<false, false>::run_dz(a, z);
 }
 
 // Slot of 16-byte chunk q (0..3) of panel row r: the LDS swizzle of the stages, applied
@@ -730,6 +825,15 @@ hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, in
         score_wide_kernel<true, true><<<grid, 256, 0, st>>>(a);
     else
         score_wide_kernel<false, true><<<grid, 256, 0, st>>>(a);
+    return hipGetLastError();
+}
+
+hipError_t launch_score_wide_dz(const ScoreArgs &a, const DzArgs &z, int grid, hipStream_t st) {
+    if (grid <= 0) return hipSuccess;
+    if (a.ds <= 0 || a.ds % XK != 0 || a.vpad % XV != 0 || !a.wps || !a.hps || !z.dz_t ||
+        z.c0 % XT != 0 || z.chunk <= 0)
+        return hipErrorInvalidValue;
+    score_wide_dz_kernel<<<grid, 256, 0, st>>>(a, z);
     return hipGetLastError();
 }
 

@@ -33,7 +33,7 @@ def custom(name, seed=0, **kw):
 
 
 def run_backward(wl, w_ce=1.0, w_kl=0.0, region=L.OLIVE_REGION_TEACHER, want=("h", "w"),
-                 layout=L.OLIVE_W_DV, ctx=None, keep_ctx=False):
+                 layout=L.OLIVE_W_DV, ctx=None, keep_ctx=False, narrow=False):
     spec = wl["spec"]
     T = wl["total_positions"]
     B = wl["cu_seqlens"].shape[0] - 1
@@ -45,7 +45,8 @@ def run_backward(wl, w_ce=1.0, w_kl=0.0, region=L.OLIVE_REGION_TEACHER, want=("h
             ws, wt = ws.t().contiguous(), wt.t().contiguous()
         desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher, L.OLIVE_BF16, layout,
                            wl["scale_student"], wl["scale_teacher"], max_positions=T,
-                           max_seqs=B, flags=L.OLIVE_FLAG_BACKWARD)
+                           max_seqs=B, flags=L.OLIVE_FLAG_BACKWARD |
+                           (L.OLIVE_FLAG_NARROW_TILE if narrow else 0))
         ctx = L.olive_score_init(desc, ws, wt)
     gh = torch.full((T, spec.d_student), float("nan"), dtype=torch.float32, device=dev) \
         if "h" in want else None
@@ -152,6 +153,18 @@ def test_backward_full(case, w_kl):
     assert list(hip["counts"]) == [m["n_scored"], m["t_valid"]]
     ref = oracle_backward(wl, 1.0, w_kl, O.REGION_TEACHER)
     check_grads(hip, ref, wl, "%s-%s" % (case, w_kl))
+
+
+# The cross-entropy's normaliser and logit-gradient passes run on the 256 x 256 kernel by
+# default; OLIVE_FLAG_NARROW_TILE keeps them on the 256 x 128 one.
+@pytest.mark.parametrize("case", ["ragged_v1000", "v257"])
+def test_backward_narrow_tile(case):
+    say("backward, 256 x 128 kernel", case)
+    wl = custom(case, **CASES[case])
+    hip = run_backward(wl, 1.0, 0.0, narrow=True)
+    assert hip["err"] == 0
+    ref = oracle_backward(wl, 1.0, 0.0, O.REGION_TEACHER)
+    check_grads(hip, ref, wl, "narrow-%s" % case)
 
 
 @pytest.mark.parametrize("region", [O.REGION_STUDENT, O.REGION_ALL])
