@@ -176,14 +176,16 @@ def test_backward_regions_and_kl_only(region):
     check_grads(hip, ref, wl, "region%d" % region)
 
 
-def test_backward_spans_and_vd_layout():
-    say("backward with span masks, weights in the [V][d] layout")
+# w_kl = 0: the cross-entropy alone takes the 256 x 256 logit-gradient pass
+@pytest.mark.parametrize("w_kl", [0.25, 0.0], ids=["ce+kl", "ce"])
+def test_backward_spans_and_vd_layout(w_kl):
+    say("backward with span masks, weights in the [V][d] layout, w_kl", w_kl)
     wl = custom("turns", num_seqs=3, vocab=1000, d_student=128, d_teacher=256,
                 target_source="teacher", turns=(4, 16, 3, 2, 4, 24, 4, 40))
-    hip = run_backward(wl, 1.0, 0.25, O.REGION_SPANS, layout=L.OLIVE_W_VD)
+    hip = run_backward(wl, 1.0, w_kl, O.REGION_SPANS, layout=L.OLIVE_W_VD)
     assert hip["err"] == 0
-    ref = oracle_backward(wl, 1.0, 0.25, O.REGION_SPANS)
-    check_grads(hip, ref, wl, "turns-vd")
+    ref = oracle_backward(wl, 1.0, w_kl, O.REGION_SPANS)
+    check_grads(hip, ref, wl, "turns-vd-%s" % w_kl)
 
 
 def test_backward_chunks_and_repeat():
