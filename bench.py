@@ -464,8 +464,8 @@ def measured_traffic(workload: str, kernel: str):
 KERNEL_SOURCES = {
     "score_mfma": ("score_mfma.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
                    "olive_internal.hpp", "phase_lock.hpp"),
-    "score_wide": ("score_wide.hip", "fold.hpp", "mfma_pipe.hpp", "olive_device.hpp",
-                   "olive_internal.hpp", "phase_lock.hpp"),
+    "score_wide": ("score_wide.hip", "wide_pipe.hpp", "fold.hpp", "mfma_pipe.hpp",
+                   "olive_device.hpp", "olive_internal.hpp", "phase_lock.hpp"),
 }
 
 
