@@ -139,6 +139,9 @@ CASES = {
                  logit_scale=2.0, cut_rule=("abs", 1, 149)),
     "v1001": dict(num_seqs=3, ragged_len=(60, 200), vocab=1001, d_student=128,
                   d_teacher=64, target_source="student", cut_rule=("frac", 0.1, 0.9)),
+    # wider hidden states over several 256-row position tiles and a ragged vocabulary
+    "d512": dict(num_seqs=4, ragged_len=(300, 700), vocab=3001, d_student=512,
+                 d_teacher=256, logit_scale=2.0, cut_rule=("frac", 0.1, 0.9)),
 }
 
 
@@ -203,6 +206,18 @@ def test_backward_chunks_and_repeat():
     assert m["n_scored"] > 8192
     ref = oracle_backward(wl, 1.0, 0.0, O.REGION_TEACHER)
     check_grads(a, ref, wl, "chunks")
+
+
+def test_backward_second_chunk_with_wider_rows():
+    """d_S = 256 (whole 256-row blocks of dL/dh) on the second gradient chunk's rows."""
+    say("backward over two chunks, d_S = 256")
+    wl = custom("chunks256", num_seqs=3, seq_len=3200, vocab=600, d_student=256,
+                d_teacher=64, cut_rule=("abs", 1, 10))
+    hip = run_backward(wl, 1.0, 0.0)
+    m = masks_of(wl, O.REGION_TEACHER)
+    assert m["n_scored"] > 8192
+    ref = oracle_backward(wl, 1.0, 0.0, O.REGION_TEACHER)
+    check_grads(hip, ref, wl, "chunks256")
 
 
 def test_backward_empty_region_gives_zero():
