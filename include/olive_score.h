@@ -52,7 +52,7 @@ typedef enum {
     OLIVE_E_RANGE = 4,       /* a value is out of range (logit scale not finite and > 0, region) */
     OLIVE_E_HIP = 5,         /* a HIP runtime call failed */
     OLIVE_E_NOMEM = 6,       /* device allocation failed at init */
-    OLIVE_E_UNSUPPORTED = 7, /* valid but not supported by this build (see each field) */
+    OLIVE_E_UNSUPPORTED = 7, /* valid but not supported by this library (see each field) */
     OLIVE_E_LIMIT = 8        /* beyond the fixed limits of olive_kl_masked_static */
 } olive_status;
 

@@ -58,7 +58,7 @@ def _task(args):
 
 
 def workers() -> int:
-    """Worker count: the host cores, at most 16 (the CPU share of one GPU machine)."""
+    """Worker count: the host cores, at most 16 (a shared host gives one GPU about 16)."""
     n = os.cpu_count() or 1
     try:
         n = min(n, len(os.sched_getaffinity(0)))
