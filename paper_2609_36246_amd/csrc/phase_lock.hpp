@@ -12,10 +12,11 @@
 // vector store into g_phase) and compares it with the start times its XCD peers had
 // published one tile earlier, which a DMA issued at its previous tile start copied into
 // x_phase (so the read costs no latency). If the peer furthest behind trails by more
-// than D/32 (some 8 K steps), it sleeps the excess, at most D/64 per tile. The wait is
-// bounded by the clock alone, never by another workgroup's progress, so no workgroup
-// can block another. The entries steer timing only: stale or foreign values (another
-// launch on the device) cost at most one bounded wait per tile, never a result.
+// than D/32 (some 6 steps of 32 K elements on long_rollout), it sleeps the excess, at
+// most D/64 per tile. The wait is bounded by the clock alone, never by another
+// workgroup's progress, so no workgroup can block another. The entries steer timing
+// only: stale or foreign values (another launch on the device) cost at most one bounded
+// wait per tile, never a result.
 #pragma once
 
 #include <hip/hip_runtime.h>
