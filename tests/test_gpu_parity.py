@@ -14,7 +14,8 @@ from oracle import olive_oracle as O
 from paper_2609_36246_amd import _lib as L
 from paper_2609_36246_amd import workloads as W
 from tests.gpu_harness import (CE_RTOL, KL_ATOL, KL_RTOL, LOGP_ATOL, compare, masks_of,
-                               oracle_rows, parity_rows, run_hip, say, stratified_rows)
+                               oracle_rows, parity_rows, run_hip, say, stratified_rows,
+                               to_np)
 
 pytestmark = pytest.mark.gpu
 
@@ -531,6 +532,50 @@ def test_deterministic_and_fully_written():
         np.testing.assert_array_equal(a[k], b[k])
     for k in ("am_s", "am_t"):
         np.testing.assert_array_equal(a[k], b[k])
+
+
+def test_concurrent_calls_on_two_streams_match_calls_alone():
+    """Two contexts score two batches at once on two streams, with tiles long enough
+    (d_S + d_T = 1024) for the 256 x 256 kernel's phase lock. Both launches then read
+    and write the one device array of tile start times; those steer timing only, so
+    every output equals, bit for bit, the same call made alone."""
+    say("two streams at once, phase-locked kernels")
+    kw = dict(num_seqs=4, ragged_len=(400, 900), vocab=6000, d_student=512, d_teacher=512,
+              cut_rule=("frac", 0.1, 0.9))
+    wls = [custom("conc%d" % i, seed=i, **kw) for i in range(2)]
+    alone = [run_hip(wl) for wl in wls]
+    assert all(r["stats"]["tile"] == "256x256" for r in alone)
+    ctxs, outs, batches = [], [], []
+    for wl in wls:
+        spec, T = wl["spec"], wl["total_positions"]
+        B = wl["cu_seqlens"].shape[0] - 1
+        desc = L.make_desc(spec.vocab, spec.d_student, spec.d_teacher, L.OLIVE_BF16,
+                           L.OLIVE_W_DV, wl["scale_student"], wl["scale_teacher"],
+                           max_positions=T, max_seqs=B)
+        ctxs.append(L.olive_score_init(desc, wl["w_student"], wl["w_teacher"]))
+        dev = wl["h_student"].device
+        outs.append(dict(kl=torch.full((T,), float("nan"), device=dev),
+                         counts=torch.full((2,), -1, dtype=torch.int64, device=dev),
+                         logp_s=torch.full((T,), float("nan"), device=dev),
+                         logp_t=torch.full((T,), float("nan"), device=dev),
+                         am_s=torch.full((T,), -7, dtype=torch.int32, device=dev),
+                         am_t=torch.full((T,), -7, dtype=torch.int32, device=dev),
+                         ce=torch.full((B,), float("nan"), device=dev)))
+        batches.append(L.make_batch(wl["cu_seqlens"], wl["cut"], wl["targets"],
+                                    wl["h_student"], wl["h_teacher"], wl["valid_len"]))
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    for _ in range(3):
+        for i in range(2):
+            o = outs[i]
+            L.olive_kl_masked(ctxs[i], batches[i], o["kl"], o["counts"], o["logp_s"],
+                              o["logp_t"], o["am_s"], o["am_t"], o["ce"], streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert L.olive_score_last_error(ctxs[i]) == 0
+        for k in ("kl", "logp_s", "logp_t", "am_s", "am_t", "ce", "counts"):
+            np.testing.assert_array_equal(to_np(outs[i][k]), alone[i][k], err_msg=k)
+        L.olive_score_free(ctxs[i])
 
 
 def test_cut_extremes():
