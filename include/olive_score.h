@@ -303,7 +303,8 @@ typedef struct {
  * Backward pass of the student's loss: dL/dh_S and dL/dW_S for the scaled logits
  * z_S = s_S h_S W_S. Per scored position the logit gradient is
  * w_ce (p_S - onehot(y)) + w_kl (p_S - p_T); it is formed in one fused pass over the
- * vocabulary (recomputing both models' logits from the forward normalisers) and held
+ * vocabulary (recomputing the student's logits, and the teacher's when w_kl != 0, from
+ * the forward normalisers) and held
  * in bf16 (round to nearest even) as the operand of the two products
  * dL/dh = s_S g W^T and dL/dW = s_S h^T g, which accumulate in fp32.
  * spans: NULL, or the scored spans when b->region is OLIVE_REGION_SPANS.
