@@ -184,6 +184,9 @@ def main():
                          "instead of the 256 x 256 one")
     ap.add_argument("--reverse-kl", action="store_true",
                     help="also form KL(student || teacher) in the same pass (olive_score_batch)")
+    ap.add_argument("--reverse-kl-only", action="store_true",
+                    help="form KL(student || teacher) instead of KL(teacher || student) "
+                         "(olive_score_batch with kl_reverse set and kl NULL)")
     ap.add_argument("--region-only", action="store_true",
                     help="score only the region's positions (OLIVE_OUT_REGION_ONLY): the rate "
                          "and the roofline then count scored positions")
@@ -256,14 +259,15 @@ def main():
     stream = torch.cuda.current_stream()
     ctx = L.olive_score_init(desc, wl["w_student"], wl["w_teacher"], stream)
     dev = wl["h_student"].device
-    kl = torch.empty(T, dtype=torch.float32, device=dev)
+    kl = None if args.reverse_kl_only else torch.empty(T, dtype=torch.float32, device=dev)
     counts = torch.empty(2, dtype=torch.int64, device=dev)
     lps = torch.empty(T, dtype=torch.float32, device=dev)
     lpt = torch.empty(T, dtype=torch.float32, device=dev)
     ams = torch.empty(T, dtype=torch.int32, device=dev)
     amt = torch.empty(T, dtype=torch.int32, device=dev)
     ce = torch.empty(B, dtype=torch.float32, device=dev)
-    klr = torch.empty(T, dtype=torch.float32, device=dev) if args.reverse_kl else None
+    klr = torch.empty(T, dtype=torch.float32, device=dev) \
+        if (args.reverse_kl or args.reverse_kl_only) else None
     tk = dict(topk_overlap=torch.empty(T, dtype=torch.float32, device=dev),
               kl_topk=torch.empty(T, dtype=torch.float32, device=dev),
               topk_student=torch.empty(T, L.OLIVE_TOPK, dtype=torch.int32, device=dev),
@@ -282,7 +286,7 @@ def main():
     def step():
         if use_spans:
             L.olive_score_batch_spans(ctx, batch, spans, outs, stream)
-        elif args.reverse_kl or args.region_only or args.topk:
+        elif args.reverse_kl or args.reverse_kl_only or args.region_only or args.topk:
             L.olive_score_batch(ctx, batch, outs, stream)
         else:
             L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
@@ -310,10 +314,11 @@ def main():
         % (args.steps, ms_step, kernel_ms, stats, err))
     flops = 2.0 * rows * spec.vocab * (spec.d_student + spec.d_teacher)
     achieved = flops / (kernel_ms * 1e-3) / 1e12
-    # the dominant kernel of the call: the 256 x 256 one, or the 256 x 128 one (reverse KL,
-    # top-K, OLIVE_FLAG_NARROW_TILE)
+    # the dominant kernel of the call: the 256 x 256 one, or the 256 x 128 one (both KL
+    # directions, top-K, OLIVE_FLAG_NARROW_TILE)
     kernel = "score_wide" if stats.get("tile") == "256x256" else "score_mfma"
-    traffic = None if (args.reverse_kl or args.region_only or args.topk) \
+    traffic = None if (args.reverse_kl or args.reverse_kl_only or args.region_only or
+                       args.topk) \
         else measured_traffic(args.workload, kernel)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
@@ -333,7 +338,8 @@ def main():
             "valid_positions": t_valid, "scored_positions": n_scored, "vocab": spec.vocab,
             "d_student": spec.d_student, "d_teacher": spec.d_teacher,
             "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
-            "reverse_kl": bool(args.reverse_kl), "region_only": bool(args.region_only),
+            "reverse_kl": bool(args.reverse_kl), "reverse_kl_only": bool(args.reverse_kl_only),
+            "region_only": bool(args.region_only),
             "topk": bool(args.topk), "topk_filtered_pairs": stats["topk_filtered"],
             "topk_scanned_pairs": stats["topk_scanned"],
             "region": "spans" if use_spans else "teacher",

@@ -108,13 +108,14 @@ typedef struct {
  * weights and a panel buffer for the hidden rows of a call (2 (V rounded up to 256 +
  * max_positions rounded up to 256) (d_S + d_T) bytes of device memory, d_T = 0 for a
  * student-only context: 1.9 GB + 0.4 GB for V = 151936, d_S + d_T = 6144 and 32768
- * positions), and its student-only calls, forward-KL calls without reverse KL or top-K
- * outputs, and the normaliser pass of olive_score_backward run the 256 x 256 kernel.
- * That kernel forms KL's cross term with the teacher's softmax weights
- * held in fp16 and normalised by their own sum (Sec. 6's KL; the weights' rounding moves
- * a KL value by at most 2^-11 (1 - 2^-11)^-1 times the mean absolute deviation of the
- * logit difference under p_T, which is at most 2 (KL + TV)); every other output is
- * formed as in the 256 x 128 kernel. */
+ * positions), and its student-only calls, calls with one KL direction (kl or kl_reverse,
+ * not both) and no top-K output, and the normaliser pass of olive_score_backward run the
+ * 256 x 256 kernel. That kernel forms KL's cross term with the softmax weights of the
+ * divergence's first distribution (p_T for kl, p_S for kl_reverse) held in fp16 and
+ * normalised by their own sum (Sec. 6's KL; the weights' rounding moves a KL value by at
+ * most 2^-11 (1 - 2^-11)^-1 times the mean absolute deviation of the logit difference
+ * under that distribution, which is at most 2 (KL + TV)); every other output is formed
+ * as in the 256 x 128 kernel. */
 #define OLIVE_FLAG_NARROW_TILE 16
 
 /* One packed batch of stitched sequences (Sec. 3.1: x, y_1..k, continuation). */

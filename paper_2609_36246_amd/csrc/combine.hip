@@ -92,7 +92,7 @@ __device__ __forceinline__ void wave_merge(Stat &st, float &acc, float c) {
 }
 
 // The same with a second accumulator rescaled like z (the 256 x 256 kernel's sum of
-// fp16 teacher weights).
+// the fp16 weights it kept, of the model whose max z follows).
 __device__ __forceinline__ void wave_merge2(Stat &st, float &acc, float &acc2, float c) {
     for (int off = 32; off > 0; off >>= 1) {
         Stat o;
@@ -162,14 +162,17 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
         ss = load_stat(a.part, a.pstride, F_BEST_S, lane, j);
         if (HAS_T) {
             st = load_stat(a.part, a.pstride, F_BEST_T, lane, j);
-            acc_a = a.part[(F_A * MAX_SPLITS + lane) * a.pstride + j];
+            if (kl) acc_a = a.part[(F_A * MAX_SPLITS + lane) * a.pstride + j];
             if (kl_rev) acc_b = a.part[(F_B * MAX_SPLITS + lane) * a.pstride + j];
             if (a.wide) acc_zh = a.part[(F_ZH * MAX_SPLITS + lane) * a.pstride + j];
         }
     }
-    wave_merge(ss, acc_b, a.cS);
+    // the 256 x 256 kernel's fp16 weight sums follow the model whose weights it kept
+    const bool zh_s = HAS_T && a.wide == 2, zh_t = HAS_T && a.wide == 1;
+    if (zh_s) wave_merge2(ss, acc_b, acc_zh, a.cS);
+    else wave_merge(ss, acc_b, a.cS);
     if (HAS_T) {
-        if (a.wide) wave_merge2(st, acc_a, acc_zh, a.cT);
+        if (zh_t) wave_merge2(st, acc_a, acc_zh, a.cT);
         else wave_merge(st, acc_a, a.cT);
     }
     // Every lane now holds the merged statistics.
@@ -205,13 +208,14 @@ combine_kernel(ScoreArgs a, int same_scale, const int32_t *__restrict__ targets,
             // the teacher-weighted mean of the logit difference: A / Z_T, or with the
             // 256 x 256 kernel's fp16 weights A / (their sum)
             float an = same_scale ? a.sT * acc_a : acc_a;
-            float v = an / (a.wide ? acc_zh : st.z) - lse_t + lse_s;
+            float v = an / (zh_t ? acc_zh : st.z) - lse_t + lse_s;
             kl[g] = inr ? v : 0.f;
         }
         if (kl_rev) {
-            // KL(student || teacher) = sum p_S (s_S zS - s_T zT) - lse_S + lse_T
+            // KL(student || teacher) = sum p_S (s_S zS - s_T zT) - lse_S + lse_T, or with
+            // the 256 x 256 kernel's fp16 student weights B / (their sum)
             float bn = same_scale ? a.sS * acc_b : acc_b;
-            float v = bn / ss.z - lse_s + lse_t;
+            float v = bn / (zh_s ? acc_zh : ss.z) - lse_s + lse_t;
             kl_rev[g] = inr ? v : 0.f;
         }
     }

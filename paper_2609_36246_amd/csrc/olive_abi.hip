@@ -200,9 +200,11 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
                       (!has_t || ((uintptr_t)b->h_teacher & 15) == 0);
     if (topk && !mfma) return OLIVE_E_UNSUPPORTED;   // the top-K lists come from the MFMA pass
     if (jsd && !mfma) return OLIVE_E_UNSUPPORTED;    // the JSD pass is an MFMA pass
-    // The 256 x 256 kernel takes student-only and forward-KL calls; the reverse KL and the
-    // top-K lists need both models' logits side by side (the 256 x 128 kernel).
-    const bool wide = mfma && ctx->wide && !kl_rev && !topk;
+    // The 256 x 256 kernel takes student-only calls and calls with one KL direction; both
+    // directions at once and the top-K lists need both models' logits side by side (the
+    // 256 x 128 kernel).
+    const bool wide = mfma && ctx->wide && !(kl && kl_rev) && !topk;
+    const bool wide_rev = wide && kl_rev;
     float *logp_tmp = (ce && !logp_s) ? ctx->logp_tmp : nullptr;
     // normalisers kept for a backward on this batch (MFMA path, backward contexts), and
     // read by the top-K stages and the JSD pass
@@ -262,7 +264,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     a.hpt = has_t ? ctx->hp_t : nullptr;
     a.vpad = ctx->wp_rows;
     a.prow = ctx->hp_rows;
-    a.wide = wide ? 1 : 0;
+    a.wide = wide ? (wide_rev ? 2 : 1) : 0;
     const bool same_scale = has_t && (a.sS == a.sT);
 
     if (wide) {
@@ -277,7 +279,7 @@ olive_status run(olive_score_ctx *ctx, const olive_batch *b, const olive_spans *
     const int slot = (int)(ctx->n_calls % 64);
     if (ctx->timing && hipEventRecord(ctx->ev[0][slot], st) != hipSuccess) return OLIVE_E_HIP;
     if (wide)
-        s = check_hip(launch_score_wide(a, same_scale, has_t, grid, st));
+        s = check_hip(launch_score_wide(a, same_scale, has_t, wide_rev, grid, st));
     else if (mfma)
         s = check_hip(launch_score_mfma(a, has_t, same_scale, has_t && kl_rev, topk, grid, st));
     else
@@ -418,7 +420,7 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
             if (!s && has_t)
                 s = check_hip(launch_panel_h(b->h_teacher, d.d_teacher, ctx->rowmap,
                                              ctx->sched, ctx->hp_rows, ctx->hp_t, st));
-            if (!s) s = check_hip(launch_score_wide(a, same_scale, has_t, grid, st));
+            if (!s) s = check_hip(launch_score_wide(a, same_scale, has_t, false, grid, st));
         } else {
             s = check_hip(launch_score_mfma(a, has_t, same_scale, false, false, grid, st));
         }

@@ -132,7 +132,8 @@ struct ScoreArgs {
     // zero past V) and of the call's compacted hidden rows (rows = prow)
     const void *wps, *wpt, *hps, *hpt;
     int64_t vpad, prow;
-    int32_t wide;                // the partials come from that kernel (KL's cross term is A / ZH)
+    int32_t wide;                // the partials come from that kernel: 1, KL(T || S)'s cross
+                                 // term is A / ZH; 2 (reverse only), KL(S || T)'s is B / ZH
 };
 
 // Logit-gradient pass of the backward (scored rows [c0, c0 + chunk) of a call).
@@ -200,8 +201,8 @@ hipError_t launch_score_simple(const ScoreArgs &a, bool bf16, bool has_t, int64_
                                hipStream_t st);
 hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bool rev,
                              bool topk, int grid, hipStream_t st);
-hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, int grid,
-                             hipStream_t st);
+hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, bool rev,
+                             int grid, hipStream_t st);
 hipError_t launch_score_wide_dz(const ScoreArgs &a, const DzArgs &z, int grid, hipStream_t st);
 hipError_t launch_panel_w(const void *w, int64_t V, int d, int64_t vpad, void *out,
                           hipStream_t st);

@@ -25,6 +25,11 @@
 // fp16 normal range add at most V * 2^-40 times the largest deviation. The
 // log-normalisers use the fp32 weights.
 //
+// KL(student || teacher) is the same sum with the roles exchanged: the student's block
+// comes first in every tile, its fold keeps the student's fp16 weights, and the
+// teacher's fold consumes them (the REV instantiation). One call holds one set of
+// weights, so a call that asks for both directions takes the other kernel.
+//
 // Pipeline: K advances 32 elements per step. W and the hidden rows are read from
 // K-blocked panels ([d/32][rows][32] bf16, 64 bytes per row per panel), so one step of
 // a tile is a contiguous 16 KB for W (256 rows) and for H (256 positions): whole
@@ -131,12 +136,13 @@ __device__ __forceinline__ float block_max(const float (&z)[16], Run &R, int vco
     return resc;
 }
 
-// Teacher, second pass over a column's logits of the tile, once the column's running
-// max over the tile is final (the first pass is block_max): mneg = 15 - c max. Adds
-// the weights 2^15 exp2(c (z - max)) in fp32 to zsum, keeps them as fp16 in eh, adds
-// the fp16 values to hsum and their products with the logits to asum. All weights of a
-// tile refer to the same max, so those kept for the student fold need no rescale.
-__device__ __forceinline__ void teacher_weights(const float (&z)[16], float c, float mneg,
+// The first model of a tile (the one whose weights the KL takes), second pass over a
+// column's logits of the tile, once the column's running max over the tile is final
+// (the first pass is block_max): mneg = 15 - c max. Adds the weights
+// 2^15 exp2(c (z - max)) in fp32 to zsum, keeps them as fp16 in eh, adds the fp16
+// values to hsum and their products with the logits to asum. All weights of a tile
+// refer to the same max, so those kept for the second model's fold need no rescale.
+__device__ __forceinline__ void first_weights(const float (&z)[16], float c, float mneg,
                                                 float one, float &zsum, float &hsum,
                                                 float &asum, uint32_t (&eh)[8]) {
 #pragma unroll
@@ -152,16 +158,16 @@ __device__ __forceinline__ void teacher_weights(const float (&z)[16], float c, f
         hsum = fmaf(f16_hi(p), one, hsum);
         asum = fmaf(f16_lo(p), z[2 * q], asum);
         asum = fmaf(f16_hi(p), z[2 * q + 1], asum);
-        // a new value for the student fold: it must re-read the packed pair rather than
+        // a new value for the second fold: it must re-read the packed pair rather than
         // share these conversions (their fp32 results would stay live across its sweep)
         asm volatile("" : "+v"(p));
         eh[q] = p;
     }
 }
 
-// Student, 16 logits of a column: running statistics, and the sum of the teacher's fp16
-// weights times the student logits into as.
-__device__ __forceinline__ void fold_student(const float (&z)[16], Run &R, float &as,
+// The second model of a tile, 16 logits of a column: running statistics, and the sum
+// of the first model's fp16 weights times these logits into as.
+__device__ __forceinline__ void fold_second(const float (&z)[16], Run &R, float &as,
                                              const uint32_t (&eh)[8], float c, int vcode0,
                                              float inf) {
     R.z *= block_max(z, R, vcode0, c, inf);
@@ -189,8 +195,8 @@ __device__ __forceinline__ void fold_student_only(const float (&z)[16], Run &R, 
     R.z = zsum;
 }
 
-// Merge the teacher record y (with its difference sum ya and weight sum yz) into x.
-__device__ __forceinline__ void merge_teacher(Run &x, float &xa, float &xz, const Run &y,
+// Merge the first model's record y (with its difference sum ya and weight sum yz) into x.
+__device__ __forceinline__ void merge_weighted(Run &x, float &xa, float &xz, const Run &y,
                                               float ya, float yz, float c) {
     if (y.best == kNegInf) return;
     if (x.best == kNegInf) {
@@ -212,10 +218,14 @@ __device__ __forceinline__ void merge_teacher(Run &x, float &xa, float &xz, cons
     xz = wz + lz * r;
 }
 
-// HAS_T: a teacher block and fold precede the student's in every tile; without it the
-// call is student-only (SAME is then unused).
-template <bool SAME, bool HAS_T>
+// HAS_T: every tile holds a block of each model, and the first one's fold keeps its fp16
+// weights for the cross term of the second's; without it the call is student-only (SAME
+// and REV are then unused). REV: the student's block comes first (KL(student ||
+// teacher)); otherwise the teacher's (KL(teacher || student)).
+template <bool SAME, bool HAS_T, bool REV>
 struct Wide {
+    static constexpr int M1 = (HAS_T && !REV) ? 1 : 0;   // first block's model (1 = teacher)
+    static constexpr int M2 = HAS_T ? 1 - M1 : 0;        // last block's model
     struct Cursor {
         const char *w, *h;       // W and H tile of the step to prefetch
         int64_t wstep, hstep;    // bytes from one panel to the next (0 past the unit's end)
@@ -237,14 +247,14 @@ struct Wide {
         C.hstep = a.prow * XROW;
     }
 
-    // Teacher block of a tile, then its student block, then the next tile's teacher
-    // block; past the unit's last block the prefetches repeat its last step.
+    // The first model's block of a tile, then the second's, then the next tile's first;
+    // past the unit's last block the prefetches repeat its last step.
     static __device__ __forceinline__ void turn(Cursor &C, const ScoreArgs &a) {
         if (C.kk == C.cnt) {
-            if (C.m == 1) {
-                enter<0>(C, a, C.vt);
+            if (HAS_T && C.m == M1) {
+                enter<M2>(C, a, C.vt);
             } else if (C.vt + 1 < C.vt1) {
-                enter<HAS_T ? 1 : 0>(C, a, C.vt + 1);
+                enter<M1>(C, a, C.vt + 1);
             } else {
                 C.w -= C.wstep;
                 C.h -= C.hstep;
@@ -334,14 +344,16 @@ struct Wide {
             const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
 
-            float ZH[4], AT[4], AS[4];
+            // per column: the first model's fp16 weight sum, its weighted logit sum, and
+            // the same weights times the second model's logits
+            float ZH[4], A1[4], A2[4];
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
                 stat_put(0, cb, Run{kNegInf, kNegInf, 0.f, 0x7fffffff});
                 stat_put(1, cb, Run{kNegInf, kNegInf, 0.f, 0x7fffffff});
                 ZH[cb] = 0.f;
-                AT[cb] = 0.f;
-                AS[cb] = 0.f;
+                A1[cb] = 0.f;
+                A2[cb] = 0.f;
             }
             uint32_t eh[4][4][8];   // [row-block quarter][cb][pair]
             floatx4 acc[16][4];
@@ -351,7 +363,7 @@ struct Wide {
             C.nS = nS;
             C.nT = nT;
             C.p = p;
-            enter<HAS_T ? 1 : 0>(C, a, vt0);
+            enter<M1>(C, a, vt0);
 #pragma unroll
             for (int i = 0; i < XNST - 1; ++i) Pipe::issue(a, L, C, i);
             __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): no scalar load pending
@@ -359,108 +371,113 @@ struct Wide {
             // the first two tiles of a unit only measure the period (it straddles the
             // unit change)
             PhaseClock PH{0u, 0u};
+            const float c1 = M1 ? a.cT : a.cS, c2 = M2 ? a.cT : a.cS;
             for (int vt = vt0; vt < vt1; ++vt) {
                 const int row0 = vt * XV;
                 const int vbase = row0 + 4 * L.g;
                 if (lock && L.wid == 0) phase_lock<XDMA_STEP * (XNST - 2)>(PH, G);
                 if constexpr (HAS_T) {
-                OLIVE_XSTEPS(nT)
+                OLIVE_XSTEPS(M1 ? nT : nS)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
                     const float inf = opaque_inf(), one = opaque_one();
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb) {
-                        Run R = stat_get(1, cb);
+                        Run R = stat_get(M1, cb);
                         const float m0 = R.best;
 #pragma unroll
                         for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
                             col16(acc, qq, cb, z);
-                            (void)block_max(z, R, vbase + qq * 64, a.cT, inf);
+                            (void)block_max(z, R, vbase + qq * 64, c1, inf);
                         }
                         // one rescale per column and tile, to the tile's max
-                        const float resc = fast_exp2((m0 - R.best) * a.cT);
-                        float zsum = R.z * resc, hsum = ZH[cb] * resc, asum = AT[cb] * resc;
-                        AS[cb] *= resc;
-                        const float mneg = fmaf(-R.best, a.cT, 15.0f);
+                        const float resc = fast_exp2((m0 - R.best) * c1);
+                        float zsum = R.z * resc, hsum = ZH[cb] * resc, asum = A1[cb] * resc;
+                        A2[cb] *= resc;
+                        const float mneg = fmaf(-R.best, c1, 15.0f);
 #pragma unroll
                         for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
                             col16(acc, qq, cb, z);
-                            teacher_weights(z, a.cT, mneg, one, zsum, hsum, asum, eh[qq][cb]);
+                            first_weights(z, c1, mneg, one, zsum, hsum, asum, eh[qq][cb]);
                         }
                         R.z = zsum;
                         ZH[cb] = hsum;
-                        AT[cb] = asum;
+                        A1[cb] = asum;
                         // Pin the weighted sums here: otherwise the compiler sinks them
-                        // past the student sweep, keeping the teacher logits alive (and
-                        // spilled) across it.
-                        asm volatile("" : "+v"(ZH[cb]), "+v"(AT[cb]), "+v"(AS[cb]));
-                        stat_put(1, cb, R);
+                        // past the second sweep, keeping the first model's logits alive
+                        // (and spilled) across it.
+                        asm volatile("" : "+v"(ZH[cb]), "+v"(A1[cb]), "+v"(A2[cb]));
+                        stat_put(M1, cb, R);
                     }
                 }
                 }
-                OLIVE_XSTEPS(nS)
+                OLIVE_XSTEPS(M2 ? nT : nS)
                 if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
                 {
                     const float inf = opaque_inf();
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb) {
-                        Run R = stat_get(0, cb);
+                        Run R = stat_get(M2, cb);
 #pragma unroll
                         for (int qq = 0; qq < 4; ++qq) {
                             __builtin_amdgcn_sched_barrier(0);
                             float z[16];
                             col16(acc, qq, cb, z);
                             if constexpr (HAS_T)
-                                fold_student(z, R, AS[cb], eh[qq][cb], a.cS, vbase + qq * 64,
-                                             inf);
+                                fold_second(z, R, A2[cb], eh[qq][cb], c2, vbase + qq * 64, inf);
                             else
                                 fold_student_only(z, R, a.cS, vbase + qq * 64, inf);
                         }
-                        stat_put(0, cb, R);
+                        stat_put(M2, cb, R);
                     }
                 }
             }
 
-            // The difference sums (unscaled with equal scales; the combine multiplies by
-            // s), then the 4 lanes of each column (row groups g = 0..3) merge.
+            // The difference sums (first model minus second; unscaled with equal scales,
+            // the combine multiplies by s), then the 4 lanes of each column (row groups
+            // g = 0..3) merge.
             __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): trailing prefetches landed
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
-                float aa = SAME ? AT[cb] - AS[cb] : a.sT * AT[cb] - a.sS * AS[cb];
+                const float s1 = M1 ? a.sT : a.sS, s2 = M1 ? a.sS : a.sT;
+                float aa = SAME ? A1[cb] - A2[cb] : s1 * A1[cb] - s2 * A2[cb];
                 float zh = ZH[cb];
-                Run RS = stat_get(0, cb), RT = stat_get(1, cb);
+                Run R1 = stat_get(M1, cb), R2 = stat_get(M2, cb);
 #pragma unroll
                 for (int off = 16; off <= 32; off <<= 1) {
-                    Run o{__shfl_xor(RS.best, off), __shfl_xor(RS.sec, off),
-                          __shfl_xor(RS.z, off), __shfl_xor(RS.idx, off)};
+                    Run o{__shfl_xor(R2.best, off), __shfl_xor(R2.sec, off),
+                          __shfl_xor(R2.z, off), __shfl_xor(R2.idx, off)};
                     float dummy = 0.f;
-                    merge_run(RS, dummy, o, 0.f, a.cS);
+                    merge_run(R2, dummy, o, 0.f, c2);
                     if constexpr (HAS_T) {
-                        Run t{__shfl_xor(RT.best, off), __shfl_xor(RT.sec, off),
-                              __shfl_xor(RT.z, off), __shfl_xor(RT.idx, off)};
+                        Run t{__shfl_xor(R1.best, off), __shfl_xor(R1.sec, off),
+                              __shfl_xor(R1.z, off), __shfl_xor(R1.idx, off)};
                         const float ta = __shfl_xor(aa, off), tz = __shfl_xor(zh, off);
-                        merge_teacher(RT, aa, zh, t, ta, tz, a.cT);
+                        merge_weighted(R1, aa, zh, t, ta, tz, c1);
                     }
                 }
+                // the student's record is the last block's unless that is the teacher's
+                const Run &RS = M2 == 0 ? R2 : R1, &RT = M2 == 0 ? R1 : R2;
                 const int j = p * XT + L.wid * 64 + cb * 16 + L.l16;
                 if (L.g == 0 && j < t_valid) {
                     float *P = a.part;
                     const int64_t ps = a.pstride;
+                    // the first model's exp-sum carries the weights' 2^15 (exact)
+                    const float zs1 = HAS_T ? 0x1p-15f : 1.f;
                     P[(F_BEST_S * MAX_SPLITS + s) * ps + j] = RS.best;
                     P[(F_SEC_S * MAX_SPLITS + s) * ps + j] = RS.sec;
                     P[(F_IDX_S * MAX_SPLITS + s) * ps + j] = __int_as_float(RS.idx);
-                    P[(F_Z_S * MAX_SPLITS + s) * ps + j] = RS.z;
+                    P[(F_Z_S * MAX_SPLITS + s) * ps + j] = M1 ? RS.z : RS.z * zs1;
                     if (!HAS_T) continue;
                     P[(F_BEST_T * MAX_SPLITS + s) * ps + j] = RT.best;
                     P[(F_SEC_T * MAX_SPLITS + s) * ps + j] = RT.sec;
                     P[(F_IDX_T * MAX_SPLITS + s) * ps + j] = __int_as_float(RT.idx);
-                    // the teacher's exp-sum carries the weights' 2^15 (exact)
-                    P[(F_Z_T * MAX_SPLITS + s) * ps + j] = RT.z * 0x1p-15f;
-                    P[(F_A * MAX_SPLITS + s) * ps + j] = aa;
+                    P[(F_Z_T * MAX_SPLITS + s) * ps + j] = M1 ? RT.z * zs1 : RT.z;
+                    P[((REV ? F_B : F_A) * MAX_SPLITS + s) * ps + j] = aa;
                     P[(F_ZH * MAX_SPLITS + s) * ps + j] = zh;
                 }
             }
@@ -567,15 +584,15 @@ struct Wide {
 #undef OLIVE_XSTEPS
 };
 
-template <bool SAME, bool HAS_T>
+template <bool SAME, bool HAS_T, bool REV>
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_wide_kernel(ScoreArgs a) {
-    Wide<SAME, HAS_T>::run(a);
+    Wide<SAME, HAS_T, REV>::run(a);
 }
 
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_wide_dz_kernel(ScoreArgs a, DzArgs z) {
-    Wide<false, false>::run_dz(a, z);
+    Wide<false, false, false>::run_dz(a, z);
 }
 
 // Slot of 16-byte chunk q (0..3) of panel row r: the LDS swizzle of the stages, applied
@@ -616,19 +633,24 @@ panel_h_kernel(const uint16_t *__restrict__ h, int d, const uint32_t *__restrict
 
 }  // namespace
 
-hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, int grid,
-                             hipStream_t st) {
+hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, bool rev,
+                             int grid, hipStream_t st) {
     if (grid <= 0) return hipSuccess;
     if (a.ds <= 0 || a.ds % XK != 0 || a.vpad % XV != 0 || a.prow % XT != 0 || !a.wps ||
         !a.hps)
         return hipErrorInvalidValue;
     if (has_t && (a.dt <= 0 || a.dt % XK != 0 || !a.wpt || !a.hpt)) return hipErrorInvalidValue;
+    if (rev && !has_t) return hipErrorInvalidValue;
     if (!has_t)
-        score_wide_kernel<false, false><<<grid, 256, 0, st>>>(a);
+        score_wide_kernel<false, false, false><<<grid, 256, 0, st>>>(a);
+    else if (rev && same_scale)
+        score_wide_kernel<true, true, true><<<grid, 256, 0, st>>>(a);
+    else if (rev)
+        score_wide_kernel<false, true, true><<<grid, 256, 0, st>>>(a);
     else if (same_scale)
-        score_wide_kernel<true, true><<<grid, 256, 0, st>>>(a);
+        score_wide_kernel<true, true, false><<<grid, 256, 0, st>>>(a);
     else
-        score_wide_kernel<false, true><<<grid, 256, 0, st>>>(a);
+        score_wide_kernel<false, true, false><<<grid, 256, 0, st>>>(a);
     return hipGetLastError();
 }
 

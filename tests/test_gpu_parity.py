@@ -65,20 +65,22 @@ def test_custom_parity_full(case, kernel):
     compare(hip, wl, label="%s/%s" % (case, kernel))
 
 
-def _teacher_weighted_mad(wl, rows):
+def _weighted_mad(wl, rows, under="teacher"):
     """Per row: the mean absolute deviation of the scaled logit difference z_T - z_S
-    under p_T (fp64, from the oracle's projections)."""
+    under p_T (or under p_S with under="student"), fp64, from the oracle's
+    projections."""
     f = lambda t: (t.float() if t.dtype == torch.bfloat16 else t).cpu().numpy()
     hs, ht = f(wl["h_student"])[rows], f(wl["h_teacher"])[rows]
     zs = O.project(hs, f(wl["w_student"]), wl["scale_student"])
     zt = O.project(ht, f(wl["w_teacher"]), wl["scale_teacher"])
+    zw = zt if under == "teacher" else zs
     out = []
     for i in range(len(rows)):
-        lt = O.log_softmax_stats(zt[i])["lse"]
-        pt = np.exp(zt[i] - lt)
+        lw = O.log_softmax_stats(zw[i])["lse"]
+        pw = np.exp(zw[i] - lw)
         d = zt[i] - zs[i]
-        dbar = float(np.sum(pt * d))
-        out.append(float(np.sum(pt * np.abs(d - dbar))))
+        dbar = float(np.sum(pw * d))
+        out.append(float(np.sum(pw * np.abs(d - dbar))))
     return np.array(out)
 
 
@@ -97,7 +99,7 @@ def test_wide_kl_error_within_its_weight_rounding_bound(case):
     rows = np.nonzero(masks_of(wl, O.REGION_TEACHER)["in_region"])[0]
     assert rows.size > 100
     ref = oracle_rows(wl, rows, extras=False)["kl"]
-    mad = _teacher_weighted_mad(wl, rows)
+    mad = _weighted_mad(wl, rows)
     u = 2.0 ** -11
     err_w = np.abs(wide["kl"][rows] - ref)
     err_n = np.abs(narrow["kl"][rows] - ref)
@@ -172,14 +174,95 @@ def test_reverse_kl_regions_and_scales(region):
         compare(hip, wl, region=region, label="rev-scales-%d" % region)
 
 
-def test_reverse_kl_on_long_rollout_sampled():
-    say("reverse KL, long_rollout sampled")
+@pytest.mark.parametrize("both", [True, False], ids=["both_directions", "reverse_only"])
+def test_reverse_kl_on_long_rollout_sampled(both):
+    say("reverse KL, long_rollout sampled", "both" if both else "reverse only")
     wl = W.make_workload("long_rollout", 0, device="cuda")
-    hip = run_hip(wl, outputs=ALL_OUT)
+    hip = run_hip(wl, outputs=ALL_OUT if both else REV_OUT)
     assert hip["stats"]["kernel"] == "mfma"
+    assert hip["stats"]["tile"] == ("256x128" if both else "256x256")
     compare(hip, wl, rows=stratified_rows(wl, n_random=64), label="rev-long_rollout")
     del wl
     torch.cuda.empty_cache()
+
+
+# The reverse KL alone: the 256 x 256 kernel with the student's block first in every
+# tile and the student's fp16 weights kept for the teacher's fold.
+REV_OUT = tuple(k for k in ALL_OUT if k != "kl")
+
+
+@pytest.mark.parametrize("case", list(CASES))
+def test_reverse_kl_alone_on_the_wide_kernel(case):
+    say("reverse KL alone", case)
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl, outputs=REV_OUT)
+    assert hip["stats"]["kernel"] == "mfma" and hip["stats"]["tile"] == "256x256"
+    assert hip["err"] == 0 and "kl" not in hip
+    compare(hip, wl, label="rev-wide-" + case)
+    # the narrow tile still takes the same call
+    nar = run_hip(wl, outputs=REV_OUT, narrow=True)
+    assert nar["stats"]["tile"] == "256x128"
+    compare(nar, wl, label="rev-narrow-" + case)
+
+
+@pytest.mark.parametrize("region", [O.REGION_TEACHER, O.REGION_STUDENT, O.REGION_ALL])
+@pytest.mark.parametrize("scales", [(2.0, 0.5), (1.5, 1.5)], ids=["scales_differ", "scales_equal"])
+def test_reverse_kl_alone_regions_and_scales(region, scales):
+    say("reverse KL alone region", region, scales)
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    wl["scale_student"], wl["scale_teacher"] = scales
+    hip = run_hip(wl, region=region, outputs=REV_OUT)
+    assert hip["stats"]["tile"] == "256x256"
+    compare(hip, wl, region=region, label="rev-wide-scales-%d" % region)
+
+
+@pytest.mark.parametrize("direction", ["forward", "reverse"])
+def test_wide_kl_of_equal_models_is_zero_to_rounding(direction):
+    # Identical weights and hidden rows: the cross term (the first model's fp16 weights
+    # times its own logits, minus the same weights times the other model's bit-identical
+    # logits) is exactly 0. The two log-normalisers come from different fold orders (the
+    # first model's sums are rescaled once per tile, the second's once per block), so
+    # the KL is their difference: zero up to the rounding of a log-normaliser.
+    say("wide kernel, teacher == student", direction)
+    wl = custom("multi_tile", **dict(CASES["multi_tile"], d_teacher=256))
+    wl["w_teacher"], wl["h_teacher"] = wl["w_student"], wl["h_student"]
+    wl["scale_teacher"] = wl["scale_student"]
+    key = "kl" if direction == "forward" else "kl_rev"
+    outs = ("kl", "counts", "logp_s", "logp_t", "am_s", "am_t") if direction == "forward" \
+        else REV_OUT
+    hip = run_hip(wl, region=O.REGION_ALL, outputs=outs)
+    assert hip["stats"]["tile"] == "256x256"
+    lse_mag = np.max(np.abs(hip["logp_s"]))
+    say("  max |%s| %.2e  max |logp_s - logp_t| %.2e  max |logp| %.1f"
+        % (key, np.max(np.abs(hip[key])), np.max(np.abs(hip["logp_s"] - hip["logp_t"])),
+           lse_mag))
+    assert np.max(np.abs(hip[key])) <= 1e-5
+    np.testing.assert_allclose(hip["logp_s"], hip["logp_t"], rtol=0, atol=1e-5)
+    np.testing.assert_array_equal(hip["am_s"], hip["am_t"])
+
+
+@pytest.mark.parametrize("case", ["multi_tile", "even_v"])
+def test_wide_reverse_kl_error_within_its_weight_rounding_bound(case):
+    # As for the forward KL, with the student's fp16 weights: the rounding moves a
+    # reverse-KL value by at most 2^-11 / (1 - 2^-11) times the student-weighted mean
+    # absolute deviation of the logit difference, beyond the 256 x 128 kernel's error.
+    say("wide reverse KL bound", case)
+    wl = custom(case, **CASES[case])
+    wide = run_hip(wl, outputs=REV_OUT)
+    narrow = run_hip(wl, outputs=REV_OUT, narrow=True)
+    assert wide["stats"]["tile"] == "256x256" and narrow["stats"]["tile"] == "256x128"
+    rows = np.nonzero(masks_of(wl, O.REGION_TEACHER)["in_region"])[0]
+    assert rows.size > 100
+    ref = oracle_rows(wl, rows)["kl_rev"]
+    mad = _weighted_mad(wl, rows, under="student")
+    u = 2.0 ** -11
+    err_w = np.abs(wide["kl_rev"][rows] - ref)
+    err_n = np.abs(narrow["kl_rev"][rows] - ref)
+    bound = u / (1 - u) * mad + 2 * err_n + 1e-6 * (1 + np.abs(ref))
+    worst = np.max(err_w / bound)
+    say("  rows %d  max |dKL_rev| wide %.2e narrow %.2e  worst error / bound %.3f"
+        % (rows.size, err_w.max(), err_n.max(), worst))
+    assert np.all(err_w <= bound)
 
 
 # ----------------------------------------------------------------------------- span masks
