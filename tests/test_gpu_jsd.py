@@ -52,6 +52,40 @@ def test_jsd_spans_and_region_only():
     compare(ro, wl, region=O.REGION_SPANS, region_only=True, label="jsd-spans-region-only")
 
 
+# Calls with one KL direction or none: the normalisers come from the 256 x 256 kernel
+# (teacher block first, or the student's for the reverse KL alone).
+ONE_DIR = {
+    "forward": ("kl", "jsd", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
+    "reverse": ("kl_rev", "jsd", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce"),
+    "jsd_alone": ("jsd", "counts", "logp_s", "am_s"),
+}
+
+
+@pytest.mark.parametrize("which", list(ONE_DIR))
+@pytest.mark.parametrize("case", ["ragged_v1000", "multi_tile", "v257"])
+def test_jsd_after_the_wide_kernel(case, which):
+    say("jsd after the 256 x 256 kernel", case, which)
+    wl = custom(case, **CASES[case])
+    hip = run_hip(wl, outputs=ONE_DIR[which])
+    assert hip["stats"]["tile"] == "256x256" and hip["err"] == 0
+    assert np.all(hip["jsd"] <= np.log(2.0) + 1e-6) and np.all(hip["jsd"] >= -1e-6)
+    compare(hip, wl, label="jsd-wide-%s-%s" % (case, which))
+
+
+@pytest.mark.parametrize("which", list(ONE_DIR))
+def test_jsd_of_identical_models_after_the_wide_kernel(which):
+    # The 256 x 256 kernel forms the two log-normalisers in different fold orders, so
+    # for identical models they may differ by a rounding step and the JSD is 0 up to
+    # its square (exactly 0 after the 256 x 128 kernel, below).
+    say("jsd, teacher == student, after the 256 x 256 kernel", which)
+    wl = custom("multi_tile", **dict(CASES["multi_tile"], d_teacher=256))
+    wl["w_teacher"], wl["h_teacher"] = wl["w_student"], wl["h_student"]
+    wl["scale_teacher"] = wl["scale_student"]
+    hip = run_hip(wl, region=O.REGION_ALL, outputs=ONE_DIR[which])
+    assert hip["stats"]["tile"] == "256x256"
+    assert np.max(np.abs(hip["jsd"])) <= 1e-6
+
+
 def test_jsd_of_identical_models_is_exactly_zero():
     say("jsd, teacher == student")
     wl = custom("multi_tile", **CASES["multi_tile"])

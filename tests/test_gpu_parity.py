@@ -152,6 +152,15 @@ def test_different_scales_general_difference_path():
 
 
 ALL_OUT = ("kl", "kl_rev", "counts", "logp_s", "logp_t", "am_s", "am_t", "ce")
+# One KL direction: the 256 x 256 kernel (teacher block first for the forward KL, the
+# student's for the reverse KL alone); both directions: the 256 x 128 kernel.
+FWD_OUT = tuple(k for k in ALL_OUT if k != "kl_rev")
+REV_OUT = tuple(k for k in ALL_OUT if k != "kl")
+OUTSETS = {"both": ALL_OUT, "forward": FWD_OUT, "reverse": REV_OUT}
+
+
+def tile_of(outs):
+    return "256x128" if outs == "both" else "256x256"
 
 
 @pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
@@ -185,10 +194,6 @@ def test_reverse_kl_on_long_rollout_sampled(both):
     del wl
     torch.cuda.empty_cache()
 
-
-# The reverse KL alone: the 256 x 256 kernel with the student's block first in every
-# tile and the student's fp16 weights kept for the teacher's fold.
-REV_OUT = tuple(k for k in ALL_OUT if k != "kl")
 
 
 @pytest.mark.parametrize("case", list(CASES))
@@ -270,17 +275,21 @@ TURNS_CASE = dict(num_seqs=3, vocab=1000, d_student=128, d_teacher=256, target_s
                   turns=(4, 16, 3, 2, 4, 24, 4, 40))
 
 
+@pytest.mark.parametrize("outs", list(OUTSETS))
 @pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
-def test_span_masks_full(simple):
-    say("span masks", "generic" if simple else "mfma")
+def test_span_masks_full(simple, outs):
+    say("span masks", "generic" if simple else "mfma", outs)
     wl = custom("turns", **TURNS_CASE)
-    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, simple=simple, outputs=ALL_OUT)
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, simple=simple, outputs=OUTSETS[outs])
     assert hip["err"] == 0
-    compare(hip, wl, region=O.REGION_SPANS, label="spans")
+    if not simple:
+        assert hip["stats"]["tile"] == tile_of(outs)
+    compare(hip, wl, region=O.REGION_SPANS, label="spans-" + outs)
 
 
-def test_spans_equal_to_the_cut_region_reproduce_it():
-    say("spans [cut, len) == teacher region")
+@pytest.mark.parametrize("outs", list(OUTSETS))
+def test_spans_equal_to_the_cut_region_reproduce_it(outs):
+    say("spans [cut, len) == teacher region", outs)
     wl = custom("ragged_v1000", **CASES["ragged_v1000"])
     cu = wl["cu_seqlens"].cpu().numpy()
     cut = wl["cut"].cpu().numpy()
@@ -289,9 +298,10 @@ def test_spans_equal_to_the_cut_region_reproduce_it():
     wl["span_offsets"] = torch.arange(len(lens) + 1, dtype=torch.int32, device="cuda")
     wl["span_pairs"] = torch.tensor([[int(c), int(n)] for c, n in zip(cut, lens)],
                                     dtype=torch.int32, device="cuda")
-    a = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
-    b = run_hip(wl, region=L.OLIVE_REGION_TEACHER, outputs=ALL_OUT)
-    for k in ("kl", "kl_rev", "ce", "logp_s", "logp_t", "am_s", "am_t", "counts"):
+    a = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=OUTSETS[outs])
+    b = run_hip(wl, region=L.OLIVE_REGION_TEACHER, outputs=OUTSETS[outs])
+    assert a["stats"]["tile"] == b["stats"]["tile"] == tile_of(outs)
+    for k in OUTSETS[outs]:
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
 
 
@@ -330,31 +340,36 @@ def test_malformed_spans_set_the_error_word():
     assert hip2["err"] & 16 and np.all(np.isnan(hip2["logp_s"]))
 
 
+@pytest.mark.parametrize("outs", list(OUTSETS))
 @pytest.mark.parametrize("simple", [False, True], ids=["mfma", "generic"])
 @pytest.mark.parametrize("case", ["ragged_v1000", "turns"])
-def test_region_only_scores_just_the_region(case, simple):
-    say("region only", case, "generic" if simple else "mfma")
+def test_region_only_scores_just_the_region(case, simple, outs):
+    say("region only", case, "generic" if simple else "mfma", outs)
     if case == "turns":
         wl, region = custom("turns", **TURNS_CASE), O.REGION_SPANS
     else:
         wl, region = custom(case, **CASES[case]), O.REGION_TEACHER
-    hip = run_hip(wl, region=region, simple=simple, outputs=ALL_OUT,
+    hip = run_hip(wl, region=region, simple=simple, outputs=OUTSETS[outs],
                   out_flags=L.OLIVE_OUT_REGION_ONLY)
     assert hip["err"] == 0
-    compare(hip, wl, region=region, region_only=True, label="region-only-" + case)
+    if not simple:
+        assert hip["stats"]["tile"] == tile_of(outs)
+    compare(hip, wl, region=region, region_only=True, label="region-only-%s-%s" % (case, outs))
     # the compacted rows are the scored ones
-    full = run_hip(wl, region=region, simple=simple, outputs=ALL_OUT)
+    full = run_hip(wl, region=region, simple=simple, outputs=OUTSETS[outs])
     np.testing.assert_array_equal(hip["counts"], full["counts"])
 
 
-def test_multi_turn_workload_sampled():
-    say("multi_turn workload sampled")
+@pytest.mark.parametrize("outs", ["both", "forward"])
+def test_multi_turn_workload_sampled(outs):
+    say("multi_turn workload sampled", outs)
     wl = W.make_workload("multi_turn", 0, device="cuda")
-    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=ALL_OUT)
+    hip = run_hip(wl, region=L.OLIVE_REGION_SPANS, outputs=OUTSETS[outs])
     say("multi_turn stats", hip["stats"])
     assert hip["stats"]["kernel"] == "mfma" and hip["err"] == 0
+    assert hip["stats"]["tile"] == tile_of(outs)
     compare(hip, wl, region=O.REGION_SPANS, rows=stratified_rows(wl, n_random=48),
-            label="multi_turn")
+            label="multi_turn-" + outs)
     del wl
     torch.cuda.empty_cache()
 
