@@ -27,6 +27,11 @@
  *   - Calls that take a stream are asynchronous on it (0 = the null stream): they
  *     only validate host-visible arguments and enqueue kernels. The caller keeps
  *     every input and output alive until the stream has finished.
+ *   - The scoring and backward calls record no memset and never synchronise, so a
+ *     call may be captured into a HIP graph and replayed: a replay repeats the
+ *     captured call on whatever the captured buffers then hold (the host-side
+ *     arguments: shapes, region, output set and span count, are those of the capture;
+ *     OLIVE_FLAG_KERNEL_TIMING's events are re-recorded into the captured slot).
  *   - No call allocates device memory except olive_score_init; every workspace is
  *     owned by the context and sized at init.
  *   - A context is not safe for concurrent use from several host threads or for

@@ -5,12 +5,12 @@
 // sweeps the vocabulary tiles of one split for one position tile; wavefront w owns all
 // 256 rows of positions 64w .. 64w+63 (16 x 4 blocks of v_mfma_f32_16x16x32_bf16, 256
 // AGPRs). Per vocabulary tile it accumulates the teacher logits (K = d_T) and then the
-// student logits (K = d_S) of the same block in the same AGPRs: one model's fp32
-// accumulators at a time, where holding both models (the other kernel) limits the tile
-// to 256 x 128. The 16x16x32 shape moves half the accumulator bytes per MFMA operation
-// of the 32x32x16 one; under this load the chip is power-limited, and a pure-MFMA loop
-// of 16x16x32 on random bf16 operands held a 14 % higher clock than one of 32x32x16 at
-// the same pipe occupancy.
+// student logits (K = d_S; the other order for the reverse KL alone) of the same block
+// in the same AGPRs: one model's fp32 accumulators at a time, where holding both models
+// (the other kernel) limits the tile to 256 x 128. The 16x16x32 shape moves half the
+// accumulator bytes per MFMA operation of the 32x32x16 one; under this load the chip is
+// power-limited, and a pure-MFMA loop of 16x16x32 on random bf16 operands held a 14 %
+// higher clock than one of 32x32x16 at the same pipe occupancy.
 //
 // KL(teacher || student) needs, per vocabulary entry, the teacher's softmax weight
 // next to the student's logit. The teacher fold keeps those weights, relative to the
