@@ -187,6 +187,9 @@ def main():
     ap.add_argument("--reverse-kl-only", action="store_true",
                     help="form KL(student || teacher) instead of KL(teacher || student) "
                          "(olive_score_batch with kl_reverse set and kl NULL)")
+    ap.add_argument("--jsd", action="store_true",
+                    help="also form the Jensen-Shannon divergence (a second pass over the "
+                         "scored rows; olive_score_batch)")
     ap.add_argument("--region-only", action="store_true",
                     help="score only the region's positions (OLIVE_OUT_REGION_ONLY): the rate "
                          "and the roofline then count scored positions")
@@ -273,7 +276,8 @@ def main():
               topk_student=torch.empty(T, L.OLIVE_TOPK, dtype=torch.int32, device=dev),
               topk_teacher=torch.empty(T, L.OLIVE_TOPK, dtype=torch.int32, device=dev)) \
         if args.topk else {}
-    outs = L.make_outputs(kl=kl, kl_reverse=klr, counts=counts, logp_student=lps,
+    jsd = torch.empty(T, dtype=torch.float32, device=dev) if args.jsd else None
+    outs = L.make_outputs(kl=kl, kl_reverse=klr, jsd=jsd, counts=counts, logp_student=lps,
                           logp_teacher=lpt, argmax_student=ams, argmax_teacher=amt,
                           ce_per_seq=ce,
                           flags=L.OLIVE_OUT_REGION_ONLY if args.region_only else 0, **tk)
@@ -286,7 +290,8 @@ def main():
     def step():
         if use_spans:
             L.olive_score_batch_spans(ctx, batch, spans, outs, stream)
-        elif args.reverse_kl or args.reverse_kl_only or args.region_only or args.topk:
+        elif args.reverse_kl or args.reverse_kl_only or args.jsd or args.region_only or \
+                args.topk:
             L.olive_score_batch(ctx, batch, outs, stream)
         else:
             L.olive_kl_masked(ctx, batch, kl, counts, lps, lpt, ams, amt, ce, stream)
@@ -317,8 +322,8 @@ def main():
     # the dominant kernel of the call: the 256 x 256 one, or the 256 x 128 one (both KL
     # directions, top-K, OLIVE_FLAG_NARROW_TILE)
     kernel = "score_wide" if stats.get("tile") == "256x256" else "score_mfma"
-    traffic = None if (args.reverse_kl or args.reverse_kl_only or args.region_only or
-                       args.topk) \
+    traffic = None if (args.reverse_kl or args.reverse_kl_only or args.jsd or
+                       args.region_only or args.topk) \
         else measured_traffic(args.workload, kernel)
     out = {
         "metric": "scored positions/sec and % bf16 MFMA peak, fused LM-head+logsoftmax+KL",
@@ -339,6 +344,7 @@ def main():
             "d_student": spec.d_student, "d_teacher": spec.d_teacher,
             "logit_scale": spec.logit_scale, "vocab_splits": stats["splits"],
             "reverse_kl": bool(args.reverse_kl), "reverse_kl_only": bool(args.reverse_kl_only),
+            "jsd": bool(args.jsd),
             "region_only": bool(args.region_only),
             "topk": bool(args.topk), "topk_filtered_pairs": stats["topk_filtered"],
             "topk_scanned_pairs": stats["topk_scanned"],
