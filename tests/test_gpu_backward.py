@@ -268,15 +268,17 @@ def test_backward_on_long_rollout_sampled():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("mode", ["ce", "ce+kl", "ce+kl-topk"])
+@pytest.mark.parametrize("mode", ["ce", "ce+kl", "ce+kl-topk", "ce+kl-reverse"])
 def test_backward_reuses_forward_normalisers(mode):
     """OLIVE_GRAD_REUSE_FORWARD: the normalisers of the preceding forward call on the same
     batch stand in for the backward's own pass (from the top-K workspace when that call
-    asked for top-K outputs). The gradients meet the same bar and repeat bit for bit; the
+    asked for top-K outputs; from the student-first 256 x 256 kernel when it asked for
+    the reverse KL alone). The gradients meet the same bar and repeat bit for bit; the
     flag is refused once no matching forward call holds them."""
     say("backward reusing the forward normalisers", mode)
     w_kl = 0.0 if mode == "ce" else 0.5
     topk = mode.endswith("topk")
+    rev = mode.endswith("reverse")
     wl = custom("ragged_v1000", **CASES["ragged_v1000"])
     spec = wl["spec"]
     T = wl["total_positions"]
@@ -295,7 +297,11 @@ def test_backward_reuses_forward_normalisers(mode):
     def forward(batch):
         kl = torch.empty(T, dtype=torch.float32, device=dev)
         ov = torch.empty(T, dtype=torch.float32, device=dev) if topk else None
-        L.olive_score_batch(ctx, batch, L.make_outputs(kl=kl, topk_overlap=ov))
+        L.olive_score_batch(ctx, batch, L.make_outputs(kl=None if rev else kl,
+                                                       kl_reverse=kl if rev else None,
+                                                       topk_overlap=ov))
+        if rev:
+            assert L.olive_score_last_stats(ctx)["tile"] == "256x256"
 
     def backward(batch, reuse, check=True):
         gh = torch.full((T, spec.d_student), float("nan"), dtype=torch.float32, device=dev)
