@@ -64,20 +64,28 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t *p, int64_t 
 // split), the smallest among equals. The passes over the scored rows (logit gradient,
 // Jensen-Shannon) and the combine of the latter use it alike.
 // Work unit q -> (position tile p, vocabulary split s) of n_p tiles x ns splits: units
-// cycle through groups of SG splits (the remainder last), so that the 32 workgroups of
-// an XCD, which take consecutive units, share 32 / SG position tiles x SG splits.
+// cycle through groups of SG splits, so that the 32 workgroups of an XCD, which take
+// consecutive units, share 32 / SG position tiles x SG splits. Two or more splits left
+// over (ns % SG) join the last group, which is then SG + rem splits wide; a single one
+// stays a group of its own, at the end. (Measured: on a pass of 987 position tiles and
+// 7 splits, 3 leftover splits as a group of their own ran 2.2 % slower than joined; on
+// one of 90 tiles and 17 splits, the leftover split joined ran 0.5 % slower than alone.)
 __device__ __forceinline__ void unit_tile_split(int64_t q, int n_p, int ns, int SG, int &p,
                                                 int &s) {
     const int nsb = ns / SG, rem = ns % SG;
-    const int64_t full_units = (int64_t)nsb * SG * n_p;
-    if (q < full_units) {
+    // the groups of SG splits before the last group
+    const int nhead = (rem >= 2 && nsb > 0) ? nsb - 1 : nsb;
+    const int64_t head_units = (int64_t)nhead * SG * n_p;
+    if (q < head_units) {
         const int64_t w = q % (SG * (int64_t)n_p);
         p = (int)(w / SG);
         s = (int)(q / (SG * (int64_t)n_p)) * SG + (int)(w % SG);
     } else {
-        const int64_t w = q - full_units;
-        p = (int)(w / rem);
-        s = nsb * SG + (int)(w % rem);
+        // the last group: ns - nhead SG splits (SG + rem, or rem)
+        const int wl = ns - nhead * SG;
+        const int64_t w = q - head_units;
+        p = (int)(w / wl);
+        s = nhead * SG + (int)(w % wl);
     }
 }
 
