@@ -427,9 +427,12 @@ def bench_backward(args, wl, L):
         flops = 2.0 * spec.vocab * (Tv * (spec.d_student + spec.d_teacher) +
                                     R * (spec.d_student + dt + 2 * spec.d_student))
     else:
-        # forward normalisers and the logit-gradient pass each project both models;
-        # the two products are 2 R V d_S each
-        flops = 2.0 * R * spec.vocab * (2 * (spec.d_student + dt) + 2 * spec.d_student)
+        # the two products are 2 R V d_S each. A cross-entropy-only backward on the
+        # 256 x 256 pipeline projects the student once (its logit-gradient pass forms the
+        # normalisers); otherwise a normaliser pass and the logit-gradient pass each
+        # project the models of the loss
+        proj = 1 if (not args.backward_kl and not args.narrow_tile) else 2
+        flops = 2.0 * R * spec.vocab * (proj * (spec.d_student + dt) + 2 * spec.d_student)
     log("timed %d %s steps: %.3f ms/step, err %d"
         % (args.steps, "training" if train else "backward", ms_step, err))
     out = {

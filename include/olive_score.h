@@ -105,8 +105,9 @@ typedef struct {
 #define OLIVE_FLAG_TOPK 4
 /* Reserve the workspace of olive_score_backward. Needs a bf16 context on which the
  * MFMA kernel applies (else init returns E_UNSUPPORTED). The workspace holds about
- * 2 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory
- * (3.1 GB for V = 151936, d_S = 2048 and 8192 or more positions). */
+ * 2 V min(max_positions, 8192) + 2 d_S V + 8 max_positions bytes of device memory, plus
+ * 4 (V / 256 + 2) min(max_positions, 8192) bytes (3.1 GB for V = 151936, d_S = 2048 and
+ * 8192 or more positions). */
 #define OLIVE_FLAG_BACKWARD 8
 /* Score with the 256 x 128 two-model MFMA kernel instead of the 256 x 256 one. Without
  * this flag a bf16 context on which the MFMA kernel applies keeps K-blocked copies of its
@@ -114,8 +115,9 @@ typedef struct {
  * max_positions rounded up to 256) (d_S + d_T) bytes of device memory, d_T = 0 for a
  * student-only context: 1.9 GB + 0.4 GB for V = 151936, d_S + d_T = 6144 and 32768
  * positions), and its student-only calls, calls with one KL direction (kl or kl_reverse,
- * not both) and no top-K output, and the normaliser pass of olive_score_backward run the
- * 256 x 256 kernel. That kernel forms KL's cross term with the softmax weights of the
+ * not both) and no top-K output, and olive_score_backward's student passes (the
+ * cross-entropy alone in one sweep that forms its own normalisers, else the normaliser
+ * pass) run the 256 x 256 kernel. That kernel forms KL's cross term with the softmax weights of the
  * divergence's first distribution (p_T for kl, p_S for kl_reverse) held in fp16 and
  * normalised by their own sum (Sec. 6's KL; the weights' rounding moves a KL value by at
  * most 2^-11 (1 - 2^-11)^-1 times the mean absolute deviation of the logit difference
@@ -310,7 +312,10 @@ typedef struct {
  * z_S = s_S h_S W_S. Per scored position the logit gradient is
  * w_ce (p_S - onehot(y)) + w_kl (p_S - p_T); it is formed in one fused pass over the
  * vocabulary (recomputing the student's logits, and the teacher's when w_kl != 0, from
- * the forward normalisers) and held
+ * the forward normalisers; for the cross-entropy alone without reused normalisers on a
+ * context with the 256 x 256 kernel, the same pass forms the normalisers and stores the
+ * weights exp(s_S z - m) of each vocabulary tile, m its running max, in fp16 (2^15
+ * scaled), which one more pass over the stored values rescales) and held
  * in bf16 (round to nearest even) as the operand of the two products
  * dL/dh = s_S g W^T and dL/dW = s_S h^T g, which accumulate in fp32.
  * spans: NULL, or the scored spans when b->region is OLIVE_REGION_SPANS.

@@ -252,6 +252,105 @@ jsd_combine_kernel(ScoreArgs a, int grid, float *__restrict__ jsd) {
     jsd[g] = 0.5f * kLn2 * sum;
 }
 
+// Normalisers of the cross-entropy pass that forms its own (one wavefront per scored row
+// of the chunk): the split records (max m_s, weight sum z_s relative to m_s) merged in a
+// fixed order, lse = s_S M + ln sum_s z_s exp2(c_S (m_s - M)) into lse_out[j][0]; the
+// realised token y, and its gradient w_ce (p_y - 1) from the exact-order dot product
+// z_y (the rescale writes it in place of the stored weight). A target out of range sets
+// the error word and makes the row's normaliser NaN, as the forward combine does.
+__global__ void __launch_bounds__(256)
+dz_lse_kernel(ScoreArgs a, DzArgs z, int grid, float *__restrict__ lse_out,
+              int32_t *__restrict__ err) {
+    const int lane = threadIdx.x & 63;
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int t_all = a.sched->t_valid - z.c0;
+    const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
+    if (t >= t_rows) return;
+    const int64_t j = (int64_t)z.c0 + t;
+    const int ns = pass_splits((t_rows + WIDE_BT - 1) / WIDE_BT, a.n_vtiles, grid);
+    float m = kNegInf, zz = 0.f;
+    if (lane < ns) {
+        m = a.part[(F_BEST_S * MAX_SPLITS + lane) * a.pstride + j];
+        zz = a.part[(F_Z_S * MAX_SPLITS + lane) * a.pstride + j];
+    }
+    float M = m;
+    for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+    zz = lane < ns ? zz * fast_exp2((m - M) * a.cS) : 0.f;
+    for (int off = 32; off > 0; off >>= 1) zz += __shfl_xor(zz, off);
+    const int64_t g = a.rowmap[j] & 0x7fffffffu;
+    const int32_t y = z.targets[g];
+    const bool ok = y >= 0 && y < a.V;
+    float zy = 0.f;
+    if (ok)
+        zy = wave_dot<uint16_t>((const uint16_t *)a.hs + g * a.ds,
+                                (const uint16_t *)a.ws + (int64_t)y * a.ds, a.ds, lane);
+    if (lane != 0) return;
+    const float lse = ok ? a.sS * M + fast_log2(zz) * kLn2 : __builtin_nanf("");
+    if (!ok) atomicOr(err, ERR_TARGET);
+    lse_out[2 * j] = lse;
+    z.yrow[t] = ok ? y : -1;
+    z.gy[t] = z.w_ce * (fast_exp2((a.sS * zy - lse) * kLog2e) - 1.f);
+}
+
+// The gradient of that pass in place: each stored weight w (fp16, 2^15 exp2(c (z - m))
+// with m the running max of its tile) becomes 2^-15 w_ce w exp(s m - lse) = w_ce p in
+// bf16 (round to nearest even), the realised token's entry w_ce (p_y - 1). Rows at or
+// past V and columns past the chunk's rows are left as they are. One 16-byte piece
+// (8 entries of one panel row) per thread and step.
+__global__ void __launch_bounds__(256)
+dz_rescale_kernel(ScoreArgs a, DzArgs z, const float *__restrict__ lse) {
+    const int t_all = a.sched->t_valid - z.c0;
+    const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
+    const int np = (int)(z.vp / 64);
+    const int64_t n = (int64_t)np * t_rows * 8;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * 256) {
+        const int64_t P = i / ((int64_t)t_rows * 8);
+        const int t = (int)((i / 8) % t_rows), c = (int)(i % 8);
+        const int v0 = (int)(P * 64) + 8 * c;
+        if (v0 >= a.V) continue;
+        const float l2 = lse[2 * ((int64_t)z.c0 + t)] * kLog2e;
+        const float mc = z.mref[(int64_t)(v0 >> 8) * z.chunk + t] * a.cS;
+        const float f = z.w_ce * 0x1p-15f * fast_exp2(mc - l2);
+        uint16_t *q = z.dz_t + ((P * z.chunk + t) * 64 + 8 * c);
+        const uint4 in = *(const uint4 *)q;
+        const uint32_t wv[4] = {in.x, in.y, in.z, in.w};
+        float gv[8];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const _Float16 lo = __builtin_bit_cast(_Float16, (uint16_t)(wv[e] & 0xffffu));
+            const _Float16 hi = __builtin_bit_cast(_Float16, (uint16_t)(wv[e] >> 16));
+            gv[2 * e] = (float)lo * f;
+            gv[2 * e + 1] = (float)hi * f;
+        }
+        const int y = z.yrow[t];
+        if (y >= v0 && y < v0 + 8) gv[y - v0] = z.gy[t];
+        // entries at or past V keep their zeros
+        const int nv = a.V - v0 < 8 ? a.V - v0 : 8;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (e >= nv) gv[e] = 0.f;
+        *(uint4 *)q = make_uint4(pack_bf16x2(gv[0], gv[1]), pack_bf16x2(gv[2], gv[3]),
+                                 pack_bf16x2(gv[4], gv[5]), pack_bf16x2(gv[6], gv[7]));
+    }
+}
+
+hipError_t launch_dz_lse(const ScoreArgs &a, const DzArgs &z, int grid, float *lse_out,
+                         int32_t *err, hipStream_t st) {
+    if (z.chunk <= 0 || !lse_out || !z.gy || !z.yrow || !a.part) return hipErrorInvalidValue;
+    dz_lse_kernel<<<(unsigned)((z.chunk + 3) / 4), 256, 0, st>>>(a, z, grid, lse_out, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_dz_rescale(const ScoreArgs &a, const DzArgs &z, const float *lse,
+                             hipStream_t st) {
+    if (z.chunk <= 0 || z.vp % 64 != 0 || !z.dz_t || !z.mref || !lse) return hipErrorInvalidValue;
+    const int64_t most = z.vp / 64 * (int64_t)z.chunk * 8;   // pieces of a full chunk
+    const int64_t blocks = (most + 255) / 256 < 8192 ? (most + 255) / 256 : 8192;
+    dz_rescale_kernel<<<(unsigned)blocks, 256, 0, st>>>(a, z, lse);
+    return hipGetLastError();
+}
+
 hipError_t launch_jsd_combine(const ScoreArgs &a, float *jsd, int grid, int64_t max_rows,
                               hipStream_t st) {
     if (max_rows <= 0) return hipSuccess;

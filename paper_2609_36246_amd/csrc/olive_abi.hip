@@ -53,6 +53,8 @@ struct olive_score_ctx {
     uint16_t *bw_wt = nullptr;                  // W_S^T panels [bw_vp/64][d_S][64] bf16
     uint16_t *bw_dzt = nullptr;                 // panels [bw_vp/64][chunk][64]
     uint16_t *bw_hrt = nullptr;                 // [d_S][chunk]
+    float *bw_mref = nullptr;                   // [vocabulary tiles][chunk], then gy [chunk]
+                                                // and yrow [chunk] (int32)
     // Normalisers of the last forward call on the MFMA path and the batch they belong
     // to, for a backward on that batch (OLIVE_GRAD_REUSE_FORWARD). Scored rows take the
     // same compacted index in every pass (scored-first compaction), so the forward's
@@ -88,7 +90,7 @@ void release(olive_score_ctx *c) {
             if (c->ev[k][i]) (void)hipEventDestroy(c->ev[k][i]);
     void *ptrs[] = {c->ws_own, c->wt_own, c->rowmap, c->seqbuf, c->sched, c->part,
                     c->logp_tmp, c->lse_buf, c->flagged, c->fx_scratch, c->wn_s, c->wn_t, c->err,
-                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_hrt,
+                    c->tk_buf, c->fx_buf, c->bw_lse, c->bw_wt, c->bw_dzt, c->bw_hrt, c->bw_mref,
                     c->wp_s, c->wp_t, c->hp_s, c->hp_t};
     for (void *p : ptrs)
         if (p) (void)hipFree(p);
@@ -379,7 +381,16 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         return e;
     };
     const bool wide = !reuse && ctx->wide;
-    olive_status s = schedule(wide ? WIDE_BT : MFMA_BT);
+    const int ch = ctx->bw_chunk;
+    // The cross-entropy's logit gradient runs on the 256 x 256 kernel where the context
+    // keeps its panels. Chunks start at multiples of 8192 rows (or at 0), so at tile
+    // boundaries of the panels. Without a forward call's normalisers that pass forms
+    // them itself (one sweep of the student instead of two): it stores each tile's
+    // weights relative to the running max, and a rescale follows once the chunk's
+    // normalisers are known.
+    const bool wide_dz = ctx->wide && !has_t && (ch % WIDE_BT == 0 || T <= ch);
+    const bool online = wide && wide_dz;
+    olive_status s = schedule(wide && !online ? WIDE_BT : MFMA_BT);
     if (s) return s;
     ScoreArgs a;
     a.hs = b->h_student;
@@ -410,7 +421,11 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
     a.prow = ctx->hp_rows;
     a.wide = wide ? 1 : 0;
     const float *lse = ctx->fwd_lse;
-    if (!reuse) {
+    if (online) {
+        // the chunk passes write the normalisers; they replace a forward call's for reuse
+        ctx->fwd_lse_ok = false;
+        lse = ctx->bw_lse;
+    } else if (!reuse) {
         // the forward normalisers of the scored rows; they replace a forward call's for
         // reuse (always, wherever that call's are kept: one rule for every output set)
         ctx->fwd_lse_ok = false;
@@ -442,13 +457,9 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         s = check_hip(launch_fill(go->grad_h_student, T * ds, st));
         if (s) return s;
     }
-    const int ch = ctx->bw_chunk;
-    // The cross-entropy's logit gradient runs on the 256 x 256 kernel where the context
-    // keeps its panels: its hidden-row panels hold every scored row (built by the
-    // normaliser pass, or here when that pass was skipped). Chunks start at multiples of
-    // 8192 rows (or at 0), so at tile boundaries of the panels.
-    const bool wide_dz = ctx->wide && !has_t && (ch % WIDE_BT == 0 || T <= ch);
-    if (wide_dz && !wide) {
+    // the hidden-row panels of every scored row (built by the normaliser pass, or here
+    // when there was none)
+    if (wide_dz && (!wide || online)) {
         s = check_hip(launch_panel_h(b->h_student, d.d_student, ctx->rowmap, ctx->sched,
                                      ctx->hp_rows, ctx->hp_s, st));
         if (s) return s;
@@ -465,13 +476,22 @@ olive_status run_backward(olive_score_ctx *ctx, const olive_batch *b, const oliv
         z.w_ce = go->w_ce;
         z.w_kl = go->w_kl;
         z.dz_t = ctx->bw_dzt;
+        z.mref = ctx->bw_mref;
+        z.gy = ctx->bw_mref + (int64_t)((V + 255) / 256) * ch;
+        z.yrow = (int32_t *)(z.gy + ch);
         if (wide_dz) {
             ScoreArgs aw = a;
             aw.wps = ctx->wp_s;
             aw.hps = (const char *)ctx->hp_s + c0 * 64;   // panel row c0 (32 bf16 per row)
             aw.vpad = ctx->wp_rows;
             aw.prow = ctx->hp_rows;
-            s = check_hip(launch_score_wide_dz(aw, z, grid, st));
+            if (online) {
+                s = check_hip(launch_score_wide_dz_online(aw, z, grid, st));
+                if (!s) s = check_hip(launch_dz_lse(a, z, grid, ctx->bw_lse, ctx->err, st));
+                if (!s) s = check_hip(launch_dz_rescale(a, z, ctx->bw_lse, st));
+            } else {
+                s = check_hip(launch_score_wide_dz(aw, z, grid, st));
+            }
         } else {
             s = check_hip(launch_score_dz(a, z, has_t, grid, st));
         }
@@ -759,6 +779,9 @@ olive_status olive_score_init(olive_score_ctx **out, const olive_score_desc *des
         if (!s) s = dev_alloc(&c->bw_wt, (size_t)ds * c->bw_vp * 2);
         if (!s) s = dev_alloc(&c->bw_dzt, (size_t)c->bw_chunk * c->bw_vp * 2);
         if (!s) s = dev_alloc(&c->bw_hrt, (size_t)ds * c->bw_chunk * 2);
+        if (!s)
+            s = dev_alloc(&c->bw_mref,
+                          ((size_t)(V + 255) / 256 + 2) * c->bw_chunk * sizeof(float));
         if (!s) s = backward_init(c, st);
     }
     c->wide = c->mfma_ok && !(d.flags & OLIVE_FLAG_NARROW_TILE);

@@ -145,6 +145,11 @@ struct DzArgs {
     const int32_t *targets;      // packed realised tokens
     float w_ce, w_kl;            // loss weights
     uint16_t *dz_t;              // [vp/64][chunk][64] bf16 logit gradient (K-blocked panels)
+    // The cross-entropy pass that forms its own normalisers (no forward pass before it):
+    float *mref;                 // [vocabulary tiles][chunk] the running max each tile's
+                                 // stored weights refer to
+    float *gy;                   // [chunk] the realised token's gradient w_ce (p_y - 1)
+    int32_t *yrow;               // [chunk] the realised token (-1 when out of range)
 };
 
 // Jensen-Shannon pass over the scored rows [0, n_scored) of a forward call (the
@@ -204,6 +209,12 @@ hipError_t launch_score_mfma(const ScoreArgs &a, bool has_t, bool same_scale, bo
 hipError_t launch_score_wide(const ScoreArgs &a, bool same_scale, bool has_t, bool rev,
                              int grid, hipStream_t st);
 hipError_t launch_score_wide_dz(const ScoreArgs &a, const DzArgs &z, int grid, hipStream_t st);
+hipError_t launch_score_wide_dz_online(const ScoreArgs &a, const DzArgs &z, int grid,
+                                       hipStream_t st);
+hipError_t launch_dz_lse(const ScoreArgs &a, const DzArgs &z, int grid, float *lse_out,
+                         int32_t *err, hipStream_t st);
+hipError_t launch_dz_rescale(const ScoreArgs &a, const DzArgs &z, const float *lse,
+                             hipStream_t st);
 hipError_t launch_panel_w(const void *w, int64_t V, int d, int64_t vpad, void *out,
                           hipStream_t st);
 hipError_t launch_panel_h(const void *h, int d, const uint32_t *rowmap, const Sched *sched,

@@ -581,6 +581,129 @@ struct Wide {
             __syncthreads();
         }
     }
+    // Logit-gradient pass of a cross-entropy-only backward that forms its own
+    // normalisers, over the scored rows [c0, c0 + chunk) (no forward pass before it).
+    // Per vocabulary tile and column it updates the running max m over the tiles swept
+    // so far (this one included) and stores w = 2^15 exp2(c (z - m)) in [0, 2^15] as
+    // fp16 (round to nearest even) into dz_t, where the gradient goes; m goes to
+    // mref[tile][row], and the split's (m, sum of w 2^-15) to the partial records. The
+    // final normaliser (dz_lse_kernel) and the rescale of each tile's weights by
+    // 2^-15 w_ce exp(s m - lse) into the bf16 gradient (dz_rescale_kernel) follow.
+    static __device__ __forceinline__ void run_dz_online(ScoreArgs a, DzArgs z) {
+        const int t_all = a.sched->t_valid - z.c0;
+        const int t_rows = t_all < 0 ? 0 : (t_all < z.chunk ? t_all : z.chunk);
+        const int n_p = (t_rows + XT - 1) / XT;
+        const int G = gridDim.x;
+        const int ns = pass_splits(n_p, a.n_vtiles, G);
+        const int64_t n_units = (int64_t)n_p * ns;
+        const XLane L = make_lane();
+        const int nS = a.ds / XK, nT = 0;
+        const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3;
+        const int my = (G & 7) == 0 ? xcd * (G >> 3) + slot : (int)blockIdx.x;
+        const bool lock = phase_lock_on(G, nS);
+
+        for (int64_t q = my; q < n_units; q += G) {
+            int p, s;
+            unit_tile_split(q, n_p, ns, XSPLIT_GROUP, p, s);
+            const int vt0 = (int)((int64_t)a.n_vtiles * s / ns);
+            const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
+            // the lane's 4 columns: chunk row (-1 past the rows), running max, weight sum
+            int tcol[4];
+            float mr[4], zs[4];
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                const int t = p * XT + L.wid * 64 + cb * 16 + L.l16;
+                tcol[cb] = t < t_rows ? t : -1;
+                mr[cb] = -0x1p127f;   // below every logit, masked rows included
+                zs[cb] = 0.f;
+            }
+            floatx4 acc[16][4];
+            Cursor C;
+            C.vt1 = vt1;
+            C.nS = nS;
+            C.nT = nT;
+            C.p = p;
+            enter<0>(C, a, vt0);
+#pragma unroll
+            for (int i = 0; i < XNST - 1; ++i) Pipe::issue(a, L, C, i);
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0): no scalar load pending
+            int st = 0;
+            PhaseClock PH{0u, 0u};
+            for (int vt = vt0; vt < vt1; ++vt) {
+                const int row0 = vt * XV;
+                if (lock && L.wid == 0) phase_lock<XDMA_STEP * (XNST - 2)>(PH, G);
+                OLIVE_XSTEPS(nS)
+                if (row0 + XV > a.V) mask_tail(L, acc, row0, a.V);
+                // the column's max over the tile: the lane's 64 rows, then its 4 row groups
+#pragma unroll
+                for (int cb = 0; cb < 4; ++cb) {
+                    float tm = agpr_read(acc[0][cb][0]);
+#pragma unroll
+                    for (int vb = 0; vb < 16; ++vb) {
+                        // (the accumulator reads of later blocks are not hoisted)
+                        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                        for (int e = 0; e < 4; ++e)
+                            if (vb || e) tm = fmaxf(tm, agpr_read(acc[vb][cb][e]));
+                    }
+                    tm = fmaxf(tm, __shfl_xor(tm, 16));
+                    tm = fmaxf(tm, __shfl_xor(tm, 32));
+                    const float mn = fmaxf(mr[cb], tm);
+                    zs[cb] *= fast_exp2((mr[cb] - mn) * a.cS);
+                    mr[cb] = mn;
+                    if (L.g == 0 && tcol[cb] >= 0) z.mref[(int64_t)vt * z.chunk + tcol[cb]] = mn;
+                }
+                // the weights: into the sums, and as fp16 into dz_t (rows at or past V are
+                // not stored; lane (l16, g) holds rows 16 vb + 4 g .. +3 of column cb)
+#pragma unroll
+                for (int vb = 0; vb < 16; ++vb) {
+                    __builtin_amdgcn_sched_barrier(0);
+                    const int v0 = row0 + vb * 16 + 4 * L.g;
+#pragma unroll
+                    for (int cb = 0; cb < 4; ++cb) {
+                        const float mneg = fmaf(-mr[cb], a.cS, 15.0f);
+                        float w[4];
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            w[e] = fast_exp2(fmaf(agpr_read(acc[vb][cb][e]), a.cS, mneg));
+                            zs[cb] += w[e];
+                        }
+                        const int t = tcol[cb];
+                        if (t < 0 || v0 >= a.V) continue;
+                        uint16_t *dst = z.dz_t + (((int64_t)(v0 >> 6) * z.chunk + t) * 64 +
+                                                  (v0 & 63));
+                        const uint32_t w01 = pack_f16x2(w[0], w[1]);
+                        const uint32_t w23 = pack_f16x2(w[2], w[3]);
+                        if (v0 + 4 <= a.V) {
+                            *(uint2 *)dst = make_uint2(w01, w23);
+                        } else {
+                            const uint16_t h4[4] = {(uint16_t)w01, (uint16_t)(w01 >> 16),
+                                                    (uint16_t)w23, (uint16_t)(w23 >> 16)};
+                            for (int e = 0; e < 4 && v0 + e < a.V; ++e) dst[e] = h4[e];
+                        }
+                    }
+                }
+            }
+            // the split's records: the 4 row groups of a column share its max, so their
+            // weight sums add
+#pragma unroll
+            for (int cb = 0; cb < 4; ++cb) {
+                float zz = zs[cb];
+                zz += __shfl_xor(zz, 16);
+                zz += __shfl_xor(zz, 32);
+                if (L.g == 0 && tcol[cb] >= 0) {
+                    const int64_t j = (int64_t)z.c0 + tcol[cb];
+                    a.part[(F_BEST_S * MAX_SPLITS + s) * a.pstride + j] = mr[cb];
+                    a.part[(F_Z_S * MAX_SPLITS + s) * a.pstride + j] = zz * 0x1p-15f;
+                }
+            }
+            // every DMA landed and every wave is done with the ring before the next
+            // unit's prologue refills it
+            __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+            compiler_fence();
+            __syncthreads();
+        }
+    }
 #undef OLIVE_XSTEPS
 };
 
@@ -593,6 +716,11 @@ score_wide_kernel(ScoreArgs a) {
 __global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
 score_wide_dz_kernel(ScoreArgs a, DzArgs z) {
     Wide<false, false, false>::run_dz(a, z);
+}
+
+__global__ void __launch_bounds__(256, 1) __attribute__((amdgpu_waves_per_eu(1, 1)))
+score_wide_dz_online_kernel(ScoreArgs a, DzArgs z) {
+    Wide<false, false, false>::run_dz_online(a, z);
 }
 
 // Slot of 16-byte chunk q (0..3) of panel row r: the LDS swizzle of the stages, applied
@@ -660,6 +788,16 @@ hipError_t launch_score_wide_dz(const ScoreArgs &a, const DzArgs &z, int grid, h
         z.c0 % XT != 0 || z.chunk <= 0)
         return hipErrorInvalidValue;
     score_wide_dz_kernel<<<grid, 256, 0, st>>>(a, z);
+    return hipGetLastError();
+}
+
+hipError_t launch_score_wide_dz_online(const ScoreArgs &a, const DzArgs &z, int grid,
+                                       hipStream_t st) {
+    if (grid <= 0) return hipSuccess;
+    if (a.ds <= 0 || a.ds % XK != 0 || a.vpad % XV != 0 || !a.wps || !a.hps || !z.dz_t ||
+        !z.mref || !a.part || z.c0 % XT != 0 || z.chunk <= 0)
+        return hipErrorInvalidValue;
+    score_wide_dz_online_kernel<<<grid, 256, 0, st>>>(a, z);
     return hipGetLastError();
 }
 

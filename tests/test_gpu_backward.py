@@ -411,3 +411,26 @@ def test_backward_argument_errors():
     w32 = torch.zeros(spec.d_teacher * spec.vocab, dtype=torch.float32, device=dev)
     status, handle = L.olive_score_init(desc32, w32, w32, check=False)
     assert status == L.OLIVE_E_UNSUPPORTED and handle is None
+
+
+@pytest.mark.parametrize("narrow", [False, True], ids=["one_pass", "narrow_tile"])
+def test_backward_bad_target_row(narrow):
+    """A realised token out of range in one scored row: the error word's target bit is
+    set, that row's normaliser and so its gradient row are NaN, and every other row of
+    dL/dh is what it is without the bad row (rows do not mix in dL/dh). The cross-entropy
+    backward of a context with the 256 x 256 kernel forms its normalisers in its own
+    logit-gradient pass; with OLIVE_FLAG_NARROW_TILE it runs the separate normaliser
+    pass: both treat the row alike."""
+    say("backward with a bad target", "narrow" if narrow else "one pass")
+    wl = custom("ragged_v1000", **CASES["ragged_v1000"])
+    ref = oracle_backward(wl, 1.0, 0.0, O.REGION_TEACHER)
+    inr = masks_of(wl, O.REGION_TEACHER)["in_region"]
+    r = int(np.nonzero(inr)[0][7])
+    wl["targets"][r] = wl["spec"].vocab
+    hip = run_backward(wl, 1.0, 0.0, want=("h",), narrow=narrow)
+    assert hip["err"] & 1
+    assert np.all(np.isnan(hip["h"][r]))
+    # every other row at the bar of the backward tests (the bad row stands in for itself)
+    rest = {"h": hip["h"].copy()}
+    rest["h"][r] = ref["grad_h"][r]
+    check_grads(rest, ref, wl, "bad-target-%s" % ("narrow" if narrow else "one-pass"))
