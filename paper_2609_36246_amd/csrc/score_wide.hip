@@ -609,13 +609,15 @@ struct Wide {
             const int vt1 = (int)((int64_t)a.n_vtiles * (s + 1) / ns);
             // the lane's 4 columns: chunk row (-1 past the rows), running max, weight sum
             int tcol[4];
-            float mr[4], zs[4];
+            // running max and weight sum per column, in LDS between tiles (each thread its
+            // own entries): in registers beside the pipeline's they spilled 63 VGPRs
+            float *mr = x_stat + threadIdx.x, *zs = x_stat + 1024 + threadIdx.x;
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
                 const int t = p * XT + L.wid * 64 + cb * 16 + L.l16;
                 tcol[cb] = t < t_rows ? t : -1;
-                mr[cb] = -0x1p127f;   // below every logit, masked rows included
-                zs[cb] = 0.f;
+                mr[cb * 256] = -0x1p127f;   // below every logit, masked rows included
+                zs[cb * 256] = 0.f;
             }
             floatx4 acc[16][4];
             Cursor C;
@@ -648,9 +650,9 @@ struct Wide {
                     }
                     tm = fmaxf(tm, __shfl_xor(tm, 16));
                     tm = fmaxf(tm, __shfl_xor(tm, 32));
-                    const float mn = fmaxf(mr[cb], tm);
-                    zs[cb] *= fast_exp2((mr[cb] - mn) * a.cS);
-                    mr[cb] = mn;
+                    const float mn = fmaxf(mr[cb * 256], tm);
+                    zs[cb * 256] *= fast_exp2((mr[cb * 256] - mn) * a.cS);
+                    mr[cb * 256] = mn;
                     if (L.g == 0 && tcol[cb] >= 0) z.mref[(int64_t)vt * z.chunk + tcol[cb]] = mn;
                 }
                 // the weights: into the sums, and as fp16 into dz_t (rows at or past V are
@@ -661,12 +663,12 @@ struct Wide {
                     const int v0 = row0 + vb * 16 + 4 * L.g;
 #pragma unroll
                     for (int cb = 0; cb < 4; ++cb) {
-                        const float mneg = fmaf(-mr[cb], a.cS, 15.0f);
+                        const float mneg = fmaf(-mr[cb * 256], a.cS, 15.0f);
                         float w[4];
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
                             w[e] = fast_exp2(fmaf(agpr_read(acc[vb][cb][e]), a.cS, mneg));
-                            zs[cb] += w[e];
+                            zs[cb * 256] += w[e];
                         }
                         const int t = tcol[cb];
                         if (t < 0 || v0 >= a.V) continue;
@@ -688,12 +690,12 @@ struct Wide {
             // weight sums add
 #pragma unroll
             for (int cb = 0; cb < 4; ++cb) {
-                float zz = zs[cb];
+                float zz = zs[cb * 256];
                 zz += __shfl_xor(zz, 16);
                 zz += __shfl_xor(zz, 32);
                 if (L.g == 0 && tcol[cb] >= 0) {
                     const int64_t j = (int64_t)z.c0 + tcol[cb];
-                    a.part[(F_BEST_S * MAX_SPLITS + s) * a.pstride + j] = mr[cb];
+                    a.part[(F_BEST_S * MAX_SPLITS + s) * a.pstride + j] = mr[cb * 256];
                     a.part[(F_Z_S * MAX_SPLITS + s) * a.pstride + j] = zz * 0x1p-15f;
                 }
             }
